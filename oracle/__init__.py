@@ -1,0 +1,206 @@
+"""Oracle for the multipoint fit: a plain fp64 CPU implementation in C.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and
+the CPU-baseline leg of ``bench.py`` may import this package.  It shares no
+code with the HIP library (``paper_2002_09049_amd``); the only module both
+sides use is the seeded input generator ``paper_2002_09049_amd.workloads``,
+which holds none of the method's arithmetic.
+
+The arithmetic lives in ``mpq_oracle.c`` (see its header for the paper
+passages and readings it follows); this module only marshals numpy arrays.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(_HERE, "mpq_oracle.c")
+LIB = os.path.join(_HERE, "libmpq_oracle.so")
+_default = None
+
+
+def build(force: bool = True, src: str = SRC, out: str = LIB) -> str:
+    """Compile the oracle with gcc (-O2, OpenMP, no fast-math, no FP contraction)."""
+    if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(src):
+        tmp = out + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared",
+                               "-fno-fast-math", "-ffp-contract=off", src, "-o", tmp, "-lm"])
+        os.replace(tmp, out)
+    return out
+
+
+def _declare(lib):
+    P = ctypes.c_void_p
+    i64, i32, f64 = ctypes.c_int64, ctypes.c_int, ctypes.c_double
+    lib.oracle_fit.argtypes = [P, i64, i64, i32, i32, P, i32, f64, P, P, P, P, i32]
+    lib.oracle_fit.restype = i32
+    lib.oracle_verify.argtypes = [P, i64, i64, i32, i32, P, i32, f64, P, P, P, P,
+                                  P, i64, P, P, P, P, P, i32]
+    lib.oracle_verify.restype = i32
+    lib.oracle_output_error.argtypes = [P, P, P, P, i64, i64, i32, P, i64, P, i64,
+                                        P, P, i32]
+    lib.oracle_output_error.restype = i32
+    lib.oracle_reconstruct.argtypes = [P, P, P, i64, i64, i32, P]
+    lib.oracle_reconstruct.restype = None
+    lib.oracle_candidate_scales.argtypes = [P, i64, i32, P, i32, P]
+    lib.oracle_candidate_scales.restype = None
+    lib.oracle_codes.argtypes = [P, i64, f64, i32, P]
+    lib.oracle_codes.restype = None
+    lib.oracle_scale_error.argtypes = [P, i64, f64, i32]
+    lib.oracle_scale_error.restype = f64
+    lib.oracle_levels.argtypes = [i32]
+    lib.oracle_levels.restype = i32
+    lib.oracle_default_grid.argtypes = [i32, P]
+    lib.oracle_default_grid.restype = None
+    return lib
+
+
+def load(path: Optional[str] = None) -> "Oracle":
+    """Oracle bound to a compiled library (default: the built one)."""
+    global _default
+    if path is not None:
+        return Oracle(_declare(ctypes.CDLL(path)))
+    if _default is None:
+        if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+            build(force=True)
+        _default = Oracle(_declare(ctypes.CDLL(LIB)))
+    return _default
+
+
+def _p(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _grid(grid, G):
+    if grid is None:
+        return None
+    g = np.ascontiguousarray(grid, dtype=np.float32)
+    assert g.shape == (G,)
+    return g
+
+
+class Oracle:
+    """numpy front end of one compiled oracle library."""
+
+    def __init__(self, lib):
+        self.lib = lib
+
+    def levels(self, bits: int) -> int:
+        return self.lib.oracle_levels(bits)
+
+    def default_grid(self, G: int) -> np.ndarray:
+        c = np.empty(G, np.float32)
+        self.lib.oracle_default_grid(G, _p(c))
+        return c
+
+    def candidate_scales(self, r: np.ndarray, bits: int, grid: np.ndarray) -> np.ndarray:
+        r = np.ascontiguousarray(r, dtype=np.float64)
+        g = np.ascontiguousarray(grid, dtype=np.float32)
+        a = np.empty(g.shape[0], np.float32)
+        self.lib.oracle_candidate_scales(_p(r), r.size, self.levels(bits), _p(g), g.size, _p(a))
+        return a
+
+    def codes(self, r: np.ndarray, a: float, bits: int) -> np.ndarray:
+        r = np.ascontiguousarray(r, dtype=np.float64)
+        q = np.empty(r.size, np.int8)
+        self.lib.oracle_codes(_p(r), r.size, float(a), self.levels(bits), _p(q))
+        return q
+
+    def scale_error(self, r: np.ndarray, a: float, bits: int) -> float:
+        r = np.ascontiguousarray(r, dtype=np.float64)
+        return self.lib.oracle_scale_error(_p(r), r.size, float(a), self.levels(bits))
+
+    def fit(self, W: np.ndarray, bits: int, max_points: int, n_grid: int, tol: float,
+            grid: Optional[np.ndarray] = None, n_threads: int = 0):
+        """Free-running greedy fit. Returns (codes[C,P,d] i8, scales[C,P] f32,
+        counts[C] i32, err[C,P] f64)."""
+        W = np.ascontiguousarray(W, dtype=np.float32)
+        C, d = W.shape
+        P = max_points
+        codes_ = np.zeros((C, P, d), np.int8)
+        scales = np.zeros((C, P), np.float32)
+        counts = np.zeros(C, np.int32)
+        err = np.zeros((C, P), np.float64)
+        g = _grid(grid, n_grid)
+        rc = self.lib.oracle_fit(_p(W), C, d, bits, P, _p(g), n_grid, float(tol),
+                                _p(codes_), _p(scales), _p(counts), _p(err), n_threads)
+        if rc != 0:
+            raise MemoryError("oracle_fit failed")
+        return codes_, scales, counts, err
+
+    def verify(self, W, bits, max_points, n_grid, tol, codes_, scales, counts, err=None,
+               grid=None, channels=None, n_threads: int = 0):
+        """Lockstep check of another implementation's fit output (rules V1-V4).
+
+        Returns a dict of per-channel arrays: status, cand_ties, code_ties,
+        stop_ties, err_relmax, and the checked channel indices.
+        """
+        W = np.ascontiguousarray(W, dtype=np.float32)
+        C, d = W.shape
+        codes_ = np.ascontiguousarray(codes_, dtype=np.int8)
+        scales = np.ascontiguousarray(scales, dtype=np.float32)
+        counts = np.ascontiguousarray(counts, dtype=np.int32)
+        assert codes_.shape == (C, max_points, d) and scales.shape == (C, max_points)
+        assert counts.shape == (C,)
+        e = None if err is None else np.ascontiguousarray(err, dtype=np.float32)
+        chan = np.arange(C, dtype=np.int64) if channels is None else \
+            np.ascontiguousarray(channels, dtype=np.int64)
+        n = chan.size
+        out = {k: np.zeros(n, np.int32) for k in ("status", "cand_ties", "code_ties", "stop_ties")}
+        out["err_relmax"] = np.zeros(n, np.float64)
+        g = _grid(grid, n_grid)
+        rc = self.lib.oracle_verify(_p(W), C, d, bits, max_points, _p(g), n_grid, float(tol),
+                                   _p(codes_), _p(scales), _p(counts), _p(e), _p(chan), n,
+                                   _p(out["status"]), _p(out["cand_ties"]), _p(out["code_ties"]),
+                                   _p(out["stop_ties"]), _p(out["err_relmax"]), n_threads)
+        if rc != 0:
+            raise MemoryError("oracle_verify failed")
+        out["channels"] = chan
+        return out
+
+    def output_error(self, W, codes_, scales, counts, X, channels=None, with_ref=True, n_threads: int = 0):
+        """Eq. (12) in fp64. Returns (err, ref) for the listed channels."""
+        W = np.ascontiguousarray(W, dtype=np.float32)
+        C, d = W.shape
+        P = codes_.shape[1]
+        X = np.ascontiguousarray(X, dtype=np.float32)
+        assert X.shape[0] == d
+        N = X.shape[1]
+        chan = None if channels is None else np.ascontiguousarray(channels, dtype=np.int64)
+        n = C if chan is None else chan.size
+        err = np.zeros(n, np.float64)
+        ref = np.zeros(n, np.float64) if with_ref else None
+        rc = self.lib.oracle_output_error(
+            _p(W), _p(np.ascontiguousarray(codes_, dtype=np.int8)),
+            _p(np.ascontiguousarray(scales, dtype=np.float32)),
+            _p(np.ascontiguousarray(counts, dtype=np.int32)), C, d, P, _p(X), N,
+            _p(chan), 0 if chan is None else chan.size, _p(err), _p(ref), n_threads)
+        if rc != 0:
+            raise MemoryError("oracle_output_error failed")
+        return err, ref
+
+    def reconstruct(self, codes_, scales, counts) -> np.ndarray:
+        codes_ = np.ascontiguousarray(codes_, dtype=np.int8)
+        C, P, d = codes_.shape
+        out = np.zeros((C, d), np.float32)
+        self.lib.oracle_reconstruct(_p(codes_), _p(np.ascontiguousarray(scales, dtype=np.float32)),
+                                   _p(np.ascontiguousarray(counts, dtype=np.int32)), C, d, P, _p(out))
+        return out
+
+
+def _delegate(name):
+    def f(*args, **kw):
+        return getattr(load(), name)(*args, **kw)
+    f.__name__ = name
+    f.__doc__ = getattr(Oracle, name).__doc__
+    return f
+
+
+for _n in ("levels", "default_grid", "candidate_scales", "codes", "scale_error", "fit",
+           "verify", "output_error", "reconstruct"):
+    globals()[_n] = _delegate(_n)

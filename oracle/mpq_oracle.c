@@ -1,0 +1,393 @@
+/*
+ * Oracle for the per-channel greedy multipoint fit, its output error and
+ * its reconstruction.  Plain, slow, fp64.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg load this library.  The HIP library never
+ * links, includes or calls it, and it shares no code with the HIP library.
+ *
+ * What it computes (Liu, Ye, Zhou, Liu, "Post-training Quantization with
+ * Multiple Points: Mixed Precision without Mixed Precision"):
+ *   Sec. 3.1, Eq. (1)-(3): the symmetric b-bit set and nearest rounding.
+ *   Sec. 3.2, Eq. (4)-(10) and Algorithm 1: approximate a channel w by
+ *     sum_i a_i * q_i, adding one (a, q) pair per step, each fitted to the
+ *     current residual; a by grid search over candidate scales (Eq. (9)),
+ *     q as the rounding of r / a (Eq. (8), (10)); residual by Eq. (7).
+ *   Sec. 3.3, Eq. (12) and Algorithm 2: output error on a calibration
+ *     batch; points are added until the error falls below a threshold.
+ *
+ * Readings taken where the paper is silent, ambiguous or garbled (the same
+ * readings bind the HIP library):
+ *   Q1/K1  Codes are the integers [-M, M], M = 2^(b-1) - 1 (Eq. (1) with
+ *          B = 0 and K * eps_b folded into the scale a).
+ *   R1     Nearest rounding breaks exact half-way ties to even.
+ *   G1/G2  Candidate scales: a_g = fl32(m * c_g / M) with m = fl32(max|r|)
+ *          recomputed at every step and multipliers 0 < c_1 < ... < c_G <= 1
+ *          (default c_g = g / G).  Products and the quotient are fp64.
+ *   T1     Among exactly equal candidate errors the smallest g wins.
+ *   S1-S3  Stop after n points when n == max_points, or ||r||^2 == 0, or
+ *          n >= 1 and ||r||^2 <= tol * ||w||^2 (the output error of Eq. (12)
+ *          under an isotropic calibration distribution).  A nonzero channel
+ *          always gets at least one point; an all-zero channel gets none.
+ *   A1     No refit of a once q is fixed.
+ *   E1     Output error: mean over the N columns of X of ((w - w~) . x)^2.
+ *   P1     Scales are stored as fp32 values (exactly the candidate value).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* Eq. (1): [-1 : eps_b : 1] with eps_b = 1 / (2^(b-1) - 1) has 2M+1 points,
+ * M = 2^(b-1) - 1. */
+int oracle_levels(int bits) { return (1 << (bits - 1)) - 1; }
+
+/* Eq. (2): nearest point of the integer code set {-M..M} to t.  nearbyint
+ * rounds to nearest with ties to even in the default rounding mode (R1);
+ * clipping to [-M, M] then gives the nearest point of the bounded set. */
+static double nearest_code(double t, int M)
+{
+    double q = nearbyint(t);
+    if (q > (double)M) q = (double)M;
+    if (q < -(double)M) q = -(double)M;
+    return q;
+}
+
+/* Default candidate multipliers c_g = g / G, g = 1..G (reading G1). */
+void oracle_default_grid(int G, float *c)
+{
+    for (int g = 0; g < G; ++g) c[g] = (float)((double)(g + 1) / (double)G);
+}
+
+/* Candidate scales of one step (reading G2):
+ * a_g = fl32( fl32(max|r|) * c_g / M ). */
+void oracle_candidate_scales(const double *r, int64_t d, int M,
+                             const float *c, int G, float *a)
+{
+    double mx = 0.0;
+    for (int64_t j = 0; j < d; ++j) {
+        double v = fabs(r[j]);
+        if (v > mx) mx = v;
+    }
+    float m = (float)mx;
+    for (int g = 0; g < G; ++g)
+        a[g] = (float)((double)m * (double)c[g] / (double)M);
+}
+
+/* Eq. (8): for a fixed scale a the best code vector is [r / a]_Q. */
+void oracle_codes(const double *r, int64_t d, double a, int M, int8_t *q)
+{
+    for (int64_t j = 0; j < d; ++j) q[j] = (int8_t)nearest_code(r[j] / a, M);
+}
+
+/* Objective of Eq. (9): || r - a [r / a]_Q ||^2, summed in index order. */
+double oracle_scale_error(const double *r, int64_t d, double a, int M)
+{
+    double e = 0.0;
+    for (int64_t j = 0; j < d; ++j) {
+        double t = r[j] - a * nearest_code(r[j] / a, M);
+        e += t * t;
+    }
+    return e;
+}
+
+static double sum_sq(const double *r, int64_t d)
+{
+    double s = 0.0;
+    for (int64_t j = 0; j < d; ++j) s += r[j] * r[j];
+    return s;
+}
+
+/* Eq. (9) by grid search: errors of all G candidates, best index by T1. */
+static int grid_search(const double *r, int64_t d, const float *a, int G, int M,
+                       double *E)
+{
+    int best = 0;
+    for (int g = 0; g < G; ++g) {
+        E[g] = oracle_scale_error(r, d, (double)a[g], M);
+        if (E[g] < E[best]) best = g;
+    }
+    return best;
+}
+
+/* Stopping rule S1-S3 with n points taken so far and Er = ||r||^2. */
+static int should_stop(int n, int P, double Er, double Ew, double tol)
+{
+    if (n >= P) return 1;
+    if (Er == 0.0) return 1;
+    if (n >= 1 && Er <= tol * Ew) return 1;
+    return 0;
+}
+
+/* Algorithm 1 with the stopping rule, one channel.  codes [P][d], scales [P],
+ * err [P] (||r||^2 after each point).  Returns the number of points. */
+static int fit_channel(const float *w, int64_t d, int M, int P, const float *c,
+                       int G, double tol, int8_t *codes, float *scales,
+                       double *err, double *r, float *a, double *E)
+{
+    for (int64_t j = 0; j < d; ++j) r[j] = (double)w[j];   /* r_1 = w, Eq. (7) */
+    double Ew = sum_sq(r, d);
+    int n = 0;
+    for (;;) {
+        double Er = sum_sq(r, d);
+        if (should_stop(n, P, Er, Ew, tol)) break;
+        oracle_candidate_scales(r, d, M, c, G, a);
+        int g = grid_search(r, d, a, G, M, E);              /* Eq. (9)  */
+        double as = (double)a[g];
+        int8_t *q = codes + (int64_t)n * d;
+        oracle_codes(r, d, as, M, q);                       /* Eq. (10) */
+        for (int64_t j = 0; j < d; ++j) r[j] = r[j] - as * (double)q[j]; /* Eq. (7) */
+        scales[n] = a[g];
+        n += 1;
+        err[n - 1] = sum_sq(r, d);
+    }
+    return n;
+}
+
+static int n_threads_or_default(int nt)
+{
+#ifdef _OPENMP
+    return nt > 0 ? nt : omp_get_max_threads();
+#else
+    (void)nt;
+    return 1;
+#endif
+}
+
+/* Free-running fit of a layer W [C][d].  grid: NULL for the default.
+ * Outputs: codes [C][P][d] int8, scales [C][P], counts [C], err [C][P]
+ * (may be NULL).  Slots at or after a channel's count are zero. */
+int oracle_fit(const float *W, int64_t C, int64_t d, int bits, int P,
+               const float *grid, int G, double tol, int8_t *codes,
+               float *scales, int32_t *counts, double *err, int n_threads)
+{
+    int M = oracle_levels(bits);
+    float *c = (float *)malloc(sizeof(float) * (size_t)G);
+    if (!c) return -1;
+    if (grid) memcpy(c, grid, sizeof(float) * (size_t)G);
+    else oracle_default_grid(G, c);
+    memset(codes, 0, (size_t)(C * P * d));
+    memset(scales, 0, sizeof(float) * (size_t)(C * P));
+    if (err) memset(err, 0, sizeof(double) * (size_t)(C * P));
+    int nt = n_threads_or_default(n_threads);
+    int fail = 0;
+#pragma omp parallel num_threads(nt)
+    {
+        double *r = (double *)malloc(sizeof(double) * (size_t)d);
+        float *a = (float *)malloc(sizeof(float) * (size_t)G);
+        double *E = (double *)malloc(sizeof(double) * (size_t)G);
+        double *e = (double *)malloc(sizeof(double) * (size_t)P);
+        if (!r || !a || !E || !e) {
+#pragma omp atomic write
+            fail = 1;
+        } else {
+#pragma omp for schedule(dynamic, 1)
+            for (int64_t k = 0; k < C; ++k) {
+                memset(e, 0, sizeof(double) * (size_t)P);
+                int n = fit_channel(W + k * d, d, M, P, c, G, tol,
+                                    codes + k * P * d, scales + k * P, e, r, a, E);
+                counts[k] = n;
+                if (err) memcpy(err + k * P, e, sizeof(double) * (size_t)P);
+            }
+        }
+        free(r); free(a); free(E); free(e);
+    }
+    free(c);
+    return fail ? -1 : 0;
+}
+
+/* ------------------------------------------------------------------------
+ * Lockstep verifier.  For each listed channel it replays the outputs of
+ * another implementation step by step on its own fp64 residual and checks:
+ *  V1 the chosen scale is a candidate of the step and its error is the
+ *     minimum, or within 1e-6 relative of it (a "candidate tie");
+ *  V2 the codes equal [r / a]_Q except at elements whose r / a lies within
+ *     1e-6 * max(1, |r / a|) of a half-integer, where either neighbour is
+ *     accepted (a "code tie");
+ *  V3 the stop decision agrees, except when ||r||^2 / (tol ||w||^2) is
+ *     within 1e-6 of 1 (a "stop tie");
+ *  V4 the per-point ||r||^2 (if given) agrees within 1e-5 relative;
+ * and that every slot at or after the count is zero.  After each accepted
+ * step it continues from the other implementation's (a, q).
+ * status: 0 ok, 1 count, 2 scale not a candidate, 3 scale not optimal,
+ *         4 code, 5 nonzero unused slot, 6 err value, 7 bad count range.
+ * ------------------------------------------------------------------------ */
+int oracle_verify(const float *W, int64_t C, int64_t d, int bits, int P,
+                  const float *grid, int G, double tol, const int8_t *codes,
+                  const float *scales, const int32_t *counts, const float *err,
+                  const int64_t *chan, int64_t n_chan, int32_t *status,
+                  int32_t *cand_ties, int32_t *code_ties, int32_t *stop_ties,
+                  double *err_relmax, int n_threads)
+{
+    int M = oracle_levels(bits);
+    float *c = (float *)malloc(sizeof(float) * (size_t)G);
+    if (!c) return -1;
+    if (grid) memcpy(c, grid, sizeof(float) * (size_t)G);
+    else oracle_default_grid(G, c);
+    int nt = n_threads_or_default(n_threads);
+    int fail = 0;
+    (void)C;
+#pragma omp parallel num_threads(nt)
+    {
+        double *r = (double *)malloc(sizeof(double) * (size_t)d);
+        float *a = (float *)malloc(sizeof(float) * (size_t)G);
+        double *E = (double *)malloc(sizeof(double) * (size_t)G);
+        if (!r || !a || !E) {
+#pragma omp atomic write
+            fail = 1;
+        } else {
+#pragma omp for schedule(dynamic, 1)
+            for (int64_t s = 0; s < n_chan; ++s) {
+                int64_t k = chan[s];
+                const float *w = W + k * d;
+                const int8_t *qk = codes + k * P * d;
+                const float *ak = scales + k * P;
+                const float *ek = err ? err + k * P : NULL;
+                int st = 0, ct = 0, qt = 0, stt = 0;
+                double emax = 0.0;
+                int n_other = counts[k];
+                if (n_other < 0 || n_other > P) st = 7;
+                for (int64_t j = 0; j < d; ++j) r[j] = (double)w[j];
+                double Ew = sum_sq(r, d);
+                for (int n = 0; st == 0; ++n) {
+                    double Er = sum_sq(r, d);
+                    if (n >= 1 && ek) {
+                        double ref = Er, got = (double)ek[n - 1];
+                        double rel = ref == 0.0 ? (got == 0.0 ? 0.0 : INFINITY)
+                                                : fabs(got - ref) / ref;
+                        if (rel > emax) emax = rel;
+                        if (rel > 1e-5) { st = 6; break; }
+                    }
+                    int stop_ref = should_stop(n, P, Er, Ew, tol);
+                    int stop_other = (n == n_other);
+                    if (stop_ref != stop_other) {
+                        double ratio = (tol * Ew) > 0 ? Er / (tol * Ew) : INFINITY;
+                        if (n >= 1 && n < P && Er != 0.0 && fabs(ratio - 1.0) <= 1e-6) {
+                            stt++;
+                        } else { st = 1; break; }
+                    }
+                    if (stop_other) break;
+                    /* V1 */
+                    oracle_candidate_scales(r, d, M, c, G, a);
+                    int gbest = grid_search(r, d, a, G, M, E);
+                    float ao = ak[n];
+                    int go = -1;
+                    for (int g = 0; g < G; ++g)
+                        if (a[g] == ao) { go = g; break; }
+                    if (go < 0) { st = 2; break; }
+                    if (go != gbest) {
+                        if (E[go] <= (1.0 + 1e-6) * E[gbest]) ct++;
+                        else { st = 3; break; }
+                    }
+                    /* V2, then continue from the other side's (a, q) */
+                    const int8_t *q = qk + (int64_t)n * d;
+                    double as = (double)ao;
+                    for (int64_t j = 0; j < d; ++j) {
+                        double t = r[j] / as;
+                        int qr = (int)nearest_code(t, M);
+                        int qo = (int)q[j];
+                        if (qo != qr) {
+                            double fl = floor(t);
+                            double half = fabs(t - (fl + 0.5));
+                            int lo = (int)nearest_code(fl, M), hi = (int)nearest_code(fl + 1.0, M);
+                            if (half <= 1e-6 * fmax(1.0, fabs(t)) && (qo == lo || qo == hi)) qt++;
+                            else { st = 4; break; }
+                        }
+                    }
+                    if (st) break;
+                    for (int64_t j = 0; j < d; ++j) r[j] = r[j] - as * (double)q[j];
+                }
+                /* unused slots must be zero */
+                if (st == 0) {
+                    for (int n = n_other; n < P && st == 0; ++n) {
+                        if (ak[n] != 0.0f) st = 5;
+                        if (ek && ek[n] != 0.0f) st = 5;
+                        for (int64_t j = 0; j < d && st == 0; ++j)
+                            if (qk[(int64_t)n * d + j] != 0) st = 5;
+                    }
+                }
+                status[s] = st; cand_ties[s] = ct; code_ties[s] = qt;
+                stop_ties[s] = stt; err_relmax[s] = emax;
+            }
+        }
+        free(r); free(a); free(E);
+    }
+    free(c);
+    return fail ? -1 : 0;
+}
+
+/* Residual D = w - sum_{i<n} a_i q_i of one channel, summed in point order
+ * (Eq. (7); the same sequence of fp64 operations as the fit). */
+static void channel_residual(const float *w, const int8_t *q, const float *a,
+                             int n, int64_t d, double *D)
+{
+    for (int64_t j = 0; j < d; ++j) D[j] = (double)w[j];
+    for (int i = 0; i < n; ++i)
+        for (int64_t j = 0; j < d; ++j)
+            D[j] = D[j] - (double)a[i] * (double)q[(int64_t)i * d + j];
+}
+
+/* Eq. (12): err[k] = (1/N) sum_n ((w_k - w~_k) . x_n)^2 and, if ref is not
+ * NULL, ref[k] = (1/N) sum_n (w_k . x_n)^2, for the listed channels
+ * (chan == NULL: all C channels, outputs indexed by channel). */
+int oracle_output_error(const float *W, const int8_t *codes, const float *scales,
+                        const int32_t *counts, int64_t C, int64_t d, int P,
+                        const float *X, int64_t N, const int64_t *chan,
+                        int64_t n_chan, double *err, double *ref, int n_threads)
+{
+    int nt = n_threads_or_default(n_threads);
+    int64_t cnt = chan ? n_chan : C;
+    int fail = 0;
+#pragma omp parallel num_threads(nt)
+    {
+        double *D = (double *)malloc(sizeof(double) * (size_t)d);
+        if (!D) {
+#pragma omp atomic write
+            fail = 1;
+        } else {
+#pragma omp for schedule(dynamic, 1)
+            for (int64_t s = 0; s < cnt; ++s) {
+                int64_t k = chan ? chan[s] : s;
+                const float *w = W + k * d;
+                channel_residual(w, codes + k * P * d, scales + k * P, counts[k], d, D);
+                double se = 0.0, sr = 0.0;
+                for (int64_t n = 0; n < N; ++n) {
+                    double y = 0.0, yr = 0.0;
+                    for (int64_t j = 0; j < d; ++j) {
+                        double x = (double)X[j * N + n];
+                        y += D[j] * x;
+                        yr += (double)w[j] * x;
+                    }
+                    se += y * y;
+                    sr += yr * yr;
+                }
+                err[s] = se / (double)N;
+                if (ref) ref[s] = sr / (double)N;
+            }
+        }
+        free(D);
+    }
+    return fail ? -1 : 0;
+}
+
+/* Eq. (4): w~ = sum_{i<n} a_i q_i, accumulated in fp64 in point order and
+ * rounded once to fp32. */
+void oracle_reconstruct(const int8_t *codes, const float *scales,
+                        const int32_t *counts, int64_t C, int64_t d, int P,
+                        float *W_hat)
+{
+    for (int64_t k = 0; k < C; ++k) {
+        const int8_t *q = codes + k * P * d;
+        const float *a = scales + k * P;
+        for (int64_t j = 0; j < d; ++j) {
+            double s = 0.0;
+            for (int i = 0; i < counts[k]; ++i)
+                s = s + (double)a[i] * (double)q[(int64_t)i * d + j];
+            W_hat[k * d + j] = (float)s;
+        }
+    }
+}

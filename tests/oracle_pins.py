@@ -1,0 +1,338 @@
+"""Pins of the oracle: each check compares it with something other than itself.
+
+Every ``check_*`` takes an ``oracle.Oracle`` and raises AssertionError when
+the oracle disagrees with the paper, a closed form, brute force or a library
+routine.  ``test_oracle_pins.py`` runs them on the oracle;
+``test_oracle_mutants.py`` runs them on deliberately broken copies of the
+oracle and requires every copy to fail at least one check.
+"""
+from __future__ import annotations
+
+import json
+import math
+import os
+
+import numpy as np
+
+import bruteforce as bf
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "worked_examples.json")
+
+
+def _golden(name):
+    with open(GOLDEN) as f:
+        cases = json.load(f)["cases"]
+    return next(c for c in cases if c["name"] == name)
+
+
+def _fl32(x):
+    return float(np.float32(x))
+
+
+# ---------------------------------------------------------------- Eq. (1)-(3)
+def check_levels(orc):
+    """Eq. (1): [-1 : eps_b : 1] with eps_b = 1/(2^(b-1)-1) has 2M+1 points."""
+    for b in range(2, 9):
+        eps = 1.0 / (2 ** (b - 1) - 1)
+        n_points = int(round(2.0 / eps)) + 1
+        assert 2 * orc.levels(b) + 1 == n_points, b
+
+
+def check_rounding_ties(orc):
+    """Eq. (2) at exact half-way points against numpy's round-half-even."""
+    g = _golden("rounding_half_ties_to_even")
+    r = np.array(g["r"], np.float64)
+    q = orc.codes(r, g["a"], g["bits"])
+    M = 2 ** (g["bits"] - 1) - 1
+    lib = np.clip(np.round(r / g["a"]), -M, M).astype(np.int64)   # numpy rounds half to even
+    assert q.tolist() == g["expect_codes"] == lib.tolist(), (q, lib)
+
+
+def check_codes_bruteforce(orc):
+    """P-a: [r/a]_Q (Eq. (8)) equals the minimiser over all (2M+1)^d code vectors."""
+    rng = np.random.default_rng(11)
+    for bits, d in ((2, 6), (3, 4), (4, 3), (4, 4)):
+        M = 2 ** (bits - 1) - 1
+        for _ in range(6):
+            r = rng.standard_normal(d)
+            m = np.abs(r).max()
+            a = float(rng.uniform(0.05, 1.0) * m / M) if rng.random() < 0.7 \
+                else float(rng.uniform(0.02, 0.3) * m)
+            q = orc.codes(r, a, bits)
+            qb, Eb, nmin = bf.best_code_vector(r, a, M)
+            assert nmin == 1
+            assert q.tolist() == qb.tolist(), (bits, r, a, q, qb)
+            assert abs(orc.scale_error(r, a, bits) - Eb) <= 1e-12 * max(Eb, 1e-300)
+
+
+def _first_step(orc, r, bits, G, grid=None):
+    """Error and scale after one point of the oracle's fit (P=1, tol=0)."""
+    W = np.asarray(r, np.float32)[None, :]
+    codes, scales, counts, err = orc.fit(W, bits, 1, G, 0.0, grid=grid)
+    return float(err[0, 0]), float(scales[0, 0]), codes[0, 0], int(counts[0])
+
+
+def check_grid_search_bruteforce(orc):
+    """Eq. (9): the chosen scale minimises, over the candidates of reading G2,
+    the brute-force error min_q ||r - a q||^2; the tie rule picks the first."""
+    rng = np.random.default_rng(12)
+    for bits, d, G in ((2, 5, 16), (3, 4, 8), (4, 3, 32)):
+        M = 2 ** (bits - 1) - 1
+        for _ in range(4):
+            r = rng.standard_normal(d).astype(np.float32).astype(np.float64)
+            m = _fl32(np.abs(r).max())
+            cands = [_fl32(m * _fl32((g + 1) / G) / M) for g in range(G)]
+            Eb = [bf.best_code_vector(r, a, M)[1] for a in cands]
+            gbest = int(np.argmin(Eb))
+            e0, a0, q0, n0 = _first_step(orc, r, bits, G)
+            assert n0 == 1
+            assert a0 == cands[gbest], (a0, cands[gbest])
+            assert abs(e0 - Eb[gbest]) <= 1e-12 * Eb[gbest]
+            assert q0.tolist() == bf.best_code_vector(r, a0, M)[0].tolist()
+
+
+def check_grid_search_bounds(orc):
+    """P-b: the grid-search error is bounded below by the continuum optimum
+    over the range (0, max|r|/M], which is bounded below by the global
+    single-point optimum; refining a nested grid never hurts and converges."""
+    rng = np.random.default_rng(13)
+    for bits, d in ((2, 6), (3, 4), (4, 3)):
+        M = 2 ** (bits - 1) - 1
+        for _ in range(3):
+            r = rng.standard_normal(d).astype(np.float32).astype(np.float64)
+            amax = _fl32(_fl32(np.abs(r).max()) / M)       # largest candidate (c_G = 1)
+            e_cont = bf.continuum_scale_optimum(r, M, amax)
+            e_range = bf.range_single_point_optimum(r, M, amax)
+            e_glob = bf.global_single_point_optimum(r, M)
+            assert abs(e_cont - e_range) <= 1e-9 * max(e_range, 1e-12), (e_cont, e_range)
+            assert e_glob <= e_range * (1 + 1e-12)
+            gaps = []
+            for G in (16, 256, 4096):
+                e, *_ = _first_step(orc, r, bits, G)
+                assert e >= e_range * (1 - 1e-9), (G, e, e_range)
+                gaps.append(e - e_range)
+            assert gaps[2] <= gaps[1] + 1e-15 and gaps[1] <= gaps[0] + 1e-15, gaps
+            assert gaps[2] <= 2e-3 * (r @ r), gaps
+
+
+def check_two_point_joint(orc):
+    """P-b: the greedy two-point error is no better than the joint optimum of Eq. (5)."""
+    rng = np.random.default_rng(14)
+    for bits, d in ((2, 4), (3, 3)):
+        M = 2 ** (bits - 1) - 1
+        for _ in range(3):
+            r = rng.standard_normal(d).astype(np.float32)
+            codes, scales, counts, err = orc.fit(r[None, :], bits, 2, 64, 0.0)
+            if counts[0] < 2:
+                continue
+            ej = bf.joint_two_point_optimum(r.astype(np.float64), M)
+            assert err[0, 1] >= ej * (1 - 1e-9) - 1e-15, (err[0, 1], ej)
+
+
+def check_naive_quantizer(orc):
+    """P-c: one candidate (grid {1}) and one point is ordinary symmetric
+    per-channel max-abs quantization; compared with torch's fake quantizer."""
+    import torch
+    rng = np.random.default_rng(15)
+    for bits in (3, 4, 8):
+        M = 2 ** (bits - 1) - 1
+        W = (rng.standard_normal((16, 200)) * np.exp(rng.standard_normal((16, 1)))).astype(np.float32)
+        codes, scales, counts, err = orc.fit(W, bits, 1, 1, 0.0, grid=np.array([1.0], np.float32))
+        wt = torch.from_numpy(W)
+        s = wt.abs().amax(dim=1) / M                       # fp32 scale max|w|/M
+        assert np.array_equal(scales[:, 0], s.numpy()), bits
+        fq = torch.fake_quantize_per_channel_affine(wt, s, torch.zeros(16, dtype=torch.int32),
+                                                    0, -M, M)
+        qt = torch.round(fq / s[:, None]).to(torch.int64).numpy()
+        t = W.astype(np.float64) / s.numpy().astype(np.float64)[:, None]
+        near_half = np.abs(np.abs(t - np.floor(t)) - 0.5) < 1e-5
+        ok = (codes[:, 0, :] == qt) | near_half
+        assert ok.all(), bits
+        assert (counts == 1).all()
+
+
+def check_equal_magnitudes(orc):
+    """P-d: all |w_j| equal (and d = 1): one point, codes sign(w)*M, scale fl32(m/M)."""
+    for bits in (2, 3, 4, 8):
+        M = 2 ** (bits - 1) - 1
+        for w in ([0.3, -0.3, 0.3, 0.3, -0.3], [-1.7]):
+            W = np.array([w], np.float32)
+            codes, scales, counts, err = orc.fit(W, bits, 4, 64, 1e-3)
+            m = float(np.float32(abs(w[0])))
+            assert counts[0] == 1, (bits, counts)
+            assert scales[0, 0] == np.float32(m / M)
+            assert codes[0, 0].tolist() == [int(np.sign(x)) * M for x in w]
+
+
+def check_worked_examples(orc):
+    """P-e and the stop-boundary case, derived by hand (tests/golden)."""
+    g = _golden("two_elements_exact_tie")
+    W = np.array([g["w"]], np.float32)
+    codes, scales, counts, err = orc.fit(W, g["bits"], g["max_points"], g["n_grid"], g["tol"])
+    e = g["expect"]
+    assert counts[0] == e["count"]
+    assert scales[0].tolist() == e["scales"]
+    assert codes[0].tolist() == e["codes"]
+    assert err[0].tolist() == e["err"]
+    g = _golden("stop_exactly_at_tolerance")
+    W = np.array([g["w"]], np.float32)
+    for v in g["variants"]:
+        codes, scales, counts, err = orc.fit(W, g["bits"], g["max_points"], g["n_grid"],
+                                             float(np.float32(v["tol"])))
+        assert counts[0] == v["count"], v
+        assert scales[0].tolist() == v["scales"]
+        assert err[0].tolist() == v["err"]
+        assert codes[0, 0].tolist() == v["codes_point0"]
+        if "codes_point1" in v:
+            assert codes[0, 1].tolist() == v["codes_point1"]
+
+
+def check_monotone_decrease(orc):
+    """P-f: ||r_{i+1}||^2 <= ||r_i||^2 - max|r_i|^2 (+1e-6 ||r_i||^2 slack);
+    err[i] is ||r_{i+1}||^2 of the residual chain of Eq. (7)."""
+    rng = np.random.default_rng(16)
+    for bits, G in ((2, 64), (3, 128), (4, 256), (8, 64)):
+        W = (rng.standard_normal((12, 97)) * np.exp(0.5 * rng.standard_normal((12, 1)))).astype(np.float32)
+        W[3, :50] = 0.0
+        codes, scales, counts, err = orc.fit(W, bits, 5, G, 0.0)
+        for k in range(W.shape[0]):
+            n = int(counts[k])
+            rs = bf.residual_chain(W[k], codes[k], scales[k], n)
+            for i in range(n):
+                e0 = float(rs[i] @ rs[i])
+                e1 = float(rs[i + 1] @ rs[i + 1])
+                m = float(np.abs(rs[i]).max())
+                assert e1 <= e0 - m * m + 1e-6 * e0, (bits, k, i, e0, e1, m)
+                assert abs(err[k, i] - e1) <= 1e-12 * max(e0, 1e-300)
+
+
+def check_reconstruct(orc):
+    """P-g: reconstruct = sum_i a_i q_i (Eq. (4)); ||w - w~||^2 equals the last err."""
+    rng = np.random.default_rng(17)
+    W = (rng.standard_normal((10, 77)) * 0.1).astype(np.float32)
+    codes, scales, counts, err = orc.fit(W, 4, 4, 128, 1e-4)
+    Wh = orc.reconstruct(codes, scales, counts)
+    ref = np.einsum("kp,kpj->kj", scales.astype(np.float64) *
+                    (np.arange(4)[None, :] < counts[:, None]), codes.astype(np.float64))
+    assert np.array_equal(Wh, ref.astype(np.float32))
+    for k in range(10):
+        n = counts[k]
+        e = float(((W[k].astype(np.float64) - Wh[k].astype(np.float64)) ** 2).sum())
+        assert abs(e - err[k, n - 1]) <= 1e-5 * err[k, n - 1] + 1e-12 * float(W[k] @ W[k])
+
+
+def check_invariances(orc):
+    """P-h: w -> -w negates codes; w -> 2^k w scales the scales by 2^k;
+    permuting elements permutes codes."""
+    rng = np.random.default_rng(18)
+    W = (rng.standard_normal((8, 60)) * 0.2).astype(np.float32)
+    base = orc.fit(W, 4, 4, 128, 1e-3)
+    neg = orc.fit(-W, 4, 4, 128, 1e-3)
+    assert np.array_equal(neg[0], -base[0]) and np.array_equal(neg[1], base[1])
+    assert np.array_equal(neg[2], base[2])
+    for k in (-3, 5):
+        sc = orc.fit((W * np.float32(2.0 ** k)).astype(np.float32), 4, 4, 128, 1e-3)
+        assert np.array_equal(sc[0], base[0]) and np.array_equal(sc[2], base[2])
+        assert np.array_equal(sc[1], (base[1] * np.float32(2.0 ** k)).astype(np.float32))
+    perm = rng.permutation(60)
+    pe = orc.fit(np.ascontiguousarray(W[:, perm]), 4, 4, 128, 1e-3)
+    assert np.array_equal(pe[2], base[2])
+    assert np.array_equal(pe[0], base[0][:, :, perm])
+    assert np.array_equal(pe[1], base[1])
+
+
+def check_output_error(orc):
+    """P-i: with X X^T = N I the output error equals ||w - w~||^2; for random X
+    it equals a numpy fp64 matmul (Eq. (12), mean over the batch)."""
+    rng = np.random.default_rng(19)
+    d, N = 24, 64
+    W = (rng.standard_normal((6, d)) * 0.3).astype(np.float32)
+    codes, scales, counts, err = orc.fit(W, 3, 3, 64, 1e-2)
+    H = bf.hadamard(N)[:d].astype(np.float32)          # rows orthogonal, norm^2 = N
+    e, r = orc.output_error(W, codes, scales, counts, H)
+    for k in range(6):
+        n = counts[k]
+        assert abs(e[k] - err[k, n - 1]) <= 1e-10 * err[k, n - 1]
+        assert abs(r[k] - float(W[k].astype(np.float64) @ W[k].astype(np.float64))) <= 1e-10 * r[k]
+    X = rng.standard_normal((d, 37)).astype(np.float32)
+    e, r = orc.output_error(W, codes, scales, counts, X)
+    Wh = np.einsum("kp,kpj->kj", scales.astype(np.float64) * (np.arange(3)[None, :] < counts[:, None]),
+                   codes.astype(np.float64))
+    D = W.astype(np.float64) - Wh
+    ye = D @ X.astype(np.float64)
+    yr = W.astype(np.float64) @ X.astype(np.float64)
+    assert np.allclose(e, (ye ** 2).mean(axis=1), rtol=1e-9, atol=0)
+    assert np.allclose(r, (yr ** 2).mean(axis=1), rtol=1e-9, atol=0)
+    sub = np.array([4, 1], np.int64)
+    e2, r2 = orc.output_error(W, codes, scales, counts, X, channels=sub)
+    assert np.array_equal(e2, e[sub]) and np.array_equal(r2, r[sub])
+
+
+def check_stop_rule(orc):
+    """S1-S3: tol >= 1 gives one point; a zero channel gets none; tol = 0 runs
+    to the cap unless the residual vanishes."""
+    rng = np.random.default_rng(20)
+    W = (rng.standard_normal((5, 40)) * 0.2).astype(np.float32)
+    W[2] = 0.0
+    c1 = orc.fit(W, 4, 6, 64, 1.0)[2]
+    assert c1.tolist() == [1, 1, 0, 1, 1]
+    c0 = orc.fit(W, 4, 6, 64, 0.0)[2]
+    assert c0.tolist() == [6, 6, 0, 6, 6]
+
+
+def check_exponential_decay(orc):
+    """Theorem 1 (qualitative): log ||r_i|| falls roughly linearly in i.
+    Parity unpinned for the rate: the constants are not given."""
+    rng = np.random.default_rng(21)
+    W = rng.standard_normal((4, 256)).astype(np.float32)
+    codes, scales, counts, err = orc.fit(W, 2, 8, 1024, 0.0)
+    for k in range(4):
+        e = np.concatenate([[float(W[k].astype(np.float64) @ W[k].astype(np.float64))], err[k]])
+        ratios = e[1:] / e[:-1]
+        assert (ratios < 0.9).all(), ratios
+
+
+def check_verifier(orc):
+    """The lockstep verifier accepts the oracle's own output and flags
+    planted mistakes (wrong count, off-grid scale, worse candidate, wrong
+    code, dirty unused slot, wrong err)."""
+    rng = np.random.default_rng(22)
+    W = (rng.standard_normal((6, 50)) * np.exp(0.5 * rng.standard_normal((6, 1)))).astype(np.float32)
+    bits, P, G, tol = 4, 4, 64, 1e-3
+    codes, scales, counts, err = orc.fit(W, bits, P, G, tol)
+    ok = orc.verify(W, bits, P, G, tol, codes, scales, counts, err.astype(np.float32))
+    assert (ok["status"] == 0).all() and ok["cand_ties"].sum() == 0 and ok["code_ties"].sum() == 0
+    assert (ok["err_relmax"] < 1e-6).all()
+
+    def status(c, s, n, e):
+        return orc.verify(W, bits, P, G, tol, c, s, n, e)["status"][0]
+
+    e32 = err.astype(np.float32)
+    n2 = counts.copy(); n2[0] = n2[0] + 1 if n2[0] < P else n2[0] - 1
+    assert status(codes, scales, n2, None) != 0
+    s2 = scales.copy(); s2[0, 0] = np.nextafter(s2[0, 0], np.float32(1))
+    assert status(codes, s2, counts, None) == 2
+    r = W[0].astype(np.float64)
+    m = _fl32(np.abs(r).max())
+    cands = np.array([_fl32(m * _fl32((g + 1) / G) / 7) for g in range(G)], np.float32)
+    E = [orc.scale_error(r, float(a), bits) for a in cands]
+    worst = int(np.argmax(E))
+    s3 = scales.copy(); s3[0, 0] = cands[worst]
+    c3 = codes.copy(); c3[0, 0] = orc.codes(r, float(cands[worst]), bits)
+    assert status(c3, s3, counts, None) == 3
+    c4 = codes.copy(); c4[0, 0, 7] += 1 if c4[0, 0, 7] < 7 else -1
+    assert status(c4, scales, counts, None) == 4
+    c5 = codes.copy(); c5[0, P - 1, 3] = 1
+    if counts[0] < P:
+        assert status(c5, scales, counts, None) == 5
+    e6 = e32.copy(); e6[0, 0] *= 1.001
+    assert status(codes, scales, counts, e6) == 6
+
+
+ALL_CHECKS = [
+    check_levels, check_rounding_ties, check_codes_bruteforce, check_grid_search_bruteforce,
+    check_grid_search_bounds, check_two_point_joint, check_naive_quantizer,
+    check_equal_magnitudes, check_worked_examples, check_monotone_decrease,
+    check_reconstruct, check_invariances, check_output_error, check_stop_rule,
+    check_exponential_decay, check_verifier,
+]

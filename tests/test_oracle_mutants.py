@@ -1,0 +1,69 @@
+"""Each plausible single mistake in the oracle must fail at least one pin.
+
+A mutant is the oracle's C source with one edit, compiled to a temporary
+library and checked in a child process (so a crash also counts as caught).
+"""
+import os
+import subprocess
+import sys
+
+import pytest
+
+import oracle
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+MUTANTS = [
+    ("ties_away_from_zero", "double q = nearbyint(t);", "double q = round(t);"),
+    ("floor_rounding", "double q = nearbyint(t);", "double q = floor(t);"),
+    ("no_upper_clip", "if (q > (double)M) q = (double)M;", ""),
+    ("levels_off_by_one", "return (1 << (bits - 1)) - 1;", "return (1 << (bits - 1));"),
+    ("argmax_not_argmin", "if (E[g] < E[best]) best = g;", "if (E[g] > E[best]) best = g;"),
+    ("ties_to_largest_scale", "if (E[g] < E[best]) best = g;", "if (E[g] <= E[best]) best = g;"),
+    ("residual_sign", "r[j] = r[j] - as * (double)q[j]; /* Eq. (7) */",
+     "r[j] = r[j] + as * (double)q[j]; /* Eq. (7) */"),
+    ("grid_missing_M", "a[g] = (float)((double)m * (double)c[g] / (double)M);",
+     "a[g] = (float)((double)m * (double)c[g]);"),
+    ("grid_descending", "c[g] = (float)((double)(g + 1) / (double)G);",
+     "c[g] = (float)((double)(G - g) / (double)G);"),
+    ("max_without_abs", "double v = fabs(r[j]);", "double v = r[j];"),
+    ("no_minimum_one_point", "if (n >= 1 && Er <= tol * Ew) return 1;",
+     "if (Er <= tol * Ew) return 1;"),
+    ("strict_stop", "if (n >= 1 && Er <= tol * Ew) return 1;",
+     "if (n >= 1 && Er < tol * Ew) return 1;"),
+    ("stop_ignores_cap", "if (n >= P) return 1;", "if (n > P) return 1;"),
+    ("err_before_update", "err[n - 1] = sum_sq(r, d);", "err[n - 1] = Er;"),
+    ("codes_at_wrong_scale", "oracle_codes(r, d, as, M, q);", "oracle_codes(r, d, (double)a[0], M, q);"),
+    ("x_transposed", "double x = (double)X[j * N + n];", "double x = (double)X[n * d + j];"),
+    ("output_error_not_mean", "err[s] = se / (double)N;", "err[s] = se;"),
+    ("reconstruct_drops_last_point", "for (int i = 0; i < counts[k]; ++i)\n                s = s +",
+     "for (int i = 0; i + 1 < counts[k]; ++i)\n                s = s +"),
+    ("verifier_accepts_any_scale", "if (E[go] <= (1.0 + 1e-6) * E[gbest]) ct++;", "if (1) ct++;"),
+    ("verifier_skips_codes", "if (qo != qr) {", "if (0) {"),
+]
+
+
+@pytest.fixture(scope="module")
+def source():
+    with open(oracle.SRC) as f:
+        return f.read()
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, source, name, old, new):
+    assert source.count(old) == 1, f"mutation site of {name} not unique/present"
+    src = tmp_path / f"{name}.c"
+    src.write_text(source.replace(old, new))
+    lib = oracle.build(force=True, src=str(src), out=str(tmp_path / f"{name}.so"))
+    env = dict(os.environ, OMP_NUM_THREADS="2")
+    p = subprocess.run([sys.executable, os.path.join(HERE, "oracle_mutant_driver.py"), lib],
+                       capture_output=True, text=True, timeout=300, env=env)
+    assert p.returncode != 0, f"mutant {name} passed every pin:\n{p.stdout}\n{p.stderr}"
+
+
+def test_unmutated_oracle_passes_driver():
+    env = dict(os.environ, OMP_NUM_THREADS="2")
+    p = subprocess.run([sys.executable, os.path.join(HERE, "oracle_mutant_driver.py"),
+                        oracle.build(force=False)], capture_output=True, text=True,
+                       timeout=300, env=env)
+    assert p.returncode == 0, p.stdout + p.stderr
