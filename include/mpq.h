@@ -1,0 +1,147 @@
+/*
+ * mpq.h - C ABI of the MI355X (gfx950) multipoint quantization library.
+ *
+ * Multipoint quantization (Liu, Ye, Zhou, Liu, "Post-training Quantization
+ * with Multiple Points: Mixed Precision without Mixed Precision") replaces
+ * each output channel's weight vector w (length d) of a linear or conv layer
+ * by a sum  sum_{i<n} a_i * q_i  of n low-bit integer vectors q_i with fp32
+ * scales a_i (Sec. 3.2, Eq. (4)).
+ *
+ * Conventions shared by every entry point
+ *  - Array arguments are DEVICE pointers (hipMalloc memory or ROCm torch
+ *    tensors) unless the comment says HOST.  Arrays are dense, row-major.
+ *  - The caller owns every buffer.  The library keeps no pointer after the
+ *    stream work of a call has completed.  Outputs must not alias inputs.
+ *  - Calls enqueue work on `stream` (a hipStream_t; NULL = default stream)
+ *    and return without waiting for it.  Argument checks are synchronous and
+ *    happen before anything is enqueued; on an error nothing is enqueued.
+ *  - Results are deterministic: identical inputs give bitwise identical
+ *    outputs.  Calls on distinct streams may run concurrently.
+ *  - Every call returns an MPQ_* status; mpq_last_error() describes the
+ *    last failure of the calling thread.  No C++ exception crosses the ABI.
+ *  - Inputs must be finite.
+ *
+ * Codes and scales (readings of the paper, shared with the test oracle)
+ *  - bits b in [2, 8]; codes are the integers [-M, M] with M = 2^(b-1) - 1,
+ *    i.e. the symmetric set of Eq. (1) with its 2M+1 points, B = 0 and the
+ *    step K * eps_b folded into the scale.  -2^(b-1) is never produced.
+ *  - Rounding to the nearest code (Eq. (2)) breaks exact half-way ties to
+ *    the even integer.
+ */
+#ifndef MPQ_H
+#define MPQ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MPQ_OK 0
+#define MPQ_ERR_INVALID_ARG (-1) /* a null pointer, a size or value out of range */
+#define MPQ_ERR_SHAPE (-2)       /* d (with n_grid) too large for one workgroup's LDS */
+#define MPQ_ERR_HIP (-3)         /* a HIP runtime call failed; see mpq_last_error() */
+#define MPQ_ERR_NOMEM (-4)       /* device scratch allocation failed */
+
+#define MPQ_MAX_BITS 8
+#define MPQ_MAX_POINTS 64
+#define MPQ_MAX_GRID 4096
+
+/*
+ * mpq_fit_layer - greedy multipoint fit of every channel of a layer
+ * (Sec. 3.2, Eq. (6)-(10), Algorithm 1, with the stopping rule of
+ * Algorithm 2 / Eq. (12)).
+ *
+ * For each channel k (row W[k], length d), independently:
+ *   r = w; n = 0
+ *   loop:
+ *     stop if n == max_points, or ||r||^2 == 0, or fl32(max|r|) == 0,
+ *       or (n >= 1 and ||r||^2 <= tol * ||w||^2)
+ *     candidate scales a_g = fl32(fl32(max_j |r_j|) * c_g / M), g = 1..G
+ *     (products and quotient in fp64; Algorithm 1 sets the search grid up
+ *     afresh from the residual at every step)
+ *     a* = argmin_g || r - a_g * clip(round(r / a_g), -M, M) ||^2
+ *          (Eq. (9); exactly equal errors: the smallest g)
+ *     q* = clip(round(r / a*), -M, M)      (Eq. (10), fp64 quotient)
+ *     r  = r - a* q*  (fp64)               (Eq. (7)); n += 1
+ *   The stopping rule reads Algorithm 2's output-error threshold for an
+ *   isotropic calibration distribution (E[x x^T] = I gives
+ *   E (r . x)^2 = ||r||^2), relative to ||w||^2.  A nonzero channel always
+ *   gets at least one point; an all-zero channel gets none.
+ *
+ * Arguments
+ *   W          [c_out][d] fp32 weights (input).
+ *   c_out, d   c_out >= 0 (0: nothing to do), d >= 1.
+ *   bits       2..8.
+ *   max_points 1..MPQ_MAX_POINTS: the per-channel cap on n.
+ *   grid_host  HOST array of n_grid multipliers c_g, strictly ascending,
+ *              each in (0, 1]; NULL selects c_g = g / n_grid (g = 1..n_grid,
+ *              rounded to fp32).  Read before the call returns.
+ *   n_grid     1..MPQ_MAX_GRID: number of candidate scales G.
+ *   tol        relative stopping tolerance, finite and >= 0.
+ *   codes      [c_out][max_points][d] int8 (output).  Rows at or after a
+ *              channel's count are zero.
+ *   scales     [c_out][max_points] fp32 (output), zero after the count.
+ *   counts     [c_out] int32 (output): the number of points n of each channel.
+ *   err_opt    NULL or [c_out][max_points] fp32 (output): ||r||^2 after
+ *              each point (fp64 sum rounded to fp32), zero after the count.
+ *   stream     hipStream_t or NULL.
+ * Errors: MPQ_ERR_INVALID_ARG, MPQ_ERR_SHAPE (see mpq_fit_max_dim),
+ *         MPQ_ERR_NOMEM, MPQ_ERR_HIP.
+ */
+int mpq_fit_layer(const float *W, int64_t c_out, int64_t d, int bits, int max_points,
+                  const float *grid_host, int n_grid, float tol, int8_t *codes,
+                  float *scales, int32_t *counts, float *err_opt, void *stream);
+
+/*
+ * mpq_fit_max_dim - largest channel length d that mpq_fit_layer accepts for
+ * n_grid candidates on the current device (the residual of one channel is
+ * staged in the LDS of one workgroup).  Returns a negative MPQ_* status on
+ * failure.
+ */
+int64_t mpq_fit_max_dim(int n_grid);
+
+/*
+ * mpq_output_error - output error of the quantized layer on a calibration
+ * batch (Sec. 3.3, Eq. (12)):
+ *   err[k] = (1/n) sum_t ( (w_k - w~_k) . x_t )^2,
+ *   ref[k] = (1/n) sum_t ( w_k . x_t )^2          (if ref_opt != NULL)
+ * where w~_k = sum_{i<counts[k]} scales[k][i] * codes[k][i] and x_t is
+ * column t of X.  The difference w_k - w~_k is formed in fp64 and rounded
+ * to fp32; the products run on fp32 MFMA with fp32 accumulation; the sum
+ * over the batch is fp64.
+ *
+ * Arguments
+ *   W, codes, scales, counts   as produced for mpq_fit_layer (inputs);
+ *                              counts[k] in [0, max_points].
+ *   c_out, d, max_points       as for mpq_fit_layer.
+ *   X          [d][n] fp32 calibration inputs (input), n >= 1.
+ *   err        [c_out] fp32 (output).
+ *   ref_opt    NULL or [c_out] fp32 (output).
+ * Errors: MPQ_ERR_INVALID_ARG, MPQ_ERR_NOMEM, MPQ_ERR_HIP.
+ */
+int mpq_output_error(const float *W, const int8_t *codes, const float *scales,
+                     const int32_t *counts, int64_t c_out, int64_t d, int max_points,
+                     const float *X, int64_t n, float *err, float *ref_opt, void *stream);
+
+/*
+ * mpq_reconstruct - the quantized weights of Eq. (4):
+ *   W_hat[k][j] = fl32( sum_{i<counts[k]} scales[k][i] * codes[k][i][j] ),
+ * summed in fp64 in point order.
+ *   codes [c_out][max_points][d] int8, scales [c_out][max_points] fp32,
+ *   counts [c_out] int32 in [0, max_points] (inputs); W_hat [c_out][d] fp32
+ *   (output).
+ * Errors: MPQ_ERR_INVALID_ARG, MPQ_ERR_HIP.
+ */
+int mpq_reconstruct(const int8_t *codes, const float *scales, const int32_t *counts,
+                    int64_t c_out, int64_t d, int max_points, float *W_hat, void *stream);
+
+/* Text of the calling thread's last failure ("" if none).  The pointer stays
+ * valid until the thread's next failing call. */
+const char *mpq_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MPQ_H */

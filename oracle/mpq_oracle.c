@@ -26,8 +26,10 @@
  *          (default c_g = g / G).  Products and the quotient are fp64.
  *   T1     Among exactly equal candidate errors the smallest g wins.
  *   S1-S3  Stop after n points when n == max_points, or ||r||^2 == 0, or
- *          n >= 1 and ||r||^2 <= tol * ||w||^2 (the output error of Eq. (12)
- *          under an isotropic calibration distribution).  A nonzero channel
+ *          every candidate scale rounds to zero in fp32 (zero candidates
+ *          are skipped in the search), or n >= 1
+ *          and ||r||^2 <= tol * ||w||^2 (the output error of Eq. (12) under
+ *          an isotropic calibration distribution).  A nonzero channel
  *          always gets at least one point; an all-zero channel gets none.
  *   A1     No refit of a once q is fixed.
  *   E1     Output error: mean over the N columns of X of ((w - w~) . x)^2.
@@ -102,14 +104,16 @@ static double sum_sq(const double *r, int64_t d)
     return s;
 }
 
-/* Eq. (9) by grid search: errors of all G candidates, best index by T1. */
+/* Eq. (9) by grid search: errors of all G candidates, best index by T1.
+ * A candidate whose fp32 scale is zero is not a scale and is skipped
+ * (E = +inf); returns -1 when every candidate is zero. */
 static int grid_search(const double *r, int64_t d, const float *a, int G, int M,
                        double *E)
 {
-    int best = 0;
+    int best = -1;
     for (int g = 0; g < G; ++g) {
-        E[g] = oracle_scale_error(r, d, (double)a[g], M);
-        if (E[g] < E[best]) best = g;
+        E[g] = a[g] == 0.0f ? INFINITY : oracle_scale_error(r, d, (double)a[g], M);
+        if (a[g] != 0.0f && (best < 0 || E[g] < E[best])) best = g;
     }
     return best;
 }
@@ -137,6 +141,7 @@ static int fit_channel(const float *w, int64_t d, int M, int P, const float *c,
         if (should_stop(n, P, Er, Ew, tol)) break;
         oracle_candidate_scales(r, d, M, c, G, a);
         int g = grid_search(r, d, a, G, M, E);              /* Eq. (9)  */
+        if (g < 0) break;                                   /* S3: no scale */
         double as = (double)a[g];
         int8_t *q = codes + (int64_t)n * d;
         oracle_codes(r, d, as, M, q);                       /* Eq. (10) */
@@ -262,7 +267,13 @@ int oracle_verify(const float *W, int64_t C, int64_t d, int bits, int P,
                         if (rel > emax) emax = rel;
                         if (rel > 1e-5) { st = 6; break; }
                     }
+                    oracle_candidate_scales(r, d, M, c, G, a);
+                    int gbest = -1;
                     int stop_ref = should_stop(n, P, Er, Ew, tol);
+                    if (!stop_ref) {
+                        gbest = grid_search(r, d, a, G, M, E);
+                        stop_ref = gbest < 0;
+                    }
                     int stop_other = (n == n_other);
                     if (stop_ref != stop_other) {
                         double ratio = (tol * Ew) > 0 ? Er / (tol * Ew) : INFINITY;
@@ -272,12 +283,14 @@ int oracle_verify(const float *W, int64_t C, int64_t d, int bits, int P,
                     }
                     if (stop_other) break;
                     /* V1 */
-                    oracle_candidate_scales(r, d, M, c, G, a);
-                    int gbest = grid_search(r, d, a, G, M, E);
+                    if (gbest < 0) {           /* the other side went on past a stop */
+                        gbest = grid_search(r, d, a, G, M, E);
+                        if (gbest < 0) { st = 1; break; }
+                    }
                     float ao = ak[n];
                     int go = -1;
                     for (int g = 0; g < G; ++g)
-                        if (a[g] == ao) { go = g; break; }
+                        if (a[g] == ao && ao != 0.0f) { go = g; break; }
                     if (go < 0) { st = 2; break; }
                     if (go != gbest) {
                         if (E[go] <= (1.0 + 1e-6) * E[gbest]) ct++;

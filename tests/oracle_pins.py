@@ -278,6 +278,13 @@ def check_stop_rule(orc):
     assert c1.tolist() == [1, 1, 0, 1, 1]
     c0 = orc.fit(W, 4, 6, 64, 0.0)[2]
     assert c0.tolist() == [6, 6, 0, 6, 6]
+    # every candidate scale of a channel at the bottom of the fp32 range
+    # rounds to zero (max|w| / 7 is below half the smallest subnormal): no point
+    tiny = np.array([[1e-45, 0.0, -1e-45]], np.float32)
+    assert orc.fit(tiny, 4, 6, 64, 0.0)[2].tolist() == [0]
+    # with bits = 2 (M = 1) the largest candidate equals max|w| and is nonzero
+    c, s, n, e = orc.fit(tiny, 2, 6, 64, 0.0)
+    assert n.tolist() == [1] and s[0, 0] == np.float32(1e-45) and c[0, 0].tolist() == [1, 0, -1]
 
 
 def check_exponential_decay(orc):
