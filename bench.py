@@ -1,0 +1,210 @@
+#!/usr/bin/env python3
+"""Throughput of the multipoint-quantization hot path on one MI355X.
+
+One step = the whole path over one synthetic workload already resident in
+HBM: for every layer, the greedy fit (mpq_fit_layer), the output error on
+the layer's calibration batch (mpq_output_error) and the reconstruction
+(mpq_reconstruct).  The default workload is the ResNet-18-shaped stack
+(21 layers, 5,800 channels, 4 bits, up to 4 points, 256 candidate scales,
+tol 1e-3, 1,024 calibration columns).
+
+Prints one JSON line.  `value` is channel-points fitted per second over the
+whole step (sum of the per-channel point counts of all layers / step time).
+`roofline` describes the kernel with the most time in the timed region,
+measured with HIP events on the stream the kernels run on.  `cpu_baseline`
+times the fp64 CPU oracle on a sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+PEAK_MFMA_F32_TFLOPS = 157.3
+PEAK_VALU_F32_TFLOPS = 157.3            # published (packed) FP32 vector peak
+PEAK_VALU_F32_NONPACKED_TFLOPS = 78.6   # 256 CU x 64 lanes x 2 FLOP x 2.4 GHz
+FLOP_PER_EVAL = 7                       # scale-mul, round, clamp, fma (2), square-acc fma (2)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="resnet18")
+    ap.add_argument("--cpu-stride", type=int, default=1,
+                    help="cpu_baseline fits every n-th channel of every layer")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the fit has no cross-GPU step to measure)", file=sys.stderr, flush=True)
+        return 2
+    import numpy as np
+    import torch
+
+    from paper_2002_09049_amd import mpq, workloads as wl
+
+    assert torch.cuda.is_available(), "bench.py needs a ROCm GPU"
+    mpq.load()
+    wk = wl.get(args.workload)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+
+    # ---- inputs and outputs resident in HBM before the timed region
+    layers = []
+    for li, (C, d) in enumerate(wk.layers):
+        W = torch.from_numpy(wl.layer_weights(wk, li)).to(dev)
+        X = torch.from_numpy(wl.layer_calib(wk, li)).to(dev)
+        P = wk.max_points
+        out = (torch.empty((C, P, d), dtype=torch.int8, device=dev),
+               torch.empty((C, P), dtype=torch.float32, device=dev),
+               torch.empty((C,), dtype=torch.int32, device=dev),
+               torch.empty((C, P), dtype=torch.float32, device=dev))
+        err = torch.empty((C,), dtype=torch.float32, device=dev)
+        what = torch.empty((C, d), dtype=torch.float32, device=dev)
+        layers.append(dict(C=C, d=d, W=W, X=X, out=out, err=err, what=what))
+    torch.cuda.synchronize()
+
+    def step(events=None):
+        for L in layers:
+            e = events.pop() if events is not None else None
+            if e: e[0].record(stream)
+            mpq.fit_layer(L["W"], wk.bits, wk.max_points, wk.n_grid, wk.tol, out=L["out"])
+            if e: e[1].record(stream)
+            codes, scales, counts, _ = L["out"]
+            mpq.output_error(L["W"], codes, scales, counts, L["X"], out=(L["err"], None))
+            if e: e[2].record(stream)
+            mpq.reconstruct(codes, scales, counts, out=L["what"])
+            if e: e[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    nl = len(layers)
+    ev = [[tuple(torch.cuda.Event(enable_timing=True) for _ in range(4)) for _ in range(nl)]
+          for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for s in range(args.steps):
+        step(events=list(reversed(ev[s])))
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_total = t_start.elapsed_time(t_end)
+    ms_step = ms_total / args.steps
+
+    # ---- per-kernel times and algorithmic work
+    t_fit = t_err = t_rec = 0.0
+    for s in range(args.steps):
+        for l in range(nl):
+            e = ev[s][l]
+            t_fit += e[0].elapsed_time(e[1])
+            t_err += e[1].elapsed_time(e[2])
+            t_rec += e[2].elapsed_time(e[3])
+    points = 0
+    evals = 0
+    gemm_flop = 0
+    rec_bytes = 0
+    fit_bytes = 0
+    for L in layers:
+        counts = L["out"][2].cpu().numpy().astype(np.int64)
+        n = int(counts.sum())
+        points += n
+        evals += n * wk.n_grid * L["d"]
+        gemm_flop += 2 * L["C"] * L["d"] * L["X"].shape[1]
+        # reconstruct: read codes of the used points + scales/counts, write fp32
+        rec_bytes += n * L["d"] + 4 * L["C"] * L["d"]
+        # fit (algorithmic): read W once, write the codes of every point
+        fit_bytes += 4 * L["C"] * L["d"] + n * L["d"]
+    steps = args.steps
+    fit_tflops = FLOP_PER_EVAL * evals * steps / (t_fit * 1e-3) / 1e12
+    gemm_tflops = gemm_flop * steps / (t_err * 1e-3) / 1e12
+    rec_gbs = rec_bytes * steps / (t_rec * 1e-3) / 1e9
+    kernels = {
+        "fit": {"bound": "alu", "ms_per_step": t_fit / steps, "achieved": fit_tflops,
+                "peak": PEAK_VALU_F32_TFLOPS, "unit": "TFLOP/s", "frac": fit_tflops / PEAK_VALU_F32_TFLOPS,
+                "frac_of_nonpacked_peak": fit_tflops / PEAK_VALU_F32_NONPACKED_TFLOPS,
+                "evals_per_step": evals, "algorithmic_hbm_bytes_per_step": fit_bytes},
+        "output_error": {"bound": "mfma", "ms_per_step": t_err / steps, "achieved": gemm_tflops,
+                         "peak": PEAK_MFMA_F32_TFLOPS, "unit": "TFLOP/s",
+                         "frac": gemm_tflops / PEAK_MFMA_F32_TFLOPS, "flop_per_step": gemm_flop},
+        "reconstruct": {"bound": "hbm", "ms_per_step": t_rec / steps, "achieved": rec_gbs,
+                        "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": rec_gbs / PEAK_HBM_GBS,
+                        "bytes_per_step": rec_bytes},
+    }
+    dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
+    K = kernels[dom]
+    roofline = {"kernel": dom, "bound": K["bound"], "achieved": round(K["achieved"], 4),
+                "peak": K["peak"], "unit": K["unit"], "frac": round(K["frac"], 5), "traffic": None}
+
+    value = points * steps / (ms_total * 1e-3)
+    res = {
+        "metric": "channel-points fitted/sec (4-bit)",
+        "value": round(value, 1),
+        "unit": "channel-points/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wk.name, "layers": nl, "channels": wk.channels,
+                   "weights": wk.weights, "bits": wk.bits, "max_points": wk.max_points,
+                   "n_grid": wk.n_grid, "tol": wk.tol, "calib_columns": wk.n_calib,
+                   "points_per_step": points, "parallelism": "none"},
+        "roofline": roofline,
+        "kernels": {k: {kk: (round(vv, 5) if isinstance(vv, float) else vv) for kk, vv in v.items()}
+                    for k, v in kernels.items()},
+        "wall_s_timed": round(wall, 3),
+    }
+
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(wk, args.cpu_stride)
+    print(json.dumps(res), flush=True)
+    return 0
+
+
+def cpu_baseline(wk, stride):
+    """The fp64 oracle, as it stands, on every stride-th channel of every layer."""
+    import numpy as np
+
+    import oracle
+    from paper_2002_09049_amd import workloads as wl
+    orc = oracle.load()
+    cores = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    pts = 0
+    secs = 0.0
+    for li in range(len(wk.layers)):
+        W = np.ascontiguousarray(wl.layer_weights(wk, li)[::stride])
+        t0 = time.perf_counter()
+        _, _, counts, _ = orc.fit(W, wk.bits, wk.max_points, wk.n_grid, float(np.float32(wk.tol)),
+                                  n_threads=cores)
+        secs += time.perf_counter() - t0
+        pts += int(counts.sum())
+    return {"value": round(pts / secs, 2), "unit": "channel-points/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"every {stride}th channel of each of the {len(wk.layers)} layers of {wk.name} "
+                      f"({pts} channel-points, {secs:.1f} s wall)"}
+
+
+if __name__ == "__main__":
+    sys.exit(main())

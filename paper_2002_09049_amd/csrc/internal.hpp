@@ -1,0 +1,51 @@
+// Launch interfaces shared by the kernels' translation units and the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mpq {
+
+// Inputs of one greedy fit of a layer (see mpq_fit_layer in mpq.h).
+struct FitParams {
+    const float *W;      // [C][d]
+    int64_t C, d;
+    int M;               // 2^(bits-1) - 1
+    int P;               // max_points
+    const float *grid;   // device [G] multipliers, or nullptr for c_g = g / G
+    int G;
+    double tol;
+    int8_t *codes;       // [C][P][d]
+    float *scales;       // [C][P]
+    int32_t *counts;     // [C]
+    float *err;          // [C][P] or nullptr
+};
+
+// Layout of the dense candidate search in one workgroup (kFitThreads threads).
+struct FitLayout {
+    int lanes;      // threads sharing one element slice (>= 64, a power of two)
+    int slices;     // element slices: kFitThreads / lanes
+    int chunk;      // candidates evaluated per pass: lanes * kCandPerThread
+    int passes;     // ceil(G / chunk)
+    int64_t dpad;   // d rounded up to a multiple of 16 * slices (zero padded)
+    size_t lds;     // dynamic LDS bytes
+};
+
+constexpr int kFitThreads = 256;
+constexpr int kCandPerThread = 2;
+
+FitLayout fit_layout(int64_t d, int G);
+hipError_t launch_fit(const FitParams &p, const FitLayout &L, hipStream_t s);
+
+// Output error of Eq. (12) for a layer; `partial` is scratch of
+// err_partial_bytes(C, n, with_ref) bytes.
+size_t err_partial_bytes(int64_t C, int64_t n, bool with_ref);
+hipError_t launch_output_error(const float *W, const int8_t *codes, const float *scales,
+                               const int32_t *counts, int64_t C, int64_t d, int P,
+                               const float *X, int64_t n, float *err, float *ref,
+                               double *partial, hipStream_t s);
+
+hipError_t launch_reconstruct(const int8_t *codes, const float *scales, const int32_t *counts,
+                              int64_t C, int64_t d, int P, float *W_hat, hipStream_t s);
+
+}  // namespace mpq

@@ -1,0 +1,174 @@
+// Wavefront and workgroup reductions for gfx950 (wave64).
+//
+// Within a wavefront the exchange steps are, in order: DPP quad_perm
+// [1,0,3,2] and [2,3,0,1], DPP row_half_mirror, DPP row_mirror (these
+// combine lanes within a row of 16), ds_swizzle with xor mask 16 (combines
+// the two rows of each half-wave) and finally a readlane of lanes 0 and 32.
+// Every step combines a lane with a partner holding the other half of its
+// group, so with a commutative, associative combine every lane of a group
+// ends with the same value; the result is uniform across the wavefront.
+// Across wavefronts the per-wave results go through LDS and every thread
+// combines them in wave order, so the result is deterministic.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mpq {
+
+constexpr int kWave = 64;
+
+template <int kCtrl>
+__device__ __forceinline__ uint32_t dpp(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, kCtrl, 0xF, 0xF, true);
+}
+
+__device__ __forceinline__ uint32_t swizzle_xor16(uint32_t v)
+{
+    // bitmask mode: and_mask = 0x1f, or_mask = 0, xor_mask = 0x10
+    return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x401F);
+}
+
+// exchange step s (0..4) of a 32-bit value
+template <int kStep>
+__device__ __forceinline__ uint32_t xstep(uint32_t v)
+{
+    if constexpr (kStep == 0) return dpp<0xB1>(v);   // quad_perm [1,0,3,2]
+    else if constexpr (kStep == 1) return dpp<0x4E>(v);  // quad_perm [2,3,0,1]
+    else if constexpr (kStep == 2) return dpp<0x141>(v); // row_half_mirror
+    else if constexpr (kStep == 3) return dpp<0x140>(v); // row_mirror
+    else return swizzle_xor16(v);
+}
+
+template <int kStep>
+__device__ __forceinline__ float xstep(float v)
+{
+    return __uint_as_float(xstep<kStep>(__float_as_uint(v)));
+}
+
+template <int kStep>
+__device__ __forceinline__ double xstep(double v)
+{
+    uint64_t u = (uint64_t)__double_as_longlong(v);
+    uint32_t lo = xstep<kStep>((uint32_t)u), hi = xstep<kStep>((uint32_t)(u >> 32));
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+template <int kStep>
+__device__ __forceinline__ int xstep(int v)
+{
+    return (int)xstep<kStep>((uint32_t)v);
+}
+
+__device__ __forceinline__ float readlane(float v, int l)
+{
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+
+__device__ __forceinline__ double readlane(double v, int l)
+{
+    uint64_t u = (uint64_t)__double_as_longlong(v);
+    uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, l);
+    uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), l);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+__device__ __forceinline__ int readlane(int v, int l)
+{
+    return __builtin_amdgcn_readlane(v, l);
+}
+
+struct MaxOp {
+    template <typename T>
+    __device__ __forceinline__ T operator()(T a, T b) const { return a > b ? a : b; }
+};
+struct SumOp {
+    template <typename T>
+    __device__ __forceinline__ T operator()(T a, T b) const { return a + b; }
+};
+
+// Reduction over the 32 lanes of each half-wave: every lane ends with its
+// half's result.
+template <typename T, typename Op>
+__device__ __forceinline__ T half_wave_reduce(T v, Op op)
+{
+    v = op(v, xstep<0>(v));
+    v = op(v, xstep<1>(v));
+    v = op(v, xstep<2>(v));
+    v = op(v, xstep<3>(v));
+    v = op(v, xstep<4>(v));
+    return v;
+}
+
+// Reduction over the whole wavefront; the result is wave-uniform.
+template <typename T, typename Op>
+__device__ __forceinline__ T wave_reduce(T v, Op op)
+{
+    v = half_wave_reduce(v, op);
+    return op(readlane(v, 0), readlane(v, 32));
+}
+
+// Lexicographic (value, index) minimum: the smaller value, then the smaller
+// index.  Used for the candidate argmin (ties go to the smaller index).
+struct ArgMin {
+    double e;
+    int g;
+};
+
+__device__ __forceinline__ ArgMin argmin_combine(ArgMin a, ArgMin b)
+{
+    return (b.e < a.e || (b.e == a.e && b.g < a.g)) ? b : a;
+}
+
+template <int kStep>
+__device__ __forceinline__ ArgMin xstep(ArgMin v)
+{
+    return ArgMin{xstep<kStep>(v.e), xstep<kStep>(v.g)};
+}
+
+__device__ __forceinline__ ArgMin wave_argmin(ArgMin v)
+{
+    v = argmin_combine(v, xstep<0>(v));
+    v = argmin_combine(v, xstep<1>(v));
+    v = argmin_combine(v, xstep<2>(v));
+    v = argmin_combine(v, xstep<3>(v));
+    v = argmin_combine(v, xstep<4>(v));
+    ArgMin lo{readlane(v.e, 0), readlane(v.g, 0)};
+    ArgMin hi{readlane(v.e, 32), readlane(v.g, 32)};
+    return argmin_combine(lo, hi);
+}
+
+// Workgroup reductions.  `scratch` must hold one T per wavefront and must
+// not be in use by another reduction between the two barriers.
+template <int kThreads, typename T, typename Op>
+__device__ __forceinline__ T block_reduce(T v, Op op, T *scratch)
+{
+    constexpr int kWaves = kThreads / kWave;
+    v = wave_reduce(v, op);
+    const int wid = threadIdx.x / kWave;
+    if ((threadIdx.x % kWave) == 0) scratch[wid] = v;
+    __syncthreads();
+    T r = scratch[0];
+#pragma unroll
+    for (int i = 1; i < kWaves; ++i) r = op(r, scratch[i]);
+    __syncthreads();
+    return r;
+}
+
+template <int kThreads>
+__device__ __forceinline__ ArgMin block_argmin(ArgMin v, ArgMin *scratch)
+{
+    constexpr int kWaves = kThreads / kWave;
+    v = wave_argmin(v);
+    const int wid = threadIdx.x / kWave;
+    if ((threadIdx.x % kWave) == 0) scratch[wid] = v;
+    __syncthreads();
+    ArgMin r = scratch[0];
+#pragma unroll
+    for (int i = 1; i < kWaves; ++i) r = argmin_combine(r, scratch[i]);
+    __syncthreads();
+    return r;
+}
+
+}  // namespace mpq

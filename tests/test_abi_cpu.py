@@ -1,0 +1,96 @@
+"""The C ABI without a GPU: the library loads, exports every entry point that
+include/mpq.h declares, and rejects invalid arguments before touching the
+device (argument checks never call HIP)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mpq.h")
+LIB = os.path.join(ROOT, "paper_2002_09049_amd", "libmpq.so")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mpq_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        from paper_2002_09049_amd import build
+        build.build()
+    from paper_2002_09049_amd import mpq
+    return mpq.load(LIB)
+
+
+def test_header_declares_the_three_calls():
+    names = _declared()
+    for n in ("mpq_fit_layer", "mpq_output_error", "mpq_reconstruct", "mpq_last_error"):
+        assert n in names
+
+
+def test_exports_every_declared_symbol(lib):
+    from paper_2002_09049_amd import mpq
+    for name in _declared():
+        assert hasattr(lib, name), name
+    assert sorted(mpq.EXPORTS) == _declared()
+
+
+def _fit(lib, **kw):
+    args = dict(W=1, c_out=4, d=16, bits=4, max_points=4, grid=None, n_grid=8, tol=1e-3,
+                codes=1, scales=1, counts=1, err=None)
+    args.update(kw)
+    g = args["grid"]
+    garr = None if g is None else (ctypes.c_float * len(g))(*g)
+    return lib.mpq_fit_layer(args["W"], args["c_out"], args["d"], args["bits"],
+                             args["max_points"], garr, args["n_grid"], args["tol"],
+                             args["codes"], args["scales"], args["counts"], args["err"], None)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(c_out=-1), dict(d=0), dict(bits=1), dict(bits=9), dict(max_points=0),
+    dict(max_points=65), dict(n_grid=0), dict(n_grid=4097), dict(tol=-1.0),
+    dict(tol=float("inf")), dict(tol=float("nan")), dict(W=None), dict(codes=None),
+    dict(scales=None), dict(counts=None),
+    dict(grid=[0.5, 0.25], n_grid=2), dict(grid=[0.0, 1.0], n_grid=2),
+    dict(grid=[0.5, 1.5], n_grid=2), dict(grid=[0.5, 0.5], n_grid=2),
+])
+def test_fit_rejects_invalid_arguments(lib, kw):
+    from paper_2002_09049_amd import mpq
+    assert _fit(lib, **kw) == mpq.MPQ_ERR_INVALID_ARG
+    assert lib.mpq_last_error()
+
+
+def test_fit_with_no_channels_is_a_no_op(lib):
+    # c_out = 0 with otherwise valid arguments returns before any device call
+    assert _fit(lib, c_out=0, W=None, codes=None, scales=None, counts=None) == 0
+
+
+def test_output_error_and_reconstruct_reject_invalid_arguments(lib):
+    from paper_2002_09049_amd import mpq
+    E = mpq.MPQ_ERR_INVALID_ARG
+    oe = lib.mpq_output_error
+    assert oe(1, 1, 1, 1, -1, 4, 2, 1, 8, 1, None, None) == E
+    assert oe(1, 1, 1, 1, 4, 0, 2, 1, 8, 1, None, None) == E
+    assert oe(1, 1, 1, 1, 4, 4, 2, 1, 0, 1, None, None) == E
+    assert oe(1, 1, 1, 1, 4, 4, 0, 1, 8, 1, None, None) == E
+    assert oe(1, 1, 1, 1, 4, 4, 2, None, 8, 1, None, None) == E
+    assert oe(1, 1, 1, 1, 4, 4, 2, 1, 8, None, None, None) == E
+    assert oe(None, None, None, None, 0, 4, 2, None, 8, None, None, None) == 0
+    rc = lib.mpq_reconstruct
+    assert rc(1, 1, 1, -1, 4, 2, 1, None) == E
+    assert rc(1, 1, 1, 4, 0, 2, 1, None) == E
+    assert rc(1, 1, 1, 4, 4, 65, 1, None) == E
+    assert b"max_points" in lib.mpq_last_error()
+    assert rc(None, 1, 1, 4, 4, 2, 1, None) == E
+    assert b"NULL" in lib.mpq_last_error()
+    assert rc(None, None, None, 0, 4, 2, None, None) == 0
+
+
+def test_fit_max_dim_rejects_bad_grid(lib):
+    from paper_2002_09049_amd import mpq
+    assert lib.mpq_fit_max_dim(0) == mpq.MPQ_ERR_INVALID_ARG
