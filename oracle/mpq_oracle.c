@@ -216,7 +216,8 @@ int oracle_fit(const float *W, int64_t C, int64_t d, int bits, int P,
  *  V3 the stop decision agrees, except when ||r||^2 / (tol ||w||^2) is
  *     within 1e-6 of 1 (a "stop tie");
  *  V4 the per-point ||r||^2 (if given) agrees within 1e-5 relative (plus
- *     one fp32 subnormal quantum, as it is an fp32 output);
+ *     one fp32 subnormal quantum, as it is an fp32 output) or equals the
+ *     fp32 rounding of the fp64 value;
  * and that every slot at or after the count is zero.  After each accepted
  * step it continues from the other implementation's (a, q).
  * status: 0 ok, 1 count, 2 scale not a candidate, 3 scale not optimal,
@@ -265,11 +266,15 @@ int oracle_verify(const float *W, int64_t C, int64_t d, int bits, int P,
                         /* err is an fp32 output: besides 1e-5 relative, allow
                          * one fp32 subnormal quantum (2^-149), the most its
                          * representation of a value below the normal range
-                         * can be off by. */
+                         * can be off by, and accept fl32(ref) itself (which is
+                         * +inf above the fp32 range). */
                         double ref = Er, got = (double)ek[n - 1];
                         double dev = fabs(got - ref);
                         if (ref >= 0x1p-126 && dev / ref > emax) emax = dev / ref;
-                        if (dev > 1e-5 * ref + 0x1p-149) { st = 6; break; }
+                        if (got != (double)(float)ref && dev > 1e-5 * ref + 0x1p-149) {
+                            st = 6;
+                            break;
+                        }
                     }
                     oracle_candidate_scales(r, d, M, c, G, a);
                     int gbest = -1;
