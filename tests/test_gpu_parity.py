@@ -98,7 +98,9 @@ def test_edge_channels(orc):
         assert_parity(orc, W, bits, P, G, tol, out)
         codes, scales, counts, err = out
         assert counts[0] == 0 and (codes[0] == 0).all() and (scales[0] == 0).all()
-        assert counts[1] == 1
+        if tol > 0:
+            assert counts[1] == 1          # equal magnitudes: one point (closed form)
+        assert counts[5] == (1 if bits == 2 else 0)   # subnormal channel
 
 
 def test_explicit_grid_and_no_err(orc):
