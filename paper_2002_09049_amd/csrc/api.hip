@@ -6,6 +6,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 
 #include "internal.hpp"
@@ -78,6 +79,43 @@ int check_fit_args(const float *W, int64_t c_out, int64_t d, int bits, int max_p
 
 }  // namespace
 
+namespace mpq {
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_pool_mu;
+hipMemPool_t g_pool[kMaxDevices];
+}  // namespace
+
+hipError_t scratch_alloc(void **p, size_t bytes, hipStream_t s)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    hipMemPool_t pool;
+    {
+        std::lock_guard<std::mutex> lk(g_pool_mu);
+        if (!g_pool[dev]) {
+            hipMemPoolProps props = {};
+            props.allocType = hipMemAllocationTypePinned;
+            props.location.type = hipMemLocationTypeDevice;
+            props.location.id = dev;
+            e = hipMemPoolCreate(&g_pool[dev], &props);
+            if (e != hipSuccess) return e;
+            uint64_t keep = ~(uint64_t)0;
+            e = hipMemPoolSetAttribute(g_pool[dev], hipMemPoolAttrReleaseThreshold, &keep);
+            if (e != hipSuccess) return e;
+        }
+        pool = g_pool[dev];
+    }
+    return hipMallocFromPoolAsync(p, bytes == 0 ? 256 : bytes, pool, s);
+}
+
+hipError_t scratch_free(void *p, hipStream_t s) { return hipFreeAsync(p, s); }
+
+}  // namespace mpq
+
 extern "C" {
 
 const char *mpq_last_error(void) { return g_last_error.c_str(); }
@@ -117,11 +155,11 @@ int mpq_fit_layer(const float *W, int64_t c_out, int64_t d, int bits, int max_po
     hipStream_t s = (hipStream_t)stream;
     float *dgrid = nullptr;
     if (grid_host) {
-        hipError_t e = hipMallocAsync((void **)&dgrid, sizeof(float) * (size_t)n_grid, s);
+        hipError_t e = mpq::scratch_alloc((void **)&dgrid, sizeof(float) * (size_t)n_grid, s);
         if (e != hipSuccess) return fail(MPQ_ERR_NOMEM, "grid upload: %s", hipGetErrorString(e));
         e = hipMemcpyAsync(dgrid, grid_host, sizeof(float) * (size_t)n_grid, hipMemcpyHostToDevice, s);
         if (e != hipSuccess) {
-            (void)hipFreeAsync(dgrid, s);
+            (void)mpq::scratch_free(dgrid, s);
             return hip_fail(e, "hipMemcpyAsync(grid)");
         }
     }
@@ -139,7 +177,7 @@ int mpq_fit_layer(const float *W, int64_t c_out, int64_t d, int bits, int max_po
     p.counts = counts;
     p.err = err_opt;
     hipError_t e = mpq::launch_fit(p, L, s);
-    if (dgrid) (void)hipFreeAsync(dgrid, s);
+    if (dgrid) (void)mpq::scratch_free(dgrid, s);
     if (e != hipSuccess) return hip_fail(e, "fit kernel launch");
     return MPQ_OK;
 }
@@ -162,13 +200,13 @@ int mpq_output_error(const float *W, const int8_t *codes, const float *scales,
         return fail(MPQ_ERR_INVALID_ARG, "n too large (%lld)", (long long)n);
     if (c_out == 0) return MPQ_OK;
     hipStream_t s = (hipStream_t)stream;
-    double *partial = nullptr;
-    const size_t bytes = mpq::err_partial_bytes(c_out, n, ref_opt != nullptr);
-    hipError_t e = hipMallocAsync((void **)&partial, bytes, s);
+    void *scratch = nullptr;
+    const size_t bytes = mpq::err_scratch_bytes(c_out, d, n);
+    hipError_t e = mpq::scratch_alloc(&scratch, bytes, s);
     if (e != hipSuccess) return fail(MPQ_ERR_NOMEM, "scratch of %zu bytes: %s", bytes, hipGetErrorString(e));
     e = mpq::launch_output_error(W, codes, scales, counts, c_out, d, max_points, X, n, err, ref_opt,
-                                 partial, s);
-    (void)hipFreeAsync(partial, s);
+                                 scratch, s);
+    (void)mpq::scratch_free(scratch, s);
     if (e != hipSuccess) return hip_fail(e, "output error kernel launch");
     return MPQ_OK;
 }

@@ -37,13 +37,18 @@ constexpr int kCandPerThread = 2;
 FitLayout fit_layout(int64_t d, int G);
 hipError_t launch_fit(const FitParams &p, const FitLayout &L, hipStream_t s);
 
-// Output error of Eq. (12) for a layer; `partial` is scratch of
-// err_partial_bytes(C, n, with_ref) bytes.
-size_t err_partial_bytes(int64_t C, int64_t n, bool with_ref);
+// Output error of Eq. (12) for a layer; `scratch` holds
+// err_scratch_bytes(C, d, n) bytes (256-byte aligned).
+size_t err_scratch_bytes(int64_t C, int64_t d, int64_t n);
 hipError_t launch_output_error(const float *W, const int8_t *codes, const float *scales,
                                const int32_t *counts, int64_t C, int64_t d, int P,
                                const float *X, int64_t n, float *err, float *ref,
-                               double *partial, hipStream_t s);
+                               void *scratch, hipStream_t s);
+
+// Stream-ordered scratch from a library-owned memory pool of the current
+// device (kept, not returned to the system, between calls).
+hipError_t scratch_alloc(void **p, size_t bytes, hipStream_t s);
+hipError_t scratch_free(void *p, hipStream_t s);
 
 hipError_t launch_reconstruct(const int8_t *codes, const float *scales, const int32_t *counts,
                               int64_t C, int64_t d, int P, float *W_hat, hipStream_t s);
