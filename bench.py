@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--cpu-stride", type=int, default=1,
                     help="cpu_baseline fits every n-th channel of every layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--dense", action="store_true",
+                    help="fit with mpq_fit_layer_dense (O(d G) search) instead of mpq_fit_layer")
     return ap.parse_args()
 
 
@@ -81,7 +83,8 @@ def main():
         for L in layers:
             e = events.pop() if events is not None else None
             if e: e[0].record(stream)
-            mpq.fit_layer(L["W"], wk.bits, wk.max_points, wk.n_grid, wk.tol, out=L["out"])
+            mpq.fit_layer(L["W"], wk.bits, wk.max_points, wk.n_grid, wk.tol, out=L["out"],
+                          dense=args.dense)
             if e: e[1].record(stream)
             codes, scales, counts, _ = L["out"]
             mpq.output_error(L["W"], codes, scales, counts, L["X"], out=(L["err"], None))

@@ -55,13 +55,14 @@ extern "C" {
  * For each channel k (row W[k], length d), independently:
  *   r = w; n = 0
  *   loop:
- *     stop if n == max_points, or ||r||^2 == 0, or fl32(max|r|) == 0,
+ *     stop if n == max_points, or ||r||^2 == 0,
  *       or (n >= 1 and ||r||^2 <= tol * ||w||^2)
  *     candidate scales a_g = fl32(fl32(max_j |r_j|) * c_g / M), g = 1..G
  *     (products and quotient in fp64; Algorithm 1 sets the search grid up
  *     afresh from the residual at every step)
  *     a* = argmin_g || r - a_g * clip(round(r / a_g), -M, M) ||^2
- *          (Eq. (9); exactly equal errors: the smallest g)
+ *          (Eq. (9); exactly equal errors: the smallest g; a candidate that
+ *          rounds to 0 in fp32 is skipped, and if all do the fit stops)
  *     q* = clip(round(r / a*), -M, M)      (Eq. (10), fp64 quotient)
  *     r  = r - a* q*  (fp64)               (Eq. (7)); n += 1
  *   The stopping rule reads Algorithm 2's output-error threshold for an
@@ -94,10 +95,30 @@ int mpq_fit_layer(const float *W, int64_t c_out, int64_t d, int bits, int max_po
                   float *scales, int32_t *counts, float *err_opt, void *stream);
 
 /*
+ * How mpq_fit_layer evaluates Eq. (9): for d <= 16384 it counts, per element
+ * and code level k, the candidates whose boundary (k + 1/2) a_g lies below
+ * |r_j|, accumulates exact integer histograms, and gets every candidate's
+ * error from ||r||^2 - 2 a A(g) + a^2 B(g) in fp64 (A, B: suffix sums), in
+ * O(d M + G) per step; candidates whose error bound overlaps the minimum are
+ * re-evaluated directly in fp64.  Longer channels use the dense search of
+ * mpq_fit_layer_dense.
+ *
+ * mpq_fit_layer_dense - mpq_fit_layer with the dense candidate search:
+ * every (element, candidate) pair is evaluated in fp32 on the residual
+ * staged in LDS, with fp64 sums of 16-element blocks, in O(d G) per step.
+ * Same arguments, outputs and errors as mpq_fit_layer; the two agree except
+ * where the top-2 candidate errors lie within fp32 rounding of each other.
+ */
+int mpq_fit_layer_dense(const float *W, int64_t c_out, int64_t d, int bits, int max_points,
+                        const float *grid_host, int n_grid, float tol, int8_t *codes,
+                        float *scales, int32_t *counts, float *err_opt, void *stream);
+
+/*
  * mpq_fit_max_dim - largest channel length d that mpq_fit_layer accepts for
- * n_grid candidates on the current device (the residual of one channel is
- * staged in the LDS of one workgroup).  Returns a negative MPQ_* status on
- * failure.
+ * n_grid candidates on the current device: the larger of 16384 (the
+ * histogram search keeps a channel's residual in the registers of one
+ * workgroup) and the dense search's limit (the residual staged in the LDS of
+ * one workgroup).  Returns a negative MPQ_* status on failure.
  */
 int64_t mpq_fit_max_dim(int n_grid);
 

@@ -120,14 +120,13 @@ extern "C" {
 
 const char *mpq_last_error(void) { return g_last_error.c_str(); }
 
-int64_t mpq_fit_max_dim(int n_grid)
+}  // extern "C"
+
+namespace {
+
+int64_t dense_max_dim(int n_grid, size_t lim)
 {
-    if (n_grid < 1 || n_grid > MPQ_MAX_GRID)
-        return fail(MPQ_ERR_INVALID_ARG, "n_grid must be in [1, %d] (got %d)", MPQ_MAX_GRID, n_grid);
-    size_t lim = 0;
-    int rc = device_lds_limit(&lim);
-    if (rc != MPQ_OK) return rc;
-    // bisect the largest d whose layout fits
+    // bisect the largest d whose dense layout fits
     int64_t lo = 0, hi = 1 << 22;
     while (lo < hi) {
         const int64_t mid = (lo + hi + 1) / 2;
@@ -137,19 +136,23 @@ int64_t mpq_fit_max_dim(int n_grid)
     return lo;
 }
 
-int mpq_fit_layer(const float *W, int64_t c_out, int64_t d, int bits, int max_points,
-                  const float *grid_host, int n_grid, float tol, int8_t *codes, float *scales,
-                  int32_t *counts, float *err_opt, void *stream)
+enum class Search { kAuto, kDense };
+
+int fit_layer_impl(Search mode, const float *W, int64_t c_out, int64_t d, int bits, int max_points,
+                   const float *grid_host, int n_grid, float tol, int8_t *codes, float *scales,
+                   int32_t *counts, float *err_opt, void *stream)
 {
     int rc = check_fit_args(W, c_out, d, bits, max_points, grid_host, n_grid, tol, codes, scales,
                             counts);
     if (rc != MPQ_OK) return rc;
     if (c_out == 0) return MPQ_OK;
-    const mpq::FitLayout L = mpq::fit_layout(d, n_grid);
     size_t lim = 0;
     rc = device_lds_limit(&lim);
     if (rc != MPQ_OK) return rc;
-    if (L.lds > lim)
+    const bool hist = mode == Search::kAuto && mpq::fit_hist_supports(d) &&
+                      mpq::fit_hist_lds(n_grid) <= lim;
+    const mpq::FitLayout L = mpq::fit_layout(d, n_grid);
+    if (!hist && L.lds > lim)
         return fail(MPQ_ERR_SHAPE, "d = %lld with n_grid = %d needs %zu bytes of LDS (limit %zu)",
                     (long long)d, n_grid, L.lds, lim);
     hipStream_t s = (hipStream_t)stream;
@@ -176,10 +179,42 @@ int mpq_fit_layer(const float *W, int64_t c_out, int64_t d, int bits, int max_po
     p.scales = scales;
     p.counts = counts;
     p.err = err_opt;
-    hipError_t e = mpq::launch_fit(p, L, s);
+    hipError_t e = hist ? mpq::launch_fit_hist(p, s) : mpq::launch_fit(p, L, s);
     if (dgrid) (void)mpq::scratch_free(dgrid, s);
     if (e != hipSuccess) return hip_fail(e, "fit kernel launch");
     return MPQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t mpq_fit_max_dim(int n_grid)
+{
+    if (n_grid < 1 || n_grid > MPQ_MAX_GRID)
+        return fail(MPQ_ERR_INVALID_ARG, "n_grid must be in [1, %d] (got %d)", MPQ_MAX_GRID, n_grid);
+    size_t lim = 0;
+    int rc = device_lds_limit(&lim);
+    if (rc != MPQ_OK) return rc;
+    int64_t dmax = dense_max_dim(n_grid, lim);
+    if (mpq::fit_hist_lds(n_grid) <= lim && mpq::kHistMaxDim > dmax) dmax = mpq::kHistMaxDim;
+    return dmax;
+}
+
+int mpq_fit_layer(const float *W, int64_t c_out, int64_t d, int bits, int max_points,
+                  const float *grid_host, int n_grid, float tol, int8_t *codes, float *scales,
+                  int32_t *counts, float *err_opt, void *stream)
+{
+    return fit_layer_impl(Search::kAuto, W, c_out, d, bits, max_points, grid_host, n_grid, tol,
+                          codes, scales, counts, err_opt, stream);
+}
+
+int mpq_fit_layer_dense(const float *W, int64_t c_out, int64_t d, int bits, int max_points,
+                        const float *grid_host, int n_grid, float tol, int8_t *codes,
+                        float *scales, int32_t *counts, float *err_opt, void *stream)
+{
+    return fit_layer_impl(Search::kDense, W, c_out, d, bits, max_points, grid_host, n_grid, tol,
+                          codes, scales, counts, err_opt, stream);
 }
 
 int mpq_output_error(const float *W, const int8_t *codes, const float *scales,

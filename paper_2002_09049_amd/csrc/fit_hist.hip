@@ -1,0 +1,320 @@
+// Greedy multipoint fit (Algorithm 1, Sec. 3.2, with the stopping rule of
+// Algorithm 2, Sec. 3.3) with an exact O(d*M + G) evaluation of the
+// candidate errors of Eq. (9).
+//
+// For a candidate scale a and x = |r_j|, the code magnitude of element j is
+// the number of levels k in [0, M) whose boundary (k + 1/2) a lies below x
+// (Eq. (2); an exact half-way point gives the same error either way, so the
+// boundary may be taken as strict).  The candidates are sorted
+// (a_g = fl32(m c_g / M) with c_g ascending), so for each (j, k) the
+// candidates that lift element j past level k are a prefix g < n_jk with
+//     n_jk = #{ g : (k + 1/2) a_g < x_j }       ((k+1/2) a_g is exact in fp64).
+// With A(g) = sum_j x_j |q_j(g)| and B(g) = sum_j q_j(g)^2,
+//     E(g) = ||r||^2 - 2 a_g A(g) + a_g^2 B(g),
+// and A, B are suffix sums of histograms that receive, per (j, k) with
+// n_jk > 0, x_j (in 64-bit fixed point) and 2k + 1 at bin n_jk - 1.  Integer
+// LDS atomics make the histograms exact and order independent.  Every E(g)
+// carries an error bound; the candidates whose interval reaches the minimum
+// are re-evaluated directly (fp64, like Eq. (9) written out) and the smallest
+// error wins, ties to the smallest g.
+//
+// One workgroup per channel.  The fp64 residual stays in registers for the
+// whole fit (EPT elements per thread, element j = t + T * u), so each step
+// reads nothing from HBM: it writes the codes of the point chosen by the
+// previous step (Eq. (10), fp64 quotient) and updates the residual (Eq. (7)).
+#include <math.h>
+
+#include "internal.hpp"
+#include "mpq.h"
+#include "reduce.hpp"
+
+namespace mpq {
+
+namespace {
+
+constexpr int kMaxFinalists = 8;
+
+struct HistShared {
+    float *a;        // [G] candidate scales
+    long long *ha;   // [G] fixed-point sum of x per bin
+    int *hb;         // [G] sum of (2k + 1) per bin
+    double *e;       // [G] approximate candidate errors
+    double *bnd;     // [G] their error bounds
+};
+
+// n = #{ g : h * a_g < x } over a non-decreasing table a[0..G).
+__device__ __forceinline__ int count_below(const float *a, int G, double h, double x, bool linear,
+                                           float est)
+{
+    if (linear) {
+        int n = (int)fminf(fmaxf(est, 0.0f), (float)G);
+        while (n < G && h * (double)a[n] < x) ++n;
+        while (n > 0 && h * (double)a[n - 1] >= x) --n;
+        return n;
+    }
+    int lo = 0, hi = G;
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (h * (double)a[mid] < x) lo = mid + 1;
+        else hi = mid;
+    }
+    return lo;
+}
+
+template <int T, int EPT>
+__global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
+{
+    constexpr int kWaves = T / kWave;
+    extern __shared__ __align__(16) double hsmem[];
+    __shared__ float s_redf[kWaves];
+    __shared__ double s_redd[kWaves];
+    __shared__ int s_fin[kMaxFinalists];
+    __shared__ int s_nfin;
+    __shared__ int s_gbest;
+
+    const int G = p.G;
+    HistShared S;
+    S.e = hsmem;
+    S.bnd = S.e + G;
+    S.ha = (long long *)(S.bnd + G);
+    S.a = (float *)(S.ha + G);
+    S.hb = (int *)(S.a + G);
+
+    const int64_t k = blockIdx.x;
+    const int t = threadIdx.x;
+    const int d = (int)p.d;          // <= kHistMaxDim; per-channel offsets fit 32 bits
+    const int P = p.P;
+    const int M = p.M;
+    const double Md = (double)M;
+    const bool linear = p.grid == nullptr;
+    int8_t *qk = p.codes + k * (int64_t)P * d;
+    const float *wk = p.W + k * (int64_t)d;
+
+    double r[EPT];
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+        const int j = t + T * u;
+        r[u] = j < d ? (double)wk[j] : 0.0;
+    }
+
+    double Ew = 0.0;
+    float apend = 0.0f;
+    int n = 0;
+    for (int i = 0;; ++i) {
+        // ---- apply the pending point: codes of Eq. (10), residual of Eq. (7)
+        float lmax = 0.0f;
+        double lsum = 0.0;
+        int8_t *qrow = qk + (int64_t)(i - 1) * d;
+#pragma unroll
+        for (int u = 0; u < EPT; ++u) {
+            const int j = t + T * u;
+            if (i >= 1 && j < d) {
+                double c = rint(r[u] / (double)apend);
+                c = fmin(fmax(c, -Md), Md);
+                qrow[j] = (int8_t)(int)c;
+                r[u] = fma(-(double)apend, c, r[u]);
+            }
+            lmax = fmaxf(lmax, fabsf((float)r[u]));
+            lsum = fma(r[u], r[u], lsum);
+        }
+        const float m = block_reduce<T>(lmax, MaxOp(), s_redf);
+        const double Er = block_reduce<T>(lsum, SumOp(), s_redd);
+
+        // ---- stop / point count
+        if (i == 0) Ew = Er;
+        else if (p.err && t == 0) p.err[k * P + (i - 1)] = (float)Er;
+        if ((i >= P) || (Er == 0.0) || (i >= 1 && Er <= p.tol * Ew)) {
+            n = i;
+            break;
+        }
+
+        // ---- candidates, cleared histograms
+        for (int g = t; g < G; g += T) {
+            const float c = p.grid ? p.grid[g] : (float)((double)(g + 1) / (double)G);
+            S.a[g] = (float)((double)m * (double)c / Md);
+            S.ha[g] = 0;
+            S.hb[g] = 0;
+        }
+        // fixed-point shift: every x < 2^(ex+1); sums of up to M*d values < 2^62
+        int ex = 0;
+        (void)frexpf(m, &ex);
+        int lg = 0;
+        while ((1LL << lg) < (long long)M * d) ++lg;
+        const int sh = 61 - (ex + 1) - lg;
+        __syncthreads();
+
+        // ---- histograms of the level boundaries
+#pragma unroll
+        for (int u = 0; u < EPT; ++u) {
+            const double x = fabs(r[u]);
+            if (x > 0.0) {
+                const long long X = (long long)rint(ldexp(x, sh));
+                // estimate of n for the default grid a_g ~ m (g+1) / (G M)
+                const float xe = (float)x * ((float)G * (float)M / m);
+                for (int kk = 0; kk < M; ++kk) {
+                    const double h = (double)kk + 0.5;
+                    const int nb = count_below(S.a, G, h, x, linear, xe / (float)h);
+                    if (nb == 0) break;
+                    atomicAdd((unsigned long long *)&S.ha[nb - 1], (unsigned long long)X);
+                    atomicAdd(&S.hb[nb - 1], 2 * kk + 1);
+                }
+            }
+        }
+        __syncthreads();
+
+        // ---- wavefront 0: suffix sums, candidate errors and bounds, argmin
+        const double q2 = ldexp(1.0, -sh);
+        const double slack = Md * (double)d * q2;   // fixed-point error of A, per unit a
+        if (t < kWave) {
+            const int per = (G + kWave - 1) / kWave;
+            const int g0 = t * per, g1 = min(g0 + per, G);
+            long long la = 0;
+            int lb = 0;
+            for (int g = g0; g < g1; ++g) {
+                la += S.ha[g];
+                lb += S.hb[g];
+            }
+            // exclusive suffix over lanes
+            long long sa = la;
+            int sb = lb;
+#pragma unroll
+            for (int off = 1; off < kWave; off <<= 1) {
+                const long long oa = __shfl_down(sa, off);
+                const int ob = __shfl_down(sb, off);
+                if (t + off < kWave) {
+                    sa += oa;
+                    sb += ob;
+                }
+            }
+            long long A = sa - la;
+            int B = sb - lb;
+            ArgMin best{INFINITY, 0x7fffffff};
+            for (int g = g1 - 1; g >= g0; --g) {
+                A += S.ha[g];
+                B += S.hb[g];
+                const double a = (double)S.a[g];
+                double e = INFINITY, b = 0.0;
+                if (a != 0.0) {
+                    const double Ad = ldexp((double)A, -sh);
+                    const double t2 = 2.0 * a * Ad, t3 = a * a * (double)B;
+                    e = (Er - t2) + t3;
+                    b = a * slack + 8.0 * 0x1p-53 * (Er + t2 + t3);
+                }
+                S.e[g] = e;
+                S.bnd[g] = b;
+                if (e < best.e || (e == best.e && g < best.g)) best = ArgMin{e, g};
+            }
+            best = wave_argmin(best);
+            // finalists: candidates whose interval reaches the best one's
+            const double thr = best.e == INFINITY ? INFINITY : best.e + S.bnd[best.g];
+            int cnt = 0;
+            for (int g = g0; g < g1; ++g)
+                if (S.e[g] != INFINITY && S.e[g] - S.bnd[g] <= thr) ++cnt;
+            cnt = wave_reduce(cnt, SumOp());
+            if (t == 0) {
+                s_gbest = best.e == INFINITY ? -1 : best.g;
+                s_nfin = cnt;
+            }
+            if (cnt > 1) {
+                // up to kMaxFinalists, smallest (E, g) first
+                int nf = 0;
+                double last_e = -INFINITY;
+                int last_g = -1;
+                for (; nf < kMaxFinalists && nf < cnt; ++nf) {
+                    ArgMin c{INFINITY, 0x7fffffff};
+                    for (int g = g0; g < g1; ++g) {
+                        const double e = S.e[g];
+                        if (e == INFINITY || e - S.bnd[g] > thr) continue;
+                        const bool after = e > last_e || (e == last_e && g > last_g);
+                        if (after && (e < c.e || (e == c.e && g < c.g))) c = ArgMin{e, g};
+                    }
+                    c = wave_argmin(c);
+                    if (t == 0) s_fin[nf] = c.g;
+                    last_e = c.e;
+                    last_g = c.g;
+                }
+                if (t == 0) s_nfin = nf;
+            }
+        }
+        __syncthreads();
+
+        int gstar = s_gbest;
+        const int nfin = s_nfin;
+        if (gstar >= 0 && nfin > 1) {
+            // direct fp64 evaluation of the finalists (Eq. (9) written out)
+            ArgMin best{INFINITY, 0x7fffffff};
+            for (int f = 0; f < nfin; ++f) {
+                const int g = s_fin[f];
+                const double a = (double)S.a[g];
+                double le = 0.0;
+#pragma unroll
+                for (int u = 0; u < EPT; ++u) {
+                    // signed form: (r - a q)^2 with q = clip(rne(r / a)) equals
+                    // (|r| - a |q|)^2, and keeps |r| from being hoisted per element
+                    const double c = fmin(fmax(rint(r[u] / a), -Md), Md);
+                    const double e = r[u] - a * c;
+                    le = fma(e, e, le);
+                }
+                const double E = block_reduce<T>(le, SumOp(), s_redd);
+                if (E < best.e || (E == best.e && g < best.g)) best = ArgMin{E, g};
+            }
+            gstar = best.g;
+        }
+        if (gstar < 0) {   // every candidate scale is zero
+            n = i;
+            break;
+        }
+        apend = S.a[gstar];
+        if (t == 0) p.scales[k * P + i] = apend;
+        __syncthreads();   // S.a is rewritten by the next step
+    }
+
+    if (t == 0) p.counts[k] = n;
+    for (int q = n + t; q < P; q += T) {
+        p.scales[k * P + q] = 0.0f;
+        if (p.err) p.err[k * P + q] = 0.0f;
+    }
+    for (int q = n; q < P; ++q)
+        for (int j = t; j < d; j += T) qk[(int64_t)q * d + j] = 0;
+}
+
+template <int T, int EPT>
+hipError_t launch_hist_t(const FitParams &p, size_t lds, hipStream_t s)
+{
+    auto kern = fit_hist_kernel<T, EPT>;
+    if (lds > 65536) {
+        hipError_t e = hipFuncSetAttribute((const void *)kern,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(kern, dim3((unsigned)p.C), dim3(T), lds, s, p);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+size_t fit_hist_lds(int G)
+{
+    return (size_t)G * (2 * sizeof(double) + sizeof(long long) + sizeof(float) + sizeof(int));
+}
+
+bool fit_hist_supports(int64_t d) { return d <= kHistMaxDim; }
+
+hipError_t launch_fit_hist(const FitParams &p, hipStream_t s)
+{
+    const size_t lds = fit_hist_lds(p.G);
+    const int64_t d = p.d;
+    if (d <= 64) return launch_hist_t<64, 1>(p, lds, s);
+    if (d <= 128) return launch_hist_t<64, 2>(p, lds, s);
+    if (d <= 256) return launch_hist_t<64, 4>(p, lds, s);
+    if (d <= 512) return launch_hist_t<256, 2>(p, lds, s);
+    if (d <= 1024) return launch_hist_t<256, 4>(p, lds, s);
+    if (d <= 2048) return launch_hist_t<256, 8>(p, lds, s);
+    if (d <= 4096) return launch_hist_t<256, 16>(p, lds, s);
+    // 512 threads leave 256 VGPRs per thread for the register-resident residual
+    if (d <= 8192) return launch_hist_t<512, 16>(p, lds, s);
+    if (d <= kHistMaxDim) return launch_hist_t<512, 32>(p, lds, s);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace mpq

@@ -34,8 +34,16 @@ struct FitLayout {
 constexpr int kFitThreads = 256;
 constexpr int kCandPerThread = 2;
 
+// Dense search: residual staged in LDS, every (element, candidate) pair
+// evaluated in fp32 with fp64 block sums.
 FitLayout fit_layout(int64_t d, int G);
 hipError_t launch_fit(const FitParams &p, const FitLayout &L, hipStream_t s);
+
+// Histogram search: exact O(d M + G) candidate errors, residual in registers.
+constexpr int64_t kHistMaxDim = 16384;
+size_t fit_hist_lds(int G);
+bool fit_hist_supports(int64_t d);
+hipError_t launch_fit_hist(const FitParams &p, hipStream_t s);
 
 // Output error of Eq. (12) for a layer; `scratch` holds
 // err_scratch_bytes(C, d, n) bytes (256-byte aligned).

@@ -28,8 +28,8 @@ MPQ_ERR_NOMEM = -4
 MAX_POINTS = 64
 MAX_GRID = 4096
 
-EXPORTS = ("mpq_fit_layer", "mpq_fit_max_dim", "mpq_output_error", "mpq_reconstruct",
-           "mpq_last_error")
+EXPORTS = ("mpq_fit_layer", "mpq_fit_layer_dense", "mpq_fit_max_dim", "mpq_output_error",
+           "mpq_reconstruct", "mpq_last_error")
 
 _lib = None
 
@@ -49,8 +49,9 @@ def load(path: str = LIB_PATH):
         raise ImportError(f"{path} is missing; build it with `python -m paper_2002_09049_amd.build`")
     lib = ctypes.CDLL(path)
     P, i64, i32, f32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float
-    lib.mpq_fit_layer.argtypes = [P, i64, i64, i32, i32, P, i32, f32, P, P, P, P, P]
-    lib.mpq_fit_layer.restype = i32
+    for name in ("mpq_fit_layer", "mpq_fit_layer_dense"):
+        getattr(lib, name).argtypes = [P, i64, i64, i32, i32, P, i32, f32, P, P, P, P, P]
+        getattr(lib, name).restype = i32
     lib.mpq_fit_max_dim.argtypes = [i32]
     lib.mpq_fit_max_dim.restype = i64
     lib.mpq_output_error.argtypes = [P, P, P, P, i64, i64, i32, P, i64, P, P, P]
@@ -88,8 +89,8 @@ def _stream(stream) -> int:
 
 
 def fit_layer(W: torch.Tensor, bits: int, max_points: int, n_grid: int, tol: float,
-              grid=None, with_err: bool = True, stream=None, out=None):
-    """mpq_fit_layer.  W: [C, d] fp32 on the device.
+              grid=None, with_err: bool = True, stream=None, out=None, dense: bool = False):
+    """mpq_fit_layer (mpq_fit_layer_dense with dense=True).  W: [C, d] fp32 on the device.
 
     Returns (codes [C, P, d] int8, scales [C, P] fp32, counts [C] int32,
     err [C, P] fp32 or None).  ``grid`` is an optional host sequence of
@@ -114,7 +115,8 @@ def fit_layer(W: torch.Tensor, bits: int, max_points: int, n_grid: int, tol: flo
             raise ValueError("grid must have n_grid entries")
         gbuf = g
     lib = load()
-    rc = lib.mpq_fit_layer(_dev(W, torch.float32, "W"), C, d, bits, max_points,
+    fn = lib.mpq_fit_layer_dense if dense else lib.mpq_fit_layer
+    rc = fn(_dev(W, torch.float32, "W"), C, d, bits, max_points,
                            None if gbuf is None else gbuf.ctypes.data_as(ctypes.c_void_p),
                            n_grid, float(tol), _dev(codes, torch.int8, "codes"),
                            _dev(scales, torch.float32, "scales"),

@@ -17,11 +17,14 @@ def to_dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-def gpu_fit(W, bits, P, G, tol, grid=None, with_err=True):
+def gpu_fit(W, bits, P, G, tol, grid=None, with_err=True, dense=False):
+    """mpq_fit_layer (histogram search up to d = 16384) or, with dense=True,
+    mpq_fit_layer_dense, through the C ABI."""
     import torch
     from paper_2002_09049_amd import mpq
     Wd = to_dev(W)
-    codes, scales, counts, err = mpq.fit_layer(Wd, bits, P, G, tol, grid=grid, with_err=with_err)
+    codes, scales, counts, err = mpq.fit_layer(Wd, bits, P, G, tol, grid=grid, with_err=with_err,
+                                               dense=dense)
     torch.cuda.synchronize()
     return (codes.cpu().numpy(), scales.cpu().numpy(), counts.cpu().numpy(),
             None if err is None else err.cpu().numpy())

@@ -67,11 +67,12 @@ SWEEP = [
 ]
 
 
+@pytest.mark.parametrize("dense", [False, True], ids=["hist", "dense"])
 @pytest.mark.parametrize("C,d,bits,P,G,tol", SWEEP, ids=[f"C{c}_d{d}_b{b}_P{p}_G{g}" for c, d, b, p, g, _ in SWEEP])
-def test_parity_sweep(orc, C, d, bits, P, G, tol):
-    say(f"case sweep C={C} d={d} bits={bits} P={P} G={G} tol={tol}")
+def test_parity_sweep(orc, C, d, bits, P, G, tol, dense):
+    say(f"case sweep C={C} d={d} bits={bits} P={P} G={G} tol={tol} dense={dense}")
     W = wl.random_weights(C, d, seed=C * 1000 + d)
-    out = gpu_fit(W, bits, P, G, tol)
+    out = gpu_fit(W, bits, P, G, tol, dense=dense)
     v = assert_parity(orc, W, bits, P, G, tol, out)
     ties = int(v["cand_ties"].sum() + v["code_ties"].sum() + v["stop_ties"].sum())
     nd = free_running_diff(orc, W, bits, P, G, tol, out)
@@ -93,8 +94,10 @@ def test_edge_channels(orc):
     W[6] = rng.standard_normal(d)
     W[6, ::2] = W[6, 1::2]                                    # repeated values
     W[7] = np.arange(d, dtype=np.float32) / 7.0
-    for bits, G, P, tol in ((4, 128, 4, 1e-3), (2, 64, 6, 0.0), (8, 32, 2, 0.0)):
-        out = gpu_fit(W, bits, P, G, tol)
+    for (bits, G, P, tol), dense in [(c, dn) for c in ((4, 128, 4, 1e-3), (2, 64, 6, 0.0), (8, 32, 2, 0.0))
+                                     for dn in (False, True)]:
+        say(f"  bits={bits} G={G} P={P} tol={tol} dense={dense}")
+        out = gpu_fit(W, bits, P, G, tol, dense=dense)
         assert_parity(orc, W, bits, P, G, tol, out)
         codes, scales, counts, err = out
         assert counts[0] == 0 and (codes[0] == 0).all() and (scales[0] == 0).all()
@@ -103,25 +106,54 @@ def test_edge_channels(orc):
         assert counts[5] == (1 if bits == 2 else 0)   # subnormal channel
 
 
-def test_explicit_grid_and_no_err(orc):
-    say("case explicit grid, err=NULL")
+@pytest.mark.parametrize("dense", [False, True], ids=["hist", "dense"])
+def test_explicit_grid_and_no_err(orc, dense):
+    say(f"case explicit grid, err=NULL, dense={dense}")
     W = wl.random_weights(32, 300, seed=77)
     grid = np.sort(np.random.default_rng(3).uniform(0.05, 1.0, 37)).astype(np.float32)
     grid[-1] = 1.0
-    out = gpu_fit(W, 4, 5, 37, 1e-4, grid=grid)
+    out = gpu_fit(W, 4, 5, 37, 1e-4, grid=grid, dense=dense)
     assert_parity(orc, W, 4, 5, 37, 1e-4, out, grid=grid)
-    out2 = gpu_fit(W, 4, 5, 37, 1e-4, grid=grid, with_err=False)
+    out2 = gpu_fit(W, 4, 5, 37, 1e-4, grid=grid, with_err=False, dense=dense)
     for a, b in zip(out[:3], out2[:3]):
         assert np.array_equal(a, b)
 
 
-def test_deterministic():
-    say("case determinism")
+@pytest.mark.parametrize("dense", [False, True], ids=["hist", "dense"])
+def test_deterministic(dense):
+    say(f"case determinism dense={dense}")
     W = wl.random_weights(48, 777, seed=9)
-    a = gpu_fit(W, 4, 6, 256, 1e-4)
-    b = gpu_fit(W, 4, 6, 256, 1e-4)
+    a = gpu_fit(W, 4, 6, 256, 1e-4, dense=dense)
+    b = gpu_fit(W, 4, 6, 256, 1e-4, dense=dense)
     for x, y in zip(a, b):
         assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("d", [8192, 8193, 16384, 16385])
+def test_search_kernel_boundaries(orc, d):
+    """Largest channels of each register-resident variant of the histogram
+    search, and the first length that falls back to the dense search."""
+    say(f"case boundary d={d}")
+    W = wl.random_weights(3, d, seed=d)
+    out = gpu_fit(W, 3, 4, 512, 5e-4)
+    assert_parity(orc, W, 3, 4, 512, 5e-4, out)
+
+
+def test_exact_ties_between_candidates(orc):
+    """Channels built so that several candidate scales give exactly the same
+    error (dyadic values): the smallest scale must win, in both searches."""
+    say("case exact candidate ties")
+    rows = [[1.0, 0.5], [1.0, 0.5, 0.5, 0.5], [0.75, 0.25, -0.5, 1.0], [2.0, 1.0, 1.0, 0.0]]
+    d = 4
+    W = np.zeros((len(rows), d), np.float32)
+    for i, r in enumerate(rows):
+        W[i, :len(r)] = r
+    for bits, G in ((2, 2), (2, 4), (3, 8), (4, 16)):
+        ref = orc.fit(W, bits, 4, G, 0.0)
+        for dense in (False, True):
+            out = gpu_fit(W, bits, 4, G, 0.0, dense=dense)
+            assert_parity(orc, W, bits, 4, G, 0.0, out)
+            assert np.array_equal(out[1], ref[1]) and np.array_equal(out[0], ref[0])
 
 
 def test_shape_limit():
