@@ -42,16 +42,10 @@ struct HistShared {
     double *bnd;     // [G] their error bounds
 };
 
-// n = #{ g : h * a_g < x } over a non-decreasing table a[0..G).
-__device__ __forceinline__ int count_below(const float *a, int G, double h, double x, bool linear,
-                                           float est)
+// n = #{ g : h * a_g < x } over a non-decreasing table a[0..G), by binary
+// search (general grids, and the fallback of count_window).
+__device__ __forceinline__ int count_bsearch(const float *a, int G, double h, double x)
 {
-    if (linear) {
-        int n = (int)fminf(fmaxf(est, 0.0f), (float)G);
-        while (n < G && h * (double)a[n] < x) ++n;
-        while (n > 0 && h * (double)a[n - 1] >= x) --n;
-        return n;
-    }
     int lo = 0, hi = G;
     while (lo < hi) {
         const int mid = (lo + hi) >> 1;
@@ -59,6 +53,30 @@ __device__ __forceinline__ int count_below(const float *a, int G, double h, doub
         else hi = mid;
     }
     return lo;
+}
+
+// The same count for the default grid a_g = fl32(m fl32((g+1)/G) / M) from an
+// estimate n0 of x G M / (h m).  The rounding of a_g (relative 2^-23) and of
+// the estimate (a few 2^-24) move the boundary by far less than one index for
+// G <= 4096, so the count lies in [n0 - 1, n0 + 1]; the window a[n0-2..n0+1]
+// decides it and proves it (the first entry below, the last at or above).
+// Anything else falls back to the binary search.
+__device__ __forceinline__ int count_window(const float *a, int G, double h, double x, float est)
+{
+    const int n0 = (int)fminf(fmaxf(est, 0.0f), (float)G);
+    bool ge[4];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        const int i = n0 - 2 + w;
+        const float ai = (i >= 0 && i < G) ? a[i] : 0.0f;
+        ge[w] = i >= G || (i >= 0 && h * (double)ai >= x);
+    }
+    if (!ge[0]) {
+        if (ge[1]) return n0 - 1;
+        if (ge[2]) return n0;
+        if (ge[3]) return n0 + 1;
+    }
+    return count_bsearch(a, G, h, x);
 }
 
 template <int T, int EPT>
@@ -144,19 +162,23 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
         __syncthreads();
 
         // ---- histograms of the level boundaries
+        const float gm = (float)G * (float)M / m;
 #pragma unroll
         for (int u = 0; u < EPT; ++u) {
             const double x = fabs(r[u]);
             if (x > 0.0) {
                 const long long X = (long long)rint(ldexp(x, sh));
                 // estimate of n for the default grid a_g ~ m (g+1) / (G M)
-                const float xe = (float)x * ((float)G * (float)M / m);
+                const float xe = (float)x * gm;
+#pragma unroll 4
                 for (int kk = 0; kk < M; ++kk) {
                     const double h = (double)kk + 0.5;
-                    const int nb = count_below(S.a, G, h, x, linear, xe / (float)h);
-                    if (nb == 0) break;
-                    atomicAdd((unsigned long long *)&S.ha[nb - 1], (unsigned long long)X);
-                    atomicAdd(&S.hb[nb - 1], 2 * kk + 1);
+                    const int nb = linear ? count_window(S.a, G, h, x, xe * __builtin_amdgcn_rcpf((float)h))
+                                          : count_bsearch(S.a, G, h, x);
+                    if (nb > 0) {
+                        atomicAdd((unsigned long long *)&S.ha[nb - 1], (unsigned long long)X);
+                        atomicAdd(&S.hb[nb - 1], 2 * kk + 1);
+                    }
                 }
             }
         }
