@@ -161,8 +161,13 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
         const int sh = 61 - (ex + 1) - lg;
         __syncthreads();
 
-        // ---- histograms of the level boundaries
+        // ---- histograms of the level boundaries.  A boundary that every
+        // candidate passes (n = G, most elements at the low levels) would send
+        // most lanes to bin G-1 at once; those are summed in registers and
+        // added with one atomic per wavefront.
         const float gm = (float)G * (float)M / m;
+        unsigned long long fullA = 0;
+        int fullB = 0;
 #pragma unroll
         for (int u = 0; u < EPT; ++u) {
             const double x = fabs(r[u]);
@@ -175,12 +180,24 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
                     const double h = (double)kk + 0.5;
                     const int nb = linear ? count_window(S.a, G, h, x, xe * __builtin_amdgcn_rcpf((float)h))
                                           : count_bsearch(S.a, G, h, x);
-                    if (nb > 0) {
+                    if (nb == G) {
+                        fullA += (unsigned long long)X;
+                        fullB += 2 * kk + 1;
+                    } else if (nb > 0) {
                         atomicAdd((unsigned long long *)&S.ha[nb - 1], (unsigned long long)X);
                         atomicAdd(&S.hb[nb - 1], 2 * kk + 1);
                     }
                 }
             }
+        }
+#pragma unroll
+        for (int off = 1; off < kWave; off <<= 1) {
+            fullA += (unsigned long long)__shfl_xor((long long)fullA, off);
+            fullB += __shfl_xor(fullB, off);
+        }
+        if ((t % kWave) == 0) {
+            atomicAdd((unsigned long long *)&S.ha[G - 1], fullA);
+            atomicAdd(&S.hb[G - 1], fullB);
         }
         __syncthreads();
 
