@@ -35,51 +35,42 @@ namespace {
 constexpr int kMaxFinalists = 8;
 
 struct HistShared {
-    float *a;        // [G] candidate scales
+    double *ad;      // [G + 2]: ad[0] = 0, ad[g + 1] = a_g (an fp32 value), ad[G + 1] = +inf
     long long *ha;   // [G] fixed-point sum of x per bin
     int *hb;         // [G] sum of (2k + 1) per bin
     double *e;       // [G] approximate candidate errors
     double *bnd;     // [G] their error bounds
 };
 
-// n = #{ g : h * a_g < x } over a non-decreasing table a[0..G), by binary
-// search (general grids, and the fallback of count_window).
-__device__ __forceinline__ int count_bsearch(const float *a, int G, double h, double x)
+// n = #{ g : h * a_g < x } over the non-decreasing candidates, by binary
+// search (general grids).  ad is the sentinel table of HistShared.
+__device__ __forceinline__ int count_bsearch(const double *ad, int G, double h, double x)
 {
     int lo = 0, hi = G;
     while (lo < hi) {
         const int mid = (lo + hi) >> 1;
-        if (h * (double)a[mid] < x) lo = mid + 1;
+        if (fma(h, ad[mid + 1], -x) < 0.0) lo = mid + 1;
         else hi = mid;
     }
     return lo;
 }
 
-// The same count for the default grid a_g = fl32(m fl32((g+1)/G) / M) from an
-// estimate n0 of x G M / (h m).  The rounding of a_g (relative 2^-23) and of
-// the estimate (a few 2^-24) move the boundary by far less than one index for
-// G <= 4096, so the count lies in [n0 - 1, n0 + 1]; the window a[n0-2..n0+1]
-// decides it and proves it (the first entry below, the last at or above).
-// Anything else falls back to the binary search.
-__device__ __forceinline__ int count_window(const float *a, int G, double h, double x, float est)
+// The same count for the default grid a_g = fl32(m fl32((g+1)/G) / M), from
+// n0 = floor(min(est, G)) with est = fl32 of x G M / (h m).  a_g is within
+// relative 2^-23 of m (g+1) / (G M) and est within a few 2^-24 of its exact
+// value E, so for G <= 4096 the only candidate whose side of the boundary is
+// not fixed by E lies within 0.002 of E, and the exact count n satisfies
+// n0 - 1 <= n <= n0 + 1.  Hence n = n0 - 1 + [a_{n0-1} below] + [a_{n0} below]
+// (ad[n0] and ad[n0 + 1]; the sentinels cover n0 = 0 and n0 = G).  The sign
+// of fma(h, a, -x) is exact: h a is exact in fp64 and the fma rounds once.
+__device__ __forceinline__ int count_linear(const double *ad, int G, double h, double x, float est)
 {
-    const int n0 = (int)fminf(fmaxf(est, 0.0f), (float)G);
-    bool ge[4];
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-        const int i = n0 - 2 + w;
-        const float ai = (i >= 0 && i < G) ? a[i] : 0.0f;
-        ge[w] = i >= G || (i >= 0 && h * (double)ai >= x);
-    }
-    if (!ge[0]) {
-        if (ge[1]) return n0 - 1;
-        if (ge[2]) return n0;
-        if (ge[3]) return n0 + 1;
-    }
-    return count_bsearch(a, G, h, x);
+    const int n0 = (int)fminf(est, (float)G);
+    const double lo = ad[n0], hi = ad[n0 + 1];
+    return n0 - 1 + (fma(h, lo, -x) < 0.0 ? 1 : 0) + (fma(h, hi, -x) < 0.0 ? 1 : 0);
 }
 
-template <int T, int EPT>
+template <int T, int EPT, bool kLinear>
 __global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
 {
     constexpr int kWaves = T / kWave;
@@ -95,8 +86,8 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
     S.e = hsmem;
     S.bnd = S.e + G;
     S.ha = (long long *)(S.bnd + G);
-    S.a = (float *)(S.ha + G);
-    S.hb = (int *)(S.a + G);
+    S.ad = (double *)(S.ha + G);
+    S.hb = (int *)(S.ad + G + 2);
 
     const int64_t k = blockIdx.x;
     const int t = threadIdx.x;
@@ -104,7 +95,6 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
     const int P = p.P;
     const int M = p.M;
     const double Md = (double)M;
-    const bool linear = p.grid == nullptr;
     int8_t *qk = p.codes + k * (int64_t)P * d;
     const float *wk = p.W + k * (int64_t)d;
 
@@ -149,9 +139,13 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
         // ---- candidates, cleared histograms
         for (int g = t; g < G; g += T) {
             const float c = p.grid ? p.grid[g] : (float)((double)(g + 1) / (double)G);
-            S.a[g] = (float)((double)m * (double)c / Md);
+            S.ad[g + 1] = (double)(float)((double)m * (double)c / Md);
             S.ha[g] = 0;
             S.hb[g] = 0;
+        }
+        if (t == 0) {
+            S.ad[0] = 0.0;
+            S.ad[G + 1] = INFINITY;
         }
         // fixed-point shift: every x < 2^(ex+1); sums of up to M*d values < 2^62
         int ex = 0;
@@ -161,31 +155,54 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
         const int sh = 61 - (ex + 1) - lg;
         __syncthreads();
 
-        // ---- histograms of the level boundaries.  A boundary that every
-        // candidate passes (n = G, most elements at the low levels) would send
-        // most lanes to bin G-1 at once; those are summed in registers and
-        // added with one atomic per wavefront.
+        // ---- histograms of the level boundaries.  Level-major: for each
+        // level, the counts of all of this thread's elements are found first
+        // (independent LDS reads in flight together), then binned.  A boundary
+        // that every candidate passes (n = G: most elements at the low levels)
+        // would send most lanes to bin G-1 at once; those are summed in
+        // registers and added with one atomic per wavefront.
         const float gm = (float)G * (float)M / m;
         unsigned long long fullA = 0;
         int fullB = 0;
+        // per element and step: fixed-point |r| and the scaled estimate base
+        constexpr bool kKeep = EPT <= 16;
+        unsigned long long Xk[kKeep ? EPT : 1];
+        float Bk[kKeep ? EPT : 1];
+        if constexpr (kKeep) {
 #pragma unroll
-        for (int u = 0; u < EPT; ++u) {
-            const double x = fabs(r[u]);
-            if (x > 0.0) {
-                const long long X = (long long)rint(ldexp(x, sh));
-                // estimate of n for the default grid a_g ~ m (g+1) / (G M)
-                const float xe = (float)x * gm;
-#pragma unroll 4
-                for (int kk = 0; kk < M; ++kk) {
-                    const double h = (double)kk + 0.5;
-                    const int nb = linear ? count_window(S.a, G, h, x, xe * __builtin_amdgcn_rcpf((float)h))
-                                          : count_bsearch(S.a, G, h, x);
-                    if (nb == G) {
-                        fullA += (unsigned long long)X;
-                        fullB += 2 * kk + 1;
-                    } else if (nb > 0) {
-                        atomicAdd((unsigned long long *)&S.ha[nb - 1], (unsigned long long)X);
-                        atomicAdd(&S.hb[nb - 1], 2 * kk + 1);
+            for (int u = 0; u < EPT; ++u) {
+                Xk[u] = (unsigned long long)rint(ldexp(fabs(r[u]), sh));
+                Bk[u] = (float)fabs(r[u]) * gm;
+            }
+        }
+        constexpr int kChunk = EPT < 8 ? EPT : 8;
+        for (int kk = 0; kk < M; ++kk) {
+            const double h = (double)kk + 0.5;
+            const float rh = __builtin_amdgcn_rcpf((float)h);
+            const int inc = 2 * kk + 1;
+#pragma unroll
+            for (int u0 = 0; u0 < EPT; u0 += kChunk) {
+                int nb[kChunk];
+#pragma unroll
+                for (int v = 0; v < kChunk; ++v) {
+                    const int u = u0 + v;
+                    const double x = fabs(r[u]);
+                    const float base = kKeep ? Bk[kKeep ? u : 0] : (float)x * gm;
+                    if constexpr (kLinear) nb[v] = count_linear(S.ad, G, h, x, base * rh);
+                    else nb[v] = count_bsearch(S.ad, G, h, x);
+                }
+#pragma unroll
+                for (int v = 0; v < kChunk; ++v) {
+                    const int u = u0 + v;
+                    const unsigned long long X =
+                        kKeep ? Xk[kKeep ? u : 0]
+                              : (unsigned long long)rint(ldexp(fabs(r[u]), sh));
+                    const bool full = nb[v] == G;
+                    fullA += full ? X : 0ull;
+                    fullB += full ? inc : 0;
+                    if (nb[v] > 0 && !full) {
+                        atomicAdd((unsigned long long *)&S.ha[nb[v] - 1], X);
+                        atomicAdd(&S.hb[nb[v] - 1], inc);
                     }
                 }
             }
@@ -205,33 +222,23 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
         const double q2 = ldexp(1.0, -sh);
         const double slack = Md * (double)d * q2;   // fixed-point error of A, per unit a
         if (t < kWave) {
+            // lane l owns the l-th chunk from the top, so a prefix over lanes
+            // is a suffix over candidates
             const int per = (G + kWave - 1) / kWave;
-            const int g0 = t * per, g1 = min(g0 + per, G);
-            long long la = 0;
-            int lb = 0;
+            const int g0 = (kWave - 1 - t) * per, g1 = min(g0 + per, G);
+            unsigned long long la = 0;
+            uint32_t lb = 0;
             for (int g = g0; g < g1; ++g) {
-                la += S.ha[g];
-                lb += S.hb[g];
+                la += (unsigned long long)S.ha[g];
+                lb += (uint32_t)S.hb[g];
             }
-            // exclusive suffix over lanes
-            long long sa = la;
-            int sb = lb;
-#pragma unroll
-            for (int off = 1; off < kWave; off <<= 1) {
-                const long long oa = __shfl_down(sa, off);
-                const int ob = __shfl_down(sb, off);
-                if (t + off < kWave) {
-                    sa += oa;
-                    sb += ob;
-                }
-            }
-            long long A = sa - la;
-            int B = sb - lb;
+            long long A = (long long)(wave_prefix_sum(la) - la);   // exclusive
+            int B = (int)(wave_prefix_sum(lb) - lb);
             ArgMin best{INFINITY, 0x7fffffff};
             for (int g = g1 - 1; g >= g0; --g) {
                 A += S.ha[g];
                 B += S.hb[g];
-                const double a = (double)S.a[g];
+                const double a = S.ad[g + 1];
                 double e = INFINITY, b = 0.0;
                 if (a != 0.0) {
                     const double Ad = ldexp((double)A, -sh);
@@ -284,7 +291,7 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
             ArgMin best{INFINITY, 0x7fffffff};
             for (int f = 0; f < nfin; ++f) {
                 const int g = s_fin[f];
-                const double a = (double)S.a[g];
+                const double a = S.ad[g + 1];
                 double le = 0.0;
 #pragma unroll
                 for (int u = 0; u < EPT; ++u) {
@@ -303,7 +310,7 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
             n = i;
             break;
         }
-        apend = S.a[gstar];
+        apend = (float)S.ad[gstar + 1];
         if (t == 0) p.scales[k * P + i] = apend;
         __syncthreads();   // S.a is rewritten by the next step
     }
@@ -320,7 +327,8 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
 template <int T, int EPT>
 hipError_t launch_hist_t(const FitParams &p, size_t lds, hipStream_t s)
 {
-    auto kern = fit_hist_kernel<T, EPT>;
+    // the default grid (grid == nullptr) has the closed-form boundary counts
+    auto kern = p.grid ? fit_hist_kernel<T, EPT, false> : fit_hist_kernel<T, EPT, true>;
     if (lds > 65536) {
         hipError_t e = hipFuncSetAttribute((const void *)kern,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -334,7 +342,7 @@ hipError_t launch_hist_t(const FitParams &p, size_t lds, hipStream_t s)
 
 size_t fit_hist_lds(int G)
 {
-    return (size_t)G * (2 * sizeof(double) + sizeof(long long) + sizeof(float) + sizeof(int));
+    return (size_t)G * (3 * sizeof(double) + sizeof(long long) + sizeof(int)) + 2 * sizeof(double);
 }
 
 bool fit_hist_supports(int64_t d) { return d <= kHistMaxDim; }

@@ -139,6 +139,46 @@ __device__ __forceinline__ ArgMin wave_argmin(ArgMin v)
     return argmin_combine(lo, hi);
 }
 
+// Inclusive prefix sum over the 64 lanes (lane 0 first), DPP only:
+// row_shr 1, 2, 4, 8 with zero fill within each row of 16, then row_bcast15
+// (rows 1 and 3 add lane 15 of the row before) and row_bcast31 (rows 2 and 3
+// add lane 31).
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint32_t dpp_zero(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, kCtrl, kRowMask, 0xF, true);
+}
+
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ unsigned long long dpp_zero64(unsigned long long v)
+{
+    const uint32_t lo = dpp_zero<kCtrl, kRowMask>((uint32_t)v);
+    const uint32_t hi = dpp_zero<kCtrl, kRowMask>((uint32_t)(v >> 32));
+    return ((unsigned long long)hi << 32) | lo;
+}
+
+__device__ __forceinline__ unsigned long long wave_prefix_sum(unsigned long long v)
+{
+    v += dpp_zero64<0x111, 0xF>(v);  // row_shr:1
+    v += dpp_zero64<0x112, 0xF>(v);  // row_shr:2
+    v += dpp_zero64<0x114, 0xF>(v);  // row_shr:4
+    v += dpp_zero64<0x118, 0xF>(v);  // row_shr:8
+    v += dpp_zero64<0x142, 0xA>(v);  // row_bcast:15
+    v += dpp_zero64<0x143, 0xC>(v);  // row_bcast:31
+    return v;
+}
+
+__device__ __forceinline__ uint32_t wave_prefix_sum(uint32_t v)
+{
+    v += dpp_zero<0x111, 0xF>(v);
+    v += dpp_zero<0x112, 0xF>(v);
+    v += dpp_zero<0x114, 0xF>(v);
+    v += dpp_zero<0x118, 0xF>(v);
+    v += dpp_zero<0x142, 0xA>(v);
+    v += dpp_zero<0x143, 0xC>(v);
+    return v;
+}
+
 // Workgroup reductions.  `scratch` must hold one T per wavefront and must
 // not be in use by another reduction between the two barriers.
 template <int kThreads, typename T, typename Op>
