@@ -157,6 +157,43 @@ int mpq_output_error(const float *W, const int8_t *codes, const float *scales,
 int mpq_reconstruct(const int8_t *codes, const float *scales, const int32_t *counts,
                     int64_t c_out, int64_t d, int max_points, float *W_hat, void *stream);
 
+/*
+ * Batched calls: one call covers the layers of a network.  Each layer is
+ * described by an mpq_layer (a HOST array of them is passed; the pointers in
+ * it are DEVICE pointers); every call reads only the fields it names.  The
+ * result is the same as calling the single-layer entry point on each layer
+ * in order, on the same stream.  Layers whose channel lengths select the
+ * same kernel share one launch, so a whole network costs a handful of
+ * launches.  Arguments are checked for every layer before anything is
+ * enqueued.
+ */
+typedef struct mpq_layer {
+    const float *W;       /* [c_out][d] fp32 weights                               */
+    int64_t c_out, d;
+    int8_t *codes;        /* [c_out][max_points][d]                                */
+    float *scales;        /* [c_out][max_points]                                   */
+    int32_t *counts;      /* [c_out]                                               */
+    float *fit_err;       /* mpq_fit_layers: NULL or [c_out][max_points] (err_opt) */
+    const float *X;       /* mpq_output_error_layers: [d][n] calibration inputs    */
+    int64_t n;            /* mpq_output_error_layers: columns of X                 */
+    float *out_err;       /* mpq_output_error_layers: [c_out]                      */
+    float *out_ref;       /* mpq_output_error_layers: NULL or [c_out]              */
+    float *W_hat;         /* mpq_reconstruct_layers: [c_out][d]                    */
+} mpq_layer;
+
+/* mpq_fit_layer on every layer (reads W, c_out, d, codes, scales, counts,
+ * fit_err).  All layers share bits, max_points, the grid and tol. */
+int mpq_fit_layers(const mpq_layer *layers, int n_layers, int bits, int max_points,
+                   const float *grid_host, int n_grid, float tol, void *stream);
+
+/* mpq_output_error on every layer (reads W, c_out, d, codes, scales, counts,
+ * X, n, out_err, out_ref). */
+int mpq_output_error_layers(const mpq_layer *layers, int n_layers, int max_points, void *stream);
+
+/* mpq_reconstruct on every layer (reads c_out, d, codes, scales, counts,
+ * W_hat). */
+int mpq_reconstruct_layers(const mpq_layer *layers, int n_layers, int max_points, void *stream);
+
 /* Text of the calling thread's last failure ("" if none).  The pointer stays
  * valid until the thread's next failing call. */
 const char *mpq_last_error(void);

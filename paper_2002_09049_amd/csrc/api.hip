@@ -32,26 +32,44 @@ int hip_fail(hipError_t e, const char *what)
     return fail(MPQ_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
 }
 
-// Largest dynamic LDS a workgroup may use on the current device.
+// Largest dynamic LDS a workgroup may use on the current device (queried
+// once per device).
+constexpr int kMaxDevices = 64;
+std::mutex g_lds_mu;
+size_t g_lds_limit[kMaxDevices];
+
 int device_lds_limit(size_t *bytes)
 {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-    int v = 0;
-    e = hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
-    if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute(MaxSharedMemoryPerBlock)");
-    // the fit kernel also holds ~1 KiB of static LDS
-    *bytes = v > 2048 ? (size_t)v - 2048 : 0;
+    if (dev < 0 || dev >= kMaxDevices) return fail(MPQ_ERR_HIP, "device index %d out of range", dev);
+    std::lock_guard<std::mutex> lk(g_lds_mu);
+    if (g_lds_limit[dev] == 0) {
+        int v = 0;
+        e = hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+        if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute(MaxSharedMemoryPerBlock)");
+        // the fit kernels also hold ~1 KiB of static LDS
+        g_lds_limit[dev] = v > 2048 ? (size_t)v - 2048 : 1;
+    }
+    *bytes = g_lds_limit[dev];
     return MPQ_OK;
 }
 
-int check_fit_args(const float *W, int64_t c_out, int64_t d, int bits, int max_points,
-                   const float *grid_host, int n_grid, float tol, const int8_t *codes,
-                   const float *scales, const int32_t *counts)
+int check_fit_layer(const float *W, int64_t c_out, int64_t d, const int8_t *codes,
+                    const float *scales, const int32_t *counts)
 {
     if (c_out < 0) return fail(MPQ_ERR_INVALID_ARG, "c_out must be >= 0 (got %lld)", (long long)c_out);
     if (d < 1) return fail(MPQ_ERR_INVALID_ARG, "d must be >= 1 (got %lld)", (long long)d);
+    if (c_out > 0 && (!W || !codes || !scales || !counts))
+        return fail(MPQ_ERR_INVALID_ARG, "W, codes, scales and counts must not be NULL");
+    if (c_out > 0x7fffffffLL)
+        return fail(MPQ_ERR_INVALID_ARG, "c_out too large (%lld)", (long long)c_out);
+    return MPQ_OK;
+}
+
+int check_fit_args(int bits, int max_points, const float *grid_host, int n_grid, float tol)
+{
     if (bits < 2 || bits > MPQ_MAX_BITS)
         return fail(MPQ_ERR_INVALID_ARG, "bits must be in [2, %d] (got %d)", MPQ_MAX_BITS, bits);
     if (max_points < 1 || max_points > MPQ_MAX_POINTS)
@@ -70,10 +88,6 @@ int check_fit_args(const float *W, int64_t c_out, int64_t d, int bits, int max_p
                 return fail(MPQ_ERR_INVALID_ARG, "grid must be strictly ascending (grid[%d])", g);
         }
     }
-    if (c_out > 0 && (!W || !codes || !scales || !counts))
-        return fail(MPQ_ERR_INVALID_ARG, "W, codes, scales and counts must not be NULL");
-    if (c_out > 0x7fffffffLL)
-        return fail(MPQ_ERR_INVALID_ARG, "c_out too large (%lld)", (long long)c_out);
     return MPQ_OK;
 }
 
@@ -82,7 +96,6 @@ int check_fit_args(const float *W, int64_t c_out, int64_t d, int bits, int max_p
 namespace mpq {
 
 namespace {
-constexpr int kMaxDevices = 64;
 std::mutex g_pool_mu;
 hipMemPool_t g_pool[kMaxDevices];
 }  // namespace
@@ -138,23 +151,35 @@ int64_t dense_max_dim(int n_grid, size_t lim)
 
 enum class Search { kAuto, kDense };
 
-int fit_layer_impl(Search mode, const float *W, int64_t c_out, int64_t d, int bits, int max_points,
-                   const float *grid_host, int n_grid, float tol, int8_t *codes, float *scales,
-                   int32_t *counts, float *err_opt, void *stream)
+int fit_layers_impl(Search mode, const mpq_layer *layers, int n_layers, int bits, int max_points,
+                    const float *grid_host, int n_grid, float tol, void *stream)
 {
-    int rc = check_fit_args(W, c_out, d, bits, max_points, grid_host, n_grid, tol, codes, scales,
-                            counts);
+    if (n_layers < 0 || (n_layers > 0 && !layers))
+        return fail(MPQ_ERR_INVALID_ARG, "layers must hold n_layers >= 0 entries");
+    int rc = check_fit_args(bits, max_points, grid_host, n_grid, tol);
     if (rc != MPQ_OK) return rc;
-    if (c_out == 0) return MPQ_OK;
+    bool any = false;
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_layer &L = layers[l];
+        rc = check_fit_layer(L.W, L.c_out, L.d, L.codes, L.scales, L.counts);
+        if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
+        any = any || L.c_out > 0;
+    }
+    if (!any) return MPQ_OK;
     size_t lim = 0;
     rc = device_lds_limit(&lim);
     if (rc != MPQ_OK) return rc;
-    const bool hist = mode == Search::kAuto && mpq::fit_hist_supports(d) &&
-                      mpq::fit_hist_lds(n_grid) <= lim;
-    const mpq::FitLayout L = mpq::fit_layout(d, n_grid);
-    if (!hist && L.lds > lim)
-        return fail(MPQ_ERR_SHAPE, "d = %lld with n_grid = %d needs %zu bytes of LDS (limit %zu)",
-                    (long long)d, n_grid, L.lds, lim);
+    // which layers take the histogram search (and which variant)
+    const bool hist_fits = mpq::fit_hist_lds(n_grid) <= lim;
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_layer &L = layers[l];
+        if (L.c_out == 0) continue;
+        const bool hist = mode == Search::kAuto && hist_fits && mpq::fit_hist_supports(L.d);
+        if (!hist && mpq::fit_layout(L.d, n_grid).lds > lim)
+            return fail(MPQ_ERR_SHAPE, "%sd = %lld with n_grid = %d needs %zu bytes of LDS (limit %zu)",
+                        n_layers > 1 ? "a layer's " : "", (long long)L.d, n_grid,
+                        mpq::fit_layout(L.d, n_grid).lds, lim);
+    }
     hipStream_t s = (hipStream_t)stream;
     float *dgrid = nullptr;
     if (grid_host) {
@@ -166,22 +191,149 @@ int fit_layer_impl(Search mode, const float *W, int64_t c_out, int64_t d, int bi
             return hip_fail(e, "hipMemcpyAsync(grid)");
         }
     }
-    mpq::FitParams p;
-    p.W = W;
-    p.C = c_out;
-    p.d = d;
-    p.M = (1 << (bits - 1)) - 1;
-    p.P = max_points;
-    p.grid = dgrid;
-    p.G = n_grid;
-    p.tol = (double)tol;
-    p.codes = codes;
-    p.scales = scales;
-    p.counts = counts;
-    p.err = err_opt;
-    hipError_t e = hist ? mpq::launch_fit_hist(p, s) : mpq::launch_fit(p, L, s);
+    const int M = (1 << (bits - 1)) - 1;
+    hipError_t e = hipSuccess;
+    // dense-search layers: one launch each
+    for (int l = 0; l < n_layers && e == hipSuccess; ++l) {
+        const mpq_layer &L = layers[l];
+        if (L.c_out == 0) continue;
+        if (mode == Search::kAuto && hist_fits && mpq::fit_hist_supports(L.d)) continue;
+        mpq::FitParams p;
+        p.W = L.W;
+        p.C = L.c_out;
+        p.d = L.d;
+        p.M = M;
+        p.P = max_points;
+        p.grid = dgrid;
+        p.G = n_grid;
+        p.tol = (double)tol;
+        p.codes = L.codes;
+        p.scales = L.scales;
+        p.counts = L.counts;
+        p.err = L.fit_err;
+        e = mpq::launch_fit(p, mpq::fit_layout(L.d, n_grid), s);
+    }
+    // histogram-search layers: one launch per kernel variant (and per
+    // kMaxBatchLayers layers)
+    if (mode == Search::kAuto && hist_fits) {
+        for (int v = 0; v <= mpq::hist_variant(mpq::kHistMaxDim) && e == hipSuccess; ++v) {
+            mpq::HistBatch b;
+            b.M = M;
+            b.P = max_points;
+            b.G = n_grid;
+            b.grid = dgrid;
+            b.tol = (double)tol;
+            b.n_layers = 0;
+            int64_t channels = 0;
+            for (int l = 0; l <= n_layers && e == hipSuccess; ++l) {
+                const bool flush = l == n_layers || b.n_layers == mpq::kMaxBatchLayers ||
+                                   channels + (l < n_layers ? layers[l].c_out : 0) > 0x7fffffffLL;
+                if (flush && b.n_layers > 0) {
+                    e = mpq::launch_fit_hist(b, v, channels, s);
+                    b.n_layers = 0;
+                    channels = 0;
+                }
+                if (l == n_layers) break;
+                const mpq_layer &L = layers[l];
+                if (L.c_out == 0 || !mpq::fit_hist_supports(L.d) || mpq::hist_variant(L.d) != v) continue;
+                mpq::HistLayer &H = b.L[b.n_layers++];
+                H.W = L.W;
+                H.codes = L.codes;
+                H.scales = L.scales;
+                H.counts = L.counts;
+                H.err = L.fit_err;
+                H.d = (int)L.d;
+                H.c_begin = (int)channels;
+                channels += L.c_out;
+            }
+        }
+    }
     if (dgrid) (void)mpq::scratch_free(dgrid, s);
     if (e != hipSuccess) return hip_fail(e, "fit kernel launch");
+    return MPQ_OK;
+}
+
+int one_layer_fit(Search mode, const float *W, int64_t c_out, int64_t d, int bits, int max_points,
+                  const float *grid_host, int n_grid, float tol, int8_t *codes, float *scales,
+                  int32_t *counts, float *err_opt, void *stream)
+{
+    mpq_layer L = {};
+    L.W = W;
+    L.c_out = c_out;
+    L.d = d;
+    L.codes = codes;
+    L.scales = scales;
+    L.counts = counts;
+    L.fit_err = err_opt;
+    return fit_layers_impl(mode, &L, 1, bits, max_points, grid_host, n_grid, tol, stream);
+}
+
+int check_error_layer(const mpq_layer &L, int max_points, bool need_x)
+{
+    if (L.c_out < 0) return fail(MPQ_ERR_INVALID_ARG, "c_out must be >= 0 (got %lld)", (long long)L.c_out);
+    if (L.d < 1) return fail(MPQ_ERR_INVALID_ARG, "d must be >= 1 (got %lld)", (long long)L.d);
+    if (max_points < 1 || max_points > MPQ_MAX_POINTS)
+        return fail(MPQ_ERR_INVALID_ARG, "max_points must be in [1, %d] (got %d)", MPQ_MAX_POINTS,
+                    max_points);
+    if (need_x) {
+        if (L.n < 1) return fail(MPQ_ERR_INVALID_ARG, "n must be >= 1 (got %lld)", (long long)L.n);
+        if (L.c_out > 0 && (!L.W || !L.codes || !L.scales || !L.counts || !L.X || !L.out_err))
+            return fail(MPQ_ERR_INVALID_ARG, "W, codes, scales, counts, X and err must not be NULL");
+        if ((L.c_out + 127) / 128 > 65535)
+            return fail(MPQ_ERR_INVALID_ARG, "c_out too large (%lld)", (long long)L.c_out);
+        if ((L.n + 127) / 128 > 0x7fffffffLL)
+            return fail(MPQ_ERR_INVALID_ARG, "n too large (%lld)", (long long)L.n);
+    } else if (L.c_out > 0 && (!L.codes || !L.scales || !L.counts || !L.W_hat)) {
+        return fail(MPQ_ERR_INVALID_ARG, "codes, scales, counts and W_hat must not be NULL");
+    }
+    return MPQ_OK;
+}
+
+int output_error_impl(const mpq_layer *layers, int n_layers, int max_points, void *stream)
+{
+    if (n_layers < 0 || (n_layers > 0 && !layers))
+        return fail(MPQ_ERR_INVALID_ARG, "layers must hold n_layers >= 0 entries");
+    size_t bytes = 0;
+    for (int l = 0; l < n_layers; ++l) {
+        int rc = check_error_layer(layers[l], max_points, true);
+        if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
+        if (layers[l].c_out > 0) {
+            const size_t b = mpq::err_scratch_bytes(layers[l].c_out, layers[l].d, layers[l].n);
+            if (b > bytes) bytes = b;
+        }
+    }
+    if (bytes == 0) return MPQ_OK;
+    hipStream_t s = (hipStream_t)stream;
+    void *scratch = nullptr;
+    hipError_t e = mpq::scratch_alloc(&scratch, bytes, s);
+    if (e != hipSuccess) return fail(MPQ_ERR_NOMEM, "scratch of %zu bytes: %s", bytes, hipGetErrorString(e));
+    for (int l = 0; l < n_layers && e == hipSuccess; ++l) {
+        const mpq_layer &L = layers[l];
+        if (L.c_out == 0) continue;
+        e = mpq::launch_output_error(L.W, L.codes, L.scales, L.counts, L.c_out, L.d, max_points, L.X,
+                                     L.n, L.out_err, L.out_ref, scratch, s);
+    }
+    (void)mpq::scratch_free(scratch, s);
+    if (e != hipSuccess) return hip_fail(e, "output error kernel launch");
+    return MPQ_OK;
+}
+
+int reconstruct_impl(const mpq_layer *layers, int n_layers, int max_points, void *stream)
+{
+    if (n_layers < 0 || (n_layers > 0 && !layers))
+        return fail(MPQ_ERR_INVALID_ARG, "layers must hold n_layers >= 0 entries");
+    for (int l = 0; l < n_layers; ++l) {
+        int rc = check_error_layer(layers[l], max_points, false);
+        if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
+    }
+    hipError_t e = hipSuccess;
+    for (int l = 0; l < n_layers && e == hipSuccess; ++l) {
+        const mpq_layer &L = layers[l];
+        if (L.c_out == 0) continue;
+        e = mpq::launch_reconstruct(L.codes, L.scales, L.counts, L.c_out, L.d, max_points, L.W_hat,
+                                    (hipStream_t)stream);
+    }
+    if (e != hipSuccess) return hip_fail(e, "reconstruct kernel launch");
     return MPQ_OK;
 }
 
@@ -205,62 +357,64 @@ int mpq_fit_layer(const float *W, int64_t c_out, int64_t d, int bits, int max_po
                   const float *grid_host, int n_grid, float tol, int8_t *codes, float *scales,
                   int32_t *counts, float *err_opt, void *stream)
 {
-    return fit_layer_impl(Search::kAuto, W, c_out, d, bits, max_points, grid_host, n_grid, tol,
-                          codes, scales, counts, err_opt, stream);
+    return one_layer_fit(Search::kAuto, W, c_out, d, bits, max_points, grid_host, n_grid, tol,
+                         codes, scales, counts, err_opt, stream);
 }
 
 int mpq_fit_layer_dense(const float *W, int64_t c_out, int64_t d, int bits, int max_points,
                         const float *grid_host, int n_grid, float tol, int8_t *codes,
                         float *scales, int32_t *counts, float *err_opt, void *stream)
 {
-    return fit_layer_impl(Search::kDense, W, c_out, d, bits, max_points, grid_host, n_grid, tol,
-                          codes, scales, counts, err_opt, stream);
+    return one_layer_fit(Search::kDense, W, c_out, d, bits, max_points, grid_host, n_grid, tol,
+                         codes, scales, counts, err_opt, stream);
+}
+
+int mpq_fit_layers(const mpq_layer *layers, int n_layers, int bits, int max_points,
+                   const float *grid_host, int n_grid, float tol, void *stream)
+{
+    return fit_layers_impl(Search::kAuto, layers, n_layers, bits, max_points, grid_host, n_grid,
+                           tol, stream);
 }
 
 int mpq_output_error(const float *W, const int8_t *codes, const float *scales,
                      const int32_t *counts, int64_t c_out, int64_t d, int max_points,
                      const float *X, int64_t n, float *err, float *ref_opt, void *stream)
 {
-    if (c_out < 0) return fail(MPQ_ERR_INVALID_ARG, "c_out must be >= 0 (got %lld)", (long long)c_out);
-    if (d < 1) return fail(MPQ_ERR_INVALID_ARG, "d must be >= 1 (got %lld)", (long long)d);
-    if (n < 1) return fail(MPQ_ERR_INVALID_ARG, "n must be >= 1 (got %lld)", (long long)n);
-    if (max_points < 1 || max_points > MPQ_MAX_POINTS)
-        return fail(MPQ_ERR_INVALID_ARG, "max_points must be in [1, %d] (got %d)", MPQ_MAX_POINTS,
-                    max_points);
-    if (c_out > 0 && (!W || !codes || !scales || !counts || !X || !err))
-        return fail(MPQ_ERR_INVALID_ARG, "W, codes, scales, counts, X and err must not be NULL");
-    if ((c_out + 127) / 128 > 65535)
-        return fail(MPQ_ERR_INVALID_ARG, "c_out too large (%lld)", (long long)c_out);
-    if ((n + 127) / 128 > 0x7fffffffLL)
-        return fail(MPQ_ERR_INVALID_ARG, "n too large (%lld)", (long long)n);
-    if (c_out == 0) return MPQ_OK;
-    hipStream_t s = (hipStream_t)stream;
-    void *scratch = nullptr;
-    const size_t bytes = mpq::err_scratch_bytes(c_out, d, n);
-    hipError_t e = mpq::scratch_alloc(&scratch, bytes, s);
-    if (e != hipSuccess) return fail(MPQ_ERR_NOMEM, "scratch of %zu bytes: %s", bytes, hipGetErrorString(e));
-    e = mpq::launch_output_error(W, codes, scales, counts, c_out, d, max_points, X, n, err, ref_opt,
-                                 scratch, s);
-    (void)mpq::scratch_free(scratch, s);
-    if (e != hipSuccess) return hip_fail(e, "output error kernel launch");
-    return MPQ_OK;
+    mpq_layer L = {};
+    L.W = W;
+    L.c_out = c_out;
+    L.d = d;
+    L.codes = (int8_t *)codes;
+    L.scales = (float *)scales;
+    L.counts = (int32_t *)counts;
+    L.X = X;
+    L.n = n;
+    L.out_err = err;
+    L.out_ref = ref_opt;
+    return output_error_impl(&L, 1, max_points, stream);
+}
+
+int mpq_output_error_layers(const mpq_layer *layers, int n_layers, int max_points, void *stream)
+{
+    return output_error_impl(layers, n_layers, max_points, stream);
 }
 
 int mpq_reconstruct(const int8_t *codes, const float *scales, const int32_t *counts, int64_t c_out,
                     int64_t d, int max_points, float *W_hat, void *stream)
 {
-    if (c_out < 0) return fail(MPQ_ERR_INVALID_ARG, "c_out must be >= 0 (got %lld)", (long long)c_out);
-    if (d < 1) return fail(MPQ_ERR_INVALID_ARG, "d must be >= 1 (got %lld)", (long long)d);
-    if (max_points < 1 || max_points > MPQ_MAX_POINTS)
-        return fail(MPQ_ERR_INVALID_ARG, "max_points must be in [1, %d] (got %d)", MPQ_MAX_POINTS,
-                    max_points);
-    if (c_out > 0 && (!codes || !scales || !counts || !W_hat))
-        return fail(MPQ_ERR_INVALID_ARG, "codes, scales, counts and W_hat must not be NULL");
-    if (c_out == 0) return MPQ_OK;
-    hipError_t e = mpq::launch_reconstruct(codes, scales, counts, c_out, d, max_points, W_hat,
-                                           (hipStream_t)stream);
-    if (e != hipSuccess) return hip_fail(e, "reconstruct kernel launch");
-    return MPQ_OK;
+    mpq_layer L = {};
+    L.c_out = c_out;
+    L.d = d;
+    L.codes = (int8_t *)codes;
+    L.scales = (float *)scales;
+    L.counts = (int32_t *)counts;
+    L.W_hat = W_hat;
+    return reconstruct_impl(&L, 1, max_points, stream);
+}
+
+int mpq_reconstruct_layers(const mpq_layer *layers, int n_layers, int max_points, void *stream)
+{
+    return reconstruct_impl(layers, n_layers, max_points, stream);
 }
 
 }  // extern "C"

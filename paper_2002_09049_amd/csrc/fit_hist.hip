@@ -71,7 +71,7 @@ __device__ __forceinline__ int count_linear(const double *ad, int G, double h, d
 }
 
 template <int T, int EPT, bool kLinear>
-__global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
+__global__ void __launch_bounds__(T) fit_hist_kernel(const HistBatch B)
 {
     constexpr int kWaves = T / kWave;
     extern __shared__ __align__(16) double hsmem[];
@@ -81,7 +81,12 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
     __shared__ int s_nfin;
     __shared__ int s_gbest;
 
-    const int G = p.G;
+    // layer of this workgroup (uniform: the descriptors are kernel arguments)
+    int li = 0;
+    while (li + 1 < B.n_layers && (int)blockIdx.x >= B.L[li + 1].c_begin) ++li;
+    const HistLayer &Ly = B.L[li];
+
+    const int G = B.G;
     HistShared S;
     S.e = hsmem;
     S.bnd = S.e + G;
@@ -89,14 +94,14 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
     S.ad = (double *)(S.ha + G);
     S.hb = (int *)(S.ad + G + 2);
 
-    const int64_t k = blockIdx.x;
+    const int64_t k = (int64_t)blockIdx.x - Ly.c_begin;
     const int t = threadIdx.x;
-    const int d = (int)p.d;          // <= kHistMaxDim; per-channel offsets fit 32 bits
-    const int P = p.P;
-    const int M = p.M;
+    const int d = Ly.d;              // <= kHistMaxDim; per-channel offsets fit 32 bits
+    const int P = B.P;
+    const int M = B.M;
     const double Md = (double)M;
-    int8_t *qk = p.codes + k * (int64_t)P * d;
-    const float *wk = p.W + k * (int64_t)d;
+    int8_t *qk = Ly.codes + k * (int64_t)P * d;
+    const float *wk = Ly.W + k * (int64_t)d;
 
     double r[EPT];
 #pragma unroll
@@ -130,15 +135,15 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
 
         // ---- stop / point count
         if (i == 0) Ew = Er;
-        else if (p.err && t == 0) p.err[k * P + (i - 1)] = (float)Er;
-        if ((i >= P) || (Er == 0.0) || (i >= 1 && Er <= p.tol * Ew)) {
+        else if (Ly.err && t == 0) Ly.err[k * P + (i - 1)] = (float)Er;
+        if ((i >= P) || (Er == 0.0) || (i >= 1 && Er <= B.tol * Ew)) {
             n = i;
             break;
         }
 
         // ---- candidates, cleared histograms
         for (int g = t; g < G; g += T) {
-            const float c = p.grid ? p.grid[g] : (float)((double)(g + 1) / (double)G);
+            const float c = B.grid ? B.grid[g] : (float)((double)(g + 1) / (double)G);
             S.ad[g + 1] = (double)(float)((double)m * (double)c / Md);
             S.ha[g] = 0;
             S.hb[g] = 0;
@@ -311,32 +316,35 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(FitParams p)
             break;
         }
         apend = (float)S.ad[gstar + 1];
-        if (t == 0) p.scales[k * P + i] = apend;
+        if (t == 0) Ly.scales[k * P + i] = apend;
         __syncthreads();   // S.a is rewritten by the next step
     }
 
-    if (t == 0) p.counts[k] = n;
+    if (t == 0) Ly.counts[k] = n;
     for (int q = n + t; q < P; q += T) {
-        p.scales[k * P + q] = 0.0f;
-        if (p.err) p.err[k * P + q] = 0.0f;
+        Ly.scales[k * P + q] = 0.0f;
+        if (Ly.err) Ly.err[k * P + q] = 0.0f;
     }
     for (int q = n; q < P; ++q)
         for (int j = t; j < d; j += T) qk[(int64_t)q * d + j] = 0;
 }
 
 template <int T, int EPT>
-hipError_t launch_hist_t(const FitParams &p, size_t lds, hipStream_t s)
+hipError_t launch_hist_t(const HistBatch &b, int64_t channels, size_t lds, hipStream_t s)
 {
     // the default grid (grid == nullptr) has the closed-form boundary counts
-    auto kern = p.grid ? fit_hist_kernel<T, EPT, false> : fit_hist_kernel<T, EPT, true>;
+    auto kern = b.grid ? fit_hist_kernel<T, EPT, false> : fit_hist_kernel<T, EPT, true>;
     if (lds > 65536) {
         hipError_t e = hipFuncSetAttribute((const void *)kern,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(kern, dim3((unsigned)p.C), dim3(T), lds, s, p);
+    hipLaunchKernelGGL(kern, dim3((unsigned)channels), dim3(T), lds, s, b);
     return hipGetLastError();
 }
+
+// (threads, elements per thread) of each variant, by channel length
+constexpr int kVariantMaxDim[] = {64, 128, 256, 512, 1024, 2048, 4096, 8192, (int)kHistMaxDim};
 
 }  // namespace
 
@@ -345,23 +353,31 @@ size_t fit_hist_lds(int G)
     return (size_t)G * (3 * sizeof(double) + sizeof(long long) + sizeof(int)) + 2 * sizeof(double);
 }
 
-bool fit_hist_supports(int64_t d) { return d <= kHistMaxDim; }
+bool fit_hist_supports(int64_t d) { return d >= 1 && d <= kHistMaxDim; }
 
-hipError_t launch_fit_hist(const FitParams &p, hipStream_t s)
+int hist_variant(int64_t d)
 {
-    const size_t lds = fit_hist_lds(p.G);
-    const int64_t d = p.d;
-    if (d <= 64) return launch_hist_t<64, 1>(p, lds, s);
-    if (d <= 128) return launch_hist_t<64, 2>(p, lds, s);
-    if (d <= 256) return launch_hist_t<64, 4>(p, lds, s);
-    if (d <= 512) return launch_hist_t<256, 2>(p, lds, s);
-    if (d <= 1024) return launch_hist_t<256, 4>(p, lds, s);
-    if (d <= 2048) return launch_hist_t<256, 8>(p, lds, s);
-    if (d <= 4096) return launch_hist_t<256, 16>(p, lds, s);
+    int v = 0;
+    while (d > kVariantMaxDim[v]) ++v;
+    return v;
+}
+
+hipError_t launch_fit_hist(const HistBatch &b, int variant, int64_t channels, hipStream_t s)
+{
+    const size_t lds = fit_hist_lds(b.G);
+    switch (variant) {
+    case 0: return launch_hist_t<64, 1>(b, channels, lds, s);
+    case 1: return launch_hist_t<64, 2>(b, channels, lds, s);
+    case 2: return launch_hist_t<64, 4>(b, channels, lds, s);
+    case 3: return launch_hist_t<256, 2>(b, channels, lds, s);
+    case 4: return launch_hist_t<256, 4>(b, channels, lds, s);
+    case 5: return launch_hist_t<256, 8>(b, channels, lds, s);
+    case 6: return launch_hist_t<256, 16>(b, channels, lds, s);
     // 512 threads leave 256 VGPRs per thread for the register-resident residual
-    if (d <= 8192) return launch_hist_t<512, 16>(p, lds, s);
-    if (d <= kHistMaxDim) return launch_hist_t<512, 32>(p, lds, s);
-    return hipErrorInvalidValue;
+    case 7: return launch_hist_t<512, 16>(b, channels, lds, s);
+    case 8: return launch_hist_t<512, 32>(b, channels, lds, s);
+    default: return hipErrorInvalidValue;
+    }
 }
 
 }  // namespace mpq

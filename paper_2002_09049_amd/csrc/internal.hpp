@@ -40,10 +40,34 @@ FitLayout fit_layout(int64_t d, int G);
 hipError_t launch_fit(const FitParams &p, const FitLayout &L, hipStream_t s);
 
 // Histogram search: exact O(d M + G) candidate errors, residual in registers.
+// One launch fits the channels of up to kMaxBatchLayers layers whose lengths
+// select the same kernel variant (hist_variant); the descriptors travel by
+// value in the kernel arguments.
 constexpr int64_t kHistMaxDim = 16384;
+constexpr int kMaxBatchLayers = 48;
+
+struct HistLayer {
+    const float *W;     // [C][d]
+    int8_t *codes;      // [C][P][d]
+    float *scales;      // [C][P]
+    int32_t *counts;    // [C]
+    float *err;         // [C][P] or nullptr
+    int d;
+    int c_begin;        // first workgroup of this layer in the launch
+};
+
+struct HistBatch {
+    int n_layers;
+    int M, P, G;
+    const float *grid;  // device multipliers or nullptr (default grid)
+    double tol;
+    HistLayer L[kMaxBatchLayers];
+};
+
 size_t fit_hist_lds(int G);
 bool fit_hist_supports(int64_t d);
-hipError_t launch_fit_hist(const FitParams &p, hipStream_t s);
+int hist_variant(int64_t d);   // layers with equal variants may share a launch
+hipError_t launch_fit_hist(const HistBatch &b, int variant, int64_t channels, hipStream_t s);
 
 // Output error of Eq. (12) for a layer; `scratch` holds
 // err_scratch_bytes(C, d, n) bytes (256-byte aligned).

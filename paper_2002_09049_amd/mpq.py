@@ -28,8 +28,18 @@ MPQ_ERR_NOMEM = -4
 MAX_POINTS = 64
 MAX_GRID = 4096
 
-EXPORTS = ("mpq_fit_layer", "mpq_fit_layer_dense", "mpq_fit_max_dim", "mpq_output_error",
-           "mpq_reconstruct", "mpq_last_error")
+EXPORTS = ("mpq_fit_layer", "mpq_fit_layer_dense", "mpq_fit_layers", "mpq_fit_max_dim",
+           "mpq_output_error", "mpq_output_error_layers", "mpq_reconstruct",
+           "mpq_reconstruct_layers", "mpq_last_error")
+
+
+class Layer(ctypes.Structure):
+    """struct mpq_layer (include/mpq.h)."""
+    _fields_ = [("W", ctypes.c_void_p), ("c_out", ctypes.c_int64), ("d", ctypes.c_int64),
+                ("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p),
+                ("counts", ctypes.c_void_p), ("fit_err", ctypes.c_void_p),
+                ("X", ctypes.c_void_p), ("n", ctypes.c_int64), ("out_err", ctypes.c_void_p),
+                ("out_ref", ctypes.c_void_p), ("W_hat", ctypes.c_void_p)]
 
 _lib = None
 
@@ -58,6 +68,12 @@ def load(path: str = LIB_PATH):
     lib.mpq_output_error.restype = i32
     lib.mpq_reconstruct.argtypes = [P, P, P, i64, i64, i32, P, P]
     lib.mpq_reconstruct.restype = i32
+    lib.mpq_fit_layers.argtypes = [P, i32, i32, i32, P, i32, f32, P]
+    lib.mpq_fit_layers.restype = i32
+    lib.mpq_output_error_layers.argtypes = [P, i32, i32, P]
+    lib.mpq_output_error_layers.restype = i32
+    lib.mpq_reconstruct_layers.argtypes = [P, i32, i32, P]
+    lib.mpq_reconstruct_layers.restype = i32
     lib.mpq_last_error.argtypes = []
     lib.mpq_last_error.restype = ctypes.c_char_p
     _lib = lib
@@ -170,3 +186,76 @@ def reconstruct(codes: torch.Tensor, scales: torch.Tensor, counts: torch.Tensor,
                                 _dev(W_hat, torch.float32, "W_hat"), _stream(stream))
     _check(rc)
     return W_hat
+
+
+class LayerSet:
+    """The layers of a network for the batched calls (mpq_fit_layers,
+    mpq_output_error_layers, mpq_reconstruct_layers).
+
+    Allocates the outputs of every layer once on the weights' device and
+    keeps the descriptor array, so each batched call is one C call.
+    ``weights``: list of [C, d] fp32 device tensors; ``calib``: optional list
+    of [d, n] fp32 device tensors (one per layer)."""
+
+    def __init__(self, weights, max_points: int, calib=None, with_fit_err: bool = True,
+                 with_ref: bool = False):
+        self.max_points = max_points
+        self.W = list(weights)
+        self.X = list(calib) if calib is not None else None
+        n = len(self.W)
+        self.arr = (Layer * max(n, 1))()
+        self.codes, self.scales, self.counts, self.fit_err = [], [], [], []
+        self.err, self.ref, self.W_hat = [], [], []
+        for i, W in enumerate(self.W):
+            C, d = W.shape
+            dev = W.device
+            codes = torch.empty((C, max_points, d), dtype=torch.int8, device=dev)
+            scales = torch.empty((C, max_points), dtype=torch.float32, device=dev)
+            counts = torch.empty((C,), dtype=torch.int32, device=dev)
+            ferr = torch.empty((C, max_points), dtype=torch.float32, device=dev) if with_fit_err else None
+            err = torch.empty((C,), dtype=torch.float32, device=dev)
+            ref = torch.empty((C,), dtype=torch.float32, device=dev) if with_ref else None
+            what = torch.empty((C, d), dtype=torch.float32, device=dev)
+            self.codes.append(codes)
+            self.scales.append(scales)
+            self.counts.append(counts)
+            self.fit_err.append(ferr)
+            self.err.append(err)
+            self.ref.append(ref)
+            self.W_hat.append(what)
+            L = self.arr[i]
+            L.W = _dev(W, torch.float32, "W")
+            L.c_out, L.d = C, d
+            L.codes, L.scales, L.counts = codes.data_ptr(), scales.data_ptr(), counts.data_ptr()
+            L.fit_err = None if ferr is None else ferr.data_ptr()
+            if self.X is not None:
+                X = self.X[i]
+                if X.dim() != 2 or X.shape[0] != d:
+                    raise ValueError(f"calib[{i}] must be [d, n]")
+                L.X = _dev(X, torch.float32, "X")
+                L.n = X.shape[1]
+            L.out_err = err.data_ptr()
+            L.out_ref = None if ref is None else ref.data_ptr()
+            L.W_hat = what.data_ptr()
+        self.n = n
+
+    def fit(self, bits: int, n_grid: int, tol: float, grid=None, stream=None):
+        g = None
+        if grid is not None:
+            import numpy as np
+            g = np.ascontiguousarray(grid, dtype=np.float32)
+            if g.shape != (n_grid,):
+                raise ValueError("grid must have n_grid entries")
+        _check(load().mpq_fit_layers(ctypes.addressof(self.arr), self.n, bits, self.max_points,
+                                     None if g is None else g.ctypes.data_as(ctypes.c_void_p),
+                                     n_grid, float(tol), _stream(stream)))
+
+    def output_error(self, stream=None):
+        if self.X is None:
+            raise ValueError("LayerSet was built without calibration batches")
+        _check(load().mpq_output_error_layers(ctypes.addressof(self.arr), self.n, self.max_points,
+                                              _stream(stream)))
+
+    def reconstruct(self, stream=None):
+        _check(load().mpq_reconstruct_layers(ctypes.addressof(self.arr), self.n, self.max_points,
+                                             _stream(stream)))

@@ -94,3 +94,54 @@ def test_output_error_and_reconstruct_reject_invalid_arguments(lib):
 def test_fit_max_dim_rejects_bad_grid(lib):
     from paper_2002_09049_amd import mpq
     assert lib.mpq_fit_max_dim(0) == mpq.MPQ_ERR_INVALID_ARG
+
+
+def test_layer_struct_matches_header(tmp_path):
+    """The binding's mpq_layer has the header's size and field offsets
+    (checked by compiling the header with gcc)."""
+    import subprocess
+    from paper_2002_09049_amd import mpq
+    fields = [f for f, _ in mpq.Layer._fields_]
+    src = tmp_path / "off.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "mpq.h"\nint main(void){\n'
+                   '  printf("%zu\\n", sizeof(mpq_layer));\n' +
+                   "".join(f'  printf("%zu\\n", offsetof(mpq_layer, {f}));\n' for f in fields) +
+                   "  return 0;\n}\n")
+    exe = tmp_path / "off"
+    subprocess.check_call(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)])
+    out = [int(x) for x in subprocess.check_output([str(exe)]).split()]
+    assert out[0] == ctypes.sizeof(mpq.Layer)
+    assert out[1:] == [getattr(mpq.Layer, f).offset for f in fields]
+
+
+def test_batched_calls_reject_invalid_arguments(lib):
+    from paper_2002_09049_amd import mpq
+    E = mpq.MPQ_ERR_INVALID_ARG
+    arr = (mpq.Layer * 2)()
+    for L in arr:
+        L.W, L.c_out, L.d, L.codes, L.scales, L.counts = 1, 4, 16, 1, 1, 1
+        L.X, L.n, L.out_err, L.W_hat = 1, 8, 1, 1
+    p = ctypes.addressof(arr)
+    assert lib.mpq_fit_layers(p, -1, 4, 4, None, 8, 1e-3, None) == E
+    assert lib.mpq_fit_layers(None, 2, 4, 4, None, 8, 1e-3, None) == E
+    assert lib.mpq_fit_layers(p, 2, 9, 4, None, 8, 1e-3, None) == E
+    arr[1].d = 0
+    assert lib.mpq_fit_layers(p, 2, 4, 4, None, 8, 1e-3, None) == E
+    assert b"layer 1" in lib.mpq_last_error()
+    arr[1].d = 16
+    arr[0].codes = None
+    assert lib.mpq_fit_layers(p, 2, 4, 4, None, 8, 1e-3, None) == E
+    assert b"layer 0" in lib.mpq_last_error()
+    arr[0].codes = 1
+    arr[1].n = 0
+    assert lib.mpq_output_error_layers(p, 2, 4, None) == E
+    arr[1].n = 8
+    arr[0].W_hat = None
+    assert lib.mpq_reconstruct_layers(p, 2, 4, None) == E
+    # no channels at all: nothing to do, no device call
+    for L in arr:
+        L.c_out = 0
+    assert lib.mpq_fit_layers(p, 2, 4, 4, None, 8, 1e-3, None) == 0
+    assert lib.mpq_output_error_layers(p, 2, 4, None) == 0
+    assert lib.mpq_reconstruct_layers(p, 2, 4, None) == 0
+    assert lib.mpq_fit_layers(p, 0, 4, 4, None, 8, 1e-3, None) == 0

@@ -272,3 +272,55 @@ def test_workload_full_size_sampled(orc, name):
         del out
         torch.cuda.empty_cache()
     say(f"  {name}: candidate ties in sampled channels: {tot_ties}")
+
+
+@pytest.mark.parametrize("name", ["resnet18", "mobilenetv2"])
+def test_batched_calls_equal_single_layer_calls(orc, name):
+    """mpq_fit_layers / mpq_output_error_layers / mpq_reconstruct_layers on a
+    whole workload give bitwise the outputs of the per-layer calls."""
+    import torch
+    from paper_2002_09049_amd import mpq
+    w = wl.get(name)
+    idx = list(range(len(w.layers)))[:12]
+    Ws = [to_dev(wl.layer_weights(w, i)) for i in idx]
+    Xs = [to_dev(wl.layer_calib(w, i, n=256)) for i in idx]
+    say(f"case batched {name} ({len(idx)} layers)")
+    ls = mpq.LayerSet(Ws, w.max_points, calib=Xs)
+    ls.fit(w.bits, w.n_grid, w.tol)
+    ls.output_error()
+    ls.reconstruct()
+    torch.cuda.synchronize()
+    for j, i in enumerate(idx):
+        c, s, n, e = mpq.fit_layer(Ws[j], w.bits, w.max_points, w.n_grid, w.tol)
+        err, _ = mpq.output_error(Ws[j], c, s, n, Xs[j])
+        Wh = mpq.reconstruct(c, s, n)
+        torch.cuda.synchronize()
+        assert torch.equal(c, ls.codes[j]) and torch.equal(s, ls.scales[j])
+        assert torch.equal(n, ls.counts[j]) and torch.equal(e, ls.fit_err[j])
+        assert torch.equal(err, ls.err[j]) and torch.equal(Wh, ls.W_hat[j])
+    # one layer in lockstep
+    j = len(idx) - 1
+    out = (ls.codes[j].cpu().numpy(), ls.scales[j].cpu().numpy(), ls.counts[j].cpu().numpy(),
+           ls.fit_err[j].cpu().numpy())
+    assert_parity(orc, Ws[j].cpu().numpy(), w.bits, w.max_points, w.n_grid, w.tol, out)
+
+
+def test_batched_fit_many_layers_one_variant(orc):
+    """More layers of one kernel variant than one launch holds (48), mixed
+    with empty layers and layers that take other variants."""
+    import torch
+    from paper_2002_09049_amd import mpq
+    shapes = [(3, 40)] * 50 + [(0, 40), (5, 9), (4, 1000), (2, 40)]
+    Ws = [to_dev(wl.random_weights(c, d, seed=i)) if c else torch.zeros((0, d), device="cuda")
+          for i, (c, d) in enumerate(shapes)]
+    say(f"case batched many layers ({len(shapes)})")
+    ls = mpq.LayerSet(Ws, 4)
+    ls.fit(4, 64, 1e-3)
+    torch.cuda.synchronize()
+    for i, (c, d) in enumerate(shapes):
+        if c == 0:
+            continue
+        W = Ws[i].cpu().numpy()
+        out = (ls.codes[i].cpu().numpy(), ls.scales[i].cpu().numpy(), ls.counts[i].cpu().numpy(),
+               ls.fit_err[i].cpu().numpy())
+        assert_parity(orc, W, 4, 4, 64, 1e-3, out)
