@@ -70,6 +70,64 @@ __device__ __forceinline__ int count_linear(const double *ad, int G, double h, d
     return n0 - 1 + (fma(h, lo, -x) < 0.0 ? 1 : 0) + (fma(h, hi, -x) < 0.0 ? 1 : 0);
 }
 
+// Histogram of the level boundaries of this thread's elements.  Level-major:
+// for each level, the counts of a chunk of elements are found first
+// (independent LDS reads in flight together), then binned.  A boundary that
+// every candidate passes (n = G: most elements at the low levels) would send
+// most lanes to bin G-1 at once; those are summed in fullA / fullB and added
+// by the caller with one atomic per wavefront.
+template <int T, int EPT, bool kLinear>
+__device__ __forceinline__ void bin_levels(const double (&r)[EPT], const HistShared &S, int G, int M,
+                                           float m, int sh, unsigned long long &fullA, int &fullB)
+{
+    const float gm = (float)G * (float)M / m;
+    // per element and step: fixed-point |r| and the scaled estimate base
+    constexpr bool kKeep = EPT <= 16;
+    unsigned long long Xk[kKeep ? EPT : 1];
+    float Bk[kKeep ? EPT : 1];
+    if constexpr (kKeep) {
+#pragma unroll
+        for (int u = 0; u < EPT; ++u) {
+            Xk[u] = (unsigned long long)rint(ldexp(fabs(r[u]), sh));
+            Bk[u] = (float)fabs(r[u]) * gm;
+        }
+    }
+    constexpr int kChunk = EPT < 8 ? EPT : 8;
+    for (int kk = 0; kk < M; ++kk) {
+        const double h = (double)kk + 0.5;
+        const float rh = __builtin_amdgcn_rcpf((float)h);
+        const int inc = 2 * kk + 1;
+#pragma unroll
+        for (int u0 = 0; u0 < EPT; u0 += kChunk) {
+            int nb[kChunk];
+#pragma unroll
+            for (int v = 0; v < kChunk; ++v) {
+                const int u = u0 + v;
+                const double x = fabs(r[u]);
+                if constexpr (kLinear) {
+                    const float base = kKeep ? Bk[kKeep ? u : 0] : (float)x * gm;
+                    nb[v] = count_linear(S.ad, G, h, x, base * rh);
+                } else {
+                    nb[v] = count_bsearch(S.ad, G, h, x);
+                }
+            }
+#pragma unroll
+            for (int v = 0; v < kChunk; ++v) {
+                const int u = u0 + v;
+                const unsigned long long X =
+                    kKeep ? Xk[kKeep ? u : 0] : (unsigned long long)rint(ldexp(fabs(r[u]), sh));
+                const bool full = nb[v] == G;
+                fullA += full ? X : 0ull;
+                fullB += full ? inc : 0;
+                if (nb[v] > 0 && !full) {
+                    atomicAdd((unsigned long long *)&S.ha[nb[v] - 1], X);
+                    atomicAdd(&S.hb[nb[v] - 1], inc);
+                }
+            }
+        }
+    }
+}
+
 template <int T, int EPT, bool kLinear>
 __global__ void __launch_bounds__(T) fit_hist_kernel(const HistBatch B)
 {
@@ -160,58 +218,14 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(const HistBatch B)
         const int sh = 61 - (ex + 1) - lg;
         __syncthreads();
 
-        // ---- histograms of the level boundaries.  Level-major: for each
-        // level, the counts of all of this thread's elements are found first
-        // (independent LDS reads in flight together), then binned.  A boundary
-        // that every candidate passes (n = G: most elements at the low levels)
-        // would send most lanes to bin G-1 at once; those are summed in
-        // registers and added with one atomic per wavefront.
-        const float gm = (float)G * (float)M / m;
+        // ---- histograms of the level boundaries (bin_levels)
         unsigned long long fullA = 0;
         int fullB = 0;
-        // per element and step: fixed-point |r| and the scaled estimate base
-        constexpr bool kKeep = EPT <= 16;
-        unsigned long long Xk[kKeep ? EPT : 1];
-        float Bk[kKeep ? EPT : 1];
-        if constexpr (kKeep) {
-#pragma unroll
-            for (int u = 0; u < EPT; ++u) {
-                Xk[u] = (unsigned long long)rint(ldexp(fabs(r[u]), sh));
-                Bk[u] = (float)fabs(r[u]) * gm;
-            }
-        }
-        constexpr int kChunk = EPT < 8 ? EPT : 8;
-        for (int kk = 0; kk < M; ++kk) {
-            const double h = (double)kk + 0.5;
-            const float rh = __builtin_amdgcn_rcpf((float)h);
-            const int inc = 2 * kk + 1;
-#pragma unroll
-            for (int u0 = 0; u0 < EPT; u0 += kChunk) {
-                int nb[kChunk];
-#pragma unroll
-                for (int v = 0; v < kChunk; ++v) {
-                    const int u = u0 + v;
-                    const double x = fabs(r[u]);
-                    const float base = kKeep ? Bk[kKeep ? u : 0] : (float)x * gm;
-                    if constexpr (kLinear) nb[v] = count_linear(S.ad, G, h, x, base * rh);
-                    else nb[v] = count_bsearch(S.ad, G, h, x);
-                }
-#pragma unroll
-                for (int v = 0; v < kChunk; ++v) {
-                    const int u = u0 + v;
-                    const unsigned long long X =
-                        kKeep ? Xk[kKeep ? u : 0]
-                              : (unsigned long long)rint(ldexp(fabs(r[u]), sh));
-                    const bool full = nb[v] == G;
-                    fullA += full ? X : 0ull;
-                    fullB += full ? inc : 0;
-                    if (nb[v] > 0 && !full) {
-                        atomicAdd((unsigned long long *)&S.ha[nb[v] - 1], X);
-                        atomicAdd(&S.hb[nb[v] - 1], inc);
-                    }
-                }
-            }
-        }
+        // the closed-form counts need normal candidates and a finite estimate
+        if (kLinear && m >= 0x1p-100f)
+            bin_levels<T, EPT, true>(r, S, G, M, m, sh, fullA, fullB);
+        else
+            bin_levels<T, EPT, false>(r, S, G, M, m, sh, fullA, fullB);
 #pragma unroll
         for (int off = 1; off < kWave; off <<= 1) {
             fullA += (unsigned long long)__shfl_xor((long long)fullA, off);
