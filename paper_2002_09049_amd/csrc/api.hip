@@ -8,6 +8,7 @@
 
 #include <mutex>
 #include <string>
+#include <vector>
 
 #include "internal.hpp"
 #include "mpq.h"
@@ -279,10 +280,8 @@ int check_error_layer(const mpq_layer &L, int max_points, bool need_x)
         if (L.n < 1) return fail(MPQ_ERR_INVALID_ARG, "n must be >= 1 (got %lld)", (long long)L.n);
         if (L.c_out > 0 && (!L.W || !L.codes || !L.scales || !L.counts || !L.X || !L.out_err))
             return fail(MPQ_ERR_INVALID_ARG, "W, codes, scales, counts, X and err must not be NULL");
-        if ((L.c_out + 127) / 128 > 65535)
-            return fail(MPQ_ERR_INVALID_ARG, "c_out too large (%lld)", (long long)L.c_out);
-        if ((L.n + 127) / 128 > 0x7fffffffLL)
-            return fail(MPQ_ERR_INVALID_ARG, "n too large (%lld)", (long long)L.n);
+        if (L.c_out > 0x7fffffffLL || L.n > 0x7fffffffLL || L.d > 0x7fffffffLL - 16)
+            return fail(MPQ_ERR_INVALID_ARG, "c_out, d or n too large");
     } else if (L.c_out > 0 && (!L.codes || !L.scales || !L.counts || !L.W_hat)) {
         return fail(MPQ_ERR_INVALID_ARG, "codes, scales, counts and W_hat must not be NULL");
     }
@@ -293,26 +292,22 @@ int output_error_impl(const mpq_layer *layers, int n_layers, int max_points, voi
 {
     if (n_layers < 0 || (n_layers > 0 && !layers))
         return fail(MPQ_ERR_INVALID_ARG, "layers must hold n_layers >= 0 entries");
-    size_t bytes = 0;
+    std::vector<mpq::ErrLayerIn> in;
     for (int l = 0; l < n_layers; ++l) {
-        int rc = check_error_layer(layers[l], max_points, true);
+        const mpq_layer &L = layers[l];
+        int rc = check_error_layer(L, max_points, true);
         if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
-        if (layers[l].c_out > 0) {
-            const size_t b = mpq::err_scratch_bytes(layers[l].c_out, layers[l].d, layers[l].n);
-            if (b > bytes) bytes = b;
-        }
+        if (L.c_out == 0) continue;
+        in.push_back(mpq::ErrLayerIn{L.W, L.codes, L.scales, L.counts, L.X, L.out_err, L.out_ref,
+                                     L.c_out, L.d, L.n});
     }
-    if (bytes == 0) return MPQ_OK;
+    if (in.empty()) return MPQ_OK;
+    const size_t bytes = mpq::err_scratch_bytes(in.data(), (int)in.size());
     hipStream_t s = (hipStream_t)stream;
     void *scratch = nullptr;
     hipError_t e = mpq::scratch_alloc(&scratch, bytes, s);
     if (e != hipSuccess) return fail(MPQ_ERR_NOMEM, "scratch of %zu bytes: %s", bytes, hipGetErrorString(e));
-    for (int l = 0; l < n_layers && e == hipSuccess; ++l) {
-        const mpq_layer &L = layers[l];
-        if (L.c_out == 0) continue;
-        e = mpq::launch_output_error(L.W, L.codes, L.scales, L.counts, L.c_out, L.d, max_points, L.X,
-                                     L.n, L.out_err, L.out_ref, scratch, s);
-    }
+    e = mpq::launch_output_error(in.data(), (int)in.size(), max_points, scratch, s);
     (void)mpq::scratch_free(scratch, s);
     if (e != hipSuccess) return hip_fail(e, "output error kernel launch");
     return MPQ_OK;

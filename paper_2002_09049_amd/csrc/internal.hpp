@@ -69,13 +69,20 @@ bool fit_hist_supports(int64_t d);
 int hist_variant(int64_t d);   // layers with equal variants may share a launch
 hipError_t launch_fit_hist(const HistBatch &b, int variant, int64_t channels, hipStream_t s);
 
-// Output error of Eq. (12) for a layer; `scratch` holds
-// err_scratch_bytes(C, d, n) bytes (256-byte aligned).
-size_t err_scratch_bytes(int64_t C, int64_t d, int64_t n);
-hipError_t launch_output_error(const float *W, const int8_t *codes, const float *scales,
-                               const int32_t *counts, int64_t C, int64_t d, int P,
-                               const float *X, int64_t n, float *err, float *ref,
-                               void *scratch, hipStream_t s);
+// Output error of Eq. (12) for a list of layers; `scratch` holds
+// err_scratch_bytes(...) bytes (256-byte aligned).
+struct ErrLayerIn {
+    const float *W;
+    const int8_t *codes;
+    const float *scales;
+    const int32_t *counts;
+    const float *X;
+    float *err;
+    float *ref;     // nullptr: no ref for this layer
+    int64_t C, d, n;
+};
+size_t err_scratch_bytes(const ErrLayerIn *in, int n_in);
+hipError_t launch_output_error(const ErrLayerIn *in, int n_in, int P, void *scratch, hipStream_t s);
 
 // Stream-ordered scratch from a library-owned memory pool of the current
 // device (kept, not returned to the system, between calls).

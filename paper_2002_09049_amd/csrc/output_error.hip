@@ -1,26 +1,30 @@
-// Output error of a quantized layer on a calibration batch (Sec. 3.3,
+// Output error of quantized layers on their calibration batches (Sec. 3.3,
 // Eq. (12)): err[k] = (1/n) sum_t ((w_k - w~_k) . x_t)^2 and optionally
 // ref[k] = (1/n) sum_t (w_k . x_t)^2.
 //
-// Three kernels:
-//  1. form_rows: A[k][j] = fl32(w_kj - sum_i a_i q_ij) (fp64 sum in point
-//     order) into a scratch matrix whose rows are padded to a multiple of 16
-//     with zeros (aligned float4 rows, no K tail).  HBM-bound, coalesced.
-//     With use_points = 0 it writes a padded copy of W (for ref).
+// Up to kMaxErrLayers layers go through three launches together (their
+// descriptors travel by value in the kernel arguments):
+//  1. form: A[k][j] = fl32(w_kj - sum_i a_i q_ij) (fp64 sum in point order)
+//     into a scratch matrix whose rows are padded to a multiple of 16 with
+//     zeros (aligned float4 rows, no K tail).  HBM-bound, coalesced.  A ref
+//     output is one more item of the group with A = W.
 //  2. gemm: Y = A X on MFMA (v_mfma_f32_32x32x2f32, fp32 in and accumulate),
-//     the path's one dense contraction.  A workgroup of four wavefronts owns
-//     a 128 x 128 tile of Y and one K range; each wavefront owns 64 x 64 as
+//     the path's one dense contraction.  A workgroup of four wavefronts owns a
+//     128 x 128 tile of Y and one K range; each wavefront owns 64 x 64 as
 //     2 x 2 MFMA blocks.  The K loop stages 16-deep slabs of A and X through
 //     double-buffered LDS, loading the next slab into registers while the
-//     MFMAs consume the current one.  When the layer has too few tiles to fill
-//     the chip, K is split across workgroups (splits).
+//     MFMAs consume the current one.  The tiles of all layers form one grid,
+//     longest first; a layer's K is split when it has too few tiles.
 //       splits == 1: the epilogue squares Y and sums each row over the tile's
 //         columns (fp64 cross-lane sums with DPP / ds_swizzle) -> one partial
 //         per (column tile, row).
 //       splits  > 1: the epilogue stores the fp32 Y tile of its K range.
-//  3. finish: splits == 1: sum the row partials in tile order; splits > 1:
-//     per row, sum the K-range tiles of every column, square, and sum over the
-//     columns (fp64), in a fixed order.  Divide by n.
+//  3. finish: one workgroup per row: sum the row partials in tile order, or
+//     sum the K-range tiles of every column, square, and sum over the columns
+//     (fp64), in a fixed order.  Divide by n.
+#include <algorithm>
+#include <vector>
+
 #include "internal.hpp"
 #include "mpq.h"
 #include "reduce.hpp"
@@ -34,57 +38,83 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 constexpr int kBM = 128, kBN = 128, kBK = 16;
 constexpr int kThreads = 256;
 constexpr int kPad = 4;  // LDS row padding (floats)
+constexpr int kMaxErrLayers = 32;
 
-__global__ void __launch_bounds__(256)
-form_rows_kernel(const float *__restrict__ W, const int8_t *__restrict__ codes,
-                 const float *__restrict__ scales, const int32_t *__restrict__ counts,
-                 int64_t C, int64_t d, int64_t ld, int P, int use_points, float *__restrict__ A)
+struct ErrLayer {
+    const float *W;
+    const int8_t *codes;
+    const float *scales;
+    const int32_t *counts;
+    const float *X;
+    float *out;        // err or ref
+    float *A;          // scratch [C][lda]
+    void *part;        // scratch: double [ntn][C] (splits == 1) or float [splits][C][n]
+    int C, d, n, lda;
+    int ntm, ntn, splits, kchunk;
+    int tile_begin;    // first gemm workgroup of this layer
+    int row_begin;     // first finish workgroup of this layer
+    int use_points;    // 1: A = residual (err), 0: A = W (ref)
+};
+
+struct ErrGroup {
+    int n_layers;
+    int P;
+    int vecx;          // every X row start is 16-byte aligned and n % 4 == 0
+    ErrLayer L[kMaxErrLayers];
+};
+
+__global__ void __launch_bounds__(256) form_rows_kernel(const ErrGroup g)
 {
-    const int64_t total = C * ld;
+    const ErrLayer &L = g.L[blockIdx.y];
+    const int64_t total = (int64_t)L.C * L.lda;
     for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
          e += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t k = e / ld, j = e - k * ld;
+        const int64_t k = e / L.lda, j = e - k * L.lda;
         float v = 0.0f;
-        if (j < d) {
-            double r = (double)W[k * d + j];
-            if (use_points) {
-                const int nk = min(max(counts[k], 0), P);  // clamp: counts is caller data
-                const int8_t *q = codes + k * (int64_t)P * d + j;
-                const float *a = scales + k * (int64_t)P;
-                for (int i = 0; i < nk; ++i) r = fma(-(double)a[i], (double)q[(int64_t)i * d], r);
+        if (j < L.d) {
+            double r = (double)L.W[k * L.d + j];
+            if (L.use_points) {
+                const int nk = min(max(L.counts[k], 0), g.P);  // clamp: counts is caller data
+                const int8_t *q = L.codes + k * (int64_t)g.P * L.d + j;
+                const float *a = L.scales + k * (int64_t)g.P;
+                for (int i = 0; i < nk; ++i) r = fma(-(double)a[i], (double)q[(int64_t)i * L.d], r);
             }
             v = (float)r;
         }
-        A[e] = v;
+        L.A[e] = v;
     }
 }
 
-// One K range [kbeg, kend) of a 128 x 128 tile; kbeg, kend multiples of 16.
-// A: [C][lda] (lda multiple of 16, zero padded), X: [d][n].
-template <bool kSquare, bool kVecX>
-__global__ void __launch_bounds__(kThreads)
-gemm_kernel(const float *__restrict__ A, int64_t lda, int64_t C, const float *__restrict__ X,
-            int64_t d, int64_t n, int64_t kchunk, double *__restrict__ rowpart,
-            float *__restrict__ ypart)
+template <bool kVecX>
+__global__ void __launch_bounds__(kThreads) gemm_kernel(const ErrGroup g)
 {
     __shared__ __align__(16) float sA[2][kBK][kBM + kPad];
     __shared__ __align__(16) float sX[2][kBK][kBN + kPad];
     __shared__ double sRow[kBM];
 
+    int li = 0;
+    while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].tile_begin) ++li;
+    const ErrLayer &L = g.L[li];
+    const int local = (int)blockIdx.x - L.tile_begin;
+    const int per_split = L.ntm * L.ntn;
+    const int split = local / per_split;
+    const int tm = (local % per_split) / L.ntn, tn = local % L.ntn;
+
     const int t = threadIdx.x;
     const int lane = t % kWave, wid = t / kWave;
     const int wm = wid / 2, wn = wid % 2;
-    const int64_t row0 = (int64_t)blockIdx.y * kBM;
-    const int64_t col0 = (int64_t)blockIdx.x * kBN;
-    const int split = blockIdx.z;
-    const int64_t kbeg = (int64_t)split * kchunk;
-    const int64_t kend = min(kbeg + kchunk, lda);
+    const int64_t C = L.C, n = L.n, d = L.d, lda = L.lda;
+    const int64_t row0 = (int64_t)tm * kBM;
+    const int64_t col0 = (int64_t)tn * kBN;
+    const int64_t kbeg = (int64_t)split * L.kchunk;
+    const int64_t kend = min(kbeg + (int64_t)L.kchunk, lda);
+    const float *__restrict__ X = L.X;
 
     // staging roles
     const int arow = t / 2, ak0 = (t % 2) * 8;     // A: 8 consecutive k of one row
     const int64_t agrow = row0 + arow;
     const bool arow_ok = agrow < C;
-    const float *ap = A + (arow_ok ? agrow : 0) * lda;
+    const float *ap = L.A + (arow_ok ? agrow : 0) * lda;
     const int xk = t / 16, xc0 = (t % 16) * 8;     // X: 8 consecutive columns of one k
 
     float ra[8], rx[8];
@@ -161,7 +191,7 @@ gemm_kernel(const float *__restrict__ A, int64_t lda, int64_t C, const float *__
 
     // Output layout of a 32 x 32 MFMA block: lane holds column lane % 32 and,
     // in register v, row 8 * (v / 4) + 4 * (lane / 32) + (v % 4).
-    if constexpr (kSquare) {
+    if (L.splits == 1) {
         for (int pass = 0; pass < 2; ++pass) {
             if (wn == pass) {
 #pragma unroll
@@ -179,13 +209,14 @@ gemm_kernel(const float *__restrict__ A, int64_t lda, int64_t C, const float *__
             }
             __syncthreads();
         }
+        double *rowpart = (double *)L.part;
         for (int r = t; r < kBM; r += kThreads) {
             const int64_t gr = row0 + r;
-            if (gr < C) rowpart[(int64_t)blockIdx.x * C + gr] = sRow[r];
+            if (gr < C) rowpart[(int64_t)tn * C + gr] = sRow[r];
         }
     } else {
         // Y tile of this K range: ypart[split][row][col]
-        float *yp = ypart + (int64_t)split * C * n;
+        float *yp = (float *)L.part + (int64_t)split * C * n;
 #pragma unroll
         for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -199,111 +230,157 @@ gemm_kernel(const float *__restrict__ A, int64_t lda, int64_t C, const float *__
     }
 }
 
-__global__ void finish_rows_kernel(const double *__restrict__ rowpart, int64_t C, int ntiles,
-                                   double inv_n, float *__restrict__ out)
-{
-    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (k >= C) return;
-    double s = 0.0;
-    for (int i = 0; i < ntiles; ++i) s += rowpart[(int64_t)i * C + k];
-    out[k] = (float)(s * inv_n);
-}
-
-// one workgroup per row: sum the K-range tiles, square, sum over columns
-__global__ void __launch_bounds__(256)
-finish_split_kernel(const float *__restrict__ ypart, int64_t C, int64_t n, int splits,
-                    double inv_n, float *__restrict__ out)
+// one workgroup per row of every layer
+__global__ void __launch_bounds__(256) finish_kernel(const ErrGroup g)
 {
     __shared__ double red[256 / kWave];
-    const int64_t k = blockIdx.x;
+    int li = 0;
+    while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].row_begin) ++li;
+    const ErrLayer &L = g.L[li];
+    const int64_t k = (int64_t)blockIdx.x - L.row_begin;
+    const int64_t C = L.C, n = L.n;
     double s = 0.0;
-    for (int64_t c = threadIdx.x; c < n; c += 256) {
-        float y = 0.0f;
-        for (int sp = 0; sp < splits; ++sp) y += ypart[((int64_t)sp * C + k) * n + c];
-        s += (double)y * (double)y;
+    if (L.splits == 1) {
+        const double *rp = (const double *)L.part;
+        if (threadIdx.x == 0)
+            for (int i = 0; i < L.ntn; ++i) s += rp[(int64_t)i * C + k];
+    } else {
+        const float *yp = (const float *)L.part;
+        for (int64_t c = threadIdx.x; c < n; c += 256) {
+            float y = 0.0f;
+            for (int sp = 0; sp < L.splits; ++sp) y += yp[((int64_t)sp * C + k) * n + c];
+            s += (double)y * (double)y;
+        }
     }
     s = block_reduce<256>(s, SumOp(), red);
-    if (threadIdx.x == 0) out[k] = (float)(s * inv_n);
+    if (threadIdx.x == 0) L.out[k] = (float)(s / (double)n);
 }
 
-struct Plan {
-    int64_t lda;       // padded row length of the scratch matrix
-    int64_t ntiles_n;  // column tiles
-    int64_t ntiles_m;  // row tiles
-    int splits;
-    int64_t kchunk;    // K per split (multiple of kBK)
+struct Item {
+    const ErrLayerIn *in;
+    int use_points;
 };
 
-Plan plan(int64_t C, int64_t d, int64_t n)
+struct Plan {
+    int64_t lda, ntm, ntn, splits, kchunk;
+    size_t a_bytes, part_bytes;
+};
+
+size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
+// err items for every layer, then ref items for the layers that want ref
+std::vector<Item> items_of(const ErrLayerIn *in, int n_in)
 {
-    Plan p;
-    p.lda = (d + kBK - 1) / kBK * kBK;
-    p.ntiles_n = (n + kBN - 1) / kBN;
-    p.ntiles_m = (C + kBM - 1) / kBM;
-    const int64_t tiles = p.ntiles_n * p.ntiles_m;
-    const int64_t kslabs = p.lda / kBK;
-    int64_t s = 1;
-    // aim for >= 2 workgroups per CU (256 CUs) with >= 16 slabs of K each
-    while (tiles * s < 512 && kslabs / (s * 2) >= 16) s *= 2;
-    p.splits = (int)s;
-    p.kchunk = (kslabs + s - 1) / s * kBK;
+    std::vector<Item> it;
+    for (int i = 0; i < n_in; ++i)
+        if (in[i].C > 0) it.push_back(Item{&in[i], 1});
+    for (int i = 0; i < n_in; ++i)
+        if (in[i].C > 0 && in[i].ref) it.push_back(Item{&in[i], 0});
+    return it;
+}
+
+// K split of a layer: tiles of about work / 512 slabs (two per CU), at least
+// 32 slabs.  It depends on the layer alone, so a layer's result does not
+// depend on the other layers of the call.
+std::vector<Plan> plan_group(const Item *it, int cnt)
+{
+    std::vector<Plan> p(cnt);
+    for (int i = 0; i < cnt; ++i) {
+        const ErrLayerIn &I = *it[i].in;
+        Plan &q = p[i];
+        q.lda = (I.d + kBK - 1) / kBK * kBK;
+        q.ntm = (I.C + kBM - 1) / kBM;
+        q.ntn = (I.n + kBN - 1) / kBN;
+        const int64_t slabs = q.lda / kBK;
+        const double work = (double)(q.ntm * q.ntn) * (double)slabs;
+        const int64_t target = std::max<int64_t>(32, (int64_t)(work / 512.0 + 0.5));
+        int64_t sp = (slabs + target / 2) / target;
+        sp = std::max<int64_t>(1, std::min<int64_t>(sp, slabs));
+        q.splits = sp;
+        q.kchunk = (slabs + sp - 1) / sp * kBK;
+        q.a_bytes = align256(sizeof(float) * (size_t)(I.C * q.lda));
+        q.part_bytes = align256(sp == 1 ? sizeof(double) * (size_t)(q.ntn * I.C)
+                                        : sizeof(float) * (size_t)(sp * I.C * I.n));
+    }
     return p;
 }
 
 }  // namespace
 
-size_t err_scratch_bytes(int64_t C, int64_t d, int64_t n)
+size_t err_scratch_bytes(const ErrLayerIn *in, int n_in)
 {
-    const Plan p = plan(C, d, n);
-    size_t a = sizeof(float) * (size_t)(C * p.lda);
-    size_t part = p.splits == 1 ? sizeof(double) * (size_t)(p.ntiles_n * C)
-                                : sizeof(float) * (size_t)(p.splits * C * n);
-    return (a + 255) / 256 * 256 + part;
+    const std::vector<Item> it = items_of(in, n_in);
+    size_t total = 0;
+    for (size_t base = 0; base < it.size(); base += kMaxErrLayers) {
+        const int cnt = (int)std::min<size_t>(kMaxErrLayers, it.size() - base);
+        std::vector<Plan> p = plan_group(it.data() + base, cnt);
+        size_t b = 0;
+        for (const Plan &q : p) b += q.a_bytes + q.part_bytes;
+        total = std::max(total, b);
+    }
+    return total;
 }
 
-hipError_t launch_output_error(const float *W, const int8_t *codes, const float *scales,
-                               const int32_t *counts, int64_t C, int64_t d, int P,
-                               const float *X, int64_t n, float *err, float *ref,
-                               void *scratch, hipStream_t s)
+hipError_t launch_output_error(const ErrLayerIn *in, int n_in, int P, void *scratch, hipStream_t s)
 {
-    const Plan p = plan(C, d, n);
-    float *A = (float *)scratch;
-    char *part = (char *)scratch + (sizeof(float) * (size_t)(C * p.lda) + 255) / 256 * 256;
-    const bool vecx = (n % 4 == 0) && (((uintptr_t)X) % 16 == 0);
-    const double inv_n = 1.0 / (double)n;
-    for (int pass = 0; pass < (ref ? 2 : 1); ++pass) {
-        const int use_points = pass == 0;
-        float *out = pass == 0 ? err : ref;
-        int64_t blocks = (C * p.lda + 255) / 256;
-        if (blocks > 65536) blocks = 65536;
-        hipLaunchKernelGGL(form_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, s, W, codes,
-                           scales, counts, C, d, p.lda, P, use_points, A);
+    const std::vector<Item> it = items_of(in, n_in);
+    for (size_t base = 0; base < it.size(); base += kMaxErrLayers) {
+        const int cnt = (int)std::min<size_t>(kMaxErrLayers, it.size() - base);
+        const Item *grp = it.data() + base;
+        std::vector<Plan> p = plan_group(grp, cnt);
+        // longest tiles first
+        std::vector<int> order(cnt);
+        for (int i = 0; i < cnt; ++i) order[i] = i;
+        std::stable_sort(order.begin(), order.end(),
+                         [&](int a, int b) { return p[a].kchunk > p[b].kchunk; });
+        ErrGroup g;
+        g.n_layers = cnt;
+        g.P = P;
+        g.vecx = 1;
+        char *cur = (char *)scratch;
+        int64_t tiles = 0, rows = 0, max_elems = 0;
+        for (int o = 0; o < cnt; ++o) {
+            const int i = order[o];
+            const ErrLayerIn &I = *grp[i].in;
+            const Plan &q = p[i];
+            ErrLayer &L = g.L[o];
+            L.W = I.W;
+            L.codes = I.codes;
+            L.scales = I.scales;
+            L.counts = I.counts;
+            L.X = I.X;
+            L.out = grp[i].use_points ? I.err : I.ref;
+            L.use_points = grp[i].use_points;
+            L.A = (float *)cur;
+            cur += q.a_bytes;
+            L.part = cur;
+            cur += q.part_bytes;
+            L.C = (int)I.C;
+            L.d = (int)I.d;
+            L.n = (int)I.n;
+            L.lda = (int)q.lda;
+            L.ntm = (int)q.ntm;
+            L.ntn = (int)q.ntn;
+            L.splits = (int)q.splits;
+            L.kchunk = (int)q.kchunk;
+            L.tile_begin = (int)tiles;
+            L.row_begin = (int)rows;
+            tiles += q.ntm * q.ntn * q.splits;
+            rows += I.C;
+            max_elems = std::max<int64_t>(max_elems, I.C * q.lda);
+            if (I.n % 4 != 0 || ((uintptr_t)I.X) % 16 != 0) g.vecx = 0;
+        }
+        const int64_t fblocks = std::min<int64_t>((max_elems + 255) / 256, 4096);
+        hipLaunchKernelGGL(form_rows_kernel, dim3((unsigned)fblocks, (unsigned)cnt), dim3(256), 0, s, g);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        dim3 grid((unsigned)p.ntiles_n, (unsigned)p.ntiles_m, (unsigned)p.splits);
-        if (p.splits == 1) {
-            if (vecx)
-                hipLaunchKernelGGL((gemm_kernel<true, true>), grid, dim3(kThreads), 0, s, A, p.lda, C,
-                                   X, d, n, p.kchunk, (double *)part, (float *)nullptr);
-            else
-                hipLaunchKernelGGL((gemm_kernel<true, false>), grid, dim3(kThreads), 0, s, A, p.lda, C,
-                                   X, d, n, p.kchunk, (double *)part, (float *)nullptr);
-            e = hipGetLastError();
-            if (e != hipSuccess) return e;
-            hipLaunchKernelGGL(finish_rows_kernel, dim3((unsigned)((C + 255) / 256)), dim3(256), 0, s,
-                               (const double *)part, C, (int)p.ntiles_n, inv_n, out);
-        } else {
-            if (vecx)
-                hipLaunchKernelGGL((gemm_kernel<false, true>), grid, dim3(kThreads), 0, s, A, p.lda, C,
-                                   X, d, n, p.kchunk, (double *)nullptr, (float *)part);
-            else
-                hipLaunchKernelGGL((gemm_kernel<false, false>), grid, dim3(kThreads), 0, s, A, p.lda, C,
-                                   X, d, n, p.kchunk, (double *)nullptr, (float *)part);
-            e = hipGetLastError();
-            if (e != hipSuccess) return e;
-            hipLaunchKernelGGL(finish_split_kernel, dim3((unsigned)C), dim3(256), 0, s,
-                               (const float *)part, C, n, p.splits, inv_n, out);
-        }
+        if (g.vecx)
+            hipLaunchKernelGGL(gemm_kernel<true>, dim3((unsigned)tiles), dim3(kThreads), 0, s, g);
+        else
+            hipLaunchKernelGGL(gemm_kernel<false>, dim3((unsigned)tiles), dim3(kThreads), 0, s, g);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(finish_kernel, dim3((unsigned)rows), dim3(256), 0, s, g);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
