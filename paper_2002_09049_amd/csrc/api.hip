@@ -317,17 +317,15 @@ int reconstruct_impl(const mpq_layer *layers, int n_layers, int max_points, void
 {
     if (n_layers < 0 || (n_layers > 0 && !layers))
         return fail(MPQ_ERR_INVALID_ARG, "layers must hold n_layers >= 0 entries");
+    std::vector<mpq::RecLayer> in;
     for (int l = 0; l < n_layers; ++l) {
-        int rc = check_error_layer(layers[l], max_points, false);
-        if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
-    }
-    hipError_t e = hipSuccess;
-    for (int l = 0; l < n_layers && e == hipSuccess; ++l) {
         const mpq_layer &L = layers[l];
-        if (L.c_out == 0) continue;
-        e = mpq::launch_reconstruct(L.codes, L.scales, L.counts, L.c_out, L.d, max_points, L.W_hat,
-                                    (hipStream_t)stream);
+        int rc = check_error_layer(L, max_points, false);
+        if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
+        if (L.c_out > 0) in.push_back(mpq::RecLayer{L.codes, L.scales, L.counts, L.W_hat, L.c_out, L.d});
     }
+    if (in.empty()) return MPQ_OK;
+    hipError_t e = mpq::launch_reconstruct(in.data(), (int)in.size(), max_points, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "reconstruct kernel launch");
     return MPQ_OK;
 }

@@ -89,7 +89,15 @@ hipError_t launch_output_error(const ErrLayerIn *in, int n_in, int P, void *scra
 hipError_t scratch_alloc(void **p, size_t bytes, hipStream_t s);
 hipError_t scratch_free(void *p, hipStream_t s);
 
-hipError_t launch_reconstruct(const int8_t *codes, const float *scales, const int32_t *counts,
-                              int64_t C, int64_t d, int P, float *W_hat, hipStream_t s);
+// Reconstruction of Eq. (4) for a list of layers.
+struct RecLayer {
+    const int8_t *codes;
+    const float *scales;
+    const int32_t *counts;
+    float *W_hat;
+    int64_t C, d;
+};
+constexpr int kMaxRecLayers = 64;
+hipError_t launch_reconstruct(const RecLayer *in, int n_in, int P, hipStream_t s);
 
 }  // namespace mpq
