@@ -36,6 +36,8 @@ constexpr int kMaxFinalists = 8;
 
 struct HistShared {
     double *ad;      // [G + 2]: ad[0] = 0, ad[g + 1] = a_g (an fp32 value), ad[G + 1] = +inf
+    float *af;       // [G + 2]: the same values in fp32 (half the LDS bytes per read)
+    float *c;        // [G]: grid multipliers c_g
     long long *ha;   // [G] fixed-point sum of x per bin
     int *hb;         // [G] sum of (2k + 1) per bin
     double *e;       // [G] approximate candidate errors
@@ -63,10 +65,10 @@ __device__ __forceinline__ int count_bsearch(const double *ad, int G, double h, 
 // n0 - 1 <= n <= n0 + 1.  Hence n = n0 - 1 + [a_{n0-1} below] + [a_{n0} below]
 // (ad[n0] and ad[n0 + 1]; the sentinels cover n0 = 0 and n0 = G).  The sign
 // of fma(h, a, -x) is exact: h a is exact in fp64 and the fma rounds once.
-__device__ __forceinline__ int count_linear(const double *ad, int G, double h, double x, float est)
+__device__ __forceinline__ int count_linear(const float *af, int G, double h, double x, float est)
 {
     const int n0 = (int)fminf(est, (float)G);
-    const double lo = ad[n0], hi = ad[n0 + 1];
+    const double lo = (double)af[n0], hi = (double)af[n0 + 1];
     return n0 - 1 + (fma(h, lo, -x) < 0.0 ? 1 : 0) + (fma(h, hi, -x) < 0.0 ? 1 : 0);
 }
 
@@ -82,7 +84,7 @@ __device__ __forceinline__ void bin_levels(const double (&r)[EPT], const HistSha
 {
     const float gm = (float)G * (float)M / m;
     // per element and step: fixed-point |r| and the scaled estimate base
-    constexpr bool kKeep = EPT <= 16;
+    constexpr bool kKeep = EPT <= 16 && T <= 256;
     unsigned long long Xk[kKeep ? EPT : 1];
     float Bk[kKeep ? EPT : 1];
     if constexpr (kKeep) {
@@ -92,7 +94,7 @@ __device__ __forceinline__ void bin_levels(const double (&r)[EPT], const HistSha
             Bk[u] = (float)fabs(r[u]) * gm;
         }
     }
-    constexpr int kChunk = EPT < 8 ? EPT : 8;
+    constexpr int kChunk = EPT < 4 ? EPT : 4;
     for (int kk = 0; kk < M; ++kk) {
         const double h = (double)kk + 0.5;
         const float rh = __builtin_amdgcn_rcpf((float)h);
@@ -106,7 +108,7 @@ __device__ __forceinline__ void bin_levels(const double (&r)[EPT], const HistSha
                 const double x = fabs(r[u]);
                 if constexpr (kLinear) {
                     const float base = kKeep ? Bk[kKeep ? u : 0] : (float)x * gm;
-                    nb[v] = count_linear(S.ad, G, h, x, base * rh);
+                    nb[v] = count_linear(S.af, G, h, x, base * rh);
                 } else {
                     nb[v] = count_bsearch(S.ad, G, h, x);
                 }
@@ -150,7 +152,9 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(const HistBatch B)
     S.bnd = S.e + G;
     S.ha = (long long *)(S.bnd + G);
     S.ad = (double *)(S.ha + G);
-    S.hb = (int *)(S.ad + G + 2);
+    S.af = (float *)(S.ad + G + 2);
+    S.c = S.af + G + 2;
+    S.hb = (int *)(S.c + G);
 
     const int64_t k = (int64_t)blockIdx.x - Ly.c_begin;
     const int t = threadIdx.x;
@@ -167,6 +171,9 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(const HistBatch B)
         const int j = t + T * u;
         r[u] = j < d ? (double)wk[j] : 0.0;
     }
+
+    for (int g = t; g < G; g += T)
+        S.c[g] = B.grid ? B.grid[g] : (float)((double)(g + 1) / (double)G);
 
     double Ew = 0.0;
     float apend = 0.0f;
@@ -188,8 +195,9 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(const HistBatch B)
             lmax = fmaxf(lmax, fabsf((float)r[u]));
             lsum = fma(r[u], r[u], lsum);
         }
-        const float m = block_reduce<T>(lmax, MaxOp(), s_redf);
-        const double Er = block_reduce<T>(lsum, SumOp(), s_redd);
+        block_max_sum<T>(lmax, lsum, s_redf, s_redd);   // also orders S.c before use
+        const float m = lmax;
+        const double Er = lsum;
 
         // ---- stop / point count
         if (i == 0) Ew = Er;
@@ -201,14 +209,17 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(const HistBatch B)
 
         // ---- candidates, cleared histograms
         for (int g = t; g < G; g += T) {
-            const float c = B.grid ? B.grid[g] : (float)((double)(g + 1) / (double)G);
-            S.ad[g + 1] = (double)(float)((double)m * (double)c / Md);
+            const float a = (float)((double)m * (double)S.c[g] / Md);
+            S.ad[g + 1] = (double)a;
+            S.af[g + 1] = a;
             S.ha[g] = 0;
             S.hb[g] = 0;
         }
         if (t == 0) {
             S.ad[0] = 0.0;
             S.ad[G + 1] = INFINITY;
+            S.af[0] = 0.0f;
+            S.af[G + 1] = INFINITY;
         }
         // fixed-point shift: every x < 2^(ex+1); sums of up to M*d values < 2^62
         int ex = 0;
@@ -359,12 +370,15 @@ hipError_t launch_hist_t(const HistBatch &b, int64_t channels, size_t lds, hipSt
 
 // (threads, elements per thread) of each variant, by channel length
 constexpr int kVariantMaxDim[] = {64, 128, 256, 512, 1024, 2048, 4096, 8192, (int)kHistMaxDim};
+// 512- and 1024-thread variants: no per-element cache, to stay within 128
+// VGPRs (1024 threads) or leave room for two workgroups per CU
 
 }  // namespace
 
 size_t fit_hist_lds(int G)
 {
-    return (size_t)G * (3 * sizeof(double) + sizeof(long long) + sizeof(int)) + 2 * sizeof(double);
+    return (size_t)G * (3 * sizeof(double) + sizeof(long long) + 2 * sizeof(float) + sizeof(int)) +
+           2 * sizeof(double) + 2 * sizeof(float);
 }
 
 bool fit_hist_supports(int64_t d) { return d >= 1 && d <= kHistMaxDim; }
@@ -386,9 +400,9 @@ hipError_t launch_fit_hist(const HistBatch &b, int variant, int64_t channels, hi
     case 3: return launch_hist_t<256, 2>(b, channels, lds, s);
     case 4: return launch_hist_t<256, 4>(b, channels, lds, s);
     case 5: return launch_hist_t<256, 8>(b, channels, lds, s);
-    case 6: return launch_hist_t<256, 16>(b, channels, lds, s);
+    case 6: return launch_hist_t<512, 8>(b, channels, lds, s);
+    case 7: return launch_hist_t<1024, 8>(b, channels, lds, s);
     // 512 threads leave 256 VGPRs per thread for the register-resident residual
-    case 7: return launch_hist_t<512, 16>(b, channels, lds, s);
     case 8: return launch_hist_t<512, 32>(b, channels, lds, s);
     default: return hipErrorInvalidValue;
     }

@@ -196,6 +196,37 @@ __device__ __forceinline__ T block_reduce(T v, Op op, T *scratch)
     return r;
 }
 
+// max of a float and sum of a double over the workgroup, with one pair of
+// barriers.  scratch_f / scratch_d hold one value per wavefront.
+template <int kThreads>
+__device__ __forceinline__ void block_max_sum(float &vmax, double &vsum, float *scratch_f,
+                                              double *scratch_d)
+{
+    constexpr int kWaves = kThreads / kWave;
+    vmax = half_wave_reduce(vmax, MaxOp());
+    vsum = half_wave_reduce(vsum, SumOp());
+    vmax = MaxOp()(readlane(vmax, 0), readlane(vmax, 32));
+    vsum = SumOp()(readlane(vsum, 0), readlane(vsum, 32));
+    if constexpr (kWaves > 1) {
+        const int wid = threadIdx.x / kWave;
+        if ((threadIdx.x % kWave) == 0) {
+            scratch_f[wid] = vmax;
+            scratch_d[wid] = vsum;
+        }
+        __syncthreads();
+        float m = scratch_f[0];
+        double sm = scratch_d[0];
+#pragma unroll
+        for (int i = 1; i < kWaves; ++i) {
+            m = MaxOp()(m, scratch_f[i]);
+            sm = SumOp()(sm, scratch_d[i]);
+        }
+        __syncthreads();
+        vmax = m;
+        vsum = sm;
+    }
+}
+
 template <int kThreads>
 __device__ __forceinline__ ArgMin block_argmin(ArgMin v, ArgMin *scratch)
 {
