@@ -43,11 +43,104 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--dense", action="store_true",
                     help="fit with mpq_fit_layer_dense (O(d G) search) instead of mpq_fit_layer")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="print the HBM-traffic summary of two rocprofv3 --pmc runs "
+                         "(FETCH_SIZE, WRITE_SIZE) of `bench.py --steps 1 --warmup 1 "
+                         "--copy-calibration` and exit")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="before the steps, copy a 256 MiB device buffer once (a kernel of known "
+                         "traffic, to scale the FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
+
+
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "resnet18_hbm_traffic.md")
+COPY_BYTES = 256 << 20
+KERNEL_KINDS = (("fit", ("fit_hist_kernel", "fit_dense_kernel")),
+                ("output_error", ("form_rows_kernel", "gemm_kernel", "finish_kernel")),
+                ("reconstruct", ("reconstruct_kernel",)))
+
+
+def sources_digest():
+    """sha256 of the HIP sources, to tell whether stored counters still apply."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2002_09049_amd", "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    return h.hexdigest()[:16]
+
+
+def summarize_pmc(fetch_dir, write_dir):
+    """HBM bytes per step and stage from the FETCH_SIZE / WRITE_SIZE counters,
+    each scaled so that the 256 MiB calibration copy reads / writes 256 MiB."""
+    import csv
+    import glob
+    import re
+
+    def per_kind(d):
+        rows = []
+        for f in glob.glob(os.path.join(d, "*counter_collection.csv")):
+            rows += list(csv.DictReader(open(f)))
+        cal = [r for r in rows if "copyBuffer" in r["Kernel_Name"] and int(r["Grid_Size"]) == 131072]
+        if not cal:
+            raise SystemExit(f"no calibration copy in {d}")
+        factor = COPY_BYTES / 1024.0 / float(cal[0]["Counter_Value"])
+        out = {k: 0.0 for k, _ in KERNEL_KINDS}
+        steps = 0
+        for r in rows:
+            m = re.search(r"(\w+_kernel)", r["Kernel_Name"])
+            name = m.group(1) if m else ""
+            for kind, names in KERNEL_KINDS:
+                if name in names:
+                    out[kind] += float(r["Counter_Value"]) * factor * 1024.0
+            if name == "finish_kernel":
+                steps += 1
+        return factor, out, steps
+
+    ff, fetch, steps = per_kind(fetch_dir)
+    wf, write, _ = per_kind(write_dir)
+    steps = max(steps, 1)
+    lines = ["# HBM traffic per step: ResNet-18-shaped workload", "",
+             "Two rocprofv3 counter runs (one counter each), from the repository root:", "",
+             "```",
+             "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_FETCH_SIZE -o p -- \\",
+             "    python3 bench.py --steps 1 --warmup 1 --no-cpu-baseline --copy-calibration",
+             "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_WRITE_SIZE -o p -- \\",
+             "    python3 bench.py --steps 1 --warmup 1 --no-cpu-baseline --copy-calibration",
+             "python3 bench.py --summarize-pmc gpurun_out/pmc_FETCH_SIZE gpurun_out/pmc_WRITE_SIZE",
+             "```", "",
+             f"Scale factors from a 256 MiB device copy: FETCH_SIZE x {ff:.4f}, WRITE_SIZE x {wf:.4f}.",
+             f"Bytes per step (the run holds {steps} steps).", "",
+             "| stage | fetch bytes | write bytes | total bytes |", "|---|---:|---:|---:|"]
+    for kind, _ in KERNEL_KINDS:
+        f_, w_ = fetch[kind] / steps, write[kind] / steps
+        lines.append(f"| {kind} | {f_:.0f} | {w_:.0f} | {f_ + w_:.0f} |")
+    lines += ["", f"sources: {sources_digest()}", ""]
+    print("\n".join(lines))
+
+
+def measured_traffic(kind):
+    """HBM bytes per step of a stage from the stored counter summary, or None
+    when the summary is missing or was taken on other kernel sources."""
+    try:
+        text = open(TRAFFIC_SUMMARY).read()
+    except OSError:
+        return None
+    if f"sources: {sources_digest()}" not in text:
+        return None
+    for ln in text.splitlines():
+        cells = [c.strip() for c in ln.strip("|").split("|")]
+        if len(cells) == 4 and cells[0] == kind:
+            return int(cells[3])
+    return None
 
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc)
+        return 0
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
               "(the fit has no cross-GPU step to measure)", file=sys.stderr, flush=True)
@@ -71,6 +164,12 @@ def main():
         Xs.append(torch.from_numpy(wl.layer_calib(wk, li)).to(dev))
     ls = mpq.LayerSet(Ws, wk.max_points, calib=Xs, with_fit_err=True)
     torch.cuda.synchronize()
+    if args.copy_calibration:
+        src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)            # reads and writes 256 MiB
+        torch.cuda.synchronize()
+        del src, dst
 
     def step(ev=None):
         if ev: ev[0].record(stream)
@@ -154,8 +253,11 @@ def main():
     }
     dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
     K = kernels[dom]
+    for k in kernels:
+        kernels[k]["hbm_bytes_per_step_measured"] = measured_traffic(k)
     roofline = {"kernel": dom, "bound": K["bound"], "achieved": round(K["achieved"], 4),
-                "peak": K["peak"], "unit": K["unit"], "frac": round(K["frac"], 5), "traffic": None}
+                "peak": K["peak"], "unit": K["unit"], "frac": round(K["frac"], 5),
+                "traffic": kernels[dom]["hbm_bytes_per_step_measured"]}
 
     value = points * steps / (ms_total * 1e-3)
     res = {
