@@ -18,6 +18,17 @@
 // are re-evaluated directly (fp64, like Eq. (9) written out) and the smallest
 // error wins, ties to the smallest g.
 //
+// Lattice mode (default grid, (2M-1) G + 1 buckets fit): with u = m / (2 G M)
+// every boundary (k + 1/2) a_g lies within relative 2^-23 of the lattice
+// point L = (2k+1)(g+1) times u.  An element whose x / u is farther than
+// delta = 2 G M 2^-22 from every integer crosses exactly the boundaries with
+// L <= floor(x / u), so it goes to that one bucket (fixed-point x and a count
+// packed in one 64-bit word); A(g) and B(g) are then sums over k of suffix
+// sums at L = (2k+1)(g+1).  An element within delta of an integer N goes to
+// bucket N - 1, and each boundary at L = N is decided exactly and, when
+// crossed, added to a per-candidate correction.  This replaces M atomics per
+// element with one and gives the same integer sums.
+//
 // One workgroup per channel.  The fp64 residual stays in registers for the
 // whole fit (EPT elements per thread, element j = t + T * u), so each step
 // reads nothing from HBM: it writes the codes of the point chosen by the
@@ -34,14 +45,21 @@ namespace {
 
 constexpr int kMaxFinalists = 8;
 
+// lattice buckets: fixed-point x in the low kLatShift bits, count above
+constexpr int kLatShift = 49;
+constexpr unsigned long long kLatOne = 1ull << kLatShift;
+constexpr unsigned long long kLatMask = kLatOne - 1;
+constexpr int kLatMaxBuckets = 4096;
+
 struct HistShared {
     double *ad;      // [G + 2]: ad[0] = 0, ad[g + 1] = a_g (an fp32 value), ad[G + 1] = +inf
     float *af;       // [G + 2]: the same values in fp32 (half the LDS bytes per read)
     float *c;        // [G]: grid multipliers c_g
-    long long *ha;   // [G] fixed-point sum of x per bin
-    int *hb;         // [G] sum of (2k + 1) per bin
+    long long *ha;   // [G] fixed-point sum of x per bin (lattice mode: per-candidate corrections)
+    int *hb;         // [G] sum of (2k + 1) per bin (lattice mode: corrections)
     double *e;       // [G] approximate candidate errors
     double *bnd;     // [G] their error bounds
+    unsigned long long *lat;   // [nlat] lattice buckets (lattice mode only)
 };
 
 // n = #{ g : h * a_g < x } over the non-decreasing candidates, by binary
@@ -130,8 +148,97 @@ __device__ __forceinline__ void bin_levels(const double (&r)[EPT], const HistSha
     }
 }
 
-template <int T, int EPT, bool kLinear>
-__global__ void __launch_bounds__(T) fit_hist_kernel(const HistBatch B)
+// Lattice-mode binning of this thread's elements (see the header).  inv =
+// 1 / u in fp64; Lmax = nlat - 1 is the largest lattice point of a boundary;
+// scale = 2^sh.
+//
+// z = x / u + delta (one rounding, error far below delta) and F = floor(z):
+// z - F > 2 delta puts x / u more than delta from every integer, with floor
+// F; otherwise x / u is within delta of N = F.  The bucket word is formed by
+// one fma: x 2^sh + 2^52 + 2^kLatShift rounds x 2^sh to the nearest integer
+// (ties to even, as rint) and its low 52 bits are that integer plus the count
+// bit.
+template <int T, int EPT>
+__device__ __forceinline__ void bin_lattice(const double (&r)[EPT], const HistShared &S, int G, int M,
+                                            int d, int Lmax, double inv, double delta, double scale)
+{
+    constexpr double kBias = 0x1p52 + (double)kLatOne;
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+        if (T * u >= d) continue;   // a slot past the channel end in every thread
+        const double x = fabs(r[u]);
+        const double z = fma(x, inv, delta);
+        const double F = floor(z);
+        const bool near = z - F <= 2.0 * delta;
+        const int Ni = (int)F;
+        const int b = near ? Ni - 1 : Ni;
+        const unsigned long long word =
+            (unsigned long long)__double_as_longlong(fma(x, scale, kBias)) & ((1ull << 52) - 1);
+        if (b >= 1) atomicAdd(&S.lat[min(b, Lmax)], word);
+        if (near && Ni >= 1) {
+            // boundaries at lattice point N: (2k+1) divides N, g + 1 = N / (2k+1) <= G
+            const unsigned long long X = word - kLatOne;
+            for (int kk = 0; kk < M; ++kk) {
+                const int o = 2 * kk + 1;
+                const int q = Ni / o;
+                if (q < 1) break;
+                if (q * o != Ni || q > G) continue;
+                const int g = q - 1;
+                if (fma((double)kk + 0.5, S.ad[g + 1], -x) < 0.0) {
+                    atomicAdd((unsigned long long *)&S.ha[g], X);
+                    atomicAdd(&S.hb[g], o);
+                }
+            }
+        }
+    }
+}
+
+// In-place inclusive suffix sums of h[0, n) by the whole workgroup: thread t
+// owns the t-th chunk from the top, so a prefix over threads is a suffix over
+// buckets.  An odd chunk length keeps the lanes of a wavefront on distinct
+// LDS banks.  scan holds one value per wavefront.  Ends with a barrier.
+template <int T>
+__device__ __forceinline__ void block_suffix_sums(unsigned long long *h, int n,
+                                                  unsigned long long *scan)
+{
+    constexpr int kWaves = T / kWave;
+    constexpr int kPerMax = ((kLatMaxBuckets + T - 1) / T) | 1;
+    const int t = threadIdx.x;
+    const int per = ((n + T - 1) / T) | 1;  // n <= kLatMaxBuckets
+    const int top = n - t * per;            // exclusive upper end of the chunk
+    const int bot = max(top - per, 0);
+    unsigned long long v = 0;
+#pragma unroll 4
+    for (int z = 0; z < kPerMax; ++z) {
+        const int i = top - 1 - z;
+        v += i >= bot ? h[max(i, 0)] : 0ull;
+    }
+    const unsigned long long incl = wave_prefix_sum(v);
+    const int wid = t / kWave;
+    if ((t % kWave) == kWave - 1) scan[wid] = incl;
+    __syncthreads();
+    unsigned long long run = incl - v;
+#pragma unroll
+    for (int w = 0; w < kWaves - 1; ++w) run += w < wid ? scan[w] : 0ull;
+#pragma unroll 4
+    for (int z = 0; z < kPerMax; ++z) {
+        const int i = top - 1 - z;
+        if (i >= bot) {
+            run += h[i];
+            h[i] = run;
+        }
+    }
+    __syncthreads();
+}
+
+// at most 128 VGPRs (four wavefronts per SIMD) unless the residual alone
+// needs more
+template <int EPT>
+constexpr int hist_waves_per_simd() { return EPT >= 32 ? 2 : 4; }
+
+template <int T, int EPT, bool kLinear, bool kLat>
+__global__ void __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(hist_waves_per_simd<EPT>())))
+fit_hist_kernel(const HistBatch B)
 {
     constexpr int kWaves = T / kWave;
     extern __shared__ __align__(16) double hsmem[];
@@ -140,6 +247,8 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(const HistBatch B)
     __shared__ int s_fin[kMaxFinalists];
     __shared__ int s_nfin;
     __shared__ int s_gbest;
+    __shared__ unsigned long long s_scan[kWaves];
+    __shared__ ArgMin s_arg[kWaves];
 
     // layer of this workgroup (uniform: the descriptors are kernel arguments)
     int li = 0;
@@ -152,7 +261,9 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(const HistBatch B)
     S.bnd = S.e + G;
     S.ha = (long long *)(S.bnd + G);
     S.ad = (double *)(S.ha + G);
-    S.af = (float *)(S.ad + G + 2);
+    S.lat = (unsigned long long *)(S.ad + G + 2);
+    const int nlat = kLat ? B.nlat : 0;
+    S.af = (float *)(S.lat + nlat);
     S.c = S.af + G + 2;
     S.hb = (int *)(S.c + G);
 
@@ -183,14 +294,22 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(const HistBatch B)
         float lmax = 0.0f;
         double lsum = 0.0;
         int8_t *qrow = qk + (int64_t)(i - 1) * d;
+        const double ap = (double)apend;
+        const double ia = 1.0 / ap;
 #pragma unroll
         for (int u = 0; u < EPT; ++u) {
             const int j = t + T * u;
             if (i >= 1 && j < d) {
-                double c = rint(r[u] / (double)apend);
+                // y is within |y| 2^-51 of the fp64 quotient fl(r / a), so the
+                // two round to the same integer unless y lies within 2^-40 of a
+                // half-integer (or |y| >= 2^10, where both clip to the same M);
+                // only then is the quotient formed
+                const double y = r[u] * ia;
+                double c = rint(y);
+                if (fabs(fabs(y - c) - 0.5) < 0x1p-40) c = rint(r[u] / ap);
                 c = fmin(fmax(c, -Md), Md);
                 qrow[j] = (int8_t)(int)c;
-                r[u] = fma(-(double)apend, c, r[u]);
+                r[u] = fma(-ap, c, r[u]);
             }
             lmax = fmaxf(lmax, fabsf((float)r[u]));
             lsum = fma(r[u], r[u], lsum);
@@ -215,47 +334,100 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(const HistBatch B)
             S.ha[g] = 0;
             S.hb[g] = 0;
         }
+        // lattice mode needs normal candidates (relative error 2^-23)
+        const bool lat = kLat && m >= 0x1p-100f;
+        if (lat)
+            for (int b = t; b < nlat; b += T) S.lat[b] = 0;
         if (t == 0) {
             S.ad[0] = 0.0;
             S.ad[G + 1] = INFINITY;
             S.af[0] = 0.0f;
             S.af[G + 1] = INFINITY;
         }
-        // fixed-point shift: every x < 2^(ex+1); sums of up to M*d values < 2^62
+        // fixed-point shift: every x < 2^(ex+1); sums of up to M*d values
+        // < 2^62, or in lattice mode sums of d values < 2^kLatShift
         int ex = 0;
         (void)frexpf(m, &ex);
-        int lg = 0;
-        while ((1LL << lg) < (long long)M * d) ++lg;
-        const int sh = 61 - (ex + 1) - lg;
+        const long long span = lat ? (long long)d : (long long)M * d;   // >= 1
+        const int lg = span <= 1 ? 0 : 64 - __clzll(span - 1);          // ceil(log2(span))
+        const int sh = (lat ? kLatShift : 61) - (ex + 1) - lg;
         __syncthreads();
 
-        // ---- histograms of the level boundaries (bin_levels)
-        unsigned long long fullA = 0;
-        int fullB = 0;
-        // the closed-form counts need normal candidates and a finite estimate
-        if (kLinear && m >= 0x1p-100f)
-            bin_levels<T, EPT, true>(r, S, G, M, m, sh, fullA, fullB);
-        else
-            bin_levels<T, EPT, false>(r, S, G, M, m, sh, fullA, fullB);
-#pragma unroll
-        for (int off = 1; off < kWave; off <<= 1) {
-            fullA += (unsigned long long)__shfl_xor((long long)fullA, off);
-            fullB += __shfl_xor(fullB, off);
-        }
-        if ((t % kWave) == 0) {
-            atomicAdd((unsigned long long *)&S.ha[G - 1], fullA);
-            atomicAdd(&S.hb[G - 1], fullB);
-        }
-        __syncthreads();
-
-        // ---- wavefront 0: suffix sums, candidate errors and bounds, argmin
         const double q2 = ldexp(1.0, -sh);
         const double slack = Md * (double)d * q2;   // fixed-point error of A, per unit a
+        ArgMin best{INFINITY, 0x7fffffff};
+        if (lat) {
+            // ---- lattice buckets, their suffix sums, then every candidate
+            const double inv = (double)(2 * G * M) / (double)m;
+            const double delta = (double)(2 * G * M) * 0x1p-22;
+            bin_lattice<T, EPT>(r, S, G, M, d, nlat - 1, inv, delta, ldexp(1.0, sh));
+            __syncthreads();
+            block_suffix_sums<T>(S.lat, nlat, s_scan);
+            for (int g = t; g < G; g += T) {
+                unsigned long long A = (unsigned long long)S.ha[g];
+                uint32_t Bc = (uint32_t)S.hb[g];
+                for (int k0 = 0; k0 < M; k0 += 8) {
+                    // eight independent reads in flight; lanes past M read
+                    // bucket 0 and drop it
+                    unsigned long long v[8];
+#pragma unroll
+                    for (int z = 0; z < 8; ++z) {
+                        const int kk = k0 + z;
+                        v[z] = S.lat[kk < M ? (2 * kk + 1) * (g + 1) : 0];
+                    }
+#pragma unroll
+                    for (int z = 0; z < 8; ++z) {
+                        const int kk = k0 + z;
+                        if (kk < M) {
+                            A += v[z] & kLatMask;
+                            Bc += (uint32_t)(2 * kk + 1) * (uint32_t)(v[z] >> kLatShift);
+                        }
+                    }
+                }
+                const double a = S.ad[g + 1];
+                double e = INFINITY, b = 0.0;
+                if (a != 0.0) {
+                    const double Ad = ldexp((double)A, -sh);
+                    const double t2 = 2.0 * a * Ad, t3 = a * a * (double)Bc;
+                    e = (Er - t2) + t3;
+                    b = a * slack + 8.0 * 0x1p-53 * (Er + t2 + t3);
+                }
+                S.e[g] = e;
+                S.bnd[g] = b;
+                if (e < best.e || (e == best.e && g < best.g)) best = ArgMin{e, g};
+            }
+            best = block_argmin<T>(best, s_arg);   // its barriers publish S.e, S.bnd
+        } else {
+            // ---- histograms of the level boundaries (bin_levels)
+            unsigned long long fullA = 0;
+            int fullB = 0;
+            // the closed-form counts need normal candidates and a finite
+            // estimate (in a lattice-mode kernel this branch only runs when
+            // they do not)
+            if (kLinear && !kLat && m >= 0x1p-100f)
+                bin_levels<T, EPT, true>(r, S, G, M, m, sh, fullA, fullB);
+            else
+                bin_levels<T, EPT, false>(r, S, G, M, m, sh, fullA, fullB);
+#pragma unroll
+            for (int off = 1; off < kWave; off <<= 1) {
+                fullA += (unsigned long long)__shfl_xor((long long)fullA, off);
+                fullB += __shfl_xor(fullB, off);
+            }
+            if ((t % kWave) == 0) {
+                atomicAdd((unsigned long long *)&S.ha[G - 1], fullA);
+                atomicAdd(&S.hb[G - 1], fullB);
+            }
+            __syncthreads();
+        }
+
+        // ---- wavefront 0: (histogram mode) suffix sums, candidate errors and
+        // bounds, argmin; then the finalists
         if (t < kWave) {
             // lane l owns the l-th chunk from the top, so a prefix over lanes
             // is a suffix over candidates
             const int per = (G + kWave - 1) / kWave;
             const int g0 = (kWave - 1 - t) * per, g1 = min(g0 + per, G);
+            if (!lat) {
             unsigned long long la = 0;
             uint32_t lb = 0;
             for (int g = g0; g < g1; ++g) {
@@ -264,7 +436,6 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(const HistBatch B)
             }
             long long A = (long long)(wave_prefix_sum(la) - la);   // exclusive
             int B = (int)(wave_prefix_sum(lb) - lb);
-            ArgMin best{INFINITY, 0x7fffffff};
             for (int g = g1 - 1; g >= g0; --g) {
                 A += S.ha[g];
                 B += S.hb[g];
@@ -281,6 +452,7 @@ __global__ void __launch_bounds__(T) fit_hist_kernel(const HistBatch B)
                 if (e < best.e || (e == best.e && g < best.g)) best = ArgMin{e, g};
             }
             best = wave_argmin(best);
+            }
             // finalists: candidates whose interval reaches the best one's
             const double thr = best.e == INFINITY ? INFINITY : best.e + S.bnd[best.g];
             int cnt = 0;
@@ -358,7 +530,10 @@ template <int T, int EPT>
 hipError_t launch_hist_t(const HistBatch &b, int64_t channels, size_t lds, hipStream_t s)
 {
     // the default grid (grid == nullptr) has the closed-form boundary counts
-    auto kern = b.grid ? fit_hist_kernel<T, EPT, false> : fit_hist_kernel<T, EPT, true>;
+    // and, when its buckets fit, the lattice mode
+    auto kern = b.grid ? fit_hist_kernel<T, EPT, false, false>
+                : b.nlat ? fit_hist_kernel<T, EPT, true, true>
+                         : fit_hist_kernel<T, EPT, true, false>;
     if (lds > 65536) {
         hipError_t e = hipFuncSetAttribute((const void *)kern,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -368,10 +543,22 @@ hipError_t launch_hist_t(const HistBatch &b, int64_t channels, size_t lds, hipSt
     return hipGetLastError();
 }
 
-// (threads, elements per thread) of each variant, by channel length
-constexpr int kVariantMaxDim[] = {64, 128, 256, 512, 1024, 2048, 4096, 8192, (int)kHistMaxDim};
-// 512- and 1024-thread variants: no per-element cache, to stay within 128
-// VGPRs (1024 threads) or leave room for two workgroups per CU
+// (threads, elements per thread) of each variant; variant v takes the
+// channels longer than the capacity T * EPT of variant v - 1, up to its own.
+// 256-thread variants let four channels share a CU (128 VGPRs, under 40 KB of
+// LDS each), so one channel's barriers and serial phases overlap another's
+// arithmetic; the 512- and 1024-thread variants cover lengths whose residual
+// would not fit 128 VGPRs at 256 threads.
+struct Variant {
+    int threads, ept;
+};
+constexpr Variant kVariants[] = {{64, 1},  {64, 2},   {64, 4},   {256, 2},   {256, 4},
+                                 {256, 8}, {512, 8},  {256, 18}, {1024, 8},  {512, 32}};
+constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
+static_assert(kVariants[kNumVariants - 1].threads * kVariants[kNumVariants - 1].ept == kHistMaxDim,
+              "the last variant covers the longest channels");
+// variants whose capacity reaches this length use the lattice mode
+constexpr int kLatMinDim = 2048;
 
 }  // namespace
 
@@ -386,13 +573,23 @@ bool fit_hist_supports(int64_t d) { return d >= 1 && d <= kHistMaxDim; }
 int hist_variant(int64_t d)
 {
     int v = 0;
-    while (d > kVariantMaxDim[v]) ++v;
+    while (v + 1 < kNumVariants && d > (int64_t)kVariants[v].threads * kVariants[v].ept) ++v;
     return v;
 }
 
-hipError_t launch_fit_hist(const HistBatch &b, int variant, int64_t channels, hipStream_t s)
+hipError_t launch_fit_hist(const HistBatch &batch, int variant, int64_t channels, hipStream_t s)
 {
-    const size_t lds = fit_hist_lds(b.G);
+    HistBatch b = batch;
+    // lattice mode: default grid, longer channels (the bucket pass costs
+    // O(nlat) per step), buckets within kLatMaxBuckets and 64 KiB of LDS
+    const int64_t nlat = (int64_t)(2 * b.M - 1) * b.G + 1;
+    if (variant < 0 || variant >= kNumVariants) return hipErrorInvalidValue;
+    b.nlat = (!b.grid && kVariants[variant].threads * kVariants[variant].ept >= kLatMinDim &&
+              nlat <= kLatMaxBuckets &&
+              fit_hist_lds(b.G) + (size_t)nlat * sizeof(unsigned long long) <= 65536)
+                 ? (int)nlat
+                 : 0;
+    const size_t lds = fit_hist_lds(b.G) + (size_t)b.nlat * sizeof(unsigned long long);
     switch (variant) {
     case 0: return launch_hist_t<64, 1>(b, channels, lds, s);
     case 1: return launch_hist_t<64, 2>(b, channels, lds, s);
@@ -401,9 +598,10 @@ hipError_t launch_fit_hist(const HistBatch &b, int variant, int64_t channels, hi
     case 4: return launch_hist_t<256, 4>(b, channels, lds, s);
     case 5: return launch_hist_t<256, 8>(b, channels, lds, s);
     case 6: return launch_hist_t<512, 8>(b, channels, lds, s);
-    case 7: return launch_hist_t<1024, 8>(b, channels, lds, s);
+    case 7: return launch_hist_t<256, 18>(b, channels, lds, s);
+    case 8: return launch_hist_t<1024, 8>(b, channels, lds, s);
     // 512 threads leave 256 VGPRs per thread for the register-resident residual
-    case 8: return launch_hist_t<512, 32>(b, channels, lds, s);
+    case 9: return launch_hist_t<512, 32>(b, channels, lds, s);
     default: return hipErrorInvalidValue;
     }
 }

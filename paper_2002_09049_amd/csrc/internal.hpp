@@ -61,6 +61,7 @@ struct HistBatch {
     int M, P, G;
     const float *grid;  // device multipliers or nullptr (default grid)
     double tol;
+    int nlat;           // lattice buckets ((2M-1) G + 1) or 0; set by launch_fit_hist
     HistLayer L[kMaxBatchLayers];
 };
 
