@@ -123,6 +123,7 @@ __device__ __forceinline__ void bin_levels(const double (&r)[EPT], const HistSha
 #pragma unroll
             for (int v = 0; v < kChunk; ++v) {
                 const int u = u0 + v;
+                if (u >= EPT) break;   // last chunk of an EPT that kChunk does not divide
                 const double x = fabs(r[u]);
                 if constexpr (kLinear) {
                     const float base = kKeep ? Bk[kKeep ? u : 0] : (float)x * gm;
@@ -134,6 +135,7 @@ __device__ __forceinline__ void bin_levels(const double (&r)[EPT], const HistSha
 #pragma unroll
             for (int v = 0; v < kChunk; ++v) {
                 const int u = u0 + v;
+                if (u >= EPT) break;
                 const unsigned long long X =
                     kKeep ? Xk[kKeep ? u : 0] : (unsigned long long)rint(ldexp(fabs(r[u]), sh));
                 const bool full = nb[v] == G;

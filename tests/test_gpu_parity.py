@@ -139,6 +139,48 @@ def test_search_kernel_boundaries(orc, d):
     assert_parity(orc, W, 3, 4, 512, 5e-4, out)
 
 
+def _lattice_rows(d, rng):
+    """Channels for the lattice mode of the histogram search (default grid):
+    random; elements exactly on level boundaries of 4-bit, G = 256 (max 1,
+    a_g = j / 256 for g + 1 = 7 j, boundaries (2k+1) j / 512, all exact in
+    fp32); a scale below 2^-100 (per-level fallback); a few outliers over many
+    tiny values; equal magnitudes."""
+    W = np.zeros((5, d), np.float32)
+    W[0] = rng.standard_normal(d)
+    k = rng.integers(0, 7, d)
+    j = rng.integers(1, 37, d)
+    W[1] = (2 * k + 1) * j / 512.0 * np.sign(rng.standard_normal(d))
+    W[1, 0] = 1.0
+    W[2] = rng.standard_normal(d) * 1e-33
+    W[3] = rng.standard_normal(d) * 1e-3
+    W[3, rng.integers(0, d, 4)] = [50.0, -80.0, 20.0, 1.0]
+    W[4] = 0.7 * np.sign(rng.standard_normal(d))
+    return W
+
+
+@pytest.mark.parametrize("d", [1025, 2049, 4097, 4608, 4609])
+def test_lattice_mode_channels(orc, d):
+    """Lattice-bucket mode of the histogram search (default grid, channels
+    longer than 1024): lockstep parity, including elements that sit exactly on
+    a boundary (exact per-boundary corrections) and a channel below the
+    mode's range; and agreement with the per-level histogram, reached by
+    passing the default grid explicitly."""
+    rng = np.random.default_rng(d)
+    W = _lattice_rows(d, rng)
+    for bits, G, P, tol in ((4, 256, 4, 1e-3), (4, 256, 8, 0.0), (3, 512, 5, 1e-4),
+                            (2, 1000, 6, 0.0), (5, 128, 3, 1e-3)):
+        say(f"case lattice d={d} bits={bits} G={G} P={P} tol={tol}")
+        out = gpu_fit(W, bits, P, G, tol)
+        v = assert_parity(orc, W, bits, P, G, tol, out)
+        grid = (np.arange(1, G + 1, dtype=np.float64) / G).astype(np.float32)
+        ref = gpu_fit(W, bits, P, G, tol, grid=grid)
+        assert_parity(orc, W, bits, P, G, tol, ref, grid=grid)
+        diff = ((out[2] != ref[2]) | (out[1] != ref[1]).any(axis=1)
+                | (out[0] != ref[0]).any(axis=(1, 2)))
+        tie = (v["cand_ties"] + v["code_ties"] + v["stop_ties"]) > 0
+        assert not (diff & ~tie).any(), f"channels {np.nonzero(diff & ~tie)[0]} differ without a tie"
+
+
 def test_exact_ties_between_candidates(orc):
     """Channels built so that several candidate scales give exactly the same
     error (dyadic values): the smallest scale must win, in both searches."""
