@@ -6,6 +6,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -130,6 +131,85 @@ hipError_t scratch_free(void *p, hipStream_t s) { return hipFreeAsync(p, s); }
 
 }  // namespace mpq
 
+namespace {
+
+// Library-owned streams (default priority) on which the independent launches
+// of one call run side by side: forked from the caller's stream by an event
+// and joined back to it by one event per stream, so the call stays ordered on
+// the caller's stream.  One set per device; its mutex serializes the enqueue
+// of concurrent callers.  Each call re-records the events; a wait that is
+// already enqueued keeps the record it saw.
+constexpr int kForkStreams = 3;   // besides the caller's stream
+
+struct ForkPool {
+    std::mutex mu;
+    bool ready = false;
+    hipStream_t st[kForkStreams];
+    hipEvent_t fork;
+    hipEvent_t join[kForkStreams];
+};
+ForkPool g_fork[kMaxDevices];
+
+// Creates the pool's streams and events on first use (mu held).
+hipError_t fork_pool_init(ForkPool &F)
+{
+    if (F.ready) return hipSuccess;
+    hipError_t e = hipEventCreateWithFlags(&F.fork, hipEventDisableTiming);
+    for (int i = 0; i < kForkStreams && e == hipSuccess; ++i) {
+        e = hipStreamCreateWithFlags(&F.st[i], hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&F.join[i], hipEventDisableTiming);
+    }
+    F.ready = e == hipSuccess;
+    return e;
+}
+
+// Runs launch(j, stream) for the jobs 0..n-1, longest work first, each on the
+// least loaded of the caller's stream and up to kForkStreams pool streams.
+// Falls back to the caller's stream alone when the pool cannot be created.
+template <class Launch>
+hipError_t run_concurrently(hipStream_t s, const std::vector<double> &work, Launch launch)
+{
+    const int n = (int)work.size();
+    std::vector<int> order(n);
+    for (int j = 0; j < n; ++j) order[j] = j;
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return work[a] > work[b]; });
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    ForkPool *F = (n > 1 && dev >= 0 && dev < kMaxDevices) ? &g_fork[dev] : nullptr;
+    std::unique_lock<std::mutex> lk;
+    if (F) {
+        lk = std::unique_lock<std::mutex>(F->mu);
+        if (fork_pool_init(*F) != hipSuccess) F = nullptr;
+    }
+    if (!F) {
+        for (int j = 0; j < n && e == hipSuccess; ++j) e = launch(order[j], s);
+        return e;
+    }
+    const int lanes = std::min(n, kForkStreams + 1);
+    e = hipEventRecord(F->fork, s);
+    for (int i = 1; i < lanes && e == hipSuccess; ++i) e = hipStreamWaitEvent(F->st[i - 1], F->fork, 0);
+    if (e != hipSuccess) return e;
+    std::vector<double> load(lanes, 0.0);
+    for (int jj = 0; jj < n && e == hipSuccess; ++jj) {
+        const int j = order[jj];
+        int best = 0;
+        for (int i = 1; i < lanes; ++i)
+            if (load[i] < load[best]) best = i;
+        load[best] += work[j];
+        e = launch(j, best == 0 ? s : F->st[best - 1]);
+    }
+    // join every lane even after a failed launch
+    for (int i = 1; i < lanes; ++i) {
+        hipError_t e2 = hipEventRecord(F->join[i - 1], F->st[i - 1]);
+        if (e2 == hipSuccess) e2 = hipStreamWaitEvent(s, F->join[i - 1], 0);
+        if (e == hipSuccess) e = e2;
+    }
+    return e;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char *mpq_last_error(void) { return g_last_error.c_str(); }
@@ -193,13 +273,24 @@ int fit_layers_impl(Search mode, const mpq_layer *layers, int n_layers, int bits
         }
     }
     const int M = (1 << (bits - 1)) - 1;
-    hipError_t e = hipSuccess;
-    // dense-search layers: one launch each
-    for (int l = 0; l < n_layers && e == hipSuccess; ++l) {
+    // independent launches: one per dense-search layer, one per histogram
+    // kernel variant (and per kMaxBatchLayers layers); they run side by side
+    struct Job {
+        bool dense;
+        int variant;
+        int64_t channels;
+        mpq::FitParams p;
+        mpq::HistBatch b;
+    };
+    std::vector<Job> jobs;
+    std::vector<double> work;   // ~ sum of c_out * d
+    for (int l = 0; l < n_layers; ++l) {
         const mpq_layer &L = layers[l];
         if (L.c_out == 0) continue;
         if (mode == Search::kAuto && hist_fits && mpq::fit_hist_supports(L.d)) continue;
-        mpq::FitParams p;
+        Job j = {};
+        j.dense = true;
+        mpq::FitParams &p = j.p;
         p.W = L.W;
         p.C = L.c_out;
         p.d = L.d;
@@ -212,27 +303,30 @@ int fit_layers_impl(Search mode, const mpq_layer *layers, int n_layers, int bits
         p.scales = L.scales;
         p.counts = L.counts;
         p.err = L.fit_err;
-        e = mpq::launch_fit(p, mpq::fit_layout(L.d, n_grid), s);
+        jobs.push_back(j);
+        // the dense search evaluates every candidate: weigh it by G
+        work.push_back((double)L.c_out * (double)L.d * (double)n_grid);
     }
-    // histogram-search layers: one launch per kernel variant (and per
-    // kMaxBatchLayers layers)
     if (mode == Search::kAuto && hist_fits) {
-        for (int v = 0; v <= mpq::hist_variant(mpq::kHistMaxDim) && e == hipSuccess; ++v) {
-            mpq::HistBatch b;
+        for (int v = 0; v <= mpq::hist_variant(mpq::kHistMaxDim); ++v) {
+            Job j = {};
+            j.variant = v;
+            mpq::HistBatch &b = j.b;
             b.M = M;
             b.P = max_points;
             b.G = n_grid;
             b.grid = dgrid;
             b.tol = (double)tol;
-            b.n_layers = 0;
-            int64_t channels = 0;
-            for (int l = 0; l <= n_layers && e == hipSuccess; ++l) {
+            double w = 0.0;
+            for (int l = 0; l <= n_layers; ++l) {
                 const bool flush = l == n_layers || b.n_layers == mpq::kMaxBatchLayers ||
-                                   channels + (l < n_layers ? layers[l].c_out : 0) > 0x7fffffffLL;
+                                   j.channels + (l < n_layers ? layers[l].c_out : 0) > 0x7fffffffLL;
                 if (flush && b.n_layers > 0) {
-                    e = mpq::launch_fit_hist(b, v, channels, s);
+                    jobs.push_back(j);
+                    work.push_back(w);
                     b.n_layers = 0;
-                    channels = 0;
+                    j.channels = 0;
+                    w = 0.0;
                 }
                 if (l == n_layers) break;
                 const mpq_layer &L = layers[l];
@@ -244,11 +338,17 @@ int fit_layers_impl(Search mode, const mpq_layer *layers, int n_layers, int bits
                 H.counts = L.counts;
                 H.err = L.fit_err;
                 H.d = (int)L.d;
-                H.c_begin = (int)channels;
-                channels += L.c_out;
+                H.c_begin = (int)j.channels;
+                j.channels += L.c_out;
+                w += (double)L.c_out * (double)L.d;
             }
         }
     }
+    const hipError_t e = run_concurrently(s, work, [&](int i, hipStream_t st) {
+        const Job &j = jobs[i];
+        return j.dense ? mpq::launch_fit(j.p, mpq::fit_layout(j.p.d, n_grid), st)
+                       : mpq::launch_fit_hist(j.b, j.variant, j.channels, st);
+    });
     if (dgrid) (void)mpq::scratch_free(dgrid, s);
     if (e != hipSuccess) return hip_fail(e, "fit kernel launch");
     return MPQ_OK;

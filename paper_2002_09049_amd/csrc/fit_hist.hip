@@ -549,13 +549,13 @@ hipError_t launch_hist_t(const HistBatch &b, int64_t channels, size_t lds, hipSt
 // channels longer than the capacity T * EPT of variant v - 1, up to its own.
 // 256-thread variants let four channels share a CU (128 VGPRs, under 40 KB of
 // LDS each), so one channel's barriers and serial phases overlap another's
-// arithmetic; the 512- and 1024-thread variants cover lengths whose residual
+// arithmetic; the 1024- and 512-thread variants cover lengths whose residual
 // would not fit 128 VGPRs at 256 threads.
 struct Variant {
     int threads, ept;
 };
-constexpr Variant kVariants[] = {{64, 1},  {64, 2},   {64, 4},   {256, 2},   {256, 4},
-                                 {256, 8}, {512, 8},  {256, 18}, {1024, 8},  {512, 32}};
+constexpr Variant kVariants[] = {{64, 1},  {64, 2},   {64, 4},    {256, 2},  {256, 4},
+                                 {256, 8}, {256, 18}, {1024, 8}, {512, 32}};
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 static_assert(kVariants[kNumVariants - 1].threads * kVariants[kNumVariants - 1].ept == kHistMaxDim,
               "the last variant covers the longest channels");
@@ -599,11 +599,10 @@ hipError_t launch_fit_hist(const HistBatch &batch, int variant, int64_t channels
     case 3: return launch_hist_t<256, 2>(b, channels, lds, s);
     case 4: return launch_hist_t<256, 4>(b, channels, lds, s);
     case 5: return launch_hist_t<256, 8>(b, channels, lds, s);
-    case 6: return launch_hist_t<512, 8>(b, channels, lds, s);
-    case 7: return launch_hist_t<256, 18>(b, channels, lds, s);
-    case 8: return launch_hist_t<1024, 8>(b, channels, lds, s);
+    case 6: return launch_hist_t<256, 18>(b, channels, lds, s);
+    case 7: return launch_hist_t<1024, 8>(b, channels, lds, s);
     // 512 threads leave 256 VGPRs per thread for the register-resident residual
-    case 9: return launch_hist_t<512, 32>(b, channels, lds, s);
+    case 8: return launch_hist_t<512, 32>(b, channels, lds, s);
     default: return hipErrorInvalidValue;
     }
 }
