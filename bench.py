@@ -47,6 +47,9 @@ def parse():
                     help="print the HBM-traffic summary of two rocprofv3 --pmc runs "
                          "(FETCH_SIZE, WRITE_SIZE) of `bench.py --steps 1 --warmup 1 "
                          "--copy-calibration` and exit")
+    ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
+                    help="print the per-kernel summary of a rocprofv3 --kernel-trace --stats run "
+                         "of `bench.py --steps 5 --warmup 1 --no-cpu-baseline` and exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before the steps, copy a 256 MiB device buffer once (a kernel of known "
                          "traffic, to scale the FETCH_SIZE / WRITE_SIZE counters)")
@@ -120,6 +123,50 @@ def summarize_pmc(fetch_dir, write_dir):
     print("\n".join(lines))
 
 
+def summarize_trace(trace_dir):
+    """Per-kernel and per-stage time of a traced bench run, from the
+    kernel_stats.csv that rocprofv3 --stats writes."""
+    import csv
+    import glob
+    import re
+
+    files = glob.glob(os.path.join(trace_dir, "*kernel_stats.csv"))
+    if not files:
+        raise SystemExit(f"no kernel_stats.csv in {trace_dir}")
+    rows = list(csv.DictReader(open(files[0])))
+    calls = max(int(r["Calls"]) for r in rows if "fit_" in r["Name"])
+    lines = ["# rocprofv3 kernel summary: ResNet-18-shaped workload, one bench step", "",
+             "Workload: 21 layers (5,800 channels, 11,678,912 weights), 4 bits, up to 4 points,",
+             "256 candidate scales, tol 1e-3, calibration batches d x 1024.  One step = fit +",
+             "output error + reconstruction of every layer through the batched C ABI calls.", "",
+             "Command (one MI355X, from the repository root):", "", "```",
+             "rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof -o kt -- \\",
+             "    python3 bench.py --steps 5 --warmup 1 --no-cpu-baseline",
+             "python3 bench.py --summarize-trace gpurun_out/prof", "```", "",
+             f"The traced process ran {calls} steps (warm-up + timed); `calls` counts all of them.",
+             "Kernels of one stage may run concurrently on several streams, so a stage's",
+             "kernel-time sum can exceed its wall time.", "",
+             "| kernel | calls | total ms | avg us | % |", "|---|---:|---:|---:|---:|"]
+    stage = {k: 0.0 for k, _ in KERNEL_KINDS}
+    stage["other"] = 0.0
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        name = r["Name"]
+        m = re.search(r"(\w+_kernel(<[^>]*>)?)", name)
+        short = m.group(1) if m else name[:40]
+        lines.append(f"| `{short}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.3f} | "
+                     f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+        kind = "other"
+        for k, names in KERNEL_KINDS:
+            if any(n in name for n in names):
+                kind = k
+        stage[kind] += float(r["TotalDurationNs"]) / 1e6
+    lines += ["", f"Kernel time per step (sum over the stage's kernels / {calls}):"]
+    for k, v in stage.items():
+        lines.append(f"- {k}: {v / calls:.3f} ms")
+    lines += ["", f"sources: {sources_digest()}", ""]
+    print("\n".join(lines))
+
+
 def measured_traffic(kind):
     """HBM bytes per step of a stage from the stored counter summary, or None
     when the summary is missing or was taken on other kernel sources."""
@@ -140,6 +187,9 @@ def main():
     args = parse()
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc)
+        return 0
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace)
         return 0
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
