@@ -59,7 +59,7 @@ def parse():
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "resnet18_hbm_traffic.md")
 COPY_BYTES = 256 << 20
 KERNEL_KINDS = (("fit", ("fit_hist_kernel", "fit_dense_kernel")),
-                ("output_error", ("form_rows_kernel", "gemm_kernel", "finish_kernel")),
+                ("output_error", ("form_dt_kernel", "gemm_err_kernel", "finish_err_kernel")),
                 ("reconstruct", ("reconstruct_kernel",)))
 
 
@@ -97,7 +97,7 @@ def summarize_pmc(fetch_dir, write_dir):
             for kind, names in KERNEL_KINDS:
                 if name in names:
                     out[kind] += float(r["Counter_Value"]) * factor * 1024.0
-            if name == "finish_kernel":
+            if name == "gemm_err_kernel":
                 steps += 1
         return factor, out, steps
 

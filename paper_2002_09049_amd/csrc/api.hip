@@ -380,10 +380,16 @@ int check_error_layer(const mpq_layer &L, int max_points, bool need_x)
         if (L.n < 1) return fail(MPQ_ERR_INVALID_ARG, "n must be >= 1 (got %lld)", (long long)L.n);
         if (L.c_out > 0 && (!L.W || !L.codes || !L.scales || !L.counts || !L.X || !L.out_err))
             return fail(MPQ_ERR_INVALID_ARG, "W, codes, scales, counts, X and err must not be NULL");
-        if (L.c_out > 0x7fffffffLL || L.n > 0x7fffffffLL || L.d > 0x7fffffffLL - 16)
-            return fail(MPQ_ERR_INVALID_ARG, "c_out, d or n too large");
-    } else if (L.c_out > 0 && (!L.codes || !L.scales || !L.counts || !L.W_hat)) {
-        return fail(MPQ_ERR_INVALID_ARG, "codes, scales, counts and W_hat must not be NULL");
+        if (L.n > MPQ_MAX_ERR_DIM || L.c_out > MPQ_MAX_ERR_DIM)
+            return fail(MPQ_ERR_INVALID_ARG, "c_out and n must be <= %d (got %lld, %lld)",
+                        MPQ_MAX_ERR_DIM, (long long)L.c_out, (long long)L.n);
+        if (L.d > 0x7fffffffLL)
+            return fail(MPQ_ERR_INVALID_ARG, "d too large (%lld)", (long long)L.d);
+    } else {
+        if (L.c_out > 0 && (!L.codes || !L.scales || !L.counts || !L.W_hat))
+            return fail(MPQ_ERR_INVALID_ARG, "codes, scales, counts and W_hat must not be NULL");
+        if (L.c_out > 0x7fffffffLL || L.d > 0x7fffffffLL)
+            return fail(MPQ_ERR_INVALID_ARG, "c_out or d too large");
     }
     return MPQ_OK;
 }

@@ -2,26 +2,39 @@
 // Eq. (12)): err[k] = (1/n) sum_t ((w_k - w~_k) . x_t)^2 and optionally
 // ref[k] = (1/n) sum_t (w_k . x_t)^2.
 //
-// Up to kMaxErrLayers layers go through three launches together (their
-// descriptors travel by value in the kernel arguments):
-//  1. form: A[k][j] = fl32(w_kj - sum_i a_i q_ij) (fp64 sum in point order)
-//     into a scratch matrix whose rows are padded to a multiple of 16 with
-//     zeros (aligned float4 rows, no K tail).  HBM-bound, coalesced.  A ref
-//     output is one more item of the group with A = W.
-//  2. gemm: Y = A X on MFMA (v_mfma_f32_32x32x2f32, fp32 in and accumulate),
-//     the path's one dense contraction.  A workgroup of four wavefronts owns a
-//     128 x 128 tile of Y and one K range; each wavefront owns 64 x 64 as
-//     2 x 2 MFMA blocks.  The K loop stages 16-deep slabs of A and X through
-//     double-buffered LDS, loading the next slab into registers while the
-//     MFMAs consume the current one.  The tiles of all layers form one grid,
-//     longest first; a layer's K is split when it has too few tiles.
-//       splits == 1: the epilogue squares Y and sums each row over the tile's
-//         columns (fp64 cross-lane sums with DPP / ds_swizzle) -> one partial
-//         per (column tile, row).
-//       splits  > 1: the epilogue stores the fp32 Y tile of its K range.
-//  3. finish: one workgroup per row: sum the row partials in tile order, or
-//     sum the K-range tiles of every column, square, and sum over the columns
-//     (fp64), in a fixed order.  Divide by n.
+// Up to kMaxErrLayers layers (items: an err item per layer, a ref item per
+// layer that asks for ref) go through three launches together, their
+// descriptors by value in the kernel arguments:
+//
+//  1. form (HBM-bound): D[k][j] = fl32(w_kj - sum_{i<n_k} a_i q_ij), the fp64
+//     sum in point order (D = W for a ref item), written K-major as
+//     Dt[j][k] (row stride ldc = C rounded up to 4) through an LDS transpose.
+//
+//  2. gemm: Y = D X on MFMA (v_mfma_f32_32x32x2f32, fp32 in and accumulate),
+//     the path's one dense contraction.  Dt and X are both K-major, so the A
+//     and B slabs are the same kind of copy: kBK rows of 128 consecutive
+//     floats.  A workgroup of four wavefronts owns a 128 x 128 tile of Y and
+//     one K range; each wavefront owns 64 x 64 as 2 x 2 MFMA blocks.  The K
+//     loop stages slabs through double-buffered LDS, loading the next slab
+//     into registers (buffer loads: offsets past a range read as zeros) while
+//     the MFMAs consume the current one.  The epilogue squares Y (fp64) and
+//     sums each row over the tile's columns into a partial per (column tile,
+//     row); a layer whose K is split (to balance a grid of long and short
+//     K ranges) stores its fp32 Y tiles per K range instead.
+//
+//  3. finish: per row, the partials summed in column-tile order, or the K
+//     ranges of Y summed in range order, squared and summed over the columns;
+//     divided by n.  Every order is fixed, so results are deterministic.  The
+//     kernel boundary publishes the partials (no cross-workgroup handshake:
+//     agent-scope fences would write back and invalidate the L2 the GEMM
+//     relies on).
+//
+// The tiles of all layers form one grid, longest K range first.  Workgroups
+// are dealt to the 8 XCDs in turn, so within a layer the tiles are
+// renumbered to give each XCD a contiguous run (rows of D and columns of X
+// reused by neighbouring tiles stay in one L2).  Tile coordinates come from
+// uniform subtraction loops, not divisions, so they and the buffer resources
+// built from them stay in scalar registers.
 #include <algorithm>
 #include <vector>
 
@@ -34,11 +47,29 @@ namespace mpq {
 namespace {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBM = 128, kBN = 128, kBK = 16;
 constexpr int kThreads = 256;
-constexpr int kPad = 4;  // LDS row padding (floats)
-constexpr int kMaxErrLayers = 32;
+constexpr int kPad = 4;          // LDS row padding (floats); rows stay 16-byte aligned
+constexpr int kVec = kBK * kBM / kThreads / 4;   // float4 per thread and operand per slab
+constexpr int kRowThreads = kBM / (4 * kVec);    // threads per slab row
+constexpr int kMaxErrLayers = 24;
+constexpr int kXcds = 8;         // MI355X: workgroups are dealt to 8 XCDs in turn
+constexpr int kFT = 64;          // form tile: 64 rows x 64 k
+
+// Raw buffer resource (gfx9 descriptor word 3: 32-bit dwords, no swizzle).
+// Loads at offsets >= num_records return zeros; kOob is past every range.
+constexpr uint32_t kOob = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t num_records)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)num_records,
+                                             0x00020000);
+}
+__device__ __forceinline__ f32x4 load4(__amdgpu_buffer_rsrc_t r, uint32_t off)
+{
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
 
 struct ErrLayer {
     const float *W;
@@ -46,126 +77,193 @@ struct ErrLayer {
     const float *scales;
     const int32_t *counts;
     const float *X;
-    float *out;        // err or ref
-    float *A;          // scratch [C][lda]
-    void *part;        // scratch: double [ntn][C] (splits == 1) or float [splits][C][n]
-    int C, d, n, lda;
+    float *out;          // err or ref
+    float *Dt;           // [d][ldc]
+    double *rowpart;     // [ntn][C]
+    float *ypart;        // [splits][C][n] (splits > 1)
+    int C, d, n, ldc;
     int ntm, ntn, splits, kchunk;
-    int tile_begin;    // first gemm workgroup of this layer
-    int row_begin;     // first finish workgroup of this layer
-    int use_points;    // 1: A = residual (err), 0: A = W (ref)
+    int tiles;           // ntm * ntn * splits
+    int block_begin;     // first gemm workgroup (a multiple of kXcds)
+    int form_begin;      // first form workgroup
+    int form_kt;         // form tiles along k: ceil(d / kFT)
+    int fin_begin;       // first finish workgroup
+    int use_points;      // 1: D = residual (err), 0: D = W (ref)
+    int vecw;            // d % 4 == 0, W 16-byte and codes 4-byte aligned
 };
 
 struct ErrGroup {
     int n_layers;
     int P;
-    int vecx;          // every X row start is 16-byte aligned and n % 4 == 0
+    int vecx;            // n % 4 == 0 and every X 16-byte aligned
     ErrLayer L[kMaxErrLayers];
 };
+static_assert(sizeof(ErrGroup) <= 4096, "kernel arguments");
 
-__global__ void __launch_bounds__(256) form_rows_kernel(const ErrGroup g)
+__device__ __forceinline__ double int8_of(uint32_t w, int u)
 {
-    const ErrLayer &L = g.L[blockIdx.y];
-    const int64_t total = (int64_t)L.C * L.lda;
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
-         e += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t k = e / L.lda, j = e - k * L.lda;
-        float v = 0.0f;
-        if (j < L.d) {
-            double r = (double)L.W[k * L.d + j];
-            if (L.use_points) {
-                const int nk = min(max(L.counts[k], 0), g.P);  // clamp: counts is caller data
-                const int8_t *q = L.codes + k * (int64_t)g.P * L.d + j;
-                const float *a = L.scales + k * (int64_t)g.P;
-                for (int i = 0; i < nk; ++i) r = fma(-(double)a[i], (double)q[(int64_t)i * L.d], r);
+    return (double)(int)(int8_t)(uint8_t)(w >> (8 * u));
+}
+
+// ---- 1. form: Dt = (W - sum a q)^T, one 64 x 64 tile per workgroup
+__global__ void __launch_bounds__(256) form_dt_kernel(const ErrGroup g)
+{
+    __shared__ float T[kFT][kFT + 1];
+
+    int li = 0;
+    while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].form_begin) ++li;
+    const ErrLayer &L = g.L[li];
+    int kt = (int)blockIdx.x - L.form_begin, rt = 0;
+    while (kt >= L.form_kt) {
+        kt -= L.form_kt;
+        ++rt;
+    }
+    const int P = g.P;
+    const int64_t d = L.d, C = L.C;
+    const int64_t row0 = (int64_t)rt * kFT, k0 = (int64_t)kt * kFT;
+    const int t = threadIdx.x;
+
+    // load: four rows (rb + 16 i) of four consecutive k (kc) per thread
+    const int kc = (t % 16) * 4, rb = t / 16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t row = row0 + rb + 16 * i, k = k0 + kc;
+        double r[4] = {0.0, 0.0, 0.0, 0.0};
+        if (row < C) {
+            const int nk = L.use_points ? min(max(L.counts[row], 0), P) : 0;  // counts is caller data
+            const float *wr = L.W + row * d;
+            const int8_t *cr = L.codes + row * (int64_t)P * d;
+            const float *sr = L.scales + row * (int64_t)P;
+            if (L.vecw && k < d) {   // d % 4 == 0: four k wholly inside
+                const float4 w = *(const float4 *)(wr + k);
+                r[0] = w.x; r[1] = w.y; r[2] = w.z; r[3] = w.w;
+                for (int p = 0; p < nk; ++p) {
+                    const double a = (double)sr[p];
+                    const uint32_t q = *(const uint32_t *)(cr + (int64_t)p * d + k);
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) r[u] = fma(-a, int8_of(q, u), r[u]);
+                }
+            } else if (!L.vecw) {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    if (k + u < d) {
+                        double v = (double)wr[k + u];
+                        for (int p = 0; p < nk; ++p)
+                            v = fma(-(double)sr[p], (double)cr[(int64_t)p * d + k + u], v);
+                        r[u] = v;
+                    }
+                }
             }
-            v = (float)r;
         }
-        L.A[e] = v;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) T[kc + u][rb + 16 * i] = (float)r[u];
+    }
+    __syncthreads();
+    // store: four k rows (kb + 16 i) of four consecutive rows of D (mc)
+    const int mc = (t % 16) * 4, kb = t / 16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t k = k0 + kb + 16 * i, m = row0 + mc;
+        if (k < d && m < L.ldc) {   // ldc % 4 == 0: the four rows lie inside
+            const int kr = kb + 16 * i;
+            *(float4 *)(L.Dt + k * L.ldc + m) = make_float4(T[kr][mc], T[kr][mc + 1], T[kr][mc + 2], T[kr][mc + 3]);
+        }
     }
 }
 
+// ---- 2. gemm: Y = D X, squared and summed per row
 template <bool kVecX>
-__global__ void __launch_bounds__(kThreads) gemm_kernel(const ErrGroup g)
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3)))
+gemm_err_kernel(const ErrGroup g)
 {
     __shared__ __align__(16) float sA[2][kBK][kBM + kPad];
     __shared__ __align__(16) float sX[2][kBK][kBN + kPad];
     __shared__ double sRow[kBM];
 
     int li = 0;
-    while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].tile_begin) ++li;
+    while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].block_begin) ++li;
     const ErrLayer &L = g.L[li];
-    const int local = (int)blockIdx.x - L.tile_begin;
+    // XCD-contiguous renumbering of this layer's tiles (block_begin is a
+    // multiple of kXcds, so b % kXcds is the XCD this block runs on)
+    const int b = (int)blockIdx.x - L.block_begin;
+    const int xcd = b % kXcds, slot = b / kXcds;
+    const int q = L.tiles / kXcds, rem = L.tiles % kXcds;
+    if (slot >= q + (xcd < rem ? 1 : 0)) return;   // padding block
+    int tn = xcd * q + min(xcd, rem) + slot;
+    // (split, tm, tn) of the tile, split-major
+    int split = 0, tm = 0;
     const int per_split = L.ntm * L.ntn;
-    const int split = local / per_split;
-    const int tm = (local % per_split) / L.ntn, tn = local % L.ntn;
+    while (tn >= per_split) {
+        tn -= per_split;
+        ++split;
+    }
+    while (tn >= L.ntn) {
+        tn -= L.ntn;
+        ++tm;
+    }
 
     const int t = threadIdx.x;
     const int lane = t % kWave, wid = t / kWave;
     const int wm = wid / 2, wn = wid % 2;
-    const int64_t C = L.C, n = L.n, d = L.d, lda = L.lda;
+    const int64_t C = L.C, n = L.n;
     const int64_t row0 = (int64_t)tm * kBM;
     const int64_t col0 = (int64_t)tn * kBN;
     const int64_t kbeg = (int64_t)split * L.kchunk;
-    const int64_t kend = min(kbeg + (int64_t)L.kchunk, lda);
-    const float *__restrict__ X = L.X;
+    const int64_t kend = min(kbeg + (int64_t)L.kchunk, (int64_t)L.d);
 
-    // staging roles
-    const int arow = t / 2, ak0 = (t % 2) * 8;     // A: 8 consecutive k of one row
-    const int64_t agrow = row0 + arow;
-    const bool arow_ok = agrow < C;
-    const float *ap = L.A + (arow_ok ? agrow : 0) * lda;
-    const int xk = t / 16, xc0 = (t % 16) * 8;     // X: 8 consecutive columns of one k
+    // buffer resources over this K range's rows of Dt and X (below 2^31
+    // bytes, see plan_item): rows past kend read as zeros
+    const __amdgpu_buffer_rsrc_t rsA =
+        make_rsrc(L.Dt + kbeg * L.ldc, (uint32_t)((kend - kbeg) * L.ldc * 4));
+    const __amdgpu_buffer_rsrc_t rsX = make_rsrc(L.X + kbeg * n, (uint32_t)((kend - kbeg) * n * 4));
+    // staging role: row sk of the slab, 4 * kVec consecutive columns from sm
+    const int sk = t / kRowThreads, sm = (t % kRowThreads) * 4 * kVec;
+    uint32_t offA[kVec], offX[kVec];
+#pragma unroll
+    for (int v = 0; v < kVec; ++v) {
+        const int64_t m = row0 + sm + 4 * v, c = col0 + sm + 4 * v;
+        offA[v] = m < L.ldc ? (uint32_t)((sk * L.ldc + m) * 4) : kOob;   // ldc % 4 == 0
+        offX[v] = (kVecX && c < n) ? (uint32_t)((sk * n + c) * 4) : kOob;   // n % 4 == 0
+    }
+    const uint32_t stepA = (uint32_t)(kBK * L.ldc * 4), stepX = (uint32_t)(kBK * n * 4);
 
-    float ra[8], rx[8];
+    f32x4 ra[kVec], rx[kVec];
     auto load = [&](int64_t k0) {
-        if (arow_ok) {
-            const float4 v0 = *(const float4 *)(ap + k0 + ak0);
-            const float4 v1 = *(const float4 *)(ap + k0 + ak0 + 4);
-            ra[0] = v0.x; ra[1] = v0.y; ra[2] = v0.z; ra[3] = v0.w;
-            ra[4] = v1.x; ra[5] = v1.y; ra[6] = v1.z; ra[7] = v1.w;
-        } else {
+        const uint32_t s = (uint32_t)((k0 - kbeg) / kBK);
 #pragma unroll
-            for (int u = 0; u < 8; ++u) ra[u] = 0.0f;
-        }
-        const int64_t j = k0 + xk;
-        const int64_t c = col0 + xc0;
-        if (j < d) {
-            const float *xp = X + j * n + c;
-            if (kVecX && c + 8 <= n) {
-                const float4 v0 = *(const float4 *)xp;
-                const float4 v1 = *(const float4 *)(xp + 4);
-                rx[0] = v0.x; rx[1] = v0.y; rx[2] = v0.z; rx[3] = v0.w;
-                rx[4] = v1.x; rx[5] = v1.y; rx[6] = v1.z; rx[7] = v1.w;
+        for (int v = 0; v < kVec; ++v) {
+            ra[v] = load4(rsA, offA[v] == kOob ? kOob : offA[v] + s * stepA);
+            if constexpr (kVecX) {
+                rx[v] = load4(rsX, offX[v] == kOob ? kOob : offX[v] + s * stepX);
             } else {
+                const int64_t c = col0 + sm + 4 * v;
 #pragma unroll
-                for (int u = 0; u < 8; ++u) rx[u] = (c + u < n) ? xp[u] : 0.0f;
+                for (int u = 0; u < 4; ++u) {
+                    const uint32_t o = c + u < n ? (uint32_t)(((k0 - kbeg + sk) * n + c + u) * 4) : kOob;
+                    rx[v][u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsX, o, 0, 0));
+                }
             }
-        } else {
-#pragma unroll
-            for (int u = 0; u < 8; ++u) rx[u] = 0.0f;
         }
     };
     auto store = [&](int buf) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u) sA[buf][ak0 + u][arow] = ra[u];
-        *(float4 *)&sX[buf][xk][xc0] = make_float4(rx[0], rx[1], rx[2], rx[3]);
-        *(float4 *)&sX[buf][xk][xc0 + 4] = make_float4(rx[4], rx[5], rx[6], rx[7]);
+        for (int v = 0; v < kVec; ++v) {
+            *(f32x4 *)&sA[buf][sk][sm + 4 * v] = ra[v];
+            *(f32x4 *)&sX[buf][sk][sm + 4 * v] = rx[v];
+        }
     };
 
     floatx16 acc[2][2];
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.0f;
+            for (int v = 0; v < 16; ++v) acc[a][bb][v] = 0.0f;
 
     int buf = 0;
-    if (kbeg < kend) {
-        load(kbeg);
-        store(0);
-    }
+    load(kbeg);
+    store(0);
     __syncthreads();
     for (int64_t k0 = kbeg; k0 < kend; k0 += kBK) {
         const bool more = k0 + kBK < kend;
@@ -177,12 +275,12 @@ __global__ void __launch_bounds__(kThreads) gemm_kernel(const ErrGroup g)
 #pragma unroll
             for (int a = 0; a < 2; ++a) af[a] = sA[buf][kr][wm * 64 + a * 32 + lane % 32];
 #pragma unroll
-            for (int b = 0; b < 2; ++b) bf[b] = sX[buf][kr][wn * 64 + b * 32 + lane % 32];
+            for (int bb = 0; bb < 2; ++bb) bf[bb] = sX[buf][kr][wn * 64 + bb * 32 + lane % 32];
 #pragma unroll
             for (int a = 0; a < 2; ++a)
 #pragma unroll
-                for (int b = 0; b < 2; ++b)
-                    acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[a], bf[b], acc[a][b], 0, 0, 0);
+                for (int bb = 0; bb < 2; ++bb)
+                    acc[a][bb] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[a], bf[bb], acc[a][bb], 0, 0, 0);
         }
         if (more) store(buf ^ 1);
         __syncthreads();
@@ -191,66 +289,77 @@ __global__ void __launch_bounds__(kThreads) gemm_kernel(const ErrGroup g)
 
     // Output layout of a 32 x 32 MFMA block: lane holds column lane % 32 and,
     // in register v, row 8 * (v / 4) + 4 * (lane / 32) + (v % 4).
-    if (L.splits == 1) {
-        for (int pass = 0; pass < 2; ++pass) {
-            if (wn == pass) {
-#pragma unroll
-                for (int a = 0; a < 2; ++a)
-#pragma unroll
-                    for (int v = 0; v < 16; ++v) {
-                        double s = (double)(acc[a][0][v] * acc[a][0][v]) +
-                                   (double)(acc[a][1][v] * acc[a][1][v]);
-                        s = half_wave_reduce(s, SumOp());
-                        if (lane % 32 == 0) {
-                            const int r = wm * 64 + a * 32 + 8 * (v / 4) + 4 * (lane / 32) + (v % 4);
-                            sRow[r] = pass == 0 ? s : sRow[r] + s;
-                        }
-                    }
-            }
-            __syncthreads();
-        }
-        double *rowpart = (double *)L.part;
-        for (int r = t; r < kBM; r += kThreads) {
-            const int64_t gr = row0 + r;
-            if (gr < C) rowpart[(int64_t)tn * C + gr] = sRow[r];
-        }
-    } else {
-        // Y tile of this K range: ypart[split][row][col]
-        float *yp = (float *)L.part + (int64_t)split * C * n;
+    auto row_of = [&](int a, int v) {
+        return row0 + wm * 64 + a * 32 + 8 * (v / 4) + 4 * (lane / 32) + (v % 4);
+    };
+    auto col_of = [&](int bb) { return col0 + wn * 64 + bb * 32 + lane % 32; };
+
+    if (L.splits > 1) {
+        // this K range's Y tile; the finish kernel sums the ranges
+        float *yp = L.ypart;
 #pragma unroll
         for (int a = 0; a < 2; ++a)
 #pragma unroll
-            for (int b = 0; b < 2; ++b)
+            for (int bb = 0; bb < 2; ++bb)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
-                    const int64_t r = row0 + wm * 64 + a * 32 + 8 * (v / 4) + 4 * (lane / 32) + (v % 4);
-                    const int64_t c = col0 + wn * 64 + b * 32 + lane % 32;
-                    if (r < C && c < n) yp[r * n + c] = acc[a][b][v];
+                    const int64_t r = row_of(a, v), c = col_of(bb);
+                    if (r < C && c < n) yp[((int64_t)split * C + r) * n + c] = acc[a][bb][v];
                 }
+        return;
+    }
+
+    // squares summed over the tile's columns, per row (fp64, fixed order)
+    for (int pass = 0; pass < 2; ++pass) {
+        if (wn == pass) {
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const double y0 = (double)acc[a][0][v], y1 = (double)acc[a][1][v];
+                    double s = fma(y0, y0, y1 * y1);
+                    s = half_wave_reduce(s, SumOp());
+                    if (lane % 32 == 0) {
+                        const int r = (int)(row_of(a, v) - row0);
+                        sRow[r] = pass == 0 ? s : sRow[r] + s;
+                    }
+                }
+        }
+        __syncthreads();
+    }
+    for (int r = t; r < kBM; r += kThreads) {
+        const int64_t gr = row0 + r;
+        if (gr < C) L.rowpart[(int64_t)tn * C + gr] = sRow[r];
     }
 }
 
-// one workgroup per row of every layer
-__global__ void __launch_bounds__(256) finish_kernel(const ErrGroup g)
+// ---- 3. finish: per row, the sum over column tiles of the row partials
+// (256 rows per workgroup), or for a split layer the sum over K ranges of Y,
+// squared and summed over the columns (one workgroup per row); fixed order,
+// fp64, divided by n
+__global__ void __launch_bounds__(256) finish_err_kernel(const ErrGroup g)
 {
     __shared__ double red[256 / kWave];
     int li = 0;
-    while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].row_begin) ++li;
+    while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].fin_begin) ++li;
     const ErrLayer &L = g.L[li];
-    const int64_t k = (int64_t)blockIdx.x - L.row_begin;
     const int64_t C = L.C, n = L.n;
-    double s = 0.0;
+    const int b = (int)blockIdx.x - L.fin_begin;
     if (L.splits == 1) {
-        const double *rp = (const double *)L.part;
-        if (threadIdx.x == 0)
-            for (int i = 0; i < L.ntn; ++i) s += rp[(int64_t)i * C + k];
-    } else {
-        const float *yp = (const float *)L.part;
-        for (int64_t c = threadIdx.x; c < n; c += 256) {
-            float y = 0.0f;
-            for (int sp = 0; sp < L.splits; ++sp) y += yp[((int64_t)sp * C + k) * n + c];
-            s += (double)y * (double)y;
+        const int64_t k = (int64_t)b * 256 + threadIdx.x;
+        if (k < C) {
+            double s = 0.0;
+            for (int i = 0; i < L.ntn; ++i) s += L.rowpart[(int64_t)i * C + k];
+            L.out[k] = (float)(s / (double)n);
         }
+        return;
+    }
+    const int64_t k = b;
+    double s = 0.0;
+    for (int64_t c = threadIdx.x; c < n; c += 256) {
+        float y = 0.0f;
+        for (int sp = 0; sp < L.splits; ++sp) y += L.ypart[((int64_t)sp * C + k) * n + c];
+        s = fma((double)y, (double)y, s);
     }
     s = block_reduce<256>(s, SumOp(), red);
     if (threadIdx.x == 0) L.out[k] = (float)(s / (double)n);
@@ -262,8 +371,8 @@ struct Item {
 };
 
 struct Plan {
-    int64_t lda, ntm, ntn, splits, kchunk;
-    size_t a_bytes, part_bytes;
+    int64_t ldc, ntm, ntn, splits, kchunk;
+    size_t dt_bytes, rowpart_bytes, ypart_bytes;
 };
 
 size_t align256(size_t b) { return (b + 255) / 256 * 256; }
@@ -280,29 +389,40 @@ std::vector<Item> items_of(const ErrLayerIn *in, int n_in)
 }
 
 // K split of a layer: tiles of about work / 512 slabs (two per CU), at least
-// 32 slabs.  It depends on the layer alone, so a layer's result does not
-// depend on the other layers of the call.
-std::vector<Plan> plan_group(const Item *it, int cnt)
+// 64 slabs, and K ranges whose rows of Dt and X stay below 2^31 bytes.  It
+// depends on the layer alone, so a layer's result does not depend on the
+// other layers of the call.
+Plan plan_item(const ErrLayerIn &I)
 {
-    std::vector<Plan> p(cnt);
+    Plan q;
+    q.ldc = (I.C + 3) / 4 * 4;
+    q.ntm = (I.C + kBM - 1) / kBM;
+    q.ntn = (I.n + kBN - 1) / kBN;
+    const int64_t slabs = (I.d + kBK - 1) / kBK;
+    const double work = (double)(q.ntm * q.ntn) * (double)slabs;
+    const int64_t target = std::max<int64_t>(64, (int64_t)(work / 512.0 + 0.5));
+    int64_t sp = (slabs + target / 2) / target;
+    sp = std::max<int64_t>(1, std::min<int64_t>(sp, slabs));
+    int64_t kchunk = (slabs + sp - 1) / sp * kBK;
+    const int64_t wide = std::max(q.ldc, I.n);
+    const int64_t max_chunk = ((1LL << 31) - 1) / (4 * wide) / kBK * kBK;   // >= kBK (C, n < 2^24)
+    kchunk = std::min(kchunk, max_chunk);
+    q.kchunk = kchunk;
+    q.splits = (I.d + kchunk - 1) / kchunk;   // no empty K range
+    q.dt_bytes = align256(sizeof(float) * (size_t)(I.d * q.ldc));
+    q.rowpart_bytes = align256(sizeof(double) * (size_t)(q.ntn * I.C));
+    q.ypart_bytes = q.splits > 1 ? align256(sizeof(float) * (size_t)(q.splits * I.C * I.n)) : 0;
+    return q;
+}
+
+size_t group_bytes(const Item *it, int cnt)
+{
+    size_t b = 0;
     for (int i = 0; i < cnt; ++i) {
-        const ErrLayerIn &I = *it[i].in;
-        Plan &q = p[i];
-        q.lda = (I.d + kBK - 1) / kBK * kBK;
-        q.ntm = (I.C + kBM - 1) / kBM;
-        q.ntn = (I.n + kBN - 1) / kBN;
-        const int64_t slabs = q.lda / kBK;
-        const double work = (double)(q.ntm * q.ntn) * (double)slabs;
-        const int64_t target = std::max<int64_t>(32, (int64_t)(work / 512.0 + 0.5));
-        int64_t sp = (slabs + target / 2) / target;
-        sp = std::max<int64_t>(1, std::min<int64_t>(sp, slabs));
-        q.splits = sp;
-        q.kchunk = (slabs + sp - 1) / sp * kBK;
-        q.a_bytes = align256(sizeof(float) * (size_t)(I.C * q.lda));
-        q.part_bytes = align256(sp == 1 ? sizeof(double) * (size_t)(q.ntn * I.C)
-                                        : sizeof(float) * (size_t)(sp * I.C * I.n));
+        const Plan q = plan_item(*it[i].in);
+        b += q.dt_bytes + q.rowpart_bytes + q.ypart_bytes;
     }
-    return p;
+    return b;
 }
 
 }  // namespace
@@ -313,10 +433,7 @@ size_t err_scratch_bytes(const ErrLayerIn *in, int n_in)
     size_t total = 0;
     for (size_t base = 0; base < it.size(); base += kMaxErrLayers) {
         const int cnt = (int)std::min<size_t>(kMaxErrLayers, it.size() - base);
-        std::vector<Plan> p = plan_group(it.data() + base, cnt);
-        size_t b = 0;
-        for (const Plan &q : p) b += q.a_bytes + q.part_bytes;
-        total = std::max(total, b);
+        total = std::max(total, group_bytes(it.data() + base, cnt));
     }
     return total;
 }
@@ -327,18 +444,19 @@ hipError_t launch_output_error(const ErrLayerIn *in, int n_in, int P, void *scra
     for (size_t base = 0; base < it.size(); base += kMaxErrLayers) {
         const int cnt = (int)std::min<size_t>(kMaxErrLayers, it.size() - base);
         const Item *grp = it.data() + base;
-        std::vector<Plan> p = plan_group(grp, cnt);
-        // longest tiles first
+        std::vector<Plan> p(cnt);
+        for (int i = 0; i < cnt; ++i) p[i] = plan_item(*grp[i].in);
+        // longest K ranges first
         std::vector<int> order(cnt);
         for (int i = 0; i < cnt; ++i) order[i] = i;
         std::stable_sort(order.begin(), order.end(),
                          [&](int a, int b) { return p[a].kchunk > p[b].kchunk; });
+        char *cur = (char *)scratch;
         ErrGroup g;
         g.n_layers = cnt;
         g.P = P;
         g.vecx = 1;
-        char *cur = (char *)scratch;
-        int64_t tiles = 0, rows = 0, max_elems = 0;
+        int64_t blocks = 0, fblocks = 0, nblocks = 0;
         for (int o = 0; o < cnt; ++o) {
             const int i = order[o];
             const ErrLayerIn &I = *grp[i].in;
@@ -351,36 +469,41 @@ hipError_t launch_output_error(const ErrLayerIn *in, int n_in, int P, void *scra
             L.X = I.X;
             L.out = grp[i].use_points ? I.err : I.ref;
             L.use_points = grp[i].use_points;
-            L.A = (float *)cur;
-            cur += q.a_bytes;
-            L.part = cur;
-            cur += q.part_bytes;
+            L.Dt = (float *)cur;
+            cur += q.dt_bytes;
+            L.rowpart = (double *)cur;
+            cur += q.rowpart_bytes;
+            L.ypart = q.splits > 1 ? (float *)cur : nullptr;
+            cur += q.ypart_bytes;
             L.C = (int)I.C;
             L.d = (int)I.d;
             L.n = (int)I.n;
-            L.lda = (int)q.lda;
+            L.ldc = (int)q.ldc;
             L.ntm = (int)q.ntm;
             L.ntn = (int)q.ntn;
             L.splits = (int)q.splits;
             L.kchunk = (int)q.kchunk;
-            L.tile_begin = (int)tiles;
-            L.row_begin = (int)rows;
-            tiles += q.ntm * q.ntn * q.splits;
-            rows += I.C;
-            max_elems = std::max<int64_t>(max_elems, I.C * q.lda);
+            L.tiles = (int)(q.ntm * q.ntn * q.splits);
+            L.block_begin = (int)blocks;
+            blocks += (L.tiles + kXcds - 1) / kXcds * kXcds;
+            L.form_kt = (int)((I.d + kFT - 1) / kFT);
+            L.form_begin = (int)fblocks;
+            fblocks += (int64_t)L.form_kt * ((I.C + kFT - 1) / kFT);
+            L.fin_begin = (int)nblocks;
+            nblocks += q.splits > 1 ? I.C : (I.C + 255) / 256;
+            L.vecw = I.d % 4 == 0 && ((uintptr_t)I.W) % 16 == 0 && ((uintptr_t)I.codes) % 4 == 0;
             if (I.n % 4 != 0 || ((uintptr_t)I.X) % 16 != 0) g.vecx = 0;
         }
-        const int64_t fblocks = std::min<int64_t>((max_elems + 255) / 256, 4096);
-        hipLaunchKernelGGL(form_rows_kernel, dim3((unsigned)fblocks, (unsigned)cnt), dim3(256), 0, s, g);
+        if (blocks > 0x7fffffffLL || fblocks > 0x7fffffffLL || nblocks > 0x7fffffffLL)
+            return hipErrorInvalidValue;
+        hipLaunchKernelGGL(form_dt_kernel, dim3((unsigned)fblocks), dim3(256), 0, s, g);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        if (g.vecx)
-            hipLaunchKernelGGL(gemm_kernel<true>, dim3((unsigned)tiles), dim3(kThreads), 0, s, g);
-        else
-            hipLaunchKernelGGL(gemm_kernel<false>, dim3((unsigned)tiles), dim3(kThreads), 0, s, g);
+        auto kern = g.vecx ? gemm_err_kernel<true> : gemm_err_kernel<false>;
+        hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kThreads), 0, s, g);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(finish_kernel, dim3((unsigned)rows), dim3(256), 0, s, g);
+        hipLaunchKernelGGL(finish_err_kernel, dim3((unsigned)nblocks), dim3(256), 0, s, g);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

@@ -1,7 +1,15 @@
 // Quantized weights of Eq. (4): W_hat[k][j] = fl32(sum_{i<n_k} a_i q_i[j]),
-// summed in fp64 in point order.  Elementwise and HBM-bound: consecutive
-// threads on consecutive j.  Up to kMaxRecLayers layers share one launch
-// (blockIdx.y = layer; descriptors by value in the kernel arguments).
+// summed in fp64 in point order.  Elementwise and HBM-bound: it reads the
+// n_k code rows of each channel and writes its fp32 row once.
+//
+// Up to kMaxRecLayers layers share one launch (descriptors by value in the
+// kernel arguments).  A workgroup takes a group of whole rows of one layer
+// (about kRowElems elements), so a row's count and scales are uniform loads:
+//  - rows of at least 256 elements: the workgroup sweeps each row in turn,
+//    four elements per thread (one 32-bit word of codes per point, one float4
+//    store) when the layer has d % 4 == 0 and aligned buffers;
+//  - shorter rows (depthwise kernels, d = 9): the group's elements are spread
+//    over the threads as one flat range.
 #include <algorithm>
 
 #include "internal.hpp"
@@ -10,26 +18,78 @@ namespace mpq {
 
 namespace {
 
+constexpr int kRecThreads = 256;
+constexpr int kRowElems = 4096;
+
+struct RecDesc {
+    const int8_t *codes;
+    const float *scales;
+    const int32_t *counts;
+    float *W_hat;
+    int C, d;
+    int rows;          // rows per workgroup
+    int block_begin;   // first workgroup of this layer
+    int vec;           // d % 4 == 0, codes 4-byte and W_hat 16-byte aligned
+};
+
 struct RecGroup {
     int n_layers;
     int P;
-    RecLayer L[kMaxRecLayers];
+    RecDesc L[kMaxRecLayers];
 };
+static_assert(sizeof(RecGroup) <= 4096, "kernel arguments");
 
-__global__ void __launch_bounds__(256) reconstruct_kernel(const RecGroup g)
+__global__ void __launch_bounds__(kRecThreads) reconstruct_kernel(const RecGroup g)
 {
-    const RecLayer &L = g.L[blockIdx.y];
+    int li = 0;
+    while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].block_begin) ++li;
+    const RecDesc &L = g.L[li];
     const int P = g.P;
-    const int64_t total = L.C * L.d;
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
-         e += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t k = e / L.d, j = e - k * L.d;
-        const int n = min(max(L.counts[k], 0), P);  // clamp: counts is caller data
-        const int8_t *q = L.codes + k * (int64_t)P * L.d + j;
+    const int d = L.d;
+    const int k0 = ((int)blockIdx.x - L.block_begin) * L.rows;
+    const int k1 = min(k0 + L.rows, L.C);
+    const int t = threadIdx.x;
+
+    if (d < kRecThreads) {
+        // flat range of short rows
+        const int total = (k1 - k0) * d;
+        for (int e = t; e < total; e += kRecThreads) {
+            const int kr = e / d, j = e - kr * d;
+            const int64_t k = k0 + kr;
+            const int n = min(max(L.counts[k], 0), P);   // clamp: counts is caller data
+            const int8_t *q = L.codes + k * (int64_t)P * d + j;
+            const float *a = L.scales + k * (int64_t)P;
+            double s = 0.0;
+            for (int i = 0; i < n; ++i) s = fma((double)a[i], (double)q[(int64_t)i * d], s);
+            L.W_hat[k * d + j] = (float)s;
+        }
+        return;
+    }
+    for (int64_t k = k0; k < k1; ++k) {
+        const int n = min(max(L.counts[k], 0), P);
+        const int8_t *crow = L.codes + k * (int64_t)P * d;
         const float *a = L.scales + k * (int64_t)P;
-        double s = 0.0;
-        for (int i = 0; i < n; ++i) s = fma((double)a[i], (double)q[(int64_t)i * L.d], s);
-        L.W_hat[e] = (float)s;
+        float *out = L.W_hat + k * d;
+        if (L.vec) {
+            for (int j = 4 * t; j < d; j += 4 * kRecThreads) {
+                double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+                for (int i = 0; i < n; ++i) {
+                    const uint32_t w = *(const uint32_t *)(crow + (int64_t)i * d + j);
+                    const double ai = (double)a[i];
+                    s0 = fma(ai, (double)(int)(int8_t)(uint8_t)w, s0);
+                    s1 = fma(ai, (double)(int)(int8_t)(uint8_t)(w >> 8), s1);
+                    s2 = fma(ai, (double)(int)(int8_t)(uint8_t)(w >> 16), s2);
+                    s3 = fma(ai, (double)(int)(int8_t)(uint8_t)(w >> 24), s3);
+                }
+                *(float4 *)(out + j) = make_float4((float)s0, (float)s1, (float)s2, (float)s3);
+            }
+        } else {
+            for (int j = t; j < d; j += kRecThreads) {
+                double s = 0.0;
+                for (int i = 0; i < n; ++i) s = fma((double)a[i], (double)crow[(int64_t)i * d + j], s);
+                out[j] = (float)s;
+            }
+        }
     }
 }
 
@@ -41,14 +101,23 @@ hipError_t launch_reconstruct(const RecLayer *in, int n_in, int P, hipStream_t s
         RecGroup g;
         g.n_layers = std::min(kMaxRecLayers, n_in - base);
         g.P = P;
-        int64_t most = 0;
+        int64_t blocks = 0;
         for (int i = 0; i < g.n_layers; ++i) {
-            g.L[i] = in[base + i];
-            most = std::max<int64_t>(most, g.L[i].C * g.L[i].d);
+            const RecLayer &I = in[base + i];
+            RecDesc &L = g.L[i];
+            L.codes = I.codes;
+            L.scales = I.scales;
+            L.counts = I.counts;
+            L.W_hat = I.W_hat;
+            L.C = (int)I.C;
+            L.d = (int)I.d;
+            L.rows = (int)std::max<int64_t>(1, kRowElems / I.d);
+            L.block_begin = (int)blocks;
+            blocks += (I.C + L.rows - 1) / L.rows;
+            L.vec = I.d % 4 == 0 && ((uintptr_t)I.codes) % 4 == 0 && ((uintptr_t)I.W_hat) % 16 == 0;
         }
-        const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((most + 255) / 256, 4096));
-        hipLaunchKernelGGL(reconstruct_kernel, dim3((unsigned)blocks, (unsigned)g.n_layers), dim3(256),
-                           0, s, g);
+        if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(reconstruct_kernel, dim3((unsigned)blocks), dim3(kRecThreads), 0, s, g);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
