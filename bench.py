@@ -2,23 +2,25 @@
 """Throughput of the multipoint-quantization hot path on one MI355X.
 
 One step = the whole path over one synthetic workload already resident in
-HBM: for every layer, the greedy fit (mpq_fit_layer), the output error on
-the layer's calibration batch (mpq_output_error) and the reconstruction
-(mpq_reconstruct).  The default workload is the ResNet-18-shaped stack
-(21 layers, 5,800 channels, 4 bits, up to 4 points, 256 candidate scales,
-tol 1e-3, 1,024 calibration columns).
+HBM: for every layer, the greedy fit (mpq_fit_layers), the output error on
+the layer's calibration batch (mpq_output_error_layers) and the
+reconstruction (mpq_reconstruct_layers).  The default workload is the
+ResNet-18-shaped stack (21 layers, 5,800 channels, 4 bits, up to 4 points,
+256 candidate scales, tol 1e-3, 1,024 calibration columns).
 
 Prints one JSON line.  `value` is channel-points fitted per second over the
 whole step (sum of the per-channel point counts of all layers / step time).
-`roofline` describes the kernel with the most time in the timed region,
-measured with HIP events on the stream the kernels run on.  `cpu_baseline`
-times the fp64 CPU oracle on a sample of the same workload.
+Every kernel launch of the timed steps is timed by HIP events that the
+library records on the launch's own stream (mpq_timing_enable); `roofline`
+describes the kernel with the most time per step, `kernels` all of them.
+`cpu_baseline` times the fp64 CPU oracle on a sample of the same workload.
 """
 from __future__ import annotations
 
 import argparse
 import json
 import os
+import re
 import sys
 import time
 
@@ -30,6 +32,12 @@ PEAK_MFMA_F32_TFLOPS = 157.3
 PEAK_VALU_F32_TFLOPS = 157.3            # published (packed) FP32 vector peak
 PEAK_VALU_F32_NONPACKED_TFLOPS = 78.6   # 256 CU x 64 lanes x 2 FLOP x 2.4 GHz
 FLOP_PER_EVAL = 7                       # scale-mul, round, clamp, fma (2), square-acc fma (2)
+
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "resnet18_hbm_traffic.md")
+COPY_BYTES = 256 << 20
+STAGES = (("fit", ("fit_hist_kernel", "fit_dense_kernel")),
+          ("output_error", ("form_dt_kernel", "gemm_err_kernel", "finish_err_kernel")),
+          ("reconstruct", ("reconstruct_kernel",)))
 
 
 def parse():
@@ -49,18 +57,14 @@ def parse():
                          "--copy-calibration` and exit")
     ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
                     help="print the per-kernel summary of a rocprofv3 --kernel-trace --stats run "
-                         "of `bench.py --steps 5 --warmup 1 --no-cpu-baseline` and exit")
+                         "and exit")
+    ap.add_argument("--bench-json", metavar="FILE",
+                    help="with --summarize-trace: the bench.py line of an untraced run of the "
+                         "same build, compared kernel by kernel")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before the steps, copy a 256 MiB device buffer once (a kernel of known "
                          "traffic, to scale the FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
-
-
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "resnet18_hbm_traffic.md")
-COPY_BYTES = 256 << 20
-KERNEL_KINDS = (("fit", ("fit_hist_kernel", "fit_dense_kernel")),
-                ("output_error", ("form_dt_kernel", "gemm_err_kernel", "finish_err_kernel")),
-                ("reconstruct", ("reconstruct_kernel",)))
 
 
 def sources_digest():
@@ -74,14 +78,31 @@ def sources_digest():
     return h.hexdigest()[:16]
 
 
+def kernel_key(profiler_name):
+    """The library's timing name of a kernel from the demangled name rocprofv3
+    prints (fit_hist_kernel<T, EPT, kLinear, kLat> -> fit_hist_kernel<T,EPT,mode>)."""
+    m = re.search(r"fit_hist_kernel<(\d+), (\d+), (true|false), (true|false)>", profiler_name)
+    if m:
+        mode = "lattice" if m.group(4) == "true" else "linear" if m.group(3) == "true" else "grid"
+        return f"fit_hist_kernel<{m.group(1)},{m.group(2)},{mode}>"
+    m = re.search(r"(\w+_kernel)\b", profiler_name)
+    return m.group(1) if m else None
+
+
+def stage_of(key):
+    for stage, names in STAGES:
+        if key and any(key.startswith(n) for n in names):
+            return stage
+    return None
+
+
 def summarize_pmc(fetch_dir, write_dir):
-    """HBM bytes per step and stage from the FETCH_SIZE / WRITE_SIZE counters,
+    """HBM bytes per step and kernel from the FETCH_SIZE / WRITE_SIZE counters,
     each scaled so that the 256 MiB calibration copy reads / writes 256 MiB."""
     import csv
     import glob
-    import re
 
-    def per_kind(d):
+    def per_kernel(d):
         rows = []
         for f in glob.glob(os.path.join(d, "*counter_collection.csv")):
             rows += list(csv.DictReader(open(f)))
@@ -89,22 +110,19 @@ def summarize_pmc(fetch_dir, write_dir):
         if not cal:
             raise SystemExit(f"no calibration copy in {d}")
         factor = COPY_BYTES / 1024.0 / float(cal[0]["Counter_Value"])
-        out = {k: 0.0 for k, _ in KERNEL_KINDS}
-        steps = 0
+        out, launches = {}, {}
         for r in rows:
-            m = re.search(r"(\w+_kernel)", r["Kernel_Name"])
-            name = m.group(1) if m else ""
-            for kind, names in KERNEL_KINDS:
-                if name in names:
-                    out[kind] += float(r["Counter_Value"]) * factor * 1024.0
-            if name == "gemm_err_kernel":
-                steps += 1
-        return factor, out, steps
+            k = kernel_key(r["Kernel_Name"])
+            if not stage_of(k):
+                continue
+            out[k] = out.get(k, 0.0) + float(r["Counter_Value"]) * factor * 1024.0
+            launches[k] = launches.get(k, 0) + 1
+        return factor, out, launches
 
-    ff, fetch, steps = per_kind(fetch_dir)
-    wf, write, _ = per_kind(write_dir)
-    steps = max(steps, 1)
-    lines = ["# HBM traffic per step: ResNet-18-shaped workload", "",
+    ff, fetch, launches = per_kernel(fetch_dir)
+    wf, write, _ = per_kernel(write_dir)
+    steps = max(launches.get("gemm_err_kernel", 1), 1)
+    lines = ["# HBM traffic per step and kernel: ResNet-18-shaped workload", "",
              "Two rocprofv3 counter runs (one counter each), from the repository root:", "",
              "```",
              "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_FETCH_SIZE -o p -- \\",
@@ -114,62 +132,20 @@ def summarize_pmc(fetch_dir, write_dir):
              "python3 bench.py --summarize-pmc gpurun_out/pmc_FETCH_SIZE gpurun_out/pmc_WRITE_SIZE",
              "```", "",
              f"Scale factors from a 256 MiB device copy: FETCH_SIZE x {ff:.4f}, WRITE_SIZE x {wf:.4f}.",
-             f"Bytes per step (the run holds {steps} steps).", "",
-             "| stage | fetch bytes | write bytes | total bytes |", "|---|---:|---:|---:|"]
-    for kind, _ in KERNEL_KINDS:
-        f_, w_ = fetch[kind] / steps, write[kind] / steps
-        lines.append(f"| {kind} | {f_:.0f} | {w_:.0f} | {f_ + w_:.0f} |")
+             f"Bytes per step (the run holds {steps} steps) and per launch.", "",
+             "| kernel | launches/step | fetch bytes/step | write bytes/step | bytes/launch |",
+             "|---|---:|---:|---:|---:|"]
+    for k in sorted(fetch, key=lambda k: -(fetch[k] + write.get(k, 0.0))):
+        f_, w_ = fetch[k] / steps, write.get(k, 0.0) / steps
+        per = launches[k] / steps
+        lines.append(f"| {k} | {per:g} | {f_:.0f} | {w_:.0f} | {(f_ + w_) / per:.0f} |")
     lines += ["", f"sources: {sources_digest()}", ""]
     print("\n".join(lines))
 
 
-def summarize_trace(trace_dir):
-    """Per-kernel and per-stage time of a traced bench run, from the
-    kernel_stats.csv that rocprofv3 --stats writes."""
-    import csv
-    import glob
-    import re
-
-    files = glob.glob(os.path.join(trace_dir, "*kernel_stats.csv"))
-    if not files:
-        raise SystemExit(f"no kernel_stats.csv in {trace_dir}")
-    rows = list(csv.DictReader(open(files[0])))
-    calls = max(int(r["Calls"]) for r in rows if "fit_" in r["Name"])
-    lines = ["# rocprofv3 kernel summary: ResNet-18-shaped workload, one bench step", "",
-             "Workload: 21 layers (5,800 channels, 11,678,912 weights), 4 bits, up to 4 points,",
-             "256 candidate scales, tol 1e-3, calibration batches d x 1024.  One step = fit +",
-             "output error + reconstruction of every layer through the batched C ABI calls.", "",
-             "Command (one MI355X, from the repository root):", "", "```",
-             "rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof -o kt -- \\",
-             "    python3 bench.py --steps 5 --warmup 1 --no-cpu-baseline",
-             "python3 bench.py --summarize-trace gpurun_out/prof", "```", "",
-             f"The traced process ran {calls} steps (warm-up + timed); `calls` counts all of them.",
-             "Kernels of one stage may run concurrently on several streams, so a stage's",
-             "kernel-time sum can exceed its wall time.", "",
-             "| kernel | calls | total ms | avg us | % |", "|---|---:|---:|---:|---:|"]
-    stage = {k: 0.0 for k, _ in KERNEL_KINDS}
-    stage["other"] = 0.0
-    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
-        name = r["Name"]
-        m = re.search(r"(\w+_kernel(<[^>]*>)?)", name)
-        short = m.group(1) if m else name[:40]
-        lines.append(f"| `{short}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.3f} | "
-                     f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
-        kind = "other"
-        for k, names in KERNEL_KINDS:
-            if any(n in name for n in names):
-                kind = k
-        stage[kind] += float(r["TotalDurationNs"]) / 1e6
-    lines += ["", f"Kernel time per step (sum over the stage's kernels / {calls}):"]
-    for k, v in stage.items():
-        lines.append(f"- {k}: {v / calls:.3f} ms")
-    lines += ["", f"sources: {sources_digest()}", ""]
-    print("\n".join(lines))
-
-
-def measured_traffic(kind):
-    """HBM bytes per step of a stage from the stored counter summary, or None
-    when the summary is missing or was taken on other kernel sources."""
+def measured_traffic(key):
+    """HBM bytes per launch of a kernel from the stored counter summary, or
+    None when it is missing or was taken on other kernel sources."""
     try:
         text = open(TRAFFIC_SUMMARY).read()
     except OSError:
@@ -178,9 +154,58 @@ def measured_traffic(kind):
         return None
     for ln in text.splitlines():
         cells = [c.strip() for c in ln.strip("|").split("|")]
-        if len(cells) == 4 and cells[0] == kind:
-            return int(cells[3])
+        if len(cells) == 5 and cells[0] == key:
+            return int(float(cells[4]))
     return None
+
+
+def summarize_trace(trace_dir, bench_json=None):
+    """Per-kernel average duration of a traced bench run (kernel_stats.csv of
+    rocprofv3 --stats), beside the event-timed averages of a bench.py line."""
+    import csv
+    import glob
+
+    files = glob.glob(os.path.join(trace_dir, "*kernel_stats.csv"))
+    if not files:
+        raise SystemExit(f"no kernel_stats.csv in {trace_dir}")
+    rows = list(csv.DictReader(open(files[0])))
+    agg = {}
+    for r in rows:
+        k = kernel_key(r["Name"])
+        if not stage_of(k):
+            continue
+        a = agg.setdefault(k, [0, 0.0])
+        a[0] += int(r["Calls"])
+        a[1] += float(r["TotalDurationNs"])
+    steps = max(agg.get("gemm_err_kernel", [1])[0], 1)
+    bench = json.load(open(bench_json)) if bench_json else None
+    lines = ["# rocprofv3 kernel summary: ResNet-18-shaped workload, bench step", "",
+             "Workload: 21 layers (5,800 channels, 11,678,912 weights), 4 bits, up to 4 points,",
+             "256 candidate scales, tol 1e-3, calibration batches d x 1024.  One step = fit +",
+             "output error + reconstruction of every layer through the batched C ABI calls.", "",
+             "Commands (one MI355X, from the repository root):", "", "```",
+             "rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof -o kt -- \\",
+             "    python3 bench.py --steps 5 --warmup 1 --no-cpu-baseline",
+             "python3 bench.py --steps 5 --warmup 1 > gpurun_out/bench.json",
+             "python3 bench.py --summarize-trace gpurun_out/prof --bench-json gpurun_out/bench.json",
+             "```", "",
+             f"The traced process ran {steps} steps (warm-up + timed).  Kernels of one stage may",
+             "run concurrently on several streams.  `bench avg us` is the untraced run's average",
+             "per launch, timed by HIP events on the launch's own stream.", "",
+             "| kernel | stage | launches/step | avg us (rocprofv3) | bench avg us | us/step |",
+             "|---|---|---:|---:|---:|---:|"]
+    bk = (bench or {}).get("kernels", {})
+    for k in sorted(agg, key=lambda k: -agg[k][1]):
+        calls, tot = agg[k]
+        b = bk.get(k, {}).get("avg_us")
+        lines.append(f"| `{k}` | {stage_of(k)} | {calls / steps:g} | {tot / calls / 1e3:.2f} | "
+                     f"{'' if b is None else f'{b:.2f}'} | {tot / steps / 1e3:.2f} |")
+    lines += ["", f"sources: {sources_digest()}", ""]
+    if bench:
+        lines += ["bench.py line of the same build (untraced run):", "", "```",
+                  json.dumps({k: bench[k] for k in ("value", "unit", "ms_per_step", "roofline")}),
+                  "```", ""]
+    print("\n".join(lines))
 
 
 def main():
@@ -189,7 +214,7 @@ def main():
         summarize_pmc(*args.summarize_pmc)
         return 0
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace)
+        summarize_trace(args.summarize_trace, args.bench_json)
         return 0
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -244,6 +269,7 @@ def main():
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
+    mpq.timing_enable(True)
     wall0 = time.perf_counter()
     t_start.record(stream)
     for s in range(args.steps):
@@ -251,63 +277,77 @@ def main():
     t_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
+    launches = mpq.timing_read()
+    mpq.timing_enable(False)
     ms_total = t_start.elapsed_time(t_end)
     ms_step = ms_total / args.steps
+    steps = args.steps
 
-    # ---- per-kernel times (HIP events on the launch stream) and algorithmic work
-    t_fit = sum(e[0].elapsed_time(e[1]) for e in ev)
-    t_err = sum(e[1].elapsed_time(e[2]) for e in ev)
-    t_rec = sum(e[2].elapsed_time(e[3]) for e in ev)
-    points = evals = gemm_flop = rec_bytes = fit_bytes = 0
+    # ---- algorithmic work per kernel and step
+    fit_kernel = {}
+    work = {}   # kernel -> dict of per-step work figures
+
+    def add(k, **kv):
+        w = work.setdefault(k, {})
+        for a, b in kv.items():
+            w[a] = w.get(a, 0) + b
+
+    points = 0
     for i, W in enumerate(Ws):
         C, d = W.shape
-        counts = ls.counts[i].cpu().numpy().astype(np.int64)
-        n = int(counts.sum())
+        n = int(ls.counts[i].cpu().numpy().astype(np.int64).sum())
+        N = Xs[i].shape[1]
         points += n
-        evals += n * wk.n_grid * d
-        gemm_flop += 2 * C * d * Xs[i].shape[1]
-        # reconstruct: read the codes of the used points, write fp32
-        rec_bytes += n * d + 4 * C * d
-        # fit (algorithmic minimum): read W once, write the codes of every point
-        fit_bytes += 4 * C * d + n * d
-    steps = args.steps
-    sec_fit = t_fit * 1e-3
-    fit_gbs = fit_bytes * steps / sec_fit / 1e9
-    fit_eff_tflops = FLOP_PER_EVAL * evals * steps / sec_fit / 1e12
-    gemm_tflops = gemm_flop * steps / (t_err * 1e-3) / 1e12
-    rec_gbs = rec_bytes * steps / (t_rec * 1e-3) / 1e9
-    if args.dense:
-        fit_k = {"search": "dense", "bound": "alu", "ms_per_step": t_fit / steps,
-                 "achieved": fit_eff_tflops, "peak": PEAK_VALU_F32_TFLOPS, "unit": "TFLOP/s",
-                 "frac": fit_eff_tflops / PEAK_VALU_F32_TFLOPS,
-                 "frac_of_nonpacked_peak": fit_eff_tflops / PEAK_VALU_F32_NONPACKED_TFLOPS,
-                 "candidate_evals_per_step": evals}
-    else:
-        # the histogram search does O(d M + G) work per channel-step instead of
-        # O(d G): its bound is memory/latency, so it is priced against HBM with
-        # the algorithmic bytes; the evaluation rate it delivers is reported apart
-        fit_k = {"search": "histogram", "bound": "hbm", "ms_per_step": t_fit / steps,
-                 "achieved": fit_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                 "frac": fit_gbs / PEAK_HBM_GBS, "algorithmic_bytes_per_step": fit_bytes,
-                 "candidate_evals_per_step": evals,
-                 "candidate_evals_per_s": evals * steps / sec_fit,
-                 "dense_equivalent_tflops": fit_eff_tflops}
-    kernels = {
-        "fit": fit_k,
-        "output_error": {"bound": "mfma", "ms_per_step": t_err / steps, "achieved": gemm_tflops,
-                         "peak": PEAK_MFMA_F32_TFLOPS, "unit": "TFLOP/s",
-                         "frac": gemm_tflops / PEAK_MFMA_F32_TFLOPS, "flop_per_step": gemm_flop},
-        "reconstruct": {"bound": "hbm", "ms_per_step": t_rec / steps, "achieved": rec_gbs,
-                        "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": rec_gbs / PEAK_HBM_GBS,
-                        "bytes_per_step": rec_bytes},
-    }
-    dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
+        fk = "fit_dense_kernel" if args.dense else fit_kernel.setdefault(
+            d, mpq.fit_kernel_of(d, wk.bits, wk.n_grid, True))
+        # fit: G candidate errors per (element, point); reads W once, writes the codes
+        add(fk, evals=n * wk.n_grid * d, bytes=4 * C * d + n * d)
+        add("gemm_err_kernel", flop=2 * C * d * N)
+        # form: reads W and the codes of the used points, writes D
+        add("form_dt_kernel", bytes=4 * C * d + n * d + 4 * C * d)
+        # reconstruct: reads the codes of the used points, writes fp32
+        add("reconstruct_kernel", bytes=n * d + 4 * C * d)
+
+    per = {}
+    for name, ms in launches:
+        p = per.setdefault(name, [0, 0.0])
+        p[0] += 1
+        p[1] += ms
+    kernels = {}
+    for name, (cnt, tot) in per.items():
+        avg_s = tot / cnt * 1e-3
+        k = {"stage": stage_of(name), "launches_per_step": cnt / steps,
+             "avg_us": tot / cnt * 1e3, "us_per_step": tot / steps * 1e3}
+        w = work.get(name, {})
+        lps = cnt / steps
+        if "evals" in w:
+            ev_launch = w["evals"] / lps
+            k.update({"bound": "alu", "unit": "TFLOP/s", "peak": PEAK_VALU_F32_TFLOPS,
+                      "candidate_evals_per_launch": ev_launch,
+                      "achieved": FLOP_PER_EVAL * ev_launch / avg_s / 1e12,
+                      "hbm_gbs_algorithmic": w["bytes"] / lps / avg_s / 1e9})
+        elif "flop" in w:
+            k.update({"bound": "mfma", "unit": "TFLOP/s", "peak": PEAK_MFMA_F32_TFLOPS,
+                      "flop_per_launch": w["flop"] / lps, "achieved": w["flop"] / lps / avg_s / 1e12})
+        elif "bytes" in w:
+            k.update({"bound": "hbm", "unit": "GB/s", "peak": PEAK_HBM_GBS,
+                      "bytes_per_launch": w["bytes"] / lps, "achieved": w["bytes"] / lps / avg_s / 1e9})
+        if "achieved" in k:
+            k["frac"] = k["achieved"] / k["peak"]
+        k["hbm_bytes_per_launch_measured"] = measured_traffic(name)
+        kernels[name] = k
+    stages = {}
+    for i, st in enumerate(("fit", "output_error", "reconstruct")):
+        stages[st] = sum(e[i].elapsed_time(e[i + 1]) for e in ev) / steps
+    dom = max((k for k in kernels if "achieved" in kernels[k]), key=lambda k: kernels[k]["us_per_step"])
     K = kernels[dom]
-    for k in kernels:
-        kernels[k]["hbm_bytes_per_step_measured"] = measured_traffic(k)
     roofline = {"kernel": dom, "bound": K["bound"], "achieved": round(K["achieved"], 4),
                 "peak": K["peak"], "unit": K["unit"], "frac": round(K["frac"], 5),
-                "traffic": kernels[dom]["hbm_bytes_per_step_measured"]}
+                "traffic": K["hbm_bytes_per_launch_measured"],
+                "avg_launch_us": round(K["avg_us"], 3)}
+    if K["bound"] == "alu":
+        roofline["achieved_is"] = ("algorithmic FLOP/s: 7 FLOP per (element, candidate) evaluation "
+                                   "of Eq. (9), G per element and point")
 
     value = points * steps / (ms_total * 1e-3)
     res = {
@@ -326,10 +366,12 @@ def main():
         "config": {"workload": wk.name, "layers": nl, "channels": wk.channels,
                    "weights": wk.weights, "bits": wk.bits, "max_points": wk.max_points,
                    "n_grid": wk.n_grid, "tol": wk.tol, "calib_columns": wk.n_calib,
-                   "points_per_step": points, "parallelism": "none"},
+                   "points_per_step": points, "search": "dense" if args.dense else "histogram",
+                   "parallelism": "none"},
         "roofline": roofline,
+        "stages_ms_per_step": {k: round(v, 5) for k, v in stages.items()},
         "kernels": {k: {kk: (round(vv, 5) if isinstance(vv, float) else vv) for kk, vv in v.items()}
-                    for k, v in kernels.items()},
+                    for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["us_per_step"])},
         "wall_s_timed": round(wall, 3),
     }
 

@@ -196,6 +196,32 @@ int mpq_output_error_layers(const mpq_layer *layers, int n_layers, int max_point
  * W_hat). */
 int mpq_reconstruct_layers(const mpq_layer *layers, int n_layers, int max_points, void *stream);
 
+/*
+ * Per-launch timing (instrumentation, not part of the method).  While it is
+ * enabled, every kernel launch of the library is bracketed by two HIP events
+ * recorded on the stream the kernel runs on (a call may run independent
+ * launches on library-owned streams, joined back to the caller's stream).
+ *
+ * mpq_timing_enable(on): drops the records collected so far and turns the
+ *   recording on (on != 0) or off.  Returns MPQ_OK.
+ * mpq_timing_read(out, cap): waits for the recorded events, writes up to cap
+ *   records (HOST array) in launch order and returns the number of records
+ *   (which may exceed cap), or MPQ_ERR_INVALID_ARG.  ms is -1 for a record
+ *   whose events could not be read.
+ * mpq_fit_kernel_of(d, bits, n_grid, default_grid, name, cap): writes to the
+ *   HOST buffer name (cap bytes) the kernel name under which mpq_fit_layer
+ *   records the fit of channels of length d (default_grid: grid_host ==
+ *   NULL).  Returns an MPQ_* status.
+ */
+typedef struct mpq_kernel_time {
+    char name[64];
+    float ms;
+} mpq_kernel_time;
+
+int mpq_timing_enable(int on);
+int mpq_timing_read(mpq_kernel_time *out, int cap);
+int mpq_fit_kernel_of(int64_t d, int bits, int n_grid, int default_grid, char *name, int cap);
+
 /* Text of the calling thread's last failure ("" if none).  The pointer stays
  * valid until the thread's next failing call. */
 const char *mpq_last_error(void);

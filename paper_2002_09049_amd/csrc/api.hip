@@ -452,6 +452,23 @@ int64_t mpq_fit_max_dim(int n_grid)
     return dmax;
 }
 
+int mpq_fit_kernel_of(int64_t d, int bits, int n_grid, int default_grid, char *name, int cap)
+{
+    if (d < 1 || bits < 2 || bits > MPQ_MAX_BITS || n_grid < 1 || n_grid > MPQ_MAX_GRID || cap < 1 || !name)
+        return fail(MPQ_ERR_INVALID_ARG, "mpq_fit_kernel_of: invalid argument");
+    size_t lim = 0;
+    const int rc = device_lds_limit(&lim);
+    if (rc != MPQ_OK) return rc;
+    const int M = (1 << (bits - 1)) - 1;
+    std::string k;
+    if (mpq::fit_hist_lds(n_grid) <= lim && mpq::fit_hist_supports(d))
+        k = mpq::hist_kernel_name(d, M, n_grid, default_grid != 0);
+    else
+        k = "fit_dense_kernel";
+    snprintf(name, (size_t)cap, "%s", k.c_str());
+    return MPQ_OK;
+}
+
 int mpq_fit_layer(const float *W, int64_t c_out, int64_t d, int bits, int max_points,
                   const float *grid_host, int n_grid, float tol, int8_t *codes, float *scales,
                   int32_t *counts, float *err_opt, void *stream)

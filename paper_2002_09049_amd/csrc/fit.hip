@@ -226,6 +226,7 @@ hipError_t launch_fit(const FitParams &p, const FitLayout &L, hipStream_t s)
                                            (int)L.lds);
         if (e != hipSuccess) return e;
     }
+    LaunchTimer timer(s, "fit_dense_kernel");
     hipLaunchKernelGGL(kern, dim3((unsigned)p.C), dim3(kFitThreads), L.lds, s, p, L);
     return hipGetLastError();
 }

@@ -34,6 +34,7 @@
 // reads nothing from HBM: it writes the codes of the point chosen by the
 // previous step (Eq. (10), fp64 quotient) and updates the residual (Eq. (7)).
 #include <math.h>
+#include <stdio.h>
 
 #include "internal.hpp"
 #include "mpq.h"
@@ -541,6 +542,10 @@ hipError_t launch_hist_t(const HistBatch &b, int64_t channels, size_t lds, hipSt
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
     }
+    char name[64];
+    snprintf(name, sizeof name, "fit_hist_kernel<%d,%d,%s>", T, EPT,
+             b.grid ? "grid" : b.nlat ? "lattice" : "linear");
+    LaunchTimer timer(s, name);
     hipLaunchKernelGGL(kern, dim3((unsigned)channels), dim3(T), lds, s, b);
     return hipGetLastError();
 }
@@ -549,13 +554,14 @@ hipError_t launch_hist_t(const HistBatch &b, int64_t channels, size_t lds, hipSt
 // channels longer than the capacity T * EPT of variant v - 1, up to its own.
 // 256-thread variants let four channels share a CU (128 VGPRs, under 40 KB of
 // LDS each), so one channel's barriers and serial phases overlap another's
-// arithmetic; the 1024- and 512-thread variants cover lengths whose residual
-// would not fit 128 VGPRs at 256 threads.
+// arithmetic; the 512- and 1024-thread variants cover lengths whose residual
+// would not fit 128 VGPRs at 256 threads without spilling to scratch (at
+// 256 x 18 the spills moved ~7x the channel's algorithmic bytes through HBM).
 struct Variant {
     int threads, ept;
 };
-constexpr Variant kVariants[] = {{64, 1},  {64, 2},   {64, 4},    {256, 2},  {256, 4},
-                                 {256, 8}, {256, 18}, {1024, 8}, {512, 32}};
+constexpr Variant kVariants[] = {{64, 1},  {64, 2},  {64, 4},   {256, 2},  {256, 4},
+                                 {256, 8}, {512, 9}, {1024, 8}, {512, 32}};
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 static_assert(kVariants[kNumVariants - 1].threads * kVariants[kNumVariants - 1].ept == kHistMaxDim,
               "the last variant covers the longest channels");
@@ -579,18 +585,36 @@ int hist_variant(int64_t d)
     return v;
 }
 
+namespace {
+
+// lattice mode: default grid, longer channels (the bucket pass costs O(nlat)
+// per step), buckets within kLatMaxBuckets and 64 KiB of LDS
+int lattice_buckets(int variant, int M, int G, bool default_grid)
+{
+    const int64_t nlat = (int64_t)(2 * M - 1) * G + 1;
+    return (default_grid && kVariants[variant].threads * kVariants[variant].ept >= kLatMinDim &&
+            nlat <= kLatMaxBuckets &&
+            fit_hist_lds(G) + (size_t)nlat * sizeof(unsigned long long) <= 65536)
+               ? (int)nlat
+               : 0;
+}
+
+}  // namespace
+
+std::string hist_kernel_name(int64_t d, int M, int G, bool default_grid)
+{
+    const int v = hist_variant(d);
+    char name[64];
+    snprintf(name, sizeof name, "fit_hist_kernel<%d,%d,%s>", kVariants[v].threads, kVariants[v].ept,
+             !default_grid ? "grid" : lattice_buckets(v, M, G, true) ? "lattice" : "linear");
+    return name;
+}
+
 hipError_t launch_fit_hist(const HistBatch &batch, int variant, int64_t channels, hipStream_t s)
 {
     HistBatch b = batch;
-    // lattice mode: default grid, longer channels (the bucket pass costs
-    // O(nlat) per step), buckets within kLatMaxBuckets and 64 KiB of LDS
-    const int64_t nlat = (int64_t)(2 * b.M - 1) * b.G + 1;
     if (variant < 0 || variant >= kNumVariants) return hipErrorInvalidValue;
-    b.nlat = (!b.grid && kVariants[variant].threads * kVariants[variant].ept >= kLatMinDim &&
-              nlat <= kLatMaxBuckets &&
-              fit_hist_lds(b.G) + (size_t)nlat * sizeof(unsigned long long) <= 65536)
-                 ? (int)nlat
-                 : 0;
+    b.nlat = lattice_buckets(variant, b.M, b.G, !b.grid);
     const size_t lds = fit_hist_lds(b.G) + (size_t)b.nlat * sizeof(unsigned long long);
     switch (variant) {
     case 0: return launch_hist_t<64, 1>(b, channels, lds, s);
@@ -599,7 +623,7 @@ hipError_t launch_fit_hist(const HistBatch &batch, int variant, int64_t channels
     case 3: return launch_hist_t<256, 2>(b, channels, lds, s);
     case 4: return launch_hist_t<256, 4>(b, channels, lds, s);
     case 5: return launch_hist_t<256, 8>(b, channels, lds, s);
-    case 6: return launch_hist_t<256, 18>(b, channels, lds, s);
+    case 6: return launch_hist_t<512, 9>(b, channels, lds, s);
     case 7: return launch_hist_t<1024, 8>(b, channels, lds, s);
     // 512 threads leave 256 VGPRs per thread for the register-resident residual
     case 8: return launch_hist_t<512, 32>(b, channels, lds, s);

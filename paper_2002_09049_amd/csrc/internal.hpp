@@ -4,7 +4,24 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <string>
+
 namespace mpq {
+
+// Brackets one kernel launch with events on its stream while timing is on
+// (mpq_timing_enable); otherwise does nothing.
+class LaunchTimer {
+public:
+    LaunchTimer(hipStream_t s, const char *name);
+    ~LaunchTimer();
+    LaunchTimer(const LaunchTimer &) = delete;
+    LaunchTimer &operator=(const LaunchTimer &) = delete;
+
+private:
+    hipStream_t s_;
+    hipEvent_t start_;
+    std::string name_;
+};
 
 // Inputs of one greedy fit of a layer (see mpq_fit_layer in mpq.h).
 struct FitParams {
@@ -68,6 +85,9 @@ struct HistBatch {
 size_t fit_hist_lds(int G);
 bool fit_hist_supports(int64_t d);
 int hist_variant(int64_t d);   // layers with equal variants may share a launch
+// Name of the histogram kernel that fits channels of length d (default grid
+// when default_grid, else a caller's grid), as LaunchTimer records it.
+std::string hist_kernel_name(int64_t d, int M, int G, bool default_grid);
 hipError_t launch_fit_hist(const HistBatch &b, int variant, int64_t channels, hipStream_t s);
 
 // Output error of Eq. (12) for a list of layers; `scratch` holds

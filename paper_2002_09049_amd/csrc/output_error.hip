@@ -496,15 +496,25 @@ hipError_t launch_output_error(const ErrLayerIn *in, int n_in, int P, void *scra
         }
         if (blocks > 0x7fffffffLL || fblocks > 0x7fffffffLL || nblocks > 0x7fffffffLL)
             return hipErrorInvalidValue;
-        hipLaunchKernelGGL(form_dt_kernel, dim3((unsigned)fblocks), dim3(256), 0, s, g);
-        hipError_t e = hipGetLastError();
+        hipError_t e;
+        {
+            LaunchTimer timer(s, "form_dt_kernel");
+            hipLaunchKernelGGL(form_dt_kernel, dim3((unsigned)fblocks), dim3(256), 0, s, g);
+            e = hipGetLastError();
+        }
         if (e != hipSuccess) return e;
-        auto kern = g.vecx ? gemm_err_kernel<true> : gemm_err_kernel<false>;
-        hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kThreads), 0, s, g);
-        e = hipGetLastError();
+        {
+            LaunchTimer timer(s, "gemm_err_kernel");
+            auto kern = g.vecx ? gemm_err_kernel<true> : gemm_err_kernel<false>;
+            hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kThreads), 0, s, g);
+            e = hipGetLastError();
+        }
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(finish_err_kernel, dim3((unsigned)nblocks), dim3(256), 0, s, g);
-        e = hipGetLastError();
+        {
+            LaunchTimer timer(s, "finish_err_kernel");
+            hipLaunchKernelGGL(finish_err_kernel, dim3((unsigned)nblocks), dim3(256), 0, s, g);
+            e = hipGetLastError();
+        }
         if (e != hipSuccess) return e;
     }
     return hipSuccess;

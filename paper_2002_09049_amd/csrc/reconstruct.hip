@@ -117,6 +117,7 @@ hipError_t launch_reconstruct(const RecLayer *in, int n_in, int P, hipStream_t s
             L.vec = I.d % 4 == 0 && ((uintptr_t)I.codes) % 4 == 0 && ((uintptr_t)I.W_hat) % 16 == 0;
         }
         if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+        LaunchTimer timer(s, "reconstruct_kernel");
         hipLaunchKernelGGL(reconstruct_kernel, dim3((unsigned)blocks), dim3(kRecThreads), 0, s, g);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;

@@ -30,7 +30,8 @@ MAX_GRID = 4096
 
 EXPORTS = ("mpq_fit_layer", "mpq_fit_layer_dense", "mpq_fit_layers", "mpq_fit_max_dim",
            "mpq_output_error", "mpq_output_error_layers", "mpq_reconstruct",
-           "mpq_reconstruct_layers", "mpq_last_error")
+           "mpq_reconstruct_layers", "mpq_last_error", "mpq_timing_enable", "mpq_timing_read",
+           "mpq_fit_kernel_of")
 
 
 class Layer(ctypes.Structure):
@@ -42,6 +43,11 @@ class Layer(ctypes.Structure):
                 ("out_ref", ctypes.c_void_p), ("W_hat", ctypes.c_void_p)]
 
 _lib = None
+
+
+class KernelTime(ctypes.Structure):
+    """struct mpq_kernel_time (include/mpq.h)."""
+    _fields_ = [("name", ctypes.c_char * 64), ("ms", ctypes.c_float)]
 
 
 class MPQError(RuntimeError):
@@ -76,6 +82,12 @@ def load(path: str = LIB_PATH):
     lib.mpq_reconstruct_layers.restype = i32
     lib.mpq_last_error.argtypes = []
     lib.mpq_last_error.restype = ctypes.c_char_p
+    lib.mpq_timing_enable.argtypes = [i32]
+    lib.mpq_timing_enable.restype = i32
+    lib.mpq_timing_read.argtypes = [P, i32]
+    lib.mpq_timing_read.restype = i32
+    lib.mpq_fit_kernel_of.argtypes = [i64, i32, i32, i32, ctypes.c_char_p, i32]
+    lib.mpq_fit_kernel_of.restype = i32
     _lib = lib
     return lib
 
@@ -186,6 +198,31 @@ def reconstruct(codes: torch.Tensor, scales: torch.Tensor, counts: torch.Tensor,
                                 _dev(W_hat, torch.float32, "W_hat"), _stream(stream))
     _check(rc)
     return W_hat
+
+
+def timing_enable(on: bool = True):
+    """mpq_timing_enable: drop earlier records; record (or stop recording)
+    HIP events around every kernel launch, on the launch's own stream."""
+    _check(load().mpq_timing_enable(1 if on else 0))
+
+
+def timing_read():
+    """mpq_timing_read: [(kernel name, ms)] in launch order (waits for the
+    recorded events)."""
+    lib = load()
+    n = lib.mpq_timing_read(None, 0)
+    if n < 0:
+        _check(n)
+    buf = (KernelTime * max(n, 1))()
+    n = lib.mpq_timing_read(ctypes.addressof(buf), n)
+    return [(buf[i].name.decode(), float(buf[i].ms)) for i in range(n)]
+
+
+def fit_kernel_of(d: int, bits: int, n_grid: int, default_grid: bool = True) -> str:
+    """mpq_fit_kernel_of: the kernel name that fits channels of length d."""
+    buf = ctypes.create_string_buffer(64)
+    _check(load().mpq_fit_kernel_of(d, bits, n_grid, 1 if default_grid else 0, buf, 64))
+    return buf.value.decode()
 
 
 class LayerSet:

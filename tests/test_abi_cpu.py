@@ -145,3 +145,36 @@ def test_batched_calls_reject_invalid_arguments(lib):
     assert lib.mpq_output_error_layers(p, 2, 4, None) == 0
     assert lib.mpq_reconstruct_layers(p, 2, 4, None) == 0
     assert lib.mpq_fit_layers(p, 0, 4, 4, None, 8, 1e-3, None) == 0
+
+
+def test_output_error_rejects_oversized_dims(lib):
+    from paper_2002_09049_amd import mpq
+    E = mpq.MPQ_ERR_INVALID_ARG
+    big = (1 << 24) + 1
+    assert lib.mpq_output_error(1, 1, 1, 1, 4, 4, 2, 1, big, 1, None, None) == E
+    assert lib.mpq_output_error(1, 1, 1, 1, big, 4, 2, 1, 8, 1, None, None) == E
+
+
+def test_timing_records_nothing_until_a_launch(lib):
+    """Turning the per-launch timing on and off, and reading it with no launch
+    recorded, touch no device."""
+    from paper_2002_09049_amd import mpq
+    assert lib.mpq_timing_enable(1) == 0
+    assert lib.mpq_timing_read(None, 0) == 0
+    assert lib.mpq_timing_read(None, -1) == mpq.MPQ_ERR_INVALID_ARG
+    assert lib.mpq_timing_enable(0) == 0
+    assert mpq.timing_read() == []
+    assert lib.mpq_fit_kernel_of(0, 4, 8, 1, ctypes.create_string_buffer(64), 64) == mpq.MPQ_ERR_INVALID_ARG
+
+
+def test_kernel_time_struct_matches_header(tmp_path):
+    import subprocess
+    from paper_2002_09049_amd import mpq
+    src = tmp_path / "kt.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "mpq.h"\nint main(void){\n'
+                   '  printf("%zu %zu %zu\\n", sizeof(mpq_kernel_time), offsetof(mpq_kernel_time, name),'
+                   ' offsetof(mpq_kernel_time, ms));\n  return 0;\n}\n')
+    exe = tmp_path / "kt"
+    subprocess.check_call(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)])
+    out = [int(x) for x in subprocess.check_output([str(exe)]).split()]
+    assert out == [ctypes.sizeof(mpq.KernelTime), mpq.KernelTime.name.offset, mpq.KernelTime.ms.offset]
