@@ -2,9 +2,10 @@
 """Throughput of the multipoint-quantization hot path on one MI355X.
 
 One step = the whole path over one synthetic workload already resident in
-HBM: for every layer, the greedy fit (mpq_fit_layers), the output error on
-the layer's calibration batch (mpq_output_error_layers) and the
-reconstruction (mpq_reconstruct_layers).  The default workload is the
+HBM: for every layer, the greedy fit, the output error on the layer's
+calibration batch and the reconstruction, in one mpq_quantize_layers call
+(--separate: mpq_fit_layers, mpq_output_error_layers, mpq_reconstruct_layers
+in turn, with the time of each stage).  The default workload is the
 ResNet-18-shaped stack (21 layers, 5,800 channels, 4 bits, up to 4 points,
 256 candidate scales, tol 1e-3, 1,024 calibration columns).
 
@@ -50,7 +51,10 @@ def parse():
                     help="cpu_baseline fits every n-th channel of every layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--dense", action="store_true",
-                    help="fit with mpq_fit_layer_dense (O(d G) search) instead of mpq_fit_layer")
+                    help="fit with mpq_fit_layer_dense (O(d G) search) instead of mpq_fit_layer "
+                         "(implies --separate)")
+    ap.add_argument("--separate", action="store_true",
+                    help="the three batched calls in turn instead of mpq_quantize_layers")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the HBM-traffic summary of two rocprofv3 --pmc runs "
                          "(FETCH_SIZE, WRITE_SIZE) of `bench.py --steps 1 --warmup 1 "
@@ -61,6 +65,9 @@ def parse():
     ap.add_argument("--bench-json", metavar="FILE",
                     help="with --summarize-trace: the bench.py line of an untraced run of the "
                          "same build, compared kernel by kernel")
+    ap.add_argument("--traced-steps", type=int, default=None,
+                    help="with --summarize-*: steps the traced process ran (warm-up + timed; "
+                         "default 2 for --summarize-pmc, 6 for --summarize-trace)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before the steps, copy a 256 MiB device buffer once (a kernel of known "
                          "traffic, to scale the FETCH_SIZE / WRITE_SIZE counters)")
@@ -96,7 +103,7 @@ def stage_of(key):
     return None
 
 
-def summarize_pmc(fetch_dir, write_dir):
+def summarize_pmc(fetch_dir, write_dir, steps=2):
     """HBM bytes per step and kernel from the FETCH_SIZE / WRITE_SIZE counters,
     each scaled so that the 256 MiB calibration copy reads / writes 256 MiB."""
     import csv
@@ -121,7 +128,6 @@ def summarize_pmc(fetch_dir, write_dir):
 
     ff, fetch, launches = per_kernel(fetch_dir)
     wf, write, _ = per_kernel(write_dir)
-    steps = max(launches.get("gemm_err_kernel", 1), 1)
     lines = ["# HBM traffic per step and kernel: ResNet-18-shaped workload", "",
              "Two rocprofv3 counter runs (one counter each), from the repository root:", "",
              "```",
@@ -159,7 +165,7 @@ def measured_traffic(key):
     return None
 
 
-def summarize_trace(trace_dir, bench_json=None):
+def summarize_trace(trace_dir, bench_json=None, steps=6):
     """Per-kernel average duration of a traced bench run (kernel_stats.csv of
     rocprofv3 --stats), beside the event-timed averages of a bench.py line."""
     import csv
@@ -177,7 +183,6 @@ def summarize_trace(trace_dir, bench_json=None):
         a = agg.setdefault(k, [0, 0.0])
         a[0] += int(r["Calls"])
         a[1] += float(r["TotalDurationNs"])
-    steps = max(agg.get("gemm_err_kernel", [1])[0], 1)
     bench = json.load(open(bench_json)) if bench_json else None
     lines = ["# rocprofv3 kernel summary: ResNet-18-shaped workload, bench step", "",
              "Workload: 21 layers (5,800 channels, 11,678,912 weights), 4 bits, up to 4 points,",
@@ -211,10 +216,10 @@ def summarize_trace(trace_dir, bench_json=None):
 def main():
     args = parse()
     if args.summarize_pmc:
-        summarize_pmc(*args.summarize_pmc)
+        summarize_pmc(*args.summarize_pmc, steps=args.traced_steps or 2)
         return 0
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace, args.bench_json)
+        summarize_trace(args.summarize_trace, args.bench_json, steps=args.traced_steps or 6)
         return 0
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -246,7 +251,12 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    separate = args.separate or args.dense
+
     def step(ev=None):
+        if not separate:
+            ls.quantize(wk.bits, wk.n_grid, wk.tol)
+            return
         if ev: ev[0].record(stream)
         if args.dense:
             for i, W in enumerate(Ws):
@@ -337,8 +347,9 @@ def main():
         k["hbm_bytes_per_launch_measured"] = measured_traffic(name)
         kernels[name] = k
     stages = {}
-    for i, st in enumerate(("fit", "output_error", "reconstruct")):
-        stages[st] = sum(e[i].elapsed_time(e[i + 1]) for e in ev) / steps
+    if separate:
+        for i, st in enumerate(("fit", "output_error", "reconstruct")):
+            stages[st] = sum(e[i].elapsed_time(e[i + 1]) for e in ev) / steps
     dom = max((k for k in kernels if "achieved" in kernels[k]), key=lambda k: kernels[k]["us_per_step"])
     K = kernels[dom]
     roofline = {"kernel": dom, "bound": K["bound"], "achieved": round(K["achieved"], 4),
@@ -367,9 +378,10 @@ def main():
                    "weights": wk.weights, "bits": wk.bits, "max_points": wk.max_points,
                    "n_grid": wk.n_grid, "tol": wk.tol, "calib_columns": wk.n_calib,
                    "points_per_step": points, "search": "dense" if args.dense else "histogram",
+                   "calls": "separate" if separate else "mpq_quantize_layers",
                    "parallelism": "none"},
         "roofline": roofline,
-        "stages_ms_per_step": {k: round(v, 5) for k, v in stages.items()},
+        "stages_ms_per_step": {k: round(v, 5) for k, v in stages.items()} or None,
         "kernels": {k: {kk: (round(vv, 5) if isinstance(vv, float) else vv) for kk, vv in v.items()}
                     for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["us_per_step"])},
         "wall_s_timed": round(wall, 3),

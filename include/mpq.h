@@ -197,6 +197,22 @@ int mpq_output_error_layers(const mpq_layer *layers, int n_layers, int max_point
 int mpq_reconstruct_layers(const mpq_layer *layers, int n_layers, int max_points, void *stream);
 
 /*
+ * mpq_quantize_layers - the whole path for a network in one call: the fit of
+ * every layer (mpq_fit_layers), then, for each layer with out_err != NULL,
+ * its output error (Eq. (12), as mpq_output_error_layers; X, n, out_err and
+ * out_ref are read) and, for each layer with W_hat != NULL, its quantized
+ * weights (Eq. (4), as mpq_reconstruct_layers).  The outputs are bitwise
+ * those of the three batched calls made in that order on the same stream.
+ * The fit launches run side by side (as in mpq_fit_layers); then the output
+ * errors of all layers run as one batch while the reconstruction runs beside
+ * them, on the caller's stream and a library-owned stream joined back to it.
+ * Arguments as for mpq_fit_layers; every layer is checked before anything is
+ * enqueued.
+ */
+int mpq_quantize_layers(const mpq_layer *layers, int n_layers, int bits, int max_points,
+                        const float *grid_host, int n_grid, float tol, void *stream);
+
+/*
  * Per-launch timing (instrumentation, not part of the method).  While it is
  * enabled, every kernel launch of the library is bracketed by two HIP events
  * recorded on the stream the kernel runs on (a call may run independent

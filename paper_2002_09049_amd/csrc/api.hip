@@ -232,63 +232,34 @@ int64_t dense_max_dim(int n_grid, size_t lim)
 
 enum class Search { kAuto, kDense };
 
-int fit_layers_impl(Search mode, const mpq_layer *layers, int n_layers, int bits, int max_points,
-                    const float *grid_host, int n_grid, float tol, void *stream)
+// One fit launch: a dense-search layer, or the histogram-search layers of one
+// kernel variant (up to kMaxBatchLayers), with the indices of its layers.
+struct FitJob {
+    bool dense;
+    int variant;
+    int64_t channels;
+    mpq::FitParams p;
+    mpq::HistBatch b;
+    std::vector<int> layers;
+    double work;   // ~ sum of c_out * d (dense: times n_grid)
+};
+
+// The fit launches of a set of layers: one per dense-search layer, one per
+// histogram variant and kMaxBatchLayers layers; a histogram layer with at
+// least own_launch_weights weights gets a launch of its own (< 0: never).
+// Batching does not change any channel's result.
+std::vector<FitJob> build_fit_jobs(Search mode, bool hist_fits, const mpq_layer *layers, int n_layers,
+                                   int M, int max_points, const float *dgrid, int n_grid, float tol,
+                                   double own_launch_weights)
 {
-    if (n_layers < 0 || (n_layers > 0 && !layers))
-        return fail(MPQ_ERR_INVALID_ARG, "layers must hold n_layers >= 0 entries");
-    int rc = check_fit_args(bits, max_points, grid_host, n_grid, tol);
-    if (rc != MPQ_OK) return rc;
-    bool any = false;
-    for (int l = 0; l < n_layers; ++l) {
-        const mpq_layer &L = layers[l];
-        rc = check_fit_layer(L.W, L.c_out, L.d, L.codes, L.scales, L.counts);
-        if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
-        any = any || L.c_out > 0;
-    }
-    if (!any) return MPQ_OK;
-    size_t lim = 0;
-    rc = device_lds_limit(&lim);
-    if (rc != MPQ_OK) return rc;
-    // which layers take the histogram search (and which variant)
-    const bool hist_fits = mpq::fit_hist_lds(n_grid) <= lim;
-    for (int l = 0; l < n_layers; ++l) {
-        const mpq_layer &L = layers[l];
-        if (L.c_out == 0) continue;
-        const bool hist = mode == Search::kAuto && hist_fits && mpq::fit_hist_supports(L.d);
-        if (!hist && mpq::fit_layout(L.d, n_grid).lds > lim)
-            return fail(MPQ_ERR_SHAPE, "%sd = %lld with n_grid = %d needs %zu bytes of LDS (limit %zu)",
-                        n_layers > 1 ? "a layer's " : "", (long long)L.d, n_grid,
-                        mpq::fit_layout(L.d, n_grid).lds, lim);
-    }
-    hipStream_t s = (hipStream_t)stream;
-    float *dgrid = nullptr;
-    if (grid_host) {
-        hipError_t e = mpq::scratch_alloc((void **)&dgrid, sizeof(float) * (size_t)n_grid, s);
-        if (e != hipSuccess) return fail(MPQ_ERR_NOMEM, "grid upload: %s", hipGetErrorString(e));
-        e = hipMemcpyAsync(dgrid, grid_host, sizeof(float) * (size_t)n_grid, hipMemcpyHostToDevice, s);
-        if (e != hipSuccess) {
-            (void)mpq::scratch_free(dgrid, s);
-            return hip_fail(e, "hipMemcpyAsync(grid)");
-        }
-    }
-    const int M = (1 << (bits - 1)) - 1;
-    // independent launches: one per dense-search layer, one per histogram
-    // kernel variant (and per kMaxBatchLayers layers); they run side by side
-    struct Job {
-        bool dense;
-        int variant;
-        int64_t channels;
-        mpq::FitParams p;
-        mpq::HistBatch b;
+    std::vector<FitJob> jobs;
+    auto hist = [&](const mpq_layer &L) {
+        return mode == Search::kAuto && hist_fits && mpq::fit_hist_supports(L.d);
     };
-    std::vector<Job> jobs;
-    std::vector<double> work;   // ~ sum of c_out * d
     for (int l = 0; l < n_layers; ++l) {
         const mpq_layer &L = layers[l];
-        if (L.c_out == 0) continue;
-        if (mode == Search::kAuto && hist_fits && mpq::fit_hist_supports(L.d)) continue;
-        Job j = {};
+        if (L.c_out == 0 || hist(L)) continue;
+        FitJob j = {};
         j.dense = true;
         mpq::FitParams &p = j.p;
         p.W = L.W;
@@ -303,51 +274,138 @@ int fit_layers_impl(Search mode, const mpq_layer *layers, int n_layers, int bits
         p.scales = L.scales;
         p.counts = L.counts;
         p.err = L.fit_err;
-        jobs.push_back(j);
+        j.layers.push_back(l);
         // the dense search evaluates every candidate: weigh it by G
-        work.push_back((double)L.c_out * (double)L.d * (double)n_grid);
+        j.work = (double)L.c_out * (double)L.d * (double)n_grid;
+        jobs.push_back(j);
     }
-    if (mode == Search::kAuto && hist_fits) {
-        for (int v = 0; v <= mpq::hist_variant(mpq::kHistMaxDim); ++v) {
-            Job j = {};
-            j.variant = v;
-            mpq::HistBatch &b = j.b;
-            b.M = M;
-            b.P = max_points;
-            b.G = n_grid;
-            b.grid = dgrid;
-            b.tol = (double)tol;
-            double w = 0.0;
-            for (int l = 0; l <= n_layers; ++l) {
-                const bool flush = l == n_layers || b.n_layers == mpq::kMaxBatchLayers ||
-                                   j.channels + (l < n_layers ? layers[l].c_out : 0) > 0x7fffffffLL;
-                if (flush && b.n_layers > 0) {
-                    jobs.push_back(j);
-                    work.push_back(w);
-                    b.n_layers = 0;
-                    j.channels = 0;
-                    w = 0.0;
-                }
-                if (l == n_layers) break;
-                const mpq_layer &L = layers[l];
-                if (L.c_out == 0 || !mpq::fit_hist_supports(L.d) || mpq::hist_variant(L.d) != v) continue;
-                mpq::HistLayer &H = b.L[b.n_layers++];
-                H.W = L.W;
-                H.codes = L.codes;
-                H.scales = L.scales;
-                H.counts = L.counts;
-                H.err = L.fit_err;
-                H.d = (int)L.d;
-                H.c_begin = (int)j.channels;
-                j.channels += L.c_out;
-                w += (double)L.c_out * (double)L.d;
+    auto own = [&](const mpq_layer &L) {
+        return own_launch_weights >= 0.0 && (double)L.c_out * (double)L.d >= own_launch_weights;
+    };
+    auto fresh = [&](int v) {
+        FitJob j = {};
+        j.variant = v;
+        j.b.M = M;
+        j.b.P = max_points;
+        j.b.G = n_grid;
+        j.b.grid = dgrid;
+        j.b.tol = (double)tol;
+        return j;
+    };
+    auto add_layer = [&](FitJob &j, int l) {
+        const mpq_layer &L = layers[l];
+        mpq::HistLayer &H = j.b.L[j.b.n_layers++];
+        H.W = L.W;
+        H.codes = L.codes;
+        H.scales = L.scales;
+        H.counts = L.counts;
+        H.err = L.fit_err;
+        H.d = (int)L.d;
+        H.c_begin = (int)j.channels;
+        j.channels += L.c_out;
+        j.work += (double)L.c_out * (double)L.d;
+        j.layers.push_back(l);
+    };
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_layer &L = layers[l];
+        if (L.c_out == 0 || !hist(L) || !own(L)) continue;
+        FitJob j = fresh(mpq::hist_variant(L.d));
+        add_layer(j, l);
+        jobs.push_back(j);
+    }
+    for (int v = 0; v <= mpq::hist_variant(mpq::kHistMaxDim); ++v) {
+        FitJob j = fresh(v);
+        for (int l = 0; l <= n_layers; ++l) {
+            const bool flush = l == n_layers || j.b.n_layers == mpq::kMaxBatchLayers ||
+                               j.channels + (l < n_layers ? layers[l].c_out : 0) > 0x7fffffffLL;
+            if (flush && j.b.n_layers > 0) {
+                jobs.push_back(j);
+                j = fresh(v);
             }
+            if (l == n_layers) break;
+            const mpq_layer &L = layers[l];
+            if (L.c_out == 0 || !hist(L) || own(L) || mpq::hist_variant(L.d) != v) continue;
+            add_layer(j, l);
         }
     }
+    return jobs;
+}
+
+hipError_t launch_fit_job(const FitJob &j, int n_grid, hipStream_t st)
+{
+    return j.dense ? mpq::launch_fit(j.p, mpq::fit_layout(j.p.d, n_grid), st)
+                   : mpq::launch_fit_hist(j.b, j.variant, j.channels, st);
+}
+
+// Checks shared by the calls that fit: arguments, every layer's buffers, and
+// that every layer fits a search kernel (*hist_fits: the histogram search's
+// LDS fits the device).  *any: some layer has channels.
+int fit_checks(Search mode, const mpq_layer *layers, int n_layers, int bits, int max_points,
+               const float *grid_host, int n_grid, float tol, bool *any, bool *hist_fits)
+{
+    if (n_layers < 0 || (n_layers > 0 && !layers))
+        return fail(MPQ_ERR_INVALID_ARG, "layers must hold n_layers >= 0 entries");
+    int rc = check_fit_args(bits, max_points, grid_host, n_grid, tol);
+    if (rc != MPQ_OK) return rc;
+    *any = false;
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_layer &L = layers[l];
+        rc = check_fit_layer(L.W, L.c_out, L.d, L.codes, L.scales, L.counts);
+        if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
+        *any = *any || L.c_out > 0;
+    }
+    if (!*any) return MPQ_OK;
+    size_t lim = 0;
+    rc = device_lds_limit(&lim);
+    if (rc != MPQ_OK) return rc;
+    // which layers take the histogram search (and which variant)
+    *hist_fits = mpq::fit_hist_lds(n_grid) <= lim;
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_layer &L = layers[l];
+        if (L.c_out == 0) continue;
+        const bool hist = mode == Search::kAuto && *hist_fits && mpq::fit_hist_supports(L.d);
+        if (!hist && mpq::fit_layout(L.d, n_grid).lds > lim)
+            return fail(MPQ_ERR_SHAPE, "%sd = %lld with n_grid = %d needs %zu bytes of LDS (limit %zu)",
+                        n_layers > 1 ? "a layer's " : "", (long long)L.d, n_grid,
+                        mpq::fit_layout(L.d, n_grid).lds, lim);
+    }
+    return MPQ_OK;
+}
+
+// A caller's grid, copied to stream-ordered scratch (NULL: the default grid).
+int upload_grid(const float *grid_host, int n_grid, hipStream_t s, float **dgrid)
+{
+    *dgrid = nullptr;
+    if (!grid_host) return MPQ_OK;
+    hipError_t e = mpq::scratch_alloc((void **)dgrid, sizeof(float) * (size_t)n_grid, s);
+    if (e != hipSuccess) return fail(MPQ_ERR_NOMEM, "grid upload: %s", hipGetErrorString(e));
+    e = hipMemcpyAsync(*dgrid, grid_host, sizeof(float) * (size_t)n_grid, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) {
+        (void)mpq::scratch_free(*dgrid, s);
+        *dgrid = nullptr;
+        return hip_fail(e, "hipMemcpyAsync(grid)");
+    }
+    return MPQ_OK;
+}
+
+int fit_layers_impl(Search mode, const mpq_layer *layers, int n_layers, int bits, int max_points,
+                    const float *grid_host, int n_grid, float tol, void *stream)
+{
+    bool any = false, hist_fits = false;
+    int rc = fit_checks(mode, layers, n_layers, bits, max_points, grid_host, n_grid, tol, &any,
+                        &hist_fits);
+    if (rc != MPQ_OK || !any) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    float *dgrid = nullptr;
+    rc = upload_grid(grid_host, n_grid, s, &dgrid);
+    if (rc != MPQ_OK) return rc;
+    const int M = (1 << (bits - 1)) - 1;
+    const std::vector<FitJob> jobs = build_fit_jobs(mode, hist_fits, layers, n_layers, M, max_points,
+                                                    dgrid, n_grid, tol, -1.0);
+    std::vector<double> work;
+    for (const FitJob &j : jobs) work.push_back(j.work);
     const hipError_t e = run_concurrently(s, work, [&](int i, hipStream_t st) {
-        const Job &j = jobs[i];
-        return j.dense ? mpq::launch_fit(j.p, mpq::fit_layout(j.p.d, n_grid), st)
-                       : mpq::launch_fit_hist(j.b, j.variant, j.channels, st);
+        return launch_fit_job(jobs[i], n_grid, st);
     });
     if (dgrid) (void)mpq::scratch_free(dgrid, s);
     if (e != hipSuccess) return hip_fail(e, "fit kernel launch");
@@ -436,6 +494,83 @@ int reconstruct_impl(const mpq_layer *layers, int n_layers, int max_points, void
     return MPQ_OK;
 }
 
+int quantize_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
+                  const float *grid_host, int n_grid, float tol, void *stream)
+{
+    if (n_layers < 0 || (n_layers > 0 && !layers))
+        return fail(MPQ_ERR_INVALID_ARG, "layers must hold n_layers >= 0 entries");
+    // the output-error and reconstruction fields first: fit_checks ends with
+    // a device query, and no check may follow a HIP call
+    int rc = MPQ_OK;
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_layer &L = layers[l];
+        if (L.out_err) rc = check_error_layer(L, max_points, true);
+        if (rc == MPQ_OK && L.W_hat) rc = check_error_layer(L, max_points, false);
+        if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
+    }
+    bool any = false, hist_fits = false;
+    rc = fit_checks(Search::kAuto, layers, n_layers, bits, max_points, grid_host, n_grid, tol, &any,
+                    &hist_fits);
+    if (rc != MPQ_OK || !any) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    float *dgrid = nullptr;
+    rc = upload_grid(grid_host, n_grid, s, &dgrid);
+    if (rc != MPQ_OK) return rc;
+    const int M = (1 << (bits - 1)) - 1;
+    // 1. every fit, side by side (as mpq_fit_layers)
+    const std::vector<FitJob> jobs = build_fit_jobs(Search::kAuto, hist_fits, layers, n_layers, M,
+                                                    max_points, dgrid, n_grid, tol, -1.0);
+    std::vector<double> work;
+    for (const FitJob &j : jobs) work.push_back(j.work);
+    hipError_t e = run_concurrently(s, work, [&](int i, hipStream_t st) {
+        return launch_fit_job(jobs[i], n_grid, st);
+    });
+    if (dgrid) (void)mpq::scratch_free(dgrid, s);
+    if (e != hipSuccess) return hip_fail(e, "fit kernel launch");
+    // 2. the output error of every layer that asks for it, in one batch (its
+    // GEMM fills the device only with all layers' tiles together), and beside
+    // it the reconstruction: both only read the fit's outputs
+    std::vector<mpq::ErrLayerIn> err;
+    std::vector<mpq::RecLayer> rec;
+    double flop = 0.0, bytes = 0.0;
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_layer &L = layers[l];
+        if (L.c_out == 0) continue;
+        if (L.out_err) {
+            err.push_back(mpq::ErrLayerIn{L.W, L.codes, L.scales, L.counts, L.X, L.out_err, L.out_ref,
+                                          L.c_out, L.d, L.n});
+            flop += 2.0 * (double)L.c_out * (double)L.d * (double)L.n;
+        }
+        if (L.W_hat) {
+            rec.push_back(mpq::RecLayer{L.codes, L.scales, L.counts, L.W_hat, L.c_out, L.d});
+            bytes += 5.0 * (double)L.c_out * (double)L.d;
+        }
+    }
+    void *scratch = nullptr;
+    if (!err.empty()) {
+        const size_t nb = mpq::err_scratch_bytes(err.data(), (int)err.size());
+        e = mpq::scratch_alloc(&scratch, nb, s);
+        if (e != hipSuccess) return fail(MPQ_ERR_NOMEM, "scratch of %zu bytes: %s", nb, hipGetErrorString(e));
+    }
+    std::vector<double> w2;
+    std::vector<int> kind;
+    if (!err.empty()) {
+        w2.push_back(flop);   // run_concurrently puts the larger job on the caller's stream
+        kind.push_back(0);
+    }
+    if (!rec.empty()) {
+        w2.push_back(bytes);
+        kind.push_back(1);
+    }
+    e = run_concurrently(s, w2, [&](int i, hipStream_t st) {
+        return kind[i] == 0 ? mpq::launch_output_error(err.data(), (int)err.size(), max_points, scratch, st)
+                            : mpq::launch_reconstruct(rec.data(), (int)rec.size(), max_points, st);
+    });
+    if (scratch) (void)mpq::scratch_free(scratch, s);
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    return MPQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -490,6 +625,12 @@ int mpq_fit_layers(const mpq_layer *layers, int n_layers, int bits, int max_poin
 {
     return fit_layers_impl(Search::kAuto, layers, n_layers, bits, max_points, grid_host, n_grid,
                            tol, stream);
+}
+
+int mpq_quantize_layers(const mpq_layer *layers, int n_layers, int bits, int max_points,
+                        const float *grid_host, int n_grid, float tol, void *stream)
+{
+    return quantize_impl(layers, n_layers, bits, max_points, grid_host, n_grid, tol, stream);
 }
 
 int mpq_output_error(const float *W, const int8_t *codes, const float *scales,

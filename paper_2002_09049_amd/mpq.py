@@ -31,7 +31,7 @@ MAX_GRID = 4096
 EXPORTS = ("mpq_fit_layer", "mpq_fit_layer_dense", "mpq_fit_layers", "mpq_fit_max_dim",
            "mpq_output_error", "mpq_output_error_layers", "mpq_reconstruct",
            "mpq_reconstruct_layers", "mpq_last_error", "mpq_timing_enable", "mpq_timing_read",
-           "mpq_fit_kernel_of")
+           "mpq_fit_kernel_of", "mpq_quantize_layers")
 
 
 class Layer(ctypes.Structure):
@@ -76,6 +76,8 @@ def load(path: str = LIB_PATH):
     lib.mpq_reconstruct.restype = i32
     lib.mpq_fit_layers.argtypes = [P, i32, i32, i32, P, i32, f32, P]
     lib.mpq_fit_layers.restype = i32
+    lib.mpq_quantize_layers.argtypes = [P, i32, i32, i32, P, i32, f32, P]
+    lib.mpq_quantize_layers.restype = i32
     lib.mpq_output_error_layers.argtypes = [P, i32, i32, P]
     lib.mpq_output_error_layers.restype = i32
     lib.mpq_reconstruct_layers.argtypes = [P, i32, i32, P]
@@ -271,21 +273,34 @@ class LayerSet:
                     raise ValueError(f"calib[{i}] must be [d, n]")
                 L.X = _dev(X, torch.float32, "X")
                 L.n = X.shape[1]
-            L.out_err = err.data_ptr()
+            L.out_err = err.data_ptr() if self.X is not None else None
             L.out_ref = None if ref is None else ref.data_ptr()
             L.W_hat = what.data_ptr()
         self.n = n
 
+    @staticmethod
+    def _grid(grid, n_grid):
+        if grid is None:
+            return None
+        import numpy as np
+        g = np.ascontiguousarray(grid, dtype=np.float32)
+        if g.shape != (n_grid,):
+            raise ValueError("grid must have n_grid entries")
+        return g
+
     def fit(self, bits: int, n_grid: int, tol: float, grid=None, stream=None):
-        g = None
-        if grid is not None:
-            import numpy as np
-            g = np.ascontiguousarray(grid, dtype=np.float32)
-            if g.shape != (n_grid,):
-                raise ValueError("grid must have n_grid entries")
+        g = self._grid(grid, n_grid)
         _check(load().mpq_fit_layers(ctypes.addressof(self.arr), self.n, bits, self.max_points,
                                      None if g is None else g.ctypes.data_as(ctypes.c_void_p),
                                      n_grid, float(tol), _stream(stream)))
+
+    def quantize(self, bits: int, n_grid: int, tol: float, grid=None, stream=None):
+        """mpq_quantize_layers: fit, output error (when calibration batches
+        were given) and reconstruction of every layer in one call."""
+        g = self._grid(grid, n_grid)
+        _check(load().mpq_quantize_layers(ctypes.addressof(self.arr), self.n, bits, self.max_points,
+                                          None if g is None else g.ctypes.data_as(ctypes.c_void_p),
+                                          n_grid, float(tol), _stream(stream)))
 
     def output_error(self, stream=None):
         if self.X is None:

@@ -178,3 +178,26 @@ def test_kernel_time_struct_matches_header(tmp_path):
     subprocess.check_call(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)])
     out = [int(x) for x in subprocess.check_output([str(exe)]).split()]
     assert out == [ctypes.sizeof(mpq.KernelTime), mpq.KernelTime.name.offset, mpq.KernelTime.ms.offset]
+
+
+def test_quantize_layers_checks_every_layer_first(lib):
+    from paper_2002_09049_amd import mpq
+    E = mpq.MPQ_ERR_INVALID_ARG
+    arr = (mpq.Layer * 2)()
+    for L in arr:
+        L.W, L.c_out, L.d, L.codes, L.scales, L.counts = 1, 4, 16, 1, 1, 1
+        L.X, L.n, L.out_err, L.W_hat = 1, 8, 1, 1
+    p = ctypes.addressof(arr)
+    q = lib.mpq_quantize_layers
+    assert q(p, 2, 9, 4, None, 8, 1e-3, None) == E
+    arr[1].n = 0            # an output-error layer without calibration columns
+    assert q(p, 2, 4, 4, None, 8, 1e-3, None) == E
+    assert b"layer 1" in lib.mpq_last_error()
+    arr[1].out_err = None   # ... is fine once it asks for no output error
+    arr[0].W_hat = None     # and a layer may skip the reconstruction
+    arr[0].codes = None
+    assert q(p, 2, 4, 4, None, 8, 1e-3, None) == E
+    assert b"layer 0" in lib.mpq_last_error()
+    for L in arr:
+        L.c_out = 0
+    assert q(p, 2, 4, 4, None, 8, 1e-3, None) == 0

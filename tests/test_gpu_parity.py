@@ -366,3 +366,42 @@ def test_batched_fit_many_layers_one_variant(orc):
         out = (ls.codes[i].cpu().numpy(), ls.scales[i].cpu().numpy(), ls.counts[i].cpu().numpy(),
                ls.fit_err[i].cpu().numpy())
         assert_parity(orc, W, 4, 4, 64, 1e-3, out)
+
+
+@pytest.mark.parametrize("name", ["resnet18", "mobilenetv2"])
+def test_quantize_layers_equals_the_three_calls(name):
+    """mpq_quantize_layers (fit, output error and reconstruction as chains on
+    several streams) gives bitwise the outputs of mpq_fit_layers,
+    mpq_output_error_layers and mpq_reconstruct_layers; a layer without
+    out_err or W_hat is left untouched there."""
+    import torch
+    from paper_2002_09049_amd import mpq
+    w = wl.get(name)
+    idx = list(range(len(w.layers)))[:24]
+    Ws = [to_dev(wl.layer_weights(w, i)) for i in idx]
+    Xs = [to_dev(wl.layer_calib(w, i, n=256)) for i in idx]
+    say(f"case quantize_layers {name} ({len(idx)} layers)")
+    ref = mpq.LayerSet(Ws, w.max_points, calib=Xs, with_ref=True)
+    ref.fit(w.bits, w.n_grid, w.tol)
+    ref.output_error()
+    ref.reconstruct()
+    q = mpq.LayerSet(Ws, w.max_points, calib=Xs, with_ref=True)
+    for t in q.err + q.W_hat:
+        t.fill_(-7.0)
+    q.arr[1].out_err = None
+    q.arr[1].out_ref = None
+    q.arr[2].W_hat = None
+    q.quantize(w.bits, w.n_grid, w.tol)
+    torch.cuda.synchronize()
+    for j in range(len(idx)):
+        for a, b in ((ref.codes, q.codes), (ref.scales, q.scales), (ref.counts, q.counts),
+                     (ref.fit_err, q.fit_err)):
+            assert torch.equal(a[j], b[j]), j
+        if j == 1:
+            assert (q.err[j] == -7.0).all()
+        else:
+            assert torch.equal(ref.err[j], q.err[j]) and torch.equal(ref.ref[j], q.ref[j]), j
+        if j == 2:
+            assert (q.W_hat[j] == -7.0).all()
+        else:
+            assert torch.equal(ref.W_hat[j], q.W_hat[j]), j
