@@ -151,6 +151,38 @@ __device__ __forceinline__ void bin_levels(const double (&r)[EPT], const HistSha
     }
 }
 
+// The per-level histogram of bin_levels, element-major: for the variant that
+// rebuilds each residual element from memory, so that an element is rebuilt
+// once per step rather than once per level.
+template <int T, int EPT, bool kLinear, class Res>
+__device__ __forceinline__ void bin_levels_elementwise(Res r, const HistShared &S, int G, int M, int d,
+                                                       float m, int sh, unsigned long long &fullA,
+                                                       int &fullB)
+{
+    const float gm = (float)G * (float)M / m;
+    for (int u = 0; u < EPT; ++u) {
+        if (T * u >= d) break;
+        const double x = fabs(r(u));
+        const unsigned long long X = (unsigned long long)rint(ldexp(x, sh));
+        const float base = (float)x * gm;
+        for (int kk = 0; kk < M; ++kk) {
+            const double h = (double)kk + 0.5;
+            int nb;
+            if constexpr (kLinear) nb = count_linear(S.af, G, h, x, base * __builtin_amdgcn_rcpf((float)h));
+            else nb = count_bsearch(S.ad, G, h, x);
+            if (nb == 0) break;   // higher levels have higher boundaries
+            const int inc = 2 * kk + 1;
+            if (nb == G) {
+                fullA += X;
+                fullB += inc;
+            } else {
+                atomicAdd((unsigned long long *)&S.ha[nb - 1], X);
+                atomicAdd(&S.hb[nb - 1], inc);
+            }
+        }
+    }
+}
+
 // Lattice-mode binning of this thread's elements (see the header).  inv =
 // 1 / u in fp64; Lmax = nlat - 1 is the largest lattice point of a boundary;
 // scale = 2^sh.
@@ -161,15 +193,15 @@ __device__ __forceinline__ void bin_levels(const double (&r)[EPT], const HistSha
 // one fma: x 2^sh + 2^52 + 2^kLatShift rounds x 2^sh to the nearest integer
 // (ties to even, as rint) and its low 52 bits are that integer plus the count
 // bit.
-template <int T, int EPT>
-__device__ __forceinline__ void bin_lattice(const double (&r)[EPT], const HistShared &S, int G, int M,
-                                            int d, int Lmax, double inv, double delta, double scale)
+template <int T, int EPT, int kUnroll, class Res>
+__device__ __forceinline__ void bin_lattice(Res r, const HistShared &S, int G, int M, int d, int Lmax,
+                                            double inv, double delta, double scale)
 {
     constexpr double kBias = 0x1p52 + (double)kLatOne;
-#pragma unroll
+#pragma unroll(kUnroll)
     for (int u = 0; u < EPT; ++u) {
         if (T * u >= d) continue;   // a slot past the channel end in every thread
-        const double x = fabs(r[u]);
+        const double x = fabs(r(u));
         const double z = fma(x, inv, delta);
         const double F = floor(z);
         const bool near = z - F <= 2.0 * delta;
@@ -235,15 +267,22 @@ __device__ __forceinline__ void block_suffix_sums(unsigned long long *h, int n,
 }
 
 // at most 128 VGPRs (four wavefronts per SIMD) unless the residual alone
-// needs more
-template <int EPT>
-constexpr int hist_waves_per_simd() { return EPT >= 32 ? 2 : 4; }
+// needs more; a workgroup of 1024 threads needs four per SIMD
+template <int T, int EPT, bool kGlobal>
+constexpr int hist_waves_per_simd() { return (EPT >= 32 && !kGlobal && T <= 512) ? 2 : 4; }
 
-template <int T, int EPT, bool kLinear, bool kLat>
-__global__ void __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(hist_waves_per_simd<EPT>())))
+// kGlobal: the residual is not held in registers; each phase rebuilds
+// element j as fl64 w_j - sum_{p<i} a_p q_pj from the weights, the codes this
+// workgroup already wrote and the scales kept in LDS, with the same fp64
+// operations in the same order as the register variants (so bitwise the same
+// value), for channels longer than the registers of a workgroup hold.
+template <int T, int EPT, bool kLinear, bool kLat, bool kGlobal>
+__global__ void __launch_bounds__(T)
+__attribute__((amdgpu_waves_per_eu(hist_waves_per_simd<T, EPT, kGlobal>())))
 fit_hist_kernel(const HistBatch B)
 {
     constexpr int kWaves = T / kWave;
+    constexpr int kUnroll = kGlobal ? 1 : EPT;   // the rebuilt residual is not an array
     extern __shared__ __align__(16) double hsmem[];
     __shared__ float s_redf[kWaves];
     __shared__ double s_redd[kWaves];
@@ -252,6 +291,7 @@ fit_hist_kernel(const HistBatch B)
     __shared__ int s_gbest;
     __shared__ unsigned long long s_scan[kWaves];
     __shared__ ArgMin s_arg[kWaves];
+    __shared__ float s_scale[kGlobal ? MPQ_MAX_POINTS : 1];
 
     // layer of this workgroup (uniform: the descriptors are kernel arguments)
     int li = 0;
@@ -279,12 +319,22 @@ fit_hist_kernel(const HistBatch B)
     int8_t *qk = Ly.codes + k * (int64_t)P * d;
     const float *wk = Ly.W + k * (int64_t)d;
 
-    double r[EPT];
+    double r[kGlobal ? 1 : EPT];
+    if constexpr (!kGlobal) {
 #pragma unroll
-    for (int u = 0; u < EPT; ++u) {
-        const int j = t + T * u;
-        r[u] = j < d ? (double)wk[j] : 0.0;
+        for (int u = 0; u < EPT; ++u) {
+            const int j = t + T * u;
+            r[u] = j < d ? (double)wk[j] : 0.0;
+        }
     }
+    // residual element u of this thread after np points (0 past the channel)
+    auto rebuild = [&](int u, int np) {
+        const int j = t + T * u;
+        if (j >= d) return 0.0;
+        double v = (double)wk[j];
+        for (int p = 0; p < np; ++p) v = fma(-(double)s_scale[p], (double)qk[(int64_t)p * d + j], v);
+        return v;
+    };
 
     for (int g = t; g < G; g += T)
         S.c[g] = B.grid ? B.grid[g] : (float)((double)(g + 1) / (double)G);
@@ -299,23 +349,26 @@ fit_hist_kernel(const HistBatch B)
         int8_t *qrow = qk + (int64_t)(i - 1) * d;
         const double ap = (double)apend;
         const double ia = 1.0 / ap;
-#pragma unroll
+#pragma unroll(kUnroll)
         for (int u = 0; u < EPT; ++u) {
             const int j = t + T * u;
+            if (kGlobal && T * u >= d) break;
+            double ru = kGlobal ? rebuild(u, i >= 1 ? i - 1 : 0) : r[u];
             if (i >= 1 && j < d) {
                 // y is within |y| 2^-51 of the fp64 quotient fl(r / a), so the
                 // two round to the same integer unless y lies within 2^-40 of a
                 // half-integer (or |y| >= 2^10, where both clip to the same M);
                 // only then is the quotient formed
-                const double y = r[u] * ia;
+                const double y = ru * ia;
                 double c = rint(y);
-                if (fabs(fabs(y - c) - 0.5) < 0x1p-40) c = rint(r[u] / ap);
+                if (fabs(fabs(y - c) - 0.5) < 0x1p-40) c = rint(ru / ap);
                 c = fmin(fmax(c, -Md), Md);
                 qrow[j] = (int8_t)(int)c;
-                r[u] = fma(-ap, c, r[u]);
+                ru = fma(-ap, c, ru);
             }
-            lmax = fmaxf(lmax, fabsf((float)r[u]));
-            lsum = fma(r[u], r[u], lsum);
+            if constexpr (!kGlobal) r[u] = ru;
+            lmax = fmaxf(lmax, fabsf((float)ru));
+            lsum = fma(ru, ru, lsum);
         }
         block_max_sum<T>(lmax, lsum, s_redf, s_redd);   // also orders S.c before use
         const float m = lmax;
@@ -363,7 +416,9 @@ fit_hist_kernel(const HistBatch B)
             // ---- lattice buckets, their suffix sums, then every candidate
             const double inv = (double)(2 * G * M) / (double)m;
             const double delta = (double)(2 * G * M) * 0x1p-22;
-            bin_lattice<T, EPT>(r, S, G, M, d, nlat - 1, inv, delta, ldexp(1.0, sh));
+            // residual after the i points so far (kGlobal: rebuilt)
+            auto res = [&](int u) { return kGlobal ? rebuild(u, i) : r[kGlobal ? 0 : u]; };
+            bin_lattice<T, EPT, kUnroll>(res, S, G, M, d, nlat - 1, inv, delta, ldexp(1.0, sh));
             __syncthreads();
             block_suffix_sums<T>(S.lat, nlat, s_scan);
             for (int g = t; g < G; g += T) {
@@ -407,10 +462,17 @@ fit_hist_kernel(const HistBatch B)
             // the closed-form counts need normal candidates and a finite
             // estimate (in a lattice-mode kernel this branch only runs when
             // they do not)
-            if (kLinear && !kLat && m >= 0x1p-100f)
+            if constexpr (kGlobal) {
+                auto res = [&](int u) { return rebuild(u, i); };
+                if (kLinear && !kLat && m >= 0x1p-100f)
+                    bin_levels_elementwise<T, EPT, true>(res, S, G, M, d, m, sh, fullA, fullB);
+                else
+                    bin_levels_elementwise<T, EPT, false>(res, S, G, M, d, m, sh, fullA, fullB);
+            } else if (kLinear && !kLat && m >= 0x1p-100f) {
                 bin_levels<T, EPT, true>(r, S, G, M, m, sh, fullA, fullB);
-            else
+            } else {
                 bin_levels<T, EPT, false>(r, S, G, M, m, sh, fullA, fullB);
+            }
 #pragma unroll
             for (int off = 1; off < kWave; off <<= 1) {
                 fullA += (unsigned long long)__shfl_xor((long long)fullA, off);
@@ -498,12 +560,14 @@ fit_hist_kernel(const HistBatch B)
                 const int g = s_fin[f];
                 const double a = S.ad[g + 1];
                 double le = 0.0;
-#pragma unroll
+#pragma unroll(kUnroll)
                 for (int u = 0; u < EPT; ++u) {
+                    if (kGlobal && T * u >= d) break;
+                    const double ru = kGlobal ? rebuild(u, i) : r[kGlobal ? 0 : u];
                     // signed form: (r - a q)^2 with q = clip(rne(r / a)) equals
                     // (|r| - a |q|)^2, and keeps |r| from being hoisted per element
-                    const double c = fmin(fmax(rint(r[u] / a), -Md), Md);
-                    const double e = r[u] - a * c;
+                    const double c = fmin(fmax(rint(ru / a), -Md), Md);
+                    const double e = ru - a * c;
                     le = fma(e, e, le);
                 }
                 const double E = block_reduce<T>(le, SumOp(), s_redd);
@@ -516,7 +580,10 @@ fit_hist_kernel(const HistBatch B)
             break;
         }
         apend = (float)S.ad[gstar + 1];
-        if (t == 0) Ly.scales[k * P + i] = apend;
+        if (t == 0) {
+            Ly.scales[k * P + i] = apend;
+            if constexpr (kGlobal) s_scale[i] = apend;
+        }
         __syncthreads();   // S.a is rewritten by the next step
     }
 
@@ -529,22 +596,22 @@ fit_hist_kernel(const HistBatch B)
         for (int j = t; j < d; j += T) qk[(int64_t)q * d + j] = 0;
 }
 
-template <int T, int EPT>
+template <int T, int EPT, bool kGlobal = false>
 hipError_t launch_hist_t(const HistBatch &b, int64_t channels, size_t lds, hipStream_t s)
 {
     // the default grid (grid == nullptr) has the closed-form boundary counts
     // and, when its buckets fit, the lattice mode
-    auto kern = b.grid ? fit_hist_kernel<T, EPT, false, false>
-                : b.nlat ? fit_hist_kernel<T, EPT, true, true>
-                         : fit_hist_kernel<T, EPT, true, false>;
+    auto kern = b.grid ? fit_hist_kernel<T, EPT, false, false, kGlobal>
+                : b.nlat ? fit_hist_kernel<T, EPT, true, true, kGlobal>
+                         : fit_hist_kernel<T, EPT, true, false, kGlobal>;
     if (lds > 65536) {
         hipError_t e = hipFuncSetAttribute((const void *)kern,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
     }
     char name[64];
-    snprintf(name, sizeof name, "fit_hist_kernel<%d,%d,%s>", T, EPT,
-             b.grid ? "grid" : b.nlat ? "lattice" : "linear");
+    snprintf(name, sizeof name, "fit_hist_kernel<%d,%d,%s%s>", T, EPT,
+             b.grid ? "grid" : b.nlat ? "lattice" : "linear", kGlobal ? ",rebuilt" : "");
     LaunchTimer timer(s, name);
     hipLaunchKernelGGL(kern, dim3((unsigned)channels), dim3(T), lds, s, b);
     return hipGetLastError();
@@ -557,11 +624,16 @@ hipError_t launch_hist_t(const HistBatch &b, int64_t channels, size_t lds, hipSt
 // arithmetic; the 512- and 1024-thread variants cover lengths whose residual
 // would not fit 128 VGPRs at 256 threads without spilling to scratch (at
 // 256 x 18 the spills moved ~7x the channel's algorithmic bytes through HBM).
+// The last variant (1024 x 32, up to 32768) holds no residual copy: it
+// rebuilds each element from the weights and the codes (kGlobal).
 struct Variant {
     int threads, ept;
+    bool rebuilt;
 };
-constexpr Variant kVariants[] = {{64, 1},  {64, 2},  {64, 4},   {256, 2},  {256, 4},
-                                 {256, 8}, {512, 9}, {1024, 8}, {512, 32}};
+constexpr Variant kVariants[] = {{64, 1, false},   {64, 2, false},   {64, 4, false},
+                                 {256, 2, false},  {256, 4, false},  {256, 8, false},
+                                 {512, 9, false},  {1024, 8, false}, {512, 32, false},
+                                 {1024, 32, true}};
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 static_assert(kVariants[kNumVariants - 1].threads * kVariants[kNumVariants - 1].ept == kHistMaxDim,
               "the last variant covers the longest channels");
@@ -605,8 +677,9 @@ std::string hist_kernel_name(int64_t d, int M, int G, bool default_grid)
 {
     const int v = hist_variant(d);
     char name[64];
-    snprintf(name, sizeof name, "fit_hist_kernel<%d,%d,%s>", kVariants[v].threads, kVariants[v].ept,
-             !default_grid ? "grid" : lattice_buckets(v, M, G, true) ? "lattice" : "linear");
+    snprintf(name, sizeof name, "fit_hist_kernel<%d,%d,%s%s>", kVariants[v].threads, kVariants[v].ept,
+             !default_grid ? "grid" : lattice_buckets(v, M, G, true) ? "lattice" : "linear",
+             kVariants[v].rebuilt ? ",rebuilt" : "");
     return name;
 }
 
@@ -627,6 +700,7 @@ hipError_t launch_fit_hist(const HistBatch &batch, int variant, int64_t channels
     case 7: return launch_hist_t<1024, 8>(b, channels, lds, s);
     // 512 threads leave 256 VGPRs per thread for the register-resident residual
     case 8: return launch_hist_t<512, 32>(b, channels, lds, s);
+    case 9: return launch_hist_t<1024, 32, true>(b, channels, lds, s);
     default: return hipErrorInvalidValue;
     }
 }

@@ -60,7 +60,7 @@ hipError_t launch_fit(const FitParams &p, const FitLayout &L, hipStream_t s);
 // One launch fits the channels of up to kMaxBatchLayers layers whose lengths
 // select the same kernel variant (hist_variant); the descriptors travel by
 // value in the kernel arguments.
-constexpr int64_t kHistMaxDim = 16384;
+constexpr int64_t kHistMaxDim = 32768;
 constexpr int kMaxBatchLayers = 48;
 
 struct HistLayer {

@@ -129,7 +129,7 @@ def test_deterministic(dense):
         assert np.array_equal(x, y)
 
 
-@pytest.mark.parametrize("d", [8192, 8193, 16384, 16385])
+@pytest.mark.parametrize("d", [8192, 8193, 16384, 16385, 32768, 32769])
 def test_search_kernel_boundaries(orc, d):
     """Largest channels of each register-resident variant of the histogram
     search, and the first length that falls back to the dense search."""
@@ -158,10 +158,11 @@ def _lattice_rows(d, rng):
     return W
 
 
-@pytest.mark.parametrize("d", [1025, 2049, 4097, 4608, 4609])
+@pytest.mark.parametrize("d", [1025, 2049, 4097, 4608, 4609, 16385, 25088, 32768])
 def test_lattice_mode_channels(orc, d):
     """Lattice-bucket mode of the histogram search (default grid, channels
-    longer than 1024): lockstep parity, including elements that sit exactly on
+    longer than 1024; past 16384 the variant that rebuilds the residual from
+    the weights and codes each phase): lockstep parity, including elements that sit exactly on
     a boundary (exact per-boundary corrections) and a channel below the
     mode's range; and agreement with the per-level histogram, reached by
     passing the default grid explicitly."""
