@@ -452,6 +452,37 @@ int check_error_layer(const mpq_layer &L, int max_points, bool need_x)
     return MPQ_OK;
 }
 
+// The independent launch groups of an output error, with one scratch block
+// holding each group's part.
+struct ErrJobs {
+    std::vector<size_t> off;
+    std::vector<double> work;
+    char *scratch = nullptr;
+};
+
+int err_jobs(const std::vector<mpq::ErrLayerIn> &in, hipStream_t s, ErrJobs *j)
+{
+    const int ng = mpq::err_group_count(in.data(), (int)in.size());
+    size_t total = 0;
+    for (int g = 0; g < ng; ++g) {
+        j->off.push_back(total);
+        total += (mpq::err_group_scratch_bytes(in.data(), (int)in.size(), g) + 255) / 256 * 256;
+        j->work.push_back(mpq::err_group_flop(in.data(), (int)in.size(), g));
+    }
+    const hipError_t e = mpq::scratch_alloc((void **)&j->scratch, total, s);
+    if (e != hipSuccess) {
+        j->scratch = nullptr;
+        return fail(MPQ_ERR_NOMEM, "scratch of %zu bytes: %s", total, hipGetErrorString(e));
+    }
+    return MPQ_OK;
+}
+
+hipError_t launch_err_job(const std::vector<mpq::ErrLayerIn> &in, const ErrJobs &j, int g, int P,
+                          hipStream_t st)
+{
+    return mpq::launch_output_error_group(in.data(), (int)in.size(), g, P, j.scratch + j.off[g], st);
+}
+
 int output_error_impl(const mpq_layer *layers, int n_layers, int max_points, void *stream)
 {
     if (n_layers < 0 || (n_layers > 0 && !layers))
@@ -466,13 +497,14 @@ int output_error_impl(const mpq_layer *layers, int n_layers, int max_points, voi
                                      L.c_out, L.d, L.n});
     }
     if (in.empty()) return MPQ_OK;
-    const size_t bytes = mpq::err_scratch_bytes(in.data(), (int)in.size());
     hipStream_t s = (hipStream_t)stream;
-    void *scratch = nullptr;
-    hipError_t e = mpq::scratch_alloc(&scratch, bytes, s);
-    if (e != hipSuccess) return fail(MPQ_ERR_NOMEM, "scratch of %zu bytes: %s", bytes, hipGetErrorString(e));
-    e = mpq::launch_output_error(in.data(), (int)in.size(), max_points, scratch, s);
-    (void)mpq::scratch_free(scratch, s);
+    ErrJobs jobs;
+    int rc = err_jobs(in, s, &jobs);
+    if (rc != MPQ_OK) return rc;
+    const hipError_t e = run_concurrently(s, jobs.work, [&](int i, hipStream_t st) {
+        return launch_err_job(in, jobs, i, max_points, st);
+    });
+    if (jobs.scratch) (void)mpq::scratch_free(jobs.scratch, s);
     if (e != hipSuccess) return hip_fail(e, "output error kernel launch");
     return MPQ_OK;
 }
@@ -527,46 +559,39 @@ int quantize_impl(const mpq_layer *layers, int n_layers, int bits, int max_point
     });
     if (dgrid) (void)mpq::scratch_free(dgrid, s);
     if (e != hipSuccess) return hip_fail(e, "fit kernel launch");
-    // 2. the output error of every layer that asks for it, in one batch (its
-    // GEMM fills the device only with all layers' tiles together), and beside
-    // it the reconstruction: both only read the fit's outputs
+    // 2. the output error of every layer that asks for it, in its launch
+    // groups (a group's GEMM fills the device only with many layers' tiles),
+    // and beside them the reconstruction: both only read the fit's outputs
     std::vector<mpq::ErrLayerIn> err;
     std::vector<mpq::RecLayer> rec;
-    double flop = 0.0, bytes = 0.0;
+    double bytes = 0.0;
     for (int l = 0; l < n_layers; ++l) {
         const mpq_layer &L = layers[l];
         if (L.c_out == 0) continue;
         if (L.out_err) {
             err.push_back(mpq::ErrLayerIn{L.W, L.codes, L.scales, L.counts, L.X, L.out_err, L.out_ref,
                                           L.c_out, L.d, L.n});
-            flop += 2.0 * (double)L.c_out * (double)L.d * (double)L.n;
         }
         if (L.W_hat) {
             rec.push_back(mpq::RecLayer{L.codes, L.scales, L.counts, L.W_hat, L.c_out, L.d});
             bytes += 5.0 * (double)L.c_out * (double)L.d;
         }
     }
-    void *scratch = nullptr;
+    ErrJobs ej;
     if (!err.empty()) {
-        const size_t nb = mpq::err_scratch_bytes(err.data(), (int)err.size());
-        e = mpq::scratch_alloc(&scratch, nb, s);
-        if (e != hipSuccess) return fail(MPQ_ERR_NOMEM, "scratch of %zu bytes: %s", nb, hipGetErrorString(e));
+        rc = err_jobs(err, s, &ej);
+        if (rc != MPQ_OK) return rc;
     }
-    std::vector<double> w2;
-    std::vector<int> kind;
-    if (!err.empty()) {
-        w2.push_back(flop);   // run_concurrently puts the larger job on the caller's stream
-        kind.push_back(0);
-    }
-    if (!rec.empty()) {
-        w2.push_back(bytes);
-        kind.push_back(1);
-    }
+    // the output error's launch groups (work in GEMM FLOP) and the
+    // reconstruction (bytes, at ~2 TB/s against ~100 TFLOP/s: x 50), side by side
+    std::vector<double> w2 = ej.work;
+    const int n_err_jobs = (int)w2.size();
+    if (!rec.empty()) w2.push_back(bytes * 50.0);
     e = run_concurrently(s, w2, [&](int i, hipStream_t st) {
-        return kind[i] == 0 ? mpq::launch_output_error(err.data(), (int)err.size(), max_points, scratch, st)
-                            : mpq::launch_reconstruct(rec.data(), (int)rec.size(), max_points, st);
+        return i < n_err_jobs ? launch_err_job(err, ej, i, max_points, st)
+                              : mpq::launch_reconstruct(rec.data(), (int)rec.size(), max_points, st);
     });
-    if (scratch) (void)mpq::scratch_free(scratch, s);
+    if (ej.scratch) (void)mpq::scratch_free(ej.scratch, s);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     return MPQ_OK;
 }

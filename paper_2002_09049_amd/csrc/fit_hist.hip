@@ -198,7 +198,7 @@ __device__ __forceinline__ void bin_lattice(Res r, const HistShared &S, int G, i
                                             double inv, double delta, double scale)
 {
     constexpr double kBias = 0x1p52 + (double)kLatOne;
-#pragma unroll(kUnroll)
+#pragma unroll kUnroll
     for (int u = 0; u < EPT; ++u) {
         if (T * u >= d) continue;   // a slot past the channel end in every thread
         const double x = fabs(r(u));
@@ -349,7 +349,7 @@ fit_hist_kernel(const HistBatch B)
         int8_t *qrow = qk + (int64_t)(i - 1) * d;
         const double ap = (double)apend;
         const double ia = 1.0 / ap;
-#pragma unroll(kUnroll)
+#pragma unroll kUnroll
         for (int u = 0; u < EPT; ++u) {
             const int j = t + T * u;
             if (kGlobal && T * u >= d) break;
@@ -560,7 +560,7 @@ fit_hist_kernel(const HistBatch B)
                 const int g = s_fin[f];
                 const double a = S.ad[g + 1];
                 double le = 0.0;
-#pragma unroll(kUnroll)
+#pragma unroll kUnroll
                 for (int u = 0; u < EPT; ++u) {
                     if (kGlobal && T * u >= d) break;
                     const double ru = kGlobal ? rebuild(u, i) : r[kGlobal ? 0 : u];

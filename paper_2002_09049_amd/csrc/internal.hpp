@@ -90,8 +90,7 @@ int hist_variant(int64_t d);   // layers with equal variants may share a launch
 std::string hist_kernel_name(int64_t d, int M, int G, bool default_grid);
 hipError_t launch_fit_hist(const HistBatch &b, int variant, int64_t channels, hipStream_t s);
 
-// Output error of Eq. (12) for a list of layers; `scratch` holds
-// err_scratch_bytes(...) bytes (256-byte aligned).
+// Output error of Eq. (12) for a list of layers.
 struct ErrLayerIn {
     const float *W;
     const int8_t *codes;
@@ -102,8 +101,14 @@ struct ErrLayerIn {
     float *ref;     // nullptr: no ref for this layer
     int64_t C, d, n;
 };
-size_t err_scratch_bytes(const ErrLayerIn *in, int n_in);
-hipError_t launch_output_error(const ErrLayerIn *in, int n_in, int P, void *scratch, hipStream_t s);
+// The items (an err item per layer, a ref item per layer that wants ref) go
+// in launch groups of up to 24; groups are independent and may run side by
+// side, each with its own scratch.
+int err_group_count(const ErrLayerIn *in, int n_in);
+size_t err_group_scratch_bytes(const ErrLayerIn *in, int n_in, int group);
+double err_group_flop(const ErrLayerIn *in, int n_in, int group);
+hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, int P, void *scratch,
+                                     hipStream_t s);
 
 // Stream-ordered scratch from a library-owned memory pool of the current
 // device (kept, not returned to the system, between calls).

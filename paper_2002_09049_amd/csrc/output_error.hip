@@ -389,7 +389,8 @@ std::vector<Item> items_of(const ErrLayerIn *in, int n_in)
 }
 
 // K split of a layer: tiles of about work / 512 slabs (two per CU), at least
-// 64 slabs, and K ranges whose rows of Dt and X stay below 2^31 bytes.  It
+// 64 slabs (or a quarter of a short K: a layer of few tiles still spreads),
+// and K ranges whose rows of Dt and X stay below 2^31 bytes.  It
 // depends on the layer alone, so a layer's result does not depend on the
 // other layers of the call.
 Plan plan_item(const ErrLayerIn &I)
@@ -400,7 +401,9 @@ Plan plan_item(const ErrLayerIn &I)
     q.ntn = (I.n + kBN - 1) / kBN;
     const int64_t slabs = (I.d + kBK - 1) / kBK;
     const double work = (double)(q.ntm * q.ntn) * (double)slabs;
-    const int64_t target = std::max<int64_t>(64, (int64_t)(work / 512.0 + 0.5));
+    // a K range of at least 64 slabs, or a quarter of a short K
+    const int64_t floor_slabs = std::min<int64_t>(64, (slabs + 3) / 4);
+    const int64_t target = std::max<int64_t>(floor_slabs, (int64_t)(work / 512.0 + 0.5));
     int64_t sp = (slabs + target / 2) / target;
     sp = std::max<int64_t>(1, std::min<int64_t>(sp, slabs));
     int64_t kchunk = (slabs + sp - 1) / sp * kBK;
@@ -427,21 +430,37 @@ size_t group_bytes(const Item *it, int cnt)
 
 }  // namespace
 
-size_t err_scratch_bytes(const ErrLayerIn *in, int n_in)
+int err_group_count(const ErrLayerIn *in, int n_in)
 {
-    const std::vector<Item> it = items_of(in, n_in);
-    size_t total = 0;
-    for (size_t base = 0; base < it.size(); base += kMaxErrLayers) {
-        const int cnt = (int)std::min<size_t>(kMaxErrLayers, it.size() - base);
-        total = std::max(total, group_bytes(it.data() + base, cnt));
-    }
-    return total;
+    const size_t n = items_of(in, n_in).size();
+    return (int)((n + kMaxErrLayers - 1) / kMaxErrLayers);
 }
 
-hipError_t launch_output_error(const ErrLayerIn *in, int n_in, int P, void *scratch, hipStream_t s)
+size_t err_group_scratch_bytes(const ErrLayerIn *in, int n_in, int group)
 {
     const std::vector<Item> it = items_of(in, n_in);
-    for (size_t base = 0; base < it.size(); base += kMaxErrLayers) {
+    const size_t base = (size_t)group * kMaxErrLayers;
+    if (base >= it.size()) return 0;
+    const int cnt = (int)std::min<size_t>(kMaxErrLayers, it.size() - base);
+    return group_bytes(it.data() + base, cnt);
+}
+
+double err_group_flop(const ErrLayerIn *in, int n_in, int group)
+{
+    const std::vector<Item> it = items_of(in, n_in);
+    double f = 0.0;
+    for (size_t i = (size_t)group * kMaxErrLayers; i < it.size() && i < (size_t)(group + 1) * kMaxErrLayers; ++i)
+        f += 2.0 * (double)it[i].in->C * (double)it[i].in->d * (double)it[i].in->n;
+    return f;
+}
+
+hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, int P, void *scratch,
+                                     hipStream_t s)
+{
+    const std::vector<Item> it = items_of(in, n_in);
+    const size_t base = (size_t)group * kMaxErrLayers;
+    if (base >= it.size()) return hipSuccess;
+    {
         const int cnt = (int)std::min<size_t>(kMaxErrLayers, it.size() - base);
         const Item *grp = it.data() + base;
         std::vector<Plan> p(cnt);
