@@ -21,13 +21,13 @@
 // Lattice mode (default grid, (2M-1) G + 1 buckets fit): with u = m / (2 G M)
 // every boundary (k + 1/2) a_g lies within relative 2^-23 of the lattice
 // point L = (2k+1)(g+1) times u.  An element whose x / u is farther than
-// delta = 2 G M 2^-22 from every integer crosses exactly the boundaries with
+// N 2^-21 from its nearest integer N crosses exactly the boundaries with
 // L <= floor(x / u), so it goes to that one bucket (fixed-point x and a count
 // packed in one 64-bit word); A(g) and B(g) are then sums over k of suffix
-// sums at L = (2k+1)(g+1).  An element within delta of an integer N goes to
-// bucket N - 1, and each boundary at L = N is decided exactly and, when
-// crossed, added to a per-candidate correction.  This replaces M atomics per
-// element with one and gives the same integer sums.
+// sums at L = (2k+1)(g+1).  An element that near N goes to bucket N - 1, and
+// each boundary at L = N is decided exactly and, when crossed, added to a
+// per-candidate correction.  This replaces M atomics per element with one
+// and gives the same integer sums.
 //
 // One workgroup per channel.  The fp64 residual stays in registers for the
 // whole fit (EPT elements per thread, element j = t + T * u), so each step
@@ -187,26 +187,31 @@ __device__ __forceinline__ void bin_levels_elementwise(Res r, const HistShared &
 // 1 / u in fp64; Lmax = nlat - 1 is the largest lattice point of a boundary;
 // scale = 2^sh.
 //
-// z = x / u + delta (one rounding, error far below delta) and F = floor(z):
-// z - F > 2 delta puts x / u more than delta from every integer, with floor
-// F; otherwise x / u is within delta of N = F.  The bucket word is formed by
-// one fma: x 2^sh + 2^52 + 2^kLatShift rounds x 2^sh to the nearest integer
-// (ties to even, as rint) and its low 52 bits are that integer plus the count
-// bit.
+// z = x inv is x / u within relative 2^-51, and N = rint(z).  The boundaries
+// at lattice point N lie within N 2^-23 of N (in units of u; a_g carries one
+// fp32 rounding of m c_g / M, relative 2^-23 with c_g's), the others at least
+// 1 - 4096 2^-23 from x / u.  So |z - N| > N 2^-21 (a 4x margin) puts x / u
+// on N's side of every boundary at N, and the element crosses exactly the
+// boundaries at L <= floor(z); otherwise it crosses every boundary below N
+// (bucket N - 1) and those at N are decided one by one.  The tolerance grows
+// with N, so the small residuals, most of a channel, are rarely near.  The
+// bucket word is formed by one fma: x 2^sh + 2^52 + 2^kLatShift rounds
+// x 2^sh to the nearest integer (ties to even, as rint) and its low 52 bits
+// are that integer plus the count bit.
 template <int T, int EPT, int kUnroll, class Res>
 __device__ __forceinline__ void bin_lattice(Res r, const HistShared &S, int G, int M, int d, int Lmax,
-                                            double inv, double delta, double scale)
+                                            double inv, double scale)
 {
     constexpr double kBias = 0x1p52 + (double)kLatOne;
 #pragma unroll kUnroll
     for (int u = 0; u < EPT; ++u) {
         if (T * u >= d) continue;   // a slot past the channel end in every thread
         const double x = fabs(r(u));
-        const double z = fma(x, inv, delta);
-        const double F = floor(z);
-        const bool near = z - F <= 2.0 * delta;
-        const int Ni = (int)F;
-        const int b = near ? Ni - 1 : Ni;
+        const double z = x * inv;
+        const double Nd = rint(z);
+        const int Ni = (int)Nd;
+        const bool near = Ni >= 1 && fabs(z - Nd) <= Nd * 0x1p-21;
+        const int b = near ? Ni - 1 : (z >= Nd ? Ni : Ni - 1);
         const unsigned long long word =
             (unsigned long long)__double_as_longlong(fma(x, scale, kBias)) & ((1ull << 52) - 1);
         if (b >= 1) atomicAdd(&S.lat[min(b, Lmax)], word);
@@ -415,10 +420,9 @@ fit_hist_kernel(const HistBatch B)
         if (lat) {
             // ---- lattice buckets, their suffix sums, then every candidate
             const double inv = (double)(2 * G * M) / (double)m;
-            const double delta = (double)(2 * G * M) * 0x1p-22;
             // residual after the i points so far (kGlobal: rebuilt)
             auto res = [&](int u) { return kGlobal ? rebuild(u, i) : r[kGlobal ? 0 : u]; };
-            bin_lattice<T, EPT, kUnroll>(res, S, G, M, d, nlat - 1, inv, delta, ldexp(1.0, sh));
+            bin_lattice<T, EPT, kUnroll>(res, S, G, M, d, nlat - 1, inv, ldexp(1.0, sh));
             __syncthreads();
             block_suffix_sums<T>(S.lat, nlat, s_scan);
             for (int g = t; g < G; g += T) {
