@@ -50,6 +50,7 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBM = 128, kBN = 128, kBK = 16;
+constexpr int kMinRangeK = 1024;  // K of a split layer's K range, at least (unless K is short)
 constexpr int kThreads = 256;
 constexpr int kPad = 4;          // LDS row padding (floats); rows stay 16-byte aligned
 constexpr int kVec = kBK * kBM / kThreads / 4;   // float4 per thread and operand per slab
@@ -388,8 +389,8 @@ std::vector<Item> items_of(const ErrLayerIn *in, int n_in)
     return it;
 }
 
-// K split of a layer: tiles of about work / 512 slabs (two per CU), at least
-// 64 slabs (or a quarter of a short K: a layer of few tiles still spreads),
+// K split of a layer: tiles of about work / 512 slabs (two per CU), K ranges
+// of at least kMinRangeK (or a quarter of a short K: a layer of few tiles still spreads),
 // and K ranges whose rows of Dt and X stay below 2^31 bytes.  It
 // depends on the layer alone, so a layer's result does not depend on the
 // other layers of the call.
@@ -401,8 +402,8 @@ Plan plan_item(const ErrLayerIn &I)
     q.ntn = (I.n + kBN - 1) / kBN;
     const int64_t slabs = (I.d + kBK - 1) / kBK;
     const double work = (double)(q.ntm * q.ntn) * (double)slabs;
-    // a K range of at least 64 slabs, or a quarter of a short K
-    const int64_t floor_slabs = std::min<int64_t>(64, (slabs + 3) / 4);
+    // a K range of at least kMinRangeK, or a quarter of a short K
+    const int64_t floor_slabs = std::min<int64_t>(kMinRangeK / kBK, (slabs + 3) / 4);
     const int64_t target = std::max<int64_t>(floor_slabs, (int64_t)(work / 512.0 + 0.5));
     int64_t sp = (slabs + target / 2) / target;
     sp = std::max<int64_t>(1, std::min<int64_t>(sp, slabs));
