@@ -42,6 +42,12 @@ def _declare(lib):
     lib.oracle_verify.argtypes = [P, i64, i64, i32, i32, P, i32, f64, P, P, P, P,
                                   P, i64, P, P, P, P, P, i32]
     lib.oracle_verify.restype = i32
+    lib.oracle_fit_calib.argtypes = [P, i64, i64, i32, i32, P, i32, P, i64, f64, i32, P, P, P, P,
+                                     P, i32]
+    lib.oracle_fit_calib.restype = i32
+    lib.oracle_verify_calib.argtypes = [P, i64, i64, i32, i32, P, i32, P, i64, f64, i32, P, P, P,
+                                        P, P, P, i64, P, P, P, P, P, i32]
+    lib.oracle_verify_calib.restype = i32
     lib.oracle_output_error.argtypes = [P, P, P, P, i64, i64, i32, P, i64, P, i64,
                                         P, P, i32]
     lib.oracle_output_error.restype = i32
@@ -163,6 +169,58 @@ class Oracle:
         out["channels"] = chan
         return out
 
+    def fit_calib(self, W: np.ndarray, bits: int, max_points: int, n_grid: int, X: np.ndarray,
+                  eps: float, relative: bool, grid: Optional[np.ndarray] = None, n_threads: int = 0):
+        """Free-running fit with Algorithm 2's stopping rule on the calibration
+        batch X [d, N] (reading S4).  Returns (codes, scales, counts, err,
+        xerr[C,P] f64: the output error after each point)."""
+        W = np.ascontiguousarray(W, dtype=np.float32)
+        C, d = W.shape
+        X = np.ascontiguousarray(X, dtype=np.float32)
+        assert X.shape[0] == d
+        P = max_points
+        codes_ = np.zeros((C, P, d), np.int8)
+        scales = np.zeros((C, P), np.float32)
+        counts = np.zeros(C, np.int32)
+        err = np.zeros((C, P), np.float64)
+        xerr = np.zeros((C, P), np.float64)
+        g = _grid(grid, n_grid)
+        rc = self.lib.oracle_fit_calib(_p(W), C, d, bits, P, _p(g), n_grid, _p(X), X.shape[1],
+                                      float(eps), 1 if relative else 0, _p(codes_), _p(scales),
+                                      _p(counts), _p(err), _p(xerr), n_threads)
+        if rc != 0:
+            raise MemoryError("oracle_fit_calib failed")
+        return codes_, scales, counts, err, xerr
+
+    def verify_calib(self, W, bits, max_points, n_grid, X, eps, relative, codes_, scales, counts,
+                     err=None, xerr=None, grid=None, channels=None, n_threads: int = 0):
+        """Lockstep check (V1, V2, V4, V4x and S4's stop decision) of another
+        implementation's fit with Algorithm 2's stopping rule."""
+        W = np.ascontiguousarray(W, dtype=np.float32)
+        C, d = W.shape
+        X = np.ascontiguousarray(X, dtype=np.float32)
+        codes_ = np.ascontiguousarray(codes_, dtype=np.int8)
+        scales = np.ascontiguousarray(scales, dtype=np.float32)
+        counts = np.ascontiguousarray(counts, dtype=np.int32)
+        assert codes_.shape == (C, max_points, d) and scales.shape == (C, max_points)
+        e = None if err is None else np.ascontiguousarray(err, dtype=np.float32)
+        xe = None if xerr is None else np.ascontiguousarray(xerr, dtype=np.float32)
+        chan = np.arange(C, dtype=np.int64) if channels is None else \
+            np.ascontiguousarray(channels, dtype=np.int64)
+        n = chan.size
+        out = {k: np.zeros(n, np.int32) for k in ("status", "cand_ties", "code_ties", "stop_ties")}
+        out["err_relmax"] = np.zeros(n, np.float64)
+        g = _grid(grid, n_grid)
+        rc = self.lib.oracle_verify_calib(
+            _p(W), C, d, bits, max_points, _p(g), n_grid, _p(X), X.shape[1], float(eps),
+            1 if relative else 0, _p(codes_), _p(scales), _p(counts), _p(e), _p(xe), _p(chan), n,
+            _p(out["status"]), _p(out["cand_ties"]), _p(out["code_ties"]), _p(out["stop_ties"]),
+            _p(out["err_relmax"]), n_threads)
+        if rc != 0:
+            raise MemoryError("oracle_verify_calib failed")
+        out["channels"] = chan
+        return out
+
     def output_error(self, W, codes_, scales, counts, X, channels=None, with_ref=True, n_threads: int = 0):
         """Eq. (12) in fp64. Returns (err, ref) for the listed channels."""
         W = np.ascontiguousarray(W, dtype=np.float32)
@@ -202,5 +260,5 @@ def _delegate(name):
 
 
 for _n in ("levels", "default_grid", "candidate_scales", "codes", "scale_error", "fit",
-           "verify", "output_error", "reconstruct"):
+           "verify", "fit_calib", "verify_calib", "output_error", "reconstruct"):
     globals()[_n] = _delegate(_n)

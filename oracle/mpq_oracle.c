@@ -31,6 +31,15 @@
  *          and ||r||^2 <= tol * ||w||^2 (the output error of Eq. (12) under
  *          an isotropic calibration distribution).  A nonzero channel
  *          always gets at least one point; an all-zero channel gets none.
+ *   S4     Algorithm 2 on a calibration batch X [d][N] (oracle_fit_calib):
+ *          after n >= 1 points the channel's output error
+ *          e_n = (1/N) sum_t ((w - sum_{i<n} a_i q_i) . x_t)^2 (Eq. (12)) is
+ *          compared with a threshold thr, eps itself (the paper's absolute
+ *          epsilon) or eps * (1/N) sum_t (w . x_t)^2 (relative); the fit
+ *          stops when e_n <= thr (Algorithm 2 applies Algorithm 1 while
+ *          e > eps), or at max_points, ||r||^2 == 0 or no nonzero scale.
+ *          The points are still chosen by Eq. (9): Algorithm 1 fits the
+ *          residual, Algorithm 2 only decides how many points to take.
  *   A1     No refit of a once q is fixed.
  *   E1     Output error: mean over the N columns of X of ((w - w~) . x)^2.
  *   P1     Scales are stored as fp32 values (exactly the candidate value).
@@ -127,18 +136,60 @@ static int should_stop(int n, int P, double Er, double Ew, double tol)
     return 0;
 }
 
+/* The calibration-batch stopping rule S4: batch X [d][N], threshold eps,
+ * relative != 0 for eps times the channel's full-precision output energy. */
+typedef struct {
+    const float *X;
+    int64_t N;
+    double eps;
+    int relative;
+} calib_rule;
+
+/* Eq. (12) for one channel: (1/N) sum_t (v . x_t)^2, every sum in index
+ * order, fp64. */
+static double calib_error(const double *v, int64_t d, const float *X, int64_t N)
+{
+    double s = 0.0;
+    for (int64_t t = 0; t < N; ++t) {
+        double y = 0.0;
+        for (int64_t j = 0; j < d; ++j) y += v[j] * (double)X[j * N + t];
+        s += y * y;
+    }
+    return s / (double)N;
+}
+
+/* Threshold of S4 for a channel whose residual is still w (r = w). */
+static double calib_threshold(const calib_rule *cal, const double *w, int64_t d)
+{
+    return cal->relative ? cal->eps * calib_error(w, d, cal->X, cal->N) : cal->eps;
+}
+
+/* S4 with n points taken: stop at P, at a zero residual, or once the output
+ * error e of the n >= 1 points is at most thr. */
+static int calib_should_stop(int n, int P, double Er, double e, double thr)
+{
+    if (n >= P || Er == 0.0) return 1;
+    if (n >= 1 && e <= thr) return 1;
+    return 0;
+}
+
 /* Algorithm 1 with the stopping rule, one channel.  codes [P][d], scales [P],
- * err [P] (||r||^2 after each point).  Returns the number of points. */
+ * err [P] (||r||^2 after each point).  cal: NULL for S1-S3, else S4 with
+ * xerr [P] (NULL or the output error after each point).  Returns the number
+ * of points. */
 static int fit_channel(const float *w, int64_t d, int M, int P, const float *c,
-                       int G, double tol, int8_t *codes, float *scales,
-                       double *err, double *r, float *a, double *E)
+                       int G, double tol, const calib_rule *cal, int8_t *codes,
+                       float *scales, double *err, double *xerr, double *r, float *a,
+                       double *E)
 {
     for (int64_t j = 0; j < d; ++j) r[j] = (double)w[j];   /* r_1 = w, Eq. (7) */
     double Ew = sum_sq(r, d);
+    double thr = cal ? calib_threshold(cal, r, d) : 0.0;
+    double e = 0.0;                                         /* S4: e_n */
     int n = 0;
     for (;;) {
         double Er = sum_sq(r, d);
-        if (should_stop(n, P, Er, Ew, tol)) break;
+        if (cal ? calib_should_stop(n, P, Er, e, thr) : should_stop(n, P, Er, Ew, tol)) break;
         oracle_candidate_scales(r, d, M, c, G, a);
         int g = grid_search(r, d, a, G, M, E);              /* Eq. (9)  */
         if (g < 0) break;                                   /* S3: no scale */
@@ -149,6 +200,10 @@ static int fit_channel(const float *w, int64_t d, int M, int P, const float *c,
         scales[n] = a[g];
         n += 1;
         err[n - 1] = sum_sq(r, d);
+        if (cal) {
+            e = calib_error(r, d, cal->X, cal->N);          /* Eq. (12) */
+            if (xerr) xerr[n - 1] = e;
+        }
     }
     return n;
 }
@@ -165,10 +220,12 @@ static int n_threads_or_default(int nt)
 
 /* Free-running fit of a layer W [C][d].  grid: NULL for the default.
  * Outputs: codes [C][P][d] int8, scales [C][P], counts [C], err [C][P]
- * (may be NULL).  Slots at or after a channel's count are zero. */
-int oracle_fit(const float *W, int64_t C, int64_t d, int bits, int P,
-               const float *grid, int G, double tol, int8_t *codes,
-               float *scales, int32_t *counts, double *err, int n_threads)
+ * (may be NULL), and with cal the output error after each point, xerr
+ * [C][P] (may be NULL).  Slots at or after a channel's count are zero. */
+static int fit_layer(const float *W, int64_t C, int64_t d, int bits, int P,
+                     const float *grid, int G, double tol, const calib_rule *cal,
+                     int8_t *codes, float *scales, int32_t *counts, double *err,
+                     double *xerr, int n_threads)
 {
     int M = oracle_levels(bits);
     float *c = (float *)malloc(sizeof(float) * (size_t)G);
@@ -178,6 +235,7 @@ int oracle_fit(const float *W, int64_t C, int64_t d, int bits, int P,
     memset(codes, 0, (size_t)(C * P * d));
     memset(scales, 0, sizeof(float) * (size_t)(C * P));
     if (err) memset(err, 0, sizeof(double) * (size_t)(C * P));
+    if (xerr) memset(xerr, 0, sizeof(double) * (size_t)(C * P));
     int nt = n_threads_or_default(n_threads);
     int fail = 0;
 #pragma omp parallel num_threads(nt)
@@ -186,23 +244,45 @@ int oracle_fit(const float *W, int64_t C, int64_t d, int bits, int P,
         float *a = (float *)malloc(sizeof(float) * (size_t)G);
         double *E = (double *)malloc(sizeof(double) * (size_t)G);
         double *e = (double *)malloc(sizeof(double) * (size_t)P);
-        if (!r || !a || !E || !e) {
+        double *xe = (double *)malloc(sizeof(double) * (size_t)P);
+        if (!r || !a || !E || !e || !xe) {
 #pragma omp atomic write
             fail = 1;
         } else {
 #pragma omp for schedule(dynamic, 1)
             for (int64_t k = 0; k < C; ++k) {
                 memset(e, 0, sizeof(double) * (size_t)P);
-                int n = fit_channel(W + k * d, d, M, P, c, G, tol,
-                                    codes + k * P * d, scales + k * P, e, r, a, E);
+                memset(xe, 0, sizeof(double) * (size_t)P);
+                int n = fit_channel(W + k * d, d, M, P, c, G, tol, cal, codes + k * P * d,
+                                    scales + k * P, e, xe, r, a, E);
                 counts[k] = n;
                 if (err) memcpy(err + k * P, e, sizeof(double) * (size_t)P);
+                if (xerr) memcpy(xerr + k * P, xe, sizeof(double) * (size_t)P);
             }
         }
-        free(r); free(a); free(E); free(e);
+        free(r); free(a); free(E); free(e); free(xe);
     }
     free(c);
     return fail ? -1 : 0;
+}
+
+int oracle_fit(const float *W, int64_t C, int64_t d, int bits, int P,
+               const float *grid, int G, double tol, int8_t *codes,
+               float *scales, int32_t *counts, double *err, int n_threads)
+{
+    return fit_layer(W, C, d, bits, P, grid, G, tol, NULL, codes, scales, counts, err, NULL,
+                     n_threads);
+}
+
+/* The fit with the stopping rule S4 on the calibration batch X [d][N]. */
+int oracle_fit_calib(const float *W, int64_t C, int64_t d, int bits, int P,
+                     const float *grid, int G, const float *X, int64_t N, double eps,
+                     int relative, int8_t *codes, float *scales, int32_t *counts,
+                     double *err, double *xerr, int n_threads)
+{
+    calib_rule cal = {X, N, eps, relative};
+    return fit_layer(W, C, d, bits, P, grid, G, 0.0, &cal, codes, scales, counts, err, xerr,
+                     n_threads);
 }
 
 /* ------------------------------------------------------------------------
@@ -220,15 +300,34 @@ int oracle_fit(const float *W, int64_t C, int64_t d, int bits, int P,
  *     fp32 rounding of the fp64 value;
  * and that every slot at or after the count is zero.  After each accepted
  * step it continues from the other implementation's (a, q).
+ * With the calibration rule S4 (oracle_verify_calib), V3 is S4's decision,
+ * tied when e_n / thr is within 1e-5 of 1 (the output error of Eq. (12) is
+ * an fp32-product value to 1e-5 on the other side), and
+ *  V4x the per-point output error (if given) agrees with the fp64 e_n as
+ *     V4 asks of ||r||^2.
  * status: 0 ok, 1 count, 2 scale not a candidate, 3 scale not optimal,
- *         4 code, 5 nonzero unused slot, 6 err value, 7 bad count range.
+ *         4 code, 5 nonzero unused slot, 6 err value, 7 bad count range,
+ *         8 output-error value.
  * ------------------------------------------------------------------------ */
-int oracle_verify(const float *W, int64_t C, int64_t d, int bits, int P,
-                  const float *grid, int G, double tol, const int8_t *codes,
-                  const float *scales, const int32_t *counts, const float *err,
-                  const int64_t *chan, int64_t n_chan, int32_t *status,
-                  int32_t *cand_ties, int32_t *code_ties, int32_t *stop_ties,
-                  double *err_relmax, int n_threads)
+
+/* V4 / V4x for one fp32 output: 1e-5 relative, one fp32 subnormal quantum
+ * (2^-149: the most an fp32 value below the normal range can be off by), or
+ * exactly fl32 of the fp64 value (which is +inf above the fp32 range).
+ * Tracks the largest relative deviation of normal values in *emax. */
+static int fp32_value_ok(double got, double ref, double *emax)
+{
+    double dev = fabs(got - ref);
+    if (ref >= 0x1p-126 && dev / ref > *emax) *emax = dev / ref;
+    return got == (double)(float)ref || dev <= 1e-5 * ref + 0x1p-149;
+}
+
+static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
+                        const float *grid, int G, double tol, const calib_rule *cal,
+                        const int8_t *codes, const float *scales, const int32_t *counts,
+                        const float *err, const float *xerr, const int64_t *chan,
+                        int64_t n_chan, int32_t *status, int32_t *cand_ties,
+                        int32_t *code_ties, int32_t *stop_ties, double *err_relmax,
+                        int n_threads)
 {
     int M = oracle_levels(bits);
     float *c = (float *)malloc(sizeof(float) * (size_t)G);
@@ -254,39 +353,40 @@ int oracle_verify(const float *W, int64_t C, int64_t d, int bits, int P,
                 const int8_t *qk = codes + k * P * d;
                 const float *ak = scales + k * P;
                 const float *ek = err ? err + k * P : NULL;
+                const float *xk = (cal && xerr) ? xerr + k * P : NULL;
                 int st = 0, ct = 0, qt = 0, stt = 0;
                 double emax = 0.0;
                 int n_other = counts[k];
                 if (n_other < 0 || n_other > P) st = 7;
                 for (int64_t j = 0; j < d; ++j) r[j] = (double)w[j];
                 double Ew = sum_sq(r, d);
+                double thr = cal ? calib_threshold(cal, r, d) : 0.0;
+                double e = 0.0;   /* S4: output error of the points so far */
                 for (int n = 0; st == 0; ++n) {
                     double Er = sum_sq(r, d);
-                    if (n >= 1 && ek) {
-                        /* err is an fp32 output: besides 1e-5 relative, allow
-                         * one fp32 subnormal quantum (2^-149), the most its
-                         * representation of a value below the normal range
-                         * can be off by, and accept fl32(ref) itself (which is
-                         * +inf above the fp32 range). */
-                        double ref = Er, got = (double)ek[n - 1];
-                        double dev = fabs(got - ref);
-                        if (ref >= 0x1p-126 && dev / ref > emax) emax = dev / ref;
-                        if (got != (double)(float)ref && dev > 1e-5 * ref + 0x1p-149) {
-                            st = 6;
-                            break;
-                        }
+                    /* err and xerr are fp32 outputs (V4, V4x) */
+                    if (n >= 1 && ek && !fp32_value_ok((double)ek[n - 1], Er, &emax)) {
+                        st = 6;
+                        break;
+                    }
+                    if (n >= 1 && xk && !fp32_value_ok((double)xk[n - 1], e, &emax)) {
+                        st = 8;
+                        break;
                     }
                     oracle_candidate_scales(r, d, M, c, G, a);
                     int gbest = -1;
-                    int stop_ref = should_stop(n, P, Er, Ew, tol);
+                    int stop_ref = cal ? calib_should_stop(n, P, Er, e, thr)
+                                       : should_stop(n, P, Er, Ew, tol);
                     if (!stop_ref) {
                         gbest = grid_search(r, d, a, G, M, E);
                         stop_ref = gbest < 0;
                     }
                     int stop_other = (n == n_other);
                     if (stop_ref != stop_other) {
-                        double ratio = (tol * Ew) > 0 ? Er / (tol * Ew) : INFINITY;
-                        if (n >= 1 && n < P && Er != 0.0 && fabs(ratio - 1.0) <= 1e-6) {
+                        double lim = cal ? thr : tol * Ew;
+                        double ratio = lim > 0 ? (cal ? e : Er) / lim : INFINITY;
+                        double band = cal ? 1e-5 : 1e-6;
+                        if (n >= 1 && n < P && Er != 0.0 && fabs(ratio - 1.0) <= band) {
                             stt++;
                         } else { st = 1; break; }
                     }
@@ -322,12 +422,14 @@ int oracle_verify(const float *W, int64_t C, int64_t d, int bits, int P,
                     }
                     if (st) break;
                     for (int64_t j = 0; j < d; ++j) r[j] = r[j] - as * (double)q[j];
+                    if (cal) e = calib_error(r, d, cal->X, cal->N);
                 }
                 /* unused slots must be zero */
                 if (st == 0) {
                     for (int n = n_other; n < P && st == 0; ++n) {
                         if (ak[n] != 0.0f) st = 5;
                         if (ek && ek[n] != 0.0f) st = 5;
+                        if (xk && xk[n] != 0.0f) st = 5;
                         for (int64_t j = 0; j < d && st == 0; ++j)
                             if (qk[(int64_t)n * d + j] != 0) st = 5;
                     }
@@ -340,6 +442,34 @@ int oracle_verify(const float *W, int64_t C, int64_t d, int bits, int P,
     }
     free(c);
     return fail ? -1 : 0;
+}
+
+int oracle_verify(const float *W, int64_t C, int64_t d, int bits, int P,
+                  const float *grid, int G, double tol, const int8_t *codes,
+                  const float *scales, const int32_t *counts, const float *err,
+                  const int64_t *chan, int64_t n_chan, int32_t *status,
+                  int32_t *cand_ties, int32_t *code_ties, int32_t *stop_ties,
+                  double *err_relmax, int n_threads)
+{
+    return verify_layer(W, C, d, bits, P, grid, G, tol, NULL, codes, scales, counts, err, NULL,
+                        chan, n_chan, status, cand_ties, code_ties, stop_ties, err_relmax,
+                        n_threads);
+}
+
+/* The lockstep check of a fit with the calibration rule S4; xerr [C][P] is
+ * the other side's output error after each point (NULL: not checked). */
+int oracle_verify_calib(const float *W, int64_t C, int64_t d, int bits, int P,
+                        const float *grid, int G, const float *X, int64_t N, double eps,
+                        int relative, const int8_t *codes, const float *scales,
+                        const int32_t *counts, const float *err, const float *xerr,
+                        const int64_t *chan, int64_t n_chan, int32_t *status,
+                        int32_t *cand_ties, int32_t *code_ties, int32_t *stop_ties,
+                        double *err_relmax, int n_threads)
+{
+    calib_rule cal = {X, N, eps, relative};
+    return verify_layer(W, C, d, bits, P, grid, G, 0.0, &cal, codes, scales, counts, err, xerr,
+                        chan, n_chan, status, cand_ties, code_ties, stop_ties, err_relmax,
+                        n_threads);
 }
 
 /* Residual D = w - sum_{i<n} a_i q_i of one channel, summed in point order

@@ -336,10 +336,135 @@ def check_verifier(orc):
     assert status(codes, scales, counts, e6) == 6
 
 
+# ------------------------------------------- S4: Algorithm 2 on a batch X
+def _calib_case(seed=21, C=10, d=24, N=40):
+    rng = np.random.default_rng(seed)
+    W = (rng.standard_normal((C, d)) * np.exp(0.5 * rng.standard_normal((C, 1)))).astype(np.float32)
+    W[C - 1] = 0.0                                   # an all-zero channel
+    # correlated, non-isotropic inputs (ReLU of mixed Gaussians), d != N
+    X = np.maximum(rng.standard_normal((d, N)) + 0.5 * rng.standard_normal((1, N)), 0.0)
+    return W, X.astype(np.float32)
+
+
+def _numpy_output_errors(W, X, codes, scales, counts):
+    """e_n of Eq. (12) for n = 1..count, from the outputs, in numpy fp64."""
+    out = []
+    Xd = X.astype(np.float64)
+    for k in range(W.shape[0]):
+        D = W[k].astype(np.float64)
+        es = []
+        for i in range(counts[k]):
+            D = D - float(scales[k, i]) * codes[k, i].astype(np.float64)
+            es.append(float(np.mean((D @ Xd) ** 2)))
+        out.append(es)
+    return out
+
+
+def check_calib_hadamard_is_isotropic(orc):
+    """S4 with X X^T = N I: e_n = ||r_n||^2 and the relative threshold is
+    eps ||w||^2, so the fit equals the isotropic rule S1 with tol = eps."""
+    rng = np.random.default_rng(5)
+    d, N = 48, 64
+    X = bf.hadamard(N)[:d].astype(np.float32)
+    W = rng.standard_normal((12, d)).astype(np.float32)
+    for bits, P, G, eps in ((4, 6, 64, 1e-3), (3, 8, 32, 2e-3), (2, 5, 16, 0.05)):
+        c1, s1, n1, e1, x1 = orc.fit_calib(W, bits, P, G, X, eps, True)
+        c0, s0, n0, e0 = orc.fit(W, bits, P, G, eps)
+        assert np.array_equal(n1, n0) and np.array_equal(s1, s0) and np.array_equal(c1, c0)
+        assert np.allclose(x1, e0, rtol=1e-9, atol=0)
+
+
+def check_calib_stop_definition(orc):
+    """S4 against its definition: the reported output errors are Eq. (12)
+    of the outputs (numpy fp64), the count is the first n >= 1 with
+    e_n <= thr (else max_points), and the points are the isotropic fit's
+    (Algorithm 1 does not see X)."""
+    W, X = _calib_case()
+    ref = np.mean((W.astype(np.float64) @ X.astype(np.float64)) ** 2, axis=1)
+    for bits, P, G, eps, rel in ((4, 6, 64, 3e-3, True), (3, 8, 32, 1e-2, True),
+                                 (4, 6, 64, 0.02 * float(np.median(ref)), False)):
+        codes, scales, counts, err, xerr = orc.fit_calib(W, bits, P, G, X, eps, rel)
+        es = _numpy_output_errors(W, X, codes, scales, counts)
+        c0, s0, n0, _ = orc.fit(W, bits, P, G, 0.0)
+        for k in range(W.shape[0]):
+            thr = eps * ref[k] if rel else eps
+            n = counts[k]
+            assert np.allclose(xerr[k, :n], es[k], rtol=1e-10, atol=1e-300), k
+            assert (xerr[k, n:] == 0).all()
+            if not W[k].any():
+                assert n == 0
+                continue
+            assert n >= 1
+            assert all(e > thr for e in es[k][:-1]), (k, es[k], thr)
+            assert n == P or es[k][-1] <= thr, (k, es[k], thr)
+            assert np.array_equal(codes[k, :n], c0[k, :n]) and np.array_equal(scales[k, :n], s0[k, :n])
+
+
+def check_calib_runs_to_cap(orc):
+    """S4 with an absolute threshold of 0: no output error of a random
+    channel reaches 0 within the cap, so every nonzero channel takes exactly
+    max_points points, and a tiny cap binds before any threshold does."""
+    W, X = _calib_case(seed=12)
+    for P in (1, 2, 5):
+        codes, scales, counts, err, xerr = orc.fit_calib(W, 4, P, 32, X, 0.0, False)
+        assert (counts[:-1] == P).all() and counts[-1] == 0, (P, counts)
+        assert (xerr[:-1, P - 1] > 0).all()
+
+
+def check_calib_zero_batch(orc):
+    """S4 with X = 0: every output error is 0 <= thr, so a nonzero channel
+    stops after the one point S2 requires."""
+    W, X = _calib_case(seed=8)
+    X = np.zeros_like(X)
+    for rel in (True, False):
+        codes, scales, counts, err, xerr = orc.fit_calib(W, 4, 5, 32, X, 0.0, rel)
+        assert (counts[:-1] == 1).all() and counts[-1] == 0, counts
+
+
+def check_calib_scaling(orc):
+    """S4 is invariant to X -> 2X with a relative threshold, and with an
+    absolute one when eps -> 4 eps (e scales by 4)."""
+    W, X = _calib_case(seed=9)
+    a = orc.fit_calib(W, 4, 6, 64, X, 3e-3, True)
+    b = orc.fit_calib(W, 4, 6, 64, 2 * X, 3e-3, True)
+    assert all(np.array_equal(u, v) for u, v in zip(a[:3], b[:3]))
+    eps = 0.01 * float(np.median(a[4][:, 0]))
+    c = orc.fit_calib(W, 4, 6, 64, X, eps, False)
+    e = orc.fit_calib(W, 4, 6, 64, 2 * X, 4 * eps, False)
+    assert all(np.array_equal(u, v) for u, v in zip(c[:3], e[:3]))
+    assert np.allclose(e[4], 4 * c[4], rtol=1e-12, atol=0)
+
+
+def check_calib_verifier(orc):
+    """The S4 verifier accepts the oracle's own fit and flags a wrong count
+    and a wrong output-error value."""
+    W, X = _calib_case(seed=10)
+    P, G, eps = 6, 64, 3e-3
+    codes, scales, counts, err, xerr = orc.fit_calib(W, 4, P, G, X, eps, True)
+    e32, x32 = err.astype(np.float32), xerr.astype(np.float32)
+
+    def status(c, s, n, e, x):
+        v = orc.verify_calib(W, 4, P, G, X, eps, True, c, s, n, e, x)
+        return int(v["status"].max())
+
+    assert status(codes, scales, counts, e32, x32) == 0
+    k = int(np.argmax((counts >= 1) & (counts < P)))
+    n2 = counts.copy(); n2[k] += 1
+    c2 = codes.copy(); s2 = scales.copy()
+    c3, s3, _, _ = orc.fit(W, 4, P, G, 0.0)
+    c2[k], s2[k] = c3[k], s3[k]          # one more genuine point, zero slots after it
+    c2[k, n2[k]:] = 0; s2[k, n2[k]:] = 0
+    assert status(c2, s2, n2, None, None) == 1
+    x8 = x32.copy(); x8[k, 0] *= 1.001
+    assert status(codes, scales, counts, e32, x8) == 8
+
+
 ALL_CHECKS = [
     check_levels, check_rounding_ties, check_codes_bruteforce, check_grid_search_bruteforce,
     check_grid_search_bounds, check_two_point_joint, check_naive_quantizer,
     check_equal_magnitudes, check_worked_examples, check_monotone_decrease,
     check_reconstruct, check_invariances, check_output_error, check_stop_rule,
-    check_exponential_decay, check_verifier,
+    check_exponential_decay, check_verifier, check_calib_hadamard_is_isotropic,
+    check_calib_stop_definition, check_calib_runs_to_cap, check_calib_zero_batch, check_calib_scaling,
+    check_calib_verifier,
 ]

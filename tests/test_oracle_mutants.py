@@ -42,6 +42,16 @@ MUTANTS = [
      "for (int i = 0; i + 1 < counts[k]; ++i)\n                s = s +"),
     ("verifier_accepts_any_scale", "if (E[go] <= (1.0 + 1e-6) * E[gbest]) ct++;", "if (1) ct++;"),
     ("verifier_skips_codes", "if (qo != qr) {", "if (0) {"),
+    ("calib_error_not_mean", "return s / (double)N;", "return s;"),
+    ("calib_strict_stop", "if (n >= 1 && e <= thr) return 1;", "if (n >= 1 && e < thr) return 1;"),
+    ("calib_threshold_never_relative",
+     "return cal->relative ? cal->eps * calib_error(w, d, cal->X, cal->N) : cal->eps;",
+     "return cal->eps;"),
+    ("calib_x_transposed", "y += v[j] * (double)X[j * N + t];", "y += v[j] * (double)X[t * d + j];"),
+    ("calib_error_of_weights", "e = calib_error(r, d, cal->X, cal->N);          /* Eq. (12) */",
+     "e = calib_error(w, d, cal->X, cal->N);          /* Eq. (12) */"),
+    ("calib_stop_ignores_cap", "if (n >= P || Er == 0.0) return 1;", "if (Er == 0.0) return 1;"),
+    ("calib_no_minimum_one_point", "if (n >= 1 && e <= thr) return 1;", "if (e <= thr) return 1;"),
 ]
 
 
