@@ -459,6 +459,32 @@ def check_calib_verifier(orc):
     assert status(codes, scales, counts, e32, x8) == 8
 
 
+def check_calib_verifier_fp32_evaluation(orc):
+    """The S4 verifier accepts output errors evaluated as the GPU does (the
+    difference rounded to fp32, fp32 products and sums: numpy float32
+    matmul), also for one- and three-column batches whose outputs can nearly
+    cancel, and still flags a 1e-4 relative change of a well-averaged one."""
+    rng = np.random.default_rng(17)
+    d, P = 300, 5
+    W = rng.standard_normal((200, d)).astype(np.float32)
+    for N in (1, 3, 512):
+        X = rng.standard_normal((d, N)).astype(np.float32)
+        codes, scales, counts, err, xerr = orc.fit_calib(W, 4, P, 64, X, 1e-3, True)
+        x32 = np.zeros((W.shape[0], P), np.float32)
+        for k in range(W.shape[0]):
+            D = W[k].astype(np.float64)
+            for i in range(counts[k]):
+                D = D - float(scales[k, i]) * codes[k, i].astype(np.float64)
+                y = D.astype(np.float32) @ X
+                x32[k, i] = np.float32(np.mean(y.astype(np.float64) ** 2))
+        v = orc.verify_calib(W, 4, P, 64, X, 1e-3, True, codes, scales, counts, None, x32)
+        assert (v["status"] == 0).all(), (N, np.nonzero(v["status"])[0][:5])
+        if N == 512:
+            x32[:, 0] *= np.float32(1 + 1e-4)
+            v = orc.verify_calib(W, 4, P, 64, X, 1e-3, True, codes, scales, counts, None, x32)
+            assert (v["status"] == 8).all()
+
+
 ALL_CHECKS = [
     check_levels, check_rounding_ties, check_codes_bruteforce, check_grid_search_bruteforce,
     check_grid_search_bounds, check_two_point_joint, check_naive_quantizer,
@@ -466,5 +492,5 @@ ALL_CHECKS = [
     check_reconstruct, check_invariances, check_output_error, check_stop_rule,
     check_exponential_decay, check_verifier, check_calib_hadamard_is_isotropic,
     check_calib_stop_definition, check_calib_runs_to_cap, check_calib_zero_batch, check_calib_scaling,
-    check_calib_verifier,
+    check_calib_verifier, check_calib_verifier_fp32_evaluation,
 ]

@@ -50,6 +50,10 @@ MUTANTS = [
     ("calib_x_transposed", "y += v[j] * (double)X[j * N + t];", "y += v[j] * (double)X[t * d + j];"),
     ("calib_error_of_weights", "e = calib_error(r, d, cal->X, cal->N);          /* Eq. (12) */",
      "e = calib_error(w, d, cal->X, cal->N);          /* Eq. (12) */"),
+    ("calib_no_fp32_allowance", "const double lam = 4.0 * 0x1p-24 * sqrt((double)d);",
+     "const double lam = 0.0;"),
+    ("calib_loose_fp32_allowance", "const double lam = 4.0 * 0x1p-24 * sqrt((double)d);",
+     "const double lam = 0x1p-8 * sqrt((double)d);"),
     ("calib_stop_ignores_cap", "if (n >= P || Er == 0.0) return 1;", "if (Er == 0.0) return 1;"),
     ("calib_no_minimum_one_point", "if (n >= 1 && e <= thr) return 1;", "if (e <= thr) return 1;"),
 ]
