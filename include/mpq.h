@@ -96,7 +96,7 @@ int mpq_fit_layer(const float *W, int64_t c_out, int64_t d, int bits, int max_po
                   float *scales, int32_t *counts, float *err_opt, void *stream);
 
 /*
- * How mpq_fit_layer evaluates Eq. (9): for d <= 16384 it counts, per element
+ * How mpq_fit_layer evaluates Eq. (9): for d <= 32768 it counts, per element
  * and code level k, the candidates whose boundary (k + 1/2) a_g lies below
  * |r_j|, accumulates exact integer histograms, and gets every candidate's
  * error from ||r||^2 - 2 a A(g) + a^2 B(g) in fp64 (A, B: suffix sums), in
@@ -116,7 +116,7 @@ int mpq_fit_layer_dense(const float *W, int64_t c_out, int64_t d, int bits, int 
 
 /*
  * mpq_fit_max_dim - largest channel length d that mpq_fit_layer accepts for
- * n_grid candidates on the current device: the larger of 16384 (the
+ * n_grid candidates on the current device: the larger of 32768 (the
  * histogram search keeps a channel's residual in the registers of one
  * workgroup) and the dense search's limit (the residual staged in the LDS of
  * one workgroup).  Returns a negative MPQ_* status on failure.
@@ -181,6 +181,7 @@ typedef struct mpq_layer {
     float *out_err;       /* mpq_output_error_layers: [c_out]                      */
     float *out_ref;       /* mpq_output_error_layers: NULL or [c_out]              */
     float *W_hat;         /* mpq_reconstruct_layers: [c_out][d]                    */
+    float *fit_xerr;      /* mpq_fit_layers_calib: [c_out][max_points]             */
 } mpq_layer;
 
 /* mpq_fit_layer on every layer (reads W, c_out, d, codes, scales, counts,
@@ -211,6 +212,45 @@ int mpq_reconstruct_layers(const mpq_layer *layers, int n_layers, int max_points
  */
 int mpq_quantize_layers(const mpq_layer *layers, int n_layers, int bits, int max_points,
                         const float *grid_host, int n_grid, float tol, void *stream);
+
+/*
+ * mpq_fit_layer_calib - the greedy fit of mpq_fit_layer with Algorithm 2's
+ * stopping rule on a calibration batch (Sec. 3.3, Eq. (12)) instead of the
+ * isotropic one.  For each channel k, after each point n >= 1:
+ *   e_n = (1/n_cols) sum_t ( (w_k - w~_k,n) . x_t )^2     (x_t: column t of X)
+ * is computed as mpq_output_error does (fp64 difference rounded to fp32,
+ * fp32 MFMA products, fp64 sum over the batch), and the channel stops once
+ *   e_n <= thr,  thr = eps * (1/n_cols) sum_t (w_k . x_t)^2   (relative != 0)
+ *                thr = eps                                  (relative == 0),
+ * or at max_points, or when its residual is zero.  The points themselves
+ * are Algorithm 1's, which does not see X: a channel's points are the first
+ * ones mpq_fit_layer would choose with tol = 0.  A nonzero channel gets at
+ * least one point.
+ *
+ * The fit runs one step at a time: step s takes point s + 1 of every channel
+ * still going, then scores those channels' output error on the batch (only
+ * theirs), so the work follows the points each channel actually takes.
+ *
+ * Arguments as for mpq_fit_layer (tol replaced by eps and relative), plus
+ *   X          [d][n] fp32 calibration inputs (input), 1 <= n <= MPQ_MAX_ERR_DIM.
+ *   eps        threshold, finite and >= 0 (relative or absolute).
+ *   relative   nonzero: thr relative to the output error of w itself.
+ *   xerr       [c_out][max_points] fp32 (output): e_n after each point n,
+ *              zero after the count.
+ *   c_out <= MPQ_MAX_ERR_DIM; d within the histogram search (d <= 32768,
+ *   else MPQ_ERR_SHAPE).
+ * Errors: MPQ_ERR_INVALID_ARG, MPQ_ERR_SHAPE, MPQ_ERR_NOMEM, MPQ_ERR_HIP.
+ */
+int mpq_fit_layer_calib(const float *W, int64_t c_out, int64_t d, int bits, int max_points,
+                        const float *grid_host, int n_grid, const float *X, int64_t n, float eps,
+                        int relative, int8_t *codes, float *scales, int32_t *counts, float *err_opt,
+                        float *xerr, void *stream);
+
+/* mpq_fit_layer_calib on every layer (reads W, c_out, d, codes, scales,
+ * counts, fit_err, X, n, fit_xerr).  Each step's fits run side by side and
+ * its output errors run as one batch over all layers. */
+int mpq_fit_layers_calib(const mpq_layer *layers, int n_layers, int bits, int max_points,
+                         const float *grid_host, int n_grid, float eps, int relative, void *stream);
 
 /*
  * Per-launch timing (instrumentation, not part of the method).  While it is

@@ -290,6 +290,7 @@ std::vector<FitJob> build_fit_jobs(Search mode, bool hist_fits, const mpq_layer 
         j.b.G = n_grid;
         j.b.grid = dgrid;
         j.b.tol = (double)tol;
+        j.b.step = -1;   // the whole fit (calibration steps set it per launch)
         return j;
     };
     auto add_layer = [&](FitJob &j, int l) {
@@ -596,6 +597,142 @@ int quantize_impl(const mpq_layer *layers, int n_layers, int bits, int max_point
     return MPQ_OK;
 }
 
+// Algorithm 2's stopping rule on a calibration batch, for every layer.  Per
+// step s = 0 .. max_points - 1: the fit launches take point s + 1 of every
+// channel that has not stopped (a channel stops once the output error of its
+// points is at most the threshold) and list those channels; then the
+// output-error pass scores the listed channels of every layer.  The relative
+// threshold's output error of W runs beside the first fit step.
+int calib_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
+               const float *grid_host, int n_grid, float eps, int relative, void *stream)
+{
+    if (n_layers < 0 || (n_layers > 0 && !layers))
+        return fail(MPQ_ERR_INVALID_ARG, "layers must hold n_layers >= 0 entries");
+    if (!(eps >= 0.0f) || !isfinite(eps))
+        return fail(MPQ_ERR_INVALID_ARG, "eps must be finite and >= 0");
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_layer &L = layers[l];
+        int rc = MPQ_OK;
+        if (L.c_out > 0) {
+            if (!L.X || !L.fit_xerr) rc = fail(MPQ_ERR_INVALID_ARG, "X and xerr must not be NULL");
+            else if (L.n < 1) rc = fail(MPQ_ERR_INVALID_ARG, "n must be >= 1 (got %lld)", (long long)L.n);
+            else if (L.n > MPQ_MAX_ERR_DIM || L.c_out > MPQ_MAX_ERR_DIM)
+                rc = fail(MPQ_ERR_INVALID_ARG, "c_out and n must be <= %d (got %lld, %lld)",
+                          MPQ_MAX_ERR_DIM, (long long)L.c_out, (long long)L.n);
+        }
+        if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
+    }
+    bool any = false, hist_fits = false;
+    int rc = fit_checks(Search::kAuto, layers, n_layers, bits, max_points, grid_host, n_grid, 0.0f,
+                        &any, &hist_fits);
+    if (rc != MPQ_OK || !any) return rc;
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_layer &L = layers[l];
+        if (L.c_out > 0 && !(hist_fits && mpq::fit_hist_supports(L.d)))
+            return fail(MPQ_ERR_SHAPE, "%sd = %lld: the calibration fit needs the histogram search "
+                        "(d <= %lld, n_grid within its LDS)", n_layers > 1 ? "a layer's " : "",
+                        (long long)L.d, (long long)mpq::kHistMaxDim);
+    }
+    hipStream_t s = (hipStream_t)stream;
+    const int P = max_points;
+
+    // state: every layer's per-step list lengths [P] (contiguous, zeroed
+    // together), then per layer its channel list [C] and W's output error [C]
+    std::vector<size_t> off_list(n_layers), off_ref(n_layers);
+    size_t bytes = (sizeof(int32_t) * (size_t)P * (size_t)n_layers + 255) / 256 * 256;
+    for (int l = 0; l < n_layers; ++l) {
+        const size_t C = (size_t)std::max<int64_t>(layers[l].c_out, 0);
+        off_list[l] = bytes;
+        bytes += (sizeof(int32_t) * C + 255) / 256 * 256;
+        off_ref[l] = bytes;
+        if (relative) bytes += (sizeof(float) * C + 255) / 256 * 256;
+    }
+    float *dgrid = nullptr;
+    rc = upload_grid(grid_host, n_grid, s, &dgrid);
+    if (rc != MPQ_OK) return rc;
+    char *state = nullptr;
+    hipError_t e = mpq::scratch_alloc((void **)&state, bytes, s);
+    if (e != hipSuccess) {
+        if (dgrid) (void)mpq::scratch_free(dgrid, s);
+        return fail(MPQ_ERR_NOMEM, "scratch of %zu bytes: %s", bytes, hipGetErrorString(e));
+    }
+    auto nlist = [&](int l) { return (int32_t *)state + (size_t)l * P; };
+    auto list = [&](int l) { return (int32_t *)(state + off_list[l]); };
+    auto ref = [&](int l) { return relative ? (float *)(state + off_ref[l]) : nullptr; };
+
+    const int M = (1 << (bits - 1)) - 1;
+    std::vector<FitJob> jobs = build_fit_jobs(Search::kAuto, true, layers, n_layers, M, P, dgrid,
+                                              n_grid, 0.0f, -1.0);
+    for (FitJob &j : jobs) {
+        j.b.eps = (double)eps;
+        for (int i = 0; i < j.b.n_layers; ++i) {
+            const int l = j.layers[i];
+            mpq::HistLayer &H = j.b.L[i];
+            H.xerr = layers[l].fit_xerr;
+            H.ref = ref(l);
+            H.list = list(l);
+            H.nlist = nlist(l);
+        }
+    }
+    // the output-error items of one step (the same groups every step), and
+    // the reference items of the relative threshold
+    std::vector<mpq::ErrLayerIn> in, in_ref;
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_layer &L = layers[l];
+        if (L.c_out == 0) continue;
+        in.push_back(mpq::ErrLayerIn{L.W, L.codes, L.scales, L.counts, L.X, L.fit_xerr, nullptr,
+                                     L.c_out, L.d, L.n, list(l), nlist(l), P});
+        if (relative)
+            in_ref.push_back(mpq::ErrLayerIn{L.W, L.codes, L.scales, L.counts, L.X, nullptr, ref(l),
+                                             L.c_out, L.d, L.n, nullptr, nullptr, 0});
+    }
+    ErrJobs ej, ej_ref;
+    rc = err_jobs(in, s, &ej);
+    if (rc == MPQ_OK && relative) rc = err_jobs(in_ref, s, &ej_ref);
+    auto release = [&]() {
+        if (ej_ref.scratch) (void)mpq::scratch_free(ej_ref.scratch, s);
+        if (ej.scratch) (void)mpq::scratch_free(ej.scratch, s);
+        (void)mpq::scratch_free(state, s);
+        if (dgrid) (void)mpq::scratch_free(dgrid, s);
+    };
+    if (rc != MPQ_OK) {
+        release();
+        return rc;
+    }
+    e = mpq::launch_zero_i32((int32_t *)state, (int64_t)P * n_layers, s);
+    std::vector<double> fit_work;
+    for (const FitJob &j : jobs) fit_work.push_back(j.work);
+    for (int step = 0; step < P && e == hipSuccess; ++step) {
+        for (FitJob &j : jobs) j.b.step = step;
+        // the fit step; at step 0 beside it the output error of W (ref)
+        std::vector<double> w = fit_work;
+        const int n_fit = (int)w.size();
+        if (step == 0) w.insert(w.end(), ej_ref.work.begin(), ej_ref.work.end());
+        e = run_concurrently(s, w, [&](int i, hipStream_t st) {
+            return i < n_fit ? launch_fit_job(jobs[i], n_grid, st)
+                             : launch_err_job(in_ref, ej_ref, i - n_fit, P, st);
+        });
+        if (e != hipSuccess) break;
+        // the output error of the channels that took point step + 1
+        std::vector<mpq::ErrLayerIn> in_s = in;
+        {
+            int i = 0;
+            for (int l = 0; l < n_layers; ++l) {
+                if (layers[l].c_out == 0) continue;
+                in_s[i].err = layers[l].fit_xerr + step;
+                in_s[i].nrows = nlist(l) + step;
+                ++i;
+            }
+        }
+        e = run_concurrently(s, ej.work, [&](int i, hipStream_t st) {
+            return launch_err_job(in_s, ej, i, P, st);
+        });
+    }
+    release();
+    if (e != hipSuccess) return hip_fail(e, "calibration fit launch");
+    return MPQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -656,6 +793,31 @@ int mpq_quantize_layers(const mpq_layer *layers, int n_layers, int bits, int max
                         const float *grid_host, int n_grid, float tol, void *stream)
 {
     return quantize_impl(layers, n_layers, bits, max_points, grid_host, n_grid, tol, stream);
+}
+
+int mpq_fit_layer_calib(const float *W, int64_t c_out, int64_t d, int bits, int max_points,
+                        const float *grid_host, int n_grid, const float *X, int64_t n, float eps,
+                        int relative, int8_t *codes, float *scales, int32_t *counts, float *err_opt,
+                        float *xerr, void *stream)
+{
+    mpq_layer L = {};
+    L.W = W;
+    L.c_out = c_out;
+    L.d = d;
+    L.codes = codes;
+    L.scales = scales;
+    L.counts = counts;
+    L.fit_err = err_opt;
+    L.X = X;
+    L.n = n;
+    L.fit_xerr = xerr;
+    return calib_impl(&L, 1, bits, max_points, grid_host, n_grid, eps, relative, stream);
+}
+
+int mpq_fit_layers_calib(const mpq_layer *layers, int n_layers, int bits, int max_points,
+                         const float *grid_host, int n_grid, float eps, int relative, void *stream)
+{
+    return calib_impl(layers, n_layers, bits, max_points, grid_host, n_grid, eps, relative, stream);
 }
 
 int mpq_output_error(const float *W, const int8_t *codes, const float *scales,

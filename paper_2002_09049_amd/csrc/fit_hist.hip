@@ -296,7 +296,7 @@ fit_hist_kernel(const HistBatch B)
     __shared__ int s_gbest;
     __shared__ unsigned long long s_scan[kWaves];
     __shared__ ArgMin s_arg[kWaves];
-    __shared__ float s_scale[kGlobal ? MPQ_MAX_POINTS : 1];
+    __shared__ float s_scale[MPQ_MAX_POINTS];
 
     // layer of this workgroup (uniform: the descriptors are kernel arguments)
     int li = 0;
@@ -324,14 +324,16 @@ fit_hist_kernel(const HistBatch B)
     int8_t *qk = Ly.codes + k * (int64_t)P * d;
     const float *wk = Ly.W + k * (int64_t)d;
 
-    double r[kGlobal ? 1 : EPT];
-    if constexpr (!kGlobal) {
-#pragma unroll
-        for (int u = 0; u < EPT; ++u) {
-            const int j = t + T * u;
-            r[u] = j < d ? (double)wk[j] : 0.0;
-        }
+    // calibration step: resume a channel that holds s0 points and has not
+    // stopped (its count is s0), from its stored points; take at most one
+    const bool stepping = B.step >= 0;
+    const int s0 = stepping ? B.step : 0;
+    if (s0 >= 1 && Ly.counts[k] != s0) return;   // uniform: one value per workgroup
+    if (s0 >= 1) {
+        for (int p = t; p < s0; p += T) s_scale[p] = Ly.scales[k * P + p];
+        __syncthreads();
     }
+
     // residual element u of this thread after np points (0 past the channel)
     auto rebuild = [&](int u, int np) {
         const int j = t + T * u;
@@ -340,6 +342,11 @@ fit_hist_kernel(const HistBatch B)
         for (int p = 0; p < np; ++p) v = fma(-(double)s_scale[p], (double)qk[(int64_t)p * d + j], v);
         return v;
     };
+    double r[kGlobal ? 1 : EPT];
+    if constexpr (!kGlobal) {
+#pragma unroll
+        for (int u = 0; u < EPT; ++u) r[u] = rebuild(u, s0);
+    }
 
     for (int g = t; g < G; g += T)
         S.c[g] = B.grid ? B.grid[g] : (float)((double)(g + 1) / (double)G);
@@ -347,7 +354,8 @@ fit_hist_kernel(const HistBatch B)
     double Ew = 0.0;
     float apend = 0.0f;
     int n = 0;
-    for (int i = 0;; ++i) {
+    bool more = false;   // calibration step: the channel took its point and goes on
+    for (int i = s0;; ++i) {
         // ---- apply the pending point: codes of Eq. (10), residual of Eq. (7)
         float lmax = 0.0f;
         double lsum = 0.0;
@@ -358,8 +366,8 @@ fit_hist_kernel(const HistBatch B)
         for (int u = 0; u < EPT; ++u) {
             const int j = t + T * u;
             if (kGlobal && T * u >= d) break;
-            double ru = kGlobal ? rebuild(u, i >= 1 ? i - 1 : 0) : r[u];
-            if (i >= 1 && j < d) {
+            double ru = kGlobal ? rebuild(u, i > s0 ? i - 1 : i) : r[u];
+            if (i > s0 && j < d) {
                 // y is within |y| 2^-51 of the fp64 quotient fl(r / a), so the
                 // two round to the same integer unless y lies within 2^-40 of a
                 // half-integer (or |y| >= 2^10, where both clip to the same M);
@@ -381,8 +389,24 @@ fit_hist_kernel(const HistBatch B)
 
         // ---- stop / point count
         if (i == 0) Ew = Er;
-        else if (Ly.err && t == 0) Ly.err[k * P + (i - 1)] = (float)Er;
-        if ((i >= P) || (Er == 0.0) || (i >= 1 && Er <= B.tol * Ew)) {
+        else if (i > s0 && Ly.err && t == 0) Ly.err[k * P + (i - 1)] = (float)Er;
+        if (stepping && i > s0) {   // one point per calibration step
+            n = i;
+            more = true;
+            break;
+        }
+        bool stop = (i >= P) || (Er == 0.0);
+        if (!stop && i >= 1) {
+            if (stepping) {
+                // output error of the i points on the batch (the error pass
+                // of the previous step) against the threshold
+                const double thr = Ly.ref ? B.eps * (double)Ly.ref[k] : B.eps;
+                stop = (double)Ly.xerr[k * P + (i - 1)] <= thr;
+            } else {
+                stop = Er <= B.tol * Ew;
+            }
+        }
+        if (stop) {
             n = i;
             break;
         }
@@ -586,15 +610,20 @@ fit_hist_kernel(const HistBatch B)
         apend = (float)S.ad[gstar + 1];
         if (t == 0) {
             Ly.scales[k * P + i] = apend;
-            if constexpr (kGlobal) s_scale[i] = apend;
+            s_scale[i] = apend;
         }
         __syncthreads();   // S.a is rewritten by the next step
     }
 
     if (t == 0) Ly.counts[k] = n;
+    if (more) {
+        if (t == 0) Ly.list[atomicAdd(Ly.nlist + s0, 1)] = (int32_t)k;
+        return;
+    }
     for (int q = n + t; q < P; q += T) {
         Ly.scales[k * P + q] = 0.0f;
         if (Ly.err) Ly.err[k * P + q] = 0.0f;
+        if (stepping) Ly.xerr[k * P + q] = 0.0f;
     }
     for (int q = n; q < P; ++q)
         for (int j = t; j < d; j += T) qk[(int64_t)q * d + j] = 0;
@@ -685,6 +714,23 @@ std::string hist_kernel_name(int64_t d, int M, int G, bool default_grid)
              !default_grid ? "grid" : lattice_buckets(v, M, G, true) ? "lattice" : "linear",
              kVariants[v].rebuilt ? ",rebuilt" : "");
     return name;
+}
+
+namespace {
+__global__ void zero_i32_kernel(int32_t *p, int64_t n)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0;
+}
+}  // namespace
+
+hipError_t launch_zero_i32(int32_t *p, int64_t n, hipStream_t s)
+{
+    if (n <= 0) return hipSuccess;
+    if (n > (int64_t)256 * 0x7fffffff) return hipErrorInvalidValue;
+    LaunchTimer timer(s, "zero_i32_kernel");
+    hipLaunchKernelGGL(zero_i32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, p, n);
+    return hipGetLastError();
 }
 
 hipError_t launch_fit_hist(const HistBatch &batch, int variant, int64_t channels, hipStream_t s)

@@ -69,6 +69,11 @@ struct HistLayer {
     float *scales;      // [C][P]
     int32_t *counts;    // [C]
     float *err;         // [C][P] or nullptr
+    // calibration steps (HistBatch::step >= 0) only:
+    float *xerr;        // [C][P] output error after each point (written by the error pass)
+    const float *ref;   // [C] output error of W itself (relative threshold) or nullptr
+    int32_t *list;      // [C] channels that took a point in this step, in any order
+    int32_t *nlist;     // [P] their number, per step (zero before the first step)
     int d;
     int c_begin;        // first workgroup of this layer in the launch
 };
@@ -79,8 +84,16 @@ struct HistBatch {
     const float *grid;  // device multipliers or nullptr (default grid)
     double tol;
     int nlat;           // lattice buckets ((2M-1) G + 1) or 0; set by launch_fit_hist
+    // -1: the whole fit with the stopping rule on ||r||^2 (tol).  s >= 0: one
+    // step of the fit on a calibration batch: a channel holding s points
+    // (all channels when s = 0) stops if s >= 1 and xerr[s-1] <= thr
+    // (thr = eps * ref, or eps when ref is null), else takes point s + 1 and
+    // enters the step's list.
+    int step;
+    double eps;
     HistLayer L[kMaxBatchLayers];
 };
+static_assert(sizeof(HistBatch) <= 4096, "kernel arguments");
 
 size_t fit_hist_lds(int G);
 bool fit_hist_supports(int64_t d);
@@ -89,6 +102,8 @@ int hist_variant(int64_t d);   // layers with equal variants may share a launch
 // when default_grid, else a caller's grid), as LaunchTimer records it.
 std::string hist_kernel_name(int64_t d, int M, int G, bool default_grid);
 hipError_t launch_fit_hist(const HistBatch &b, int variant, int64_t channels, hipStream_t s);
+// Zeroes n int32 (a fill kernel: safe under stream capture).
+hipError_t launch_zero_i32(int32_t *p, int64_t n, hipStream_t s);
 
 // Output error of Eq. (12) for a list of layers.
 struct ErrLayerIn {
@@ -97,11 +112,17 @@ struct ErrLayerIn {
     const float *scales;
     const int32_t *counts;
     const float *X;
-    float *err;
+    float *err;     // nullptr: no err item for this layer
     float *ref;     // nullptr: no ref for this layer
     int64_t C, d, n;
+    // err item restricted to the channels rows[0 .. *nrows) (device, read
+    // when the kernels run), err[rows[m] * err_stride] written; rows ==
+    // nullptr: every channel, err[k * err_stride] (err_stride 0 means 1)
+    const int32_t *rows;
+    const int32_t *nrows;
+    int64_t err_stride;
 };
-// The items (an err item per layer, a ref item per layer that wants ref) go
+// The items (an err item per layer with err, a ref item per layer with ref) go
 // in launch groups of up to 24; groups are independent and may run side by
 // side, each with its own scratch.
 int err_group_count(const ErrLayerIn *in, int n_in);

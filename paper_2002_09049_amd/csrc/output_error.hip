@@ -22,6 +22,12 @@
 //     row); a layer whose K is split (to balance a grid of long and short
 //     K ranges) stores its fp32 Y tiles per K range instead.
 //
+// An err item may be restricted to a device list of channels (rows of D =
+// the listed channels, in list order; the list length is read by each
+// kernel, and workgroups past it return at once), with the result of row m
+// written to err[rows[m] * stride].  A row's result does not depend on its
+// position, so the list order does not matter.
+//
 //  3. finish: per row, the partials summed in column-tile order, or the K
 //     ranges of Y summed in range order, squared and summed over the columns;
 //     divided by n.  Every order is fixed, so results are deterministic.  The
@@ -82,6 +88,9 @@ struct ErrLayer {
     float *Dt;           // [d][ldc]
     double *rowpart;     // [ntn][C]
     float *ypart;        // [splits][C][n] (splits > 1)
+    const int32_t *rows; // nullptr, or the channels of rows 0 .. *nrows of D
+    const int32_t *nrows;
+    int64_t stride;      // out[channel * stride]
     int C, d, n, ldc;
     int ntm, ntn, splits, kchunk;
     int tiles;           // ntm * ntn * splits
@@ -123,14 +132,17 @@ __global__ void __launch_bounds__(256) form_dt_kernel(const ErrGroup g)
     const int64_t d = L.d, C = L.C;
     const int64_t row0 = (int64_t)rt * kFT, k0 = (int64_t)kt * kFT;
     const int t = threadIdx.x;
+    const int64_t nact = L.rows ? (int64_t)*L.nrows : C;
+    if (row0 >= nact) return;
 
     // load: four rows (rb + 16 i) of four consecutive k (kc) per thread
     const int kc = (t % 16) * 4, rb = t / 16;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int64_t row = row0 + rb + 16 * i, k = k0 + kc;
+        const int64_t m = row0 + rb + 16 * i, k = k0 + kc;
         double r[4] = {0.0, 0.0, 0.0, 0.0};
-        if (row < C) {
+        if (m < nact) {
+            const int64_t row = L.rows ? (int64_t)L.rows[m] : m;
             const int nk = L.use_points ? min(max(L.counts[row], 0), P) : 0;  // counts is caller data
             const float *wr = L.W + row * d;
             const int8_t *cr = L.codes + row * (int64_t)P * d;
@@ -203,11 +215,13 @@ gemm_err_kernel(const ErrGroup g)
         ++tm;
     }
 
+    const int64_t row0 = (int64_t)tm * kBM;
+    if (L.rows && row0 >= (int64_t)*L.nrows) return;   // past the listed channels
+
     const int t = threadIdx.x;
     const int lane = t % kWave, wid = t / kWave;
     const int wm = wid / 2, wn = wid % 2;
     const int64_t C = L.C, n = L.n;
-    const int64_t row0 = (int64_t)tm * kBM;
     const int64_t col0 = (int64_t)tn * kBN;
     const int64_t kbeg = (int64_t)split * L.kchunk;
     const int64_t kend = min(kbeg + (int64_t)L.kchunk, (int64_t)L.d);
@@ -346,16 +360,20 @@ __global__ void __launch_bounds__(256) finish_err_kernel(const ErrGroup g)
     const ErrLayer &L = g.L[li];
     const int64_t C = L.C, n = L.n;
     const int b = (int)blockIdx.x - L.fin_begin;
+    const int64_t nact = L.rows ? (int64_t)*L.nrows : C;
+    // output slot of row m of D
+    auto slot = [&](int64_t m) { return (L.rows ? (int64_t)L.rows[m] : m) * L.stride; };
     if (L.splits == 1) {
         const int64_t k = (int64_t)b * 256 + threadIdx.x;
-        if (k < C) {
+        if (k < nact) {
             double s = 0.0;
             for (int i = 0; i < L.ntn; ++i) s += L.rowpart[(int64_t)i * C + k];
-            L.out[k] = (float)(s / (double)n);
+            L.out[slot(k)] = (float)(s / (double)n);
         }
         return;
     }
     const int64_t k = b;
+    if (k >= nact) return;
     double s = 0.0;
     for (int64_t c = threadIdx.x; c < n; c += 256) {
         float y = 0.0f;
@@ -363,7 +381,7 @@ __global__ void __launch_bounds__(256) finish_err_kernel(const ErrGroup g)
         s = fma((double)y, (double)y, s);
     }
     s = block_reduce<256>(s, SumOp(), red);
-    if (threadIdx.x == 0) L.out[k] = (float)(s / (double)n);
+    if (threadIdx.x == 0) L.out[slot(k)] = (float)(s / (double)n);
 }
 
 struct Item {
@@ -378,12 +396,12 @@ struct Plan {
 
 size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
-// err items for every layer, then ref items for the layers that want ref
+// err items for the layers that want err, then ref items for the layers that want ref
 std::vector<Item> items_of(const ErrLayerIn *in, int n_in)
 {
     std::vector<Item> it;
     for (int i = 0; i < n_in; ++i)
-        if (in[i].C > 0) it.push_back(Item{&in[i], 1});
+        if (in[i].C > 0 && in[i].err) it.push_back(Item{&in[i], 1});
     for (int i = 0; i < n_in; ++i)
         if (in[i].C > 0 && in[i].ref) it.push_back(Item{&in[i], 0});
     return it;
@@ -489,6 +507,9 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
             L.X = I.X;
             L.out = grp[i].use_points ? I.err : I.ref;
             L.use_points = grp[i].use_points;
+            L.rows = grp[i].use_points ? I.rows : nullptr;
+            L.nrows = grp[i].use_points ? I.nrows : nullptr;
+            L.stride = grp[i].use_points && I.err_stride > 0 ? I.err_stride : 1;
             L.Dt = (float *)cur;
             cur += q.dt_bytes;
             L.rowpart = (double *)cur;

@@ -31,7 +31,8 @@ MAX_GRID = 4096
 EXPORTS = ("mpq_fit_layer", "mpq_fit_layer_dense", "mpq_fit_layers", "mpq_fit_max_dim",
            "mpq_output_error", "mpq_output_error_layers", "mpq_reconstruct",
            "mpq_reconstruct_layers", "mpq_last_error", "mpq_timing_enable", "mpq_timing_read",
-           "mpq_fit_kernel_of", "mpq_quantize_layers")
+           "mpq_fit_kernel_of", "mpq_quantize_layers", "mpq_fit_layer_calib",
+           "mpq_fit_layers_calib")
 
 
 class Layer(ctypes.Structure):
@@ -40,7 +41,8 @@ class Layer(ctypes.Structure):
                 ("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p),
                 ("counts", ctypes.c_void_p), ("fit_err", ctypes.c_void_p),
                 ("X", ctypes.c_void_p), ("n", ctypes.c_int64), ("out_err", ctypes.c_void_p),
-                ("out_ref", ctypes.c_void_p), ("W_hat", ctypes.c_void_p)]
+                ("out_ref", ctypes.c_void_p), ("W_hat", ctypes.c_void_p),
+                ("fit_xerr", ctypes.c_void_p)]
 
 _lib = None
 
@@ -68,6 +70,11 @@ def load(path: str = LIB_PATH):
     for name in ("mpq_fit_layer", "mpq_fit_layer_dense"):
         getattr(lib, name).argtypes = [P, i64, i64, i32, i32, P, i32, f32, P, P, P, P, P]
         getattr(lib, name).restype = i32
+    lib.mpq_fit_layer_calib.argtypes = [P, i64, i64, i32, i32, P, i32, P, i64, f32, i32, P, P, P, P,
+                                         P, P]
+    lib.mpq_fit_layer_calib.restype = i32
+    lib.mpq_fit_layers_calib.argtypes = [P, i32, i32, i32, P, i32, f32, i32, P]
+    lib.mpq_fit_layers_calib.restype = i32
     lib.mpq_fit_max_dim.argtypes = [i32]
     lib.mpq_fit_max_dim.restype = i64
     lib.mpq_output_error.argtypes = [P, P, P, P, i64, i64, i32, P, i64, P, P, P]
@@ -157,6 +164,39 @@ def fit_layer(W: torch.Tensor, bits: int, max_points: int, n_grid: int, tol: flo
     return codes, scales, counts, err
 
 
+def fit_layer_calib(W: torch.Tensor, bits: int, max_points: int, n_grid: int, X: torch.Tensor,
+                    eps: float, relative: bool = True, grid=None, with_err: bool = True,
+                    stream=None, out=None):
+    """mpq_fit_layer_calib: the fit with Algorithm 2's stopping rule on the
+    calibration batch X [d, n] fp32.  Returns (codes, scales, counts, err or
+    None, xerr [C, P]).  ``out`` may hold preallocated (codes, scales,
+    counts, err, xerr)."""
+    if W.dim() != 2:
+        raise ValueError("W must be 2-D [C_out, d]")
+    C, d = W.shape
+    if X.dim() != 2 or X.shape[0] != d:
+        raise ValueError("X must be [d, n]")
+    dev = W.device
+    if out is None:
+        codes = torch.empty((C, max_points, d), dtype=torch.int8, device=dev)
+        scales = torch.empty((C, max_points), dtype=torch.float32, device=dev)
+        counts = torch.empty((C,), dtype=torch.int32, device=dev)
+        err = torch.empty((C, max_points), dtype=torch.float32, device=dev) if with_err else None
+        xerr = torch.empty((C, max_points), dtype=torch.float32, device=dev)
+    else:
+        codes, scales, counts, err, xerr = out
+    g = LayerSet._grid(grid, n_grid)
+    rc = load().mpq_fit_layer_calib(
+        _dev(W, torch.float32, "W"), C, d, bits, max_points,
+        None if g is None else g.ctypes.data_as(ctypes.c_void_p), n_grid,
+        _dev(X, torch.float32, "X"), X.shape[1], float(eps), 1 if relative else 0,
+        _dev(codes, torch.int8, "codes"), _dev(scales, torch.float32, "scales"),
+        _dev(counts, torch.int32, "counts"), None if err is None else _dev(err, torch.float32, "err"),
+        _dev(xerr, torch.float32, "xerr"), _stream(stream))
+    _check(rc)
+    return codes, scales, counts, err, xerr
+
+
 def fit_max_dim(n_grid: int) -> int:
     v = load().mpq_fit_max_dim(n_grid)
     if v < 0:
@@ -244,7 +284,7 @@ class LayerSet:
         n = len(self.W)
         self.arr = (Layer * max(n, 1))()
         self.codes, self.scales, self.counts, self.fit_err = [], [], [], []
-        self.err, self.ref, self.W_hat = [], [], []
+        self.err, self.ref, self.W_hat, self.xerr = [], [], [], []
         for i, W in enumerate(self.W):
             C, d = W.shape
             dev = W.device
@@ -255,6 +295,8 @@ class LayerSet:
             err = torch.empty((C,), dtype=torch.float32, device=dev)
             ref = torch.empty((C,), dtype=torch.float32, device=dev) if with_ref else None
             what = torch.empty((C, d), dtype=torch.float32, device=dev)
+            xerr = torch.empty((C, max_points), dtype=torch.float32, device=dev) if calib is not None else None
+            self.xerr.append(xerr)
             self.codes.append(codes)
             self.scales.append(scales)
             self.counts.append(counts)
@@ -276,6 +318,7 @@ class LayerSet:
             L.out_err = err.data_ptr() if self.X is not None else None
             L.out_ref = None if ref is None else ref.data_ptr()
             L.W_hat = what.data_ptr()
+            L.fit_xerr = None if xerr is None else xerr.data_ptr()
         self.n = n
 
     @staticmethod
@@ -301,6 +344,17 @@ class LayerSet:
         _check(load().mpq_quantize_layers(ctypes.addressof(self.arr), self.n, bits, self.max_points,
                                           None if g is None else g.ctypes.data_as(ctypes.c_void_p),
                                           n_grid, float(tol), _stream(stream)))
+
+    def fit_calib(self, bits: int, n_grid: int, eps: float, relative: bool = True, grid=None,
+                  stream=None):
+        """mpq_fit_layers_calib: the fit of every layer with Algorithm 2's
+        stopping rule on its calibration batch; xerr [C, P] per layer."""
+        if self.X is None:
+            raise ValueError("LayerSet was built without calibration batches")
+        g = self._grid(grid, n_grid)
+        _check(load().mpq_fit_layers_calib(ctypes.addressof(self.arr), self.n, bits, self.max_points,
+                                           None if g is None else g.ctypes.data_as(ctypes.c_void_p),
+                                           n_grid, float(eps), 1 if relative else 0, _stream(stream)))
 
     def output_error(self, stream=None):
         if self.X is None:

@@ -18,7 +18,7 @@ def to_dev(a):
 
 
 def gpu_fit(W, bits, P, G, tol, grid=None, with_err=True, dense=False):
-    """mpq_fit_layer (histogram search up to d = 16384) or, with dense=True,
+    """mpq_fit_layer (histogram search up to d = 32768) or, with dense=True,
     mpq_fit_layer_dense, through the C ABI."""
     import torch
     from paper_2002_09049_amd import mpq

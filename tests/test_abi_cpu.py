@@ -201,3 +201,51 @@ def test_quantize_layers_checks_every_layer_first(lib):
     for L in arr:
         L.c_out = 0
     assert q(p, 2, 4, 4, None, 8, 1e-3, None) == 0
+
+
+def _calib(lib, **kw):
+    args = dict(W=1, c_out=4, d=16, bits=4, max_points=4, grid=None, n_grid=8, X=1, n=8, eps=1e-3,
+                relative=1, codes=1, scales=1, counts=1, err=None, xerr=1)
+    args.update(kw)
+    g = args["grid"]
+    garr = None if g is None else (ctypes.c_float * len(g))(*g)
+    return lib.mpq_fit_layer_calib(args["W"], args["c_out"], args["d"], args["bits"],
+                                   args["max_points"], garr, args["n_grid"], args["X"], args["n"],
+                                   args["eps"], args["relative"], args["codes"], args["scales"],
+                                   args["counts"], args["err"], args["xerr"], None)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(c_out=-1), dict(d=0), dict(bits=1), dict(max_points=0), dict(max_points=65),
+    dict(n_grid=0), dict(eps=-1.0), dict(eps=float("inf")), dict(eps=float("nan")),
+    dict(W=None), dict(codes=None), dict(X=None), dict(xerr=None), dict(n=0),
+    dict(n=16777217), dict(c_out=16777217), dict(grid=[0.5, 0.25], n_grid=2),
+])
+def test_calib_fit_rejects_invalid_arguments(lib, kw):
+    from paper_2002_09049_amd import mpq
+    assert _calib(lib, **kw) == mpq.MPQ_ERR_INVALID_ARG
+    assert lib.mpq_last_error()
+
+
+def test_calib_fit_with_no_channels_is_a_no_op(lib):
+    assert _calib(lib, c_out=0, W=None, codes=None, scales=None, counts=None, X=None, xerr=None) == 0
+
+
+def test_calib_layers_check_every_layer_first(lib):
+    from paper_2002_09049_amd import mpq
+    E = mpq.MPQ_ERR_INVALID_ARG
+    arr = (mpq.Layer * 2)()
+    for L in arr:
+        L.W, L.c_out, L.d, L.codes, L.scales, L.counts = 1, 4, 16, 1, 1, 1
+        L.X, L.n, L.fit_xerr = 1, 8, 1
+    p = ctypes.addressof(arr)
+    f = lib.mpq_fit_layers_calib
+    arr[1].fit_xerr = None
+    assert f(p, 2, 4, 4, None, 8, 1e-3, 1, None) == E
+    assert b"layer 1" in lib.mpq_last_error()
+    arr[1].fit_xerr = 1
+    assert f(p, 2, 4, 4, None, 8, -1.0, 1, None) == E
+    assert f(p, 2, 9, 4, None, 8, 1e-3, 1, None) == E
+    for L in arr:
+        L.c_out = 0
+    assert f(p, 2, 4, 4, None, 8, 1e-3, 0, None) == 0

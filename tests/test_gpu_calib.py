@@ -1,0 +1,233 @@
+"""Parity of the calibration-batch fit (Algorithm 2's stopping rule, reading
+S4) with the oracle, through the C ABI.
+
+The oracle's lockstep verifier judges every channel: codes, scales and counts
+as for the isotropic fit (V1, V2, V4), the output error after each point
+within 1e-5 relative of the fp64 oracle (V4x), and each stop decision exact
+except within 1e-5 of the threshold (the GPU's e_n is an fp32 GEMM over d).
+"""
+import numpy as np
+import pytest
+
+import bruteforce as bf
+from gpu_util import gpu_fit, say, to_dev
+from paper_2002_09049_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from paper_2002_09049_amd import mpq
+    mpq.load()   # fails loudly if libmpq.so is missing
+    yield
+
+
+def gpu_fit_calib(W, bits, P, G, X, eps, relative, grid=None, with_err=True):
+    import torch
+    from paper_2002_09049_amd import mpq
+    codes, scales, counts, err, xerr = mpq.fit_layer_calib(to_dev(W), bits, P, G, to_dev(X), eps,
+                                                           relative, grid=grid, with_err=with_err)
+    torch.cuda.synchronize()
+    return (codes.cpu().numpy(), scales.cpu().numpy(), counts.cpu().numpy(),
+            None if err is None else err.cpu().numpy(), xerr.cpu().numpy())
+
+
+def assert_calib_parity(orc, W, bits, P, G, X, eps, relative, out, grid=None, channels=None):
+    codes, scales, counts, err, xerr = out
+    v = orc.verify_calib(W, bits, P, G, X, float(np.float32(eps)), relative, codes, scales, counts,
+                         err, xerr, grid=grid, channels=channels)
+    bad = np.nonzero(v["status"])[0]
+    assert bad.size == 0, (f"{bad.size} channels fail: channels {v['channels'][bad][:8]} "
+                           f"status {v['status'][bad][:8]}")
+    return v
+
+
+CASES = [
+    # (C, d, bits, P, G, N, eps, relative)
+    (3, 1, 4, 4, 128, 1, 1e-3, True),
+    (40, 9, 4, 8, 512, 64, 1e-3, True),
+    (33, 17, 3, 8, 7, 5, 1e-2, True),
+    (130, 147, 4, 4, 256, 300, 1e-3, True),
+    (64, 576, 4, 4, 128, 256, 1e-3, True),
+    (257, 64, 3, 8, 512, 129, 5e-4, True),
+    (20, 1000, 2, 6, 64, 200, 1e-2, True),
+    (24, 2305, 4, 8, 256, 1024, 1e-4, True),
+    (12, 4608, 4, 4, 256, 1024, 1e-3, True),
+    (6, 9000, 3, 4, 64, 130, 1e-3, True),
+    (40, 333, 4, 6, 64, 100, 0.0, False),
+]
+
+
+@pytest.mark.parametrize("C,d,bits,P,G,N,eps,rel", CASES,
+                         ids=[f"C{c}_d{d}_b{b}_P{p}_G{g}_N{n}" for c, d, b, p, g, n, _, _ in CASES])
+def test_calib_parity(orc, C, d, bits, P, G, N, eps, rel):
+    say(f"case calib C={C} d={d} bits={bits} P={P} G={G} N={N} eps={eps} rel={rel}")
+    W = wl.random_weights(C, d, seed=7 * C + d)
+    X = wl.random_calib(d, N, seed=N + d)
+    out = gpu_fit_calib(W, bits, P, G, X, eps, rel)
+    v = assert_calib_parity(orc, W, bits, P, G, X, eps, rel, out)
+    counts = out[2]
+    say(f"  counts={np.bincount(counts, minlength=P + 1).tolist()} "
+        f"stop ties={int(v['stop_ties'].sum())} cand ties={int(v['cand_ties'].sum())}")
+    assert (counts >= 1).all()
+
+
+def test_calib_absolute_threshold(orc):
+    """An absolute threshold (the paper's form), set near the median of the
+    first point's output error so that counts spread over 1 .. P."""
+    C, d, N = 96, 576, 256
+    W = wl.random_weights(C, d, seed=3)
+    X = wl.random_calib(d, N, seed=4)
+    say("case calib absolute threshold")
+    _, _, _, _, xe = orc.fit_calib(W, 4, 6, 128, X, 0.0, False)
+    eps = float(np.median(xe[:, 1]))
+    out = gpu_fit_calib(W, 4, 6, 128, X, eps, False)
+    assert_calib_parity(orc, W, 4, 6, 128, X, eps, False, out)
+    assert len(np.unique(out[2])) >= 2
+
+
+def test_calib_points_are_the_isotropic_prefix():
+    """Algorithm 1 does not see X: the calibration fit's points are the
+    first points of the fit that runs to the cap (tol = 0), bitwise, and
+    its fit_err too."""
+    C, d, N, P = 70, 1152, 512, 6
+    W = wl.random_weights(C, d, seed=21)
+    X = wl.random_calib(d, N, seed=22)
+    say("case calib prefix of the uncapped fit")
+    codes, scales, counts, err, xerr = gpu_fit_calib(W, 4, P, 256, X, 2e-3, True)
+    c0, s0, n0, e0 = gpu_fit(W, 4, P, 256, 0.0)
+    for k in range(C):
+        n = counts[k]
+        assert n <= n0[k]
+        assert np.array_equal(codes[k, :n], c0[k, :n]) and np.array_equal(scales[k, :n], s0[k, :n])
+        assert np.array_equal(err[k, :n], e0[k, :n])
+        assert not codes[k, n:].any() and not scales[k, n:].any() and not err[k, n:].any()
+        assert not xerr[k, n:].any()
+
+
+def test_calib_edge_cases(orc):
+    """Zero channels, a zero batch (every output error is 0: one point per
+    nonzero channel), eps = 0 absolute (every channel to the cap), a cap of
+    one point, a single calibration column."""
+    d, N = 200, 64
+    W = wl.random_weights(9, d, seed=5)
+    W[2] = 0.0
+    W[7] = 0.0
+    X = wl.random_calib(d, N, seed=6)
+    say("case calib zero channels")
+    out = gpu_fit_calib(W, 4, 5, 64, X, 1e-3, True)
+    assert_calib_parity(orc, W, 4, 5, 64, X, 1e-3, True, out)
+    assert out[2][2] == 0 and out[2][7] == 0
+    say("case calib zero batch")
+    Z = np.zeros_like(X)
+    out = gpu_fit_calib(W, 4, 5, 64, Z, 1e-3, True)
+    assert_calib_parity(orc, W, 4, 5, 64, Z, 1e-3, True, out)
+    assert (out[2][W.any(axis=1)] == 1).all()
+    say("case calib eps = 0")
+    out = gpu_fit_calib(W, 4, 5, 64, X, 0.0, False)
+    assert_calib_parity(orc, W, 4, 5, 64, X, 0.0, False, out)
+    assert (out[2][W.any(axis=1)] == 5).all()
+    say("case calib cap 1, one column")
+    out = gpu_fit_calib(W, 4, 1, 64, X[:, :1].copy(), 1e-3, True)
+    assert_calib_parity(orc, W, 4, 1, 64, X[:, :1].copy(), 1e-3, True, out)
+
+
+def test_calib_hadamard_batch(orc):
+    """With X X^T = N I the output error is ||r||^2: xerr equals the fit's
+    own err within the output error's tolerance."""
+    d, N = 100, 128
+    W = wl.random_weights(50, d, seed=12)
+    X = bf.hadamard(N)[:d].astype(np.float32)
+    say("case calib Hadamard batch")
+    out = gpu_fit_calib(W, 3, 5, 64, X, 1e-2, True)
+    assert_calib_parity(orc, W, 3, 5, 64, X, 1e-2, True, out)
+    codes, scales, counts, err, xerr = out
+    assert np.allclose(xerr, err, rtol=2e-5, atol=0)
+
+
+def test_calib_explicit_grid_and_no_err(orc):
+    rng = np.random.default_rng(9)
+    grid = np.sort(rng.uniform(0.05, 1.0, 97)).astype(np.float32)
+    W = wl.random_weights(30, 300, seed=8)
+    X = wl.random_calib(300, 90, seed=9)
+    say("case calib explicit grid")
+    out = gpu_fit_calib(W, 4, 6, 97, X, 1e-3, True, grid=grid, with_err=False)
+    assert out[3] is None
+    assert_calib_parity(orc, W, 4, 6, 97, X, 1e-3, True, out, grid=grid)
+
+
+def test_calib_deterministic():
+    W = wl.random_weights(64, 700, seed=31)
+    X = wl.random_calib(700, 300, seed=32)
+    a = gpu_fit_calib(W, 4, 6, 256, X, 1e-3, True)
+    b = gpu_fit_calib(W, 4, 6, 256, X, 1e-3, True)
+    assert all(np.array_equal(x, y) for x, y in zip(a, b))
+
+
+def test_calib_shape_limit():
+    from paper_2002_09049_amd import mpq
+    W = wl.random_weights(2, 40000, seed=1)
+    X = wl.random_calib(40000, 8, seed=2)
+    with pytest.raises(mpq.MPQError) as e:
+        gpu_fit_calib(W, 4, 2, 16, X, 1e-3, True)
+    assert e.value.status == mpq.MPQ_ERR_SHAPE
+
+
+@pytest.mark.parametrize("name", ["resnet18", "mobilenetv2"])
+def test_calib_batched_equals_single_layer_calls(orc, name):
+    """mpq_fit_layers_calib over many layers gives bitwise the outputs of
+    per-layer mpq_fit_layer_calib calls; one layer in lockstep."""
+    import torch
+    from paper_2002_09049_amd import mpq
+    w = wl.get(name)
+    idx = list(range(len(w.layers)))[:14]
+    Ws = [to_dev(wl.layer_weights(w, i)) for i in idx]
+    Xs = [to_dev(wl.layer_calib(w, i, n=256)) for i in idx]
+    say(f"case calib batched {name} ({len(idx)} layers)")
+    ls = mpq.LayerSet(Ws, w.max_points, calib=Xs)
+    ls.fit_calib(w.bits, w.n_grid, w.tol, True)
+    torch.cuda.synchronize()
+    for j in range(len(idx)):
+        c, s, n, e, xe = mpq.fit_layer_calib(Ws[j], w.bits, w.max_points, w.n_grid, Xs[j], w.tol, True)
+        torch.cuda.synchronize()
+        assert torch.equal(c, ls.codes[j]) and torch.equal(s, ls.scales[j])
+        assert torch.equal(n, ls.counts[j]) and torch.equal(e, ls.fit_err[j])
+        assert torch.equal(xe, ls.xerr[j])
+    j = len(idx) - 1
+    out = (ls.codes[j].cpu().numpy(), ls.scales[j].cpu().numpy(), ls.counts[j].cpu().numpy(),
+           ls.fit_err[j].cpu().numpy(), ls.xerr[j].cpu().numpy())
+    assert_calib_parity(orc, Ws[j].cpu().numpy(), w.bits, w.max_points, w.n_grid,
+                        Xs[j].cpu().numpy(), w.tol, True, out)
+
+
+@pytest.mark.parametrize("name", ["resnet18", "vgg16fc"])
+def test_calib_workload_full_size_sampled(orc, name):
+    """Every layer of the workload through mpq_fit_layers_calib at full size
+    with its full calibration batch (the benchmark's launch configuration);
+    sampled channels per layer checked in lockstep."""
+    import torch
+    from paper_2002_09049_amd import mpq
+    w = wl.get(name)
+    Ws = [to_dev(wl.layer_weights(w, i)) for i in range(len(w.layers))]
+    Xs = [to_dev(wl.layer_calib(w, i)) for i in range(len(w.layers))]
+    say(f"case calib workload {name} full size")
+    ls = mpq.LayerSet(Ws, w.max_points, calib=Xs)
+    ls.fit_calib(w.bits, w.n_grid, w.tol, True)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(1)
+    hist = np.zeros(w.max_points + 1, np.int64)
+    for li, (C, d) in enumerate(w.layers):
+        k = 3 if d > 4096 else 8
+        ch = np.unique(np.concatenate([[0, C - 1], rng.choice(C, size=min(k, C), replace=False)]))
+        counts = ls.counts[li].cpu().numpy()
+        hist += np.bincount(counts, minlength=w.max_points + 1)
+        out = (ls.codes[li].cpu().numpy(), ls.scales[li].cpu().numpy(), counts,
+               ls.fit_err[li].cpu().numpy(), ls.xerr[li].cpu().numpy())
+        say(f"  layer {li} ({C}x{d})")
+        assert_calib_parity(orc, Ws[li].cpu().numpy(), w.bits, w.max_points, w.n_grid,
+                            Xs[li].cpu().numpy(), w.tol, True, out, channels=ch)
+        assert (counts >= 1).all() and (counts <= w.max_points).all()
+    say(f"  {name}: point counts {hist.tolist()}")
