@@ -9,6 +9,11 @@ in turn, with the time of each stage).  The default workload is the
 ResNet-18-shaped stack (21 layers, 5,800 channels, 4 bits, up to 4 points,
 256 candidate scales, tol 1e-3, 1,024 calibration columns).
 
+--rule calib times the path with Algorithm 2's stopping rule on the
+calibration batch instead (mpq_fit_layers_calib, whose per-point output
+errors are the scoring, then mpq_reconstruct_layers); tol is then the
+relative threshold eps.
+
 Prints one JSON line.  `value` is channel-points fitted per second over the
 whole step (sum of the per-channel point counts of all layers / step time).
 Every kernel launch of the timed steps is timed by HIP events that the
@@ -53,6 +58,9 @@ def parse():
     ap.add_argument("--dense", action="store_true",
                     help="fit with mpq_fit_layer_dense (O(d G) search) instead of mpq_fit_layer "
                          "(implies --separate)")
+    ap.add_argument("--rule", choices=("tol", "calib"), default="tol",
+                    help="stopping rule: ||r||^2 <= tol ||w||^2 (default), or Algorithm 2's on the "
+                         "calibration batch (output error <= tol x that of W)")
     ap.add_argument("--separate", action="store_true",
                     help="the three batched calls in turn instead of mpq_quantize_layers")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -87,11 +95,14 @@ def sources_digest():
 
 def kernel_key(profiler_name):
     """The library's timing name of a kernel from the demangled name rocprofv3
-    prints (fit_hist_kernel<T, EPT, kLinear, kLat> -> fit_hist_kernel<T,EPT,mode>)."""
-    m = re.search(r"fit_hist_kernel<(\d+), (\d+), (true|false), (true|false)>", profiler_name)
+    prints (fit_hist_kernel<T, EPT, kLinear, kLat, kGlobal> ->
+    fit_hist_kernel<T,EPT,mode[,rebuilt]>)."""
+    m = re.search(r"fit_hist_kernel<(\d+), (\d+), (true|false), (true|false), (true|false)>",
+                  profiler_name)
     if m:
         mode = "lattice" if m.group(4) == "true" else "linear" if m.group(3) == "true" else "grid"
-        return f"fit_hist_kernel<{m.group(1)},{m.group(2)},{mode}>"
+        rebuilt = ",rebuilt" if m.group(5) == "true" else ""
+        return f"fit_hist_kernel<{m.group(1)},{m.group(2)},{mode}{rebuilt}>"
     m = re.search(r"(\w+_kernel)\b", profiler_name)
     return m.group(1) if m else None
 
@@ -165,7 +176,7 @@ def measured_traffic(key):
     return None
 
 
-def summarize_trace(trace_dir, bench_json=None, steps=6):
+def summarize_trace(trace_dir, bench_json=None, steps=6, rule="tol"):
     """Per-kernel average duration of a traced bench run (kernel_stats.csv of
     rocprofv3 --stats), beside the event-timed averages of a bench.py line."""
     import csv
@@ -184,15 +195,22 @@ def summarize_trace(trace_dir, bench_json=None, steps=6):
         a[0] += int(r["Calls"])
         a[1] += float(r["TotalDurationNs"])
     bench = json.load(open(bench_json)) if bench_json else None
-    lines = ["# rocprofv3 kernel summary: ResNet-18-shaped workload, bench step", "",
+    calib = rule == "calib"
+    r = " --rule calib" if calib else ""
+    what = ("the fit with Algorithm 2's stopping rule on each layer's calibration batch (one point\n"
+            "per step, each step scored on the batch; relative threshold 1e-3) and the\n"
+            "reconstruction, through mpq_fit_layers_calib and mpq_reconstruct_layers."
+            if calib else
+            "fit + output error + reconstruction of every layer through the batched C ABI calls.")
+    lines = [f"# rocprofv3 kernel summary: ResNet-18-shaped workload, bench step{r}", "",
              "Workload: 21 layers (5,800 channels, 11,678,912 weights), 4 bits, up to 4 points,",
-             "256 candidate scales, tol 1e-3, calibration batches d x 1024.  One step = fit +",
-             "output error + reconstruction of every layer through the batched C ABI calls.", "",
+             "256 candidate scales, tol 1e-3, calibration batches d x 1024.  One step =",
+             what, "",
              "Commands (one MI355X, from the repository root):", "", "```",
              "rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof -o kt -- \\",
-             "    python3 bench.py --steps 5 --warmup 1 --no-cpu-baseline",
-             "python3 bench.py --steps 5 --warmup 1 > gpurun_out/bench.json",
-             "python3 bench.py --summarize-trace gpurun_out/prof --bench-json gpurun_out/bench.json",
+             f"    python3 bench.py{r} --steps 5 --warmup 1 --no-cpu-baseline",
+             f"python3 bench.py{r} --steps 5 --warmup 1 > gpurun_out/bench.json",
+             f"python3 bench.py{r} --summarize-trace gpurun_out/prof --bench-json gpurun_out/bench.json",
              "```", "",
              f"The traced process ran {steps} steps (warm-up + timed).  Kernels of one stage may",
              "run concurrently on several streams.  `bench avg us` is the untraced run's average",
@@ -219,7 +237,8 @@ def main():
         summarize_pmc(*args.summarize_pmc, steps=args.traced_steps or 2)
         return 0
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace, args.bench_json, steps=args.traced_steps or 6)
+        summarize_trace(args.summarize_trace, args.bench_json, steps=args.traced_steps or 6,
+                        rule=args.rule)
         return 0
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -252,8 +271,15 @@ def main():
         del src, dst
 
     separate = args.separate or args.dense
+    calib = args.rule == "calib"
+    if calib and separate:
+        raise SystemExit("--rule calib has its own call sequence (no --separate / --dense)")
 
     def step(ev=None):
+        if calib:
+            ls.fit_calib(wk.bits, wk.n_grid, wk.tol, True)
+            ls.reconstruct()
+            return
         if not separate:
             ls.quantize(wk.bits, wk.n_grid, wk.tol)
             return
@@ -303,18 +329,30 @@ def main():
             w[a] = w.get(a, 0) + b
 
     points = 0
+    count_hist = np.zeros(wk.max_points + 1, np.int64)
     for i, W in enumerate(Ws):
         C, d = W.shape
-        n = int(ls.counts[i].cpu().numpy().astype(np.int64).sum())
+        cnt = ls.counts[i].cpu().numpy().astype(np.int64)
+        count_hist += np.bincount(cnt, minlength=wk.max_points + 1)
+        n = int(cnt.sum())
         N = Xs[i].shape[1]
         points += n
         fk = "fit_dense_kernel" if args.dense else fit_kernel.setdefault(
             d, mpq.fit_kernel_of(d, wk.bits, wk.n_grid, True))
-        # fit: G candidate errors per (element, point); reads W once, writes the codes
-        add(fk, evals=n * wk.n_grid * d, bytes=4 * C * d + n * d)
-        add("gemm_err_kernel", flop=2 * C * d * N)
-        # form: reads W and the codes of the used points, writes D
-        add("form_dt_kernel", bytes=4 * C * d + n * d + 4 * C * d)
+        if calib:
+            # step s scores the channels that took point s + 1 (sum of counts
+            # rows in all), plus W itself once for the relative threshold;
+            # a fit step re-reads W and the codes of the points so far
+            code_reads = int((cnt * (cnt - 1) // 2).sum())
+            add(fk, evals=n * wk.n_grid * d, bytes=4 * n * d + code_reads * d + n * d)
+            add("gemm_err_kernel", flop=2 * (n + C) * d * N)
+            add("form_dt_kernel", bytes=8 * (n + C) * d + (n + code_reads) * d)
+        else:
+            # fit: G candidate errors per (element, point); reads W once, writes the codes
+            add(fk, evals=n * wk.n_grid * d, bytes=4 * C * d + n * d)
+            add("gemm_err_kernel", flop=2 * C * d * N)
+            # form: reads W and the codes of the used points, writes D
+            add("form_dt_kernel", bytes=4 * C * d + n * d + 4 * C * d)
         # reconstruct: reads the codes of the used points, writes fp32
         add("reconstruct_kernel", bytes=n * d + 4 * C * d)
 
@@ -378,7 +416,11 @@ def main():
                    "weights": wk.weights, "bits": wk.bits, "max_points": wk.max_points,
                    "n_grid": wk.n_grid, "tol": wk.tol, "calib_columns": wk.n_calib,
                    "points_per_step": points, "search": "dense" if args.dense else "histogram",
-                   "calls": "separate" if separate else "mpq_quantize_layers",
+                   "rule": ("Algorithm 2 on the calibration batch, relative" if calib
+                            else "||r||^2 <= tol ||w||^2"),
+                   "point_counts": count_hist.tolist(),
+                   "calls": ("mpq_fit_layers_calib + mpq_reconstruct_layers" if calib else
+                             "separate" if separate else "mpq_quantize_layers"),
                    "parallelism": "none"},
         "roofline": roofline,
         "stages_ms_per_step": {k: round(v, 5) for k, v in stages.items()} or None,
@@ -388,13 +430,14 @@ def main():
     }
 
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(wk, args.cpu_stride)
+        res["cpu_baseline"] = cpu_baseline(wk, args.cpu_stride, calib)
     print(json.dumps(res), flush=True)
     return 0
 
 
-def cpu_baseline(wk, stride):
-    """The fp64 oracle, as it stands, on every stride-th channel of every layer."""
+def cpu_baseline(wk, stride, calib=False):
+    """The fp64 oracle, as it stands, on every stride-th channel of every layer
+    (calib: its fit with Algorithm 2's rule on the layer's batch)."""
     import numpy as np
 
     import oracle
@@ -405,14 +448,20 @@ def cpu_baseline(wk, stride):
     secs = 0.0
     for li in range(len(wk.layers)):
         W = np.ascontiguousarray(wl.layer_weights(wk, li)[::stride])
+        X = wl.layer_calib(wk, li) if calib else None
         t0 = time.perf_counter()
-        _, _, counts, _ = orc.fit(W, wk.bits, wk.max_points, wk.n_grid, float(np.float32(wk.tol)),
-                                  n_threads=cores)
+        if calib:
+            counts = orc.fit_calib(W, wk.bits, wk.max_points, wk.n_grid, X, float(np.float32(wk.tol)),
+                                   True, n_threads=cores)[2]
+        else:
+            _, _, counts, _ = orc.fit(W, wk.bits, wk.max_points, wk.n_grid,
+                                      float(np.float32(wk.tol)), n_threads=cores)
         secs += time.perf_counter() - t0
         pts += int(counts.sum())
     return {"value": round(pts / secs, 2), "unit": "channel-points/s", "cores": cores,
             "kind": "oracle",
-            "sample": f"every {stride}th channel of each of the {len(wk.layers)} layers of {wk.name} "
+            "sample": f"{'calibration-rule fit, ' if calib else ''}"
+                      f"every {stride}th channel of each of the {len(wk.layers)} layers of {wk.name} "
                       f"({pts} channel-points, {secs:.1f} s wall)"}
 
 
