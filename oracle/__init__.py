@@ -63,6 +63,10 @@ def _declare(lib):
     lib.oracle_levels.restype = i32
     lib.oracle_default_grid.argtypes = [i32, P]
     lib.oracle_default_grid.restype = None
+    lib.oracle_integer_scales.argtypes = [P, P, i64, i32, i32, P]
+    lib.oracle_integer_scales.restype = i64
+    lib.oracle_integer_forward.argtypes = [P, P, P, i64, i64, i32, P, i64, i32, P]
+    lib.oracle_integer_forward.restype = i32
     return lib
 
 
@@ -250,6 +254,31 @@ class Oracle:
                                    _p(np.ascontiguousarray(counts, dtype=np.int32)), C, d, P, _p(out))
         return out
 
+    def integer_scales(self, scales, counts, p: int):
+        """Eq. (14) (reading I1). Returns (A [C,P] int32, number clamped)."""
+        scales = np.ascontiguousarray(scales, dtype=np.float32)
+        counts = np.ascontiguousarray(counts, dtype=np.int32)
+        C, P = scales.shape
+        A = np.zeros((C, P), np.int32)
+        n = self.lib.oracle_integer_scales(_p(scales), _p(counts), C, P, int(p), _p(A))
+        return A, int(n)
+
+    def integer_forward(self, codes_, A, counts, X, p: int):
+        """Eq. (15), Steps 1-3 (readings B1, I2).  codes [C,P,d] int8, A [C,P]
+        int32, X [N,d] int8.  Returns Y [C,N] int64."""
+        codes_ = np.ascontiguousarray(codes_, dtype=np.int8)
+        C, P, d = codes_.shape
+        X = np.ascontiguousarray(X, dtype=np.int8)
+        assert X.shape[1] == d
+        N = X.shape[0]
+        Y = np.zeros((C, N), np.int64)
+        rc = self.lib.oracle_integer_forward(
+            _p(codes_), _p(np.ascontiguousarray(A, dtype=np.int32)),
+            _p(np.ascontiguousarray(counts, dtype=np.int32)), C, d, P, _p(X), N, int(p), _p(Y))
+        if rc != 0:
+            raise OverflowError("oracle_integer_forward: a sum left its integer range")
+        return Y
+
 
 def _delegate(name):
     def f(*args, **kw):
@@ -260,5 +289,6 @@ def _delegate(name):
 
 
 for _n in ("levels", "default_grid", "candidate_scales", "codes", "scale_error", "fit",
-           "verify", "fit_calib", "verify_calib", "output_error", "reconstruct"):
+           "verify", "fit_calib", "verify_calib", "output_error", "reconstruct",
+           "integer_scales", "integer_forward"):
     globals()[_n] = _delegate(_n)

@@ -15,6 +15,9 @@
  *     q as the rounding of r / a (Eq. (8), (10)); residual by Eq. (7).
  *   Sec. 3.3, Eq. (12) and Algorithm 2: output error on a calibration
  *     batch; points are added until the error falls below a threshold.
+ *   Sec. 3.4, Eq. (14)-(15): integer scales A_i = [2^p a_i] and the layer's
+ *     integer dot products in three steps (point products in 32-bit
+ *     accumulators, the A_i-weighted sum, a shift by p).
  *
  * Readings taken where the paper is silent, ambiguous or garbled (the same
  * readings bind the HIP library):
@@ -43,6 +46,13 @@
  *   A1     No refit of a once q is fixed.
  *   E1     Output error: mean over the N columns of X of ((w - w~) . x)^2.
  *   P1     Scales are stored as fp32 values (exactly the candidate value).
+ *   I1     Eq. (14) rounds 2^p a_i to the nearest integer with ties to even
+ *          (R1); a value outside the 32-bit range is clamped to
+ *          [-(2^31 - 1), 2^31 - 1] and counted.
+ *   B1     Step 3's "shift by p bits" is a division by 2^p: an arithmetic
+ *          right shift of the 64-bit sum, i.e. the floor of sum / 2^p.
+ *   I2     Activations are signed integers held in int8, one vector of d per
+ *          column of the batch; Step 2 sums in 64 bits.
  */
 #include <math.h>
 #include <stdint.h>
@@ -574,4 +584,58 @@ void oracle_reconstruct(const int8_t *codes, const float *scales,
             W_hat[k * d + j] = (float)s;
         }
     }
+}
+
+/* ------------------------------------------------------------------------
+ * Sec. 3.4: deployment arithmetic.
+ * ------------------------------------------------------------------------ */
+
+/* Eq. (14), reading I1: A_i = nearest integer to 2^p a_i (ties to even) for
+ * the points i < counts[k] of each channel, zero after the count.  2^p a_i is
+ * exact in fp64.  Returns the number of values clamped to the 32-bit range. */
+int64_t oracle_integer_scales(const float *scales, const int32_t *counts, int64_t C, int P, int p,
+                              int32_t *A)
+{
+    const double lim = 2147483647.0;
+    int64_t clamped = 0;
+    for (int64_t k = 0; k < C; ++k) {
+        for (int i = 0; i < P; ++i) {
+            double v = 0.0;
+            if (i < counts[k]) {
+                v = rint(ldexp((double)scales[k * P + i], p));   /* round to nearest, ties even */
+                if (v > lim) { v = lim; ++clamped; }
+                if (v < -lim) { v = -lim; ++clamped; }
+            }
+            A[k * P + i] = (int32_t)v;
+        }
+    }
+    return clamped;
+}
+
+/* Eq. (15), Steps 1-3, for channel k and column t of the batch (X [N][d]):
+ *   Step 1: z_i = q_i . x_t for every point i < counts[k], each in a 32-bit
+ *           accumulator;
+ *   Step 2: s = sum_{i < counts[k]} A_i z_i, in 64 bits;
+ *   Step 3: y = s shifted right by p (reading B1: floor(s / 2^p)).
+ * Y [C][N] int64.  Returns -1 if some z_i leaves the 32-bit range or some s
+ * the 64-bit range (checked with 128-bit arithmetic), else 0. */
+int oracle_integer_forward(const int8_t *codes, const int32_t *A, const int32_t *counts, int64_t C,
+                           int64_t d, int P, const int8_t *X, int64_t N, int p, int64_t *Y)
+{
+    int bad = 0;
+    for (int64_t k = 0; k < C; ++k) {
+        for (int64_t t = 0; t < N; ++t) {
+            __int128 s = 0;
+            for (int i = 0; i < counts[k]; ++i) {
+                const int8_t *q = codes + (k * P + i) * d;
+                int64_t z = 0;
+                for (int64_t j = 0; j < d; ++j) z += (int64_t)q[j] * (int64_t)X[t * d + j];
+                if (z > INT32_MAX || z < INT32_MIN) bad = 1;
+                s += (__int128)A[k * P + i] * (__int128)z;
+            }
+            if (s > (__int128)INT64_MAX || s < (__int128)INT64_MIN) bad = 1;
+            Y[k * N + t] = (int64_t)s >> p;   /* arithmetic shift: floor division */
+        }
+    }
+    return bad ? -1 : 0;
 }

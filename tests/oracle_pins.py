@@ -485,6 +485,88 @@ def check_calib_verifier_fp32_evaluation(orc):
             assert (v["status"] == 8).all()
 
 
+# ------------------------------------------- Sec. 3.4: deployment arithmetic
+def check_integer_scales(orc):
+    """Eq. (14), reading I1: exact values, half-way ties to even (worked by
+    hand), |A - 2^p a| <= 1/2, zero after the count, clamping counted."""
+    p = 6
+    u = 2.0 ** -p
+    a = np.array([[2.5 * u, 3.5 * u, -2.5 * u, 0.5 * u, 1.5 * u, 5 * u, -7 * u]], np.float32)
+    A, n = orc.integer_scales(a, np.array([7], np.int32), p)
+    assert A[0].tolist() == [2, 4, -2, 0, 2, 5, -7] and n == 0
+    rng = np.random.default_rng(2)
+    s = rng.standard_normal((40, 5)).astype(np.float32) * 0.1
+    counts = rng.integers(0, 6, 40).astype(np.int32)
+    for p in (0, 7, 13, 20):
+        A, n = orc.integer_scales(s, counts, p)
+        assert n == 0
+        for k in range(40):
+            c = counts[k]
+            assert (A[k, c:] == 0).all()
+            assert (np.abs(A[k, :c].astype(np.float64) - np.ldexp(s[k, :c].astype(np.float64), p))
+                    <= 0.5).all()
+    A, n = orc.integer_scales(np.array([[1.0, -1.0, 0.25]], np.float32), np.array([3], np.int32), 31)
+    assert A[0].tolist() == [2 ** 31 - 1, -(2 ** 31 - 1), 2 ** 29] and n == 2
+
+
+def _int_case(seed, C=6, P=3, d=13, N=7):
+    rng = np.random.default_rng(seed)
+    codes = rng.integers(-7, 8, (C, P, d)).astype(np.int8)     # nonzero past the counts too
+    A = rng.integers(-(2 ** 20), 2 ** 20, (C, P)).astype(np.int32)
+    counts = rng.integers(0, P + 1, C).astype(np.int32)
+    counts[0], counts[1] = 0, P
+    X = rng.integers(-128, 128, (N, d)).astype(np.int8)
+    return codes, A, counts, X
+
+
+def check_integer_forward_exact(orc):
+    """Eq. (15), Steps 1-3 against exact Python integers: floor of
+    sum_{i<n} A_i (q_i . x) over 2^p; rows and A past the count ignored;
+    negative sums floor (reading B1)."""
+    for seed, p in ((1, 0), (2, 5), (3, 17), (4, 40)):
+        codes, A, counts, X = _int_case(seed)
+        Y = orc.integer_forward(codes, A, counts, X, p)
+        C, P, d = codes.shape
+        neg = 0
+        for k in range(C):
+            for t in range(X.shape[0]):
+                s = 0
+                for i in range(int(counts[k])):
+                    z = sum(int(codes[k, i, j]) * int(X[t, j]) for j in range(d))
+                    s += int(A[k, i]) * z
+                neg += s < 0 and s % (1 << p) != 0
+                assert int(Y[k, t]) == s // (1 << p), (seed, k, t)
+        assert p == 0 or neg > 0
+
+
+def check_integer_forward_one_point(orc):
+    """One point with A = 2^p (a = 1): Step 3 undoes the scale, Y = Q X^T."""
+    codes, _, _, X = _int_case(5, C=9, P=2, d=40, N=11)
+    counts = np.ones(9, np.int32)
+    p = 12
+    A = np.full((9, 2), 1 << p, np.int32)
+    Y = orc.integer_forward(codes, A, counts, X, p)
+    assert np.array_equal(Y, codes[:, 0, :].astype(np.int64) @ X.T.astype(np.int64))
+
+
+def check_integer_forward_approximates(orc):
+    """Eq. (14)-(15) approximate the real multipoint product: with A from the
+    fitted scales, |y - sum_i a_i z_i| <= 2^(-p-1) sum_i |z_i| + 1."""
+    rng = np.random.default_rng(7)
+    W = rng.standard_normal((20, 64)).astype(np.float32)
+    codes, scales, counts, _ = orc.fit(W, 4, 4, 64, 0.0)
+    X = rng.integers(-128, 128, (15, 64)).astype(np.int8)
+    for p in (8, 16, 24):
+        A, n = orc.integer_scales(scales * 64, counts, p)
+        assert n == 0
+        Y = orc.integer_forward(codes, A, counts, X, p)
+        Z = np.einsum("kij,tj->kit", codes.astype(np.float64), X.astype(np.float64))
+        mask = (np.arange(4)[None, :] < counts[:, None]).astype(np.float64)
+        exact = np.einsum("ki,kit->kt", (scales * 64).astype(np.float64) * mask, Z)
+        bound = np.einsum("ki,kit->kt", mask, np.abs(Z)) * 2.0 ** (-p - 1) + 1.0
+        assert (np.abs(Y - exact) <= bound).all(), p
+
+
 ALL_CHECKS = [
     check_levels, check_rounding_ties, check_codes_bruteforce, check_grid_search_bruteforce,
     check_grid_search_bounds, check_two_point_joint, check_naive_quantizer,
@@ -492,5 +574,6 @@ ALL_CHECKS = [
     check_reconstruct, check_invariances, check_output_error, check_stop_rule,
     check_exponential_decay, check_verifier, check_calib_hadamard_is_isotropic,
     check_calib_stop_definition, check_calib_runs_to_cap, check_calib_zero_batch, check_calib_scaling,
-    check_calib_verifier, check_calib_verifier_fp32_evaluation,
+    check_calib_verifier, check_calib_verifier_fp32_evaluation, check_integer_scales,
+    check_integer_forward_exact, check_integer_forward_one_point, check_integer_forward_approximates,
 ]

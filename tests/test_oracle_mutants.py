@@ -54,6 +54,16 @@ MUTANTS = [
      "const double lam = 0.0;"),
     ("calib_loose_fp32_allowance", "const double lam = 4.0 * 0x1p-24 * sqrt((double)d);",
      "const double lam = 0x1p-8 * sqrt((double)d);"),
+    ("int_shift_truncates", "Y[k * N + t] = (int64_t)s >> p;",
+     "Y[k * N + t] = (int64_t)s / ((int64_t)1 << p);"),
+    ("int_scale_floor", "v = rint(ldexp((double)scales[k * P + i], p));",
+     "v = floor(ldexp((double)scales[k * P + i], p));"),
+    ("int_scale_ties_away", "v = rint(ldexp((double)scales[k * P + i], p));",
+     "v = round(ldexp((double)scales[k * P + i], p));"),
+    ("int_forward_all_points", "for (int i = 0; i < counts[k]; ++i) {\n                const int8_t *q",
+     "for (int i = 0; i < P; ++i) {\n                const int8_t *q"),
+    ("int_x_transposed", "(int64_t)X[t * d + j]", "(int64_t)X[j * N + t]"),
+    ("int_scale_no_clamp", "if (v > lim) { v = lim; ++clamped; }", "if (v > lim) { ++clamped; }"),
     ("calib_stop_ignores_cap", "if (n >= P || Er == 0.0) return 1;", "if (Er == 0.0) return 1;"),
     ("calib_no_minimum_one_point", "if (n >= 1 && e <= thr) return 1;", "if (e <= thr) return 1;"),
 ]
