@@ -47,6 +47,7 @@ extern "C" {
 #define MPQ_MAX_POINTS 64
 #define MPQ_MAX_GRID 4096
 #define MPQ_MAX_ERR_DIM 16777216   /* c_out and n of mpq_output_error */
+#define MPQ_MAX_INT_DIM 131072     /* d of mpq_integer_forward */
 
 /*
  * mpq_fit_layer - greedy multipoint fit of every channel of a layer
@@ -251,6 +252,62 @@ int mpq_fit_layer_calib(const float *W, int64_t c_out, int64_t d, int bits, int 
  * its output errors run as one batch over all layers. */
 int mpq_fit_layers_calib(const mpq_layer *layers, int n_layers, int bits, int max_points,
                          const float *grid_host, int n_grid, float eps, int relative, void *stream);
+
+/*
+ * Deployment arithmetic (Sec. 3.4).
+ *
+ * mpq_integer_scales - the integer scales of Eq. (14):
+ *   A[k][i] = nearest integer to 2^p * scales[k][i] (ties to even; 2^p a is
+ *   exact in fp64) for i < counts[k], 0 after the count.  A value beyond
+ *   the 32-bit range is clamped to +-(2^31 - 1); if n_clamped_opt is not
+ *   NULL, the number of clamped values is added to it (a DEVICE uint64 the
+ *   caller zeroes).
+ *   scales [c_out][max_points] fp32, counts [c_out] int32 in [0, max_points]
+ *   (inputs); A [c_out][max_points] int32 (output); 0 <= p <= 62.
+ * Errors: MPQ_ERR_INVALID_ARG, MPQ_ERR_HIP.
+ */
+int mpq_integer_scales(const float *scales, const int32_t *counts, int64_t c_out, int max_points, int p,
+                       int32_t *A, unsigned long long *n_clamped_opt, void *stream);
+
+/*
+ * mpq_integer_forward - a multipoint layer's integer dot products on a batch
+ * of integer activations (Eq. (15), Steps 1-3).  For channel k and column t:
+ *   Step 1  z_i = q_{k,i} . x_t   for i < counts[k], in 32-bit accumulators
+ *           (int8 MFMA; exact for codes in [-127, 127], as the fit writes
+ *           them, any int8 activations and d <= MPQ_MAX_INT_DIM)
+ *   Step 2  s = sum_{i < counts[k]} A[k][i] * z_i, in 64 bits
+ *   Step 3  Y[k][t] = s >> p, an arithmetic right shift (floor(s / 2^p))
+ * Y is exact while |s| < 2^63 (e.g. |A| < 2^31 and counts[k] * d * 128 * 128
+ * < 2^32).  Codes past a channel's count, and their A, are not read.
+ *
+ * Arguments
+ *   codes    [c_out][max_points][d] int8 (the fit's codes), A [c_out][max_points]
+ *            int32 (mpq_integer_scales), counts [c_out] int32 in [0, max_points].
+ *   X        [n][d] int8: column t of the batch is the contiguous row X[t]
+ *            (signed activation integers; the batch is stored transposed
+ *            with respect to mpq_output_error's fp32 X).
+ *   Y        [c_out][n] int64 (output).
+ *   c_out, n >= 0; 1 <= d <= MPQ_MAX_INT_DIM; codes and X each below 2^31
+ *   bytes; 0 <= p <= 62.
+ * Errors: MPQ_ERR_INVALID_ARG, MPQ_ERR_HIP.
+ */
+int mpq_integer_forward(const int8_t *codes, const int32_t *A, const int32_t *counts, int64_t c_out,
+                        int64_t d, int max_points, const int8_t *X, int64_t n, int p, int64_t *Y,
+                        void *stream);
+
+/* mpq_integer_forward on a list of layers (HOST array; DEVICE pointers),
+ * with one launch per 32 layers.  All layers share max_points and p. */
+typedef struct mpq_int_layer {
+    const int8_t *codes;    /* [c_out][max_points][d] */
+    const int32_t *A;       /* [c_out][max_points]    */
+    const int32_t *counts;  /* [c_out]                */
+    int64_t c_out, d;
+    const int8_t *X;        /* [n][d]                 */
+    int64_t n;
+    int64_t *Y;             /* [c_out][n]             */
+} mpq_int_layer;
+int mpq_integer_forward_layers(const mpq_int_layer *layers, int n_layers, int max_points, int p,
+                               void *stream);
 
 /*
  * Per-launch timing (instrumentation, not part of the method).  While it is

@@ -733,9 +733,91 @@ int calib_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
     return MPQ_OK;
 }
 
+// Sec. 3.4: integer forward of a list of layers, in launches of up to
+// kMaxIntLayers layers (all checks first).
+int int_forward_impl(const mpq_int_layer *layers, int n_layers, int max_points, int p, void *stream)
+{
+    if (n_layers < 0 || (n_layers > 0 && !layers))
+        return fail(MPQ_ERR_INVALID_ARG, "layers must hold n_layers >= 0 entries");
+    if (max_points < 1 || max_points > MPQ_MAX_POINTS)
+        return fail(MPQ_ERR_INVALID_ARG, "max_points must be in [1, %d] (got %d)", MPQ_MAX_POINTS,
+                    max_points);
+    if (p < 0 || p > 62) return fail(MPQ_ERR_INVALID_ARG, "p must be in [0, 62] (got %d)", p);
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_int_layer &L = layers[l];
+        int rc = MPQ_OK;
+        if (L.c_out < 0 || L.d < 1 || L.n < 0)
+            rc = fail(MPQ_ERR_INVALID_ARG, "need c_out >= 0, d >= 1, n >= 0 (got %lld, %lld, %lld)",
+                      (long long)L.c_out, (long long)L.d, (long long)L.n);
+        else if (L.d > MPQ_MAX_INT_DIM)
+            rc = fail(MPQ_ERR_INVALID_ARG, "d must be <= %d (got %lld)", MPQ_MAX_INT_DIM, (long long)L.d);
+        else if (L.c_out > 0 && L.n > 0 && (!L.codes || !L.A || !L.counts || !L.X || !L.Y))
+            rc = fail(MPQ_ERR_INVALID_ARG, "codes, A, counts, X and Y must not be NULL");
+        else if ((double)L.c_out * max_points * (double)L.d >= 2147483648.0 ||
+                 (double)L.n * (double)L.d >= 2147483648.0)
+            rc = fail(MPQ_ERR_INVALID_ARG, "codes and X must each be below 2^31 bytes");
+        if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    mpq::IntGroup g;
+    g.P = max_points;
+    g.p = p;
+    g.n_layers = 0;
+    for (int l = 0; l <= n_layers; ++l) {
+        if ((l == n_layers || g.n_layers == mpq::kMaxIntLayers) && g.n_layers > 0) {
+            const hipError_t e = mpq::launch_int_forward(g, s);
+            if (e != hipSuccess) return hip_fail(e, "integer forward kernel launch");
+            g.n_layers = 0;
+        }
+        if (l == n_layers) break;
+        const mpq_int_layer &L = layers[l];
+        if (L.c_out == 0 || L.n == 0) continue;
+        mpq::IntLayer &I = g.L[g.n_layers++];
+        I.codes = L.codes;
+        I.A = L.A;
+        I.counts = L.counts;
+        I.X = L.X;
+        I.Y = L.Y;
+        I.C = L.c_out;
+        I.d = L.d;
+        I.N = L.n;
+    }
+    return MPQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+int mpq_integer_scales(const float *scales, const int32_t *counts, int64_t c_out, int max_points, int p,
+                       int32_t *A, unsigned long long *n_clamped_opt, void *stream)
+{
+    if (c_out < 0) return fail(MPQ_ERR_INVALID_ARG, "c_out must be >= 0 (got %lld)", (long long)c_out);
+    if (max_points < 1 || max_points > MPQ_MAX_POINTS)
+        return fail(MPQ_ERR_INVALID_ARG, "max_points must be in [1, %d] (got %d)", MPQ_MAX_POINTS,
+                    max_points);
+    if (p < 0 || p > 62) return fail(MPQ_ERR_INVALID_ARG, "p must be in [0, 62] (got %d)", p);
+    if (c_out > 0 && (!scales || !counts || !A))
+        return fail(MPQ_ERR_INVALID_ARG, "scales, counts and A must not be NULL");
+    const hipError_t e = mpq::launch_integer_scales(scales, counts, c_out, max_points, p, A, n_clamped_opt,
+                                                    (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "integer scales kernel launch");
+    return MPQ_OK;
+}
+
+int mpq_integer_forward(const int8_t *codes, const int32_t *A, const int32_t *counts, int64_t c_out,
+                        int64_t d, int max_points, const int8_t *X, int64_t n, int p, int64_t *Y,
+                        void *stream)
+{
+    mpq_int_layer L = {codes, A, counts, c_out, d, X, n, Y};
+    return int_forward_impl(&L, 1, max_points, p, stream);
+}
+
+int mpq_integer_forward_layers(const mpq_int_layer *layers, int n_layers, int max_points, int p,
+                               void *stream)
+{
+    return int_forward_impl(layers, n_layers, max_points, p, stream);
+}
 
 int64_t mpq_fit_max_dim(int n_grid)
 {

@@ -147,4 +147,29 @@ struct RecLayer {
 constexpr int kMaxRecLayers = 64;
 hipError_t launch_reconstruct(const RecLayer *in, int n_in, int P, hipStream_t s);
 
+// Deployment arithmetic (Sec. 3.4).
+hipError_t launch_integer_scales(const float *scales, const int32_t *counts, int64_t C, int P, int p,
+                                 int32_t *A, unsigned long long *clamped, hipStream_t s);
+
+// Integer forward of up to kMaxIntLayers layers in one launch (one
+// workgroup per 128 x 128 tile of Y); ntn and block_begin are set by
+// launch_int_forward.  Each layer's codes and X are below 2^31 bytes.
+struct IntLayer {
+    const int8_t *codes;    // [C][P][d]
+    const int32_t *A;       // [C][P]
+    const int32_t *counts;  // [C]
+    const int8_t *X;        // [N][d]
+    int64_t *Y;             // [C][N]
+    int64_t C, d, N;
+    int ntn, block_begin;
+};
+constexpr int kMaxIntLayers = 32;
+struct IntGroup {
+    int n_layers;
+    int P, p;
+    IntLayer L[kMaxIntLayers];
+};
+static_assert(sizeof(IntGroup) <= 4096, "kernel arguments");
+hipError_t launch_int_forward(IntGroup &g, hipStream_t s);
+
 }  // namespace mpq

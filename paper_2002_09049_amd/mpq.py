@@ -32,7 +32,8 @@ EXPORTS = ("mpq_fit_layer", "mpq_fit_layer_dense", "mpq_fit_layers", "mpq_fit_ma
            "mpq_output_error", "mpq_output_error_layers", "mpq_reconstruct",
            "mpq_reconstruct_layers", "mpq_last_error", "mpq_timing_enable", "mpq_timing_read",
            "mpq_fit_kernel_of", "mpq_quantize_layers", "mpq_fit_layer_calib",
-           "mpq_fit_layers_calib")
+           "mpq_fit_layers_calib", "mpq_integer_scales", "mpq_integer_forward",
+           "mpq_integer_forward_layers")
 
 
 class Layer(ctypes.Structure):
@@ -43,6 +44,15 @@ class Layer(ctypes.Structure):
                 ("X", ctypes.c_void_p), ("n", ctypes.c_int64), ("out_err", ctypes.c_void_p),
                 ("out_ref", ctypes.c_void_p), ("W_hat", ctypes.c_void_p),
                 ("fit_xerr", ctypes.c_void_p)]
+
+
+
+class IntLayer(ctypes.Structure):
+    """struct mpq_int_layer (include/mpq.h)."""
+    _fields_ = [("codes", ctypes.c_void_p), ("A", ctypes.c_void_p), ("counts", ctypes.c_void_p),
+                ("c_out", ctypes.c_int64), ("d", ctypes.c_int64), ("X", ctypes.c_void_p),
+                ("n", ctypes.c_int64), ("Y", ctypes.c_void_p)]
+
 
 _lib = None
 
@@ -75,6 +85,12 @@ def load(path: str = LIB_PATH):
     lib.mpq_fit_layer_calib.restype = i32
     lib.mpq_fit_layers_calib.argtypes = [P, i32, i32, i32, P, i32, f32, i32, P]
     lib.mpq_fit_layers_calib.restype = i32
+    lib.mpq_integer_scales.argtypes = [P, P, i64, i32, i32, P, P, P]
+    lib.mpq_integer_scales.restype = i32
+    lib.mpq_integer_forward.argtypes = [P, P, P, i64, i64, i32, P, i64, i32, P, P]
+    lib.mpq_integer_forward.restype = i32
+    lib.mpq_integer_forward_layers.argtypes = [P, i32, i32, i32, P]
+    lib.mpq_integer_forward_layers.restype = i32
     lib.mpq_fit_max_dim.argtypes = [i32]
     lib.mpq_fit_max_dim.restype = i64
     lib.mpq_output_error.argtypes = [P, P, P, P, i64, i64, i32, P, i64, P, P, P]
@@ -240,6 +256,51 @@ def reconstruct(codes: torch.Tensor, scales: torch.Tensor, counts: torch.Tensor,
                                 _dev(W_hat, torch.float32, "W_hat"), _stream(stream))
     _check(rc)
     return W_hat
+
+
+def integer_scales(scales: torch.Tensor, counts: torch.Tensor, p: int, stream=None,
+                   out: Optional[torch.Tensor] = None, count_clamped: bool = True):
+    """mpq_integer_scales (Eq. (14)).  Returns (A [C, P] int32, number of
+    clamped values as a 1-element uint64 device tensor (int64 view) or None)."""
+    C, P = scales.shape
+    A = torch.empty((C, P), dtype=torch.int32, device=scales.device) if out is None else out
+    cl = torch.zeros((1,), dtype=torch.int64, device=scales.device) if count_clamped else None
+    _check(load().mpq_integer_scales(_dev(scales, torch.float32, "scales"),
+                                     _dev(counts, torch.int32, "counts"), C, P, int(p),
+                                     _dev(A, torch.int32, "A"),
+                                     None if cl is None else cl.data_ptr(), _stream(stream)))
+    return A, cl
+
+
+def integer_forward(codes: torch.Tensor, A: torch.Tensor, counts: torch.Tensor, X: torch.Tensor,
+                    p: int, stream=None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """mpq_integer_forward (Eq. (15), Steps 1-3).  X [n, d] int8.  Returns Y [C, n] int64."""
+    C, P, d = codes.shape
+    if X.dim() != 2 or X.shape[1] != d:
+        raise ValueError("X must be [n, d]")
+    n = X.shape[0]
+    Y = torch.empty((C, n), dtype=torch.int64, device=codes.device) if out is None else out
+    _check(load().mpq_integer_forward(_dev(codes, torch.int8, "codes"), _dev(A, torch.int32, "A"),
+                                      _dev(counts, torch.int32, "counts"), C, d, P,
+                                      _dev(X, torch.int8, "X"), n, int(p), _dev(Y, torch.int64, "Y"),
+                                      _stream(stream)))
+    return Y
+
+
+def integer_forward_layers(layers, max_points: int, p: int, stream=None):
+    """mpq_integer_forward_layers.  layers: list of (codes, A, counts, X, Y) device tensors."""
+    arr = (IntLayer * max(len(layers), 1))()
+    for i, (codes, A, counts, X, Y) in enumerate(layers):
+        C, P, d = codes.shape
+        if P != max_points or X.shape[1] != d or Y.shape != (C, X.shape[0]):
+            raise ValueError(f"layer {i}: shapes do not match")
+        L = arr[i]
+        L.codes, L.A = _dev(codes, torch.int8, "codes"), _dev(A, torch.int32, "A")
+        L.counts, L.X = _dev(counts, torch.int32, "counts"), _dev(X, torch.int8, "X")
+        L.Y = _dev(Y, torch.int64, "Y")
+        L.c_out, L.d, L.n = C, d, X.shape[0]
+    _check(load().mpq_integer_forward_layers(ctypes.addressof(arr), len(layers), max_points, int(p),
+                                             _stream(stream)))
 
 
 def timing_enable(on: bool = True):

@@ -249,3 +249,46 @@ def test_calib_layers_check_every_layer_first(lib):
     for L in arr:
         L.c_out = 0
     assert f(p, 2, 4, 4, None, 8, 1e-3, 0, None) == 0
+
+
+def test_integer_calls_reject_invalid_arguments(lib):
+    from paper_2002_09049_amd import mpq
+    E = mpq.MPQ_ERR_INVALID_ARG
+    sc = lib.mpq_integer_scales
+    assert sc(1, 1, 4, 4, -1, 1, None, None) == E
+    assert sc(1, 1, 4, 4, 63, 1, None, None) == E
+    assert sc(1, 1, 4, 0, 8, 1, None, None) == E
+    assert sc(None, 1, 4, 4, 8, 1, None, None) == E
+    assert sc(1, 1, -1, 4, 8, 1, None, None) == E
+    assert sc(None, None, 0, 4, 8, None, None, None) == 0
+    fw = lib.mpq_integer_forward
+    ok = dict(codes=1, A=1, counts=1, c=4, d=16, P=4, X=1, n=8, p=8, Y=1)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return fw(a["codes"], a["A"], a["counts"], a["c"], a["d"], a["P"], a["X"], a["n"], a["p"],
+                  a["Y"], None)
+    for kw in (dict(p=-1), dict(p=63), dict(d=0), dict(d=131073), dict(P=0), dict(P=65),
+               dict(c=-1), dict(n=-1), dict(codes=None), dict(A=None), dict(counts=None),
+               dict(X=None), dict(Y=None), dict(c=1 << 20, d=4096, P=4),
+               dict(n=1 << 20, d=4096)):
+        assert call(**kw) == E, kw
+    assert call(c=0, codes=None, A=None, counts=None, Y=None) == 0
+    assert call(n=0, X=None, Y=None) == 0
+
+
+def test_int_layer_struct_matches_header(tmp_path):
+    import subprocess
+    from paper_2002_09049_amd import mpq
+    fields = [f for f, _ in mpq.IntLayer._fields_]
+    src = tmp_path / "off.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "mpq.h"\nint main(void){\n'
+                   '  printf("%zu\\n", sizeof(mpq_int_layer));\n' +
+                   "".join(f'  printf("%zu\\n", offsetof(mpq_int_layer, {f}));\n' for f in fields) +
+                   "  return 0;\n}\n")
+    exe = tmp_path / "off"
+    subprocess.check_call(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)])
+    out = [int(x) for x in subprocess.check_output([str(exe)]).split()]
+    assert out[0] == ctypes.sizeof(mpq.IntLayer)
+    assert out[1:] == [getattr(mpq.IntLayer, f).offset for f in fields]
