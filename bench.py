@@ -14,6 +14,14 @@ calibration batch instead (mpq_fit_layers_calib, whose per-point output
 errors are the scoring, then mpq_reconstruct_layers); tol is then the
 relative threshold eps.
 
+--deploy times the deployment arithmetic of Sec. 3.4 instead: after the fit
+(untimed) and the integer scales A_i = [2^p a_i] (off-line, as the paper
+does it), one step is the integer forward of every layer (Eq. (15): int8
+MFMA point products, the A_i-weighted 64-bit sum, the shift) on a batch of
+synthetic int8 activations of the layer's real size for --images 224 x 224
+images (N = images x output positions); value is int8 OP/s (2 per
+multiply-add of the points actually used).
+
 Prints one JSON line.  `value` is channel-points fitted per second over the
 whole step (sum of the per-channel point counts of all layers / step time).
 Every kernel launch of the timed steps is timed by HIP events that the
@@ -36,6 +44,7 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0
 PEAK_MFMA_F32_TFLOPS = 157.3
 PEAK_VALU_F32_TFLOPS = 157.3            # published (packed) FP32 vector peak
+PEAK_MFMA_I8_TOPS = 5000.0              # dense int8 MFMA
 PEAK_VALU_F32_NONPACKED_TFLOPS = 78.6   # 256 CU x 64 lanes x 2 FLOP x 2.4 GHz
 FLOP_PER_EVAL = 7                       # scale-mul, round, clamp, fma (2), square-acc fma (2)
 
@@ -43,7 +52,8 @@ TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "resnet18_hbm_traffic.md")
 COPY_BYTES = 256 << 20
 STAGES = (("fit", ("fit_hist_kernel", "fit_dense_kernel")),
           ("output_error", ("form_dt_kernel", "gemm_err_kernel", "finish_err_kernel")),
-          ("reconstruct", ("reconstruct_kernel",)))
+          ("reconstruct", ("reconstruct_kernel",)),
+          ("deploy", ("int_forward_kernel", "integer_scales_kernel")))
 
 
 def parse():
@@ -61,6 +71,11 @@ def parse():
     ap.add_argument("--rule", choices=("tol", "calib"), default="tol",
                     help="stopping rule: ||r||^2 <= tol ||w||^2 (default), or Algorithm 2's on the "
                          "calibration batch (output error <= tol x that of W)")
+    ap.add_argument("--deploy", action="store_true",
+                    help="time the integer forward of Sec. 3.4 (Eq. (15)) of every layer instead")
+    ap.add_argument("--images", type=int, default=8,
+                    help="--deploy: images of 224 x 224 in the activation batch")
+    ap.add_argument("--shift", type=int, default=16, help="--deploy: p of Eq. (14)")
     ap.add_argument("--separate", action="store_true",
                     help="the three batched calls in turn instead of mpq_quantize_layers")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -103,6 +118,9 @@ def kernel_key(profiler_name):
         mode = "lattice" if m.group(4) == "true" else "linear" if m.group(3) == "true" else "grid"
         rebuilt = ",rebuilt" if m.group(5) == "true" else ""
         return f"fit_hist_kernel<{m.group(1)},{m.group(2)},{mode}{rebuilt}>"
+    m = re.search(r"int_forward_kernel<(\d)>", profiler_name)
+    if m:
+        return f"int_forward_kernel<{(16, 4, 1)[int(m.group(1))]}>"
     m = re.search(r"(\w+_kernel)\b", profiler_name)
     return m.group(1) if m else None
 
@@ -191,24 +209,28 @@ def summarize_trace(trace_dir, bench_json=None, steps=6, rule="tol"):
         k = kernel_key(r["Name"])
         if not stage_of(k):
             continue
+        if rule == "deploy" and not k.startswith("int_forward_kernel"):
+            continue   # the fit and the scales are untimed set-up
         a = agg.setdefault(k, [0, 0.0])
         a[0] += int(r["Calls"])
         a[1] += float(r["TotalDurationNs"])
     bench = json.load(open(bench_json)) if bench_json else None
     calib = rule == "calib"
-    r = " --rule calib" if calib else ""
-    what = ("the fit with Algorithm 2's stopping rule on each layer's calibration batch (one point\n"
-            "per step, each step scored on the batch; relative threshold 1e-3) and the\n"
-            "reconstruction, through mpq_fit_layers_calib and mpq_reconstruct_layers."
-            if calib else
-            "fit + output error + reconstruction of every layer through the batched C ABI calls.")
+    r = {"calib": " --rule calib", "deploy": " --deploy"}.get(rule, "")
+    what = {"calib": "the fit with Algorithm 2's stopping rule on each layer's calibration batch (one point\n"
+                     "per step, each step scored on the batch; relative threshold 1e-3) and the\n"
+                     "reconstruction, through mpq_fit_layers_calib and mpq_reconstruct_layers.",
+            "deploy": "the integer forward of Eq. (15) of every layer (fitted codes, integer scales with\n"
+                      "p = 16) on int8 activations of 8 images of 224 x 224 (N = 8 x output positions),\n"
+                      "through mpq_integer_forward_layers; the fit and the scales are untimed set-up."
+            }.get(rule, "fit + output error + reconstruction of every layer through the batched C ABI calls.")
     lines = [f"# rocprofv3 kernel summary: ResNet-18-shaped workload, bench step{r}", "",
              "Workload: 21 layers (5,800 channels, 11,678,912 weights), 4 bits, up to 4 points,",
              "256 candidate scales, tol 1e-3, calibration batches d x 1024.  One step =",
              what, "",
              "Commands (one MI355X, from the repository root):", "", "```",
              "rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof -o kt -- \\",
-             f"    python3 bench.py{r} --steps 5 --warmup 1 --no-cpu-baseline",
+             f"    python3 bench.py{r} --steps 5 --warmup 1" + ("" if rule == "deploy" else " --no-cpu-baseline"),
              f"python3 bench.py{r} --steps 5 --warmup 1 > gpurun_out/bench.json",
              f"python3 bench.py{r} --summarize-trace gpurun_out/prof --bench-json gpurun_out/bench.json",
              "```", "",
@@ -238,7 +260,7 @@ def main():
         return 0
     if args.summarize_trace:
         summarize_trace(args.summarize_trace, args.bench_json, steps=args.traced_steps or 6,
-                        rule=args.rule)
+                        rule="deploy" if args.deploy else args.rule)
         return 0
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -250,6 +272,8 @@ def main():
     from paper_2002_09049_amd import mpq, workloads as wl
 
     assert torch.cuda.is_available(), "bench.py needs a ROCm GPU"
+    if args.deploy:
+        return deploy_main(args)
     mpq.load()
     wk = wl.get(args.workload)
     dev = torch.device("cuda", 0)
@@ -431,6 +455,100 @@ def main():
 
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wk, args.cpu_stride, calib)
+    print(json.dumps(res), flush=True)
+    return 0
+
+
+def deploy_main(args):
+    """--deploy: the integer forward of Sec. 3.4 of every layer."""
+    import numpy as np
+    import torch
+
+    from paper_2002_09049_amd import accounting as ac, mpq, workloads as wl
+
+    wk = wl.get(args.workload)
+    hw = {"resnet18": wl.resnet18_out_hw, "resnet50": wl.resnet50_out_hw}.get(wk.name)
+    if hw is None:
+        raise SystemExit("--deploy knows the output sizes of resnet18 and resnet50")
+    hw = hw()
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    Ws = [torch.from_numpy(wl.layer_weights(wk, li)).to(dev) for li in range(len(wk.layers))]
+    ls = mpq.LayerSet(Ws, wk.max_points)
+    ls.fit(wk.bits, wk.n_grid, wk.tol)
+    p = args.shift
+    As = []
+    for i in range(len(Ws)):
+        A, cl = mpq.integer_scales(ls.scales[i], ls.counts[i], p)
+        As.append(A)
+        assert int(cl.item()) == 0, "integer scales clamped: lower --shift"
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(wk.seed)
+    layers, macs = [], 0
+    kmacs = {}   # useful multiply-adds per kernel (layers go to a kernel by their load width)
+    counts = [ls.counts[i].cpu().numpy().astype(np.int64) for i in range(len(Ws))]
+    for i, (C, d) in enumerate(wk.layers):
+        N = args.images * hw[i] * hw[i]
+        X = torch.randint(-128, 128, (N, d), generator=gen, dtype=torch.int8, device=dev)
+        Y = torch.empty((C, N), dtype=torch.int64, device=dev)
+        layers.append((ls.codes[i], As[i], ls.counts[i], X, Y))
+        m = int(counts[i].sum()) * d * N
+        macs += m
+        kname = f"int_forward_kernel<{16 if d % 16 == 0 else 4 if d % 4 == 0 else 1}>"
+        kmacs[kname] = kmacs.get(kname, 0) + m
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        mpq.integer_forward_layers(layers, wk.max_points, p)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    mpq.timing_enable(True)
+    t0.record(stream)
+    for _ in range(args.steps):
+        mpq.integer_forward_layers(layers, wk.max_points, p)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    launches = mpq.timing_read()
+    mpq.timing_enable(False)
+    ms = t0.elapsed_time(t1) / args.steps
+    per = {}
+    for name, t in launches:
+        e = per.setdefault(name, [0, 0.0])
+        e[0] += 1
+        e[1] += t
+    kernels = {}
+    for name, (cnt, tot) in per.items():
+        avg_s = tot / cnt * 1e-3
+        lps = cnt / args.steps
+        k = {"launches_per_step": lps, "avg_us": tot / cnt * 1e3, "us_per_step": tot / args.steps * 1e3}
+        if name in kmacs:
+            k.update({"bound": "mfma", "unit": "TOP/s", "peak": PEAK_MFMA_I8_TOPS,
+                      "ops_per_launch": 2 * kmacs[name] / lps,
+                      "achieved": 2 * kmacs[name] / lps / avg_s / 1e12})
+            k["frac"] = k["achieved"] / k["peak"]
+        kernels[name] = k
+    dom = max(kernels, key=lambda k: kernels[k]["us_per_step"])
+    K = kernels[dom]
+    layers_acct = [(C, d, h * h) for (C, d), h in zip(wk.layers, hw)][1:-1]
+    acct_mp = ac.network_cost(layers_acct, wk.bits, 8, counts[1:-1])
+    acct_nv = ac.network_cost(layers_acct, wk.bits, 8)
+    res = {
+        "metric": "multipoint integer forward (Eq. 15), int8 OP/s",
+        "value": round(2 * macs / (ms * 1e-3), 1),
+        "unit": "OP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "i8", "data": "synthetic",
+        "config": {"workload": f"{wk.name} integer forward, {args.images} images of 224 x 224",
+                   "layers": len(wk.layers), "bits": wk.bits, "activation_bits": 8, "p": p,
+                   "points": int(sum(c.sum() for c in counts)), "macs_per_step": macs,
+                   "paper_ops_per_image_W4A8": {"multipoint": acct_mp["ops"], "naive": acct_nv["ops"]},
+                   "parallelism": "none"},
+        "roofline": {"kernel": dom, "bound": K.get("bound"), "achieved": round(K.get("achieved", 0.0), 3),
+                     "peak": K.get("peak"), "unit": K.get("unit"), "frac": round(K.get("frac", 0.0), 5),
+                     "traffic": None, "avg_launch_us": round(K["avg_us"], 3)},
+        "kernels": kernels,
+    }
     print(json.dumps(res), flush=True)
     return 0
 

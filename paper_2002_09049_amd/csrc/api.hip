@@ -758,30 +758,46 @@ int int_forward_impl(const mpq_int_layer *layers, int n_layers, int max_points, 
             rc = fail(MPQ_ERR_INVALID_ARG, "codes and X must each be below 2^31 bytes");
         if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
     }
-    hipStream_t s = (hipStream_t)stream;
-    mpq::IntGroup g;
-    g.P = max_points;
-    g.p = p;
-    g.n_layers = 0;
-    for (int l = 0; l <= n_layers; ++l) {
-        if ((l == n_layers || g.n_layers == mpq::kMaxIntLayers) && g.n_layers > 0) {
-            const hipError_t e = mpq::launch_int_forward(g, s);
-            if (e != hipSuccess) return hip_fail(e, "integer forward kernel launch");
-            g.n_layers = 0;
+    // launches of up to kMaxIntLayers layers of one load mode, side by side
+    std::vector<mpq::IntGroup> groups;
+    std::vector<int> modes;
+    std::vector<double> work;
+    for (int mode = 0; mode < mpq::kIntModes; ++mode) {
+        mpq::IntGroup g;
+        g.P = max_points;
+        g.p = p;
+        g.n_layers = 0;
+        double w = 0.0;
+        for (int l = 0; l <= n_layers; ++l) {
+            if ((l == n_layers || g.n_layers == mpq::kMaxIntLayers) && g.n_layers > 0) {
+                groups.push_back(g);
+                modes.push_back(mode);
+                work.push_back(w);
+                g.n_layers = 0;
+                w = 0.0;
+            }
+            if (l == n_layers) break;
+            const mpq_int_layer &L = layers[l];
+            if (L.c_out == 0 || L.n == 0) continue;
+            mpq::IntLayer I = {};
+            I.codes = L.codes;
+            I.A = L.A;
+            I.counts = L.counts;
+            I.X = L.X;
+            I.Y = L.Y;
+            I.C = L.c_out;
+            I.d = L.d;
+            I.N = L.n;
+            if (mpq::int_forward_mode(I) != mode) continue;
+            g.L[g.n_layers++] = I;
+            w += (double)L.c_out * (double)L.d * (double)L.n;
         }
-        if (l == n_layers) break;
-        const mpq_int_layer &L = layers[l];
-        if (L.c_out == 0 || L.n == 0) continue;
-        mpq::IntLayer &I = g.L[g.n_layers++];
-        I.codes = L.codes;
-        I.A = L.A;
-        I.counts = L.counts;
-        I.X = L.X;
-        I.Y = L.Y;
-        I.C = L.c_out;
-        I.d = L.d;
-        I.N = L.n;
     }
+    if (groups.empty()) return MPQ_OK;
+    const hipError_t e = run_concurrently((hipStream_t)stream, work, [&](int i, hipStream_t st) {
+        return mpq::launch_int_forward(groups[i], modes[i], st);
+    });
+    if (e != hipSuccess) return hip_fail(e, "integer forward kernel launch");
     return MPQ_OK;
 }
 

@@ -151,8 +151,9 @@ hipError_t launch_reconstruct(const RecLayer *in, int n_in, int P, hipStream_t s
 hipError_t launch_integer_scales(const float *scales, const int32_t *counts, int64_t C, int P, int p,
                                  int32_t *A, unsigned long long *clamped, hipStream_t s);
 
-// Integer forward of up to kMaxIntLayers layers in one launch (one
-// workgroup per 128 x 128 tile of Y); ntn and block_begin are set by
+// Integer forward of up to kMaxIntLayers layers of one load mode in one
+// launch (one workgroup per 128-row x 128-column tile of the (channel,
+// point) x column product); ntn, block_begin and log2_pp are set by
 // launch_int_forward.  Each layer's codes and X are below 2^31 bytes.
 struct IntLayer {
     const int8_t *codes;    // [C][P][d]
@@ -167,9 +168,14 @@ constexpr int kMaxIntLayers = 32;
 struct IntGroup {
     int n_layers;
     int P, p;
+    int log2_pp;            // rows per channel: max_points rounded up to a power of two
     IntLayer L[kMaxIntLayers];
 };
 static_assert(sizeof(IntGroup) <= 4096, "kernel arguments");
-hipError_t launch_int_forward(IntGroup &g, hipStream_t s);
+// The operand load width a layer takes (0: 16 bytes, 1: 4 bytes, 2: bytes);
+// the layers of one launch share it.
+constexpr int kIntModes = 3;
+int int_forward_mode(const IntLayer &L);
+hipError_t launch_int_forward(IntGroup &g, int mode, hipStream_t s);
 
 }  // namespace mpq

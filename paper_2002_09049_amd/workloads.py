@@ -84,6 +84,50 @@ def vgg16_fc_shapes() -> List[Shape]:
     return [(4096, 25088), (4096, 4096), (1000, 4096)]
 
 
+# ------------------------------------------- output sizes at a 224 x 224 input
+def resnet18_out_hw() -> List[int]:
+    """Output height (= width) of each layer of resnet18_shapes() for a 224 x
+    224 image (the stem conv has stride 2, then a stride-2 max pool; each
+    later stage halves the size in its first 3x3 and its downsample)."""
+    return [112] + [56] * 4 + [28] * 5 + [14] * 5 + [7] * 5 + [1]
+
+
+def resnet50_out_hw() -> List[int]:
+    """Output size of each layer of resnet50_shapes() for a 224 x 224 image
+    (the stride of a stage's first block sits in its 3x3 conv and its
+    downsample)."""
+    out, res = [112], 56
+    for w, nblocks in ((64, 3), (128, 4), (256, 6), (512, 3)):
+        for b in range(nblocks):
+            o = res // 2 if (b == 0 and w != 64) else res
+            out += [res, o, o] + ([o] if b == 0 else [])
+            res = o
+    out.append(1)
+    return out
+
+
+def mobilenetv2_full_layers() -> List[Tuple[Shape, int, str]]:
+    """Every weight layer of MobileNetV2 with its output size for a 224 x 224
+    image: the stem 3x3 conv (32 x 27, stride 2), the inverted-residual
+    blocks of mobilenetv2_shapes() (a block's stride sits in its depthwise
+    conv), the final 1x1 conv and the classifier.  ((C_out, d), hw, kind)."""
+    out: List[Tuple[Shape, int, str]] = [((32, 27), 112, "stem")]
+    cin, res = 32, 112
+    for t, c, n, st in ((1, 16, 1, 1), (6, 24, 2, 2), (6, 32, 3, 2), (6, 64, 4, 2),
+                        (6, 96, 3, 1), (6, 160, 3, 2), (6, 320, 1, 1)):
+        for b in range(n):
+            h = cin * t
+            if t != 1:
+                out.append(((h, cin), res, "pw"))
+            o = res // (st if b == 0 else 1)
+            out.append(((h, 9), o, "dw"))
+            out.append(((c, h), o, "pw"))
+            cin, res = c, o
+    out.append(((1280, 320), 7, "pw"))
+    out.append(((1000, 1280), 1, "fc"))
+    return out
+
+
 # ------------------------------------------------------------------- workloads
 @dataclasses.dataclass(frozen=True)
 class Workload:

@@ -22,6 +22,9 @@ def test_kernel_key_maps_profiler_names():
     assert bench.stage_of("form_dt_kernel") == "output_error"
     assert bench.stage_of("fit_hist_kernel<64,1,linear>") == "fit"
     assert bench.stage_of("zero_i32_kernel") is None
+    assert k("void mpq::(anonymous namespace)::int_forward_kernel<0>(mpq::IntGroup)") == "int_forward_kernel<16>"
+    assert k("int_forward_kernel<2>(mpq::IntGroup)") == "int_forward_kernel<1>"
+    assert bench.stage_of("int_forward_kernel<16>") == "deploy"
 
 
 def test_more_than_one_gpu_is_refused():
