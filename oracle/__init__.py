@@ -63,6 +63,12 @@ def _declare(lib):
     lib.oracle_levels.restype = i32
     lib.oracle_default_grid.argtypes = [i32, P]
     lib.oracle_default_grid.restype = None
+    lib.oracle_fit_ex.argtypes = [P, i64, i64, i32, i32, P, i32, f64, P, i64, f64, i32, i32, P, P, P,
+                                  P, P, i32]
+    lib.oracle_fit_ex.restype = i32
+    lib.oracle_verify_ex.argtypes = [P, i64, i64, i32, i32, P, i32, f64, P, i64, f64, i32, i32, P, P,
+                                     P, P, P, P, i64, P, P, P, P, P, i32]
+    lib.oracle_verify_ex.restype = i32
     lib.oracle_integer_scales.argtypes = [P, P, i64, i32, i32, P]
     lib.oracle_integer_scales.restype = i64
     lib.oracle_integer_forward.argtypes = [P, P, P, i64, i64, i32, P, i64, i32, P]
@@ -126,87 +132,54 @@ class Oracle:
         return self.lib.oracle_scale_error(_p(r), r.size, float(a), self.levels(bits))
 
     def fit(self, W: np.ndarray, bits: int, max_points: int, n_grid: int, tol: float,
-            grid: Optional[np.ndarray] = None, n_threads: int = 0):
-        """Free-running greedy fit. Returns (codes[C,P,d] i8, scales[C,P] f32,
-        counts[C] i32, err[C,P] f64)."""
+            grid: Optional[np.ndarray] = None, n_threads: int = 0, refit: bool = False):
+        """Free-running greedy fit (refit: reading A2). Returns (codes[C,P,d] i8,
+        scales[C,P] f32, counts[C] i32, err[C,P] f64)."""
+        return self._fit(W, bits, max_points, n_grid, tol, None, 0.0, False, refit, grid,
+                         n_threads)[:4]
+
+    def _fit(self, W, bits, P, n_grid, tol, X, eps, relative, refit, grid, n_threads):
         W = np.ascontiguousarray(W, dtype=np.float32)
         C, d = W.shape
-        P = max_points
-        codes_ = np.zeros((C, P, d), np.int8)
-        scales = np.zeros((C, P), np.float32)
-        counts = np.zeros(C, np.int32)
-        err = np.zeros((C, P), np.float64)
-        g = _grid(grid, n_grid)
-        rc = self.lib.oracle_fit(_p(W), C, d, bits, P, _p(g), n_grid, float(tol),
-                                _p(codes_), _p(scales), _p(counts), _p(err), n_threads)
-        if rc != 0:
-            raise MemoryError("oracle_fit failed")
-        return codes_, scales, counts, err
-
-    def verify(self, W, bits, max_points, n_grid, tol, codes_, scales, counts, err=None,
-               grid=None, channels=None, n_threads: int = 0):
-        """Lockstep check of another implementation's fit output (rules V1-V4).
-
-        Returns a dict of per-channel arrays: status, cand_ties, code_ties,
-        stop_ties, err_relmax, and the checked channel indices.
-        """
-        W = np.ascontiguousarray(W, dtype=np.float32)
-        C, d = W.shape
-        codes_ = np.ascontiguousarray(codes_, dtype=np.int8)
-        scales = np.ascontiguousarray(scales, dtype=np.float32)
-        counts = np.ascontiguousarray(counts, dtype=np.int32)
-        assert codes_.shape == (C, max_points, d) and scales.shape == (C, max_points)
-        assert counts.shape == (C,)
-        e = None if err is None else np.ascontiguousarray(err, dtype=np.float32)
-        chan = np.arange(C, dtype=np.int64) if channels is None else \
-            np.ascontiguousarray(channels, dtype=np.int64)
-        n = chan.size
-        out = {k: np.zeros(n, np.int32) for k in ("status", "cand_ties", "code_ties", "stop_ties")}
-        out["err_relmax"] = np.zeros(n, np.float64)
-        g = _grid(grid, n_grid)
-        rc = self.lib.oracle_verify(_p(W), C, d, bits, max_points, _p(g), n_grid, float(tol),
-                                   _p(codes_), _p(scales), _p(counts), _p(e), _p(chan), n,
-                                   _p(out["status"]), _p(out["cand_ties"]), _p(out["code_ties"]),
-                                   _p(out["stop_ties"]), _p(out["err_relmax"]), n_threads)
-        if rc != 0:
-            raise MemoryError("oracle_verify failed")
-        out["channels"] = chan
-        return out
-
-    def fit_calib(self, W: np.ndarray, bits: int, max_points: int, n_grid: int, X: np.ndarray,
-                  eps: float, relative: bool, grid: Optional[np.ndarray] = None, n_threads: int = 0):
-        """Free-running fit with Algorithm 2's stopping rule on the calibration
-        batch X [d, N] (reading S4).  Returns (codes, scales, counts, err,
-        xerr[C,P] f64: the output error after each point)."""
-        W = np.ascontiguousarray(W, dtype=np.float32)
-        C, d = W.shape
-        X = np.ascontiguousarray(X, dtype=np.float32)
-        assert X.shape[0] == d
-        P = max_points
+        if X is not None:
+            X = np.ascontiguousarray(X, dtype=np.float32)
+            assert X.shape[0] == d
         codes_ = np.zeros((C, P, d), np.int8)
         scales = np.zeros((C, P), np.float32)
         counts = np.zeros(C, np.int32)
         err = np.zeros((C, P), np.float64)
         xerr = np.zeros((C, P), np.float64)
         g = _grid(grid, n_grid)
-        rc = self.lib.oracle_fit_calib(_p(W), C, d, bits, P, _p(g), n_grid, _p(X), X.shape[1],
-                                      float(eps), 1 if relative else 0, _p(codes_), _p(scales),
-                                      _p(counts), _p(err), _p(xerr), n_threads)
+        rc = self.lib.oracle_fit_ex(_p(W), C, d, bits, P, _p(g), n_grid, float(tol), _p(X),
+                                    0 if X is None else X.shape[1], float(eps), 1 if relative else 0,
+                                    1 if refit else 0, _p(codes_), _p(scales), _p(counts), _p(err),
+                                    _p(xerr), n_threads)
         if rc != 0:
-            raise MemoryError("oracle_fit_calib failed")
+            raise MemoryError("oracle_fit_ex failed")
         return codes_, scales, counts, err, xerr
 
-    def verify_calib(self, W, bits, max_points, n_grid, X, eps, relative, codes_, scales, counts,
-                     err=None, xerr=None, grid=None, channels=None, n_threads: int = 0):
-        """Lockstep check (V1, V2, V4, V4x and S4's stop decision) of another
-        implementation's fit with Algorithm 2's stopping rule."""
+    def verify(self, W, bits, max_points, n_grid, tol, codes_, scales, counts, err=None,
+               grid=None, channels=None, n_threads: int = 0, refit: bool = False):
+        """Lockstep check of another implementation's fit output (rules V1-V4;
+        refit: reading A2).
+
+        Returns a dict of per-channel arrays: status, cand_ties, code_ties,
+        stop_ties, err_relmax, and the checked channel indices.
+        """
+        return self._verify(W, bits, max_points, n_grid, tol, None, 0.0, False, refit, codes_,
+                            scales, counts, err, None, grid, channels, n_threads)
+
+    def _verify(self, W, bits, P, n_grid, tol, X, eps, relative, refit, codes_, scales, counts,
+                err, xerr, grid, channels, n_threads):
         W = np.ascontiguousarray(W, dtype=np.float32)
         C, d = W.shape
-        X = np.ascontiguousarray(X, dtype=np.float32)
+        if X is not None:
+            X = np.ascontiguousarray(X, dtype=np.float32)
         codes_ = np.ascontiguousarray(codes_, dtype=np.int8)
         scales = np.ascontiguousarray(scales, dtype=np.float32)
         counts = np.ascontiguousarray(counts, dtype=np.int32)
-        assert codes_.shape == (C, max_points, d) and scales.shape == (C, max_points)
+        assert codes_.shape == (C, P, d) and scales.shape == (C, P)
+        assert counts.shape == (C,)
         e = None if err is None else np.ascontiguousarray(err, dtype=np.float32)
         xe = None if xerr is None else np.ascontiguousarray(xerr, dtype=np.float32)
         chan = np.arange(C, dtype=np.int64) if channels is None else \
@@ -215,15 +188,31 @@ class Oracle:
         out = {k: np.zeros(n, np.int32) for k in ("status", "cand_ties", "code_ties", "stop_ties")}
         out["err_relmax"] = np.zeros(n, np.float64)
         g = _grid(grid, n_grid)
-        rc = self.lib.oracle_verify_calib(
-            _p(W), C, d, bits, max_points, _p(g), n_grid, _p(X), X.shape[1], float(eps),
-            1 if relative else 0, _p(codes_), _p(scales), _p(counts), _p(e), _p(xe), _p(chan), n,
-            _p(out["status"]), _p(out["cand_ties"]), _p(out["code_ties"]), _p(out["stop_ties"]),
-            _p(out["err_relmax"]), n_threads)
+        rc = self.lib.oracle_verify_ex(
+            _p(W), C, d, bits, P, _p(g), n_grid, float(tol), _p(X), 0 if X is None else X.shape[1],
+            float(eps), 1 if relative else 0, 1 if refit else 0, _p(codes_), _p(scales),
+            _p(counts), _p(e), _p(xe), _p(chan), n, _p(out["status"]), _p(out["cand_ties"]),
+            _p(out["code_ties"]), _p(out["stop_ties"]), _p(out["err_relmax"]), n_threads)
         if rc != 0:
-            raise MemoryError("oracle_verify_calib failed")
+            raise MemoryError("oracle_verify_ex failed")
         out["channels"] = chan
         return out
+
+    def fit_calib(self, W: np.ndarray, bits: int, max_points: int, n_grid: int, X: np.ndarray,
+                  eps: float, relative: bool, grid: Optional[np.ndarray] = None, n_threads: int = 0,
+                  refit: bool = False):
+        """Free-running fit with Algorithm 2's stopping rule on the calibration
+        batch X [d, N] (reading S4; refit: reading A2).  Returns (codes, scales,
+        counts, err, xerr[C,P] f64: the output error after each point)."""
+        return self._fit(W, bits, max_points, n_grid, 0.0, X, eps, relative, refit, grid, n_threads)
+
+    def verify_calib(self, W, bits, max_points, n_grid, X, eps, relative, codes_, scales, counts,
+                     err=None, xerr=None, grid=None, channels=None, n_threads: int = 0,
+                     refit: bool = False):
+        """Lockstep check (V1, V2, V4, V4x and S4's stop decision) of another
+        implementation's fit with Algorithm 2's stopping rule."""
+        return self._verify(W, bits, max_points, n_grid, 0.0, X, eps, relative, refit, codes_,
+                            scales, counts, err, xerr, grid, channels, n_threads)
 
     def output_error(self, W, codes_, scales, counts, X, channels=None, with_ref=True, n_threads: int = 0):
         """Eq. (12) in fp64. Returns (err, ref) for the listed channels."""

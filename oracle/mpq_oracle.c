@@ -43,7 +43,11 @@
  *          e > eps), or at max_points, ||r||^2 == 0 or no nonzero scale.
  *          The points are still chosen by Eq. (9): Algorithm 1 fits the
  *          residual, Algorithm 2 only decides how many points to take.
- *   A1     No refit of a once q is fixed.
+ *   A1     No refit of a once q is fixed (the method as printed).
+ *   A2     Variant (refit != 0): once q is fixed by Eq. (10) at the searched
+ *          a*, the point's scale is the least-squares one for that q,
+ *          a = fl32(<r, q> / <q, q>) (fp64 sums in index order), and the
+ *          residual of Eq. (7) uses it.
  *   E1     Output error: mean over the N columns of X of ((w - w~) . x)^2.
  *   P1     Scales are stored as fp32 values (exactly the candidate value).
  *   I1     Eq. (14) rounds 2^p a_i to the nearest integer with ties to even
@@ -212,8 +216,19 @@ static int calib_should_stop(int n, int P, double Er, double e, double thr)
  * err [P] (||r||^2 after each point).  cal: NULL for S1-S3, else S4 with
  * xerr [P] (NULL or the output error after each point).  Returns the number
  * of points. */
+/* Reading A2: the least-squares scale of the codes q for the residual r. */
+static double refit_scale(const double *r, const int8_t *q, int64_t d)
+{
+    double rq = 0.0, qq = 0.0;
+    for (int64_t j = 0; j < d; ++j) {
+        rq += r[j] * (double)q[j];
+        qq += (double)q[j] * (double)q[j];
+    }
+    return rq / qq;
+}
+
 static int fit_channel(const float *w, int64_t d, int M, int P, const float *c,
-                       int G, double tol, const calib_rule *cal, int8_t *codes,
+                       int G, double tol, const calib_rule *cal, int refit, int8_t *codes,
                        float *scales, double *err, double *xerr, double *r, float *a,
                        double *E)
 {
@@ -231,8 +246,13 @@ static int fit_channel(const float *w, int64_t d, int M, int P, const float *c,
         double as = (double)a[g];
         int8_t *q = codes + (int64_t)n * d;
         oracle_codes(r, d, as, M, q);                       /* Eq. (10) */
+        float a_pt = a[g];
+        if (refit) {                                        /* A2 */
+            a_pt = (float)refit_scale(r, q, d);
+            as = (double)a_pt;
+        }
         for (int64_t j = 0; j < d; ++j) r[j] = r[j] - as * (double)q[j]; /* Eq. (7) */
-        scales[n] = a[g];
+        scales[n] = a_pt;
         n += 1;
         err[n - 1] = sum_sq(r, d);
         if (cal) {
@@ -258,7 +278,7 @@ static int n_threads_or_default(int nt)
  * (may be NULL), and with cal the output error after each point, xerr
  * [C][P] (may be NULL).  Slots at or after a channel's count are zero. */
 static int fit_layer(const float *W, int64_t C, int64_t d, int bits, int P,
-                     const float *grid, int G, double tol, const calib_rule *cal,
+                     const float *grid, int G, double tol, const calib_rule *cal, int refit,
                      int8_t *codes, float *scales, int32_t *counts, double *err,
                      double *xerr, int n_threads)
 {
@@ -288,7 +308,7 @@ static int fit_layer(const float *W, int64_t C, int64_t d, int bits, int P,
             for (int64_t k = 0; k < C; ++k) {
                 memset(e, 0, sizeof(double) * (size_t)P);
                 memset(xe, 0, sizeof(double) * (size_t)P);
-                int n = fit_channel(W + k * d, d, M, P, c, G, tol, cal, codes + k * P * d,
+                int n = fit_channel(W + k * d, d, M, P, c, G, tol, cal, refit, codes + k * P * d,
                                     scales + k * P, e, xe, r, a, E);
                 counts[k] = n;
                 if (err) memcpy(err + k * P, e, sizeof(double) * (size_t)P);
@@ -305,8 +325,20 @@ int oracle_fit(const float *W, int64_t C, int64_t d, int bits, int P,
                const float *grid, int G, double tol, int8_t *codes,
                float *scales, int32_t *counts, double *err, int n_threads)
 {
-    return fit_layer(W, C, d, bits, P, grid, G, tol, NULL, codes, scales, counts, err, NULL,
+    return fit_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, codes, scales, counts, err, NULL,
                      n_threads);
+}
+
+/* The fit with its options: X == NULL for the stopping rule S1 with tol,
+ * else S4 on X [d][N] with eps / relative; refit != 0 for reading A2. */
+int oracle_fit_ex(const float *W, int64_t C, int64_t d, int bits, int P, const float *grid, int G,
+                  double tol, const float *X, int64_t N, double eps, int relative, int refit,
+                  int8_t *codes, float *scales, int32_t *counts, double *err, double *xerr,
+                  int n_threads)
+{
+    calib_rule cal = {X, N, eps, relative};
+    return fit_layer(W, C, d, bits, P, grid, G, tol, X ? &cal : NULL, refit, codes, scales, counts,
+                     err, X ? xerr : NULL, n_threads);
 }
 
 /* The fit with the stopping rule S4 on the calibration batch X [d][N]. */
@@ -316,7 +348,7 @@ int oracle_fit_calib(const float *W, int64_t C, int64_t d, int bits, int P,
                      double *err, double *xerr, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
-    return fit_layer(W, C, d, bits, P, grid, G, 0.0, &cal, codes, scales, counts, err, xerr,
+    return fit_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, codes, scales, counts, err, xerr,
                      n_threads);
 }
 
@@ -341,6 +373,11 @@ int oracle_fit_calib(const float *W, int64_t C, int64_t d, int bits, int P,
  * with fp32 products and sums), and
  *  V4x the per-point output error (if given) agrees with the fp64 e_n as
  *     V4 asks of ||r||^2, plus the allowance of e_n.
+ * With the refit of reading A2 (oracle_verify_ex, refit != 0), V1 and V2 ask
+ * instead that the codes be those of the best candidate, or of a candidate
+ * within 1e-6 relative of it (a candidate tie), up to code ties, and that
+ * the scale be the least-squares scale of those codes (fl32 of the fp64
+ * quotient, or one fp32 ulp from it: the sums may run in another order).
  * status: 0 ok, 1 count, 2 scale not a candidate, 3 scale not optimal,
  *         4 code, 5 nonzero unused slot, 6 err value, 7 bad count range,
  *         8 output-error value.
@@ -358,8 +395,29 @@ static int fp32_value_ok(double got, double ref, double slack, double *emax)
     return got == (double)(float)ref || dev <= 1e-5 * ref + slack + 0x1p-149;
 }
 
+/* V2 for one point: do the codes q equal [r / a]_Q except at code ties?
+ * Adds the ties to *ties; returns 0 on a mismatch. */
+static int codes_agree(const double *r, int64_t d, double as, int M, const int8_t *q, int *ties)
+{
+    int qt = 0;
+    for (int64_t j = 0; j < d; ++j) {
+        double t = r[j] / as;
+        int qr = (int)nearest_code(t, M);
+        int qo = (int)q[j];
+        if (qo != qr) {
+            double fl = floor(t);
+            double half = fabs(t - (fl + 0.5));
+            int lo = (int)nearest_code(fl, M), hi = (int)nearest_code(fl + 1.0, M);
+            if (half <= 1e-6 * fmax(1.0, fabs(t)) && (qo == lo || qo == hi)) qt++;
+            else return 0;
+        }
+    }
+    *ties += qt;
+    return 1;
+}
+
 static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
-                        const float *grid, int G, double tol, const calib_rule *cal,
+                        const float *grid, int G, double tol, const calib_rule *cal, int refit,
                         const int8_t *codes, const float *scales, const int32_t *counts,
                         const float *err, const float *xerr, const int64_t *chan,
                         int64_t n_chan, int32_t *status, int32_t *cand_ties,
@@ -439,30 +497,35 @@ static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                         if (gbest < 0) { st = 1; break; }
                     }
                     float ao = ak[n];
-                    int go = -1;
-                    for (int g = 0; g < G; ++g)
-                        if (a[g] == ao && ao != 0.0f) { go = g; break; }
-                    if (go < 0) { st = 2; break; }
-                    if (go != gbest) {
-                        if (E[go] <= (1.0 + 1e-6) * E[gbest]) ct++;
-                        else { st = 3; break; }
-                    }
-                    /* V2, then continue from the other side's (a, q) */
                     const int8_t *q = qk + (int64_t)n * d;
                     double as = (double)ao;
-                    for (int64_t j = 0; j < d; ++j) {
-                        double t = r[j] / as;
-                        int qr = (int)nearest_code(t, M);
-                        int qo = (int)q[j];
-                        if (qo != qr) {
-                            double fl = floor(t);
-                            double half = fabs(t - (fl + 0.5));
-                            int lo = (int)nearest_code(fl, M), hi = (int)nearest_code(fl + 1.0, M);
-                            if (half <= 1e-6 * fmax(1.0, fabs(t)) && (qo == lo || qo == hi)) qt++;
-                            else { st = 4; break; }
+                    if (refit) {
+                        /* A2: codes of the best candidate or a tied one, then
+                         * the least-squares scale of those codes */
+                        int got = codes_agree(r, d, (double)a[gbest], M, q, &qt) ? gbest : -1;
+                        for (int g = 0; g < G && got < 0; ++g) {
+                            if (g == gbest || a[g] == 0.0f || !(E[g] <= (1.0 + 1e-6) * E[gbest]))
+                                continue;
+                            if (codes_agree(r, d, (double)a[g], M, q, &qt)) { got = g; ct++; }
                         }
+                        if (got < 0) { st = 4; break; }
+                        const double aref = refit_scale(r, q, d);
+                        if (!(ao == (float)aref || fabs(as - aref) <= 0x1p-23 * fabs(aref))) {
+                            st = 2;
+                            break;
+                        }
+                    } else {
+                        int go = -1;
+                        for (int g = 0; g < G; ++g)
+                            if (a[g] == ao && ao != 0.0f) { go = g; break; }
+                        if (go < 0) { st = 2; break; }
+                        if (go != gbest) {
+                            if (E[go] <= (1.0 + 1e-6) * E[gbest]) ct++;
+                            else { st = 3; break; }
+                        }
+                        /* V2, then continue from the other side's (a, q) */
+                        if (!codes_agree(r, d, as, M, q, &qt)) { st = 4; break; }
                     }
-                    if (st) break;
                     for (int64_t j = 0; j < d; ++j) r[j] = r[j] - as * (double)q[j];
                     if (cal) e = calib_error(r, d, cal->X, cal->N);
                 }
@@ -493,9 +556,23 @@ int oracle_verify(const float *W, int64_t C, int64_t d, int bits, int P,
                   int32_t *cand_ties, int32_t *code_ties, int32_t *stop_ties,
                   double *err_relmax, int n_threads)
 {
-    return verify_layer(W, C, d, bits, P, grid, G, tol, NULL, codes, scales, counts, err, NULL,
+    return verify_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, codes, scales, counts, err, NULL,
                         chan, n_chan, status, cand_ties, code_ties, stop_ties, err_relmax,
                         n_threads);
+}
+
+/* The lockstep check of a fit with its options (as oracle_fit_ex). */
+int oracle_verify_ex(const float *W, int64_t C, int64_t d, int bits, int P, const float *grid,
+                     int G, double tol, const float *X, int64_t N, double eps, int relative,
+                     int refit, const int8_t *codes, const float *scales, const int32_t *counts,
+                     const float *err, const float *xerr, const int64_t *chan, int64_t n_chan,
+                     int32_t *status, int32_t *cand_ties, int32_t *code_ties, int32_t *stop_ties,
+                     double *err_relmax, int n_threads)
+{
+    calib_rule cal = {X, N, eps, relative};
+    return verify_layer(W, C, d, bits, P, grid, G, tol, X ? &cal : NULL, refit, codes, scales,
+                        counts, err, X ? xerr : NULL, chan, n_chan, status, cand_ties, code_ties,
+                        stop_ties, err_relmax, n_threads);
 }
 
 /* The lockstep check of a fit with the calibration rule S4; xerr [C][P] is
@@ -509,7 +586,7 @@ int oracle_verify_calib(const float *W, int64_t C, int64_t d, int bits, int P,
                         double *err_relmax, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
-    return verify_layer(W, C, d, bits, P, grid, G, 0.0, &cal, codes, scales, counts, err, xerr,
+    return verify_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, codes, scales, counts, err, xerr,
                         chan, n_chan, status, cand_ties, code_ties, stop_ties, err_relmax,
                         n_threads);
 }

@@ -485,6 +485,62 @@ def check_calib_verifier_fp32_evaluation(orc):
             assert (v["status"] == 8).all()
 
 
+# ------------------------------------------- reading A2: least-squares refit
+def check_refit_one_point(orc):
+    """One point: the codes are Eq. (10)'s at the searched scale (unchanged
+    by the refit) and the scale is fl32(<w, q> / <q, q>) (numpy fp64); the
+    error is never larger than without the refit."""
+    rng = np.random.default_rng(31)
+    W = (rng.standard_normal((60, 50)) * rng.uniform(0.1, 3, (60, 1))).astype(np.float32)
+    for bits, G in ((4, 64), (2, 16), (3, 7)):
+        c0, s0, n0, e0 = orc.fit(W, bits, 1, G, 0.0)
+        c1, s1, n1, e1 = orc.fit(W, bits, 1, G, 0.0, refit=True)
+        assert np.array_equal(c0, c1) and np.array_equal(n0, n1)
+        w, q = W.astype(np.float64), c1[:, 0, :].astype(np.float64)
+        a = np.float32((w * q).sum(1) / (q * q).sum(1))
+        assert np.array_equal(s1[:, 0], a)
+        assert (e1[:, 0] <= e0[:, 0] * (1 + 1e-15)).all()
+
+
+def check_refit_residual_chain(orc):
+    """Several points with the refit: the reported err equals ||w - sum a q||^2
+    rebuilt from the outputs; each new residual is orthogonal to its codes up
+    to the fp32 rounding of a; the error never increases."""
+    rng = np.random.default_rng(32)
+    W = rng.standard_normal((40, 90)).astype(np.float32)
+    codes, scales, counts, err = orc.fit(W, 4, 5, 64, 0.0, refit=True)
+    for k in range(40):
+        r = W[k].astype(np.float64)
+        prev = (r * r).sum()
+        for i in range(counts[k]):
+            q = codes[k, i].astype(np.float64)
+            r = r - float(scales[k, i]) * q
+            e = (r * r).sum()
+            assert abs(e - err[k, i]) <= 1e-12 * max(err[k, i], 1e-300), (k, i)
+            assert abs((r * q).sum()) <= 2.0 ** -23 * abs(float(scales[k, i])) * (q * q).sum() + 1e-300
+            assert e <= prev
+            prev = e
+
+
+def check_refit_verifier(orc):
+    """The refit verifier accepts the oracle's refit output and flags plain
+    grid scales, a refit scale off by 1e-5, and (as the plain verifier) the
+    refit output itself."""
+    rng = np.random.default_rng(33)
+    W = rng.standard_normal((30, 70)).astype(np.float32)
+    codes, scales, counts, err = orc.fit(W, 4, 4, 64, 0.0, refit=True)
+    e32 = err.astype(np.float32)
+    v = orc.verify(W, 4, 4, 64, 0.0, codes, scales, counts, e32, refit=True)
+    assert (v["status"] == 0).all()
+    assert (orc.verify(W, 4, 4, 64, 0.0, codes, scales, counts, e32)["status"] == 2).all()
+    c0, s0, n0, e0 = orc.fit(W, 4, 4, 64, 0.0)
+    v = orc.verify(W, 4, 4, 64, 0.0, c0, s0, n0, None, refit=True)
+    assert (v["status"] == 2).all()
+    s2 = scales.copy()
+    s2[:, 0] *= np.float32(1 + 1e-5)
+    assert (orc.verify(W, 4, 4, 64, 0.0, codes, s2, counts, None, refit=True)["status"] == 2).all()
+
+
 # ------------------------------------------- Sec. 3.4: deployment arithmetic
 def check_integer_scales(orc):
     """Eq. (14), reading I1: exact values, half-way ties to even (worked by
@@ -574,6 +630,7 @@ ALL_CHECKS = [
     check_reconstruct, check_invariances, check_output_error, check_stop_rule,
     check_exponential_decay, check_verifier, check_calib_hadamard_is_isotropic,
     check_calib_stop_definition, check_calib_runs_to_cap, check_calib_zero_batch, check_calib_scaling,
-    check_calib_verifier, check_calib_verifier_fp32_evaluation, check_integer_scales,
+    check_calib_verifier, check_calib_verifier_fp32_evaluation, check_refit_one_point,
+    check_refit_residual_chain, check_refit_verifier, check_integer_scales,
     check_integer_forward_exact, check_integer_forward_one_point, check_integer_forward_approximates,
 ]

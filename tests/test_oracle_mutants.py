@@ -64,6 +64,10 @@ MUTANTS = [
      "for (int i = 0; i < P; ++i) {\n                const int8_t *q"),
     ("int_x_transposed", "(int64_t)X[t * d + j]", "(int64_t)X[j * N + t]"),
     ("int_scale_no_clamp", "if (v > lim) { v = lim; ++clamped; }", "if (v > lim) { ++clamped; }"),
+    ("refit_abs_norm", "qq += (double)q[j] * (double)q[j];", "qq += fabs((double)q[j]);"),
+    ("refit_residual_at_grid_scale", "            as = (double)a_pt;\n", "            (void)0;\n"),
+    ("refit_verifier_any_scale",
+     "if (!(ao == (float)aref || fabs(as - aref) <= 0x1p-23 * fabs(aref))) {", "if (0) {"),
     ("calib_stop_ignores_cap", "if (n >= P || Er == 0.0) return 1;", "if (Er == 0.0) return 1;"),
     ("calib_no_minimum_one_point", "if (n >= 1 && e <= thr) return 1;", "if (e <= thr) return 1;"),
 ]
