@@ -76,6 +76,9 @@ def parse():
     ap.add_argument("--images", type=int, default=8,
                     help="--deploy: images of 224 x 224 in the activation batch")
     ap.add_argument("--shift", type=int, default=16, help="--deploy: p of Eq. (14)")
+    ap.add_argument("--refit", action="store_true",
+                    help="least-squares refit of each point's scale (mpq_fit_layers_ex; implies "
+                         "--separate for the isotropic rule)")
     ap.add_argument("--separate", action="store_true",
                     help="the three batched calls in turn instead of mpq_quantize_layers")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -294,14 +297,17 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    separate = args.separate or args.dense
+    separate = args.separate or args.dense or (args.refit and args.rule != "calib")
     calib = args.rule == "calib"
     if calib and separate:
         raise SystemExit("--rule calib has its own call sequence (no --separate / --dense)")
 
     def step(ev=None):
         if calib:
-            ls.fit_calib(wk.bits, wk.n_grid, wk.tol, True)
+            if args.refit:
+                ls.fit_ex(wk.bits, wk.n_grid, refit=True, calib=True, eps=wk.tol, relative=True)
+            else:
+                ls.fit_calib(wk.bits, wk.n_grid, wk.tol, True)
             ls.reconstruct()
             return
         if not separate:
@@ -312,6 +318,8 @@ def main():
             for i, W in enumerate(Ws):
                 mpq.fit_layer(W, wk.bits, wk.max_points, wk.n_grid, wk.tol, dense=True,
                               out=(ls.codes[i], ls.scales[i], ls.counts[i], ls.fit_err[i]))
+        elif args.refit:
+            ls.fit_ex(wk.bits, wk.n_grid, wk.tol, refit=True)
         else:
             ls.fit(wk.bits, wk.n_grid, wk.tol)
         if ev: ev[1].record(stream)
@@ -440,6 +448,7 @@ def main():
                    "weights": wk.weights, "bits": wk.bits, "max_points": wk.max_points,
                    "n_grid": wk.n_grid, "tol": wk.tol, "calib_columns": wk.n_calib,
                    "points_per_step": points, "search": "dense" if args.dense else "histogram",
+                   "refit": bool(args.refit),
                    "rule": ("Algorithm 2 on the calibration batch, relative" if calib
                             else "||r||^2 <= tol ||w||^2"),
                    "point_counts": count_hist.tolist(),

@@ -254,6 +254,29 @@ int mpq_fit_layers_calib(const mpq_layer *layers, int n_layers, int bits, int ma
                          const float *grid_host, int n_grid, float eps, int relative, void *stream);
 
 /*
+ * mpq_fit_layers_ex - mpq_fit_layers with options (opt == NULL: exactly
+ * mpq_fit_layers).
+ *   refit     nonzero: once a point's codes q are fixed (Eq. (10) at the
+ *             scale Eq. (9) chose), its scale becomes the least-squares
+ *             scale for them, fl32(<r, q> / <q, q>) (fp64 sums), and the
+ *             residual of Eq. (7) uses that scale.  A variant of Algorithm 1
+ *             (which keeps the searched scale).
+ *   calib     nonzero: the stopping rule of mpq_fit_layers_calib with eps and
+ *             relative (reads X, n and fit_xerr of every layer; tol unused).
+ * refit and calib need the histogram search for every layer (d <= 32768;
+ * else MPQ_ERR_SHAPE).  Errors as for mpq_fit_layers / mpq_fit_layers_calib.
+ */
+typedef struct mpq_fit_options {
+    int refit;
+    int calib;
+    float eps;
+    int relative;
+} mpq_fit_options;
+int mpq_fit_layers_ex(const mpq_layer *layers, int n_layers, int bits, int max_points,
+                      const float *grid_host, int n_grid, float tol, const mpq_fit_options *opt,
+                      void *stream);
+
+/*
  * Deployment arithmetic (Sec. 3.4).
  *
  * mpq_integer_scales - the integer scales of Eq. (14):

@@ -250,7 +250,7 @@ struct FitJob {
 // Batching does not change any channel's result.
 std::vector<FitJob> build_fit_jobs(Search mode, bool hist_fits, const mpq_layer *layers, int n_layers,
                                    int M, int max_points, const float *dgrid, int n_grid, float tol,
-                                   double own_launch_weights)
+                                   double own_launch_weights, int refit = 0)
 {
     std::vector<FitJob> jobs;
     auto hist = [&](const mpq_layer &L) {
@@ -291,6 +291,7 @@ std::vector<FitJob> build_fit_jobs(Search mode, bool hist_fits, const mpq_layer 
         j.b.grid = dgrid;
         j.b.tol = (double)tol;
         j.b.step = -1;   // the whole fit (calibration steps set it per launch)
+        j.b.refit = refit;
         return j;
     };
     auto add_layer = [&](FitJob &j, int l) {
@@ -389,20 +390,35 @@ int upload_grid(const float *grid_host, int n_grid, hipStream_t s, float **dgrid
     return MPQ_OK;
 }
 
+// Layers that need the histogram search (the refit and the calibration
+// steps exist only there): MPQ_ERR_SHAPE for a layer it does not take.
+int require_hist(const mpq_layer *layers, int n_layers, bool hist_fits, const char *what)
+{
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_layer &L = layers[l];
+        if (L.c_out > 0 && !(hist_fits && mpq::fit_hist_supports(L.d)))
+            return fail(MPQ_ERR_SHAPE, "%sd = %lld: %s needs the histogram search "
+                        "(d <= %lld, n_grid within its LDS)", n_layers > 1 ? "a layer's " : "",
+                        (long long)L.d, what, (long long)mpq::kHistMaxDim);
+    }
+    return MPQ_OK;
+}
+
 int fit_layers_impl(Search mode, const mpq_layer *layers, int n_layers, int bits, int max_points,
-                    const float *grid_host, int n_grid, float tol, void *stream)
+                    const float *grid_host, int n_grid, float tol, void *stream, int refit = 0)
 {
     bool any = false, hist_fits = false;
     int rc = fit_checks(mode, layers, n_layers, bits, max_points, grid_host, n_grid, tol, &any,
                         &hist_fits);
     if (rc != MPQ_OK || !any) return rc;
+    if (refit && (rc = require_hist(layers, n_layers, hist_fits, "the refit")) != MPQ_OK) return rc;
     hipStream_t s = (hipStream_t)stream;
     float *dgrid = nullptr;
     rc = upload_grid(grid_host, n_grid, s, &dgrid);
     if (rc != MPQ_OK) return rc;
     const int M = (1 << (bits - 1)) - 1;
     const std::vector<FitJob> jobs = build_fit_jobs(mode, hist_fits, layers, n_layers, M, max_points,
-                                                    dgrid, n_grid, tol, -1.0);
+                                                    dgrid, n_grid, tol, -1.0, refit);
     std::vector<double> work;
     for (const FitJob &j : jobs) work.push_back(j.work);
     const hipError_t e = run_concurrently(s, work, [&](int i, hipStream_t st) {
@@ -604,7 +620,8 @@ int quantize_impl(const mpq_layer *layers, int n_layers, int bits, int max_point
 // output-error pass scores the listed channels of every layer.  The relative
 // threshold's output error of W runs beside the first fit step.
 int calib_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
-               const float *grid_host, int n_grid, float eps, int relative, void *stream)
+               const float *grid_host, int n_grid, float eps, int relative, void *stream,
+               int refit = 0)
 {
     if (n_layers < 0 || (n_layers > 0 && !layers))
         return fail(MPQ_ERR_INVALID_ARG, "layers must hold n_layers >= 0 entries");
@@ -626,13 +643,7 @@ int calib_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
     int rc = fit_checks(Search::kAuto, layers, n_layers, bits, max_points, grid_host, n_grid, 0.0f,
                         &any, &hist_fits);
     if (rc != MPQ_OK || !any) return rc;
-    for (int l = 0; l < n_layers; ++l) {
-        const mpq_layer &L = layers[l];
-        if (L.c_out > 0 && !(hist_fits && mpq::fit_hist_supports(L.d)))
-            return fail(MPQ_ERR_SHAPE, "%sd = %lld: the calibration fit needs the histogram search "
-                        "(d <= %lld, n_grid within its LDS)", n_layers > 1 ? "a layer's " : "",
-                        (long long)L.d, (long long)mpq::kHistMaxDim);
-    }
+    if ((rc = require_hist(layers, n_layers, hist_fits, "the calibration fit")) != MPQ_OK) return rc;
     hipStream_t s = (hipStream_t)stream;
     const int P = max_points;
 
@@ -662,7 +673,7 @@ int calib_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
 
     const int M = (1 << (bits - 1)) - 1;
     std::vector<FitJob> jobs = build_fit_jobs(Search::kAuto, true, layers, n_layers, M, P, dgrid,
-                                              n_grid, 0.0f, -1.0);
+                                              n_grid, 0.0f, -1.0, refit);
     for (FitJob &j : jobs) {
         j.b.eps = (double)eps;
         for (int i = 0; i < j.b.n_layers; ++i) {
@@ -916,6 +927,19 @@ int mpq_fit_layers_calib(const mpq_layer *layers, int n_layers, int bits, int ma
                          const float *grid_host, int n_grid, float eps, int relative, void *stream)
 {
     return calib_impl(layers, n_layers, bits, max_points, grid_host, n_grid, eps, relative, stream);
+}
+
+int mpq_fit_layers_ex(const mpq_layer *layers, int n_layers, int bits, int max_points,
+                      const float *grid_host, int n_grid, float tol, const mpq_fit_options *opt,
+                      void *stream)
+{
+    if (!opt) return fit_layers_impl(Search::kAuto, layers, n_layers, bits, max_points, grid_host,
+                                     n_grid, tol, stream);
+    if (opt->calib)
+        return calib_impl(layers, n_layers, bits, max_points, grid_host, n_grid, opt->eps,
+                          opt->relative, stream, opt->refit != 0);
+    return fit_layers_impl(Search::kAuto, layers, n_layers, bits, max_points, grid_host, n_grid, tol,
+                           stream, opt->refit != 0);
 }
 
 int mpq_output_error(const float *W, const int8_t *codes, const float *scales,

@@ -291,6 +291,7 @@ fit_hist_kernel(const HistBatch B)
     extern __shared__ __align__(16) double hsmem[];
     __shared__ float s_redf[kWaves];
     __shared__ double s_redd[kWaves];
+    __shared__ double s_redd2[kWaves];
     __shared__ int s_fin[kMaxFinalists];
     __shared__ int s_nfin;
     __shared__ int s_gbest;
@@ -362,22 +363,50 @@ fit_hist_kernel(const HistBatch B)
         int8_t *qrow = qk + (int64_t)(i - 1) * d;
         const double ap = (double)apend;
         const double ia = 1.0 / ap;
+        // code of Eq. (10) at the searched scale: y is within |y| 2^-51 of
+        // the fp64 quotient fl(r / a), so the two round to the same integer
+        // unless y lies within 2^-40 of a half-integer (or |y| >= 2^10, where
+        // both clip to the same M); only then is the quotient formed
+        auto code_of = [&](double ru) {
+            const double y = ru * ia;
+            double c = rint(y);
+            if (fabs(fabs(y - c) - 0.5) < 0x1p-40) c = rint(ru / ap);
+            return fmin(fmax(c, -Md), Md);
+        };
+        // the scale the residual update uses: the searched one, or (refit)
+        // the least-squares scale of the codes, fl32(<r, q> / <q, q>)
+        double aupd = ap;
+        if (B.refit && i > s0) {
+            double rq = 0.0, qq = 0.0;
+#pragma unroll kUnroll
+            for (int u = 0; u < EPT; ++u) {
+                const int j = t + T * u;
+                if (kGlobal && T * u >= d) break;
+                if (j < d) {
+                    const double ru = kGlobal ? rebuild(u, i - 1) : r[u];
+                    const double c = code_of(ru);
+                    qrow[j] = (int8_t)(int)c;
+                    rq = fma(ru, c, rq);
+                    qq = fma(c, c, qq);
+                }
+            }
+            block_sum2<T>(rq, qq, s_redd, s_redd2);
+            const float afit = (float)(rq / qq);
+            if (t == 0) {
+                Ly.scales[k * P + (i - 1)] = afit;
+                s_scale[i - 1] = afit;   // read only after the next barrier
+            }
+            aupd = (double)afit;
+        }
 #pragma unroll kUnroll
         for (int u = 0; u < EPT; ++u) {
             const int j = t + T * u;
             if (kGlobal && T * u >= d) break;
             double ru = kGlobal ? rebuild(u, i > s0 ? i - 1 : i) : r[u];
             if (i > s0 && j < d) {
-                // y is within |y| 2^-51 of the fp64 quotient fl(r / a), so the
-                // two round to the same integer unless y lies within 2^-40 of a
-                // half-integer (or |y| >= 2^10, where both clip to the same M);
-                // only then is the quotient formed
-                const double y = ru * ia;
-                double c = rint(y);
-                if (fabs(fabs(y - c) - 0.5) < 0x1p-40) c = rint(ru / ap);
-                c = fmin(fmax(c, -Md), Md);
-                qrow[j] = (int8_t)(int)c;
-                ru = fma(-ap, c, ru);
+                const double c = code_of(ru);
+                if (!B.refit) qrow[j] = (int8_t)(int)c;
+                ru = fma(-aupd, c, ru);
             }
             if constexpr (!kGlobal) r[u] = ru;
             lmax = fmaxf(lmax, fabsf((float)ru));

@@ -91,6 +91,8 @@ struct HistBatch {
     // enters the step's list.
     int step;
     double eps;
+    // reading A2: each point's scale refitted by least squares for its codes
+    int refit;
     HistLayer L[kMaxBatchLayers];
 };
 static_assert(sizeof(HistBatch) <= 4096, "kernel arguments");

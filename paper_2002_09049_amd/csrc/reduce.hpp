@@ -227,6 +227,33 @@ __device__ __forceinline__ void block_max_sum(float &vmax, double &vsum, float *
     }
 }
 
+// two sums of doubles over the workgroup, with one pair of barriers; fixed
+// order.  scratch_a / scratch_b hold one value per wavefront.
+template <int kThreads>
+__device__ __forceinline__ void block_sum2(double &a, double &b, double *scratch_a, double *scratch_b)
+{
+    constexpr int kWaves = kThreads / kWave;
+    a = wave_reduce(a, SumOp());
+    b = wave_reduce(b, SumOp());
+    if constexpr (kWaves > 1) {
+        const int wid = threadIdx.x / kWave;
+        if ((threadIdx.x % kWave) == 0) {
+            scratch_a[wid] = a;
+            scratch_b[wid] = b;
+        }
+        __syncthreads();
+        double x = scratch_a[0], y = scratch_b[0];
+#pragma unroll
+        for (int i = 1; i < kWaves; ++i) {
+            x += scratch_a[i];
+            y += scratch_b[i];
+        }
+        __syncthreads();
+        a = x;
+        b = y;
+    }
+}
+
 template <int kThreads>
 __device__ __forceinline__ ArgMin block_argmin(ArgMin v, ArgMin *scratch)
 {

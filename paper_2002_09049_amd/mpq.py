@@ -33,7 +33,7 @@ EXPORTS = ("mpq_fit_layer", "mpq_fit_layer_dense", "mpq_fit_layers", "mpq_fit_ma
            "mpq_reconstruct_layers", "mpq_last_error", "mpq_timing_enable", "mpq_timing_read",
            "mpq_fit_kernel_of", "mpq_quantize_layers", "mpq_fit_layer_calib",
            "mpq_fit_layers_calib", "mpq_integer_scales", "mpq_integer_forward",
-           "mpq_integer_forward_layers")
+           "mpq_integer_forward_layers", "mpq_fit_layers_ex")
 
 
 class Layer(ctypes.Structure):
@@ -45,6 +45,12 @@ class Layer(ctypes.Structure):
                 ("out_ref", ctypes.c_void_p), ("W_hat", ctypes.c_void_p),
                 ("fit_xerr", ctypes.c_void_p)]
 
+
+
+class FitOptions(ctypes.Structure):
+    """struct mpq_fit_options (include/mpq.h)."""
+    _fields_ = [("refit", ctypes.c_int), ("calib", ctypes.c_int), ("eps", ctypes.c_float),
+                ("relative", ctypes.c_int)]
 
 
 class IntLayer(ctypes.Structure):
@@ -91,6 +97,8 @@ def load(path: str = LIB_PATH):
     lib.mpq_integer_forward.restype = i32
     lib.mpq_integer_forward_layers.argtypes = [P, i32, i32, i32, P]
     lib.mpq_integer_forward_layers.restype = i32
+    lib.mpq_fit_layers_ex.argtypes = [P, i32, i32, i32, P, i32, f32, P, P]
+    lib.mpq_fit_layers_ex.restype = i32
     lib.mpq_fit_max_dim.argtypes = [i32]
     lib.mpq_fit_max_dim.restype = i64
     lib.mpq_output_error.argtypes = [P, P, P, P, i64, i64, i32, P, i64, P, P, P]
@@ -391,6 +399,18 @@ class LayerSet:
         if g.shape != (n_grid,):
             raise ValueError("grid must have n_grid entries")
         return g
+
+    def fit_ex(self, bits: int, n_grid: int, tol: float = 0.0, refit: bool = False,
+               calib: bool = False, eps: float = 0.0, relative: bool = True, grid=None, stream=None):
+        """mpq_fit_layers_ex: the fit with options (refit: reading A2; calib:
+        Algorithm 2's stopping rule on the calibration batches)."""
+        if calib and self.X is None:
+            raise ValueError("LayerSet was built without calibration batches")
+        g = self._grid(grid, n_grid)
+        opt = FitOptions(1 if refit else 0, 1 if calib else 0, float(eps), 1 if relative else 0)
+        _check(load().mpq_fit_layers_ex(ctypes.addressof(self.arr), self.n, bits, self.max_points,
+                                        None if g is None else g.ctypes.data_as(ctypes.c_void_p),
+                                        n_grid, float(tol), ctypes.addressof(opt), _stream(stream)))
 
     def fit(self, bits: int, n_grid: int, tol: float, grid=None, stream=None):
         g = self._grid(grid, n_grid)

@@ -292,3 +292,36 @@ def test_int_layer_struct_matches_header(tmp_path):
     out = [int(x) for x in subprocess.check_output([str(exe)]).split()]
     assert out[0] == ctypes.sizeof(mpq.IntLayer)
     assert out[1:] == [getattr(mpq.IntLayer, f).offset for f in fields]
+
+
+def test_fit_options_struct_matches_header(tmp_path):
+    import subprocess
+    from paper_2002_09049_amd import mpq
+    fields = [f for f, _ in mpq.FitOptions._fields_]
+    src = tmp_path / "off.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "mpq.h"\nint main(void){\n'
+                   '  printf("%zu\\n", sizeof(mpq_fit_options));\n' +
+                   "".join(f'  printf("%zu\\n", offsetof(mpq_fit_options, {f}));\n' for f in fields) +
+                   "  return 0;\n}\n")
+    exe = tmp_path / "off"
+    subprocess.check_call(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)])
+    out = [int(x) for x in subprocess.check_output([str(exe)]).split()]
+    assert out[0] == ctypes.sizeof(mpq.FitOptions)
+    assert out[1:] == [getattr(mpq.FitOptions, f).offset for f in fields]
+
+
+def test_fit_layers_ex_checks_arguments(lib):
+    from paper_2002_09049_amd import mpq
+    E = mpq.MPQ_ERR_INVALID_ARG
+    arr = (mpq.Layer * 1)()
+    L = arr[0]
+    L.W, L.c_out, L.d, L.codes, L.scales, L.counts = 1, 4, 16, 1, 1, 1
+    p = ctypes.addressof(arr)
+    for opt in (None, mpq.FitOptions(1, 0, 0.0, 0), mpq.FitOptions(1, 1, 1e-3, 1)):
+        o = None if opt is None else ctypes.addressof(opt)
+        assert lib.mpq_fit_layers_ex(p, 1, 9, 4, None, 8, 1e-3, o, None) == E
+        assert lib.mpq_fit_layers_ex(p, 1, 4, 0, None, 8, 1e-3, o, None) == E
+    opt = mpq.FitOptions(0, 1, 1e-3, 1)          # calib needs X and fit_xerr
+    assert lib.mpq_fit_layers_ex(p, 1, 4, 4, None, 8, 1e-3, ctypes.addressof(opt), None) == E
+    L.c_out = 0
+    assert lib.mpq_fit_layers_ex(p, 1, 4, 4, None, 8, 1e-3, ctypes.addressof(opt), None) == 0

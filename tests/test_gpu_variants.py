@@ -1,0 +1,106 @@
+"""Parity of the fit's variants with the oracle, through the C ABI:
+the least-squares refit of each point's scale (reading A2), alone and with
+Algorithm 2's stopping rule.  Judged by the oracle's lockstep verifier in its
+refit mode (codes of the best or a tied candidate, the least-squares scale of
+those codes within one fp32 ulp, the other rules as for the plain fit)."""
+import numpy as np
+import pytest
+
+from gpu_util import say, to_dev
+from paper_2002_09049_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from paper_2002_09049_amd import mpq
+    mpq.load()
+    yield
+
+
+def _fit_ex(W, bits, P, G, tol=0.0, refit=True, X=None, eps=0.0, relative=True):
+    import torch
+    from paper_2002_09049_amd import mpq
+    ls = mpq.LayerSet([to_dev(W)], P, calib=None if X is None else [to_dev(X)])
+    ls.fit_ex(bits, G, tol, refit=refit, calib=X is not None, eps=eps, relative=relative)
+    torch.cuda.synchronize()
+    out = (ls.codes[0].cpu().numpy(), ls.scales[0].cpu().numpy(), ls.counts[0].cpu().numpy(),
+           ls.fit_err[0].cpu().numpy())
+    return out if X is None else out + (ls.xerr[0].cpu().numpy(),)
+
+
+def _ok(v):
+    bad = np.nonzero(v["status"])[0]
+    assert bad.size == 0, (f"{bad.size} channels fail: channels {v['channels'][bad][:8]} "
+                           f"status {v['status'][bad][:8]}")
+
+
+REFIT = [
+    # (C, d, bits, P, G, tol): the variants and modes of the search kernel
+    (3, 1, 4, 4, 128, 1e-3),
+    (40, 9, 4, 8, 512, 1e-3),
+    (33, 17, 3, 8, 7, 1e-4),
+    (64, 147, 4, 4, 256, 1e-3),
+    (64, 576, 4, 4, 128, 1e-3),
+    (20, 1000, 2, 6, 1000, 0.0),
+    (10, 2304, 4, 8, 256, 1e-5),
+    (7, 4608, 3, 8, 512, 5e-4),
+    (6, 9000, 4, 4, 64, 0.0),
+    (4, 20000, 3, 4, 256, 1e-4),
+]
+
+
+@pytest.mark.parametrize("C,d,bits,P,G,tol", REFIT, ids=[f"C{c}_d{d}_b{b}_P{p}_G{g}" for c, d, b, p, g, _ in REFIT])
+def test_refit_parity(orc, C, d, bits, P, G, tol):
+    say(f"case refit C={C} d={d} bits={bits} P={P} G={G} tol={tol}")
+    W = wl.random_weights(C, d, seed=C * 7 + d)
+    codes, scales, counts, err = _fit_ex(W, bits, P, G, tol)
+    _ok(orc.verify(W, bits, P, G, float(np.float32(tol)), codes, scales, counts, err, refit=True))
+
+
+def test_refit_improves_every_first_point():
+    """The refit keeps the first point's codes and never raises its error."""
+    W = wl.random_weights(200, 300, seed=4)
+    c0, s0, n0, e0 = _fit_ex(W, 4, 1, 128, refit=False)
+    c1, s1, n1, e1 = _fit_ex(W, 4, 1, 128, refit=True)
+    assert np.array_equal(c0, c1)
+    assert (e1[:, 0] <= e0[:, 0] * (1 + 1e-6)).all() and (e1[:, 0] < e0[:, 0]).mean() > 0.9
+
+
+def test_refit_with_calibration_rule(orc):
+    C, d, N = 50, 576, 256
+    W = wl.random_weights(C, d, seed=9)
+    X = wl.random_calib(d, N, seed=10)
+    say("case refit + Algorithm 2 rule")
+    codes, scales, counts, err, xerr = _fit_ex(W, 4, 6, 128, X=X, eps=2e-3)
+    _ok(orc.verify_calib(W, 4, 6, 128, X, float(np.float32(2e-3)), True, codes, scales, counts, err,
+                         xerr, refit=True))
+
+
+def test_refit_rejects_dense_only_lengths():
+    from paper_2002_09049_amd import mpq
+    W = wl.random_weights(2, 40000, seed=1)
+    with pytest.raises(mpq.MPQError) as e:
+        _fit_ex(W, 4, 2, 16)
+    assert e.value.status == mpq.MPQ_ERR_SHAPE
+
+
+def test_refit_workload_resnet18_sampled(orc):
+    import torch
+    from paper_2002_09049_amd import mpq
+    w = wl.get("resnet18")
+    Ws = [to_dev(wl.layer_weights(w, i)) for i in range(len(w.layers))]
+    say("case refit resnet18 full size")
+    ls = mpq.LayerSet(Ws, w.max_points)
+    ls.fit_ex(w.bits, w.n_grid, w.tol, refit=True)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(2)
+    for li, (C, d) in enumerate(w.layers):
+        ch = np.unique(np.concatenate([[0, C - 1], rng.choice(C, size=min(8, C), replace=False)]))
+        out = (ls.codes[li].cpu().numpy(), ls.scales[li].cpu().numpy(), ls.counts[li].cpu().numpy(),
+               ls.fit_err[li].cpu().numpy())
+        _ok(orc.verify(Ws[li].cpu().numpy(), w.bits, w.max_points, w.n_grid,
+                       float(np.float32(w.tol)), *out, channels=ch, refit=True))
