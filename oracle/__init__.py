@@ -63,11 +63,11 @@ def _declare(lib):
     lib.oracle_levels.restype = i32
     lib.oracle_default_grid.argtypes = [i32, P]
     lib.oracle_default_grid.restype = None
-    lib.oracle_fit_ex.argtypes = [P, i64, i64, i32, i32, P, i32, f64, P, i64, f64, i32, i32, P, P, P,
-                                  P, P, i32]
+    lib.oracle_fit_ex.argtypes = [P, i64, i64, i32, i32, P, i32, f64, P, i64, i32, f64, i32, i32,
+                                  i32, P, P, P, P, P, i32]
     lib.oracle_fit_ex.restype = i32
-    lib.oracle_verify_ex.argtypes = [P, i64, i64, i32, i32, P, i32, f64, P, i64, f64, i32, i32, P, P,
-                                     P, P, P, P, i64, P, P, P, P, P, i32]
+    lib.oracle_verify_ex.argtypes = [P, i64, i64, i32, i32, P, i32, f64, P, i64, i32, f64, i32, i32,
+                                     i32, P, P, P, P, P, P, i64, P, P, P, P, P, i32]
     lib.oracle_verify_ex.restype = i32
     lib.oracle_integer_scales.argtypes = [P, P, i64, i32, i32, P]
     lib.oracle_integer_scales.restype = i64
@@ -138,7 +138,18 @@ class Oracle:
         return self._fit(W, bits, max_points, n_grid, tol, None, 0.0, False, refit, grid,
                          n_threads)[:4]
 
-    def _fit(self, W, bits, P, n_grid, tol, X, eps, relative, refit, grid, n_threads):
+    def fit_clip(self, W, bits: int, max_points: int, n_grid: int, X, tol: float = 0.0,
+                 calib: bool = False, eps: float = 0.0, relative: bool = True, clip_grid: int = 20,
+                 grid=None, n_threads: int = 0):
+        """Fit whose first point is the clipping of Eq. (13) on X (reading C1),
+        then Algorithm 1 with the stopping rule S1 (tol) or, with calib, S4.
+        Returns (codes, scales, counts, err, xerr)."""
+        return self._fit(W, bits, max_points, n_grid, tol, X, eps, relative, False, grid,
+                         n_threads, calib=calib, clip_grid=clip_grid)
+
+    def _fit(self, W, bits, P, n_grid, tol, X, eps, relative, refit, grid, n_threads, calib=None,
+             clip_grid=0):
+        calib = (X is not None) if calib is None else calib
         W = np.ascontiguousarray(W, dtype=np.float32)
         C, d = W.shape
         if X is not None:
@@ -151,9 +162,9 @@ class Oracle:
         xerr = np.zeros((C, P), np.float64)
         g = _grid(grid, n_grid)
         rc = self.lib.oracle_fit_ex(_p(W), C, d, bits, P, _p(g), n_grid, float(tol), _p(X),
-                                    0 if X is None else X.shape[1], float(eps), 1 if relative else 0,
-                                    1 if refit else 0, _p(codes_), _p(scales), _p(counts), _p(err),
-                                    _p(xerr), n_threads)
+                                    0 if X is None else X.shape[1], 1 if calib else 0, float(eps),
+                                    1 if relative else 0, 1 if refit else 0, int(clip_grid),
+                                    _p(codes_), _p(scales), _p(counts), _p(err), _p(xerr), n_threads)
         if rc != 0:
             raise MemoryError("oracle_fit_ex failed")
         return codes_, scales, counts, err, xerr
@@ -169,8 +180,18 @@ class Oracle:
         return self._verify(W, bits, max_points, n_grid, tol, None, 0.0, False, refit, codes_,
                             scales, counts, err, None, grid, channels, n_threads)
 
+    def verify_clip(self, W, bits, max_points, n_grid, X, codes_, scales, counts, err=None,
+                    xerr=None, tol: float = 0.0, calib: bool = False, eps: float = 0.0,
+                    relative: bool = True, clip_grid: int = 20, grid=None, channels=None,
+                    n_threads: int = 0):
+        """Lockstep check of a fit whose first point is the clipping of reading C1."""
+        return self._verify(W, bits, max_points, n_grid, tol, X, eps, relative, False, codes_,
+                            scales, counts, err, xerr, grid, channels, n_threads, calib=calib,
+                            clip_grid=clip_grid)
+
     def _verify(self, W, bits, P, n_grid, tol, X, eps, relative, refit, codes_, scales, counts,
-                err, xerr, grid, channels, n_threads):
+                err, xerr, grid, channels, n_threads, calib=None, clip_grid=0):
+        calib = (X is not None) if calib is None else calib
         W = np.ascontiguousarray(W, dtype=np.float32)
         C, d = W.shape
         if X is not None:
@@ -190,7 +211,8 @@ class Oracle:
         g = _grid(grid, n_grid)
         rc = self.lib.oracle_verify_ex(
             _p(W), C, d, bits, P, _p(g), n_grid, float(tol), _p(X), 0 if X is None else X.shape[1],
-            float(eps), 1 if relative else 0, 1 if refit else 0, _p(codes_), _p(scales),
+            1 if calib else 0, float(eps), 1 if relative else 0, 1 if refit else 0, int(clip_grid),
+            _p(codes_), _p(scales),
             _p(counts), _p(e), _p(xe), _p(chan), n, _p(out["status"]), _p(out["cand_ties"]),
             _p(out["code_ties"]), _p(out["stop_ties"]), _p(out["err_relmax"]), n_threads)
         if rc != 0:
@@ -279,5 +301,5 @@ def _delegate(name):
 
 for _n in ("levels", "default_grid", "candidate_scales", "codes", "scale_error", "fit",
            "verify", "fit_calib", "verify_calib", "output_error", "reconstruct",
-           "integer_scales", "integer_forward"):
+           "integer_scales", "integer_forward", "fit_clip", "verify_clip"):
     globals()[_n] = _delegate(_n)

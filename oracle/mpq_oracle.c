@@ -50,6 +50,14 @@
  *          residual of Eq. (7) uses it.
  *   E1     Output error: mean over the N columns of X of ((w - w~) . x)^2.
  *   P1     Scales are stored as fp32 values (exactly the candidate value).
+ *   C1     Variant (clip != 0): the clipping of Eq. (13) per channel (the set
+ *          of weights sharing K is one channel).  K runs over
+ *          [0.05 : 0.05 : 1] * max|w|, i.e. the candidate scales a_j =
+ *          fl32(fl32(max|w|) c_j / M), c_j = fl32(j / 20); the first point is
+ *          (a_j, [w / a_j]_Q) for the j whose output error on X is smallest
+ *          (ties: the smallest j; zero scales skipped); Algorithm 1 then
+ *          continues from that point with the stopping rule, as the paper
+ *          fixes K before adding points.
  *   I1     Eq. (14) rounds 2^p a_i to the nearest integer with ties to even
  *          (R1); a value outside the 32-bit range is clamped to
  *          [-(2^31 - 1), 2^31 - 1] and counted.
@@ -203,6 +211,17 @@ static double calib_threshold(const calib_rule *cal, const double *w, int64_t d)
     return cal->relative ? cal->eps * calib_error(w, d, cal->X, cal->N) : cal->eps;
 }
 
+/* Reading C1's inputs, with per-thread work arrays. */
+typedef struct {
+    const float *X;
+    int64_t N;
+    const float *c;   /* [G] the multipliers j / G */
+    int G;
+    float *a;         /* [G] work */
+    double *e;        /* [G] work */
+    double *D;        /* [2 d] work */
+} clip_rule;
+
 /* S4 with n points taken: stop at P, at a zero residual, or once the output
  * error e of the n >= 1 points is at most thr. */
 static int calib_should_stop(int n, int P, double Er, double e, double thr)
@@ -227,9 +246,30 @@ static double refit_scale(const double *r, const int8_t *q, int64_t d)
     return rq / qq;
 }
 
+/* Reading C1: the clipping candidates of a channel and their output errors
+ * on X [d][N] (Eq. (13) for one channel); returns the chosen index, or -1
+ * if every candidate scale is zero.  a [clipG], e [clipG], D [d] work. */
+static int clip_choose(const float *w, int64_t d, int M, const float *cc, int clipG, const float *X,
+                       int64_t N, float *a, double *e, double *D, int8_t *q)
+{
+    for (int64_t j = 0; j < d; ++j) D[j] = (double)w[j];
+    oracle_candidate_scales(D, d, M, cc, clipG, a);
+    int best = -1;
+    for (int g = 0; g < clipG; ++g) {
+        e[g] = INFINITY;
+        if (a[g] == 0.0f) continue;
+        oracle_codes(D, d, (double)a[g], M, q);
+        double *R = D + d;                                   /* w - a q, fp64 */
+        for (int64_t j = 0; j < d; ++j) R[j] = (double)w[j] - (double)a[g] * (double)q[j];
+        e[g] = calib_error(R, d, X, N);                      /* Eq. (12) / (13) */
+        if (best < 0 || e[g] < e[best]) best = g;
+    }
+    return best;
+}
+
 static int fit_channel(const float *w, int64_t d, int M, int P, const float *c,
-                       int G, double tol, const calib_rule *cal, int refit, int8_t *codes,
-                       float *scales, double *err, double *xerr, double *r, float *a,
+                       int G, double tol, const calib_rule *cal, int refit, const clip_rule *clip,
+                       int8_t *codes, float *scales, double *err, double *xerr, double *r, float *a,
                        double *E)
 {
     for (int64_t j = 0; j < d; ++j) r[j] = (double)w[j];   /* r_1 = w, Eq. (7) */
@@ -237,6 +277,22 @@ static int fit_channel(const float *w, int64_t d, int M, int P, const float *c,
     double thr = cal ? calib_threshold(cal, r, d) : 0.0;
     double e = 0.0;                                         /* S4: e_n */
     int n = 0;
+    if (clip && Ew > 0.0 && P >= 1) {                       /* C1: the first point */
+        int g = clip_choose(w, d, M, clip->c, clip->G, clip->X, clip->N, clip->a, clip->e,
+                            clip->D, codes);
+        if (g >= 0) {
+            double as = (double)clip->a[g];
+            oracle_codes(r, d, as, M, codes);
+            for (int64_t j = 0; j < d; ++j) r[j] = r[j] - as * (double)codes[j];
+            scales[0] = clip->a[g];
+            n = 1;
+            err[0] = sum_sq(r, d);
+            if (cal) {
+                e = calib_error(r, d, cal->X, cal->N);
+                if (xerr) xerr[0] = e;
+            }
+        }
+    }
     for (;;) {
         double Er = sum_sq(r, d);
         if (cal ? calib_should_stop(n, P, Er, e, thr) : should_stop(n, P, Er, Ew, tol)) break;
@@ -279,14 +335,17 @@ static int n_threads_or_default(int nt)
  * [C][P] (may be NULL).  Slots at or after a channel's count are zero. */
 static int fit_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                      const float *grid, int G, double tol, const calib_rule *cal, int refit,
+                     const float *clipX, int64_t clipN, int clipG,
                      int8_t *codes, float *scales, int32_t *counts, double *err,
                      double *xerr, int n_threads)
 {
     int M = oracle_levels(bits);
     float *c = (float *)malloc(sizeof(float) * (size_t)G);
-    if (!c) return -1;
+    float *cc = (float *)malloc(sizeof(float) * (size_t)(clipG > 0 ? clipG : 1));
+    if (!c || !cc) { free(c); free(cc); return -1; }
     if (grid) memcpy(c, grid, sizeof(float) * (size_t)G);
     else oracle_default_grid(G, c);
+    if (clipG > 0) oracle_default_grid(clipG, cc);
     memset(codes, 0, (size_t)(C * P * d));
     memset(scales, 0, sizeof(float) * (size_t)(C * P));
     if (err) memset(err, 0, sizeof(double) * (size_t)(C * P));
@@ -300,7 +359,13 @@ static int fit_layer(const float *W, int64_t C, int64_t d, int bits, int P,
         double *E = (double *)malloc(sizeof(double) * (size_t)G);
         double *e = (double *)malloc(sizeof(double) * (size_t)P);
         double *xe = (double *)malloc(sizeof(double) * (size_t)P);
-        if (!r || !a || !E || !e || !xe) {
+        clip_rule cl = {clipX, clipN, cc, clipG, NULL, NULL, NULL};
+        if (clipG > 0) {
+            cl.a = (float *)malloc(sizeof(float) * (size_t)clipG);
+            cl.e = (double *)malloc(sizeof(double) * (size_t)clipG);
+            cl.D = (double *)malloc(sizeof(double) * (size_t)(2 * d));
+        }
+        if (!r || !a || !E || !e || !xe || (clipG > 0 && (!cl.a || !cl.e || !cl.D))) {
 #pragma omp atomic write
             fail = 1;
         } else {
@@ -308,7 +373,8 @@ static int fit_layer(const float *W, int64_t C, int64_t d, int bits, int P,
             for (int64_t k = 0; k < C; ++k) {
                 memset(e, 0, sizeof(double) * (size_t)P);
                 memset(xe, 0, sizeof(double) * (size_t)P);
-                int n = fit_channel(W + k * d, d, M, P, c, G, tol, cal, refit, codes + k * P * d,
+                int n = fit_channel(W + k * d, d, M, P, c, G, tol, cal, refit,
+                                    clipG > 0 ? &cl : NULL, codes + k * P * d,
                                     scales + k * P, e, xe, r, a, E);
                 counts[k] = n;
                 if (err) memcpy(err + k * P, e, sizeof(double) * (size_t)P);
@@ -316,8 +382,10 @@ static int fit_layer(const float *W, int64_t C, int64_t d, int bits, int P,
             }
         }
         free(r); free(a); free(E); free(e); free(xe);
+        free(cl.a); free(cl.e); free(cl.D);
     }
     free(c);
+    free(cc);
     return fail ? -1 : 0;
 }
 
@@ -325,20 +393,21 @@ int oracle_fit(const float *W, int64_t C, int64_t d, int bits, int P,
                const float *grid, int G, double tol, int8_t *codes,
                float *scales, int32_t *counts, double *err, int n_threads)
 {
-    return fit_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, codes, scales, counts, err, NULL,
-                     n_threads);
+    return fit_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, NULL, 0, 0, codes, scales, counts,
+                     err, NULL, n_threads);
 }
 
-/* The fit with its options: X == NULL for the stopping rule S1 with tol,
- * else S4 on X [d][N] with eps / relative; refit != 0 for reading A2. */
+/* The fit with its options: calib == 0 for the stopping rule S1 with tol,
+ * else S4 on X [d][N] with eps / relative; refit != 0 for reading A2;
+ * clipG > 0 for reading C1 on X with clipG candidates (the paper's 20). */
 int oracle_fit_ex(const float *W, int64_t C, int64_t d, int bits, int P, const float *grid, int G,
-                  double tol, const float *X, int64_t N, double eps, int relative, int refit,
-                  int8_t *codes, float *scales, int32_t *counts, double *err, double *xerr,
-                  int n_threads)
+                  double tol, const float *X, int64_t N, int calib, double eps, int relative,
+                  int refit, int clipG, int8_t *codes, float *scales, int32_t *counts, double *err,
+                  double *xerr, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
-    return fit_layer(W, C, d, bits, P, grid, G, tol, X ? &cal : NULL, refit, codes, scales, counts,
-                     err, X ? xerr : NULL, n_threads);
+    return fit_layer(W, C, d, bits, P, grid, G, tol, calib ? &cal : NULL, refit, X, N, clipG,
+                     codes, scales, counts, err, calib ? xerr : NULL, n_threads);
 }
 
 /* The fit with the stopping rule S4 on the calibration batch X [d][N]. */
@@ -348,8 +417,8 @@ int oracle_fit_calib(const float *W, int64_t C, int64_t d, int bits, int P,
                      double *err, double *xerr, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
-    return fit_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, codes, scales, counts, err, xerr,
-                     n_threads);
+    return fit_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, NULL, 0, 0, codes, scales, counts, err,
+                     xerr, n_threads);
 }
 
 /* ------------------------------------------------------------------------
@@ -378,6 +447,10 @@ int oracle_fit_calib(const float *W, int64_t C, int64_t d, int bits, int P,
  * within 1e-6 relative of it (a candidate tie), up to code ties, and that
  * the scale be the least-squares scale of those codes (fl32 of the fp64
  * quotient, or one fp32 ulp from it: the sums may run in another order).
+ * With the clipping of reading C1 (clipG > 0), the first point's scale must
+ * be a clipping candidate whose output error is within 1e-5 relative plus
+ * the fp32 evaluation allowance (calib_slack) of the smallest one, and its
+ * codes Eq. (10)'s at that scale (up to code ties).
  * status: 0 ok, 1 count, 2 scale not a candidate, 3 scale not optimal,
  *         4 code, 5 nonzero unused slot, 6 err value, 7 bad count range,
  *         8 output-error value.
@@ -418,6 +491,7 @@ static int codes_agree(const double *r, int64_t d, double as, int M, const int8_
 
 static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                         const float *grid, int G, double tol, const calib_rule *cal, int refit,
+                        const float *clipX, int64_t clipN, int clipG,
                         const int8_t *codes, const float *scales, const int32_t *counts,
                         const float *err, const float *xerr, const int64_t *chan,
                         int64_t n_chan, int32_t *status, int32_t *cand_ties,
@@ -426,9 +500,11 @@ static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
 {
     int M = oracle_levels(bits);
     float *c = (float *)malloc(sizeof(float) * (size_t)G);
-    if (!c) return -1;
+    float *cc = (float *)malloc(sizeof(float) * (size_t)(clipG > 0 ? clipG : 1));
+    if (!c || !cc) { free(c); free(cc); return -1; }
     if (grid) memcpy(c, grid, sizeof(float) * (size_t)G);
     else oracle_default_grid(G, c);
+    if (clipG > 0) oracle_default_grid(clipG, cc);
     int nt = n_threads_or_default(n_threads);
     int fail = 0;
     (void)C;
@@ -437,7 +513,15 @@ static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
         double *r = (double *)malloc(sizeof(double) * (size_t)d);
         float *a = (float *)malloc(sizeof(float) * (size_t)G);
         double *E = (double *)malloc(sizeof(double) * (size_t)G);
-        if (!r || !a || !E) {
+        clip_rule cl = {clipX, clipN, cc, clipG, NULL, NULL, NULL};
+        int8_t *cq = NULL;
+        if (clipG > 0) {
+            cl.a = (float *)malloc(sizeof(float) * (size_t)clipG);
+            cl.e = (double *)malloc(sizeof(double) * (size_t)clipG);
+            cl.D = (double *)malloc(sizeof(double) * (size_t)(2 * d));
+            cq = (int8_t *)malloc((size_t)d);
+        }
+        if (!r || !a || !E || (clipG > 0 && (!cl.a || !cl.e || !cl.D || !cq))) {
 #pragma omp atomic write
             fail = 1;
         } else {
@@ -499,7 +583,25 @@ static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                     float ao = ak[n];
                     const int8_t *q = qk + (int64_t)n * d;
                     double as = (double)ao;
-                    if (refit) {
+                    int cbest = (clipG > 0 && n == 0)
+                                    ? clip_choose(w, d, M, cc, clipG, clipX, clipN, cl.a, cl.e, cl.D, cq)
+                                    : -1;
+                    if (cbest >= 0) {
+                        /* C1: a clipping candidate within the evaluation allowance of the best */
+                        int go = -1;
+                        for (int g = 0; g < clipG; ++g)
+                            if (cl.a[g] == ao && ao != 0.0f) { go = g; break; }
+                        if (go < 0) { st = 2; break; }
+                        if (go != cbest) {
+                            double *R = cl.D + d;
+                            for (int64_t j = 0; j < d; ++j)
+                                R[j] = (double)w[j] - (double)cl.a[go] * (double)q[j];
+                            const double sg = calib_slack(R, d, clipX, clipN);
+                            if (cl.e[go] <= cl.e[cbest] * (1.0 + 1e-5) + sg) ct++;
+                            else { st = 3; break; }
+                        }
+                        if (!codes_agree(r, d, as, M, q, &qt)) { st = 4; break; }
+                    } else if (refit) {
                         /* A2: codes of the best candidate or a tied one, then
                          * the least-squares scale of those codes */
                         int got = codes_agree(r, d, (double)a[gbest], M, q, &qt) ? gbest : -1;
@@ -544,8 +646,10 @@ static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
             }
         }
         free(r); free(a); free(E);
+        free(cl.a); free(cl.e); free(cl.D); free(cq);
     }
     free(c);
+    free(cc);
     return fail ? -1 : 0;
 }
 
@@ -556,23 +660,23 @@ int oracle_verify(const float *W, int64_t C, int64_t d, int bits, int P,
                   int32_t *cand_ties, int32_t *code_ties, int32_t *stop_ties,
                   double *err_relmax, int n_threads)
 {
-    return verify_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, codes, scales, counts, err, NULL,
-                        chan, n_chan, status, cand_ties, code_ties, stop_ties, err_relmax,
+    return verify_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, NULL, 0, 0, codes, scales, counts,
+                        err, NULL, chan, n_chan, status, cand_ties, code_ties, stop_ties, err_relmax,
                         n_threads);
 }
 
 /* The lockstep check of a fit with its options (as oracle_fit_ex). */
 int oracle_verify_ex(const float *W, int64_t C, int64_t d, int bits, int P, const float *grid,
-                     int G, double tol, const float *X, int64_t N, double eps, int relative,
-                     int refit, const int8_t *codes, const float *scales, const int32_t *counts,
-                     const float *err, const float *xerr, const int64_t *chan, int64_t n_chan,
-                     int32_t *status, int32_t *cand_ties, int32_t *code_ties, int32_t *stop_ties,
-                     double *err_relmax, int n_threads)
+                     int G, double tol, const float *X, int64_t N, int calib, double eps,
+                     int relative, int refit, int clipG, const int8_t *codes, const float *scales,
+                     const int32_t *counts, const float *err, const float *xerr,
+                     const int64_t *chan, int64_t n_chan, int32_t *status, int32_t *cand_ties,
+                     int32_t *code_ties, int32_t *stop_ties, double *err_relmax, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
-    return verify_layer(W, C, d, bits, P, grid, G, tol, X ? &cal : NULL, refit, codes, scales,
-                        counts, err, X ? xerr : NULL, chan, n_chan, status, cand_ties, code_ties,
-                        stop_ties, err_relmax, n_threads);
+    return verify_layer(W, C, d, bits, P, grid, G, tol, calib ? &cal : NULL, refit, X, N, clipG,
+                        codes, scales, counts, err, calib ? xerr : NULL, chan, n_chan, status,
+                        cand_ties, code_ties, stop_ties, err_relmax, n_threads);
 }
 
 /* The lockstep check of a fit with the calibration rule S4; xerr [C][P] is
@@ -586,9 +690,9 @@ int oracle_verify_calib(const float *W, int64_t C, int64_t d, int bits, int P,
                         double *err_relmax, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
-    return verify_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, codes, scales, counts, err, xerr,
-                        chan, n_chan, status, cand_ties, code_ties, stop_ties, err_relmax,
-                        n_threads);
+    return verify_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, NULL, 0, 0, codes, scales, counts,
+                        err, xerr, chan, n_chan, status, cand_ties, code_ties, stop_ties,
+                        err_relmax, n_threads);
 }
 
 /* Residual D = w - sum_{i<n} a_i q_i of one channel, summed in point order

@@ -541,6 +541,100 @@ def check_refit_verifier(orc):
     assert (orc.verify(W, 4, 4, 64, 0.0, codes, s2, counts, None, refit=True)["status"] == 2).all()
 
 
+# ------------------------------------------- reading C1: clipping of Eq. (13)
+def _clip_case(seed, C=25, d=40, N=30):
+    rng = np.random.default_rng(seed)
+    W = (rng.standard_normal((C, d)) * np.exp(0.4 * rng.standard_normal((C, 1)))).astype(np.float32)
+    # correlated inputs, so the output error ranks the candidates unlike ||w - a q||^2
+    X = (rng.standard_normal((d, N)) + 2.0 * rng.standard_normal((1, N))).astype(np.float32)
+    return W, X
+
+
+def check_clip_bruteforce(orc):
+    """The first point is the candidate of [0.05:0.05:1] * max|w| / M whose
+    output error, in numpy fp64, is smallest (first minimum), with Eq. (10)'s
+    codes at that scale."""
+    W, X = _clip_case(41)
+    c20 = orc.default_grid(20)
+    for bits in (4, 3, 2):
+        codes, scales, counts, err, _ = orc.fit_clip(W, bits, 1, 64, X)
+        for k in range(W.shape[0]):
+            w = W[k].astype(np.float64)
+            a = orc.candidate_scales(w, bits, c20)
+            e = []
+            for aj in a:
+                q = orc.codes(w, float(aj), bits).astype(np.float64)
+                e.append(np.mean(((w - float(aj) * q) @ X.astype(np.float64)) ** 2))
+            j = int(np.argmin(e))
+            assert scales[k, 0] == a[j], (bits, k)
+            assert np.array_equal(codes[k, 0], orc.codes(w, float(a[j]), bits))
+
+
+def check_clip_hadamard_is_eq9(orc):
+    """With X X^T = N I the output error is ||w - a q||^2, so the clipped
+    first point is Eq. (9)'s search on the same 20-point grid."""
+    rng = np.random.default_rng(42)
+    W = rng.standard_normal((30, 48)).astype(np.float32)
+    X = bf.hadamard(64)[:48].astype(np.float32)
+    c1, s1, n1, _, _ = orc.fit_clip(W, 4, 1, 64, X)
+    c0, s0, n0, _ = orc.fit(W, 4, 1, 20, 0.0)
+    assert np.array_equal(s1, s0) and np.array_equal(c1, c0)
+
+
+def check_clip_then_algorithm1(orc):
+    """After the clipped point the fit is Algorithm 1 on the residual: the
+    second scale is Eq. (9)'s argmin over the grid of the fp64 residual."""
+    W, X = _clip_case(43)
+    codes, scales, counts, err, _ = orc.fit_clip(W, 4, 3, 64, X)
+    grid = orc.default_grid(64)
+    for k in range(W.shape[0]):
+        assert counts[k] == 3
+        r = W[k].astype(np.float64) - float(scales[k, 0]) * codes[k, 0].astype(np.float64)
+        a = orc.candidate_scales(r, 4, grid)
+        E = [orc.scale_error(r, float(aj), 4) for aj in a]
+        assert scales[k, 1] == a[int(np.argmin(E))], k
+        assert abs(err[k, 0] - (r * r).sum()) <= 1e-12 * (r * r).sum()
+
+
+def check_clip_zero_batch(orc):
+    """X = 0: every candidate's output error is 0, the tie goes to the
+    smallest clipping factor, 0.05 max|w|."""
+    W, X = _clip_case(44)
+    codes, scales, counts, err, _ = orc.fit_clip(W, 4, 1, 64, np.zeros_like(X))
+    c20 = orc.default_grid(20)
+    for k in range(W.shape[0]):
+        assert scales[k, 0] == orc.candidate_scales(W[k].astype(np.float64), 4, c20)[0]
+
+
+def check_clip_verifier(orc):
+    """The clip verifier accepts the oracle's clipped fit, with either
+    stopping rule, and flags fits whose first point is Eq. (9)'s."""
+    W, X = _clip_case(45)
+    out = orc.fit_clip(W, 4, 4, 64, X, tol=1e-3)
+    v = orc.verify_clip(W, 4, 4, 64, X, *out[:3], out[3].astype(np.float32), tol=1e-3)
+    assert (v["status"] == 0).all()
+    out = orc.fit_clip(W, 4, 4, 64, X, calib=True, eps=1e-2)
+    v = orc.verify_clip(W, 4, 4, 64, X, *out[:3], out[3].astype(np.float32), out[4].astype(np.float32),
+                        calib=True, eps=1e-2)
+    assert (v["status"] == 0).all()
+    c0, s0, n0, e0 = orc.fit(W, 4, 4, 64, 1e-3)
+    v = orc.verify_clip(W, 4, 4, 64, X, c0, s0, n0, tol=1e-3)
+    assert (v["status"] != 0).mean() > 0.5
+    # a genuine clipping candidate, but the one with the largest output error
+    codes, scales, counts, _, _ = orc.fit_clip(W, 4, 1, 64, X)
+    c20 = orc.default_grid(20)
+    for k in range(W.shape[0]):
+        w = W[k].astype(np.float64)
+        a = orc.candidate_scales(w, 4, c20)
+        e = [np.mean(((w - float(aj) * orc.codes(w, float(aj), 4)) @ X.astype(np.float64)) ** 2)
+             for aj in a]
+        j = int(np.argmax(e))
+        scales[k, 0] = a[j]
+        codes[k, 0] = orc.codes(w, float(a[j]), 4)
+    v = orc.verify_clip(W, 4, 1, 64, X, codes, scales, counts)
+    assert (v["status"] == 3).all()
+
+
 # ------------------------------------------- Sec. 3.4: deployment arithmetic
 def check_integer_scales(orc):
     """Eq. (14), reading I1: exact values, half-way ties to even (worked by
@@ -631,6 +725,7 @@ ALL_CHECKS = [
     check_exponential_decay, check_verifier, check_calib_hadamard_is_isotropic,
     check_calib_stop_definition, check_calib_runs_to_cap, check_calib_zero_batch, check_calib_scaling,
     check_calib_verifier, check_calib_verifier_fp32_evaluation, check_refit_one_point,
-    check_refit_residual_chain, check_refit_verifier, check_integer_scales,
+    check_refit_residual_chain, check_refit_verifier, check_clip_bruteforce, check_clip_hadamard_is_eq9,
+    check_clip_then_algorithm1, check_clip_zero_batch, check_clip_verifier, check_integer_scales,
     check_integer_forward_exact, check_integer_forward_one_point, check_integer_forward_approximates,
 ]

@@ -68,6 +68,12 @@ MUTANTS = [
     ("refit_residual_at_grid_scale", "            as = (double)a_pt;\n", "            (void)0;\n"),
     ("refit_verifier_any_scale",
      "if (!(ao == (float)aref || fabs(as - aref) <= 0x1p-23 * fabs(aref))) {", "if (0) {"),
+    ("clip_argmax", "if (best < 0 || e[g] < e[best]) best = g;", "if (best < 0 || e[g] > e[best]) best = g;"),
+    ("clip_ties_largest", "if (best < 0 || e[g] < e[best]) best = g;", "if (best < 0 || e[g] <= e[best]) best = g;"),
+    ("clip_error_of_weights", "e[g] = calib_error(R, d, X, N);", "e[g] = calib_error(D, d, X, N);"),
+    ("clip_wrong_levels", "oracle_candidate_scales(D, d, M, cc, clipG, a);",
+     "oracle_candidate_scales(D, d, M + 1, cc, clipG, a);"),
+    ("clip_verifier_any", "if (cl.e[go] <= cl.e[cbest] * (1.0 + 1e-5) + sg) ct++;", "if (1) ct++;"),
     ("calib_stop_ignores_cap", "if (n >= P || Er == 0.0) return 1;", "if (Er == 0.0) return 1;"),
     ("calib_no_minimum_one_point", "if (n >= 1 && e <= thr) return 1;", "if (e <= thr) return 1;"),
 ]
