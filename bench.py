@@ -79,6 +79,9 @@ def parse():
     ap.add_argument("--refit", action="store_true",
                     help="least-squares refit of each point's scale (mpq_fit_layers_ex; implies "
                          "--separate for the isotropic rule)")
+    ap.add_argument("--clip", type=int, default=0, metavar="GC",
+                    help="point 1 from the clipping of Eq. (13) with GC factors (the paper: 20; "
+                         "mpq_fit_layers_ex; implies --separate for the isotropic rule)")
     ap.add_argument("--separate", action="store_true",
                     help="the three batched calls in turn instead of mpq_quantize_layers")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -297,15 +300,16 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    separate = args.separate or args.dense or (args.refit and args.rule != "calib")
+    separate = args.separate or args.dense or ((args.refit or args.clip) and args.rule != "calib")
     calib = args.rule == "calib"
     if calib and separate:
         raise SystemExit("--rule calib has its own call sequence (no --separate / --dense)")
 
     def step(ev=None):
         if calib:
-            if args.refit:
-                ls.fit_ex(wk.bits, wk.n_grid, refit=True, calib=True, eps=wk.tol, relative=True)
+            if args.refit or args.clip:
+                ls.fit_ex(wk.bits, wk.n_grid, refit=args.refit, calib=True, eps=wk.tol, relative=True,
+                          clip_grid=args.clip)
             else:
                 ls.fit_calib(wk.bits, wk.n_grid, wk.tol, True)
             ls.reconstruct()
@@ -318,8 +322,8 @@ def main():
             for i, W in enumerate(Ws):
                 mpq.fit_layer(W, wk.bits, wk.max_points, wk.n_grid, wk.tol, dense=True,
                               out=(ls.codes[i], ls.scales[i], ls.counts[i], ls.fit_err[i]))
-        elif args.refit:
-            ls.fit_ex(wk.bits, wk.n_grid, wk.tol, refit=True)
+        elif args.refit or args.clip:
+            ls.fit_ex(wk.bits, wk.n_grid, wk.tol, refit=args.refit, clip_grid=args.clip)
         else:
             ls.fit(wk.bits, wk.n_grid, wk.tol)
         if ev: ev[1].record(stream)
@@ -376,15 +380,22 @@ def main():
             # rows in all), plus W itself once for the relative threshold;
             # a fit step re-reads W and the codes of the points so far
             code_reads = int((cnt * (cnt - 1) // 2).sum())
-            add(fk, evals=n * wk.n_grid * d, bytes=4 * n * d + code_reads * d + n * d)
+            searched = n - int((cnt > 0).sum()) if args.clip else n
+            add(fk, evals=searched * wk.n_grid * d, bytes=4 * n * d + code_reads * d + n * d)
             add("gemm_err_kernel", flop=2 * (n + C) * d * N)
             add("form_dt_kernel", bytes=8 * (n + C) * d + (n + code_reads) * d)
         else:
             # fit: G candidate errors per (element, point); reads W once, writes the codes
-            add(fk, evals=n * wk.n_grid * d, bytes=4 * C * d + n * d)
+            # (with --clip, point 1 comes from the clipping pass, not the search)
+            searched = n - int((cnt > 0).sum()) if args.clip else n
+            add(fk, evals=searched * wk.n_grid * d, bytes=4 * C * d + n * d)
             add("gemm_err_kernel", flop=2 * C * d * N)
             # form: reads W and the codes of the used points, writes D
             add("form_dt_kernel", bytes=4 * C * d + n * d + 4 * C * d)
+        if args.clip:
+            # the clipping pass: output errors of C * GC candidate rows
+            add("gemm_err_kernel", flop=2 * C * args.clip * d * N)
+            add("form_dt_kernel", bytes=4 * C * d + 4 * C * args.clip * d)
         # reconstruct: reads the codes of the used points, writes fp32
         add("reconstruct_kernel", bytes=n * d + 4 * C * d)
 
@@ -448,7 +459,7 @@ def main():
                    "weights": wk.weights, "bits": wk.bits, "max_points": wk.max_points,
                    "n_grid": wk.n_grid, "tol": wk.tol, "calib_columns": wk.n_calib,
                    "points_per_step": points, "search": "dense" if args.dense else "histogram",
-                   "refit": bool(args.refit),
+                   "refit": bool(args.refit), "clip_grid": args.clip,
                    "rule": ("Algorithm 2 on the calibration batch, relative" if calib
                             else "||r||^2 <= tol ||w||^2"),
                    "point_counts": count_hist.tolist(),

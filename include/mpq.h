@@ -263,14 +263,24 @@ int mpq_fit_layers_calib(const mpq_layer *layers, int n_layers, int bits, int ma
  *             (which keeps the searched scale).
  *   calib     nonzero: the stopping rule of mpq_fit_layers_calib with eps and
  *             relative (reads X, n and fit_xerr of every layer; tol unused).
- * refit and calib need the histogram search for every layer (d <= 32768;
- * else MPQ_ERR_SHAPE).  Errors as for mpq_fit_layers / mpq_fit_layers_calib.
+ *   clip_grid 0, or the number Gc of clipping factors of Eq. (13) (the paper
+ *             uses 20, K in [0.05 : 0.05 : 1] * max|w|): point 1 of each
+ *             channel is the naive quantization, at the code step
+ *             fl32(fl32(max|w|) * fl32(j / Gc) / M), j = 1..Gc, whose output
+ *             error on the layer's X is smallest (ties: the smallest j); the
+ *             points after it follow Algorithm 1 with the stopping rule.
+ *             Reads X and n of every layer; c_out * Gc <= MPQ_MAX_ERR_DIM.
+ *             Cannot be combined with refit.
+ * refit, calib and clip_grid need the histogram search for every layer
+ * (d <= 32768; else MPQ_ERR_SHAPE).  Errors as for mpq_fit_layers /
+ * mpq_fit_layers_calib.
  */
 typedef struct mpq_fit_options {
     int refit;
     int calib;
     float eps;
     int relative;
+    int clip_grid;
 } mpq_fit_options;
 int mpq_fit_layers_ex(const mpq_layer *layers, int n_layers, int bits, int max_points,
                       const float *grid_host, int n_grid, float tol, const mpq_fit_options *opt,

@@ -290,7 +290,8 @@ std::vector<FitJob> build_fit_jobs(Search mode, bool hist_fits, const mpq_layer 
         j.b.G = n_grid;
         j.b.grid = dgrid;
         j.b.tol = (double)tol;
-        j.b.step = -1;   // the whole fit (calibration steps set it per launch)
+        j.b.start = 0;   // a fresh fit (calibration steps and resumed fits set these)
+        j.b.single = 0;
         j.b.refit = refit;
         return j;
     };
@@ -338,6 +339,10 @@ hipError_t launch_fit_job(const FitJob &j, int n_grid, hipStream_t st)
     return j.dense ? mpq::launch_fit(j.p, mpq::fit_layout(j.p.d, n_grid), st)
                    : mpq::launch_fit_hist(j.b, j.variant, j.channels, st);
 }
+
+int clip_checks(const mpq_layer *layers, int n_layers, int clip_grid);
+int clip_first_points(const mpq_layer *layers, int n_layers, int M, int P, int Gc, bool with_xerr,
+                      const std::vector<mpq::ErrLayerIn> &extra, hipStream_t s);
 
 // Checks shared by the calls that fit: arguments, every layer's buffers, and
 // that every layer fits a search kernel (*hist_fits: the histogram search's
@@ -405,20 +410,35 @@ int require_hist(const mpq_layer *layers, int n_layers, bool hist_fits, const ch
 }
 
 int fit_layers_impl(Search mode, const mpq_layer *layers, int n_layers, int bits, int max_points,
-                    const float *grid_host, int n_grid, float tol, void *stream, int refit = 0)
+                    const float *grid_host, int n_grid, float tol, void *stream, int refit = 0,
+                    int clip_grid = 0)
 {
+    if (clip_grid && n_layers > 0 && layers) {
+        const int rc0 = clip_checks(layers, n_layers, clip_grid);
+        if (rc0 != MPQ_OK) return rc0;
+    }
     bool any = false, hist_fits = false;
     int rc = fit_checks(mode, layers, n_layers, bits, max_points, grid_host, n_grid, tol, &any,
                         &hist_fits);
     if (rc != MPQ_OK || !any) return rc;
     if (refit && (rc = require_hist(layers, n_layers, hist_fits, "the refit")) != MPQ_OK) return rc;
+    if (clip_grid && (rc = require_hist(layers, n_layers, hist_fits, "the clipping")) != MPQ_OK)
+        return rc;
     hipStream_t s = (hipStream_t)stream;
     float *dgrid = nullptr;
     rc = upload_grid(grid_host, n_grid, s, &dgrid);
     if (rc != MPQ_OK) return rc;
     const int M = (1 << (bits - 1)) - 1;
-    const std::vector<FitJob> jobs = build_fit_jobs(mode, hist_fits, layers, n_layers, M, max_points,
-                                                    dgrid, n_grid, tol, -1.0, refit);
+    std::vector<FitJob> jobs = build_fit_jobs(mode, hist_fits, layers, n_layers, M, max_points,
+                                              dgrid, n_grid, tol, -1.0, refit);
+    if (clip_grid) {   // point 1 from the clipping, then the fit resumes from it
+        rc = clip_first_points(layers, n_layers, M, max_points, clip_grid, false, {}, s);
+        if (rc != MPQ_OK) {
+            if (dgrid) (void)mpq::scratch_free(dgrid, s);
+            return rc;
+        }
+        for (FitJob &j : jobs) j.b.start = 1;
+    }
     std::vector<double> work;
     for (const FitJob &j : jobs) work.push_back(j.work);
     const hipError_t e = run_concurrently(s, work, [&](int i, hipStream_t st) {
@@ -613,6 +633,106 @@ int quantize_impl(const mpq_layer *layers, int n_layers, int bits, int max_point
     return MPQ_OK;
 }
 
+// Checks of a clipped fit (reading C1): every layer needs its batch.
+int clip_checks(const mpq_layer *layers, int n_layers, int clip_grid)
+{
+    if (clip_grid < 1 || clip_grid > MPQ_MAX_GRID)
+        return fail(MPQ_ERR_INVALID_ARG, "clip_grid must be in [1, %d] (got %d)", MPQ_MAX_GRID, clip_grid);
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_layer &L = layers[l];
+        int rc = MPQ_OK;
+        if (L.c_out > 0) {
+            if (!L.X) rc = fail(MPQ_ERR_INVALID_ARG, "the clipping needs X");
+            else if (L.n < 1 || L.n > MPQ_MAX_ERR_DIM)
+                rc = fail(MPQ_ERR_INVALID_ARG, "n must be in [1, %d] (got %lld)", MPQ_MAX_ERR_DIM,
+                          (long long)L.n);
+            else if ((double)L.c_out * clip_grid > MPQ_MAX_ERR_DIM)
+                rc = fail(MPQ_ERR_INVALID_ARG, "c_out * clip_grid must be <= %d", MPQ_MAX_ERR_DIM);
+        }
+        if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
+    }
+    return MPQ_OK;
+}
+
+// Reading C1 for every layer: the clipping candidates of each channel, their
+// output errors on X (one batched output-error pass, together with `extra`
+// items such as the relative threshold's reference errors), then point 1 of
+// every channel.  with_xerr: point 1's output error goes to fit_xerr.
+int clip_first_points(const mpq_layer *layers, int n_layers, int M, int P, int Gc, bool with_xerr,
+                      const std::vector<mpq::ErrLayerIn> &extra, hipStream_t s)
+{
+    std::vector<size_t> off(n_layers);
+    size_t total = 0;
+    for (int l = 0; l < n_layers; ++l) {
+        off[l] = total;
+        total += (size_t)std::max<int64_t>(layers[l].c_out, 0) * (size_t)Gc;
+    }
+    float *buf = nullptr;   // cand [total], then ecand [total]
+    hipError_t e = mpq::scratch_alloc((void **)&buf, 2 * sizeof(float) * total, s);
+    if (e != hipSuccess) return fail(MPQ_ERR_NOMEM, "scratch: %s", hipGetErrorString(e));
+    float *cand = buf, *ecand = buf + total;
+    // the launches of the candidate and choice kernels
+    std::vector<std::pair<mpq::ClipBatch, int64_t>> batches;
+    {
+        mpq::ClipBatch b = {};
+        b.M = M;
+        b.P = P;
+        b.Gc = Gc;
+        int64_t ch = 0;
+        for (int l = 0; l <= n_layers; ++l) {
+            if ((l == n_layers || b.n_layers == mpq::kMaxClipLayers ||
+                 (l < n_layers && ch + layers[l].c_out > 0x7fffffffLL)) && b.n_layers > 0) {
+                batches.push_back({b, ch});
+                b.n_layers = 0;
+                ch = 0;
+            }
+            if (l == n_layers) break;
+            const mpq_layer &L = layers[l];
+            if (L.c_out == 0) continue;
+            mpq::ClipLayer &C = b.L[b.n_layers++];
+            C = mpq::ClipLayer{L.W, cand + off[l], ecand + off[l], L.codes, L.scales, L.counts,
+                               L.fit_err, with_xerr ? L.fit_xerr : nullptr, (int)L.d, (int)ch};
+            ch += L.c_out;
+        }
+    }
+    std::vector<mpq::ErrLayerIn> in;
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_layer &L = layers[l];
+        if (L.c_out == 0) continue;
+        mpq::ErrLayerIn I = {};
+        I.W = L.W;
+        I.codes = L.codes;
+        I.scales = L.scales;
+        I.counts = L.counts;
+        I.X = L.X;
+        I.err = ecand + off[l];
+        I.C = L.c_out;
+        I.d = L.d;
+        I.n = L.n;
+        I.cand = cand + off[l];
+        I.Gc = Gc;
+        I.M = M;
+        in.push_back(I);
+    }
+    in.insert(in.end(), extra.begin(), extra.end());
+    ErrJobs ej;
+    int rc = err_jobs(in, s, &ej);
+    if (rc != MPQ_OK) {
+        (void)mpq::scratch_free(buf, s);
+        return rc;
+    }
+    for (size_t i = 0; i < batches.size() && e == hipSuccess; ++i)
+        e = mpq::launch_clip(batches[i].first, batches[i].second, false, s);
+    if (e == hipSuccess)
+        e = run_concurrently(s, ej.work, [&](int i, hipStream_t st) { return launch_err_job(in, ej, i, P, st); });
+    for (size_t i = 0; i < batches.size() && e == hipSuccess; ++i)
+        e = mpq::launch_clip(batches[i].first, batches[i].second, true, s);
+    if (ej.scratch) (void)mpq::scratch_free(ej.scratch, s);
+    (void)mpq::scratch_free(buf, s);
+    if (e != hipSuccess) return hip_fail(e, "clipping kernel launch");
+    return MPQ_OK;
+}
+
 // Algorithm 2's stopping rule on a calibration batch, for every layer.  Per
 // step s = 0 .. max_points - 1: the fit launches take point s + 1 of every
 // channel that has not stopped (a channel stops once the output error of its
@@ -621,7 +741,7 @@ int quantize_impl(const mpq_layer *layers, int n_layers, int bits, int max_point
 // threshold's output error of W runs beside the first fit step.
 int calib_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
                const float *grid_host, int n_grid, float eps, int relative, void *stream,
-               int refit = 0)
+               int refit = 0, int clip_grid = 0)
 {
     if (n_layers < 0 || (n_layers > 0 && !layers))
         return fail(MPQ_ERR_INVALID_ARG, "layers must hold n_layers >= 0 entries");
@@ -638,6 +758,10 @@ int calib_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
                           MPQ_MAX_ERR_DIM, (long long)L.c_out, (long long)L.n);
         }
         if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
+    }
+    if (clip_grid) {
+        const int rc0 = clip_checks(layers, n_layers, clip_grid);
+        if (rc0 != MPQ_OK) return rc0;
     }
     bool any = false, hist_fits = false;
     int rc = fit_checks(Search::kAuto, layers, n_layers, bits, max_points, grid_host, n_grid, 0.0f,
@@ -713,12 +837,26 @@ int calib_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
     e = mpq::launch_zero_i32((int32_t *)state, (int64_t)P * n_layers, s);
     std::vector<double> fit_work;
     for (const FitJob &j : jobs) fit_work.push_back(j.work);
-    for (int step = 0; step < P && e == hipSuccess; ++step) {
-        for (FitJob &j : jobs) j.b.step = step;
+    int first = 0;
+    if (clip_grid && e == hipSuccess) {
+        // point 1 from the clipping (its output error is e_1), with the
+        // reference errors of the relative threshold in the same pass
+        rc = clip_first_points(layers, n_layers, M, P, clip_grid, true, in_ref, s);
+        if (rc != MPQ_OK) {
+            release();
+            return rc;
+        }
+        first = 1;
+    }
+    for (int step = first; step < P && e == hipSuccess; ++step) {
+        for (FitJob &j : jobs) {
+            j.b.start = step;
+            j.b.single = 1;
+        }
         // the fit step; at step 0 beside it the output error of W (ref)
         std::vector<double> w = fit_work;
         const int n_fit = (int)w.size();
-        if (step == 0) w.insert(w.end(), ej_ref.work.begin(), ej_ref.work.end());
+        if (step == 0 && !clip_grid) w.insert(w.end(), ej_ref.work.begin(), ej_ref.work.end());
         e = run_concurrently(s, w, [&](int i, hipStream_t st) {
             return i < n_fit ? launch_fit_job(jobs[i], n_grid, st)
                              : launch_err_job(in_ref, ej_ref, i - n_fit, P, st);
@@ -935,11 +1073,14 @@ int mpq_fit_layers_ex(const mpq_layer *layers, int n_layers, int bits, int max_p
 {
     if (!opt) return fit_layers_impl(Search::kAuto, layers, n_layers, bits, max_points, grid_host,
                                      n_grid, tol, stream);
+    if (opt->clip_grid && opt->refit)
+        return fail(MPQ_ERR_INVALID_ARG, "refit and clip_grid cannot be combined");
+    if (opt->clip_grid < 0) return fail(MPQ_ERR_INVALID_ARG, "clip_grid must be >= 0");
     if (opt->calib)
         return calib_impl(layers, n_layers, bits, max_points, grid_host, n_grid, opt->eps,
-                          opt->relative, stream, opt->refit != 0);
+                          opt->relative, stream, opt->refit != 0, opt->clip_grid);
     return fit_layers_impl(Search::kAuto, layers, n_layers, bits, max_points, grid_host, n_grid, tol,
-                           stream, opt->refit != 0);
+                           stream, opt->refit != 0, opt->clip_grid);
 }
 
 int mpq_output_error(const float *W, const int8_t *codes, const float *scales,

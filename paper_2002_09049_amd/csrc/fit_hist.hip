@@ -325,10 +325,10 @@ fit_hist_kernel(const HistBatch B)
     int8_t *qk = Ly.codes + k * (int64_t)P * d;
     const float *wk = Ly.W + k * (int64_t)d;
 
-    // calibration step: resume a channel that holds s0 points and has not
-    // stopped (its count is s0), from its stored points; take at most one
-    const bool stepping = B.step >= 0;
-    const int s0 = stepping ? B.step : 0;
+    // resume a channel that holds s0 points and has not stopped (its count
+    // is s0) from its stored points; in a calibration step take at most one
+    const bool stepping = B.single != 0;
+    const int s0 = B.start;
     if (s0 >= 1 && Ly.counts[k] != s0) return;   // uniform: one value per workgroup
     if (s0 >= 1) {
         for (int p = t; p < s0; p += T) s_scale[p] = Ly.scales[k * P + p];
@@ -353,6 +353,11 @@ fit_hist_kernel(const HistBatch B)
         S.c[g] = B.grid ? B.grid[g] : (float)((double)(g + 1) / (double)G);
 
     double Ew = 0.0;
+    if (s0 >= 1 && !stepping) {   // ||w||^2 for the stopping rule of a resumed fit
+        double sw = 0.0;
+        for (int j = t; j < d; j += T) sw = fma((double)wk[j], (double)wk[j], sw);
+        Ew = block_reduce<T>(sw, SumOp(), s_redd);
+    }
     float apend = 0.0f;
     int n = 0;
     bool more = false;   // calibration step: the channel took its point and goes on
@@ -652,7 +657,7 @@ fit_hist_kernel(const HistBatch B)
     for (int q = n + t; q < P; q += T) {
         Ly.scales[k * P + q] = 0.0f;
         if (Ly.err) Ly.err[k * P + q] = 0.0f;
-        if (stepping) Ly.xerr[k * P + q] = 0.0f;
+        if (Ly.xerr) Ly.xerr[k * P + q] = 0.0f;
     }
     for (int q = n; q < P; ++q)
         for (int j = t; j < d; j += T) qk[(int64_t)q * d + j] = 0;

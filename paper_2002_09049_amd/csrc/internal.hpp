@@ -69,7 +69,7 @@ struct HistLayer {
     float *scales;      // [C][P]
     int32_t *counts;    // [C]
     float *err;         // [C][P] or nullptr
-    // calibration steps (HistBatch::step >= 0) only:
+    // calibration steps (HistBatch::single) only:
     float *xerr;        // [C][P] output error after each point (written by the error pass)
     const float *ref;   // [C] output error of W itself (relative threshold) or nullptr
     int32_t *list;      // [C] channels that took a point in this step, in any order
@@ -84,12 +84,15 @@ struct HistBatch {
     const float *grid;  // device multipliers or nullptr (default grid)
     double tol;
     int nlat;           // lattice buckets ((2M-1) G + 1) or 0; set by launch_fit_hist
-    // -1: the whole fit with the stopping rule on ||r||^2 (tol).  s >= 0: one
-    // step of the fit on a calibration batch: a channel holding s points
-    // (all channels when s = 0) stops if s >= 1 and xerr[s-1] <= thr
-    // (thr = eps * ref, or eps when ref is null), else takes point s + 1 and
-    // enters the step's list.
-    int step;
+    // Points already stored per channel (start = s >= 1: only the channels
+    // whose count is s take part; their residual is rebuilt from the stored
+    // points).  single == 0: the fit runs to its end with the stopping rule
+    // on ||r||^2 (tol).  single != 0: one step of the fit on a calibration
+    // batch: a channel stops if s >= 1 and xerr[s-1] <= thr (thr = eps * ref,
+    // or eps when ref is null), else takes point s + 1 and enters the
+    // step's list.
+    int start;
+    int single;
     double eps;
     // reading A2: each point's scale refitted by least squares for its codes
     int refit;
@@ -123,15 +126,44 @@ struct ErrLayerIn {
     const int32_t *rows;
     const int32_t *nrows;
     int64_t err_stride;
+    // clipping candidates (cand != nullptr): the item's D rows are the C * Gc
+    // candidate residuals w_k - a_kj [w_k / a_kj]_Q (a_kj = cand[k * Gc + j],
+    // codes in [-M, M]); err[k * Gc + j] is written
+    const float *cand;
+    int Gc, M;
 };
 // The items (an err item per layer with err, a ref item per layer with ref) go
-// in launch groups of up to 24; groups are independent and may run side by
+// in launch groups of up to 22; groups are independent and may run side by
 // side, each with its own scratch.
 int err_group_count(const ErrLayerIn *in, int n_in);
 size_t err_group_scratch_bytes(const ErrLayerIn *in, int n_in, int group);
 double err_group_flop(const ErrLayerIn *in, int n_in, int group);
 hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, int P, void *scratch,
                                      hipStream_t s);
+
+// Clipping of Eq. (13) as the first point: candidate scales, then (after the
+// output error of the candidates) the choice of point 1.  One workgroup per
+// channel; up to kMaxClipLayers layers per launch.
+struct ClipLayer {
+    const float *W;        // [C][d]
+    float *cand;           // [C][Gc] candidate scales
+    const float *ecand;    // [C][Gc] their output errors
+    int8_t *codes;         // [C][P][d]
+    float *scales;         // [C][P]
+    int32_t *counts;       // [C]
+    float *err;            // [C][P] or nullptr
+    float *xerr;           // [C][P] or nullptr (calibration rule: e_1)
+    int d;
+    int c_begin;           // first workgroup of this layer
+};
+constexpr int kMaxClipLayers = 48;
+struct ClipBatch {
+    int n_layers;
+    int M, P, Gc;
+    ClipLayer L[kMaxClipLayers];
+};
+static_assert(sizeof(ClipBatch) <= 4096, "kernel arguments");
+hipError_t launch_clip(const ClipBatch &b, int64_t channels, bool choose, hipStream_t s);
 
 // Stream-ordered scratch from a library-owned memory pool of the current
 // device (kept, not returned to the system, between calls).

@@ -61,7 +61,7 @@ constexpr int kThreads = 256;
 constexpr int kPad = 4;          // LDS row padding (floats); rows stay 16-byte aligned
 constexpr int kVec = kBK * kBM / kThreads / 4;   // float4 per thread and operand per slab
 constexpr int kRowThreads = kBM / (4 * kVec);    // threads per slab row
-constexpr int kMaxErrLayers = 24;
+constexpr int kMaxErrLayers = 22;
 constexpr int kXcds = 8;         // MI355X: workgroups are dealt to 8 XCDs in turn
 constexpr int kFT = 64;          // form tile: 64 rows x 64 k
 
@@ -98,7 +98,9 @@ struct ErrLayer {
     int form_begin;      // first form workgroup
     int form_kt;         // form tiles along k: ceil(d / kFT)
     int fin_begin;       // first finish workgroup
-    int use_points;      // 1: D = residual (err), 0: D = W (ref)
+    int use_points;      // 1: D = residual (err), 0: D = W (ref), 2: D = clipping candidates
+    const float *cand;   // use_points == 2: [C / Gc][Gc] candidate scales (C counts rows of D)
+    int Gc, M;
     int vecw;            // d % 4 == 0, W 16-byte and codes 4-byte aligned
 };
 
@@ -141,7 +143,28 @@ __global__ void __launch_bounds__(256) form_dt_kernel(const ErrGroup g)
     for (int i = 0; i < 4; ++i) {
         const int64_t m = row0 + rb + 16 * i, k = k0 + kc;
         double r[4] = {0.0, 0.0, 0.0, 0.0};
-        if (m < nact) {
+        if (L.use_points == 2 && m < C) {
+            // clipping candidate j of channel ch: w - a [w / a]_Q (Eq. (10)'s
+            // rounding of the fp64 quotient, formed only near a half-integer)
+            const int64_t ch = m / L.Gc;
+            const double a = (double)L.cand[m];
+            const double ia = 1.0 / a, Md = (double)L.M;
+            const float *wr = L.W + ch * d;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (k + u < d) {
+                    const double wj = (double)wr[k + u];
+                    double c = 0.0;
+                    if (a != 0.0) {
+                        const double y = wj * ia;
+                        c = rint(y);
+                        if (fabs(fabs(y - c) - 0.5) < 0x1p-40) c = rint(wj / a);
+                        c = fmin(fmax(c, -Md), Md);
+                    }
+                    r[u] = fma(-a, c, wj);
+                }
+            }
+        } else if (L.use_points != 2 && m < nact) {
             const int64_t row = L.rows ? (int64_t)L.rows[m] : m;
             const int nk = L.use_points ? min(max(L.counts[row], 0), P) : 0;  // counts is caller data
             const float *wr = L.W + row * d;
@@ -389,6 +412,9 @@ struct Item {
     int use_points;
 };
 
+// rows of D of an item: the channels, or their clipping candidates
+int64_t item_rows(const ErrLayerIn &I) { return I.cand ? I.C * I.Gc : I.C; }
+
 struct Plan {
     int64_t ldc, ntm, ntn, splits, kchunk;
     size_t dt_bytes, rowpart_bytes, ypart_bytes;
@@ -401,7 +427,7 @@ std::vector<Item> items_of(const ErrLayerIn *in, int n_in)
 {
     std::vector<Item> it;
     for (int i = 0; i < n_in; ++i)
-        if (in[i].C > 0 && in[i].err) it.push_back(Item{&in[i], 1});
+        if (in[i].C > 0 && in[i].err) it.push_back(Item{&in[i], in[i].cand ? 2 : 1});
     for (int i = 0; i < n_in; ++i)
         if (in[i].C > 0 && in[i].ref) it.push_back(Item{&in[i], 0});
     return it;
@@ -415,8 +441,9 @@ std::vector<Item> items_of(const ErrLayerIn *in, int n_in)
 Plan plan_item(const ErrLayerIn &I)
 {
     Plan q;
-    q.ldc = (I.C + 3) / 4 * 4;
-    q.ntm = (I.C + kBM - 1) / kBM;
+    const int64_t C = item_rows(I);
+    q.ldc = (C + 3) / 4 * 4;
+    q.ntm = (C + kBM - 1) / kBM;
     q.ntn = (I.n + kBN - 1) / kBN;
     const int64_t slabs = (I.d + kBK - 1) / kBK;
     const double work = (double)(q.ntm * q.ntn) * (double)slabs;
@@ -432,8 +459,8 @@ Plan plan_item(const ErrLayerIn &I)
     q.kchunk = kchunk;
     q.splits = (I.d + kchunk - 1) / kchunk;   // no empty K range
     q.dt_bytes = align256(sizeof(float) * (size_t)(I.d * q.ldc));
-    q.rowpart_bytes = align256(sizeof(double) * (size_t)(q.ntn * I.C));
-    q.ypart_bytes = q.splits > 1 ? align256(sizeof(float) * (size_t)(q.splits * I.C * I.n)) : 0;
+    q.rowpart_bytes = align256(sizeof(double) * (size_t)(q.ntn * C));
+    q.ypart_bytes = q.splits > 1 ? align256(sizeof(float) * (size_t)(q.splits * C * I.n)) : 0;
     return q;
 }
 
@@ -469,7 +496,7 @@ double err_group_flop(const ErrLayerIn *in, int n_in, int group)
     const std::vector<Item> it = items_of(in, n_in);
     double f = 0.0;
     for (size_t i = (size_t)group * kMaxErrLayers; i < it.size() && i < (size_t)(group + 1) * kMaxErrLayers; ++i)
-        f += 2.0 * (double)it[i].in->C * (double)it[i].in->d * (double)it[i].in->n;
+        f += 2.0 * (double)item_rows(*it[i].in) * (double)it[i].in->d * (double)it[i].in->n;
     return f;
 }
 
@@ -507,16 +534,19 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
             L.X = I.X;
             L.out = grp[i].use_points ? I.err : I.ref;
             L.use_points = grp[i].use_points;
-            L.rows = grp[i].use_points ? I.rows : nullptr;
-            L.nrows = grp[i].use_points ? I.nrows : nullptr;
-            L.stride = grp[i].use_points && I.err_stride > 0 ? I.err_stride : 1;
+            L.rows = grp[i].use_points == 1 ? I.rows : nullptr;
+            L.nrows = grp[i].use_points == 1 ? I.nrows : nullptr;
+            L.stride = grp[i].use_points == 1 && I.err_stride > 0 ? I.err_stride : 1;
+            L.cand = grp[i].use_points == 2 ? I.cand : nullptr;
+            L.Gc = I.Gc;
+            L.M = I.M;
             L.Dt = (float *)cur;
             cur += q.dt_bytes;
             L.rowpart = (double *)cur;
             cur += q.rowpart_bytes;
             L.ypart = q.splits > 1 ? (float *)cur : nullptr;
             cur += q.ypart_bytes;
-            L.C = (int)I.C;
+            L.C = (int)item_rows(I);
             L.d = (int)I.d;
             L.n = (int)I.n;
             L.ldc = (int)q.ldc;
@@ -529,9 +559,9 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
             blocks += (L.tiles + kXcds - 1) / kXcds * kXcds;
             L.form_kt = (int)((I.d + kFT - 1) / kFT);
             L.form_begin = (int)fblocks;
-            fblocks += (int64_t)L.form_kt * ((I.C + kFT - 1) / kFT);
+            fblocks += (int64_t)L.form_kt * ((L.C + kFT - 1) / kFT);
             L.fin_begin = (int)nblocks;
-            nblocks += q.splits > 1 ? I.C : (I.C + 255) / 256;
+            nblocks += q.splits > 1 ? L.C : (L.C + 255) / 256;
             L.vecw = I.d % 4 == 0 && ((uintptr_t)I.W) % 16 == 0 && ((uintptr_t)I.codes) % 4 == 0;
             if (I.n % 4 != 0 || ((uintptr_t)I.X) % 16 != 0) g.vecx = 0;
         }

@@ -104,3 +104,92 @@ def test_refit_workload_resnet18_sampled(orc):
                ls.fit_err[li].cpu().numpy())
         _ok(orc.verify(Ws[li].cpu().numpy(), w.bits, w.max_points, w.n_grid,
                        float(np.float32(w.tol)), *out, channels=ch, refit=True))
+
+
+def _fit_clip(W, X, bits, P, G, tol=0.0, calib=False, eps=0.0, clip_grid=20):
+    import torch
+    from paper_2002_09049_amd import mpq
+    ls = mpq.LayerSet([to_dev(W)], P, calib=[to_dev(X)])
+    ls.fit_ex(bits, G, tol, calib=calib, eps=eps, relative=True, clip_grid=clip_grid)
+    torch.cuda.synchronize()
+    return (ls.codes[0].cpu().numpy(), ls.scales[0].cpu().numpy(), ls.counts[0].cpu().numpy(),
+            ls.fit_err[0].cpu().numpy(), ls.xerr[0].cpu().numpy())
+
+
+CLIP = [
+    # (C, d, bits, P, G, N, tol)
+    (3, 1, 4, 4, 128, 5, 1e-3),
+    (40, 9, 4, 8, 512, 64, 1e-3),
+    (70, 147, 4, 4, 256, 300, 1e-3),
+    (64, 576, 3, 6, 128, 256, 1e-4),
+    (20, 2304, 4, 4, 256, 1024, 1e-3),
+    (6, 9000, 4, 3, 64, 130, 0.0),
+]
+
+
+@pytest.mark.parametrize("C,d,bits,P,G,N,tol", CLIP, ids=[f"C{c}_d{d}_b{b}_P{p}_G{g}_N{n}" for c, d, b, p, g, n, _ in CLIP])
+def test_clip_parity(orc, C, d, bits, P, G, N, tol):
+    say(f"case clip C={C} d={d} bits={bits} P={P} G={G} N={N} tol={tol}")
+    W = wl.random_weights(C, d, seed=C + 3 * d)
+    X = wl.random_calib(d, N, seed=N)
+    codes, scales, counts, err, _ = _fit_clip(W, X, bits, P, G, tol)
+    _ok(orc.verify_clip(W, bits, P, G, X, codes, scales, counts, err, tol=float(np.float32(tol))))
+    assert (counts >= 1).all()
+
+
+def test_clip_with_calibration_rule(orc):
+    C, d, N = 48, 576, 256
+    W = wl.random_weights(C, d, seed=17)
+    X = wl.random_calib(d, N, seed=18)
+    say("case clip + Algorithm 2 rule")
+    codes, scales, counts, err, xerr = _fit_clip(W, X, 4, 6, 128, calib=True, eps=2e-3)
+    _ok(orc.verify_clip(W, 4, 6, 128, X, codes, scales, counts, err, xerr, calib=True,
+                        eps=float(np.float32(2e-3))))
+
+
+def test_clip_grid_size_and_edges(orc):
+    """Another number of clipping factors; an all-zero channel (no point);
+    a cap of one point; one calibration column."""
+    d, N = 200, 64
+    W = wl.random_weights(9, d, seed=5)
+    W[4] = 0.0
+    X = wl.random_calib(d, N, seed=6)
+    for Gc, P, n in ((8, 4, N), (20, 1, N), (20, 3, 1)):
+        say(f"case clip edges Gc={Gc} P={P} n={n}")
+        Xn = np.ascontiguousarray(X[:, :n])
+        codes, scales, counts, err, _ = _fit_clip(W, Xn, 4, P, 64, 1e-3, clip_grid=Gc)
+        _ok(orc.verify_clip(W, 4, P, 64, Xn, codes, scales, counts, err,
+                            tol=float(np.float32(1e-3)), clip_grid=Gc))
+        assert counts[4] == 0 and (np.delete(counts, 4) >= 1).all()
+
+
+def test_clip_rejects_refit():
+    import torch
+    from paper_2002_09049_amd import mpq
+    W = wl.random_weights(4, 64, seed=1)
+    X = wl.random_calib(64, 16, seed=2)
+    ls = mpq.LayerSet([to_dev(W)], 4, calib=[to_dev(X)])
+    with pytest.raises(mpq.MPQError) as e:
+        ls.fit_ex(4, 64, 1e-3, refit=True, clip_grid=20)
+    assert e.value.status == mpq.MPQ_ERR_INVALID_ARG
+    torch.cuda.synchronize()
+
+
+def test_clip_workload_resnet18_sampled(orc):
+    import torch
+    from paper_2002_09049_amd import mpq
+    w = wl.get("resnet18")
+    Ws = [to_dev(wl.layer_weights(w, i)) for i in range(len(w.layers))]
+    Xs = [to_dev(wl.layer_calib(w, i)) for i in range(len(w.layers))]
+    say("case clip resnet18 full size")
+    ls = mpq.LayerSet(Ws, w.max_points, calib=Xs)
+    ls.fit_ex(w.bits, w.n_grid, w.tol, clip_grid=20)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(3)
+    for li, (C, d) in enumerate(w.layers):
+        ch = np.unique(np.concatenate([[0, C - 1], rng.choice(C, size=min(6, C), replace=False)]))
+        out = (ls.codes[li].cpu().numpy(), ls.scales[li].cpu().numpy(), ls.counts[li].cpu().numpy(),
+               ls.fit_err[li].cpu().numpy())
+        say(f"  layer {li} ({C}x{d})")
+        _ok(orc.verify_clip(Ws[li].cpu().numpy(), w.bits, w.max_points, w.n_grid, Xs[li].cpu().numpy(),
+                            *out, tol=float(np.float32(w.tol)), channels=ch))
