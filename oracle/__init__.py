@@ -64,10 +64,16 @@ def _declare(lib):
     lib.oracle_default_grid.argtypes = [i32, P]
     lib.oracle_default_grid.restype = None
     lib.oracle_fit_ex.argtypes = [P, i64, i64, i32, i32, P, i32, f64, P, i64, i32, f64, i32, i32,
-                                  i32, P, P, P, P, P, i32]
+                                  i32, f64, P, P, P, P, P, i32]
     lib.oracle_fit_ex.restype = i32
     lib.oracle_verify_ex.argtypes = [P, i64, i64, i32, i32, P, i32, f64, P, i64, i32, f64, i32, i32,
-                                     i32, P, P, P, P, P, P, i64, P, P, P, P, P, i32]
+                                     i32, f64, P, P, P, P, P, P, i64, P, P, P, P, P, i32]
+    lib.oracle_min_gap.argtypes = [P, i64, P]
+    lib.oracle_min_gap.restype = f64
+    lib.oracle_paper_grid.argtypes = [P, i64, i32, f64, P, P, P]
+    lib.oracle_paper_grid.restype = None
+    lib.oracle_paper_grid_search.argtypes = [P, i64, i32, f64, i64, P]
+    lib.oracle_paper_grid_search.restype = i64
     lib.oracle_verify_ex.restype = i32
     lib.oracle_integer_scales.argtypes = [P, P, i64, i32, i32, P]
     lib.oracle_integer_scales.restype = i64
@@ -147,8 +153,36 @@ class Oracle:
         return self._fit(W, bits, max_points, n_grid, tol, X, eps, relative, False, grid,
                          n_threads, calib=calib, clip_grid=clip_grid)
 
+    def fit_paper(self, W, bits: int, max_points: int, tol: float, eta: float = 2.0 ** -10,
+                  n_threads: int = 0):
+        """Greedy fit on the paper's own grid, Eq. (11) (readings D1, G3).
+        Returns (codes, scales, counts, err)."""
+        return self._fit(W, bits, max_points, 1, tol, None, 0.0, False, False, None, n_threads,
+                         eta=eta)[:4]
+
+    def min_gap(self, r) -> float:
+        r = np.ascontiguousarray(r, dtype=np.float64)
+        return self.lib.oracle_min_gap(_p(r), r.size, _p(np.empty(r.size)))
+
+    def paper_grid(self, r, bits: int, eta: float = 2.0 ** -10):
+        """(gamma, number of grid points) of Eq. (11) for the residual r."""
+        r = np.ascontiguousarray(r, dtype=np.float64)
+        g = ctypes.c_double()
+        n = ctypes.c_int64()
+        self.lib.oracle_paper_grid(_p(r), r.size, self.levels(bits), float(eta), _p(np.empty(r.size)),
+                                   ctypes.byref(g), ctypes.byref(n))
+        return g.value, n.value
+
+    def paper_grid_search(self, r, bits: int, gamma: float, count: int):
+        """(g, E) of the grid argmin of Eq. (9) over g gamma, 1 <= g <= count."""
+        r = np.ascontiguousarray(r, dtype=np.float64)
+        E = ctypes.c_double()
+        g = self.lib.oracle_paper_grid_search(_p(r), r.size, self.levels(bits), float(gamma),
+                                              int(count), ctypes.byref(E))
+        return int(g), E.value
+
     def _fit(self, W, bits, P, n_grid, tol, X, eps, relative, refit, grid, n_threads, calib=None,
-             clip_grid=0):
+             clip_grid=0, eta=0.0):
         calib = (X is not None) if calib is None else calib
         W = np.ascontiguousarray(W, dtype=np.float32)
         C, d = W.shape
@@ -164,7 +198,8 @@ class Oracle:
         rc = self.lib.oracle_fit_ex(_p(W), C, d, bits, P, _p(g), n_grid, float(tol), _p(X),
                                     0 if X is None else X.shape[1], 1 if calib else 0, float(eps),
                                     1 if relative else 0, 1 if refit else 0, int(clip_grid),
-                                    _p(codes_), _p(scales), _p(counts), _p(err), _p(xerr), n_threads)
+                                    float(eta), _p(codes_), _p(scales), _p(counts), _p(err), _p(xerr),
+                                    n_threads)
         if rc != 0:
             raise MemoryError("oracle_fit_ex failed")
         return codes_, scales, counts, err, xerr
@@ -189,8 +224,14 @@ class Oracle:
                             scales, counts, err, xerr, grid, channels, n_threads, calib=calib,
                             clip_grid=clip_grid)
 
+    def verify_paper(self, W, bits, max_points, tol, codes_, scales, counts, err=None,
+                     eta: float = 2.0 ** -10, channels=None, n_threads: int = 0):
+        """Lockstep check of a fit on the paper's grid (readings D1, G3)."""
+        return self._verify(W, bits, max_points, 1, tol, None, 0.0, False, False, codes_, scales,
+                            counts, err, None, None, channels, n_threads, eta=eta)
+
     def _verify(self, W, bits, P, n_grid, tol, X, eps, relative, refit, codes_, scales, counts,
-                err, xerr, grid, channels, n_threads, calib=None, clip_grid=0):
+                err, xerr, grid, channels, n_threads, calib=None, clip_grid=0, eta=0.0):
         calib = (X is not None) if calib is None else calib
         W = np.ascontiguousarray(W, dtype=np.float32)
         C, d = W.shape
@@ -212,7 +253,7 @@ class Oracle:
         rc = self.lib.oracle_verify_ex(
             _p(W), C, d, bits, P, _p(g), n_grid, float(tol), _p(X), 0 if X is None else X.shape[1],
             1 if calib else 0, float(eps), 1 if relative else 0, 1 if refit else 0, int(clip_grid),
-            _p(codes_), _p(scales),
+            float(eta), _p(codes_), _p(scales),
             _p(counts), _p(e), _p(xe), _p(chan), n, _p(out["status"]), _p(out["cand_ties"]),
             _p(out["code_ties"]), _p(out["stop_ties"]), _p(out["err_relmax"]), n_threads)
         if rc != 0:
@@ -301,5 +342,6 @@ def _delegate(name):
 
 for _n in ("levels", "default_grid", "candidate_scales", "codes", "scale_error", "fit",
            "verify", "fit_calib", "verify_calib", "output_error", "reconstruct",
-           "integer_scales", "integer_forward", "fit_clip", "verify_clip"):
+           "integer_scales", "integer_forward", "fit_clip", "verify_clip", "fit_paper",
+           "verify_paper", "min_gap", "paper_grid", "paper_grid_search"):
     globals()[_n] = _delegate(_n)

@@ -58,6 +58,22 @@
  *          (ties: the smallest j; zero scales skipped); Algorithm 1 then
  *          continues from that point with the stopping rule, as the paper
  *          fixes K before adding points.
+ *   D1     Def. 1's minimal gap: half the smallest difference | |t_i| - |t_j| |
+ *          over pairs with |t_i| != |t_j| (the printed constraint t_i != t_j
+ *          would make it zero for t_i = -t_j); none such: no gap.
+ *   G3     Variant (paper_grid != 0), Eq. (11) with eta: the candidates of a
+ *          step are a_g = g * gamma (fp64), g = 1 .. floor(2 M ||r|| / gamma),
+ *          gamma = min(Delta_r / M, eta) in fp64 (no gap: gamma = eta); the
+ *          scale 0 is left out (Theorem 1 searches (0 : gamma : 2M||r||]).
+ *          The chosen scale is stored as fl32(a_g) (P1) and the point's codes
+ *          (Eq. (10)) and residual use that stored value.
+ *          The grid's argmin of Eq. (9) is found without enumerating it: the
+ *          codes are constant between consecutive breakpoints |r_j| / (k+1/2),
+ *          where E is a convex quadratic, so the argmin is one of the three
+ *          grid points around a breakpoint or one of the two next to the
+ *          vertex A / B of the piece that holds such a point; every such
+ *          candidate is evaluated by Eq. (9) and the smallest error wins
+ *          (ties: the smallest g).
  *   I1     Eq. (14) rounds 2^p a_i to the nearest integer with ties to even
  *          (R1); a value outside the 32-bit range is clamped to
  *          [-(2^31 - 1), 2^31 - 1] and counted.
@@ -180,6 +196,99 @@ static double calib_error(const double *v, int64_t d, const float *X, int64_t N)
     return s / (double)N;
 }
 
+/* ------------------------------------------------------------------------
+ * Eq. (11): the paper's own grid (readings D1, G3).
+ * ------------------------------------------------------------------------ */
+
+static int cmp_desc(const void *x, const void *y)
+{
+    double a = *(const double *)x, b = *(const double *)y;
+    return (a < b) - (a > b);
+}
+
+/* Def. 1 (reading D1): half the smallest positive difference of |r_j|;
+ * 0 when all magnitudes are equal.  work [d]. */
+double oracle_min_gap(const double *r, int64_t d, double *work)
+{
+    for (int64_t j = 0; j < d; ++j) work[j] = fabs(r[j]);
+    qsort(work, (size_t)d, sizeof(double), cmp_desc);
+    double gap = 0.0;
+    for (int64_t j = 1; j < d; ++j) {
+        double diff = work[j - 1] - work[j];
+        if (diff > 0.0 && (gap == 0.0 || diff < gap)) gap = diff;
+    }
+    return gap / 2.0;
+}
+
+/* Eq. (11): the step gamma and the number of grid points (reading G3). */
+void oracle_paper_grid(const double *r, int64_t d, int M, double eta, double *work, double *gamma,
+                       int64_t *count)
+{
+    double gap = oracle_min_gap(r, d, work);
+    double g = gap > 0.0 ? gap / (double)M : eta;
+    if (g > eta) g = eta;
+    *gamma = g;
+    *count = (int64_t)floor(2.0 * (double)M * sqrt(sum_sq(r, d)) / g);
+}
+
+/* A = sum |r_j| |q_j| and B = sum q_j^2 of the codes at scale a. */
+static void codes_ab(const double *r, int64_t d, double a, int M, double *A, double *B)
+{
+    double sa = 0.0, sb = 0.0;
+    for (int64_t j = 0; j < d; ++j) {
+        double q = fabs(nearest_code(r[j] / a, M));
+        sa += fabs(r[j]) * q;
+        sb += q * q;
+    }
+    *A = sa;
+    *B = sb;
+}
+
+/* The grid argmin of Eq. (9) over a_g = g gamma, 1 <= g <= count (reading
+ * G3).  Returns the chosen g (0 if there is none) and its error in *Ebest. */
+int64_t oracle_paper_grid_search(const double *r, int64_t d, int M, double gamma, int64_t count,
+                                 double *Ebest)
+{
+    int64_t best = 0;
+    double Eb = INFINITY;
+    /* evaluate grid point g (and, with vertex != 0, the points nearest the
+     * vertex of its piece) */
+    for (int64_t j = 0; j < d; ++j) {
+        for (int k = 0; k < M; ++k) {
+            double b = fabs(r[j]) / ((double)k + 0.5);     /* a breakpoint */
+            if (b == 0.0) continue;
+            /* the grid points next to the breakpoint; one of them lies inside
+             * each piece it bounds (a grid point exactly at b belongs to one
+             * side by the rounding tie) */
+            int64_t g0 = (int64_t)floor(b / gamma);
+            int64_t around[3] = {g0 - 1, g0, g0 + 1};
+            for (int u = 0; u < 3; ++u) {
+                int64_t g = around[u];
+                if (g < 1 || g > count) continue;
+                int64_t cand[3] = {g, 0, 0};
+                double a = (double)g * gamma;
+                {
+                    double A, B;
+                    codes_ab(r, d, a, M, &A, &B);
+                    if (B > 0.0) {
+                        int64_t gv = (int64_t)floor((A / B) / gamma);
+                        cand[1] = gv;
+                        cand[2] = gv + 1;
+                    }
+                }
+                for (int c = 0; c < 3; ++c) {
+                    int64_t h = cand[c];
+                    if (h < 1 || h > count) continue;
+                    double E = oracle_scale_error(r, d, (double)h * gamma, M);    /* Eq. (9) */
+                    if (E < Eb || (E == Eb && h < best)) { Eb = E; best = h; }
+                }
+            }
+        }
+    }
+    *Ebest = Eb;
+    return best;
+}
+
 /* Verifier only: how far an fp32 evaluation of Eq. (12) may lie from the
  * fp64 value when the outputs of the batch nearly cancel.  The other side
  * rounds v to fp32 and sums each length-d product in fp32; the usual
@@ -269,8 +378,8 @@ static int clip_choose(const float *w, int64_t d, int M, const float *cc, int cl
 
 static int fit_channel(const float *w, int64_t d, int M, int P, const float *c,
                        int G, double tol, const calib_rule *cal, int refit, const clip_rule *clip,
-                       int8_t *codes, float *scales, double *err, double *xerr, double *r, float *a,
-                       double *E)
+                       double eta, double *gwork, int8_t *codes, float *scales, double *err,
+                       double *xerr, double *r, float *a, double *E)
 {
     for (int64_t j = 0; j < d; ++j) r[j] = (double)w[j];   /* r_1 = w, Eq. (7) */
     double Ew = sum_sq(r, d);
@@ -296,13 +405,23 @@ static int fit_channel(const float *w, int64_t d, int M, int P, const float *c,
     for (;;) {
         double Er = sum_sq(r, d);
         if (cal ? calib_should_stop(n, P, Er, e, thr) : should_stop(n, P, Er, Ew, tol)) break;
-        oracle_candidate_scales(r, d, M, c, G, a);
-        int g = grid_search(r, d, a, G, M, E);              /* Eq. (9)  */
-        if (g < 0) break;                                   /* S3: no scale */
-        double as = (double)a[g];
+        float a_pt;
+        if (eta > 0.0) {                                    /* G3: Eq. (11)'s grid */
+            double gamma, Eb;
+            int64_t cnt;
+            oracle_paper_grid(r, d, M, eta, gwork, &gamma, &cnt);
+            int64_t g = oracle_paper_grid_search(r, d, M, gamma, cnt, &Eb);
+            a_pt = (float)((double)g * gamma);
+            if (g < 1 || a_pt == 0.0f) break;               /* S3: no scale */
+        } else {
+            oracle_candidate_scales(r, d, M, c, G, a);
+            int g = grid_search(r, d, a, G, M, E);          /* Eq. (9)  */
+            if (g < 0) break;                               /* S3: no scale */
+            a_pt = a[g];
+        }
+        double as = (double)a_pt;
         int8_t *q = codes + (int64_t)n * d;
         oracle_codes(r, d, as, M, q);                       /* Eq. (10) */
-        float a_pt = a[g];
         if (refit) {                                        /* A2 */
             a_pt = (float)refit_scale(r, q, d);
             as = (double)a_pt;
@@ -335,7 +454,7 @@ static int n_threads_or_default(int nt)
  * [C][P] (may be NULL).  Slots at or after a channel's count are zero. */
 static int fit_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                      const float *grid, int G, double tol, const calib_rule *cal, int refit,
-                     const float *clipX, int64_t clipN, int clipG,
+                     const float *clipX, int64_t clipN, int clipG, double eta,
                      int8_t *codes, float *scales, int32_t *counts, double *err,
                      double *xerr, int n_threads)
 {
@@ -365,7 +484,8 @@ static int fit_layer(const float *W, int64_t C, int64_t d, int bits, int P,
             cl.e = (double *)malloc(sizeof(double) * (size_t)clipG);
             cl.D = (double *)malloc(sizeof(double) * (size_t)(2 * d));
         }
-        if (!r || !a || !E || !e || !xe || (clipG > 0 && (!cl.a || !cl.e || !cl.D))) {
+        double *gw = (double *)malloc(sizeof(double) * (size_t)d);
+        if (!r || !a || !E || !e || !xe || !gw || (clipG > 0 && (!cl.a || !cl.e || !cl.D))) {
 #pragma omp atomic write
             fail = 1;
         } else {
@@ -374,14 +494,14 @@ static int fit_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                 memset(e, 0, sizeof(double) * (size_t)P);
                 memset(xe, 0, sizeof(double) * (size_t)P);
                 int n = fit_channel(W + k * d, d, M, P, c, G, tol, cal, refit,
-                                    clipG > 0 ? &cl : NULL, codes + k * P * d,
+                                    clipG > 0 ? &cl : NULL, eta, gw, codes + k * P * d,
                                     scales + k * P, e, xe, r, a, E);
                 counts[k] = n;
                 if (err) memcpy(err + k * P, e, sizeof(double) * (size_t)P);
                 if (xerr) memcpy(xerr + k * P, xe, sizeof(double) * (size_t)P);
             }
         }
-        free(r); free(a); free(E); free(e); free(xe);
+        free(r); free(a); free(E); free(e); free(xe); free(gw);
         free(cl.a); free(cl.e); free(cl.D);
     }
     free(c);
@@ -393,20 +513,22 @@ int oracle_fit(const float *W, int64_t C, int64_t d, int bits, int P,
                const float *grid, int G, double tol, int8_t *codes,
                float *scales, int32_t *counts, double *err, int n_threads)
 {
-    return fit_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, NULL, 0, 0, codes, scales, counts,
+    return fit_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, NULL, 0, 0, 0.0, codes, scales, counts,
                      err, NULL, n_threads);
 }
 
 /* The fit with its options: calib == 0 for the stopping rule S1 with tol,
  * else S4 on X [d][N] with eps / relative; refit != 0 for reading A2;
- * clipG > 0 for reading C1 on X with clipG candidates (the paper's 20). */
+ * clipG > 0 for reading C1 on X with clipG candidates (the paper's 20);
+ * eta > 0 for the paper's grid of Eq. (11) (reading G3; the paper's 2^-10)
+ * instead of the G-point grid. */
 int oracle_fit_ex(const float *W, int64_t C, int64_t d, int bits, int P, const float *grid, int G,
                   double tol, const float *X, int64_t N, int calib, double eps, int relative,
-                  int refit, int clipG, int8_t *codes, float *scales, int32_t *counts, double *err,
-                  double *xerr, int n_threads)
+                  int refit, int clipG, double eta, int8_t *codes, float *scales, int32_t *counts,
+                  double *err, double *xerr, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
-    return fit_layer(W, C, d, bits, P, grid, G, tol, calib ? &cal : NULL, refit, X, N, clipG,
+    return fit_layer(W, C, d, bits, P, grid, G, tol, calib ? &cal : NULL, refit, X, N, clipG, eta,
                      codes, scales, counts, err, calib ? xerr : NULL, n_threads);
 }
 
@@ -417,8 +539,8 @@ int oracle_fit_calib(const float *W, int64_t C, int64_t d, int bits, int P,
                      double *err, double *xerr, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
-    return fit_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, NULL, 0, 0, codes, scales, counts, err,
-                     xerr, n_threads);
+    return fit_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, NULL, 0, 0, 0.0, codes, scales, counts,
+                     err, xerr, n_threads);
 }
 
 /* ------------------------------------------------------------------------
@@ -491,7 +613,7 @@ static int codes_agree(const double *r, int64_t d, double as, int M, const int8_
 
 static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                         const float *grid, int G, double tol, const calib_rule *cal, int refit,
-                        const float *clipX, int64_t clipN, int clipG,
+                        const float *clipX, int64_t clipN, int clipG, double eta,
                         const int8_t *codes, const float *scales, const int32_t *counts,
                         const float *err, const float *xerr, const int64_t *chan,
                         int64_t n_chan, int32_t *status, int32_t *cand_ties,
@@ -513,6 +635,7 @@ static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
         double *r = (double *)malloc(sizeof(double) * (size_t)d);
         float *a = (float *)malloc(sizeof(float) * (size_t)G);
         double *E = (double *)malloc(sizeof(double) * (size_t)G);
+        double *gw = (double *)malloc(sizeof(double) * (size_t)d);
         clip_rule cl = {clipX, clipN, cc, clipG, NULL, NULL, NULL};
         int8_t *cq = NULL;
         if (clipG > 0) {
@@ -521,7 +644,7 @@ static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
             cl.D = (double *)malloc(sizeof(double) * (size_t)(2 * d));
             cq = (int8_t *)malloc((size_t)d);
         }
-        if (!r || !a || !E || (clipG > 0 && (!cl.a || !cl.e || !cl.D || !cq))) {
+        if (!r || !a || !E || !gw || (clipG > 0 && (!cl.a || !cl.e || !cl.D || !cq))) {
 #pragma omp atomic write
             fail = 1;
         } else {
@@ -560,7 +683,14 @@ static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                     int gbest = -1;
                     int stop_ref = cal ? calib_should_stop(n, P, Er, e, thr)
                                        : should_stop(n, P, Er, Ew, tol);
-                    if (!stop_ref) {
+                    double pg_gamma = 0.0, pg_E = INFINITY;   /* G3 */
+                    int64_t pg_cnt = 0, pg_best = 0;
+                    if (!stop_ref && eta > 0.0) {
+                        oracle_paper_grid(r, d, M, eta, gw, &pg_gamma, &pg_cnt);
+                        pg_best = oracle_paper_grid_search(r, d, M, pg_gamma, pg_cnt, &pg_E);
+                        stop_ref = pg_best < 1 || (float)((double)pg_best * pg_gamma) == 0.0f;
+                        gbest = stop_ref ? -1 : 0;
+                    } else if (!stop_ref) {
                         gbest = grid_search(r, d, a, G, M, E);
                         stop_ref = gbest < 0;
                     }
@@ -577,6 +707,7 @@ static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                     if (stop_other) break;
                     /* V1 */
                     if (gbest < 0) {           /* the other side went on past a stop */
+                        if (eta > 0.0) { st = 1; break; }
                         gbest = grid_search(r, d, a, G, M, E);
                         if (gbest < 0) { st = 1; break; }
                     }
@@ -586,7 +717,23 @@ static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                     int cbest = (clipG > 0 && n == 0)
                                     ? clip_choose(w, d, M, cc, clipG, clipX, clipN, cl.a, cl.e, cl.D, cq)
                                     : -1;
-                    if (cbest >= 0) {
+                    if (eta > 0.0) {
+                        /* G3: fl32 of a grid point g gamma whose error is the
+                         * smallest, or within 1e-6 relative of it */
+                        const int64_t g0 = llround(as / pg_gamma);
+                        double Eo = INFINITY;
+                        for (int64_t h = g0 - 2; h <= g0 + 2; ++h) {
+                            if (h < 1 || h > pg_cnt || (float)((double)h * pg_gamma) != ao) continue;
+                            const double Eh = oracle_scale_error(r, d, (double)h * pg_gamma, M);
+                            if (Eh < Eo) Eo = Eh;
+                        }
+                        if (Eo == INFINITY) { st = 2; break; }
+                        if (Eo > pg_E) {
+                            if (Eo <= (1.0 + 1e-6) * pg_E) ct++;
+                            else { st = 3; break; }
+                        }
+                        if (!codes_agree(r, d, as, M, q, &qt)) { st = 4; break; }
+                    } else if (cbest >= 0) {
                         /* C1: a clipping candidate within the evaluation allowance of the best */
                         int go = -1;
                         for (int g = 0; g < clipG; ++g)
@@ -645,7 +792,7 @@ static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                 stop_ties[s] = stt; err_relmax[s] = emax;
             }
         }
-        free(r); free(a); free(E);
+        free(r); free(a); free(E); free(gw);
         free(cl.a); free(cl.e); free(cl.D); free(cq);
     }
     free(c);
@@ -660,21 +807,22 @@ int oracle_verify(const float *W, int64_t C, int64_t d, int bits, int P,
                   int32_t *cand_ties, int32_t *code_ties, int32_t *stop_ties,
                   double *err_relmax, int n_threads)
 {
-    return verify_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, NULL, 0, 0, codes, scales, counts,
-                        err, NULL, chan, n_chan, status, cand_ties, code_ties, stop_ties, err_relmax,
-                        n_threads);
+    return verify_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, NULL, 0, 0, 0.0, codes, scales,
+                        counts, err, NULL, chan, n_chan, status, cand_ties, code_ties, stop_ties,
+                        err_relmax, n_threads);
 }
 
 /* The lockstep check of a fit with its options (as oracle_fit_ex). */
 int oracle_verify_ex(const float *W, int64_t C, int64_t d, int bits, int P, const float *grid,
                      int G, double tol, const float *X, int64_t N, int calib, double eps,
-                     int relative, int refit, int clipG, const int8_t *codes, const float *scales,
+                     int relative, int refit, int clipG, double eta, const int8_t *codes,
+                     const float *scales,
                      const int32_t *counts, const float *err, const float *xerr,
                      const int64_t *chan, int64_t n_chan, int32_t *status, int32_t *cand_ties,
                      int32_t *code_ties, int32_t *stop_ties, double *err_relmax, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
-    return verify_layer(W, C, d, bits, P, grid, G, tol, calib ? &cal : NULL, refit, X, N, clipG,
+    return verify_layer(W, C, d, bits, P, grid, G, tol, calib ? &cal : NULL, refit, X, N, clipG, eta,
                         codes, scales, counts, err, calib ? xerr : NULL, chan, n_chan, status,
                         cand_ties, code_ties, stop_ties, err_relmax, n_threads);
 }
@@ -690,8 +838,8 @@ int oracle_verify_calib(const float *W, int64_t C, int64_t d, int bits, int P,
                         double *err_relmax, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
-    return verify_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, NULL, 0, 0, codes, scales, counts,
-                        err, xerr, chan, n_chan, status, cand_ties, code_ties, stop_ties,
+    return verify_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, NULL, 0, 0, 0.0, codes, scales,
+                        counts, err, xerr, chan, n_chan, status, cand_ties, code_ties, stop_ties,
                         err_relmax, n_threads);
 }
 

@@ -635,6 +635,73 @@ def check_clip_verifier(orc):
     assert (v["status"] == 3).all()
 
 
+# ------------------------------------------- Eq. (11): the paper's own grid
+def check_min_gap(orc):
+    """Def. 1 (reading D1), worked by hand and by pairwise brute force."""
+    assert orc.min_gap([3.0, -1.0, 2.0, -3.0]) == 0.5
+    assert orc.min_gap([-2.0, 2.0]) == 0.0                      # only t and -t: no gap
+    assert orc.min_gap([0.5, 0.25, 0.125, -0.5]) == 0.0625
+    assert orc.min_gap([3.0, 1.0, -1.0]) == 1.0                 # equal magnitudes after a gap
+    rng = np.random.default_rng(51)
+    for _ in range(20):
+        t = rng.standard_normal(rng.integers(2, 40))
+        m = np.abs(t)
+        diffs = np.abs(m[:, None] - m[None, :])
+        ref = diffs[diffs > 0].min() / 2 if (diffs > 0).any() else 0.0
+        assert orc.min_gap(t) == ref
+
+
+def check_paper_grid_size(orc):
+    """Eq. (11): gamma = min(Delta / M, eta), count = floor(2 M ||r|| / gamma)."""
+    r = np.array([0.75, -0.25, 0.5, 0.125])
+    g, n = orc.paper_grid(r, 3, eta=2.0 ** -10)                 # M = 3, Delta = 0.0625
+    assert g == 2.0 ** -10 and n == int(np.floor(2 * 3 * np.linalg.norm(r) / g))
+    g, n = orc.paper_grid(r, 3, eta=0.1)
+    assert g == 0.0625 / 3 and n == int(np.floor(2 * 3 * np.linalg.norm(r) / g))
+    g, n = orc.paper_grid(np.array([1.0, -1.0]), 4, eta=0.01)  # no gap: eta
+    assert g == 0.01
+
+
+def check_paper_search_bruteforce(orc):
+    """The candidate-set argmin equals the enumeration of the whole grid,
+    every g from 1 to the count, errors in numpy fp64 (ties: smallest g)."""
+    rng = np.random.default_rng(52)
+    for bits in (2, 3, 4):
+        M = 2 ** (bits - 1) - 1
+        for case in range(10):
+            d = int(rng.integers(2, 9))
+            r = rng.integers(-96, 97, d) / 64.0                 # magnitudes 1/64 apart or equal
+            if not r.any():
+                continue
+            eta = 2.0 ** -10 if case % 2 else 2.0 ** -6
+            gamma, count = orc.paper_grid(r, bits, eta)
+            a = np.arange(1, count + 1) * gamma
+            q = np.clip(np.rint(r[None, :] / a[:, None]), -M, M)
+            E = ((r[None, :] - a[:, None] * q) ** 2).sum(1)
+            gref = int(np.argmin(E)) + 1
+            g, Eg = orc.paper_grid_search(r, bits, gamma, count)
+            assert E[g - 1] <= E[gref - 1] * (1 + 1e-12) and abs(Eg - E[gref - 1]) <= 1e-12 * E[gref - 1] + 1e-300
+            # dyadic r and a power-of-two gamma: every error is exact, so exact
+            # ties are ties on both sides and the smallest g must win
+            exact = gamma == 2.0 ** np.round(np.log2(gamma))
+            assert g == gref or (not exact and E[g - 1] == E[gref - 1]), (bits, case, g, gref)
+
+
+def check_paper_fit(orc):
+    """A fit on the paper's grid: the error never increases, each point's
+    scale is fl32 of a grid point, and the verifier accepts it and flags a
+    fit on the G-point grid."""
+    rng = np.random.default_rng(53)
+    W = (rng.standard_normal((12, 24)) * 0.3).astype(np.float32)
+    codes, scales, counts, err = orc.fit_paper(W, 3, 4, 0.0)
+    for k in range(12):
+        assert (np.diff(err[k, :counts[k]]) <= 0).all()
+    v = orc.verify_paper(W, 3, 4, 0.0, codes, scales, counts, err.astype(np.float32))
+    assert (v["status"] == 0).all()
+    c0, s0, n0, _ = orc.fit(W, 3, 4, 64, 0.0)
+    assert (orc.verify_paper(W, 3, 4, 0.0, c0, s0, n0)["status"] != 0).mean() > 0.5
+
+
 # ------------------------------------------- Sec. 3.4: deployment arithmetic
 def check_integer_scales(orc):
     """Eq. (14), reading I1: exact values, half-way ties to even (worked by
@@ -726,6 +793,7 @@ ALL_CHECKS = [
     check_calib_stop_definition, check_calib_runs_to_cap, check_calib_zero_batch, check_calib_scaling,
     check_calib_verifier, check_calib_verifier_fp32_evaluation, check_refit_one_point,
     check_refit_residual_chain, check_refit_verifier, check_clip_bruteforce, check_clip_hadamard_is_eq9,
-    check_clip_then_algorithm1, check_clip_zero_batch, check_clip_verifier, check_integer_scales,
+    check_clip_then_algorithm1, check_clip_zero_batch, check_clip_verifier, check_min_gap,
+    check_paper_grid_size, check_paper_search_bruteforce, check_paper_fit, check_integer_scales,
     check_integer_forward_exact, check_integer_forward_one_point, check_integer_forward_approximates,
 ]

@@ -74,6 +74,18 @@ MUTANTS = [
     ("clip_wrong_levels", "oracle_candidate_scales(D, d, M, cc, clipG, a);",
      "oracle_candidate_scales(D, d, M + 1, cc, clipG, a);"),
     ("clip_verifier_any", "if (cl.e[go] <= cl.e[cbest] * (1.0 + 1e-5) + sg) ct++;", "if (1) ct++;"),
+    ("gap_not_halved", "    return gap / 2.0;", "    return gap;"),
+    ("gap_counts_zero_diff", "if (diff > 0.0 && (gap == 0.0 || diff < gap)) gap = diff;",
+     "if (diff >= 0.0 && (gap == 0.0 || diff < gap)) gap = diff;"),
+    ("paper_step_max", "    if (g > eta) g = eta;", "    if (g < eta) g = eta;"),
+    ("paper_range_half", "*count = (int64_t)floor(2.0 * (double)M * sqrt(sum_sq(r, d)) / g);",
+     "*count = (int64_t)floor((double)M * sqrt(sum_sq(r, d)) / g);"),
+    ("paper_no_vertex", "                        cand[1] = gv;\n                        cand[2] = gv + 1;",
+     "                        cand[1] = 0;\n                        cand[2] = 0;"),
+    ("paper_two_point_bracket", "int64_t around[3] = {g0 - 1, g0, g0 + 1};",
+     "int64_t around[3] = {g0, g0 + 1, g0 + 1};"),
+    ("paper_ties_largest", "if (E < Eb || (E == Eb && h < best)) { Eb = E; best = h; }",
+     "if (E <= Eb) { Eb = E; best = h; }"),
     ("calib_stop_ignores_cap", "if (n >= P || Er == 0.0) return 1;", "if (Er == 0.0) return 1;"),
     ("calib_no_minimum_one_point", "if (n >= 1 && e <= thr) return 1;", "if (e <= thr) return 1;"),
 ]
