@@ -20,7 +20,7 @@ MUTANTS = [
     ("levels_off_by_one", "return (1 << (bits - 1)) - 1;", "return (1 << (bits - 1));"),
     ("argmax_not_argmin", "(best < 0 || E[g] < E[best])", "(best < 0 || E[g] > E[best])"),
     ("ties_to_largest_scale", "(best < 0 || E[g] < E[best])", "(best < 0 || E[g] <= E[best])"),
-    ("zero_scale_not_skipped", "if (g < 0) break;                                   /* S3: no scale */",
+    ("zero_scale_not_skipped", "if (g < 0) break;                               /* S3: no scale */",
      "if (g < 0) g = 0;"),
     ("residual_sign", "r[j] = r[j] - as * (double)q[j]; /* Eq. (7) */",
      "r[j] = r[j] + as * (double)q[j]; /* Eq. (7) */"),
