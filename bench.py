@@ -82,6 +82,9 @@ def parse():
     ap.add_argument("--clip", type=int, default=0, metavar="GC",
                     help="point 1 from the clipping of Eq. (13) with GC factors (the paper: 20; "
                          "mpq_fit_layers_ex; implies --separate for the isotropic rule)")
+    ap.add_argument("--paper-eta", type=float, default=0.0, metavar="ETA",
+                    help="fit on the paper's own grid of Eq. (11) with maximal step ETA (the paper: "
+                         "2^-10 = 0.0009765625; mpq_fit_layers_ex; implies --separate)")
     ap.add_argument("--separate", action="store_true",
                     help="the three batched calls in turn instead of mpq_quantize_layers")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -300,7 +303,8 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    separate = args.separate or args.dense or ((args.refit or args.clip) and args.rule != "calib")
+    separate = (args.separate or args.dense or args.paper_eta > 0
+                or ((args.refit or args.clip) and args.rule != "calib"))
     calib = args.rule == "calib"
     if calib and separate:
         raise SystemExit("--rule calib has its own call sequence (no --separate / --dense)")
@@ -322,6 +326,8 @@ def main():
             for i, W in enumerate(Ws):
                 mpq.fit_layer(W, wk.bits, wk.max_points, wk.n_grid, wk.tol, dense=True,
                               out=(ls.codes[i], ls.scales[i], ls.counts[i], ls.fit_err[i]))
+        elif args.paper_eta > 0:
+            ls.fit_ex(wk.bits, 1, wk.tol, paper_eta=args.paper_eta)
         elif args.refit or args.clip:
             ls.fit_ex(wk.bits, wk.n_grid, wk.tol, refit=args.refit, clip_grid=args.clip)
         else:
@@ -375,6 +381,8 @@ def main():
         points += n
         fk = "fit_dense_kernel" if args.dense else fit_kernel.setdefault(
             d, mpq.fit_kernel_of(d, wk.bits, wk.n_grid, True))
+        if args.paper_eta > 0:
+            fk = "fit_paper_kernel"   # no algorithmic count: its candidates depend on the data
         if calib:
             # step s scores the channels that took point s + 1 (sum of counts
             # rows in all), plus W itself once for the relative threshold;
@@ -459,7 +467,7 @@ def main():
                    "weights": wk.weights, "bits": wk.bits, "max_points": wk.max_points,
                    "n_grid": wk.n_grid, "tol": wk.tol, "calib_columns": wk.n_calib,
                    "points_per_step": points, "search": "dense" if args.dense else "histogram",
-                   "refit": bool(args.refit), "clip_grid": args.clip,
+                   "refit": bool(args.refit), "clip_grid": args.clip, "paper_eta": args.paper_eta,
                    "rule": ("Algorithm 2 on the calibration batch, relative" if calib
                             else "||r||^2 <= tol ||w||^2"),
                    "point_counts": count_hist.tolist(),

@@ -271,6 +271,16 @@ int mpq_fit_layers_calib(const mpq_layer *layers, int n_layers, int bits, int ma
  *             points after it follow Algorithm 1 with the stopping rule.
  *             Reads X and n of every layer; c_out * Gc <= MPQ_MAX_ERR_DIM.
  *             Cannot be combined with refit.
+ *   paper_eta 0, or eta > 0: the candidate scales of each step are the
+ *             paper's own grid (Eq. (11), Def. 1): a = g * gamma,
+ *             g = 1 .. floor(2 M ||r|| / gamma), gamma = min(Delta_r / M, eta),
+ *             Delta_r half the smallest positive difference of the |r_j|
+ *             (none: gamma = eta); the paper uses eta = 2^-10.  The grid is
+ *             searched exactly without enumerating it; the chosen scale is
+ *             stored as fl32(g * gamma), and the point's codes and residual
+ *             use that value.  grid_host and n_grid are ignored.  Only with
+ *             the isotropic stopping rule (not with refit, calib or
+ *             clip_grid); d <= 8192 (else MPQ_ERR_SHAPE).
  * refit, calib and clip_grid need the histogram search for every layer
  * (d <= 32768; else MPQ_ERR_SHAPE).  Errors as for mpq_fit_layers /
  * mpq_fit_layers_calib.
@@ -281,6 +291,7 @@ typedef struct mpq_fit_options {
     float eps;
     int relative;
     int clip_grid;
+    float paper_eta;
 } mpq_fit_options;
 int mpq_fit_layers_ex(const mpq_layer *layers, int n_layers, int bits, int max_points,
                       const float *grid_host, int n_grid, float tol, const mpq_fit_options *opt,

@@ -950,6 +950,89 @@ int int_forward_impl(const mpq_int_layer *layers, int n_layers, int max_points, 
     return MPQ_OK;
 }
 
+// The fit on the paper's own grid (Eq. (11), readings D1 and G3), with the
+// isotropic stopping rule: one launch per kernel variant (up to
+// kMaxBatchLayers layers), side by side.
+int paper_impl(const mpq_layer *layers, int n_layers, int bits, int max_points, float tol, float eta,
+               void *stream)
+{
+    if (n_layers < 0 || (n_layers > 0 && !layers))
+        return fail(MPQ_ERR_INVALID_ARG, "layers must hold n_layers >= 0 entries");
+    int rc = check_fit_args(bits, max_points, nullptr, 1, tol);
+    if (rc != MPQ_OK) return rc;
+    if (!(eta > 0.0f) || !isfinite(eta)) return fail(MPQ_ERR_INVALID_ARG, "paper_eta must be finite and > 0");
+    bool any = false;
+    int64_t dmax = 0;
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_layer &L = layers[l];
+        rc = check_fit_layer(L.W, L.c_out, L.d, L.codes, L.scales, L.counts);
+        if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
+        if (L.c_out > 0) {
+            any = true;
+            dmax = std::max(dmax, L.d);
+        }
+    }
+    if (!any) return MPQ_OK;
+    if (dmax > mpq::kPaperMaxDim)
+        return fail(MPQ_ERR_SHAPE, "the paper's grid takes d <= %lld (got %lld)",
+                    (long long)mpq::kPaperMaxDim, (long long)dmax);
+    size_t lim = 0;
+    rc = device_lds_limit(&lim);
+    if (rc != MPQ_OK) return rc;
+    if (mpq::paper_lds(dmax) > lim)
+        return fail(MPQ_ERR_SHAPE, "d = %lld needs %zu bytes of LDS (limit %zu)", (long long)dmax,
+                    mpq::paper_lds(dmax), lim);
+    struct Job {
+        mpq::PaperBatch b;
+        int variant;
+        int64_t channels, dmax;
+        double work;
+    };
+    std::vector<Job> jobs;
+    const int M = (1 << (bits - 1)) - 1;
+    for (int v = 0; v <= mpq::paper_variant(mpq::kPaperMaxDim); ++v) {
+        Job j = {};
+        auto fresh = [&]() {
+            j = Job{};
+            j.b.M = M;
+            j.b.P = max_points;
+            j.b.tol = (double)tol;
+            j.b.eta = (double)eta;
+            j.variant = v;
+        };
+        fresh();
+        for (int l = 0; l <= n_layers; ++l) {
+            const bool flush = l == n_layers || j.b.n_layers == mpq::kMaxBatchLayers ||
+                               j.channels + (l < n_layers ? layers[l].c_out : 0) > 0x7fffffffLL;
+            if (flush && j.b.n_layers > 0) {
+                jobs.push_back(j);
+                fresh();
+            }
+            if (l == n_layers) break;
+            const mpq_layer &L = layers[l];
+            if (L.c_out == 0 || mpq::paper_variant(L.d) != v) continue;
+            mpq::HistLayer &H = j.b.L[j.b.n_layers++];
+            H.W = L.W;
+            H.codes = L.codes;
+            H.scales = L.scales;
+            H.counts = L.counts;
+            H.err = L.fit_err;
+            H.d = (int)L.d;
+            H.c_begin = (int)j.channels;
+            j.channels += L.c_out;
+            j.dmax = std::max(j.dmax, L.d);
+            j.work += (double)L.c_out * (double)L.d * (double)L.d;
+        }
+    }
+    std::vector<double> work;
+    for (const Job &j : jobs) work.push_back(j.work);
+    const hipError_t e = run_concurrently((hipStream_t)stream, work, [&](int i, hipStream_t st) {
+        return mpq::launch_fit_paper(jobs[i].b, jobs[i].variant, jobs[i].channels, jobs[i].dmax, st);
+    });
+    if (e != hipSuccess) return hip_fail(e, "paper-grid fit kernel launch");
+    return MPQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1071,6 +1154,11 @@ int mpq_fit_layers_ex(const mpq_layer *layers, int n_layers, int bits, int max_p
                       const float *grid_host, int n_grid, float tol, const mpq_fit_options *opt,
                       void *stream)
 {
+    if (opt && opt->paper_eta != 0.0f) {
+        if (opt->calib || opt->refit || opt->clip_grid)
+            return fail(MPQ_ERR_INVALID_ARG, "paper_eta cannot be combined with calib, refit or clip_grid");
+        return paper_impl(layers, n_layers, bits, max_points, tol, opt->paper_eta, stream);
+    }
     if (!opt) return fit_layers_impl(Search::kAuto, layers, n_layers, bits, max_points, grid_host,
                                      n_grid, tol, stream);
     if (opt->clip_grid && opt->refit)

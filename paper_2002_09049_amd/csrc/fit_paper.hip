@@ -1,0 +1,317 @@
+// Greedy multipoint fit on the paper's own grid (Eq. (11), Def. 1): at each
+// step the candidate scales are a_g = g * gamma, g = 1 .. floor(2 M ||r|| /
+// gamma), gamma = min(Delta_r / M, eta), Delta_r half the smallest positive
+// difference of the |r_j| (no gap: gamma = eta).  The chosen scale is stored
+// as fl32(a_g); the codes (Eq. (10)) and the residual (Eq. (7)) use that
+// stored value.  Stopping rule as for the other fits (||r||^2 <= tol ||w||^2,
+// cap, zero residual, no nonzero scale).
+//
+// The grid can hold far more points than can be enumerated (10^8 and more).
+// The codes are constant between consecutive breakpoints b = |r_j| / (k+1/2),
+// where E(a) = ||r||^2 - 2 a A + a^2 B is a convex quadratic, so the argmin
+// over the grid is one of the three grid points around some breakpoint, or
+// one of the two next to the vertex A / B of a piece that holds such a point.
+// With the magnitudes sorted (descending) and their prefix sums S,
+//   c_k(a) = #{ j : |r_j| > a (k + 1/2) }   (binary search; a magnitude
+//            exactly on the boundary counts when k is odd, ties to even),
+//   A(a) = sum_k S[c_k],  B(a) = sum_k (2k + 1) c_k,
+// so each candidate costs O(M log d).  The d M breakpoints are spread over
+// the threads; the smallest error wins, ties to the smallest g.  A piece
+// whose quadratic minimum R - A^2 / B exceeds the best error a thread has
+// found cannot hold the argmin, so its vertex candidates are skipped.
+//
+// One workgroup of 256 threads per channel; the fp64 residual stays in
+// registers (EPT elements per thread); the sorted magnitudes and their
+// prefix sums occupy 2 dpad doubles of LDS (dpad = d rounded up to a power
+// of two, at most kPaperMaxDim).
+#include <math.h>
+#include <stdio.h>
+
+#include "internal.hpp"
+#include "mpq.h"
+#include "reduce.hpp"
+
+namespace mpq {
+
+namespace {
+
+constexpr int kPT = 256;   // threads per workgroup
+
+struct Best {
+    double e;
+    long long g;
+};
+
+__device__ __forceinline__ Best better(Best x, Best y)
+{
+    return (y.e < x.e || (y.e == x.e && y.g < x.g)) ? y : x;
+}
+
+__device__ __forceinline__ Best block_best(Best v, double *se, long long *sg)
+{
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        Best o{__shfl_xor(v.e, off), __shfl_xor(v.g, off)};
+        v = better(v, o);
+    }
+    const int wid = threadIdx.x / kWave;
+    if ((threadIdx.x % kWave) == 0) {
+        se[wid] = v.e;
+        sg[wid] = v.g;
+    }
+    __syncthreads();
+    Best r{se[0], sg[0]};
+#pragma unroll
+    for (int i = 1; i < kPT / kWave; ++i) r = better(r, Best{se[i], sg[i]});
+    __syncthreads();
+    return r;
+}
+
+// number of sorted (descending) magnitudes s[0 .. d) greater than x, or with
+// or_equal, greater than or equal to x
+__device__ __forceinline__ int count_above(const double *s, int d, double x, bool or_equal)
+{
+    int lo = 0, hi = d;
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (s[mid] > x || (or_equal && s[mid] == x)) lo = mid + 1;
+        else hi = mid;
+    }
+    return lo;
+}
+
+// E(a) from the sorted magnitudes s and their prefix sums S; also A, B.  A
+// magnitude exactly at a (k + 1/2) has the code of the even neighbour (Eq.
+// (2)'s ties to even): past level k when k + 1 is even.
+__device__ __forceinline__ double paper_error(const double *s, const double *S, int d, int M, double R,
+                                              double a, double &A, double &B)
+{
+    double sa = 0.0, sb = 0.0;
+    for (int k = 0; k < M; ++k) {
+        const int c = count_above(s, d, a * ((double)k + 0.5), (k & 1) != 0);
+        sa += S[c];
+        sb += (double)(2 * k + 1) * (double)c;
+    }
+    A = sa;
+    B = sb;
+    return (R - 2.0 * a * sa) + a * a * sb;
+}
+
+template <int EPT>
+__global__ void __launch_bounds__(kPT) fit_paper_kernel(const PaperBatch B)
+{
+    extern __shared__ __align__(16) double psmem[];
+    __shared__ float s_redf[kPT / kWave];
+    __shared__ double s_redd[kPT / kWave];
+    __shared__ long long s_redg[kPT / kWave];
+
+    int li = 0;
+    while (li + 1 < B.n_layers && (int)blockIdx.x >= B.L[li + 1].c_begin) ++li;
+    const HistLayer &Ly = B.L[li];
+    const int64_t k = (int64_t)blockIdx.x - Ly.c_begin;
+    const int t = threadIdx.x, d = Ly.d, P = B.P, M = B.M;
+    const double Md = (double)M;
+    int dpad = 1;
+    while (dpad < d) dpad <<= 1;
+    double *s = psmem;          // [dpad] magnitudes, sorted descending (pads -1)
+    double *S = psmem + dpad;   // [d + 1] prefix sums of s
+    int8_t *qk = Ly.codes + k * (int64_t)P * d;
+    const float *wk = Ly.W + k * (int64_t)d;
+
+    double r[EPT];
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+        const int j = t + kPT * u;
+        r[u] = j < d ? (double)wk[j] : 0.0;
+    }
+    double Ew = 0.0;
+    float apend = 0.0f;
+    int n = 0;
+    for (int i = 0;; ++i) {
+        // ---- apply the pending point (codes of Eq. (10) at the stored scale)
+        float lmax = 0.0f;
+        double lsum = 0.0;
+        if (i >= 1) {
+            const double ap = (double)apend, ia = 1.0 / ap;
+            int8_t *qrow = qk + (int64_t)(i - 1) * d;
+#pragma unroll
+            for (int u = 0; u < EPT; ++u) {
+                const int j = t + kPT * u;
+                if (j < d) {
+                    const double y = r[u] * ia;
+                    double c = rint(y);
+                    if (fabs(fabs(y - c) - 0.5) < 0x1p-40) c = rint(r[u] / ap);
+                    c = fmin(fmax(c, -Md), Md);
+                    qrow[j] = (int8_t)(int)c;
+                    r[u] = fma(-ap, c, r[u]);
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < EPT; ++u) {
+            lmax = fmaxf(lmax, fabsf((float)r[u]));
+            lsum = fma(r[u], r[u], lsum);
+        }
+        block_max_sum<kPT>(lmax, lsum, s_redf, s_redd);
+        const double Er = lsum;
+        if (i == 0) Ew = Er;
+        else if (Ly.err && t == 0) Ly.err[k * P + (i - 1)] = (float)Er;
+        if (i >= P || Er == 0.0 || (i >= 1 && Er <= B.tol * Ew)) {
+            n = i;
+            break;
+        }
+
+        // ---- sorted magnitudes (bitonic, descending; pads -1 sort last)
+        for (int j = t; j < dpad; j += kPT) s[j] = -1.0;
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < EPT; ++u) {
+            const int j = t + kPT * u;
+            if (j < d) s[j] = fabs(r[u]);
+        }
+        __syncthreads();
+        for (int kk = 2; kk <= dpad; kk <<= 1) {
+            for (int jj = kk >> 1; jj > 0; jj >>= 1) {
+                for (int x = t; x < dpad; x += kPT) {
+                    const int y = x ^ jj;
+                    if (y > x) {
+                        const double a = s[x], b = s[y];
+                        const bool desc = (x & kk) == 0;
+                        if (desc ? (a < b) : (a > b)) {
+                            s[x] = b;
+                            s[y] = a;
+                        }
+                    }
+                }
+                __syncthreads();
+            }
+        }
+        // ---- minimal gap (Def. 1), gamma and the grid size (Eq. (11))
+        double lgap = INFINITY;
+        for (int j = t; j + 1 < d; j += kPT) {
+            const double diff = s[j] - s[j + 1];
+            if (diff > 0.0) lgap = fmin(lgap, diff);
+        }
+        lgap = block_reduce<kPT>(lgap, MinOp(), s_redd);
+        double gamma = lgap == INFINITY ? B.eta : fmin(lgap / 2.0 / Md, B.eta);
+        // (grid indices stay far below 2^63: clamped at 4e18)
+        const long long count = (long long)fmin(floor(2.0 * Md * sqrt(Er) / gamma), 4e18);
+        // ---- prefix sums S[0..d] of the sorted magnitudes (fixed order)
+        {
+            const int per = (d + kPT - 1) / kPT, j0 = min(t * per, d), j1 = min(j0 + per, d);
+            double loc = 0.0;
+            for (int j = j0; j < j1; ++j) loc += s[j];
+            // exclusive scan of the per-thread sums over the workgroup
+            double v = loc;
+#pragma unroll
+            for (int off = 1; off < kWave; off <<= 1) {
+                const double o = __shfl_up(v, off);
+                if ((t % kWave) >= off) v += o;
+            }
+            if ((t % kWave) == kWave - 1) s_redd[t / kWave] = v;
+            __syncthreads();
+            double base = 0.0;
+            for (int w = 0; w < t / kWave; ++w) base += s_redd[w];
+            double run = base + v - loc;
+            for (int j = j0; j < j1; ++j) {
+                S[j] = run;
+                run += s[j];
+            }
+            if (t == kPT - 1) S[d] = run;
+            __syncthreads();
+        }
+        // ---- candidates around every breakpoint and at the pieces' vertices
+        Best best{INFINITY, 0x7fffffffffffffffLL};
+        auto try_g = [&](long long g) {
+            if (g < 1 || g > count) return;
+            double A, Bq;
+            const double E = paper_error(s, S, d, M, Er, (double)g * gamma, A, Bq);
+            best = better(best, Best{E, g});
+        };
+        for (int e = t; e < d * M; e += kPT) {
+            const int j = e / M, kl = e - j * M;
+            const double b = s[j] / ((double)kl + 0.5);
+            if (!(b > 0.0)) continue;
+            const long long g0 = (long long)fmin(floor(b / gamma), 4e18);
+            for (long long g = g0 - 1; g <= g0 + 1; ++g) {
+                if (g < 1 || g > count) continue;
+                double A, Bq;
+                const double E = paper_error(s, S, d, M, Er, (double)g * gamma, A, Bq);
+                best = better(best, Best{E, g});
+                // the piece's quadratic has its minimum R - A^2 / B at the
+                // vertex, a lower bound for every grid point of the piece:
+                // skip the vertex candidates when it already exceeds the best
+                // error found (with a margin for rounding)
+                if (Bq > 0.0 && Er - A * A / Bq <= best.e + 1e-12 * Er) {
+                    const long long gv = (long long)fmin(floor((A / Bq) / gamma), 4e18);
+                    try_g(gv);
+                    try_g(gv + 1);
+                }
+            }
+        }
+        best = block_best(best, s_redd, s_redg);
+        const float af = best.e == INFINITY ? 0.0f : (float)((double)best.g * gamma);
+        if (af == 0.0f) {   // no candidate with a nonzero scale
+            n = i;
+            break;
+        }
+        apend = af;
+        if (t == 0) Ly.scales[k * P + i] = af;
+        __syncthreads();   // s and S are rewritten by the next step
+    }
+
+    if (t == 0) Ly.counts[k] = n;
+    for (int q = n + t; q < P; q += kPT) {
+        Ly.scales[k * P + q] = 0.0f;
+        if (Ly.err) Ly.err[k * P + q] = 0.0f;
+    }
+    for (int q = n; q < P; ++q)
+        for (int j = t; j < d; j += kPT) qk[(int64_t)q * d + j] = 0;
+}
+
+template <int EPT>
+hipError_t launch_paper_t(const PaperBatch &b, int64_t channels, size_t lds, hipStream_t s)
+{
+    auto kern = fit_paper_kernel<EPT>;
+    if (lds > 65536) {
+        hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)lds);
+        if (e != hipSuccess) return e;
+    }
+    char name[48];
+    snprintf(name, sizeof name, "fit_paper_kernel<%d>", EPT);
+    LaunchTimer timer(s, name);
+    hipLaunchKernelGGL(kern, dim3((unsigned)channels), dim3(kPT), lds, s, b);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+int paper_variant(int64_t d)
+{
+    return d <= 2 * kPT ? 0 : d <= 4 * kPT ? 1 : d <= 8 * kPT ? 2 : d <= 16 * kPT ? 3 : 4;
+}
+
+size_t paper_lds(int64_t dmax)
+{
+    int64_t dpad = 1;
+    while (dpad < dmax) dpad <<= 1;
+    return (size_t)(2 * dpad + 1) * sizeof(double);
+}
+
+hipError_t launch_fit_paper(const PaperBatch &b, int variant, int64_t channels, int64_t dmax, hipStream_t s)
+{
+    if (channels <= 0) return hipSuccess;
+    if (channels > 0x7fffffffLL || dmax > kPaperMaxDim) return hipErrorInvalidValue;
+    const size_t lds = paper_lds(dmax);
+    switch (variant) {
+    case 0: return launch_paper_t<2>(b, channels, lds, s);
+    case 1: return launch_paper_t<4>(b, channels, lds, s);
+    case 2: return launch_paper_t<8>(b, channels, lds, s);
+    case 3: return launch_paper_t<16>(b, channels, lds, s);
+    case 4: return launch_paper_t<32>(b, channels, lds, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace mpq

@@ -107,6 +107,23 @@ int hist_variant(int64_t d);   // layers with equal variants may share a launch
 // when default_grid, else a caller's grid), as LaunchTimer records it.
 std::string hist_kernel_name(int64_t d, int M, int G, bool default_grid);
 hipError_t launch_fit_hist(const HistBatch &b, int variant, int64_t channels, hipStream_t s);
+// The paper's own grid (Eq. (11), Def. 1): one workgroup of 256 threads per
+// channel, channels of up to kPaperMaxDim weights, the layer descriptors of
+// the histogram search (HistLayer; the calibration fields unused).
+constexpr int64_t kPaperMaxDim = 8192;
+struct PaperBatch {
+    int n_layers;
+    int M, P;
+    double tol;
+    double eta;          // the maximal step of Eq. (11)
+    HistLayer L[kMaxBatchLayers];
+};
+static_assert(sizeof(PaperBatch) <= 4096, "kernel arguments");
+int paper_variant(int64_t d);        // layers with equal variants may share a launch
+size_t paper_lds(int64_t dmax);      // dynamic LDS for channels of up to dmax weights
+hipError_t launch_fit_paper(const PaperBatch &b, int variant, int64_t channels, int64_t dmax,
+                            hipStream_t s);
+
 // Zeroes n int32 (a fill kernel: safe under stream capture).
 hipError_t launch_zero_i32(int32_t *p, int64_t n, hipStream_t s);
 

@@ -83,6 +83,10 @@ struct MaxOp {
     template <typename T>
     __device__ __forceinline__ T operator()(T a, T b) const { return a > b ? a : b; }
 };
+struct MinOp {
+    template <typename T>
+    __device__ __forceinline__ T operator()(T a, T b) const { return a < b ? a : b; }
+};
 struct SumOp {
     template <typename T>
     __device__ __forceinline__ T operator()(T a, T b) const { return a + b; }

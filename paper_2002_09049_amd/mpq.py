@@ -50,7 +50,8 @@ class Layer(ctypes.Structure):
 class FitOptions(ctypes.Structure):
     """struct mpq_fit_options (include/mpq.h)."""
     _fields_ = [("refit", ctypes.c_int), ("calib", ctypes.c_int), ("eps", ctypes.c_float),
-                ("relative", ctypes.c_int), ("clip_grid", ctypes.c_int)]
+                ("relative", ctypes.c_int), ("clip_grid", ctypes.c_int),
+                ("paper_eta", ctypes.c_float)]
 
 
 class IntLayer(ctypes.Structure):
@@ -402,15 +403,16 @@ class LayerSet:
 
     def fit_ex(self, bits: int, n_grid: int, tol: float = 0.0, refit: bool = False,
                calib: bool = False, eps: float = 0.0, relative: bool = True, clip_grid: int = 0,
-               grid=None, stream=None):
+               paper_eta: float = 0.0, grid=None, stream=None):
         """mpq_fit_layers_ex: the fit with options (refit: reading A2; calib:
         Algorithm 2's stopping rule on the calibration batches; clip_grid:
-        point 1 from the clipping of Eq. (13) with that many factors)."""
+        point 1 from the clipping of Eq. (13) with that many factors;
+        paper_eta: the paper's own grid of Eq. (11) with that maximal step)."""
         if (calib or clip_grid) and self.X is None:
             raise ValueError("LayerSet was built without calibration batches")
         g = self._grid(grid, n_grid)
         opt = FitOptions(1 if refit else 0, 1 if calib else 0, float(eps), 1 if relative else 0,
-                         int(clip_grid))
+                         int(clip_grid), float(paper_eta))
         _check(load().mpq_fit_layers_ex(ctypes.addressof(self.arr), self.n, bits, self.max_points,
                                         None if g is None else g.ctypes.data_as(ctypes.c_void_p),
                                         n_grid, float(tol), ctypes.addressof(opt), _stream(stream)))

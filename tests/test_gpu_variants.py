@@ -193,3 +193,64 @@ def test_clip_workload_resnet18_sampled(orc):
         say(f"  layer {li} ({C}x{d})")
         _ok(orc.verify_clip(Ws[li].cpu().numpy(), w.bits, w.max_points, w.n_grid, Xs[li].cpu().numpy(),
                             *out, tol=float(np.float32(w.tol)), channels=ch))
+
+
+def _fit_paper(W, bits, P, tol, eta):
+    import torch
+    from paper_2002_09049_amd import mpq
+    ls = mpq.LayerSet([to_dev(W)], P)
+    ls.fit_ex(bits, 1, tol, paper_eta=eta)
+    torch.cuda.synchronize()
+    return (ls.codes[0].cpu().numpy(), ls.scales[0].cpu().numpy(), ls.counts[0].cpu().numpy(),
+            ls.fit_err[0].cpu().numpy())
+
+
+PAPER = [
+    # (C, d, bits, P, tol, eta): every kernel variant; Gaussian weights make
+    # Delta_r tiny, so the grids hold 10^8 points and more
+    (3, 1, 4, 4, 1e-3, 2.0 ** -10),
+    (20, 9, 4, 6, 0.0, 2.0 ** -10),
+    (30, 147, 4, 4, 1e-3, 2.0 ** -10),
+    (10, 576, 3, 4, 1e-4, 2.0 ** -10),
+    (6, 1000, 2, 5, 0.0, 2.0 ** -6),
+    (3, 2304, 4, 3, 0.0, 2.0 ** -10),
+    (2, 4608, 4, 2, 1e-3, 2.0 ** -10),
+    (2, 8192, 2, 2, 0.0, 2.0 ** -10),
+]
+
+
+@pytest.mark.parametrize("C,d,bits,P,tol,eta", PAPER, ids=[f"C{c}_d{d}_b{b}_P{p}" for c, d, b, p, _, _ in PAPER])
+def test_paper_grid_parity(orc, C, d, bits, P, tol, eta):
+    say(f"case paper grid C={C} d={d} bits={bits} P={P} tol={tol} eta={eta}")
+    W = wl.random_weights(C, d, seed=11 * C + d)
+    codes, scales, counts, err = _fit_paper(W, bits, P, tol, eta)
+    _ok(orc.verify_paper(W, bits, P, float(np.float32(tol)), codes, scales, counts, err, eta=eta))
+
+
+def test_paper_grid_exact_on_dyadic_weights(orc):
+    """Weights on a 1/64 lattice and eta = 2^-10: the first step's gamma is
+    2^-10 and every error of it is exact (ties included), so the GPU's first
+    point equals the oracle's bit for bit; later steps (gamma = Delta / M,
+    no longer dyadic) are checked in lockstep."""
+    rng = np.random.default_rng(61)
+    W = (rng.integers(-96, 97, (40, 24)) / 64.0).astype(np.float32)
+    W[5] = 0.0
+    for bits in (2, 3, 4):
+        say(f"case paper grid dyadic bits={bits}")
+        codes, scales, counts, err = _fit_paper(W, bits, 1, 0.0, 2.0 ** -10)
+        oc, os_, on, _ = orc.fit_paper(W, bits, 1, 0.0)
+        assert np.array_equal(counts, on) and np.array_equal(scales, os_) and np.array_equal(codes, oc)
+        out = _fit_paper(W, bits, 4, 0.0, 2.0 ** -10)
+        _ok(orc.verify_paper(W, bits, 4, 0.0, *out))
+
+
+def test_paper_grid_limits():
+    from paper_2002_09049_amd import mpq
+    W = wl.random_weights(2, 9000, seed=1)
+    with pytest.raises(mpq.MPQError) as e:
+        _fit_paper(W, 4, 2, 0.0, 2.0 ** -10)
+    assert e.value.status == mpq.MPQ_ERR_SHAPE
+    ls = mpq.LayerSet([to_dev(wl.random_weights(2, 64, seed=2))], 2)
+    with pytest.raises(mpq.MPQError) as e:
+        ls.fit_ex(4, 1, 0.0, refit=True, paper_eta=2.0 ** -10)
+    assert e.value.status == mpq.MPQ_ERR_INVALID_ARG
