@@ -64,10 +64,14 @@ def _declare(lib):
     lib.oracle_default_grid.argtypes = [i32, P]
     lib.oracle_default_grid.restype = None
     lib.oracle_fit_ex.argtypes = [P, i64, i64, i32, i32, P, i32, f64, P, i64, i32, f64, i32, i32,
-                                  i32, f64, P, P, P, P, P, i32]
+                                  i32, f64, P, P, P, P, P, P, i32]
     lib.oracle_fit_ex.restype = i32
     lib.oracle_verify_ex.argtypes = [P, i64, i64, i32, i32, P, i32, f64, P, i64, i32, f64, i32, i32,
-                                     i32, f64, P, P, P, P, P, P, i64, P, P, P, P, P, i32]
+                                     i32, f64, P, P, P, P, P, P, P, i64, P, P, P, P, P, i32]
+    lib.oracle_output_error_ex.argtypes = [P, P, P, P, P, i64, i64, i32, P, i64, P, i64, P, P, i32]
+    lib.oracle_output_error_ex.restype = i32
+    lib.oracle_reconstruct_ex.argtypes = [P, P, P, P, i64, i64, i32, P]
+    lib.oracle_reconstruct_ex.restype = None
     lib.oracle_min_gap.argtypes = [P, i64, P]
     lib.oracle_min_gap.restype = f64
     lib.oracle_paper_grid.argtypes = [P, i64, i32, f64, P, P, P]
@@ -181,8 +185,16 @@ class Oracle:
                                               int(count), ctypes.byref(E))
         return int(g), E.value
 
+    def fit_asym(self, W, bits: int, max_points: int, n_grid: int, tol: float = 0.0, X=None,
+                 calib: bool = False, eps: float = 0.0, relative: bool = True, refit: bool = False,
+                 grid=None, n_threads: int = 0):
+        """Fit with the per-channel offset of reading B2 (the asymmetric set of
+        Eq. (1)).  Returns (codes, scales, counts, err, xerr, offsets[C] f32)."""
+        return self._fit(W, bits, max_points, n_grid, tol, X, eps, relative, refit, grid, n_threads,
+                         calib=calib, asym=True)
+
     def _fit(self, W, bits, P, n_grid, tol, X, eps, relative, refit, grid, n_threads, calib=None,
-             clip_grid=0, eta=0.0):
+             clip_grid=0, eta=0.0, asym=False):
         calib = (X is not None) if calib is None else calib
         W = np.ascontiguousarray(W, dtype=np.float32)
         C, d = W.shape
@@ -194,15 +206,16 @@ class Oracle:
         counts = np.zeros(C, np.int32)
         err = np.zeros((C, P), np.float64)
         xerr = np.zeros((C, P), np.float64)
+        offsets = np.zeros(C, np.float32) if asym else None
         g = _grid(grid, n_grid)
         rc = self.lib.oracle_fit_ex(_p(W), C, d, bits, P, _p(g), n_grid, float(tol), _p(X),
                                     0 if X is None else X.shape[1], 1 if calib else 0, float(eps),
                                     1 if relative else 0, 1 if refit else 0, int(clip_grid),
-                                    float(eta), _p(codes_), _p(scales), _p(counts), _p(err), _p(xerr),
-                                    n_threads)
+                                    float(eta), _p(offsets), _p(codes_), _p(scales), _p(counts),
+                                    _p(err), _p(xerr), n_threads)
         if rc != 0:
             raise MemoryError("oracle_fit_ex failed")
-        return codes_, scales, counts, err, xerr
+        return (codes_, scales, counts, err, xerr) + ((offsets,) if asym else ())
 
     def verify(self, W, bits, max_points, n_grid, tol, codes_, scales, counts, err=None,
                grid=None, channels=None, n_threads: int = 0, refit: bool = False):
@@ -230,9 +243,21 @@ class Oracle:
         return self._verify(W, bits, max_points, 1, tol, None, 0.0, False, False, codes_, scales,
                             counts, err, None, None, channels, n_threads, eta=eta)
 
+    def verify_asym(self, W, bits, max_points, n_grid, codes_, scales, counts, offsets, err=None,
+                    xerr=None, tol: float = 0.0, X=None, calib: bool = False, eps: float = 0.0,
+                    relative: bool = True, refit: bool = False, grid=None, channels=None,
+                    n_threads: int = 0):
+        """Lockstep check of a fit with the per-channel offset of reading B2
+        (status 9: an offset that is not the fp32 midpoint)."""
+        return self._verify(W, bits, max_points, n_grid, tol, X, eps, relative, refit, codes_,
+                            scales, counts, err, xerr, grid, channels, n_threads, calib=calib,
+                            offsets=offsets)
+
     def _verify(self, W, bits, P, n_grid, tol, X, eps, relative, refit, codes_, scales, counts,
-                err, xerr, grid, channels, n_threads, calib=None, clip_grid=0, eta=0.0):
+                err, xerr, grid, channels, n_threads, calib=None, clip_grid=0, eta=0.0, offsets=None):
         calib = (X is not None) if calib is None else calib
+        if offsets is not None:
+            offsets = np.ascontiguousarray(offsets, dtype=np.float32)
         W = np.ascontiguousarray(W, dtype=np.float32)
         C, d = W.shape
         if X is not None:
@@ -253,7 +278,7 @@ class Oracle:
         rc = self.lib.oracle_verify_ex(
             _p(W), C, d, bits, P, _p(g), n_grid, float(tol), _p(X), 0 if X is None else X.shape[1],
             1 if calib else 0, float(eps), 1 if relative else 0, 1 if refit else 0, int(clip_grid),
-            float(eta), _p(codes_), _p(scales),
+            float(eta), _p(offsets), _p(codes_), _p(scales),
             _p(counts), _p(e), _p(xe), _p(chan), n, _p(out["status"]), _p(out["cand_ties"]),
             _p(out["code_ties"]), _p(out["stop_ties"]), _p(out["err_relmax"]), n_threads)
         if rc != 0:
@@ -277,8 +302,9 @@ class Oracle:
         return self._verify(W, bits, max_points, n_grid, 0.0, X, eps, relative, refit, codes_,
                             scales, counts, err, xerr, grid, channels, n_threads)
 
-    def output_error(self, W, codes_, scales, counts, X, channels=None, with_ref=True, n_threads: int = 0):
-        """Eq. (12) in fp64. Returns (err, ref) for the listed channels."""
+    def output_error(self, W, codes_, scales, counts, X, channels=None, with_ref=True, n_threads: int = 0,
+                     offsets=None):
+        """Eq. (12) in fp64 (offsets: reading B2). Returns (err, ref) for the listed channels."""
         W = np.ascontiguousarray(W, dtype=np.float32)
         C, d = W.shape
         P = codes_.shape[1]
@@ -289,8 +315,9 @@ class Oracle:
         n = C if chan is None else chan.size
         err = np.zeros(n, np.float64)
         ref = np.zeros(n, np.float64) if with_ref else None
-        rc = self.lib.oracle_output_error(
-            _p(W), _p(np.ascontiguousarray(codes_, dtype=np.int8)),
+        off = None if offsets is None else np.ascontiguousarray(offsets, dtype=np.float32)
+        rc = self.lib.oracle_output_error_ex(
+            _p(W), _p(off), _p(np.ascontiguousarray(codes_, dtype=np.int8)),
             _p(np.ascontiguousarray(scales, dtype=np.float32)),
             _p(np.ascontiguousarray(counts, dtype=np.int32)), C, d, P, _p(X), N,
             _p(chan), 0 if chan is None else chan.size, _p(err), _p(ref), n_threads)
@@ -298,12 +325,15 @@ class Oracle:
             raise MemoryError("oracle_output_error failed")
         return err, ref
 
-    def reconstruct(self, codes_, scales, counts) -> np.ndarray:
+    def reconstruct(self, codes_, scales, counts, offsets=None) -> np.ndarray:
         codes_ = np.ascontiguousarray(codes_, dtype=np.int8)
         C, P, d = codes_.shape
         out = np.zeros((C, d), np.float32)
-        self.lib.oracle_reconstruct(_p(codes_), _p(np.ascontiguousarray(scales, dtype=np.float32)),
-                                   _p(np.ascontiguousarray(counts, dtype=np.int32)), C, d, P, _p(out))
+        off = None if offsets is None else np.ascontiguousarray(offsets, dtype=np.float32)
+        self.lib.oracle_reconstruct_ex(_p(off), _p(codes_),
+                                      _p(np.ascontiguousarray(scales, dtype=np.float32)),
+                                      _p(np.ascontiguousarray(counts, dtype=np.int32)), C, d, P,
+                                      _p(out))
         return out
 
     def integer_scales(self, scales, counts, p: int):
@@ -343,5 +373,6 @@ def _delegate(name):
 for _n in ("levels", "default_grid", "candidate_scales", "codes", "scale_error", "fit",
            "verify", "fit_calib", "verify_calib", "output_error", "reconstruct",
            "integer_scales", "integer_forward", "fit_clip", "verify_clip", "fit_paper",
-           "verify_paper", "min_gap", "paper_grid", "paper_grid_search"):
+           "verify_paper", "min_gap", "paper_grid", "paper_grid_search", "fit_asym",
+           "verify_asym"):
     globals()[_n] = _delegate(_n)

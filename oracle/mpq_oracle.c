@@ -74,6 +74,12 @@
  *          vertex A / B of the piece that holds such a point; every such
  *          candidate is evaluated by Eq. (9) and the smallest error wins
  *          (ties: the smallest g).
+ *   B2     Variant (asym != 0), the asymmetric set of Eq. (1) with B != 0
+ *          per channel: the offset beta = fl32((max_j w_j + min_j w_j) / 2)
+ *          (fp64 midpoint) takes B's place, the points fit w - beta
+ *          (Algorithm 1 on the centred weights, r_1 = w - beta), and
+ *          w~ = beta + sum_i a_i q_i.  The stopping rules still compare the
+ *          error of w~ with w's own (||w||^2, or the output energy of w).
  *   I1     Eq. (14) rounds 2^p a_i to the nearest integer with ties to even
  *          (R1); a value outside the 32-bit range is clamped to
  *          [-(2^31 - 1), 2^31 - 1] and counted.
@@ -378,15 +384,25 @@ static int clip_choose(const float *w, int64_t d, int M, const float *cc, int cl
 
 static int fit_channel(const float *w, int64_t d, int M, int P, const float *c,
                        int G, double tol, const calib_rule *cal, int refit, const clip_rule *clip,
-                       double eta, double *gwork, int8_t *codes, float *scales, double *err,
-                       double *xerr, double *r, float *a, double *E)
+                       double eta, double *gwork, int asym, float *offset, int8_t *codes,
+                       float *scales, double *err, double *xerr, double *r, float *a, double *E)
 {
     for (int64_t j = 0; j < d; ++j) r[j] = (double)w[j];   /* r_1 = w, Eq. (7) */
     double Ew = sum_sq(r, d);
     double thr = cal ? calib_threshold(cal, r, d) : 0.0;
+    if (asym) {                                             /* B2: r_1 = w - beta */
+        double mx = (double)w[0], mn = (double)w[0];
+        for (int64_t j = 1; j < d; ++j) {
+            if ((double)w[j] > mx) mx = (double)w[j];
+            if ((double)w[j] < mn) mn = (double)w[j];
+        }
+        const float beta = (float)((mx + mn) / 2.0);   /* B2: the midpoint */
+        *offset = beta;
+        for (int64_t j = 0; j < d; ++j) r[j] = (double)w[j] - (double)beta;   /* B2 */
+    }
     double e = 0.0;                                         /* S4: e_n */
     int n = 0;
-    if (clip && Ew > 0.0 && P >= 1) {                       /* C1: the first point */
+    if (clip && !asym && Ew > 0.0 && P >= 1) {              /* C1: the first point */
         int g = clip_choose(w, d, M, clip->c, clip->G, clip->X, clip->N, clip->a, clip->e,
                             clip->D, codes);
         if (g >= 0) {
@@ -454,7 +470,7 @@ static int n_threads_or_default(int nt)
  * [C][P] (may be NULL).  Slots at or after a channel's count are zero. */
 static int fit_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                      const float *grid, int G, double tol, const calib_rule *cal, int refit,
-                     const float *clipX, int64_t clipN, int clipG, double eta,
+                     const float *clipX, int64_t clipN, int clipG, double eta, float *offsets,
                      int8_t *codes, float *scales, int32_t *counts, double *err,
                      double *xerr, int n_threads)
 {
@@ -493,9 +509,11 @@ static int fit_layer(const float *W, int64_t C, int64_t d, int bits, int P,
             for (int64_t k = 0; k < C; ++k) {
                 memset(e, 0, sizeof(double) * (size_t)P);
                 memset(xe, 0, sizeof(double) * (size_t)P);
+                float beta = 0.0f;
                 int n = fit_channel(W + k * d, d, M, P, c, G, tol, cal, refit,
-                                    clipG > 0 ? &cl : NULL, eta, gw, codes + k * P * d,
-                                    scales + k * P, e, xe, r, a, E);
+                                    clipG > 0 ? &cl : NULL, eta, gw, offsets != NULL, &beta,
+                                    codes + k * P * d, scales + k * P, e, xe, r, a, E);
+                if (offsets) offsets[k] = beta;
                 counts[k] = n;
                 if (err) memcpy(err + k * P, e, sizeof(double) * (size_t)P);
                 if (xerr) memcpy(xerr + k * P, xe, sizeof(double) * (size_t)P);
@@ -513,8 +531,8 @@ int oracle_fit(const float *W, int64_t C, int64_t d, int bits, int P,
                const float *grid, int G, double tol, int8_t *codes,
                float *scales, int32_t *counts, double *err, int n_threads)
 {
-    return fit_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, NULL, 0, 0, 0.0, codes, scales, counts,
-                     err, NULL, n_threads);
+    return fit_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, NULL, 0, 0, 0.0, NULL, codes, scales,
+                     counts, err, NULL, n_threads);
 }
 
 /* The fit with its options: calib == 0 for the stopping rule S1 with tol,
@@ -524,12 +542,12 @@ int oracle_fit(const float *W, int64_t C, int64_t d, int bits, int P,
  * instead of the G-point grid. */
 int oracle_fit_ex(const float *W, int64_t C, int64_t d, int bits, int P, const float *grid, int G,
                   double tol, const float *X, int64_t N, int calib, double eps, int relative,
-                  int refit, int clipG, double eta, int8_t *codes, float *scales, int32_t *counts,
-                  double *err, double *xerr, int n_threads)
+                  int refit, int clipG, double eta, float *offsets, int8_t *codes, float *scales,
+                  int32_t *counts, double *err, double *xerr, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
     return fit_layer(W, C, d, bits, P, grid, G, tol, calib ? &cal : NULL, refit, X, N, clipG, eta,
-                     codes, scales, counts, err, calib ? xerr : NULL, n_threads);
+                     offsets, codes, scales, counts, err, calib ? xerr : NULL, n_threads);
 }
 
 /* The fit with the stopping rule S4 on the calibration batch X [d][N]. */
@@ -539,8 +557,8 @@ int oracle_fit_calib(const float *W, int64_t C, int64_t d, int bits, int P,
                      double *err, double *xerr, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
-    return fit_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, NULL, 0, 0, 0.0, codes, scales, counts,
-                     err, xerr, n_threads);
+    return fit_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, NULL, 0, 0, 0.0, NULL, codes, scales,
+                     counts, err, xerr, n_threads);
 }
 
 /* ------------------------------------------------------------------------
@@ -575,7 +593,7 @@ int oracle_fit_calib(const float *W, int64_t C, int64_t d, int bits, int P,
  * codes Eq. (10)'s at that scale (up to code ties).
  * status: 0 ok, 1 count, 2 scale not a candidate, 3 scale not optimal,
  *         4 code, 5 nonzero unused slot, 6 err value, 7 bad count range,
- *         8 output-error value.
+ *         8 output-error value, 9 offset (reading B2).
  * ------------------------------------------------------------------------ */
 
 /* V4 / V4x for one fp32 output: 1e-5 relative plus slack, one fp32
@@ -614,6 +632,7 @@ static int codes_agree(const double *r, int64_t d, double as, int M, const int8_
 static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                         const float *grid, int G, double tol, const calib_rule *cal, int refit,
                         const float *clipX, int64_t clipN, int clipG, double eta,
+                        const float *offsets,
                         const int8_t *codes, const float *scales, const int32_t *counts,
                         const float *err, const float *xerr, const int64_t *chan,
                         int64_t n_chan, int32_t *status, int32_t *cand_ties,
@@ -664,6 +683,16 @@ static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                 double Ew = sum_sq(r, d);
                 double thr = cal ? calib_threshold(cal, r, d) : 0.0;
                 double thr_slack = (cal && cal->relative) ? cal->eps * calib_slack(r, d, cal->X, cal->N) : 0.0;
+                if (offsets) {   /* B2: the other side's offset is the midpoint, exactly */
+                    double mx = (double)w[0], mn = (double)w[0];
+                    for (int64_t j = 1; j < d; ++j) {
+                        if ((double)w[j] > mx) mx = (double)w[j];
+                        if ((double)w[j] < mn) mn = (double)w[j];
+                    }
+                    const float beta = (float)((mx + mn) / 2.0);
+                    if (offsets[k] != beta) st = 9;
+                    for (int64_t j = 0; j < d; ++j) r[j] = (double)w[j] - (double)beta;
+                }
                 double e = 0.0;   /* S4: output error of the points so far */
                 for (int n = 0; st == 0; ++n) {
                     double Er = sum_sq(r, d);
@@ -807,7 +836,7 @@ int oracle_verify(const float *W, int64_t C, int64_t d, int bits, int P,
                   int32_t *cand_ties, int32_t *code_ties, int32_t *stop_ties,
                   double *err_relmax, int n_threads)
 {
-    return verify_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, NULL, 0, 0, 0.0, codes, scales,
+    return verify_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, NULL, 0, 0, 0.0, NULL, codes, scales,
                         counts, err, NULL, chan, n_chan, status, cand_ties, code_ties, stop_ties,
                         err_relmax, n_threads);
 }
@@ -815,15 +844,15 @@ int oracle_verify(const float *W, int64_t C, int64_t d, int bits, int P,
 /* The lockstep check of a fit with its options (as oracle_fit_ex). */
 int oracle_verify_ex(const float *W, int64_t C, int64_t d, int bits, int P, const float *grid,
                      int G, double tol, const float *X, int64_t N, int calib, double eps,
-                     int relative, int refit, int clipG, double eta, const int8_t *codes,
-                     const float *scales,
+                     int relative, int refit, int clipG, double eta, const float *offsets,
+                     const int8_t *codes, const float *scales,
                      const int32_t *counts, const float *err, const float *xerr,
                      const int64_t *chan, int64_t n_chan, int32_t *status, int32_t *cand_ties,
                      int32_t *code_ties, int32_t *stop_ties, double *err_relmax, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
     return verify_layer(W, C, d, bits, P, grid, G, tol, calib ? &cal : NULL, refit, X, N, clipG, eta,
-                        codes, scales, counts, err, calib ? xerr : NULL, chan, n_chan, status,
+                        offsets, codes, scales, counts, err, calib ? xerr : NULL, chan, n_chan, status,
                         cand_ties, code_ties, stop_ties, err_relmax, n_threads);
 }
 
@@ -838,17 +867,17 @@ int oracle_verify_calib(const float *W, int64_t C, int64_t d, int bits, int P,
                         double *err_relmax, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
-    return verify_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, NULL, 0, 0, 0.0, codes, scales,
+    return verify_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, NULL, 0, 0, 0.0, NULL, codes, scales,
                         counts, err, xerr, chan, n_chan, status, cand_ties, code_ties, stop_ties,
                         err_relmax, n_threads);
 }
 
 /* Residual D = w - sum_{i<n} a_i q_i of one channel, summed in point order
  * (Eq. (7); the same sequence of fp64 operations as the fit). */
-static void channel_residual(const float *w, const int8_t *q, const float *a,
+static void channel_residual(const float *w, float beta, const int8_t *q, const float *a,
                              int n, int64_t d, double *D)
 {
-    for (int64_t j = 0; j < d; ++j) D[j] = (double)w[j];
+    for (int64_t j = 0; j < d; ++j) D[j] = (double)w[j] - (double)beta;
     for (int i = 0; i < n; ++i)
         for (int64_t j = 0; j < d; ++j)
             D[j] = D[j] - (double)a[i] * (double)q[(int64_t)i * d + j];
@@ -857,10 +886,10 @@ static void channel_residual(const float *w, const int8_t *q, const float *a,
 /* Eq. (12): err[k] = (1/N) sum_n ((w_k - w~_k) . x_n)^2 and, if ref is not
  * NULL, ref[k] = (1/N) sum_n (w_k . x_n)^2, for the listed channels
  * (chan == NULL: all C channels, outputs indexed by channel). */
-int oracle_output_error(const float *W, const int8_t *codes, const float *scales,
-                        const int32_t *counts, int64_t C, int64_t d, int P,
-                        const float *X, int64_t N, const int64_t *chan,
-                        int64_t n_chan, double *err, double *ref, int n_threads)
+int oracle_output_error_ex(const float *W, const float *offsets, const int8_t *codes,
+                           const float *scales, const int32_t *counts, int64_t C, int64_t d, int P,
+                           const float *X, int64_t N, const int64_t *chan,
+                           int64_t n_chan, double *err, double *ref, int n_threads)
 {
     int nt = n_threads_or_default(n_threads);
     int64_t cnt = chan ? n_chan : C;
@@ -876,7 +905,8 @@ int oracle_output_error(const float *W, const int8_t *codes, const float *scales
             for (int64_t s = 0; s < cnt; ++s) {
                 int64_t k = chan ? chan[s] : s;
                 const float *w = W + k * d;
-                channel_residual(w, codes + k * P * d, scales + k * P, counts[k], d, D);
+                channel_residual(w, offsets ? offsets[k] : 0.0f, codes + k * P * d, scales + k * P,
+                                 counts[k], d, D);
                 double se = 0.0, sr = 0.0;
                 for (int64_t n = 0; n < N; ++n) {
                     double y = 0.0, yr = 0.0;
@@ -897,17 +927,25 @@ int oracle_output_error(const float *W, const int8_t *codes, const float *scales
     return fail ? -1 : 0;
 }
 
-/* Eq. (4): w~ = sum_{i<n} a_i q_i, accumulated in fp64 in point order and
- * rounded once to fp32. */
-void oracle_reconstruct(const int8_t *codes, const float *scales,
+int oracle_output_error(const float *W, const int8_t *codes, const float *scales,
                         const int32_t *counts, int64_t C, int64_t d, int P,
-                        float *W_hat)
+                        const float *X, int64_t N, const int64_t *chan,
+                        int64_t n_chan, double *err, double *ref, int n_threads)
+{
+    return oracle_output_error_ex(W, NULL, codes, scales, counts, C, d, P, X, N, chan, n_chan, err,
+                                  ref, n_threads);
+}
+
+/* Eq. (4): w~ = sum_{i<n} a_i q_i (plus the offset of reading B2, first),
+ * accumulated in fp64 in point order and rounded once to fp32. */
+void oracle_reconstruct_ex(const float *offsets, const int8_t *codes, const float *scales,
+                           const int32_t *counts, int64_t C, int64_t d, int P, float *W_hat)
 {
     for (int64_t k = 0; k < C; ++k) {
         const int8_t *q = codes + k * P * d;
         const float *a = scales + k * P;
         for (int64_t j = 0; j < d; ++j) {
-            double s = 0.0;
+            double s = offsets ? (double)offsets[k] : 0.0;
             for (int i = 0; i < counts[k]; ++i)
                 s = s + (double)a[i] * (double)q[(int64_t)i * d + j];
             W_hat[k * d + j] = (float)s;
@@ -967,4 +1005,10 @@ int oracle_integer_forward(const int8_t *codes, const int32_t *A, const int32_t 
         }
     }
     return bad ? -1 : 0;
+}
+
+void oracle_reconstruct(const int8_t *codes, const float *scales, const int32_t *counts, int64_t C,
+                        int64_t d, int P, float *W_hat)
+{
+    oracle_reconstruct_ex(NULL, codes, scales, counts, C, d, P, W_hat);
 }

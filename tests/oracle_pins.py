@@ -702,6 +702,79 @@ def check_paper_fit(orc):
     assert (orc.verify_paper(W, 3, 4, 0.0, c0, s0, n0)["status"] != 0).mean() > 0.5
 
 
+# ------------------------------------------- reading B2: asymmetric codes
+def _dyadic(seed, C=20, d=30):
+    rng = np.random.default_rng(seed)
+    return (rng.integers(-96, 97, (C, d)) / 64.0 + rng.integers(-8, 9, (C, 1)) / 4.0).astype(np.float32)
+
+
+def check_asym_translation(orc):
+    """Shifting a channel by a constant (exactly representable) leaves the
+    points unchanged and moves the offset by that constant."""
+    W = _dyadic(71)
+    a = orc.fit_asym(W, 4, 4, 64, 0.0)
+    b = orc.fit_asym(W + np.float32(3.25), 4, 4, 64, 0.0)
+    assert all(np.array_equal(x, y) for x, y in zip(a[:3], b[:3]))
+    assert np.array_equal(b[5], a[5] + np.float32(3.25))
+
+
+def check_asym_is_the_centred_fit(orc):
+    """The points of the asymmetric fit are the symmetric fit of w - beta
+    (exact in fp32 on this lattice); beta is the midpoint of the range."""
+    W = _dyadic(72)
+    codes, scales, counts, err, _, off = orc.fit_asym(W, 3, 5, 32, 0.0)
+    assert np.array_equal(off, ((W.max(1).astype(np.float64) + W.min(1)) / 2).astype(np.float32))
+    c0, s0, n0, e0 = orc.fit(W - off[:, None], 3, 5, 32, 0.0)
+    assert np.array_equal(codes, c0) and np.array_equal(scales, s0) and np.array_equal(counts, n0)
+
+
+def check_asym_edges(orc):
+    """Two distinct values per channel are reproduced exactly by one point;
+    a constant channel needs no point (beta alone); 10 + small noise stops
+    after one point, as the stopping rule compares with ||w||^2."""
+    rng = np.random.default_rng(73)
+    lo, hi = rng.integers(-128, 0, 10) / 64.0, rng.integers(32, 192, 10) / 64.0   # exact midpoints
+    W = np.where(rng.random((10, 16)) < 0.5, lo[:, None], hi[:, None]).astype(np.float32)
+    W[:, 0], W[:, 1] = lo, hi
+    # 2 bits (M = 1): the top candidate is the half range itself, codes +-1
+    codes, scales, counts, err, _, off = orc.fit_asym(W, 2, 3, 64, 0.0)
+    assert (counts == 1).all() and np.array_equal(orc.reconstruct(codes, scales, counts, off), W)
+    C = np.full((3, 8), 5.0, np.float32)
+    codes, scales, counts, err, _, off = orc.fit_asym(C, 4, 3, 64, 1e-3)
+    assert (counts == 0).all() and (off == 5.0).all()
+    N = (10.0 + 0.01 * rng.standard_normal((8, 40))).astype(np.float32)
+    codes, scales, counts, err, _, off = orc.fit_asym(N, 4, 4, 64, 1e-3)
+    assert (counts == 1).all()
+
+
+def check_asym_error_and_reconstruct(orc):
+    """Output error and reconstruction with offsets against numpy fp64
+    (w~ = beta + sum a q, the offset first)."""
+    rng = np.random.default_rng(74)
+    W = (rng.standard_normal((15, 50)) + 1.5).astype(np.float32)
+    X = rng.standard_normal((50, 20)).astype(np.float32)
+    codes, scales, counts, err, _, off = orc.fit_asym(W, 4, 3, 64, 1e-3)
+    what = np.zeros((15, 50))
+    for k in range(15):
+        s = np.full(50, float(off[k]))
+        for i in range(counts[k]):
+            s = s + float(scales[k, i]) * codes[k, i].astype(np.float64)
+        what[k] = s
+    assert np.array_equal(orc.reconstruct(codes, scales, counts, off), what.astype(np.float32))
+    e, _ = orc.output_error(W, codes, scales, counts, X, offsets=off)
+    ref = np.mean(((W.astype(np.float64) - what) @ X.astype(np.float64)) ** 2, axis=1)
+    assert np.allclose(e, ref, rtol=1e-12, atol=0)
+
+
+def check_asym_verifier(orc):
+    W = (np.random.default_rng(75).standard_normal((12, 40)) + 0.7).astype(np.float32)
+    codes, scales, counts, err, _, off = orc.fit_asym(W, 4, 4, 64, 1e-3)
+    v = orc.verify_asym(W, 4, 4, 64, codes, scales, counts, off, err.astype(np.float32), tol=1e-3)
+    assert (v["status"] == 0).all()
+    off2 = np.nextafter(off, np.float32(np.inf))
+    assert (orc.verify_asym(W, 4, 4, 64, codes, scales, counts, off2, tol=1e-3)["status"] == 9).all()
+
+
 # ------------------------------------------- Sec. 3.4: deployment arithmetic
 def check_integer_scales(orc):
     """Eq. (14), reading I1: exact values, half-way ties to even (worked by
@@ -794,6 +867,8 @@ ALL_CHECKS = [
     check_calib_verifier, check_calib_verifier_fp32_evaluation, check_refit_one_point,
     check_refit_residual_chain, check_refit_verifier, check_clip_bruteforce, check_clip_hadamard_is_eq9,
     check_clip_then_algorithm1, check_clip_zero_batch, check_clip_verifier, check_min_gap,
-    check_paper_grid_size, check_paper_search_bruteforce, check_paper_fit, check_integer_scales,
+    check_paper_grid_size, check_paper_search_bruteforce, check_paper_fit, check_asym_translation,
+    check_asym_is_the_centred_fit, check_asym_edges, check_asym_error_and_reconstruct,
+    check_asym_verifier, check_integer_scales,
     check_integer_forward_exact, check_integer_forward_one_point, check_integer_forward_approximates,
 ]

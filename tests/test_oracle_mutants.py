@@ -86,6 +86,13 @@ MUTANTS = [
      "int64_t around[3] = {g0, g0 + 1, g0 + 1};"),
     ("paper_ties_largest", "if (E < Eb || (E == Eb && h < best)) { Eb = E; best = h; }",
      "if (E <= Eb) { Eb = E; best = h; }"),
+    ("asym_offset_max", "const float beta = (float)((mx + mn) / 2.0);   /* B2: the midpoint */",
+     "const float beta = (float)mx;"),
+    ("asym_stop_centred",
+     "for (int64_t j = 0; j < d; ++j) r[j] = (double)w[j] - (double)beta;   /* B2 */",
+     "for (int64_t j = 0; j < d; ++j) r[j] = (double)w[j] - (double)beta;\n        Ew = sum_sq(r, d);"),
+    ("asym_recon_no_offset", "double s = offsets ? (double)offsets[k] : 0.0;", "double s = 0.0;"),
+    ("asym_error_no_offset", "D[j] = (double)w[j] - (double)beta;", "D[j] = (double)w[j];"),
     ("calib_stop_ignores_cap", "if (n >= P || Er == 0.0) return 1;", "if (Er == 0.0) return 1;"),
     ("calib_no_minimum_one_point", "if (n >= 1 && e <= thr) return 1;", "if (e <= thr) return 1;"),
 ]
