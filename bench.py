@@ -82,6 +82,9 @@ def parse():
     ap.add_argument("--clip", type=int, default=0, metavar="GC",
                     help="point 1 from the clipping of Eq. (13) with GC factors (the paper: 20; "
                          "mpq_fit_layers_ex; implies --separate for the isotropic rule)")
+    ap.add_argument("--asym", action="store_true",
+                    help="asymmetric per-channel codes (offset + points; mpq_fit_layers_ex; implies "
+                         "--separate)")
     ap.add_argument("--paper-eta", type=float, default=0.0, metavar="ETA",
                     help="fit on the paper's own grid of Eq. (11) with maximal step ETA (the paper: "
                          "2^-10 = 0.0009765625; mpq_fit_layers_ex; implies --separate)")
@@ -304,16 +307,16 @@ def main():
         del src, dst
 
     separate = (args.separate or args.dense or args.paper_eta > 0
-                or ((args.refit or args.clip) and args.rule != "calib"))
+                or ((args.refit or args.clip or args.asym) and args.rule != "calib"))
     calib = args.rule == "calib"
     if calib and separate:
         raise SystemExit("--rule calib has its own call sequence (no --separate / --dense)")
 
     def step(ev=None):
         if calib:
-            if args.refit or args.clip:
+            if args.refit or args.clip or args.asym:
                 ls.fit_ex(wk.bits, wk.n_grid, refit=args.refit, calib=True, eps=wk.tol, relative=True,
-                          clip_grid=args.clip)
+                          clip_grid=args.clip, asym=args.asym)
             else:
                 ls.fit_calib(wk.bits, wk.n_grid, wk.tol, True)
             ls.reconstruct()
@@ -328,8 +331,8 @@ def main():
                               out=(ls.codes[i], ls.scales[i], ls.counts[i], ls.fit_err[i]))
         elif args.paper_eta > 0:
             ls.fit_ex(wk.bits, 1, wk.tol, paper_eta=args.paper_eta)
-        elif args.refit or args.clip:
-            ls.fit_ex(wk.bits, wk.n_grid, wk.tol, refit=args.refit, clip_grid=args.clip)
+        elif args.refit or args.clip or args.asym:
+            ls.fit_ex(wk.bits, wk.n_grid, wk.tol, refit=args.refit, clip_grid=args.clip, asym=args.asym)
         else:
             ls.fit(wk.bits, wk.n_grid, wk.tol)
         if ev: ev[1].record(stream)
@@ -468,6 +471,7 @@ def main():
                    "n_grid": wk.n_grid, "tol": wk.tol, "calib_columns": wk.n_calib,
                    "points_per_step": points, "search": "dense" if args.dense else "histogram",
                    "refit": bool(args.refit), "clip_grid": args.clip, "paper_eta": args.paper_eta,
+                   "asym": bool(args.asym),
                    "rule": ("Algorithm 2 on the calibration batch, relative" if calib
                             else "||r||^2 <= tol ||w||^2"),
                    "point_counts": count_hist.tolist(),

@@ -183,6 +183,9 @@ typedef struct mpq_layer {
     float *out_ref;       /* mpq_output_error_layers: NULL or [c_out]              */
     float *W_hat;         /* mpq_reconstruct_layers: [c_out][d]                    */
     float *fit_xerr;      /* mpq_fit_layers_calib: [c_out][max_points]             */
+    float *offsets;       /* NULL, or [c_out]: asymmetric codes (mpq_fit_options.asym):
+                             written by the fit, read by mpq_output_error_layers and
+                             mpq_reconstruct_layers (w~ = offset + sum a q)      */
 } mpq_layer;
 
 /* mpq_fit_layer on every layer (reads W, c_out, d, codes, scales, counts,
@@ -208,6 +211,7 @@ int mpq_reconstruct_layers(const mpq_layer *layers, int n_layers, int max_points
  * The fit launches run side by side (as in mpq_fit_layers); then the output
  * errors of all layers run as one batch while the reconstruction runs beside
  * them, on the caller's stream and a library-owned stream joined back to it.
+ * The fit is symmetric: the layers' offsets fields are ignored.
  * Arguments as for mpq_fit_layers; every layer is checked before anything is
  * enqueued.
  */
@@ -271,6 +275,14 @@ int mpq_fit_layers_calib(const mpq_layer *layers, int n_layers, int bits, int ma
  *             points after it follow Algorithm 1 with the stopping rule.
  *             Reads X and n of every layer; c_out * Gc <= MPQ_MAX_ERR_DIM.
  *             Cannot be combined with refit.
+ *   asym      nonzero: asymmetric per-channel codes (Eq. (1) with B != 0): the
+ *             offset beta = fl32((max_j w_j + min_j w_j) / 2) is written to the
+ *             layer's offsets [c_out] (must not be NULL), the points fit
+ *             w - beta, and w~ = beta + sum a q.  The stopping rules still
+ *             compare with w's own error (||w||^2, or w's output energy).
+ *             With either stopping rule and refit; not with clip_grid or
+ *             paper_eta.  The batched output error and reconstruction add the
+ *             offsets of layers whose offsets are not NULL.
  *   paper_eta 0, or eta > 0: the candidate scales of each step are the
  *             paper's own grid (Eq. (11), Def. 1): a = g * gamma,
  *             g = 1 .. floor(2 M ||r|| / gamma), gamma = min(Delta_r / M, eta),
@@ -292,6 +304,7 @@ typedef struct mpq_fit_options {
     int relative;
     int clip_grid;
     float paper_eta;
+    int asym;
 } mpq_fit_options;
 int mpq_fit_layers_ex(const mpq_layer *layers, int n_layers, int bits, int max_points,
                       const float *grid_host, int n_grid, float tol, const mpq_fit_options *opt,

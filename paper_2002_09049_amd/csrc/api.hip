@@ -411,8 +411,13 @@ int require_hist(const mpq_layer *layers, int n_layers, bool hist_fits, const ch
 
 int fit_layers_impl(Search mode, const mpq_layer *layers, int n_layers, int bits, int max_points,
                     const float *grid_host, int n_grid, float tol, void *stream, int refit = 0,
-                    int clip_grid = 0)
+                    int clip_grid = 0, int asym = 0)
 {
+    if (asym && n_layers > 0 && layers) {
+        for (int l = 0; l < n_layers; ++l)
+            if (layers[l].c_out > 0 && !layers[l].offsets)
+                return fail(MPQ_ERR_INVALID_ARG, "%sasym needs offsets", n_layers > 1 ? "a layer: " : "");
+    }
     if (clip_grid && n_layers > 0 && layers) {
         const int rc0 = clip_checks(layers, n_layers, clip_grid);
         if (rc0 != MPQ_OK) return rc0;
@@ -424,6 +429,7 @@ int fit_layers_impl(Search mode, const mpq_layer *layers, int n_layers, int bits
     if (refit && (rc = require_hist(layers, n_layers, hist_fits, "the refit")) != MPQ_OK) return rc;
     if (clip_grid && (rc = require_hist(layers, n_layers, hist_fits, "the clipping")) != MPQ_OK)
         return rc;
+    if (asym && (rc = require_hist(layers, n_layers, hist_fits, "asym")) != MPQ_OK) return rc;
     hipStream_t s = (hipStream_t)stream;
     float *dgrid = nullptr;
     rc = upload_grid(grid_host, n_grid, s, &dgrid);
@@ -431,6 +437,9 @@ int fit_layers_impl(Search mode, const mpq_layer *layers, int n_layers, int bits
     const int M = (1 << (bits - 1)) - 1;
     std::vector<FitJob> jobs = build_fit_jobs(mode, hist_fits, layers, n_layers, M, max_points,
                                               dgrid, n_grid, tol, -1.0, refit);
+    if (asym)
+        for (FitJob &j : jobs)
+            for (int i = 0; i < j.b.n_layers; ++i) j.b.L[i].offsets = layers[j.layers[i]].offsets;
     if (clip_grid) {   // point 1 from the clipping, then the fit resumes from it
         rc = clip_first_points(layers, n_layers, M, max_points, clip_grid, false, {}, s);
         if (rc != MPQ_OK) {
@@ -530,8 +539,10 @@ int output_error_impl(const mpq_layer *layers, int n_layers, int max_points, voi
         int rc = check_error_layer(L, max_points, true);
         if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
         if (L.c_out == 0) continue;
-        in.push_back(mpq::ErrLayerIn{L.W, L.codes, L.scales, L.counts, L.X, L.out_err, L.out_ref,
-                                     L.c_out, L.d, L.n});
+        mpq::ErrLayerIn I = {L.W, L.codes, L.scales, L.counts, L.X, L.out_err, L.out_ref,
+                             L.c_out, L.d, L.n};
+        I.offsets = L.offsets;   // reading B2 (NULL: symmetric)
+        in.push_back(I);
     }
     if (in.empty()) return MPQ_OK;
     hipStream_t s = (hipStream_t)stream;
@@ -555,7 +566,8 @@ int reconstruct_impl(const mpq_layer *layers, int n_layers, int max_points, void
         const mpq_layer &L = layers[l];
         int rc = check_error_layer(L, max_points, false);
         if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
-        if (L.c_out > 0) in.push_back(mpq::RecLayer{L.codes, L.scales, L.counts, L.W_hat, L.c_out, L.d});
+        if (L.c_out > 0)
+            in.push_back(mpq::RecLayer{L.codes, L.scales, L.counts, L.W_hat, L.c_out, L.d, L.offsets});
     }
     if (in.empty()) return MPQ_OK;
     hipError_t e = mpq::launch_reconstruct(in.data(), (int)in.size(), max_points, (hipStream_t)stream);
@@ -610,7 +622,7 @@ int quantize_impl(const mpq_layer *layers, int n_layers, int bits, int max_point
                                           L.c_out, L.d, L.n});
         }
         if (L.W_hat) {
-            rec.push_back(mpq::RecLayer{L.codes, L.scales, L.counts, L.W_hat, L.c_out, L.d});
+            rec.push_back(mpq::RecLayer{L.codes, L.scales, L.counts, L.W_hat, L.c_out, L.d, nullptr});
             bytes += 5.0 * (double)L.c_out * (double)L.d;
         }
     }
@@ -741,8 +753,13 @@ int clip_first_points(const mpq_layer *layers, int n_layers, int M, int P, int G
 // threshold's output error of W runs beside the first fit step.
 int calib_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
                const float *grid_host, int n_grid, float eps, int relative, void *stream,
-               int refit = 0, int clip_grid = 0)
+               int refit = 0, int clip_grid = 0, int asym = 0)
 {
+    if (asym && n_layers > 0 && layers) {
+        for (int l = 0; l < n_layers; ++l)
+            if (layers[l].c_out > 0 && !layers[l].offsets)
+                return fail(MPQ_ERR_INVALID_ARG, "%sasym needs offsets", n_layers > 1 ? "a layer: " : "");
+    }
     if (n_layers < 0 || (n_layers > 0 && !layers))
         return fail(MPQ_ERR_INVALID_ARG, "layers must hold n_layers >= 0 entries");
     if (!(eps >= 0.0f) || !isfinite(eps))
@@ -807,6 +824,7 @@ int calib_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
             H.ref = ref(l);
             H.list = list(l);
             H.nlist = nlist(l);
+            H.offsets = asym ? layers[l].offsets : nullptr;
         }
     }
     // the output-error items of one step (the same groups every step), and
@@ -815,8 +833,10 @@ int calib_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
     for (int l = 0; l < n_layers; ++l) {
         const mpq_layer &L = layers[l];
         if (L.c_out == 0) continue;
-        in.push_back(mpq::ErrLayerIn{L.W, L.codes, L.scales, L.counts, L.X, L.fit_xerr, nullptr,
-                                     L.c_out, L.d, L.n, list(l), nlist(l), P});
+        mpq::ErrLayerIn I = {L.W, L.codes, L.scales, L.counts, L.X, L.fit_xerr, nullptr,
+                             L.c_out, L.d, L.n, list(l), nlist(l), P};
+        I.offsets = asym ? L.offsets : nullptr;
+        in.push_back(I);
         if (relative)
             in_ref.push_back(mpq::ErrLayerIn{L.W, L.codes, L.scales, L.counts, L.X, nullptr, ref(l),
                                              L.c_out, L.d, L.n, nullptr, nullptr, 0});
@@ -1155,20 +1175,23 @@ int mpq_fit_layers_ex(const mpq_layer *layers, int n_layers, int bits, int max_p
                       void *stream)
 {
     if (opt && opt->paper_eta != 0.0f) {
-        if (opt->calib || opt->refit || opt->clip_grid)
-            return fail(MPQ_ERR_INVALID_ARG, "paper_eta cannot be combined with calib, refit or clip_grid");
+        if (opt->calib || opt->refit || opt->clip_grid || opt->asym)
+            return fail(MPQ_ERR_INVALID_ARG,
+                        "paper_eta cannot be combined with calib, refit, clip_grid or asym");
         return paper_impl(layers, n_layers, bits, max_points, tol, opt->paper_eta, stream);
     }
     if (!opt) return fit_layers_impl(Search::kAuto, layers, n_layers, bits, max_points, grid_host,
                                      n_grid, tol, stream);
     if (opt->clip_grid && opt->refit)
         return fail(MPQ_ERR_INVALID_ARG, "refit and clip_grid cannot be combined");
+    if (opt->asym && opt->clip_grid)
+        return fail(MPQ_ERR_INVALID_ARG, "asym and clip_grid cannot be combined");
     if (opt->clip_grid < 0) return fail(MPQ_ERR_INVALID_ARG, "clip_grid must be >= 0");
     if (opt->calib)
         return calib_impl(layers, n_layers, bits, max_points, grid_host, n_grid, opt->eps,
-                          opt->relative, stream, opt->refit != 0, opt->clip_grid);
+                          opt->relative, stream, opt->refit != 0, opt->clip_grid, opt->asym != 0);
     return fit_layers_impl(Search::kAuto, layers, n_layers, bits, max_points, grid_host, n_grid, tol,
-                           stream, opt->refit != 0, opt->clip_grid);
+                           stream, opt->refit != 0, opt->clip_grid, opt->asym != 0);
 }
 
 int mpq_output_error(const float *W, const int8_t *codes, const float *scales,

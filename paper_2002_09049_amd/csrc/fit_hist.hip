@@ -335,11 +335,34 @@ fit_hist_kernel(const HistBatch B)
         __syncthreads();
     }
 
+    // asymmetric codes (reading B2): the points fit w - beta, beta the fp32
+    // midpoint of the channel's range; the stopping rule keeps ||w||^2
+    double beta = 0.0;
+    double Ew = 0.0;
+    const bool asym = Ly.offsets != nullptr;
+    if (asym) {
+        float mx = -INFINITY, mn = INFINITY;
+        for (int j = t; j < d; j += T) {
+            mx = fmaxf(mx, wk[j]);
+            mn = fminf(mn, wk[j]);
+        }
+        mx = block_reduce<T>(mx, MaxOp(), s_redf);
+        mn = block_reduce<T>(mn, MinOp(), s_redf);
+        const float b = (float)(((double)mx + (double)mn) / 2.0);
+        beta = (double)b;
+        if (t == 0) Ly.offsets[k] = b;
+    }
+    if (asym || (s0 >= 1 && !stepping)) {   // ||w||^2 when the first residual is not w
+        double sw = 0.0;
+        for (int j = t; j < d; j += T) sw = fma((double)wk[j], (double)wk[j], sw);
+        Ew = block_reduce<T>(sw, SumOp(), s_redd);
+    }
+
     // residual element u of this thread after np points (0 past the channel)
     auto rebuild = [&](int u, int np) {
         const int j = t + T * u;
         if (j >= d) return 0.0;
-        double v = (double)wk[j];
+        double v = (double)wk[j] - beta;
         for (int p = 0; p < np; ++p) v = fma(-(double)s_scale[p], (double)qk[(int64_t)p * d + j], v);
         return v;
     };
@@ -352,12 +375,6 @@ fit_hist_kernel(const HistBatch B)
     for (int g = t; g < G; g += T)
         S.c[g] = B.grid ? B.grid[g] : (float)((double)(g + 1) / (double)G);
 
-    double Ew = 0.0;
-    if (s0 >= 1 && !stepping) {   // ||w||^2 for the stopping rule of a resumed fit
-        double sw = 0.0;
-        for (int j = t; j < d; j += T) sw = fma((double)wk[j], (double)wk[j], sw);
-        Ew = block_reduce<T>(sw, SumOp(), s_redd);
-    }
     float apend = 0.0f;
     int n = 0;
     bool more = false;   // calibration step: the channel took its point and goes on
@@ -422,7 +439,7 @@ fit_hist_kernel(const HistBatch B)
         const double Er = lsum;
 
         // ---- stop / point count
-        if (i == 0) Ew = Er;
+        if (i == 0 && !asym) Ew = Er;
         else if (i > s0 && Ly.err && t == 0) Ly.err[k * P + (i - 1)] = (float)Er;
         if (stepping && i > s0) {   // one point per calibration step
             n = i;

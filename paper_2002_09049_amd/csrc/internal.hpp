@@ -61,7 +61,7 @@ hipError_t launch_fit(const FitParams &p, const FitLayout &L, hipStream_t s);
 // select the same kernel variant (hist_variant); the descriptors travel by
 // value in the kernel arguments.
 constexpr int64_t kHistMaxDim = 32768;
-constexpr int kMaxBatchLayers = 48;
+constexpr int kMaxBatchLayers = 44;
 
 struct HistLayer {
     const float *W;     // [C][d]
@@ -74,6 +74,9 @@ struct HistLayer {
     const float *ref;   // [C] output error of W itself (relative threshold) or nullptr
     int32_t *list;      // [C] channels that took a point in this step, in any order
     int32_t *nlist;     // [P] their number, per step (zero before the first step)
+    // asymmetric codes (reading B2): nullptr, or [C] per-channel offsets
+    // (the midpoint of w, written by the fit; the points fit w - offset)
+    float *offsets;
     int d;
     int c_begin;        // first workgroup of this layer in the launch
 };
@@ -143,6 +146,9 @@ struct ErrLayerIn {
     const int32_t *rows;
     const int32_t *nrows;
     int64_t err_stride;
+    // per-channel offsets (reading B2) subtracted from the err item's D rows,
+    // or nullptr
+    const float *offsets;
     // clipping candidates (cand != nullptr): the item's D rows are the C * Gc
     // candidate residuals w_k - a_kj [w_k / a_kj]_Q (a_kj = cand[k * Gc + j],
     // codes in [-M, M]); err[k * Gc + j] is written
@@ -194,8 +200,9 @@ struct RecLayer {
     const int32_t *counts;
     float *W_hat;
     int64_t C, d;
+    const float *offsets;   // reading B2: added first, or nullptr
 };
-constexpr int kMaxRecLayers = 64;
+constexpr int kMaxRecLayers = 56;
 hipError_t launch_reconstruct(const RecLayer *in, int n_in, int P, hipStream_t s);
 
 // Deployment arithmetic (Sec. 3.4).

@@ -101,6 +101,7 @@ struct ErrLayer {
     int use_points;      // 1: D = residual (err), 0: D = W (ref), 2: D = clipping candidates
     const float *cand;   // use_points == 2: [C / Gc][Gc] candidate scales (C counts rows of D)
     int Gc, M;
+    const float *offsets;   // use_points == 1: per-channel offsets (reading B2) or nullptr
     int vecw;            // d % 4 == 0, W 16-byte and codes 4-byte aligned
 };
 
@@ -167,12 +168,14 @@ __global__ void __launch_bounds__(256) form_dt_kernel(const ErrGroup g)
         } else if (L.use_points != 2 && m < nact) {
             const int64_t row = L.rows ? (int64_t)L.rows[m] : m;
             const int nk = L.use_points ? min(max(L.counts[row], 0), P) : 0;  // counts is caller data
+            const double beta = (L.use_points && L.offsets) ? (double)L.offsets[row] : 0.0;
             const float *wr = L.W + row * d;
             const int8_t *cr = L.codes + row * (int64_t)P * d;
             const float *sr = L.scales + row * (int64_t)P;
             if (L.vecw && k < d) {   // d % 4 == 0: four k wholly inside
                 const float4 w = *(const float4 *)(wr + k);
-                r[0] = w.x; r[1] = w.y; r[2] = w.z; r[3] = w.w;
+                r[0] = (double)w.x - beta; r[1] = (double)w.y - beta;
+                r[2] = (double)w.z - beta; r[3] = (double)w.w - beta;
                 for (int p = 0; p < nk; ++p) {
                     const double a = (double)sr[p];
                     const uint32_t q = *(const uint32_t *)(cr + (int64_t)p * d + k);
@@ -183,7 +186,7 @@ __global__ void __launch_bounds__(256) form_dt_kernel(const ErrGroup g)
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
                     if (k + u < d) {
-                        double v = (double)wr[k + u];
+                        double v = (double)wr[k + u] - beta;
                         for (int p = 0; p < nk; ++p)
                             v = fma(-(double)sr[p], (double)cr[(int64_t)p * d + k + u], v);
                         r[u] = v;
@@ -538,6 +541,7 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
             L.nrows = grp[i].use_points == 1 ? I.nrows : nullptr;
             L.stride = grp[i].use_points == 1 && I.err_stride > 0 ? I.err_stride : 1;
             L.cand = grp[i].use_points == 2 ? I.cand : nullptr;
+            L.offsets = grp[i].use_points == 1 ? I.offsets : nullptr;
             L.Gc = I.Gc;
             L.M = I.M;
             L.Dt = (float *)cur;

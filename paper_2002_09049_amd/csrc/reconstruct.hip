@@ -1,5 +1,6 @@
 // Quantized weights of Eq. (4): W_hat[k][j] = fl32(sum_{i<n_k} a_i q_i[j]),
-// summed in fp64 in point order.  Elementwise and HBM-bound: it reads the
+// summed in fp64 in point order (with asymmetric codes, reading B2, the sum
+// starts at the channel's offset).  Elementwise and HBM-bound: it reads the
 // n_k code rows of each channel and writes its fp32 row once.
 //
 // Up to kMaxRecLayers layers share one launch (descriptors by value in the
@@ -30,6 +31,7 @@ struct RecDesc {
     int rows;          // rows per workgroup
     int block_begin;   // first workgroup of this layer
     int vec;           // d % 4 == 0, codes 4-byte and W_hat 16-byte aligned
+    const float *offsets;   // reading B2: each row's sum starts at its offset, or nullptr
 };
 
 struct RecGroup {
@@ -59,7 +61,7 @@ __global__ void __launch_bounds__(kRecThreads) reconstruct_kernel(const RecGroup
             const int n = min(max(L.counts[k], 0), P);   // clamp: counts is caller data
             const int8_t *q = L.codes + k * (int64_t)P * d + j;
             const float *a = L.scales + k * (int64_t)P;
-            double s = 0.0;
+            double s = L.offsets ? (double)L.offsets[k] : 0.0;
             for (int i = 0; i < n; ++i) s = fma((double)a[i], (double)q[(int64_t)i * d], s);
             L.W_hat[k * d + j] = (float)s;
         }
@@ -70,9 +72,10 @@ __global__ void __launch_bounds__(kRecThreads) reconstruct_kernel(const RecGroup
         const int8_t *crow = L.codes + k * (int64_t)P * d;
         const float *a = L.scales + k * (int64_t)P;
         float *out = L.W_hat + k * d;
+        const double beta = L.offsets ? (double)L.offsets[k] : 0.0;
         if (L.vec) {
             for (int j = 4 * t; j < d; j += 4 * kRecThreads) {
-                double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+                double s0 = beta, s1 = beta, s2 = beta, s3 = beta;
                 for (int i = 0; i < n; ++i) {
                     const uint32_t w = *(const uint32_t *)(crow + (int64_t)i * d + j);
                     const double ai = (double)a[i];
@@ -85,7 +88,7 @@ __global__ void __launch_bounds__(kRecThreads) reconstruct_kernel(const RecGroup
             }
         } else {
             for (int j = t; j < d; j += kRecThreads) {
-                double s = 0.0;
+                double s = beta;
                 for (int i = 0; i < n; ++i) s = fma((double)a[i], (double)crow[(int64_t)i * d + j], s);
                 out[j] = (float)s;
             }
@@ -115,6 +118,7 @@ hipError_t launch_reconstruct(const RecLayer *in, int n_in, int P, hipStream_t s
             L.block_begin = (int)blocks;
             blocks += (I.C + L.rows - 1) / L.rows;
             L.vec = I.d % 4 == 0 && ((uintptr_t)I.codes) % 4 == 0 && ((uintptr_t)I.W_hat) % 16 == 0;
+            L.offsets = I.offsets;
         }
         if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
         LaunchTimer timer(s, "reconstruct_kernel");

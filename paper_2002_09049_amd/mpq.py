@@ -43,7 +43,7 @@ class Layer(ctypes.Structure):
                 ("counts", ctypes.c_void_p), ("fit_err", ctypes.c_void_p),
                 ("X", ctypes.c_void_p), ("n", ctypes.c_int64), ("out_err", ctypes.c_void_p),
                 ("out_ref", ctypes.c_void_p), ("W_hat", ctypes.c_void_p),
-                ("fit_xerr", ctypes.c_void_p)]
+                ("fit_xerr", ctypes.c_void_p), ("offsets", ctypes.c_void_p)]
 
 
 
@@ -51,7 +51,7 @@ class FitOptions(ctypes.Structure):
     """struct mpq_fit_options (include/mpq.h)."""
     _fields_ = [("refit", ctypes.c_int), ("calib", ctypes.c_int), ("eps", ctypes.c_float),
                 ("relative", ctypes.c_int), ("clip_grid", ctypes.c_int),
-                ("paper_eta", ctypes.c_float)]
+                ("paper_eta", ctypes.c_float), ("asym", ctypes.c_int)]
 
 
 class IntLayer(ctypes.Structure):
@@ -354,7 +354,7 @@ class LayerSet:
         n = len(self.W)
         self.arr = (Layer * max(n, 1))()
         self.codes, self.scales, self.counts, self.fit_err = [], [], [], []
-        self.err, self.ref, self.W_hat, self.xerr = [], [], [], []
+        self.err, self.ref, self.W_hat, self.xerr, self.offsets = [], [], [], [], []
         for i, W in enumerate(self.W):
             C, d = W.shape
             dev = W.device
@@ -367,6 +367,7 @@ class LayerSet:
             what = torch.empty((C, d), dtype=torch.float32, device=dev)
             xerr = torch.empty((C, max_points), dtype=torch.float32, device=dev) if calib is not None else None
             self.xerr.append(xerr)
+            self.offsets.append(torch.zeros((C,), dtype=torch.float32, device=dev))
             self.codes.append(codes)
             self.scales.append(scales)
             self.counts.append(counts)
@@ -403,7 +404,7 @@ class LayerSet:
 
     def fit_ex(self, bits: int, n_grid: int, tol: float = 0.0, refit: bool = False,
                calib: bool = False, eps: float = 0.0, relative: bool = True, clip_grid: int = 0,
-               paper_eta: float = 0.0, grid=None, stream=None):
+               paper_eta: float = 0.0, asym: bool = False, grid=None, stream=None):
         """mpq_fit_layers_ex: the fit with options (refit: reading A2; calib:
         Algorithm 2's stopping rule on the calibration batches; clip_grid:
         point 1 from the clipping of Eq. (13) with that many factors;
@@ -412,12 +413,23 @@ class LayerSet:
             raise ValueError("LayerSet was built without calibration batches")
         g = self._grid(grid, n_grid)
         opt = FitOptions(1 if refit else 0, 1 if calib else 0, float(eps), 1 if relative else 0,
-                         int(clip_grid), float(paper_eta))
+                         int(clip_grid), float(paper_eta), 1 if asym else 0)
+        # the offsets take part in the fit and, afterwards, in the layer's
+        # output error and reconstruction only when the fit is asymmetric
+        for i in range(self.n):
+            self.arr[i].offsets = self.offsets[i].data_ptr() if asym and self.offsets[i] is not None else None
         _check(load().mpq_fit_layers_ex(ctypes.addressof(self.arr), self.n, bits, self.max_points,
                                         None if g is None else g.ctypes.data_as(ctypes.c_void_p),
                                         n_grid, float(tol), ctypes.addressof(opt), _stream(stream)))
 
+    def _symmetric(self):
+        """A symmetric fit follows: the layers' output error and
+        reconstruction take no offsets."""
+        for i in range(self.n):
+            self.arr[i].offsets = None
+
     def fit(self, bits: int, n_grid: int, tol: float, grid=None, stream=None):
+        self._symmetric()
         g = self._grid(grid, n_grid)
         _check(load().mpq_fit_layers(ctypes.addressof(self.arr), self.n, bits, self.max_points,
                                      None if g is None else g.ctypes.data_as(ctypes.c_void_p),
@@ -426,6 +438,7 @@ class LayerSet:
     def quantize(self, bits: int, n_grid: int, tol: float, grid=None, stream=None):
         """mpq_quantize_layers: fit, output error (when calibration batches
         were given) and reconstruction of every layer in one call."""
+        self._symmetric()
         g = self._grid(grid, n_grid)
         _check(load().mpq_quantize_layers(ctypes.addressof(self.arr), self.n, bits, self.max_points,
                                           None if g is None else g.ctypes.data_as(ctypes.c_void_p),
@@ -437,6 +450,7 @@ class LayerSet:
         stopping rule on its calibration batch; xerr [C, P] per layer."""
         if self.X is None:
             raise ValueError("LayerSet was built without calibration batches")
+        self._symmetric()
         g = self._grid(grid, n_grid)
         _check(load().mpq_fit_layers_calib(ctypes.addressof(self.arr), self.n, bits, self.max_points,
                                            None if g is None else g.ctypes.data_as(ctypes.c_void_p),

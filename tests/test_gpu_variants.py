@@ -254,3 +254,75 @@ def test_paper_grid_limits():
     with pytest.raises(mpq.MPQError) as e:
         ls.fit_ex(4, 1, 0.0, refit=True, paper_eta=2.0 ** -10)
     assert e.value.status == mpq.MPQ_ERR_INVALID_ARG
+
+
+def _fit_asym(W, bits, P, G, tol=0.0, X=None, calib=False, eps=0.0, refit=False):
+    import torch
+    from paper_2002_09049_amd import mpq
+    ls = mpq.LayerSet([to_dev(W)], P, calib=None if X is None else [to_dev(X)])
+    ls.fit_ex(bits, G, tol, refit=refit, calib=calib, eps=eps, relative=True, asym=True)
+    if X is not None:
+        ls.output_error()
+    ls.reconstruct()
+    torch.cuda.synchronize()
+    out = (ls.codes[0].cpu().numpy(), ls.scales[0].cpu().numpy(), ls.counts[0].cpu().numpy(),
+           ls.fit_err[0].cpu().numpy(), None if X is None else ls.xerr[0].cpu().numpy(),
+           ls.offsets[0].cpu().numpy())
+    extra = (None if X is None else ls.err[0].cpu().numpy(), ls.W_hat[0].cpu().numpy())
+    return out, extra
+
+
+ASYM = [
+    # (C, d, bits, P, G, tol, shift): channels with a common offset exercise B2
+    (5, 1, 4, 4, 128, 1e-3, 0.0),
+    (40, 9, 4, 8, 512, 1e-3, 0.3),
+    (64, 147, 4, 4, 256, 1e-3, 1.0),
+    (64, 576, 3, 6, 128, 1e-4, -0.5),
+    (10, 2304, 4, 4, 256, 1e-3, 2.0),
+    (4, 20000, 3, 4, 256, 1e-4, 0.1),
+]
+
+
+@pytest.mark.parametrize("C,d,bits,P,G,tol,shift", ASYM, ids=[f"C{c}_d{d}_b{b}_P{p}_G{g}" for c, d, b, p, g, _, _ in ASYM])
+def test_asym_parity(orc, C, d, bits, P, G, tol, shift):
+    say(f"case asym C={C} d={d} bits={bits} P={P} G={G} tol={tol}")
+    W = wl.random_weights(C, d, seed=5 * C + d) + np.float32(shift)
+    W[0] = np.float32(shift)          # a constant channel: no point
+    (codes, scales, counts, err, _, off), (_, what) = _fit_asym(W, bits, P, G, tol)
+    _ok(orc.verify_asym(W, bits, P, G, codes, scales, counts, off, err, tol=float(np.float32(tol))))
+    assert counts[0] == 0
+    assert np.array_equal(what, orc.reconstruct(codes, scales, counts, off))
+
+
+def test_asym_with_calibration_rule_and_output_error(orc):
+    C, d, N = 48, 576, 256
+    W = wl.random_weights(C, d, seed=19) + np.float32(0.8)
+    X = wl.random_calib(d, N, seed=20)
+    say("case asym + Algorithm 2 rule")
+    (codes, scales, counts, err, xerr, off), (oe, what) = _fit_asym(W, 4, 6, 128, X=X, calib=True, eps=2e-3)
+    _ok(orc.verify_asym(W, 4, 6, 128, codes, scales, counts, off, err, xerr, X=X, calib=True,
+                        eps=float(np.float32(2e-3))))
+    ref, _ = orc.output_error(W, codes, scales, counts, X, with_ref=False, offsets=off)
+    assert np.all(np.abs(oe - ref) <= 1e-5 * ref + 1e-30)
+
+
+def test_asym_with_refit(orc):
+    W = wl.random_weights(30, 300, seed=21) + np.float32(-0.4)
+    (codes, scales, counts, err, _, off), _ = _fit_asym(W, 4, 4, 64, 1e-3, refit=True)
+    _ok(orc.verify_asym(W, 4, 4, 64, codes, scales, counts, off, err, tol=float(np.float32(1e-3)),
+                        refit=True))
+
+
+def test_symmetric_fit_after_asym_takes_no_offsets(orc):
+    """A LayerSet's symmetric fit after an asymmetric one reconstructs
+    without offsets."""
+    import torch
+    from paper_2002_09049_amd import mpq
+    W = wl.random_weights(16, 64, seed=3) + np.float32(1.0)
+    ls = mpq.LayerSet([to_dev(W)], 4)
+    ls.fit_ex(4, 64, 1e-3, asym=True)
+    ls.fit(4, 64, 1e-3)
+    ls.reconstruct()
+    torch.cuda.synchronize()
+    out = (ls.codes[0].cpu().numpy(), ls.scales[0].cpu().numpy(), ls.counts[0].cpu().numpy())
+    assert np.array_equal(ls.W_hat[0].cpu().numpy(), orc.reconstruct(*out))
