@@ -705,7 +705,9 @@ hipError_t launch_hist_t(const HistBatch &b, int64_t channels, size_t lds, hipSt
 // channels longer than the capacity T * EPT of variant v - 1, up to its own.
 // 256-thread variants let four channels share a CU (128 VGPRs, under 40 KB of
 // LDS each), so one channel's barriers and serial phases overlap another's
-// arithmetic; the 512- and 1024-thread variants cover lengths whose residual
+// arithmetic (256 x 9 takes d = 2304, the 3 x 3 kernels over 256 input
+// channels, which a 512-thread workgroup would run half idle, two per CU);
+// the 512- and 1024-thread variants cover lengths whose residual
 // would not fit 128 VGPRs at 256 threads without spilling to scratch (at
 // 256 x 18 the spills moved ~7x the channel's algorithmic bytes through HBM).
 // The last variant (1024 x 32, up to 32768) holds no residual copy: it
@@ -716,8 +718,8 @@ struct Variant {
 };
 constexpr Variant kVariants[] = {{64, 1, false},   {64, 2, false},   {64, 4, false},
                                  {256, 2, false},  {256, 4, false},  {256, 8, false},
-                                 {512, 9, false},  {1024, 8, false}, {512, 32, false},
-                                 {1024, 32, true}};
+                                 {256, 9, false},  {512, 9, false},  {1024, 8, false},
+                                 {512, 32, false}, {1024, 32, true}};
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 static_assert(kVariants[kNumVariants - 1].threads * kVariants[kNumVariants - 1].ept == kHistMaxDim,
               "the last variant covers the longest channels");
@@ -797,11 +799,12 @@ hipError_t launch_fit_hist(const HistBatch &batch, int variant, int64_t channels
     case 3: return launch_hist_t<256, 2>(b, channels, lds, s);
     case 4: return launch_hist_t<256, 4>(b, channels, lds, s);
     case 5: return launch_hist_t<256, 8>(b, channels, lds, s);
-    case 6: return launch_hist_t<512, 9>(b, channels, lds, s);
-    case 7: return launch_hist_t<1024, 8>(b, channels, lds, s);
+    case 6: return launch_hist_t<256, 9>(b, channels, lds, s);
+    case 7: return launch_hist_t<512, 9>(b, channels, lds, s);
+    case 8: return launch_hist_t<1024, 8>(b, channels, lds, s);
     // 512 threads leave 256 VGPRs per thread for the register-resident residual
-    case 8: return launch_hist_t<512, 32>(b, channels, lds, s);
-    case 9: return launch_hist_t<1024, 32, true>(b, channels, lds, s);
+    case 9: return launch_hist_t<512, 32>(b, channels, lds, s);
+    case 10: return launch_hist_t<1024, 32, true>(b, channels, lds, s);
     default: return hipErrorInvalidValue;
     }
 }

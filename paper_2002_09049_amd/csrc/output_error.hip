@@ -13,11 +13,14 @@
 //  2. gemm: Y = D X on MFMA (v_mfma_f32_32x32x2f32, fp32 in and accumulate),
 //     the path's one dense contraction.  Dt and X are both K-major, so the A
 //     and B slabs are the same kind of copy: kBK rows of 128 consecutive
-//     floats.  A workgroup of four wavefronts owns a 128 x 128 tile of Y and
-//     one K range; each wavefront owns 64 x 64 as 2 x 2 MFMA blocks.  The K
-//     loop stages slabs through double-buffered LDS, loading the next slab
-//     into registers (buffer loads: offsets past a range read as zeros) while
-//     the MFMAs consume the current one.  The epilogue squares Y (fp64) and
+//     floats.  A workgroup of eight wavefronts owns a 128 x 128 tile of Y and
+//     one K range; each wavefront owns 64 x 32 as 2 MFMA blocks.  The K
+//     loop stages slabs through double-buffered LDS from two register sets:
+//     while the MFMAs consume one slab, the next waits in registers for its
+//     LDS buffer and the one after is in flight (buffer loads: offsets past a
+//     range read as zeros), so a load has two slabs of MFMA time to arrive.
+//     Two wavefronts per SIMD cover each other's LDS and barrier waits.
+//     The epilogue squares Y (fp64) and
 //     sums each row over the tile's columns into a partial per (column tile,
 //     row); a layer whose K is split (to balance a grid of long and short
 //     K ranges) stores its fp32 Y tiles per K range instead.
@@ -55,12 +58,11 @@ namespace {
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kBM = 128, kBN = 128, kBK = 16;
-constexpr int kMinRangeK = 1024;  // K of a split layer's K range, at least (unless K is short)
-constexpr int kThreads = 256;
+constexpr int kBM = 128, kBN = 128, kBK = 32;
+constexpr int kRangeK = 768;      // K of a split layer's K range, about
+constexpr int kThreads = 512;   // GEMM workgroup: eight wavefronts, two per SIMD
 constexpr int kPad = 4;          // LDS row padding (floats); rows stay 16-byte aligned
 constexpr int kVec = kBK * kBM / kThreads / 4;   // float4 per thread and operand per slab
-constexpr int kRowThreads = kBM / (4 * kVec);    // threads per slab row
 constexpr int kMaxErrLayers = 22;
 constexpr int kXcds = 8;         // MI355X: workgroups are dealt to 8 XCDs in turn
 constexpr int kFT = 64;          // form tile: 64 rows x 64 k
@@ -212,12 +214,12 @@ __global__ void __launch_bounds__(256) form_dt_kernel(const ErrGroup g)
 
 // ---- 2. gemm: Y = D X, squared and summed per row
 template <bool kVecX>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3)))
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
 gemm_err_kernel(const ErrGroup g)
 {
     __shared__ __align__(16) float sA[2][kBK][kBM + kPad];
     __shared__ __align__(16) float sX[2][kBK][kBN + kPad];
-    __shared__ double sRow[kBM];
+    __shared__ double sPart[kBN / 32][kBM];
 
     int li = 0;
     while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].block_begin) ++li;
@@ -246,94 +248,104 @@ gemm_err_kernel(const ErrGroup g)
 
     const int t = threadIdx.x;
     const int lane = t % kWave, wid = t / kWave;
-    const int wm = wid / 2, wn = wid % 2;
+    const int wm = wid / 4, wn = wid % 4;   // rows wm * 64 + [0, 64), columns wn * 32 + [0, 32)
     const int64_t C = L.C, n = L.n;
     const int64_t col0 = (int64_t)tn * kBN;
     const int64_t kbeg = (int64_t)split * L.kchunk;
     const int64_t kend = min(kbeg + (int64_t)L.kchunk, (int64_t)L.d);
+    const int nslab = (int)((kend - kbeg + kBK - 1) / kBK);
 
     // buffer resources over this K range's rows of Dt and X (below 2^31
     // bytes, see plan_item): rows past kend read as zeros
     const __amdgpu_buffer_rsrc_t rsA =
         make_rsrc(L.Dt + kbeg * L.ldc, (uint32_t)((kend - kbeg) * L.ldc * 4));
     const __amdgpu_buffer_rsrc_t rsX = make_rsrc(L.X + kbeg * n, (uint32_t)((kend - kbeg) * n * 4));
-    // staging role: row sk of the slab, 4 * kVec consecutive columns from sm
-    const int sk = t / kRowThreads, sm = (t % kRowThreads) * 4 * kVec;
+    // staging role: float4 number t + kThreads v of the slab, rows of
+    // kBM / 4 float4: row sk + kRowStep v, columns sm .. sm + 3, so each load
+    // instruction of a wavefront covers whole rows
+    constexpr int kF4Row = kBM / 4;
+    constexpr int kRowStep = kThreads / kF4Row;
+    const int sk = t / kF4Row, sm = (t % kF4Row) * 4;
     uint32_t offA[kVec], offX[kVec];
 #pragma unroll
     for (int v = 0; v < kVec; ++v) {
-        const int64_t m = row0 + sm + 4 * v, c = col0 + sm + 4 * v;
-        offA[v] = m < L.ldc ? (uint32_t)((sk * L.ldc + m) * 4) : kOob;   // ldc % 4 == 0
-        offX[v] = (kVecX && c < n) ? (uint32_t)((sk * n + c) * 4) : kOob;   // n % 4 == 0
+        const int64_t m = row0 + sm, c = col0 + sm;
+        const int64_t kr = sk + kRowStep * v;
+        offA[v] = m < L.ldc ? (uint32_t)((kr * L.ldc + m) * 4) : kOob;   // ldc % 4 == 0
+        offX[v] = (kVecX && c < n) ? (uint32_t)((kr * n + c) * 4) : kOob;   // n % 4 == 0
     }
     const uint32_t stepA = (uint32_t)(kBK * L.ldc * 4), stepX = (uint32_t)(kBK * n * 4);
 
-    f32x4 ra[kVec], rx[kVec];
-    auto load = [&](int64_t k0) {
-        const uint32_t s = (uint32_t)((k0 - kbeg) / kBK);
+    // two register sets: the slab after next is in flight while a slab is
+    // multiplied and the next one is stored
+    f32x4 ra0[kVec], rx0[kVec], ra1[kVec], rx1[kVec];
+    auto load = [&](f32x4 (&ra)[kVec], f32x4 (&rx)[kVec], int s) {
 #pragma unroll
         for (int v = 0; v < kVec; ++v) {
-            ra[v] = load4(rsA, offA[v] == kOob ? kOob : offA[v] + s * stepA);
+            ra[v] = load4(rsA, offA[v] == kOob ? kOob : offA[v] + (uint32_t)s * stepA);
             if constexpr (kVecX) {
-                rx[v] = load4(rsX, offX[v] == kOob ? kOob : offX[v] + s * stepX);
+                rx[v] = load4(rsX, offX[v] == kOob ? kOob : offX[v] + (uint32_t)s * stepX);
             } else {
-                const int64_t c = col0 + sm + 4 * v;
+                const int64_t c = col0 + sm, kr = (int64_t)s * kBK + sk + kRowStep * v;
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
-                    const uint32_t o = c + u < n ? (uint32_t)(((k0 - kbeg + sk) * n + c + u) * 4) : kOob;
+                    const uint32_t o = c + u < n ? (uint32_t)((kr * n + c + u) * 4) : kOob;
                     rx[v][u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsX, o, 0, 0));
                 }
             }
         }
     };
-    auto store = [&](int buf) {
+    auto store = [&](const f32x4 (&ra)[kVec], const f32x4 (&rx)[kVec], int buf) {
 #pragma unroll
         for (int v = 0; v < kVec; ++v) {
-            *(f32x4 *)&sA[buf][sk][sm + 4 * v] = ra[v];
-            *(f32x4 *)&sX[buf][sk][sm + 4 * v] = rx[v];
+            *(f32x4 *)&sA[buf][sk + kRowStep * v][sm] = ra[v];
+            *(f32x4 *)&sX[buf][sk + kRowStep * v][sm] = rx[v];
         }
     };
 
-    floatx16 acc[2][2];
+    floatx16 acc[2];
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) acc[a][bb][v] = 0.0f;
+        for (int v = 0; v < 16; ++v) acc[a][v] = 0.0f;
 
-    int buf = 0;
-    load(kbeg);
-    store(0);
-    __syncthreads();
-    for (int64_t k0 = kbeg; k0 < kend; k0 += kBK) {
-        const bool more = k0 + kBK < kend;
-        if (more) load(k0 + kBK);   // global loads in flight during the MFMAs
+    // MFMA block a of a wavefront takes its rows 2 i + a (i < 32), so one
+    // 8-byte LDS read gives a lane both blocks' A operands
+    auto compute = [&](int buf) {
 #pragma unroll
         for (int kk = 0; kk < kBK; kk += 2) {
             const int kr = kk + lane / 32;
-            float af[2], bf[2];
-#pragma unroll
-            for (int a = 0; a < 2; ++a) af[a] = sA[buf][kr][wm * 64 + a * 32 + lane % 32];
-#pragma unroll
-            for (int bb = 0; bb < 2; ++bb) bf[bb] = sX[buf][kr][wn * 64 + bb * 32 + lane % 32];
-#pragma unroll
-            for (int a = 0; a < 2; ++a)
-#pragma unroll
-                for (int bb = 0; bb < 2; ++bb)
-                    acc[a][bb] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[a], bf[bb], acc[a][bb], 0, 0, 0);
+            const float2 a2 = *(const float2 *)&sA[buf][kr][wm * 64 + 2 * (lane % 32)];
+            const float bx = sX[buf][kr][wn * 32 + lane % 32];
+            acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a2.x, bx, acc[0], 0, 0, 0);
+            acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a2.y, bx, acc[1], 0, 0, 0);
         }
-        if (more) store(buf ^ 1);
+    };
+
+    load(ra0, rx0, 0);
+    if (nslab > 1) load(ra1, rx1, 1);
+    store(ra0, rx0, 0);
+    __syncthreads();
+    if (nslab > 2) load(ra0, rx0, 2);
+    for (int s = 0; s < nslab; s += 2) {
+        // buffer 0 holds slab s, set 1 slab s + 1, set 0 slab s + 2 (in flight)
+        compute(0);
+        if (s + 1 < nslab) store(ra1, rx1, 1);
         __syncthreads();
-        buf ^= 1;
+        if (s + 1 >= nslab) break;
+        if (s + 3 < nslab) load(ra1, rx1, s + 3);
+        compute(1);
+        if (s + 2 < nslab) store(ra0, rx0, 0);
+        __syncthreads();
+        if (s + 4 < nslab) load(ra0, rx0, s + 4);
     }
 
-    // Output layout of a 32 x 32 MFMA block: lane holds column lane % 32 and,
-    // in register v, row 8 * (v / 4) + 4 * (lane / 32) + (v % 4).
+    // Output layout of a 32 x 32 MFMA block: lane holds block column
+    // lane % 32 and, in register v, block row 8 (v / 4) + 4 (lane / 32) + v % 4
     auto row_of = [&](int a, int v) {
-        return row0 + wm * 64 + a * 32 + 8 * (v / 4) + 4 * (lane / 32) + (v % 4);
+        return row0 + wm * 64 + 2 * (8 * (v / 4) + 4 * (lane / 32) + (v % 4)) + a;
     };
-    auto col_of = [&](int bb) { return col0 + wn * 64 + bb * 32 + lane % 32; };
+    const int64_t col = col0 + wn * 32 + lane % 32;
 
     if (L.splits > 1) {
         // this K range's Y tile; the finish kernel sums the ranges
@@ -341,36 +353,27 @@ gemm_err_kernel(const ErrGroup g)
 #pragma unroll
         for (int a = 0; a < 2; ++a)
 #pragma unroll
-            for (int bb = 0; bb < 2; ++bb)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int64_t r = row_of(a, v), c = col_of(bb);
-                    if (r < C && c < n) yp[((int64_t)split * C + r) * n + c] = acc[a][bb][v];
-                }
+            for (int v = 0; v < 16; ++v) {
+                const int64_t r = row_of(a, v);
+                if (r < C && col < n) yp[((int64_t)split * C + r) * n + col] = acc[a][v];
+            }
         return;
     }
 
-    // squares summed over the tile's columns, per row (fp64, fixed order)
-    for (int pass = 0; pass < 2; ++pass) {
-        if (wn == pass) {
+    // squares summed over the tile's columns, per row (fp64, fixed order):
+    // each wavefront's 32 columns, then the four column quarters in order
 #pragma unroll
-            for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < 2; ++a)
 #pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const double y0 = (double)acc[a][0][v], y1 = (double)acc[a][1][v];
-                    double s = fma(y0, y0, y1 * y1);
-                    s = half_wave_reduce(s, SumOp());
-                    if (lane % 32 == 0) {
-                        const int r = (int)(row_of(a, v) - row0);
-                        sRow[r] = pass == 0 ? s : sRow[r] + s;
-                    }
-                }
+        for (int v = 0; v < 16; ++v) {
+            const double y = (double)acc[a][v];
+            const double s = half_wave_reduce(y * y, SumOp());
+            if (lane % 32 == 0) sPart[wn][(int)(row_of(a, v) - row0)] = s;
         }
-        __syncthreads();
-    }
+    __syncthreads();
     for (int r = t; r < kBM; r += kThreads) {
         const int64_t gr = row0 + r;
-        if (gr < C) L.rowpart[(int64_t)tn * C + gr] = sRow[r];
+        if (gr < C) L.rowpart[(int64_t)tn * C + gr] = ((sPart[0][r] + sPart[1][r]) + sPart[2][r]) + sPart[3][r];
     }
 }
 
@@ -401,10 +404,30 @@ __global__ void __launch_bounds__(256) finish_err_kernel(const ErrGroup g)
     const int64_t k = b;
     if (k >= nact) return;
     double s = 0.0;
-    for (int64_t c = threadIdx.x; c < n; c += 256) {
-        float y = 0.0f;
-        for (int sp = 0; sp < L.splits; ++sp) y += L.ypart[((int64_t)sp * C + k) * n + c];
-        s = fma((double)y, (double)y, s);
+    if (g.vecx) {
+        // n % 4 == 0: four columns per thread and pass, the K ranges' loads
+        // of up to four ranges issued together
+        for (int64_t c = 4 * threadIdx.x; c < n; c += 4 * 256) {
+            f32x4 y = {0.0f, 0.0f, 0.0f, 0.0f};
+            for (int sp0 = 0; sp0 < L.splits; sp0 += 4) {
+                f32x4 v[4];
+#pragma unroll
+                for (int z = 0; z < 4; ++z)
+                    if (sp0 + z < L.splits)
+                        v[z] = *(const f32x4 *)(L.ypart + ((int64_t)(sp0 + z) * C + k) * n + c);
+#pragma unroll
+                for (int z = 0; z < 4; ++z)
+                    if (sp0 + z < L.splits) y += v[z];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) s = fma((double)y[u], (double)y[u], s);
+        }
+    } else {
+        for (int64_t c = threadIdx.x; c < n; c += 256) {
+            float y = 0.0f;
+            for (int sp = 0; sp < L.splits; ++sp) y += L.ypart[((int64_t)sp * C + k) * n + c];
+            s = fma((double)y, (double)y, s);
+        }
     }
     s = block_reduce<256>(s, SumOp(), red);
     if (threadIdx.x == 0) L.out[slot(k)] = (float)(s / (double)n);
@@ -436,9 +459,11 @@ std::vector<Item> items_of(const ErrLayerIn *in, int n_in)
     return it;
 }
 
-// K split of a layer: tiles of about work / 512 slabs (two per CU), K ranges
-// of at least kMinRangeK (or a quarter of a short K: a layer of few tiles still spreads),
-// and K ranges whose rows of Dt and X stay below 2^31 bytes.  It
+// K split of a layer: K ranges of about kRangeK, or of work / 512 slabs (two
+// tiles per CU) for a layer that alone fills the GPU, and K ranges whose rows
+// of Dt and X stay below 2^31 bytes.  The ranges of a split layer make the
+// GEMM store fp32 Y tiles that the finish kernel reads back, so a layer of
+// short K stays whole: the other layers of a call fill the GPU.  The split
 // depends on the layer alone, so a layer's result does not depend on the
 // other layers of the call.
 Plan plan_item(const ErrLayerIn &I)
@@ -450,9 +475,7 @@ Plan plan_item(const ErrLayerIn &I)
     q.ntn = (I.n + kBN - 1) / kBN;
     const int64_t slabs = (I.d + kBK - 1) / kBK;
     const double work = (double)(q.ntm * q.ntn) * (double)slabs;
-    // a K range of at least kMinRangeK, or a quarter of a short K
-    const int64_t floor_slabs = std::min<int64_t>(kMinRangeK / kBK, (slabs + 3) / 4);
-    const int64_t target = std::max<int64_t>(floor_slabs, (int64_t)(work / 512.0 + 0.5));
+    const int64_t target = std::max<int64_t>(kRangeK / kBK, (int64_t)(work / 512.0 + 0.5));
     int64_t sp = (slabs + target / 2) / target;
     sp = std::max<int64_t>(1, std::min<int64_t>(sp, slabs));
     int64_t kchunk = (slabs + sp - 1) / sp * kBK;

@@ -6,11 +6,12 @@
 // Up to kMaxRecLayers layers share one launch (descriptors by value in the
 // kernel arguments).  A workgroup takes a group of whole rows of one layer
 // (about kRowElems elements), so a row's count and scales are uniform loads:
-//  - rows of at least 256 elements: the workgroup sweeps each row in turn,
-//    four elements per thread (one 32-bit word of codes per point, one float4
-//    store) when the layer has d % 4 == 0 and aligned buffers;
-//  - shorter rows (depthwise kernels, d = 9): the group's elements are spread
-//    over the threads as one flat range.
+//  - a layer with d % 4 == 0 and aligned buffers: the group's rows form one
+//    flat range of 4-element chunks (one 32-bit word of codes per point, one
+//    float4 store per chunk);
+//  - other rows of fewer than 256 elements (depthwise kernels, d = 9): the
+//    group's elements are spread over the threads as one flat range;
+//  - other rows: the workgroup sweeps each row in turn.
 #include <algorithm>
 
 #include "internal.hpp"
@@ -52,6 +53,44 @@ __global__ void __launch_bounds__(kRecThreads) reconstruct_kernel(const RecGroup
     const int k1 = min(k0 + L.rows, L.C);
     const int t = threadIdx.x;
 
+    if (L.vec) {
+        // the group's rows as one flat range of 4-element chunks; per chunk
+        // the code words and scales of up to four points are loaded before
+        // any is used (points past the fourth follow in order)
+        const int q4 = d / 4;
+        const int total = (k1 - k0) * q4;
+        for (int e = t; e < total; e += kRecThreads) {
+            const int kr = e / q4, j = (e - kr * q4) * 4;
+            const int64_t k = k0 + kr;
+            const int n = min(max(L.counts[k], 0), P);   // clamp: counts is caller data
+            const int8_t *crow = L.codes + k * (int64_t)P * d + j;
+            const float *a = L.scales + k * (int64_t)P;
+            uint32_t w[4];
+            float ai[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                w[i] = i < n ? *(const uint32_t *)(crow + (int64_t)i * d) : 0u;
+                ai[i] = i < n ? a[i] : 0.0f;
+            }
+            const double beta = L.offsets ? (double)L.offsets[k] : 0.0;
+            double s[4] = {beta, beta, beta, beta};
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (i < n) {
+#pragma unroll
+                    for (int u = 0; u < 4; ++u)
+                        s[u] = fma((double)ai[i], (double)(int)(int8_t)(uint8_t)(w[i] >> (8 * u)), s[u]);
+                }
+            for (int i = 4; i < n; ++i) {
+                const uint32_t wi = *(const uint32_t *)(crow + (int64_t)i * d);
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    s[u] = fma((double)a[i], (double)(int)(int8_t)(uint8_t)(wi >> (8 * u)), s[u]);
+            }
+            *(float4 *)(L.W_hat + k * d + j) = make_float4((float)s[0], (float)s[1], (float)s[2], (float)s[3]);
+        }
+        return;
+    }
     if (d < kRecThreads) {
         // flat range of short rows
         const int total = (k1 - k0) * d;
@@ -73,25 +112,10 @@ __global__ void __launch_bounds__(kRecThreads) reconstruct_kernel(const RecGroup
         const float *a = L.scales + k * (int64_t)P;
         float *out = L.W_hat + k * d;
         const double beta = L.offsets ? (double)L.offsets[k] : 0.0;
-        if (L.vec) {
-            for (int j = 4 * t; j < d; j += 4 * kRecThreads) {
-                double s0 = beta, s1 = beta, s2 = beta, s3 = beta;
-                for (int i = 0; i < n; ++i) {
-                    const uint32_t w = *(const uint32_t *)(crow + (int64_t)i * d + j);
-                    const double ai = (double)a[i];
-                    s0 = fma(ai, (double)(int)(int8_t)(uint8_t)w, s0);
-                    s1 = fma(ai, (double)(int)(int8_t)(uint8_t)(w >> 8), s1);
-                    s2 = fma(ai, (double)(int)(int8_t)(uint8_t)(w >> 16), s2);
-                    s3 = fma(ai, (double)(int)(int8_t)(uint8_t)(w >> 24), s3);
-                }
-                *(float4 *)(out + j) = make_float4((float)s0, (float)s1, (float)s2, (float)s3);
-            }
-        } else {
-            for (int j = t; j < d; j += kRecThreads) {
-                double s = beta;
-                for (int i = 0; i < n; ++i) s = fma((double)a[i], (double)crow[(int64_t)i * d + j], s);
-                out[j] = (float)s;
-            }
+        for (int j = t; j < d; j += kRecThreads) {
+            double s = beta;
+            for (int i = 0; i < n; ++i) s = fma((double)a[i], (double)crow[(int64_t)i * d + j], s);
+            out[j] = (float)s;
         }
     }
 }

@@ -129,7 +129,7 @@ def test_deterministic(dense):
         assert np.array_equal(x, y)
 
 
-@pytest.mark.parametrize("d", [8192, 8193, 16384, 16385, 32768, 32769])
+@pytest.mark.parametrize("d", [2048, 2049, 2304, 2305, 8192, 8193, 16384, 16385, 32768, 32769])
 def test_search_kernel_boundaries(orc, d):
     """Largest channels of each register-resident variant of the histogram
     search, and the first length that falls back to the dense search."""
