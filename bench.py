@@ -59,8 +59,8 @@ STAGES = (("fit", ("fit_hist_kernel", "fit_dense_kernel")),
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="resnet18")
     ap.add_argument("--cpu-stride", type=int, default=1,
                     help="cpu_baseline fits every n-th channel of every layer")
@@ -345,25 +345,6 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    nl = len(Ws)
-    ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4)) for _ in range(args.steps)]
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    mpq.timing_enable(True)
-    wall0 = time.perf_counter()
-    t_start.record(stream)
-    for s in range(args.steps):
-        step(ev[s])
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    launches = mpq.timing_read()
-    mpq.timing_enable(False)
-    ms_total = t_start.elapsed_time(t_end)
-    ms_step = ms_total / args.steps
-    steps = args.steps
-
     # ---- algorithmic work per kernel and step
     fit_kernel = {}
     work = {}   # kernel -> dict of per-step work figures
@@ -410,39 +391,76 @@ def main():
         # reconstruct: reads the codes of the used points, writes fp32
         add("reconstruct_kernel", bytes=n * d + 4 * C * d)
 
-    per = {}
-    for name, ms in launches:
-        p = per.setdefault(name, [0, 0.0])
-        p[0] += 1
-        p[1] += ms
-    kernels = {}
-    for name, (cnt, tot) in per.items():
-        avg_s = tot / cnt * 1e-3
-        k = {"stage": stage_of(name), "launches_per_step": cnt / steps,
-             "avg_us": tot / cnt * 1e3, "us_per_step": tot / steps * 1e3}
-        w = work.get(name, {})
-        lps = cnt / steps
-        if "evals" in w:
-            ev_launch = w["evals"] / lps
-            k.update({"bound": "alu", "unit": "TFLOP/s", "peak": PEAK_VALU_F32_TFLOPS,
-                      "candidate_evals_per_launch": ev_launch,
-                      "achieved": FLOP_PER_EVAL * ev_launch / avg_s / 1e12,
-                      "hbm_gbs_algorithmic": w["bytes"] / lps / avg_s / 1e9})
-        elif "flop" in w:
-            k.update({"bound": "mfma", "unit": "TFLOP/s", "peak": PEAK_MFMA_F32_TFLOPS,
-                      "flop_per_launch": w["flop"] / lps, "achieved": w["flop"] / lps / avg_s / 1e12})
-        elif "bytes" in w:
-            k.update({"bound": "hbm", "unit": "GB/s", "peak": PEAK_HBM_GBS,
-                      "bytes_per_launch": w["bytes"] / lps, "achieved": w["bytes"] / lps / avg_s / 1e9})
-        if "achieved" in k:
-            k["frac"] = k["achieved"] / k["peak"]
-        k["hbm_bytes_per_launch_measured"] = measured_traffic(name)
-        kernels[name] = k
+    def kernel_table(launches, nsteps):
+        per = {}
+        for name, ms in launches:
+            p = per.setdefault(name, [0, 0.0])
+            p[0] += 1
+            p[1] += ms
+        kernels = {}
+        for name, (cnt, tot) in per.items():
+            avg_s = tot / cnt * 1e-3
+            k = {"stage": stage_of(name), "launches_per_step": cnt / nsteps,
+                 "avg_us": tot / cnt * 1e3, "us_per_step": tot / nsteps * 1e3}
+            w = work.get(name, {})
+            lps = cnt / nsteps
+            if "evals" in w:
+                ev_launch = w["evals"] / lps
+                k.update({"bound": "alu", "unit": "TFLOP/s", "peak": PEAK_VALU_F32_TFLOPS,
+                          "candidate_evals_per_launch": ev_launch,
+                          "achieved": FLOP_PER_EVAL * ev_launch / avg_s / 1e12,
+                          "hbm_gbs_algorithmic": w["bytes"] / lps / avg_s / 1e9})
+            elif "flop" in w:
+                k.update({"bound": "mfma", "unit": "TFLOP/s", "peak": PEAK_MFMA_F32_TFLOPS,
+                          "flop_per_launch": w["flop"] / lps, "achieved": w["flop"] / lps / avg_s / 1e12})
+            elif "bytes" in w:
+                k.update({"bound": "hbm", "unit": "GB/s", "peak": PEAK_HBM_GBS,
+                          "bytes_per_launch": w["bytes"] / lps, "achieved": w["bytes"] / lps / avg_s / 1e9})
+            if "achieved" in k:
+                k["frac"] = k["achieved"] / k["peak"]
+            k["hbm_bytes_per_launch_measured"] = measured_traffic(name)
+            kernels[name] = k
+        return kernels
+
+    # profile step (untimed): every launch between HIP events, to rank the
+    # kernels; then the timed steps carry events around the dominant kernel
+    # only, so the instrumentation barely touches the timed region
+    mpq.timing_only(None)
+    mpq.timing_enable(True)
+    step()
+    torch.cuda.synchronize()
+    kernels = kernel_table(mpq.timing_read(), 1)
+    mpq.timing_enable(False)
+    for k in kernels.values():
+        k["timed_in"] = "profile step"
+    dom = max((k for k in kernels if "achieved" in kernels[k]), key=lambda k: kernels[k]["us_per_step"])
+
+    nl = len(Ws)
+    ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4)) for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    mpq.timing_only(dom)
+    mpq.timing_enable(True)
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for s in range(args.steps):
+        step(ev[s])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    launches = mpq.timing_read()
+    mpq.timing_enable(False)
+    mpq.timing_only(None)
+    ms_total = t_start.elapsed_time(t_end)
+    ms_step = ms_total / args.steps
+    steps = args.steps
+    kernels[dom] = kernel_table(launches, steps)[dom]
+    kernels[dom]["timed_in"] = "timed region"
     stages = {}
     if separate:
         for i, st in enumerate(("fit", "output_error", "reconstruct")):
             stages[st] = sum(e[i].elapsed_time(e[i + 1]) for e in ev) / steps
-    dom = max((k for k in kernels if "achieved" in kernels[k]), key=lambda k: kernels[k]["us_per_step"])
     K = kernels[dom]
     roofline = {"kernel": dom, "bound": K["bound"], "achieved": round(K["achieved"], 4),
                 "peak": K["peak"], "unit": K["unit"], "frac": round(K["frac"], 5),

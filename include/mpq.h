@@ -374,6 +374,11 @@ int mpq_integer_forward_layers(const mpq_int_layer *layers, int n_layers, int ma
  *
  * mpq_timing_enable(on): drops the records collected so far and turns the
  *   recording on (on != 0) or off.  Returns MPQ_OK.
+ * mpq_timing_only(name): while the recording is on, record only the
+ *   launches of the kernel of this name (a HOST string of up to 63 bytes, as
+ *   mpq_timing_read reports it), so that timing one kernel adds no events
+ *   around the others; NULL or "" records every launch again.  Returns MPQ_OK,
+ *   or MPQ_ERR_INVALID_ARG for a longer name.
  * mpq_timing_read(out, cap): waits for the recorded events, writes up to cap
  *   records (HOST array) in launch order and returns the number of records
  *   (which may exceed cap), or MPQ_ERR_INVALID_ARG.  ms is -1 for a record
@@ -389,6 +394,7 @@ typedef struct mpq_kernel_time {
 } mpq_kernel_time;
 
 int mpq_timing_enable(int on);
+int mpq_timing_only(const char *name);
 int mpq_timing_read(mpq_kernel_time *out, int cap);
 int mpq_fit_kernel_of(int64_t d, int bits, int n_grid, int default_grid, char *name, int cap);
 

@@ -1,5 +1,6 @@
-// Optional per-launch timing (mpq_timing_enable / mpq_timing_read): while it
-// is on, every kernel launch of the library is bracketed by two events
+// Optional per-launch timing (mpq_timing_enable / mpq_timing_only /
+// mpq_timing_read): while it is on, every kernel launch of the library (or
+// of the one kernel mpq_timing_only names) is bracketed by two events
 // recorded on the stream the kernel is launched on, so a kernel that runs on
 // one of the library's own streams is timed there.  Off by default; then a
 // LaunchTimer does nothing.
@@ -26,6 +27,7 @@ struct Record {
 constexpr size_t kTimingEventPool = 1024;
 std::atomic<bool> g_on{false};
 std::mutex g_mu;
+std::string g_only;               // record only this kernel ("" = every kernel)
 std::vector<Record> g_records;
 std::vector<hipEvent_t> g_free;   // events for reuse
 
@@ -47,6 +49,7 @@ LaunchTimer::LaunchTimer(hipStream_t s, const char *name) : s_(s), start_(nullpt
 {
     if (!g_on.load(std::memory_order_relaxed)) return;
     std::lock_guard<std::mutex> lk(g_mu);
+    if (!g_only.empty() && g_only != name) return;
     start_ = take_event();
     if (start_ && hipEventRecord(start_, s) != hipSuccess) {
         g_free.push_back(start_);
@@ -88,6 +91,14 @@ int mpq_timing_enable(int on)
         mpq::g_free.push_back(e);
     }
     mpq::g_on.store(on != 0);
+    return MPQ_OK;
+}
+
+int mpq_timing_only(const char *name)
+{
+    if (name && strlen(name) >= sizeof(((mpq_kernel_time *)nullptr)->name)) return MPQ_ERR_INVALID_ARG;
+    std::lock_guard<std::mutex> lk(mpq::g_mu);
+    mpq::g_only = name ? name : "";
     return MPQ_OK;
 }
 

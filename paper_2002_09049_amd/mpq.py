@@ -30,7 +30,7 @@ MAX_GRID = 4096
 
 EXPORTS = ("mpq_fit_layer", "mpq_fit_layer_dense", "mpq_fit_layers", "mpq_fit_max_dim",
            "mpq_output_error", "mpq_output_error_layers", "mpq_reconstruct",
-           "mpq_reconstruct_layers", "mpq_last_error", "mpq_timing_enable", "mpq_timing_read",
+           "mpq_reconstruct_layers", "mpq_last_error", "mpq_timing_enable", "mpq_timing_only", "mpq_timing_read",
            "mpq_fit_kernel_of", "mpq_quantize_layers", "mpq_fit_layer_calib",
            "mpq_fit_layers_calib", "mpq_integer_scales", "mpq_integer_forward",
            "mpq_integer_forward_layers", "mpq_fit_layers_ex")
@@ -118,6 +118,8 @@ def load(path: str = LIB_PATH):
     lib.mpq_last_error.restype = ctypes.c_char_p
     lib.mpq_timing_enable.argtypes = [i32]
     lib.mpq_timing_enable.restype = i32
+    lib.mpq_timing_only.argtypes = [ctypes.c_char_p]
+    lib.mpq_timing_only.restype = i32
     lib.mpq_timing_read.argtypes = [P, i32]
     lib.mpq_timing_read.restype = i32
     lib.mpq_fit_kernel_of.argtypes = [i64, i32, i32, i32, ctypes.c_char_p, i32]
@@ -316,6 +318,12 @@ def timing_enable(on: bool = True):
     """mpq_timing_enable: drop earlier records; record (or stop recording)
     HIP events around every kernel launch, on the launch's own stream."""
     _check(load().mpq_timing_enable(1 if on else 0))
+
+
+def timing_only(name=None):
+    """mpq_timing_only: time only the launches of the kernel ``name`` (None:
+    every launch)."""
+    _check(load().mpq_timing_only(None if name is None else name.encode()))
 
 
 def timing_read():

@@ -164,6 +164,9 @@ def test_timing_records_nothing_until_a_launch(lib):
     assert lib.mpq_timing_read(None, -1) == mpq.MPQ_ERR_INVALID_ARG
     assert lib.mpq_timing_enable(0) == 0
     assert mpq.timing_read() == []
+    assert lib.mpq_timing_only(b"x" * 64) == mpq.MPQ_ERR_INVALID_ARG
+    assert lib.mpq_timing_only(b"gemm_err_kernel") == 0
+    assert lib.mpq_timing_only(None) == 0
     assert lib.mpq_fit_kernel_of(0, 4, 8, 1, ctypes.create_string_buffer(64), 64) == mpq.MPQ_ERR_INVALID_ARG
 
 

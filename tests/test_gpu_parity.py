@@ -406,3 +406,30 @@ def test_quantize_layers_equals_the_three_calls(name):
             assert (q.W_hat[j] == -7.0).all()
         else:
             assert torch.equal(ref.W_hat[j], q.W_hat[j]), j
+
+
+def test_timing_only_records_the_named_kernel():
+    """mpq_timing_only: with the recording on, only the named kernel's
+    launches carry events (and positive durations); None records every
+    launch again."""
+    import torch
+    from paper_2002_09049_amd import mpq
+    w = wl.get("conv64x576")
+    W = to_dev(wl.layer_weights(w, 0))
+    X = to_dev(wl.layer_calib(w, 0))
+    ls = mpq.LayerSet([W], w.max_points, calib=[X])
+    say("case timing_only")
+    mpq.timing_only("reconstruct_kernel")
+    mpq.timing_enable(True)
+    ls.quantize(w.bits, w.n_grid, w.tol)
+    torch.cuda.synchronize()
+    rec = mpq.timing_read()
+    mpq.timing_enable(False)
+    assert rec and all(n == "reconstruct_kernel" and ms > 0 for n, ms in rec)
+    mpq.timing_only(None)
+    mpq.timing_enable(True)
+    ls.quantize(w.bits, w.n_grid, w.tol)
+    torch.cuda.synchronize()
+    names = {n for n, _ in mpq.timing_read()}
+    mpq.timing_enable(False)
+    assert {"reconstruct_kernel", "gemm_err_kernel", "form_dt_kernel"} <= names
