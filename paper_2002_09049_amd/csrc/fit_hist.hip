@@ -190,7 +190,7 @@ __device__ __forceinline__ void bin_levels_elementwise(Res r, const HistShared &
 // z = x inv is x / u within relative 2^-51, and N = rint(z).  The boundaries
 // at lattice point N lie within N 2^-23 of N (in units of u; a_g carries one
 // fp32 rounding of m c_g / M, relative 2^-23 with c_g's), the others at least
-// 1 - 4096 2^-23 from x / u.  So |z - N| > N 2^-21 (a 4x margin) puts x / u
+// 1 - 4096 2^-23 from x / u.  So |z - N| > N 2^-22 (a 2x margin) puts x / u
 // on N's side of every boundary at N, and the element crosses exactly the
 // boundaries at L <= floor(z); otherwise it crosses every boundary below N
 // (bucket N - 1) and those at N are decided one by one.  The tolerance grows
@@ -210,7 +210,7 @@ __device__ __forceinline__ void bin_lattice(Res r, const HistShared &S, int G, i
         const double z = x * inv;
         const double Nd = rint(z);
         const int Ni = (int)Nd;
-        const bool near = Ni >= 1 && fabs(z - Nd) <= Nd * 0x1p-21;
+        const bool near = Ni >= 1 && fabs(z - Nd) <= Nd * 0x1p-22;
         const int b = near ? Ni - 1 : (z >= Nd ? Ni : Ni - 1);
         const unsigned long long word =
             (unsigned long long)__double_as_longlong(fma(x, scale, kBias)) & ((1ull << 52) - 1);
@@ -220,7 +220,9 @@ __device__ __forceinline__ void bin_lattice(Res r, const HistShared &S, int G, i
             const unsigned long long X = word - kLatOne;
             for (int kk = 0; kk < M; ++kk) {
                 const int o = 2 * kk + 1;
-                const int q = Ni / o;
+                // N / o rounded from fp32 (N < 2^12, o < 2^8): exact when o
+                // divides N, and q o == N tells whether it does
+                const int q = (int)rintf((float)Ni * __builtin_amdgcn_rcpf((float)o));
                 if (q < 1) break;
                 if (q * o != Ni || q > G) continue;
                 const int g = q - 1;
@@ -385,11 +387,22 @@ fit_hist_kernel(const HistBatch B)
         int8_t *qrow = qk + (int64_t)(i - 1) * d;
         const double ap = (double)apend;
         const double ia = 1.0 / ap;
-        // code of Eq. (10) at the searched scale: y is within |y| 2^-51 of
-        // the fp64 quotient fl(r / a), so the two round to the same integer
-        // unless y lies within 2^-40 of a half-integer (or |y| >= 2^10, where
-        // both clip to the same M); only then is the quotient formed
+        // code of Eq. (10) at the searched scale.  First in fp32: with
+        // 2^-100 <= a <= 2^100, y32 = fl32(r) fl32(1 / a) is within |y| 3 2^-24 of
+        // r / a, under 2^-12 for |y| < 2^10 (larger quotients clip to the
+        // same M either way), so unless y32 lies within 2^-12 of a
+        // half-integer it rounds as r / a does.  Else in fp64: y is within
+        // |y| 2^-51 of the fp64 quotient fl(r / a), and only within 2^-40 of
+        // a half-integer is the quotient formed.
+        const bool fast = ap >= 0x1p-100 && ap <= 0x1p100;   // 1 / a a normal fp32
+        const float ia32 = (float)ia;
+        const float Mf = (float)M;
         auto code_of = [&](double ru) {
+            if (fast) {
+                const float y32 = (float)ru * ia32;
+                const float c32 = rintf(y32);
+                if (fabsf(fabsf(y32 - c32) - 0.5f) > 0x1p-12f) return (double)fminf(fmaxf(c32, -Mf), Mf);
+            }
             const double y = ru * ia;
             double c = rint(y);
             if (fabs(fabs(y - c) - 0.5) < 0x1p-40) c = rint(ru / ap);
@@ -434,7 +447,9 @@ fit_hist_kernel(const HistBatch B)
             lmax = fmaxf(lmax, fabsf((float)ru));
             lsum = fma(ru, ru, lsum);
         }
-        block_max_sum<T>(lmax, lsum, s_redf, s_redd);   // also orders S.c before use
+        // also orders S.c before use; no trailing barrier: the scratch is next
+        // written after the setup barrier below
+        block_max_sum<T, false>(lmax, lsum, s_redf, s_redd);
         const float m = lmax;
         const double Er = lsum;
 
@@ -533,7 +548,8 @@ fit_hist_kernel(const HistBatch B)
                 S.bnd[g] = b;
                 if (e < best.e || (e == best.e && g < best.g)) best = ArgMin{e, g};
             }
-            best = block_argmin<T>(best, s_arg);   // its barriers publish S.e, S.bnd
+            // its barrier publishes S.e, S.bnd; s_arg is next written a step later
+            best = block_argmin<T, false>(best, s_arg);
         } else {
             // ---- histograms of the level boundaries (bin_levels)
             unsigned long long fullA = 0;
@@ -663,7 +679,11 @@ fit_hist_kernel(const HistBatch B)
             Ly.scales[k * P + i] = apend;
             s_scale[i] = apend;
         }
-        __syncthreads();   // S.a is rewritten by the next step
+        // the next step rewrites S.ad only after its first barrier; this one
+        // is needed when the finalists' reductions used s_redd, which the next
+        // step's first reduction writes, or when the rebuilt residual reads
+        // s_scale[i]
+        if (kGlobal || nfin > 1) __syncthreads();
     }
 
     if (t == 0) Ly.counts[k] = n;

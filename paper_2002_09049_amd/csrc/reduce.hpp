@@ -201,8 +201,10 @@ __device__ __forceinline__ T block_reduce(T v, Op op, T *scratch)
 }
 
 // max of a float and sum of a double over the workgroup, with one pair of
-// barriers.  scratch_f / scratch_d hold one value per wavefront.
-template <int kThreads>
+// barriers (kTrail = false: the first barrier only; the caller then passes
+// another barrier before scratch_f / scratch_d are written again).
+// scratch_f / scratch_d hold one value per wavefront.
+template <int kThreads, bool kTrail = true>
 __device__ __forceinline__ void block_max_sum(float &vmax, double &vsum, float *scratch_f,
                                               double *scratch_d)
 {
@@ -225,7 +227,7 @@ __device__ __forceinline__ void block_max_sum(float &vmax, double &vsum, float *
             m = MaxOp()(m, scratch_f[i]);
             sm = SumOp()(sm, scratch_d[i]);
         }
-        __syncthreads();
+        if constexpr (kTrail) __syncthreads();
         vmax = m;
         vsum = sm;
     }
@@ -258,7 +260,8 @@ __device__ __forceinline__ void block_sum2(double &a, double &b, double *scratch
     }
 }
 
-template <int kThreads>
+// kTrail = false: the first barrier only (as block_max_sum)
+template <int kThreads, bool kTrail = true>
 __device__ __forceinline__ ArgMin block_argmin(ArgMin v, ArgMin *scratch)
 {
     constexpr int kWaves = kThreads / kWave;
@@ -269,7 +272,7 @@ __device__ __forceinline__ ArgMin block_argmin(ArgMin v, ArgMin *scratch)
     ArgMin r = scratch[0];
 #pragma unroll
     for (int i = 1; i < kWaves; ++i) r = argmin_combine(r, scratch[i]);
-    __syncthreads();
+    if constexpr (kTrail) __syncthreads();
     return r;
 }
 
