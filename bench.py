@@ -101,8 +101,9 @@ def parse():
                     help="with --summarize-trace: the bench.py line of an untraced run of the "
                          "same build, compared kernel by kernel")
     ap.add_argument("--traced-steps", type=int, default=None,
-                    help="with --summarize-*: steps the traced process ran (warm-up + timed; "
-                         "default 2 for --summarize-pmc, 6 for --summarize-trace)")
+                    help="with --summarize-*: steps the traced process ran (warm-up, profile "
+                         "step and timed; default 3 for --summarize-pmc, 7 for --summarize-trace, "
+                         "6 with --deploy, which has no profile step)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before the steps, copy a 256 MiB device buffer once (a kernel of known "
                          "traffic, to scale the FETCH_SIZE / WRITE_SIZE counters)")
@@ -144,7 +145,7 @@ def stage_of(key):
     return None
 
 
-def summarize_pmc(fetch_dir, write_dir, steps=2):
+def summarize_pmc(fetch_dir, write_dir, steps=3):
     """HBM bytes per step and kernel from the FETCH_SIZE / WRITE_SIZE counters,
     each scaled so that the 256 MiB calibration copy reads / writes 256 MiB."""
     import csv
@@ -206,7 +207,7 @@ def measured_traffic(key):
     return None
 
 
-def summarize_trace(trace_dir, bench_json=None, steps=6, rule="tol"):
+def summarize_trace(trace_dir, bench_json=None, steps=7, rule="tol"):
     """Per-kernel average duration of a traced bench run (kernel_stats.csv of
     rocprofv3 --stats), beside the event-timed averages of a bench.py line."""
     import csv
@@ -246,7 +247,7 @@ def summarize_trace(trace_dir, bench_json=None, steps=6, rule="tol"):
              f"python3 bench.py{r} --steps 5 --warmup 1 > gpurun_out/bench.json",
              f"python3 bench.py{r} --summarize-trace gpurun_out/prof --bench-json gpurun_out/bench.json",
              "```", "",
-             f"The traced process ran {steps} steps (warm-up + timed).  Kernels of one stage may",
+             f"The traced process ran {steps} steps (warm-up, profile step, timed).  Kernels of one stage may",
              "run concurrently on several streams.  `bench avg us` is the untraced run's average",
              "per launch, timed by HIP events on the launch's own stream.", "",
              "| kernel | stage | launches/step | avg us (rocprofv3) | bench avg us | us/step |",
@@ -268,10 +269,11 @@ def summarize_trace(trace_dir, bench_json=None, steps=6, rule="tol"):
 def main():
     args = parse()
     if args.summarize_pmc:
-        summarize_pmc(*args.summarize_pmc, steps=args.traced_steps or 2)
+        summarize_pmc(*args.summarize_pmc, steps=args.traced_steps or 3)
         return 0
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace, args.bench_json, steps=args.traced_steps or 6,
+        summarize_trace(args.summarize_trace, args.bench_json,
+                        steps=args.traced_steps or (6 if args.deploy else 7),
                         rule="deploy" if args.deploy else args.rule)
         return 0
     if args.gpus != 1:
