@@ -41,7 +41,8 @@
 // The tiles of all layers form one grid, longest K range first.  Workgroups
 // are dealt to the 8 XCDs in turn, so within a layer the tiles are
 // renumbered to give each XCD a contiguous run (rows of D and columns of X
-// reused by neighbouring tiles stay in one L2).  Tile coordinates come from
+// reused by neighbouring tiles stay in one L2), and a layer's tiles % 8
+// spare tiles go to the XCDs after those that took the previous layer's.  Tile coordinates come from
 // uniform subtraction loops, not divisions, so they and the buffer resources
 // built from them stay in scalar registers.
 #include <algorithm>
@@ -92,18 +93,19 @@ struct ErrLayer {
     float *ypart;        // [splits][C][n] (splits > 1)
     const int32_t *rows; // nullptr, or the channels of rows 0 .. *nrows of D
     const int32_t *nrows;
+    const float *cand;   // use_points == 2: [C / Gc][Gc] candidate scales (C counts rows of D)
+    const float *offsets;   // use_points == 1: per-channel offsets (reading B2) or nullptr
     int64_t stride;      // out[channel * stride]
     int C, d, n, ldc;
     int ntm, ntn, splits, kchunk;
     int tiles;           // ntm * ntn * splits
     int block_begin;     // first gemm workgroup (a multiple of kXcds)
+    int xoff;            // XCD rank offset: the layer's spare tiles go to XCDs xoff, xoff + 1, ...
     int form_begin;      // first form workgroup
     int form_kt;         // form tiles along k: ceil(d / kFT)
     int fin_begin;       // first finish workgroup
     int use_points;      // 1: D = residual (err), 0: D = W (ref), 2: D = clipping candidates
-    const float *cand;   // use_points == 2: [C / Gc][Gc] candidate scales (C counts rows of D)
     int Gc, M;
-    const float *offsets;   // use_points == 1: per-channel offsets (reading B2) or nullptr
     int vecw;            // d % 4 == 0, W 16-byte and codes 4-byte aligned
 };
 
@@ -229,8 +231,9 @@ gemm_err_kernel(const ErrGroup g)
     const int b = (int)blockIdx.x - L.block_begin;
     const int xcd = b % kXcds, slot = b / kXcds;
     const int q = L.tiles / kXcds, rem = L.tiles % kXcds;
-    if (slot >= q + (xcd < rem ? 1 : 0)) return;   // padding block
-    int tn = xcd * q + min(xcd, rem) + slot;
+    const int xr = (xcd - L.xoff + kXcds) % kXcds;   // the XCD's rank for this layer
+    if (slot >= q + (xr < rem ? 1 : 0)) return;   // padding block
+    int tn = xr * q + min(xr, rem) + slot;
     // (split, tm, tn) of the tile, split-major
     int split = 0, tm = 0;
     const int per_split = L.ntm * L.ntn;
@@ -548,6 +551,7 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
         g.P = P;
         g.vecx = 1;
         int64_t blocks = 0, fblocks = 0, nblocks = 0;
+        int xoff = 0;
         for (int o = 0; o < cnt; ++o) {
             const int i = order[o];
             const ErrLayerIn &I = *grp[i].in;
@@ -584,6 +588,10 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
             L.tiles = (int)(q.ntm * q.ntn * q.splits);
             L.block_begin = (int)blocks;
             blocks += (L.tiles + kXcds - 1) / kXcds * kXcds;
+            // the spare tiles (tiles % kXcds) of successive layers go to
+            // successive XCDs, so no XCD collects one from every layer
+            L.xoff = xoff;
+            xoff = (xoff + L.tiles % kXcds) % kXcds;
             L.form_kt = (int)((I.d + kFT - 1) / kFT);
             L.form_begin = (int)fblocks;
             fblocks += (int64_t)L.form_kt * ((L.C + kFT - 1) / kFT);
