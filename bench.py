@@ -102,8 +102,8 @@ def parse():
                          "same build, compared kernel by kernel")
     ap.add_argument("--traced-steps", type=int, default=None,
                     help="with --summarize-*: steps the traced process ran (warm-up, profile "
-                         "step and timed; default 3 for --summarize-pmc, 7 for --summarize-trace, "
-                         "6 with --deploy, which has no profile step)")
+                         "step and timed; default 3 for --summarize-pmc; for --summarize-trace "
+                         "those of the --bench-json line, which has no profile step with --deploy)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before the steps, copy a 256 MiB device buffer once (a kernel of known "
                          "traffic, to scale the FETCH_SIZE / WRITE_SIZE counters)")
@@ -207,9 +207,11 @@ def measured_traffic(key):
     return None
 
 
-def summarize_trace(trace_dir, bench_json=None, steps=7, rule="tol"):
+def summarize_trace(trace_dir, bench_json=None, steps=None, rule="tol"):
     """Per-kernel average duration of a traced bench run (kernel_stats.csv of
-    rocprofv3 --stats), beside the event-timed averages of a bench.py line."""
+    rocprofv3 --stats), beside the event-timed averages of a bench.py line
+    whose --steps / --warmup the traced run used too (steps: the steps the
+    traced run held, by default those of the bench line)."""
     import csv
     import glob
 
@@ -228,6 +230,9 @@ def summarize_trace(trace_dir, bench_json=None, steps=7, rule="tol"):
         a[0] += int(r["Calls"])
         a[1] += float(r["TotalDurationNs"])
     bench = json.load(open(bench_json)) if bench_json else None
+    K, W = (bench["steps"], bench["warmup"]) if bench else (5, 1)
+    if steps is None:
+        steps = W + K + (0 if rule == "deploy" else 1)   # deploy has no profile step
     calib = rule == "calib"
     r = {"calib": " --rule calib", "deploy": " --deploy"}.get(rule, "")
     what = {"calib": "the fit with Algorithm 2's stopping rule on each layer's calibration batch (one point\n"
@@ -243,11 +248,12 @@ def summarize_trace(trace_dir, bench_json=None, steps=7, rule="tol"):
              what, "",
              "Commands (one MI355X, from the repository root):", "", "```",
              "rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof -o kt -- \\",
-             f"    python3 bench.py{r} --steps 5 --warmup 1" + ("" if rule == "deploy" else " --no-cpu-baseline"),
-             f"python3 bench.py{r} --steps 5 --warmup 1 > gpurun_out/bench.json",
+             f"    python3 bench.py{r} --steps {K} --warmup {W}" + ("" if rule == "deploy" else " --no-cpu-baseline"),
+             f"python3 bench.py{r} --steps {K} --warmup {W} > gpurun_out/bench.json",
              f"python3 bench.py{r} --summarize-trace gpurun_out/prof --bench-json gpurun_out/bench.json",
              "```", "",
-             f"The traced process ran {steps} steps (warm-up, profile step, timed).  Kernels of one stage may",
+             f"The traced process ran {steps} steps ({W} warm-up" + ("" if rule == "deploy" else ", 1 profile")
+             + f", {K} timed).  Kernels of one stage may",
              "run concurrently on several streams.  `bench avg us` is the untraced run's average",
              "per launch, timed by HIP events on the launch's own stream.", "",
              "| kernel | stage | launches/step | avg us (rocprofv3) | bench avg us | us/step |",
@@ -272,8 +278,7 @@ def main():
         summarize_pmc(*args.summarize_pmc, steps=args.traced_steps or 3)
         return 0
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace, args.bench_json,
-                        steps=args.traced_steps or (6 if args.deploy else 7),
+        summarize_trace(args.summarize_trace, args.bench_json, steps=args.traced_steps,
                         rule="deploy" if args.deploy else args.rule)
         return 0
     if args.gpus != 1:

@@ -238,7 +238,7 @@ def _gpu_err(W, out, X, with_ref=True):
 
 
 @pytest.mark.parametrize("C,d,n", [(1, 1, 1), (130, 147, 300), (64, 576, 256), (257, 64, 129),
-                                   (40, 2305, 1024)])
+                                   (40, 2305, 1024), (33, 1600, 77), (5, 4608, 3), (1000, 512, 130)])
 def test_output_error_and_reconstruct(orc, C, d, n):
     say(f"case output error C={C} d={d} n={n}")
     W = wl.random_weights(C, d, seed=C + d)
