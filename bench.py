@@ -111,13 +111,18 @@ def parse():
 
 
 def sources_digest():
-    """sha256 of the HIP sources, to tell whether stored counters still apply."""
+    """sha256 of the HIP sources without their comments and blank space, to
+    tell whether stored counters still apply to the kernels."""
     import glob
     import hashlib
+    import re
     h = hashlib.sha256()
     for f in sorted(glob.glob(os.path.join(ROOT, "paper_2002_09049_amd", "csrc", "*"))):
-        with open(f, "rb") as fh:
-            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+        with open(f, encoding="utf-8") as fh:
+            code = re.sub(r"/\*.*?\*/", " ", fh.read(), flags=re.S)
+        code = re.sub(r"//[^\n]*", " ", code)
+        code = " ".join(code.split())
+        h.update(os.path.basename(f).encode() + b"\0" + code.encode())
     return h.hexdigest()[:16]
 
 

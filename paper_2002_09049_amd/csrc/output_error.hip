@@ -19,11 +19,11 @@
 //     while the MFMAs consume one slab, the next waits in registers for its
 //     LDS buffer and the one after is in flight (buffer loads: offsets past a
 //     range read as zeros), so a load has two slabs of MFMA time to arrive.
-//     Two wavefronts per SIMD cover each other's LDS and barrier waits.
-//     The epilogue squares Y (fp64) and
-//     sums each row over the tile's columns into a partial per (column tile,
-//     row); a layer whose K is split (to balance a grid of long and short
-//     K ranges) stores its fp32 Y tiles per K range instead.
+//     Two workgroups per CU (four wavefronts per SIMD) cover each other's
+//     LDS and barrier waits.  The epilogue squares Y (fp64) and sums each row
+//     over the tile's columns into a partial per (column tile, row); a layer
+//     whose K is split (to balance a grid of long and short K ranges) stores
+//     its fp32 Y tiles per K range instead.
 //
 // An err item may be restricted to a device list of channels (rows of D =
 // the listed channels, in list order; the list length is read by each
@@ -42,9 +42,9 @@
 // are dealt to the 8 XCDs in turn, so within a layer the tiles are
 // renumbered to give each XCD a contiguous run (rows of D and columns of X
 // reused by neighbouring tiles stay in one L2), and a layer's tiles % 8
-// spare tiles go to the XCDs after those that took the previous layer's.  Tile coordinates come from
-// uniform subtraction loops, not divisions, so they and the buffer resources
-// built from them stay in scalar registers.
+// spare tiles go to the XCDs after those that took the previous layer's.
+// Tile coordinates come from uniform subtraction loops, not divisions, so
+// they and the buffer resources built from them stay in scalar registers.
 #include <algorithm>
 #include <vector>
 
