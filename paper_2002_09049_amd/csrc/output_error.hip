@@ -67,6 +67,7 @@ constexpr int kVec = kBK * kBM / kThreads / 4;   // float4 per thread and operan
 constexpr int kMaxErrLayers = 22;
 constexpr int kXcds = 8;         // MI355X: workgroups are dealt to 8 XCDs in turn
 constexpr int kFT = 64;          // form tile: 64 rows x 64 k
+constexpr int kFinRows = 256 / kWave;   // finish: rows of a split layer per workgroup
 
 // Raw buffer resource (gfx9 descriptor word 3: 32-bit dwords, no swizzle).
 // Loads at offsets >= num_records return zeros; kOob is past every range.
@@ -382,11 +383,10 @@ gemm_err_kernel(const ErrGroup g)
 
 // ---- 3. finish: per row, the sum over column tiles of the row partials
 // (256 rows per workgroup), or for a split layer the sum over K ranges of Y,
-// squared and summed over the columns (one workgroup per row); fixed order,
-// fp64, divided by n
+// squared and summed over the columns (one wavefront per row, four rows per
+// workgroup); fixed order, fp64, divided by n
 __global__ void __launch_bounds__(256) finish_err_kernel(const ErrGroup g)
 {
-    __shared__ double red[256 / kWave];
     int li = 0;
     while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].fin_begin) ++li;
     const ErrLayer &L = g.L[li];
@@ -404,13 +404,15 @@ __global__ void __launch_bounds__(256) finish_err_kernel(const ErrGroup g)
         }
         return;
     }
-    const int64_t k = b;
-    if (k >= nact) return;
+    // a split layer: one wavefront per row, four rows per workgroup
+    const int lane = (int)threadIdx.x % kWave;
+    const int64_t k = (int64_t)b * kFinRows + (int64_t)threadIdx.x / kWave;
+    if (k >= nact) return;   // uniform per wavefront
     double s = 0.0;
     if (g.vecx) {
-        // n % 4 == 0: four columns per thread and pass, the K ranges' loads
+        // n % 4 == 0: four columns per lane and pass, the K ranges' loads
         // of up to four ranges issued together
-        for (int64_t c = 4 * threadIdx.x; c < n; c += 4 * 256) {
+        for (int64_t c = 4 * lane; c < n; c += 4 * kWave) {
             f32x4 y = {0.0f, 0.0f, 0.0f, 0.0f};
             for (int sp0 = 0; sp0 < L.splits; sp0 += 4) {
                 f32x4 v[4];
@@ -426,14 +428,14 @@ __global__ void __launch_bounds__(256) finish_err_kernel(const ErrGroup g)
             for (int u = 0; u < 4; ++u) s = fma((double)y[u], (double)y[u], s);
         }
     } else {
-        for (int64_t c = threadIdx.x; c < n; c += 256) {
+        for (int64_t c = lane; c < n; c += kWave) {
             float y = 0.0f;
             for (int sp = 0; sp < L.splits; ++sp) y += L.ypart[((int64_t)sp * C + k) * n + c];
             s = fma((double)y, (double)y, s);
         }
     }
-    s = block_reduce<256>(s, SumOp(), red);
-    if (threadIdx.x == 0) L.out[slot(k)] = (float)(s / (double)n);
+    s = wave_reduce(s, SumOp());
+    if (lane == 0) L.out[slot(k)] = (float)(s / (double)n);
 }
 
 struct Item {
@@ -596,7 +598,7 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
             L.form_begin = (int)fblocks;
             fblocks += (int64_t)L.form_kt * ((L.C + kFT - 1) / kFT);
             L.fin_begin = (int)nblocks;
-            nblocks += q.splits > 1 ? L.C : (L.C + 255) / 256;
+            nblocks += q.splits > 1 ? (L.C + kFinRows - 1) / kFinRows : (L.C + 255) / 256;
             L.vecw = I.d % 4 == 0 && ((uintptr_t)I.W) % 16 == 0 && ((uintptr_t)I.codes) % 4 == 0;
             if (I.n % 4 != 0 || ((uintptr_t)I.X) % 16 != 0) g.vecx = 0;
         }
