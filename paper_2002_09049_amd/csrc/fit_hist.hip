@@ -297,6 +297,7 @@ fit_hist_kernel(const HistBatch B)
     __shared__ int s_fin[kMaxFinalists];
     __shared__ int s_nfin;
     __shared__ int s_gbest;
+    __shared__ int s_other;   // lattice mode: a candidate besides the best may be a finalist
     __shared__ unsigned long long s_scan[kWaves];
     __shared__ ArgMin s_arg[kWaves];
     __shared__ float s_scale[MPQ_MAX_POINTS];
@@ -490,6 +491,7 @@ fit_hist_kernel(const HistBatch B)
         if (lat)
             for (int b = t; b < nlat; b += T) S.lat[b] = 0;
         if (t == 0) {
+            s_other = 0;
             S.ad[0] = 0.0;
             S.ad[G + 1] = INFINITY;
             S.af[0] = 0.0f;
@@ -550,6 +552,15 @@ fit_hist_kernel(const HistBatch B)
             }
             // its barrier publishes S.e, S.bnd; s_arg is next written a step later
             best = block_argmin<T, false>(best, s_arg);
+            // another candidate whose interval reaches the best one's (rare)
+            // is flagged by its own thread, so that in the common case no
+            // wavefront scans the candidates again
+            const double thr0 = best.e == INFINITY ? INFINITY : best.e + S.bnd[best.g];
+            bool other = false;
+            for (int g = t; g < G; g += T)
+                other = other || (g != best.g && S.e[g] != INFINITY && S.e[g] - S.bnd[g] <= thr0);
+            if (other) s_other = 1;
+            __syncthreads();
         } else {
             // ---- histograms of the level boundaries (bin_levels)
             unsigned long long fullA = 0;
@@ -581,8 +592,9 @@ fit_hist_kernel(const HistBatch B)
         }
 
         // ---- wavefront 0: (histogram mode) suffix sums, candidate errors and
-        // bounds, argmin; then the finalists
-        if (t < kWave) {
+        // bounds, argmin; then the finalists (lattice mode: only when flagged)
+        const bool pick = !lat || s_other != 0;   // uniform
+        if (pick && t < kWave) {
             // lane l owns the l-th chunk from the top, so a prefix over lanes
             // is a suffix over candidates
             const int per = (G + kWave - 1) / kWave;
@@ -644,10 +656,10 @@ fit_hist_kernel(const HistBatch B)
                 if (t == 0) s_nfin = nf;
             }
         }
-        __syncthreads();
+        if (pick) __syncthreads();
 
-        int gstar = s_gbest;
-        const int nfin = s_nfin;
+        int gstar = pick ? s_gbest : (best.e == INFINITY ? -1 : best.g);
+        const int nfin = pick ? s_nfin : 1;
         if (gstar >= 0 && nfin > 1) {
             // direct fp64 evaluation of the finalists (Eq. (9) written out)
             ArgMin best{INFINITY, 0x7fffffff};
