@@ -61,6 +61,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBM = 128, kBN = 128, kBK = 32;
 constexpr int kRangeK = 768;      // K of a split layer's K range, about
+constexpr int kMinSlabs = 4;      // shortest K range (slabs) of a listed layer's live rows
 constexpr int kThreads = 512;   // GEMM workgroup: eight wavefronts, two per SIMD
 constexpr int kPad = 4;          // LDS row padding (floats); rows stay 16-byte aligned
 constexpr int kVec = kBK * kBM / kThreads / 4;   // float4 per thread and operand per slab
@@ -91,7 +92,7 @@ struct ErrLayer {
     float *out;          // err or ref
     float *Dt;           // [d][ldc]
     double *rowpart;     // [ntn][C]
-    float *ypart;        // [splits][C][n] (splits > 1)
+    float *ypart;        // [splits][rows][n] (a split layer's K ranges of Y)
     const int32_t *rows; // nullptr, or the channels of rows 0 .. *nrows of D
     const int32_t *nrows;
     const float *cand;   // use_points == 2: [C / Gc][Gc] candidate scales (C counts rows of D)
@@ -99,11 +100,11 @@ struct ErrLayer {
     int64_t stride;      // out[channel * stride]
     int C, d, n, ldc;
     int ntm, ntn, splits, kchunk;
-    int tiles;           // ntm * ntn * splits
+    int tiles;           // gemm workgroups: ntm * ntn * splits, more for a listed layer
     int block_begin;     // first gemm workgroup (a multiple of kXcds)
+    int extra_begin;     // first of the workgroups past the plan's tiles (a multiple of kXcds)
     int xoff;            // XCD rank offset: the layer's spare tiles go to XCDs xoff, xoff + 1, ...
     int form_begin;      // first form workgroup
-    int form_kt;         // form tiles along k: ceil(d / kFT)
     int fin_begin;       // first finish workgroup
     int use_points;      // 1: D = residual (err), 0: D = W (ref), 2: D = clipping candidates
     int Gc, M;
@@ -113,10 +114,31 @@ struct ErrLayer {
 struct ErrGroup {
     int n_layers;
     int P;
+    int extra_start;     // gemm workgroups past every layer's planned tiles start here
     int vecx;            // n % 4 == 0 and every X 16-byte aligned
     ErrLayer L[kMaxErrLayers];
 };
 static_assert(sizeof(ErrGroup) <= 4096, "kernel arguments");
+
+// The K split of the live rows 0 .. nact of D.  A layer's full rows take the
+// host's plan.  When a listed layer scores fewer rows (the later steps of the
+// calibration rule), its workgroups take shorter K ranges (at least
+// kMinSlabs slabs), so the few live rows still spread over the layer's
+// workgroups.  The split depends on the layer and nact alone; the GEMM and
+// the finish kernel derive it alike.
+struct LiveSplit {
+    int ntm, splits, kchunk;
+};
+__device__ __forceinline__ LiveSplit live_split(const ErrLayer &L, int64_t nact)
+{
+    const int ntm = (int)((nact + kBM - 1) / kBM);
+    if (!L.rows || nact >= L.C) return LiveSplit{L.ntm, L.splits, L.kchunk};
+    if (ntm == 0) return LiveSplit{0, 1, L.kchunk};
+    const int slabs = (L.d + kBK - 1) / kBK;
+    const int s = max(1, min(L.tiles / (ntm * L.ntn), slabs / kMinSlabs));
+    const int kch = min((slabs + s - 1) / s * kBK, L.kchunk);   // never above the plan's
+    return LiveSplit{ntm, (L.d + kch - 1) / kch, kch};
+}
 
 __device__ __forceinline__ double int8_of(uint32_t w, int u)
 {
@@ -131,9 +153,10 @@ __global__ void __launch_bounds__(256) form_dt_kernel(const ErrGroup g)
     int li = 0;
     while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].form_begin) ++li;
     const ErrLayer &L = g.L[li];
+    const int form_kt = (L.d + kFT - 1) / kFT;   // form tiles along k
     int kt = (int)blockIdx.x - L.form_begin, rt = 0;
-    while (kt >= L.form_kt) {
-        kt -= L.form_kt;
+    while (kt >= form_kt) {
+        kt -= form_kt;
         ++rt;
     }
     const int P = g.P;
@@ -224,20 +247,36 @@ gemm_err_kernel(const ErrGroup g)
     __shared__ __align__(16) float sX[2][kBK][kBN + kPad];
     __shared__ double sPart[kBN / 32][kBM];
 
+    // a layer's workgroups: the planned tiles' from block_begin, and any
+    // more (for the short K ranges of a listed layer's few live rows) from
+    // extra_begin, after every layer's planned ones
+    const bool extra = (int)blockIdx.x >= g.extra_start;
     int li = 0;
-    while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].block_begin) ++li;
+    if (!extra)
+        while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].block_begin) ++li;
+    else
+        while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].extra_begin) ++li;
     const ErrLayer &L = g.L[li];
-    // XCD-contiguous renumbering of this layer's tiles (block_begin is a
-    // multiple of kXcds, so b % kXcds is the XCD this block runs on)
-    const int b = (int)blockIdx.x - L.block_begin;
-    const int xcd = b % kXcds, slot = b / kXcds;
-    const int q = L.tiles / kXcds, rem = L.tiles % kXcds;
+    // the live tiles: (split, tm, tn) over the live row tiles, split-major
+    const int64_t nact = L.rows ? (int64_t)*L.nrows : (int64_t)L.C;
+    LiveSplit ls = live_split(L, nact);
+    // uniform values: keep them in scalar registers
+    ls.ntm = __builtin_amdgcn_readfirstlane(ls.ntm);
+    ls.splits = __builtin_amdgcn_readfirstlane(ls.splits);
+    ls.kchunk = __builtin_amdgcn_readfirstlane(ls.kchunk);
+    const int per_split = ls.ntm * L.ntn;
+    const int live = per_split * ls.splits;   // <= L.tiles
+    // XCD-contiguous renumbering of the live tiles (block_begin and
+    // extra_begin are multiples of kXcds, so b % kXcds is the XCD this block
+    // runs on); an XCD's slots continue from the planned region into the extra one
+    const int planned = (L.ntm * L.ntn * L.splits + kXcds - 1) / kXcds;   // slots per XCD
+    const int b = (int)blockIdx.x - (extra ? L.extra_begin : L.block_begin);
+    const int xcd = b % kXcds, slot = b / kXcds + (extra ? planned : 0);
+    const int q = live / kXcds, rem = live % kXcds;
     const int xr = (xcd - L.xoff + kXcds) % kXcds;   // the XCD's rank for this layer
     if (slot >= q + (xr < rem ? 1 : 0)) return;   // padding block
     int tn = xr * q + min(xr, rem) + slot;
-    // (split, tm, tn) of the tile, split-major
     int split = 0, tm = 0;
-    const int per_split = L.ntm * L.ntn;
     while (tn >= per_split) {
         tn -= per_split;
         ++split;
@@ -248,15 +287,14 @@ gemm_err_kernel(const ErrGroup g)
     }
 
     const int64_t row0 = (int64_t)tm * kBM;
-    if (L.rows && row0 >= (int64_t)*L.nrows) return;   // past the listed channels
 
     const int t = threadIdx.x;
     const int lane = t % kWave, wid = t / kWave;
     const int wm = wid / 4, wn = wid % 4;   // rows wm * 64 + [0, 64), columns wn * 32 + [0, 32)
     const int64_t C = L.C, n = L.n;
     const int64_t col0 = (int64_t)tn * kBN;
-    const int64_t kbeg = (int64_t)split * L.kchunk;
-    const int64_t kend = min(kbeg + (int64_t)L.kchunk, (int64_t)L.d);
+    const int64_t kbeg = (int64_t)split * ls.kchunk;
+    const int64_t kend = min(kbeg + (int64_t)ls.kchunk, (int64_t)L.d);
     const int nslab = (int)((kend - kbeg + kBK - 1) / kBK);
 
     // buffer resources over this K range's rows of Dt and X (below 2^31
@@ -351,15 +389,16 @@ gemm_err_kernel(const ErrGroup g)
     };
     const int64_t col = col0 + wn * 32 + lane % 32;
 
-    if (L.splits > 1) {
-        // this K range's Y tile; the finish kernel sums the ranges
+    if (ls.splits > 1) {
+        // this K range's Y tile (rows of stride nact); the finish kernel sums
+        // the ranges
         float *yp = L.ypart;
 #pragma unroll
         for (int a = 0; a < 2; ++a)
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int64_t r = row_of(a, v);
-                if (r < C && col < n) yp[((int64_t)split * C + r) * n + col] = acc[a][v];
+                if (r < nact && col < n) yp[((int64_t)split * nact + r) * n + col] = acc[a][v];
             }
         return;
     }
@@ -393,9 +432,10 @@ __global__ void __launch_bounds__(256) finish_err_kernel(const ErrGroup g)
     const int64_t C = L.C, n = L.n;
     const int b = (int)blockIdx.x - L.fin_begin;
     const int64_t nact = L.rows ? (int64_t)*L.nrows : C;
+    const int splits = live_split(L, nact).splits;
     // output slot of row m of D
     auto slot = [&](int64_t m) { return (L.rows ? (int64_t)L.rows[m] : m) * L.stride; };
-    if (L.splits == 1) {
+    if (splits == 1) {
         const int64_t k = (int64_t)b * 256 + threadIdx.x;
         if (k < nact) {
             double s = 0.0;
@@ -414,15 +454,15 @@ __global__ void __launch_bounds__(256) finish_err_kernel(const ErrGroup g)
         // of up to four ranges issued together
         for (int64_t c = 4 * lane; c < n; c += 4 * kWave) {
             f32x4 y = {0.0f, 0.0f, 0.0f, 0.0f};
-            for (int sp0 = 0; sp0 < L.splits; sp0 += 4) {
+            for (int sp0 = 0; sp0 < splits; sp0 += 4) {
                 f32x4 v[4];
 #pragma unroll
                 for (int z = 0; z < 4; ++z)
-                    if (sp0 + z < L.splits)
-                        v[z] = *(const f32x4 *)(L.ypart + ((int64_t)(sp0 + z) * C + k) * n + c);
+                    if (sp0 + z < splits)
+                        v[z] = *(const f32x4 *)(L.ypart + ((int64_t)(sp0 + z) * nact + k) * n + c);
 #pragma unroll
                 for (int z = 0; z < 4; ++z)
-                    if (sp0 + z < L.splits) y += v[z];
+                    if (sp0 + z < splits) y += v[z];
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u) s = fma((double)y[u], (double)y[u], s);
@@ -430,7 +470,7 @@ __global__ void __launch_bounds__(256) finish_err_kernel(const ErrGroup g)
     } else {
         for (int64_t c = lane; c < n; c += kWave) {
             float y = 0.0f;
-            for (int sp = 0; sp < L.splits; ++sp) y += L.ypart[((int64_t)sp * C + k) * n + c];
+            for (int sp = 0; sp < splits; ++sp) y += L.ypart[((int64_t)sp * nact + k) * n + c];
             s = fma((double)y, (double)y, s);
         }
     }
@@ -446,8 +486,12 @@ struct Item {
 // rows of D of an item: the channels, or their clipping candidates
 int64_t item_rows(const ErrLayerIn &I) { return I.cand ? I.C * I.Gc : I.C; }
 
+// an item whose rows are the first *nrows channels of a list
+bool listed(const ErrLayerIn &I, int use_points) { return use_points == 1 && I.rows; }
+
 struct Plan {
     int64_t ldc, ntm, ntn, splits, kchunk;
+    int64_t budget;   // splits of the workgroup budget (ntm * ntn * budget workgroups)
     size_t dt_bytes, rowpart_bytes, ypart_bytes;
 };
 
@@ -470,8 +514,10 @@ std::vector<Item> items_of(const ErrLayerIn *in, int n_in)
 // GEMM store fp32 Y tiles that the finish kernel reads back, so a layer of
 // short K stays whole: the other layers of a call fill the GPU.  The split
 // depends on the layer alone, so a layer's result does not depend on the
-// other layers of the call.
-Plan plan_item(const ErrLayerIn &I)
+// other layers of the call.  A listed layer gets workgroups for
+// ceil(slabs / kMinSlabs / ntm) K ranges if that is more, and Y room for
+// them, so live_split can spread a few live rows over shorter K ranges.
+Plan plan_item(const ErrLayerIn &I, bool list)
 {
     Plan q;
     const int64_t C = item_rows(I);
@@ -491,7 +537,15 @@ Plan plan_item(const ErrLayerIn &I)
     q.splits = (I.d + kchunk - 1) / kchunk;   // no empty K range
     q.dt_bytes = align256(sizeof(float) * (size_t)(I.d * q.ldc));
     q.rowpart_bytes = align256(sizeof(double) * (size_t)(q.ntn * C));
-    q.ypart_bytes = q.splits > 1 ? align256(sizeof(float) * (size_t)(q.splits * C * I.n)) : 0;
+    q.budget = q.splits;
+    if (list) {
+        const int64_t want = (slabs / kMinSlabs + q.ntm - 1) / q.ntm;
+        q.budget = std::max(q.splits, want);
+        // live_split: splits * nact <= budget * ntm * kBM rows of Y
+        q.ypart_bytes = align256(sizeof(float) * (size_t)(q.budget * q.ntm * kBM * I.n));
+    } else {
+        q.ypart_bytes = q.splits > 1 ? align256(sizeof(float) * (size_t)(q.splits * C * I.n)) : 0;
+    }
     return q;
 }
 
@@ -499,7 +553,7 @@ size_t group_bytes(const Item *it, int cnt)
 {
     size_t b = 0;
     for (int i = 0; i < cnt; ++i) {
-        const Plan q = plan_item(*it[i].in);
+        const Plan q = plan_item(*it[i].in, listed(*it[i].in, it[i].use_points));
         b += q.dt_bytes + q.rowpart_bytes + q.ypart_bytes;
     }
     return b;
@@ -541,7 +595,7 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
         const int cnt = (int)std::min<size_t>(kMaxErrLayers, it.size() - base);
         const Item *grp = it.data() + base;
         std::vector<Plan> p(cnt);
-        for (int i = 0; i < cnt; ++i) p[i] = plan_item(*grp[i].in);
+        for (int i = 0; i < cnt; ++i) p[i] = plan_item(*grp[i].in, listed(*grp[i].in, grp[i].use_points));
         // longest K ranges first
         std::vector<int> order(cnt);
         for (int i = 0; i < cnt; ++i) order[i] = i;
@@ -577,7 +631,7 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
             cur += q.dt_bytes;
             L.rowpart = (double *)cur;
             cur += q.rowpart_bytes;
-            L.ypart = q.splits > 1 ? (float *)cur : nullptr;
+            L.ypart = q.ypart_bytes ? (float *)cur : nullptr;
             cur += q.ypart_bytes;
             L.C = (int)item_rows(I);
             L.d = (int)I.d;
@@ -587,20 +641,32 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
             L.ntn = (int)q.ntn;
             L.splits = (int)q.splits;
             L.kchunk = (int)q.kchunk;
-            L.tiles = (int)(q.ntm * q.ntn * q.splits);
+            if (q.ntm * q.ntn * q.budget > 0x7fffffffLL) return hipErrorInvalidValue;
+            L.tiles = (int)(q.ntm * q.ntn * q.budget);
+            const int64_t planned = q.ntm * q.ntn * q.splits;
             L.block_begin = (int)blocks;
-            blocks += (L.tiles + kXcds - 1) / kXcds * kXcds;
-            // the spare tiles (tiles % kXcds) of successive layers go to
+            blocks += (planned + kXcds - 1) / kXcds * kXcds;
+            // the spare tiles (planned % kXcds) of successive layers go to
             // successive XCDs, so no XCD collects one from every layer
             L.xoff = xoff;
-            xoff = (xoff + L.tiles % kXcds) % kXcds;
-            L.form_kt = (int)((I.d + kFT - 1) / kFT);
+            xoff = (xoff + (int)(planned % kXcds)) % kXcds;
             L.form_begin = (int)fblocks;
-            fblocks += (int64_t)L.form_kt * ((L.C + kFT - 1) / kFT);
+            fblocks += (I.d + kFT - 1) / kFT * ((L.C + kFT - 1) / kFT);
             L.fin_begin = (int)nblocks;
-            nblocks += q.splits > 1 ? (L.C + kFinRows - 1) / kFinRows : (L.C + 255) / 256;
+            nblocks += q.ypart_bytes ? (L.C + kFinRows - 1) / kFinRows : (L.C + 255) / 256;
             L.vecw = I.d % 4 == 0 && ((uintptr_t)I.W) % 16 == 0 && ((uintptr_t)I.codes) % 4 == 0;
             if (I.n % 4 != 0 || ((uintptr_t)I.X) % 16 != 0) g.vecx = 0;
+        }
+        // the workgroup budget past the planned tiles, after every layer's
+        // planned ones: per XCD, ceil(tiles / kXcds) slots in all
+        if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+        g.extra_start = (int)blocks;
+        for (int o = 0; o < cnt; ++o) {
+            ErrLayer &L = g.L[o];
+            const int64_t planned = (int64_t)L.ntm * L.ntn * L.splits;
+            L.extra_begin = (int)blocks;
+            blocks += ((int64_t)L.tiles + kXcds - 1) / kXcds * kXcds -
+                      (planned + kXcds - 1) / kXcds * kXcds;
         }
         if (blocks > 0x7fffffffLL || fblocks > 0x7fffffffLL || nblocks > 0x7fffffffLL)
             return hipErrorInvalidValue;
