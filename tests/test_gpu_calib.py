@@ -56,6 +56,7 @@ CASES = [
     (20, 1000, 2, 6, 64, 200, 1e-2, True),
     (24, 2305, 4, 8, 256, 1024, 1e-4, True),
     (12, 4608, 4, 4, 256, 1024, 1e-3, True),
+    (300, 2304, 4, 4, 256, 256, 1e-3, True),   # several row tiles, fewer live each step
     (6, 9000, 3, 4, 64, 130, 1e-3, True),
     (40, 333, 4, 6, 64, 100, 0.0, False),
 ]
