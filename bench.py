@@ -51,7 +51,7 @@ FLOP_PER_EVAL = 7                       # scale-mul, round, clamp, fma (2), squa
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "resnet18_hbm_traffic.md")
 COPY_BYTES = 256 << 20
 STAGES = (("fit", ("fit_hist_kernel", "fit_dense_kernel")),
-          ("output_error", ("form_dt_kernel", "gemm_err_kernel", "finish_err_kernel")),
+          ("output_error", ("form_d_kernel", "gemm_err_kernel", "finish_err_kernel")),
           ("reconstruct", ("reconstruct_kernel",)),
           ("deploy", ("int_forward_kernel", "integer_scales_kernel")))
 
@@ -387,7 +387,7 @@ def main():
             searched = n - int((cnt > 0).sum()) if args.clip else n
             add(fk, evals=searched * wk.n_grid * d, bytes=4 * n * d + code_reads * d + n * d)
             add("gemm_err_kernel", flop=2 * (n + C) * d * N)
-            add("form_dt_kernel", bytes=8 * (n + C) * d + (n + code_reads) * d)
+            add("form_d_kernel", bytes=8 * (n + C) * d + (n + code_reads) * d)
         else:
             # fit: G candidate errors per (element, point); reads W once, writes the codes
             # (with --clip, point 1 comes from the clipping pass, not the search)
@@ -395,11 +395,11 @@ def main():
             add(fk, evals=searched * wk.n_grid * d, bytes=4 * C * d + n * d)
             add("gemm_err_kernel", flop=2 * C * d * N)
             # form: reads W and the codes of the used points, writes D
-            add("form_dt_kernel", bytes=4 * C * d + n * d + 4 * C * d)
+            add("form_d_kernel", bytes=4 * C * d + n * d + 4 * C * d)
         if args.clip:
             # the clipping pass: output errors of C * GC candidate rows
             add("gemm_err_kernel", flop=2 * C * args.clip * d * N)
-            add("form_dt_kernel", bytes=4 * C * d + 4 * C * args.clip * d)
+            add("form_d_kernel", bytes=4 * C * d + 4 * C * args.clip * d)
         # reconstruct: reads the codes of the used points, writes fp32
         add("reconstruct_kernel", bytes=n * d + 4 * C * d)
 

@@ -47,6 +47,7 @@ extern "C" {
 #define MPQ_MAX_POINTS 64
 #define MPQ_MAX_GRID 4096
 #define MPQ_MAX_ERR_DIM 16777216   /* c_out and n of mpq_output_error */
+#define MPQ_MAX_ERR_D 4194272      /* d of mpq_output_error (128 rows of the residual below 2 GiB) */
 #define MPQ_MAX_INT_DIM 131072     /* d of mpq_integer_forward */
 
 /*
@@ -139,7 +140,7 @@ int64_t mpq_fit_max_dim(int n_grid);
  *                              counts[k] in [0, max_points].
  *   c_out, d, max_points       as for mpq_fit_layer.
  *   X          [d][n] fp32 calibration inputs (input), n >= 1.
- *   c_out and n are at most MPQ_MAX_ERR_DIM.
+ *   c_out and n are at most MPQ_MAX_ERR_DIM, d at most MPQ_MAX_ERR_D.
  *   err        [c_out] fp32 (output).
  *   ref_opt    NULL or [c_out] fp32 (output).
  * Errors: MPQ_ERR_INVALID_ARG, MPQ_ERR_NOMEM, MPQ_ERR_HIP.

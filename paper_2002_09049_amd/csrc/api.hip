@@ -487,8 +487,8 @@ int check_error_layer(const mpq_layer &L, int max_points, bool need_x)
         if (L.n > MPQ_MAX_ERR_DIM || L.c_out > MPQ_MAX_ERR_DIM)
             return fail(MPQ_ERR_INVALID_ARG, "c_out and n must be <= %d (got %lld, %lld)",
                         MPQ_MAX_ERR_DIM, (long long)L.c_out, (long long)L.n);
-        if (L.d > 0x7fffffffLL)
-            return fail(MPQ_ERR_INVALID_ARG, "d too large (%lld)", (long long)L.d);
+        if (L.d > MPQ_MAX_ERR_D)
+            return fail(MPQ_ERR_INVALID_ARG, "d must be <= %d (got %lld)", MPQ_MAX_ERR_D, (long long)L.d);
     } else {
         if (L.c_out > 0 && (!L.codes || !L.scales || !L.counts || !L.W_hat))
             return fail(MPQ_ERR_INVALID_ARG, "codes, scales, counts and W_hat must not be NULL");
@@ -598,26 +598,20 @@ int quantize_impl(const mpq_layer *layers, int n_layers, int bits, int max_point
     rc = upload_grid(grid_host, n_grid, s, &dgrid);
     if (rc != MPQ_OK) return rc;
     const int M = (1 << (bits - 1)) - 1;
-    // 1. every fit, side by side (as mpq_fit_layers)
-    const std::vector<FitJob> jobs = build_fit_jobs(Search::kAuto, hist_fits, layers, n_layers, M,
-                                                    max_points, dgrid, n_grid, tol, -1.0);
-    std::vector<double> work;
-    for (const FitJob &j : jobs) work.push_back(j.work);
-    hipError_t e = run_concurrently(s, work, [&](int i, hipStream_t st) {
-        return launch_fit_job(jobs[i], n_grid, st);
-    });
-    if (dgrid) (void)mpq::scratch_free(dgrid, s);
-    if (e != hipSuccess) return hip_fail(e, "fit kernel launch");
-    // 2. the output error of every layer that asks for it, in its launch
-    // groups (a group's GEMM fills the device only with many layers' tiles),
-    // and beside them the reconstruction: both only read the fit's outputs
+    std::vector<FitJob> jobs = build_fit_jobs(Search::kAuto, hist_fits, layers, n_layers, M,
+                                              max_points, dgrid, n_grid, tol, -1.0);
+    // the output error of every layer that asks for it, in its launch groups
+    // (a group's GEMM fills the device only with many layers' tiles), and the
+    // reconstruction: both only read the fit's outputs
     std::vector<mpq::ErrLayerIn> err;
     std::vector<mpq::RecLayer> rec;
+    std::vector<int> err_of(n_layers, -1);
     double bytes = 0.0;
     for (int l = 0; l < n_layers; ++l) {
         const mpq_layer &L = layers[l];
         if (L.c_out == 0) continue;
         if (L.out_err) {
+            err_of[l] = (int)err.size();
             err.push_back(mpq::ErrLayerIn{L.W, L.codes, L.scales, L.counts, L.X, L.out_err, L.out_ref,
                                           L.c_out, L.d, L.n});
         }
@@ -629,9 +623,65 @@ int quantize_impl(const mpq_layer *layers, int n_layers, int bits, int max_point
     ErrJobs ej;
     if (!err.empty()) {
         rc = err_jobs(err, s, &ej);
-        if (rc != MPQ_OK) return rc;
+        if (rc != MPQ_OK) {
+            if (dgrid) (void)mpq::scratch_free(dgrid, s);
+            return rc;
+        }
     }
-    // the output error's launch groups (work in GEMM FLOP) and the
+    // a fit that keeps its residual in registers writes its layers' rows of
+    // D for the output error, which then forms none for them
+    for (FitJob &j : jobs) {
+        if (j.dense || !mpq::hist_variant_writes_d(j.variant)) continue;
+        for (int i = 0; i < j.b.n_layers; ++i) {
+            const int l = j.layers[i];
+            if (err_of[l] < 0) continue;
+            int grp = 0;
+            const int64_t off = mpq::err_item_d_offset(err.data(), (int)err.size(), err_of[l], &grp);
+            if (off < 0) continue;
+            j.b.L[i].dres = (float *)(ej.scratch + ej.off[grp] + off);
+            err[err_of[l]].d_ready = 1;
+        }
+    }
+    // The reconstruction of a fit launch's layers follows it on its stream,
+    // in the longest fit's shadow, but for the longest fit's own layers:
+    // theirs runs beside the output error.
+    int big = 0;
+    for (int i = 1; i < (int)jobs.size(); ++i)
+        if (jobs[i].work > jobs[big].work) big = i;
+    std::vector<std::vector<mpq::RecLayer>> rec_after(jobs.size());
+    {
+        std::vector<int> rec_of(n_layers, -1);
+        for (int l = 0, r = 0; l < n_layers; ++l)
+            if (layers[l].c_out > 0 && layers[l].W_hat) rec_of[l] = r++;
+        std::vector<mpq::RecLayer> rest;
+        bytes = 0.0;
+        for (int i = 0; i < (int)jobs.size(); ++i)
+            for (int l : jobs[i].layers) {
+                if (rec_of[l] < 0) continue;
+                if (i != big) {
+                    rec_after[i].push_back(rec[rec_of[l]]);
+                } else {
+                    rest.push_back(rec[rec_of[l]]);
+                    bytes += 5.0 * (double)layers[l].c_out * (double)layers[l].d;
+                }
+            }
+        rec.swap(rest);
+    }
+    // 1. every fit, side by side (as mpq_fit_layers)
+    std::vector<double> work;
+    for (const FitJob &j : jobs) work.push_back(j.work);
+    hipError_t e = run_concurrently(s, work, [&](int i, hipStream_t st) {
+        hipError_t e1 = launch_fit_job(jobs[i], n_grid, st);
+        if (e1 == hipSuccess && !rec_after[i].empty())
+            e1 = mpq::launch_reconstruct(rec_after[i].data(), (int)rec_after[i].size(), max_points, st);
+        return e1;
+    });
+    if (dgrid) (void)mpq::scratch_free(dgrid, s);
+    if (e != hipSuccess) {
+        if (ej.scratch) (void)mpq::scratch_free(ej.scratch, s);
+        return hip_fail(e, "fit kernel launch");
+    }
+    // 2. the output error's launch groups (work in GEMM FLOP) and the
     // reconstruction (bytes, at ~2 TB/s against ~100 TFLOP/s: x 50), side by side
     std::vector<double> w2 = ej.work;
     const int n_err_jobs = (int)w2.size();

@@ -370,6 +370,20 @@ fit_hist_kernel(const HistBatch B)
         return v;
     };
     double r[kGlobal ? 1 : EPT];
+    // The channel's row of the output error's D, outside calibration steps:
+    // the residual after the points so far in fp32 (the same fp64 steps, in
+    // the same order, as forming it from the stored points; zero past d, up
+    // to nkb * 32 <= T * EPT).  D holds tiles of 128 rows by 32 k, row-major
+    // inside: element j of row k is float ((k / 128) nkb + j / 32) 4096 +
+    // (k % 128) 32 + j % 32.  A buffer resource from the row's first element
+    // drops the stores past its last (and all, with no row).
+    static_assert(T % 32 == 0, "a thread's elements keep their place in a 32-k chunk");
+    const int nkb = (d + 31) / 32;
+    const bool has_d = !kGlobal && Ly.dres && !stepping;
+    const __amdgpu_buffer_rsrc_t rs_d = __builtin_amdgcn_make_buffer_rsrc(
+        has_d ? (void *)(Ly.dres + (k / 128) * nkb * 4096 + (k % 128) * 32) : nullptr, (short)0,
+        has_d ? (nkb * 4096 - (int)(k % 128) * 32) * 4 : 0, 0x00020000);
+    const int d_voff = ((t / 32) * 4096 + t % 32) * 4;   // element t; + u (T / 32) 4096 floats
     if constexpr (!kGlobal) {
 #pragma unroll
         for (int u = 0; u < EPT; ++u) r[u] = rebuild(u, s0);
@@ -444,7 +458,12 @@ fit_hist_kernel(const HistBatch B)
                 if (!B.refit) qrow[j] = (int8_t)(int)c;
                 ru = fma(-aupd, c, ru);
             }
-            if constexpr (!kGlobal) r[u] = ru;
+            if constexpr (!kGlobal) {
+                r[u] = ru;
+                // rewritten each step: the last write holds the n points
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint((float)ru), rs_d, d_voff,
+                                                      u * (T / 32) * 4096 * 4, 0);
+            }
             lmax = fmaxf(lmax, fabsf((float)ru));
             lsum = fma(ru, ru, lsum);
         }
@@ -767,6 +786,8 @@ size_t fit_hist_lds(int G)
 }
 
 bool fit_hist_supports(int64_t d) { return d >= 1 && d <= kHistMaxDim; }
+
+bool hist_variant_writes_d(int v) { return v >= 0 && v < kNumVariants && !kVariants[v].rebuilt; }
 
 int hist_variant(int64_t d)
 {

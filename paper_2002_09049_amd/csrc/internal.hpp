@@ -61,7 +61,7 @@ hipError_t launch_fit(const FitParams &p, const FitLayout &L, hipStream_t s);
 // select the same kernel variant (hist_variant); the descriptors travel by
 // value in the kernel arguments.
 constexpr int64_t kHistMaxDim = 32768;
-constexpr int kMaxBatchLayers = 44;
+constexpr int kMaxBatchLayers = 40;
 
 struct HistLayer {
     const float *W;     // [C][d]
@@ -77,6 +77,11 @@ struct HistLayer {
     // asymmetric codes (reading B2): nullptr, or [C] per-channel offsets
     // (the midpoint of w, written by the fit; the points fit w - offset)
     float *offsets;
+    // nullptr, or the output error's D for this layer (tiles of 128 rows by
+    // 32 k, row-major inside; see err_item_d_offset): the fit (not in
+    // calibration steps) writes each channel's final residual there in fp32,
+    // k past d zero (variants that keep the residual in registers only)
+    float *dres;
     int d;
     int c_begin;        // first workgroup of this layer in the launch
 };
@@ -106,6 +111,7 @@ static_assert(sizeof(HistBatch) <= 4096, "kernel arguments");
 size_t fit_hist_lds(int G);
 bool fit_hist_supports(int64_t d);
 int hist_variant(int64_t d);   // layers with equal variants may share a launch
+bool hist_variant_writes_d(int v);   // the variant's fit fills HistLayer::dres
 // Name of the histogram kernel that fits channels of length d (default grid
 // when default_grid, else a caller's grid), as LaunchTimer records it.
 std::string hist_kernel_name(int64_t d, int M, int G, bool default_grid);
@@ -154,6 +160,8 @@ struct ErrLayerIn {
     // codes in [-M, M]); err[k * Gc + j] is written
     const float *cand;
     int Gc, M;
+    // err item whose D rows the fit already wrote (at err_item_d): no forming
+    int d_ready;
 };
 // The items (an err item per layer with err, a ref item per layer with ref) go
 // in launch groups of up to 22; groups are independent and may run side by
@@ -163,6 +171,11 @@ size_t err_group_scratch_bytes(const ErrLayerIn *in, int n_in, int group);
 double err_group_flop(const ErrLayerIn *in, int n_in, int group);
 hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, int P, void *scratch,
                                      hipStream_t s);
+// Where the err item of in[i] keeps its rows of D (fp32 tiles [ceil(C / 128)]
+// [ceil(d / 32)][128][32], row-major inside, k past d zero):
+// the byte offset inside its group's scratch, and the group in *group; -1
+// when in[i] has no err item or its rows are clipping candidates.
+int64_t err_item_d_offset(const ErrLayerIn *in, int n_in, int i, int *group);
 
 // Clipping of Eq. (13) as the first point: candidate scales, then (after the
 // output error of the candidates) the choice of point 1.  One workgroup per

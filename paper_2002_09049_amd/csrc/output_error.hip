@@ -67,7 +67,8 @@ constexpr int kPad = 4;          // LDS row padding (floats); rows stay 16-byte 
 constexpr int kVec = kBK * kBM / kThreads / 4;   // float4 per thread and operand per slab
 constexpr int kMaxErrLayers = 22;
 constexpr int kXcds = 8;         // MI355X: workgroups are dealt to 8 XCDs in turn
-constexpr int kFT = 64;          // form tile: 64 rows x 64 k
+constexpr int kFormThreads = 256;
+constexpr int kPadA = 2;         // A slab rows: 130 floats, so a wavefront's 4-byte stores hit 64 banks
 constexpr int kFinRows = 256 / kWave;   // finish: rows of a split layer per workgroup
 
 // Raw buffer resource (gfx9 descriptor word 3: 32-bit dwords, no swizzle).
@@ -90,7 +91,7 @@ struct ErrLayer {
     const int32_t *counts;
     const float *X;
     float *out;          // err or ref
-    float *Dt;           // [d][ldc]
+    float *D;            // tiles [ntm][nkb][kBM][kBK] of the rows; k past d zero
     double *rowpart;     // [ntn][C]
     float *ypart;        // [splits][rows][n] (a split layer's K ranges of Y)
     const int32_t *rows; // nullptr, or the channels of rows 0 .. *nrows of D
@@ -98,7 +99,7 @@ struct ErrLayer {
     const float *cand;   // use_points == 2: [C / Gc][Gc] candidate scales (C counts rows of D)
     const float *offsets;   // use_points == 1: per-channel offsets (reading B2) or nullptr
     int64_t stride;      // out[channel * stride]
-    int C, d, n, ldc;
+    int C, d, n, nkb;    // nkb = ceil(d / kBK)
     int ntm, ntn, splits, kchunk;
     int tiles;           // gemm workgroups: ntm * ntn * splits, more for a listed layer
     int block_begin;     // first gemm workgroup (a multiple of kXcds)
@@ -145,105 +146,87 @@ __device__ __forceinline__ double int8_of(uint32_t w, int u)
     return (double)(int)(int8_t)(uint8_t)(w >> (8 * u));
 }
 
-// ---- 1. form: Dt = (W - sum a q)^T, one 64 x 64 tile per workgroup
-__global__ void __launch_bounds__(256) form_dt_kernel(const ErrGroup g)
+// Float index in D of row m, k (a multiple of 4 for a float4): tiles of
+// kBM rows by kBK k, row-major inside, so a GEMM slab of a row tile is one
+// contiguous block and a row's kBK consecutive k are 128 contiguous bytes.
+__device__ __forceinline__ int64_t d_index(int64_t m, int64_t k, int nkb)
 {
-    __shared__ float T[kFT][kFT + 1];
+    return ((m / kBM) * nkb + k / kBK) * (kBM * kBK) + (m % kBM) * kBK + k % kBK;
+}
 
+// ---- 1. form: rows of D, four consecutive k (one float4) per thread, k
+// past d written as zeros
+__global__ void __launch_bounds__(kFormThreads) form_d_kernel(const ErrGroup g)
+{
     int li = 0;
     while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].form_begin) ++li;
     const ErrLayer &L = g.L[li];
-    const int form_kt = (L.d + kFT - 1) / kFT;   // form tiles along k
-    int kt = (int)blockIdx.x - L.form_begin, rt = 0;
-    while (kt >= form_kt) {
-        kt -= form_kt;
-        ++rt;
-    }
     const int P = g.P;
-    const int64_t d = L.d, C = L.C;
-    const int64_t row0 = (int64_t)rt * kFT, k0 = (int64_t)kt * kFT;
-    const int t = threadIdx.x;
+    const int64_t d = L.d, C = L.C, q4 = (int64_t)L.nkb * (kBK / 4);
+    const int64_t e = (int64_t)((int)blockIdx.x - L.form_begin) * kFormThreads + threadIdx.x;
+    const int64_t m = e / q4, k = (e - m * q4) * 4;
     const int64_t nact = L.rows ? (int64_t)*L.nrows : C;
-    if (row0 >= nact) return;
-
-    // load: four rows (rb + 16 i) of four consecutive k (kc) per thread
-    const int kc = (t % 16) * 4, rb = t / 16;
+    if (m >= nact) return;   // rows past the list feed only output rows nobody reads
+    double r[4] = {0.0, 0.0, 0.0, 0.0};
+    if (L.use_points == 2) {
+        // clipping candidate j of channel ch: w - a [w / a]_Q (Eq. (10)'s
+        // rounding of the fp64 quotient, formed only near a half-integer)
+        const int64_t ch = m / L.Gc;
+        const double a = (double)L.cand[m];
+        const double ia = 1.0 / a, Md = (double)L.M;
+        const float *wr = L.W + ch * d;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int64_t m = row0 + rb + 16 * i, k = k0 + kc;
-        double r[4] = {0.0, 0.0, 0.0, 0.0};
-        if (L.use_points == 2 && m < C) {
-            // clipping candidate j of channel ch: w - a [w / a]_Q (Eq. (10)'s
-            // rounding of the fp64 quotient, formed only near a half-integer)
-            const int64_t ch = m / L.Gc;
-            const double a = (double)L.cand[m];
-            const double ia = 1.0 / a, Md = (double)L.M;
-            const float *wr = L.W + ch * d;
+        for (int u = 0; u < 4; ++u) {
+            if (k + u < d) {
+                const double wj = (double)wr[k + u];
+                double c = 0.0;
+                if (a != 0.0) {
+                    const double y = wj * ia;
+                    c = rint(y);
+                    if (fabs(fabs(y - c) - 0.5) < 0x1p-40) c = rint(wj / a);
+                    c = fmin(fmax(c, -Md), Md);
+                }
+                r[u] = fma(-a, c, wj);
+            }
+        }
+    } else {
+        const int64_t row = L.rows ? (int64_t)L.rows[m] : m;
+        const int nk = L.use_points ? min(max(L.counts[row], 0), P) : 0;  // counts is caller data
+        const double beta = (L.use_points && L.offsets) ? (double)L.offsets[row] : 0.0;
+        const float *wr = L.W + row * d;
+        const int8_t *cr = L.codes + row * (int64_t)P * d;
+        const float *sr = L.scales + row * (int64_t)P;
+        if (L.vecw && k < d) {   // d % 4 == 0: the four k lie inside the row
+            const float4 w = *(const float4 *)(wr + k);
+            r[0] = (double)w.x - beta; r[1] = (double)w.y - beta;
+            r[2] = (double)w.z - beta; r[3] = (double)w.w - beta;
+            for (int p = 0; p < nk; ++p) {
+                const double a = (double)sr[p];
+                const uint32_t q = *(const uint32_t *)(cr + (int64_t)p * d + k);
+#pragma unroll
+                for (int u = 0; u < 4; ++u) r[u] = fma(-a, int8_of(q, u), r[u]);
+            }
+        } else {
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 if (k + u < d) {
-                    const double wj = (double)wr[k + u];
-                    double c = 0.0;
-                    if (a != 0.0) {
-                        const double y = wj * ia;
-                        c = rint(y);
-                        if (fabs(fabs(y - c) - 0.5) < 0x1p-40) c = rint(wj / a);
-                        c = fmin(fmax(c, -Md), Md);
-                    }
-                    r[u] = fma(-a, c, wj);
-                }
-            }
-        } else if (L.use_points != 2 && m < nact) {
-            const int64_t row = L.rows ? (int64_t)L.rows[m] : m;
-            const int nk = L.use_points ? min(max(L.counts[row], 0), P) : 0;  // counts is caller data
-            const double beta = (L.use_points && L.offsets) ? (double)L.offsets[row] : 0.0;
-            const float *wr = L.W + row * d;
-            const int8_t *cr = L.codes + row * (int64_t)P * d;
-            const float *sr = L.scales + row * (int64_t)P;
-            if (L.vecw && k < d) {   // d % 4 == 0: four k wholly inside
-                const float4 w = *(const float4 *)(wr + k);
-                r[0] = (double)w.x - beta; r[1] = (double)w.y - beta;
-                r[2] = (double)w.z - beta; r[3] = (double)w.w - beta;
-                for (int p = 0; p < nk; ++p) {
-                    const double a = (double)sr[p];
-                    const uint32_t q = *(const uint32_t *)(cr + (int64_t)p * d + k);
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) r[u] = fma(-a, int8_of(q, u), r[u]);
-                }
-            } else if (!L.vecw) {
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    if (k + u < d) {
-                        double v = (double)wr[k + u] - beta;
-                        for (int p = 0; p < nk; ++p)
-                            v = fma(-(double)sr[p], (double)cr[(int64_t)p * d + k + u], v);
-                        r[u] = v;
-                    }
+                    double v = (double)wr[k + u] - beta;
+                    for (int p = 0; p < nk; ++p)
+                        v = fma(-(double)sr[p], (double)cr[(int64_t)p * d + k + u], v);
+                    r[u] = v;
                 }
             }
         }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) T[kc + u][rb + 16 * i] = (float)r[u];
     }
-    __syncthreads();
-    // store: four k rows (kb + 16 i) of four consecutive rows of D (mc)
-    const int mc = (t % 16) * 4, kb = t / 16;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int64_t k = k0 + kb + 16 * i, m = row0 + mc;
-        if (k < d && m < L.ldc) {   // ldc % 4 == 0: the four rows lie inside
-            const int kr = kb + 16 * i;
-            *(float4 *)(L.Dt + k * L.ldc + m) = make_float4(T[kr][mc], T[kr][mc + 1], T[kr][mc + 2], T[kr][mc + 3]);
-        }
-    }
+    *(float4 *)(L.D + d_index(m, k, L.nkb)) = make_float4((float)r[0], (float)r[1], (float)r[2], (float)r[3]);
 }
 
 // ---- 2. gemm: Y = D X, squared and summed per row
 template <bool kVecX>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4)))
 gemm_err_kernel(const ErrGroup g)
 {
-    __shared__ __align__(16) float sA[2][kBK][kBM + kPad];
+    __shared__ __align__(16) float sA[2][kBK][kBM + kPadA];
     __shared__ __align__(16) float sX[2][kBK][kBN + kPad];
     __shared__ double sPart[kBN / 32][kBM];
 
@@ -297,26 +280,33 @@ gemm_err_kernel(const ErrGroup g)
     const int64_t kend = min(kbeg + (int64_t)ls.kchunk, (int64_t)L.d);
     const int nslab = (int)((kend - kbeg + kBK - 1) / kBK);
 
-    // buffer resources over this K range's rows of Dt and X (below 2^31
-    // bytes, see plan_item): rows past kend read as zeros
+    // buffer resources: this row tile's slabs of D (one contiguous block
+    // each; rows past C feed only output rows nobody reads) and this K
+    // range's rows of X (below 2^31 bytes, see plan_item; rows past kend read
+    // as zeros)
     const __amdgpu_buffer_rsrc_t rsA =
-        make_rsrc(L.Dt + kbeg * L.ldc, (uint32_t)((kend - kbeg) * L.ldc * 4));
+        make_rsrc(L.D + (int64_t)tm * L.nkb * (kBM * kBK), (uint32_t)L.nkb * (kBM * kBK * 4));
     const __amdgpu_buffer_rsrc_t rsX = make_rsrc(L.X + kbeg * n, (uint32_t)((kend - kbeg) * n * 4));
-    // staging role: float4 number t + kThreads v of the slab, rows of
-    // kBM / 4 float4: row sk + kRowStep v, columns sm .. sm + 3, so each load
-    // instruction of a wavefront covers whole rows
-    constexpr int kF4Row = kBM / 4;
+    // staging roles.  A: float4 number t + kThreads v of the slab block, rows
+    // of kBK / 4 float4: row ar + kARowStep v, k ak .. ak + 3 (D's k past d
+    // are zeros).
+    // X: float4 number t + kThreads v, rows of kBN / 4 float4: row sk +
+    // kRowStep v, columns sm .. sm + 3, so each load instruction of a
+    // wavefront covers whole rows
+    constexpr int kF4RowA = kBK / 4;
+    constexpr int kARowStep = kThreads / kF4RowA;
+    const int ar = t / kF4RowA, ak = (t % kF4RowA) * 4;
+    constexpr int kF4Row = kBN / 4;
     constexpr int kRowStep = kThreads / kF4Row;
     const int sk = t / kF4Row, sm = (t % kF4Row) * 4;
     uint32_t offA[kVec], offX[kVec];
 #pragma unroll
     for (int v = 0; v < kVec; ++v) {
-        const int64_t m = row0 + sm, c = col0 + sm;
-        const int64_t kr = sk + kRowStep * v;
-        offA[v] = m < L.ldc ? (uint32_t)((kr * L.ldc + m) * 4) : kOob;   // ldc % 4 == 0
-        offX[v] = (kVecX && c < n) ? (uint32_t)((kr * n + c) * 4) : kOob;   // n % 4 == 0
+        const int64_t c = col0 + sm;
+        offA[v] = (uint32_t)((kbeg / kBK * (kBM * kBK) + (ar + kARowStep * v) * kBK + ak) * 4);
+        offX[v] = (kVecX && c < n) ? (uint32_t)(((int64_t)(sk + kRowStep * v) * n + c) * 4) : kOob;   // n % 4 == 0
     }
-    const uint32_t stepA = (uint32_t)(kBK * L.ldc * 4), stepX = (uint32_t)(kBK * n * 4);
+    const uint32_t stepA = (uint32_t)(kBM * kBK * 4), stepX = (uint32_t)(kBK * n * 4);
 
     // two register sets: the slab after next is in flight while a slab is
     // multiplied and the next one is stored
@@ -324,7 +314,7 @@ gemm_err_kernel(const ErrGroup g)
     auto load = [&](f32x4 (&ra)[kVec], f32x4 (&rx)[kVec], int s) {
 #pragma unroll
         for (int v = 0; v < kVec; ++v) {
-            ra[v] = load4(rsA, offA[v] == kOob ? kOob : offA[v] + (uint32_t)s * stepA);
+            ra[v] = load4(rsA, offA[v] + (uint32_t)s * stepA);
             if constexpr (kVecX) {
                 rx[v] = load4(rsX, offX[v] == kOob ? kOob : offX[v] + (uint32_t)s * stepX);
             } else {
@@ -340,7 +330,9 @@ gemm_err_kernel(const ErrGroup g)
     auto store = [&](const f32x4 (&ra)[kVec], const f32x4 (&rx)[kVec], int buf) {
 #pragma unroll
         for (int v = 0; v < kVec; ++v) {
-            *(f32x4 *)&sA[buf][sk + kRowStep * v][sm] = ra[v];
+            // A transposed into K-major rows: four 4-byte stores
+#pragma unroll
+            for (int u = 0; u < 4; ++u) sA[buf][ak + u][ar + kARowStep * v] = ra[v][u];
             *(f32x4 *)&sX[buf][sk + kRowStep * v][sm] = rx[v];
         }
     };
@@ -490,9 +482,9 @@ int64_t item_rows(const ErrLayerIn &I) { return I.cand ? I.C * I.Gc : I.C; }
 bool listed(const ErrLayerIn &I, int use_points) { return use_points == 1 && I.rows; }
 
 struct Plan {
-    int64_t ldc, ntm, ntn, splits, kchunk;
+    int64_t nkb, ntm, ntn, splits, kchunk;
     int64_t budget;   // splits of the workgroup budget (ntm * ntn * budget workgroups)
-    size_t dt_bytes, rowpart_bytes, ypart_bytes;
+    size_t d_bytes, rowpart_bytes, ypart_bytes;
 };
 
 size_t align256(size_t b) { return (b + 255) / 256 * 256; }
@@ -521,7 +513,7 @@ Plan plan_item(const ErrLayerIn &I, bool list)
 {
     Plan q;
     const int64_t C = item_rows(I);
-    q.ldc = (C + 3) / 4 * 4;
+    q.nkb = (I.d + kBK - 1) / kBK;
     q.ntm = (C + kBM - 1) / kBM;
     q.ntn = (I.n + kBN - 1) / kBN;
     const int64_t slabs = (I.d + kBK - 1) / kBK;
@@ -530,12 +522,11 @@ Plan plan_item(const ErrLayerIn &I, bool list)
     int64_t sp = (slabs + target / 2) / target;
     sp = std::max<int64_t>(1, std::min<int64_t>(sp, slabs));
     int64_t kchunk = (slabs + sp - 1) / sp * kBK;
-    const int64_t wide = std::max(q.ldc, I.n);
-    const int64_t max_chunk = ((1LL << 31) - 1) / (4 * wide) / kBK * kBK;   // >= kBK (C, n < 2^24)
+    const int64_t max_chunk = ((1LL << 31) - 1) / (4 * I.n) / kBK * kBK;   // >= kBK (n < 2^24)
     kchunk = std::min(kchunk, max_chunk);
     q.kchunk = kchunk;
     q.splits = (I.d + kchunk - 1) / kchunk;   // no empty K range
-    q.dt_bytes = align256(sizeof(float) * (size_t)(I.d * q.ldc));
+    q.d_bytes = align256(sizeof(float) * (size_t)(q.ntm * q.nkb * kBM * kBK));
     q.rowpart_bytes = align256(sizeof(double) * (size_t)(q.ntn * C));
     q.budget = q.splits;
     if (list) {
@@ -549,12 +540,38 @@ Plan plan_item(const ErrLayerIn &I, bool list)
     return q;
 }
 
+// A group's items in launch order (longest K ranges first) and the byte
+// offset of each item's scratch (D, row partials, Y ranges) in the group's.
+struct GroupLayout {
+    std::vector<Plan> p;
+    std::vector<int> order;
+    std::vector<size_t> off;   // by item
+};
+GroupLayout group_layout(const Item *grp, int cnt)
+{
+    GroupLayout G;
+    G.p.resize(cnt);
+    for (int i = 0; i < cnt; ++i) G.p[i] = plan_item(*grp[i].in, listed(*grp[i].in, grp[i].use_points));
+    G.order.resize(cnt);
+    for (int i = 0; i < cnt; ++i) G.order[i] = i;
+    std::stable_sort(G.order.begin(), G.order.end(),
+                     [&](int a, int b) { return G.p[a].kchunk > G.p[b].kchunk; });
+    G.off.assign(cnt, 0);
+    size_t cur = 0;
+    for (int o = 0; o < cnt; ++o) {
+        const int i = G.order[o];
+        G.off[i] = cur;
+        cur += G.p[i].d_bytes + G.p[i].rowpart_bytes + G.p[i].ypart_bytes;
+    }
+    return G;
+}
+
 size_t group_bytes(const Item *it, int cnt)
 {
     size_t b = 0;
     for (int i = 0; i < cnt; ++i) {
         const Plan q = plan_item(*it[i].in, listed(*it[i].in, it[i].use_points));
-        b += q.dt_bytes + q.rowpart_bytes + q.ypart_bytes;
+        b += q.d_bytes + q.rowpart_bytes + q.ypart_bytes;
     }
     return b;
 }
@@ -576,6 +593,19 @@ size_t err_group_scratch_bytes(const ErrLayerIn *in, int n_in, int group)
     return group_bytes(it.data() + base, cnt);
 }
 
+int64_t err_item_d_offset(const ErrLayerIn *in, int n_in, int i, int *group)
+{
+    const std::vector<Item> it = items_of(in, n_in);
+    for (size_t x = 0; x < it.size(); ++x) {
+        if (it[x].in != &in[i] || it[x].use_points != 1) continue;
+        const size_t base = x / kMaxErrLayers * kMaxErrLayers;
+        const int cnt = (int)std::min<size_t>(kMaxErrLayers, it.size() - base);
+        *group = (int)(x / kMaxErrLayers);
+        return (int64_t)group_layout(it.data() + base, cnt).off[x - base];
+    }
+    return -1;
+}
+
 double err_group_flop(const ErrLayerIn *in, int n_in, int group)
 {
     const std::vector<Item> it = items_of(in, n_in);
@@ -594,14 +624,9 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
     {
         const int cnt = (int)std::min<size_t>(kMaxErrLayers, it.size() - base);
         const Item *grp = it.data() + base;
-        std::vector<Plan> p(cnt);
-        for (int i = 0; i < cnt; ++i) p[i] = plan_item(*grp[i].in, listed(*grp[i].in, grp[i].use_points));
-        // longest K ranges first
-        std::vector<int> order(cnt);
-        for (int i = 0; i < cnt; ++i) order[i] = i;
-        std::stable_sort(order.begin(), order.end(),
-                         [&](int a, int b) { return p[a].kchunk > p[b].kchunk; });
-        char *cur = (char *)scratch;
+        const GroupLayout lay = group_layout(grp, cnt);   // longest K ranges first
+        const std::vector<Plan> &p = lay.p;
+        const std::vector<int> &order = lay.order;
         ErrGroup g;
         g.n_layers = cnt;
         g.P = P;
@@ -627,16 +652,16 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
             L.offsets = grp[i].use_points == 1 ? I.offsets : nullptr;
             L.Gc = I.Gc;
             L.M = I.M;
-            L.Dt = (float *)cur;
-            cur += q.dt_bytes;
+            char *cur = (char *)scratch + lay.off[i];
+            L.D = (float *)cur;
+            cur += q.d_bytes;
             L.rowpart = (double *)cur;
             cur += q.rowpart_bytes;
             L.ypart = q.ypart_bytes ? (float *)cur : nullptr;
-            cur += q.ypart_bytes;
             L.C = (int)item_rows(I);
             L.d = (int)I.d;
             L.n = (int)I.n;
-            L.ldc = (int)q.ldc;
+            L.nkb = (int)q.nkb;
             L.ntm = (int)q.ntm;
             L.ntn = (int)q.ntn;
             L.splits = (int)q.splits;
@@ -651,7 +676,9 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
             L.xoff = xoff;
             xoff = (xoff + (int)(planned % kXcds)) % kXcds;
             L.form_begin = (int)fblocks;
-            fblocks += (I.d + kFT - 1) / kFT * ((L.C + kFT - 1) / kFT);
+            // rows the fit wrote need no forming
+            const bool ready = grp[i].use_points == 1 && I.d_ready && !I.cand;
+            if (!ready) fblocks += ((int64_t)L.C * L.nkb * (kBK / 4) + kFormThreads - 1) / kFormThreads;
             L.fin_begin = (int)nblocks;
             nblocks += q.ypart_bytes ? (L.C + kFinRows - 1) / kFinRows : (L.C + 255) / 256;
             L.vecw = I.d % 4 == 0 && ((uintptr_t)I.W) % 16 == 0 && ((uintptr_t)I.codes) % 4 == 0;
@@ -670,10 +697,10 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
         }
         if (blocks > 0x7fffffffLL || fblocks > 0x7fffffffLL || nblocks > 0x7fffffffLL)
             return hipErrorInvalidValue;
-        hipError_t e;
-        {
-            LaunchTimer timer(s, "form_dt_kernel");
-            hipLaunchKernelGGL(form_dt_kernel, dim3((unsigned)fblocks), dim3(256), 0, s, g);
+        hipError_t e = hipSuccess;
+        if (fblocks > 0) {
+            LaunchTimer timer(s, "form_d_kernel");
+            hipLaunchKernelGGL(form_d_kernel, dim3((unsigned)fblocks), dim3(kFormThreads), 0, s, g);
             e = hipGetLastError();
         }
         if (e != hipSuccess) return e;

@@ -153,6 +153,11 @@ def test_output_error_rejects_oversized_dims(lib):
     big = (1 << 24) + 1
     assert lib.mpq_output_error(1, 1, 1, 1, 4, 4, 2, 1, big, 1, None, None) == E
     assert lib.mpq_output_error(1, 1, 1, 1, big, 4, 2, 1, 8, 1, None, None) == E
+    # d: a tile of 128 rows of D stays below 2 GiB
+    max_d = int(re.search(r"#define MPQ_MAX_ERR_D (\d+)", open(HEADER).read()).group(1))
+    assert (max_d + 31) // 32 * 32 * 128 * 4 < 2 ** 31
+    assert lib.mpq_output_error(1, 1, 1, 1, 4, max_d + 1, 2, 1, 8, 1, None, None) == E
+    assert "d must be <=" in mpq.last_error()
 
 
 def test_timing_records_nothing_until_a_launch(lib):

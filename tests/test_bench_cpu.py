@@ -19,7 +19,7 @@ def test_kernel_key_maps_profiler_names():
     assert k("fit_hist_kernel<256, 4, false, false, false>(x)") == "fit_hist_kernel<256,4,grid>"
     assert k("fit_hist_kernel<1024, 32, true, true, true>(x)") == "fit_hist_kernel<1024,32,lattice,rebuilt>"
     assert k("void mpq::(anonymous namespace)::gemm_err_kernel<true>(mpq::ErrGroup)") == "gemm_err_kernel"
-    assert bench.stage_of("form_dt_kernel") == "output_error"
+    assert bench.stage_of("form_d_kernel") == "output_error"
     assert bench.stage_of("fit_hist_kernel<64,1,linear>") == "fit"
     assert bench.stage_of("zero_i32_kernel") is None
     assert k("void mpq::(anonymous namespace)::int_forward_kernel<0>(mpq::IntGroup)") == "int_forward_kernel<16>"

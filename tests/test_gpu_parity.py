@@ -419,17 +419,27 @@ def test_timing_only_records_the_named_kernel():
     X = to_dev(wl.layer_calib(w, 0))
     ls = mpq.LayerSet([W], w.max_points, calib=[X])
     say("case timing_only")
-    mpq.timing_only("reconstruct_kernel")
+    mpq.timing_only("gemm_err_kernel")
     mpq.timing_enable(True)
     ls.quantize(w.bits, w.n_grid, w.tol)
     torch.cuda.synchronize()
     rec = mpq.timing_read()
     mpq.timing_enable(False)
-    assert rec and all(n == "reconstruct_kernel" and ms > 0 for n, ms in rec)
+    assert rec and all(n == "gemm_err_kernel" and ms > 0 for n, ms in rec)
     mpq.timing_only(None)
     mpq.timing_enable(True)
     ls.quantize(w.bits, w.n_grid, w.tol)
     torch.cuda.synchronize()
     names = {n for n, _ in mpq.timing_read()}
     mpq.timing_enable(False)
-    assert {"reconstruct_kernel", "gemm_err_kernel", "form_dt_kernel"} <= names
+    assert {"gemm_err_kernel", "finish_err_kernel", "reconstruct_kernel"} <= names
+    # the fit wrote the rows of D, so the whole-path call forms none; the
+    # output error alone forms them from the stored points
+    assert "form_d_kernel" not in names
+    mpq.timing_enable(True)
+    ls.output_error()
+    ls.reconstruct()
+    torch.cuda.synchronize()
+    names = {n for n, _ in mpq.timing_read()}
+    mpq.timing_enable(False)
+    assert {"form_d_kernel", "gemm_err_kernel", "finish_err_kernel", "reconstruct_kernel"} <= names
