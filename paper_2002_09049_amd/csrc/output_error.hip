@@ -7,13 +7,16 @@
 // descriptors by value in the kernel arguments:
 //
 //  1. form (HBM-bound): D[k][j] = fl32(w_kj - sum_{i<n_k} a_i q_ij), the fp64
-//     sum in point order (D = W for a ref item), written K-major as
-//     Dt[j][k] (row stride ldc = C rounded up to 4) through an LDS transpose.
+//     sum in point order (D = W for a ref item), one float4 of a row per
+//     thread.  D is stored as tiles of kBM rows by kBK k (row-major inside,
+//     k past d zero), so a row is written in 128-byte pieces and a GEMM
+//     slab of a row tile is one contiguous block.  Items whose rows the fit
+//     already wrote (d_ready) are not formed.
 //
 //  2. gemm: Y = D X on MFMA (v_mfma_f32_32x32x2f32, fp32 in and accumulate),
-//     the path's one dense contraction.  Dt and X are both K-major, so the A
-//     and B slabs are the same kind of copy: kBK rows of 128 consecutive
-//     floats.  A workgroup of eight wavefronts owns a 128 x 128 tile of Y and
+//     the path's one dense contraction.  A slab of D (one block) is staged
+//     transposed into K-major LDS rows; X is K-major, its slab kBK rows of
+//     128 consecutive floats.  A workgroup of eight wavefronts owns a 128 x 128 tile of Y and
 //     one K range; each wavefront owns 64 x 32 as 2 MFMA blocks.  The K
 //     loop stages slabs through double-buffered LDS from two register sets:
 //     while the MFMAs consume one slab, the next waits in registers for its
@@ -502,7 +505,7 @@ std::vector<Item> items_of(const ErrLayerIn *in, int n_in)
 
 // K split of a layer: K ranges of about kRangeK, or of work / 512 slabs (two
 // tiles per CU) for a layer that alone fills the GPU, and K ranges whose rows
-// of Dt and X stay below 2^31 bytes.  The ranges of a split layer make the
+// of X stay below 2^31 bytes (a row tile of D does: d <= MPQ_MAX_ERR_D).  The ranges of a split layer make the
 // GEMM store fp32 Y tiles that the finish kernel reads back, so a layer of
 // short K stays whole: the other layers of a call fill the GPU.  The split
 // depends on the layer alone, so a layer's result does not depend on the
