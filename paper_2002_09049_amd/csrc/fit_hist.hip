@@ -375,15 +375,19 @@ fit_hist_kernel(const HistBatch B)
     // the same order, as forming it from the stored points; zero past d, up
     // to nkb * 32 <= T * EPT).  D holds tiles of 128 rows by 32 k, row-major
     // inside: element j of row k is float ((k / 128) nkb + j / 32) 4096 +
-    // (k % 128) 32 + j % 32.  A buffer resource from the row's first element
-    // drops the stores past its last (and all, with no row).
+    // (k % 128) 32 + j % 32.  Element j = t + T u lies in 32-k chunk
+    // t / 32 + u T / 32 at place t % 32; a lane stores only while that chunk
+    // is one of the row's nkb, so every store stays inside the row (the
+    // chunk's elements past d store the zero residual of j >= d).  The
+    // buffer resource spans the row as a second guard.
     static_assert(T % 32 == 0, "a thread's elements keep their place in a 32-k chunk");
     const int nkb = (d + 31) / 32;
     const bool has_d = !kGlobal && Ly.dres && !stepping;
     const __amdgpu_buffer_rsrc_t rs_d = __builtin_amdgcn_make_buffer_rsrc(
         has_d ? (void *)(Ly.dres + (k / 128) * nkb * 4096 + (k % 128) * 32) : nullptr, (short)0,
         has_d ? (nkb * 4096 - (int)(k % 128) * 32) * 4 : 0, 0x00020000);
-    const int d_voff = ((t / 32) * 4096 + t % 32) * 4;   // element t; + u (T / 32) 4096 floats
+    const int d_chunk = t / 32;                          // chunk of element t (u = 0)
+    const int d_voff = (d_chunk * 4096 + t % 32) * 4;   // element t; + u (T / 32) 4096 floats
     if constexpr (!kGlobal) {
 #pragma unroll
         for (int u = 0; u < EPT; ++u) r[u] = rebuild(u, s0);
@@ -461,8 +465,9 @@ fit_hist_kernel(const HistBatch B)
             if constexpr (!kGlobal) {
                 r[u] = ru;
                 // rewritten each step: the last write holds the n points
-                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint((float)ru), rs_d, d_voff,
-                                                      u * (T / 32) * 4096 * 4, 0);
+                if (has_d && d_chunk + u * (T / 32) < nkb)
+                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint((float)ru), rs_d,
+                                                          d_voff + u * (T / 32) * 4096 * 4, 0, 0);
             }
             lmax = fmaxf(lmax, fabsf((float)ru));
             lsum = fma(ru, ru, lsum);
