@@ -64,10 +64,10 @@ def _declare(lib):
     lib.oracle_default_grid.argtypes = [i32, P]
     lib.oracle_default_grid.restype = None
     lib.oracle_fit_ex.argtypes = [P, i64, i64, i32, i32, P, i32, f64, P, i64, i32, f64, i32, i32,
-                                  i32, f64, P, P, P, P, P, P, i32]
+                                  i32, f64, i32, P, P, P, P, P, P, i32]
     lib.oracle_fit_ex.restype = i32
     lib.oracle_verify_ex.argtypes = [P, i64, i64, i32, i32, P, i32, f64, P, i64, i32, f64, i32, i32,
-                                     i32, f64, P, P, P, P, P, P, P, i64, P, P, P, P, P, i32]
+                                     i32, f64, i32, P, P, P, P, P, P, P, i64, P, P, P, P, P, i32]
     lib.oracle_output_error_ex.argtypes = [P, P, P, P, P, i64, i64, i32, P, i64, P, i64, P, P, i32]
     lib.oracle_output_error_ex.restype = i32
     lib.oracle_reconstruct_ex.argtypes = [P, P, P, P, i64, i64, i32, P]
@@ -142,11 +142,13 @@ class Oracle:
         return self.lib.oracle_scale_error(_p(r), r.size, float(a), self.levels(bits))
 
     def fit(self, W: np.ndarray, bits: int, max_points: int, n_grid: int, tol: float,
-            grid: Optional[np.ndarray] = None, n_threads: int = 0, refit: bool = False):
-        """Free-running greedy fit (refit: reading A2). Returns (codes[C,P,d] i8,
-        scales[C,P] f32, counts[C] i32, err[C,P] f64)."""
+            grid: Optional[np.ndarray] = None, n_threads: int = 0, refit: bool = False,
+            gate: bool = False):
+        """Free-running greedy fit (refit: reading A2; gate: Algorithm 2's naive
+        first point, reading F1). Returns (codes[C,P,d] i8, scales[C,P] f32,
+        counts[C] i32, err[C,P] f64)."""
         return self._fit(W, bits, max_points, n_grid, tol, None, 0.0, False, refit, grid,
-                         n_threads)[:4]
+                         n_threads, gate=gate)[:4]
 
     def fit_clip(self, W, bits: int, max_points: int, n_grid: int, X, tol: float = 0.0,
                  calib: bool = False, eps: float = 0.0, relative: bool = True, clip_grid: int = 20,
@@ -194,7 +196,7 @@ class Oracle:
                          calib=calib, asym=True)
 
     def _fit(self, W, bits, P, n_grid, tol, X, eps, relative, refit, grid, n_threads, calib=None,
-             clip_grid=0, eta=0.0, asym=False):
+             clip_grid=0, eta=0.0, asym=False, gate=False):
         calib = (X is not None) if calib is None else calib
         W = np.ascontiguousarray(W, dtype=np.float32)
         C, d = W.shape
@@ -211,22 +213,24 @@ class Oracle:
         rc = self.lib.oracle_fit_ex(_p(W), C, d, bits, P, _p(g), n_grid, float(tol), _p(X),
                                     0 if X is None else X.shape[1], 1 if calib else 0, float(eps),
                                     1 if relative else 0, 1 if refit else 0, int(clip_grid),
-                                    float(eta), _p(offsets), _p(codes_), _p(scales), _p(counts),
-                                    _p(err), _p(xerr), n_threads)
+                                    float(eta), 1 if gate else 0, _p(offsets), _p(codes_),
+                                    _p(scales), _p(counts), _p(err), _p(xerr), n_threads)
         if rc != 0:
             raise MemoryError("oracle_fit_ex failed")
         return (codes_, scales, counts, err, xerr) + ((offsets,) if asym else ())
 
     def verify(self, W, bits, max_points, n_grid, tol, codes_, scales, counts, err=None,
-               grid=None, channels=None, n_threads: int = 0, refit: bool = False):
+               grid=None, channels=None, n_threads: int = 0, refit: bool = False,
+               gate: bool = False):
         """Lockstep check of another implementation's fit output (rules V1-V4;
-        refit: reading A2).
+        refit: reading A2; gate: reading F1, status 10 for a wrong naive-point
+        decision).
 
         Returns a dict of per-channel arrays: status, cand_ties, code_ties,
         stop_ties, err_relmax, and the checked channel indices.
         """
         return self._verify(W, bits, max_points, n_grid, tol, None, 0.0, False, refit, codes_,
-                            scales, counts, err, None, grid, channels, n_threads)
+                            scales, counts, err, None, grid, channels, n_threads, gate=gate)
 
     def verify_clip(self, W, bits, max_points, n_grid, X, codes_, scales, counts, err=None,
                     xerr=None, tol: float = 0.0, calib: bool = False, eps: float = 0.0,
@@ -254,7 +258,8 @@ class Oracle:
                             offsets=offsets)
 
     def _verify(self, W, bits, P, n_grid, tol, X, eps, relative, refit, codes_, scales, counts,
-                err, xerr, grid, channels, n_threads, calib=None, clip_grid=0, eta=0.0, offsets=None):
+                err, xerr, grid, channels, n_threads, calib=None, clip_grid=0, eta=0.0, offsets=None,
+                gate=False):
         calib = (X is not None) if calib is None else calib
         if offsets is not None:
             offsets = np.ascontiguousarray(offsets, dtype=np.float32)
@@ -278,7 +283,7 @@ class Oracle:
         rc = self.lib.oracle_verify_ex(
             _p(W), C, d, bits, P, _p(g), n_grid, float(tol), _p(X), 0 if X is None else X.shape[1],
             1 if calib else 0, float(eps), 1 if relative else 0, 1 if refit else 0, int(clip_grid),
-            float(eta), _p(offsets), _p(codes_), _p(scales),
+            float(eta), 1 if gate else 0, _p(offsets), _p(codes_), _p(scales),
             _p(counts), _p(e), _p(xe), _p(chan), n, _p(out["status"]), _p(out["cand_ties"]),
             _p(out["code_ties"]), _p(out["stop_ties"]), _p(out["err_relmax"]), n_threads)
         if rc != 0:
@@ -288,19 +293,21 @@ class Oracle:
 
     def fit_calib(self, W: np.ndarray, bits: int, max_points: int, n_grid: int, X: np.ndarray,
                   eps: float, relative: bool, grid: Optional[np.ndarray] = None, n_threads: int = 0,
-                  refit: bool = False):
+                  refit: bool = False, gate: bool = False):
         """Free-running fit with Algorithm 2's stopping rule on the calibration
-        batch X [d, N] (reading S4; refit: reading A2).  Returns (codes, scales,
-        counts, err, xerr[C,P] f64: the output error after each point)."""
-        return self._fit(W, bits, max_points, n_grid, 0.0, X, eps, relative, refit, grid, n_threads)
+        batch X [d, N] (reading S4; refit: reading A2; gate: Algorithm 2's
+        naive first point, reading F1).  Returns (codes, scales, counts, err,
+        xerr[C,P] f64: the output error after each point)."""
+        return self._fit(W, bits, max_points, n_grid, 0.0, X, eps, relative, refit, grid, n_threads,
+                         gate=gate)
 
     def verify_calib(self, W, bits, max_points, n_grid, X, eps, relative, codes_, scales, counts,
                      err=None, xerr=None, grid=None, channels=None, n_threads: int = 0,
-                     refit: bool = False):
+                     refit: bool = False, gate: bool = False):
         """Lockstep check (V1, V2, V4, V4x and S4's stop decision) of another
-        implementation's fit with Algorithm 2's stopping rule."""
+        implementation's fit with Algorithm 2's stopping rule (gate: reading F1)."""
         return self._verify(W, bits, max_points, n_grid, 0.0, X, eps, relative, refit, codes_,
-                            scales, counts, err, xerr, grid, channels, n_threads)
+                            scales, counts, err, xerr, grid, channels, n_threads, gate=gate)
 
     def output_error(self, W, codes_, scales, counts, X, channels=None, with_ref=True, n_threads: int = 0,
                      offsets=None):

@@ -43,6 +43,16 @@
  *          e > eps), or at max_points, ||r||^2 == 0 or no nonzero scale.
  *          The points are still chosen by Eq. (9): Algorithm 1 fits the
  *          residual, Algorithm 2 only decides how many points to take.
+ *   F1     Variant (gate != 0), Algorithm 2's first step: the channel is
+ *          first quantized naively, w~ = a_N [w / a_N]_Q with the max-abs
+ *          code step a_N = fl32(fl32(max|w|) / M) (fp64 quotient; the
+ *          candidate c = 1 of reading G2); if the stopping rule in force
+ *          (S1, or S4 on the batch) already holds for that one point, it is
+ *          the channel's only point; otherwise it is discarded and
+ *          Algorithm 1 runs from r_1 = w as without the gate.  Without the
+ *          gate (the default) point 1 is Algorithm 1's grid search from the
+ *          start, so a channel whose naive point would pass can get a
+ *          different first point, and under S4 more points.
  *   A1     No refit of a once q is fixed (the method as printed).
  *   A2     Variant (refit != 0): once q is fixed by Eq. (10) at the searched
  *          a*, the point's scale is the least-squares one for that q,
@@ -87,6 +97,11 @@
  *          right shift of the 64-bit sum, i.e. the floor of sum / 2^p.
  *   I2     Activations are signed integers held in int8, one vector of d per
  *          column of the batch; Step 2 sums in 64 bits.
+ *
+ * Pins (tests/oracle_pins.py) tie every function here to the paper, exact
+ * arithmetic, brute force or library routines; the only part left without
+ * one ("parity unpinned") is the exponential rate of Theorem 1, whose
+ * constants the paper does not give.
  */
 #include <math.h>
 #include <stdint.h>
@@ -384,8 +399,9 @@ static int clip_choose(const float *w, int64_t d, int M, const float *cc, int cl
 
 static int fit_channel(const float *w, int64_t d, int M, int P, const float *c,
                        int G, double tol, const calib_rule *cal, int refit, const clip_rule *clip,
-                       double eta, double *gwork, int asym, float *offset, int8_t *codes,
-                       float *scales, double *err, double *xerr, double *r, float *a, double *E)
+                       double eta, double *gwork, int asym, int gate, float *offset,
+                       int8_t *codes, float *scales, double *err, double *xerr, double *r,
+                       float *a, double *E)
 {
     for (int64_t j = 0; j < d; ++j) r[j] = (double)w[j];   /* r_1 = w, Eq. (7) */
     double Ew = sum_sq(r, d);
@@ -416,6 +432,26 @@ static int fit_channel(const float *w, int64_t d, int M, int P, const float *c,
                 e = calib_error(r, d, cal->X, cal->N);
                 if (xerr) xerr[0] = e;
             }
+        }
+    }
+    if (gate && !clip && Ew > 0.0 && P >= 1) {              /* F1: Algorithm 2's naive point */
+        const float one = 1.0f;
+        float aN;
+        oracle_candidate_scales(r, d, M, &one, 1, &aN);    /* a_N = fl32(m / M) */
+        if (aN != 0.0f) {
+            double *R = gwork;                              /* r_1 - a_N [r_1 / a_N]_Q */
+            oracle_codes(r, d, (double)aN, M, codes);
+            for (int64_t j = 0; j < d; ++j) R[j] = r[j] - (double)aN * (double)codes[j];
+            const double EN = sum_sq(R, d);
+            const double eN = cal ? calib_error(R, d, cal->X, cal->N) : 0.0;
+            if (cal ? calib_should_stop(1, P, EN, eN, thr) : should_stop(1, P, EN, Ew, tol)) {
+                memcpy(r, R, sizeof(double) * (size_t)d);  /* kept: the only point */
+                scales[0] = aN;
+                err[0] = EN;
+                if (cal && xerr) xerr[0] = eN;
+                return 1;
+            }
+            memset(codes, 0, (size_t)d);                    /* discarded: Algorithm 1 from w */
         }
     }
     for (;;) {
@@ -470,8 +506,8 @@ static int n_threads_or_default(int nt)
  * [C][P] (may be NULL).  Slots at or after a channel's count are zero. */
 static int fit_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                      const float *grid, int G, double tol, const calib_rule *cal, int refit,
-                     const float *clipX, int64_t clipN, int clipG, double eta, float *offsets,
-                     int8_t *codes, float *scales, int32_t *counts, double *err,
+                     const float *clipX, int64_t clipN, int clipG, double eta, int gate,
+                     float *offsets, int8_t *codes, float *scales, int32_t *counts, double *err,
                      double *xerr, int n_threads)
 {
     int M = oracle_levels(bits);
@@ -511,7 +547,7 @@ static int fit_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                 memset(xe, 0, sizeof(double) * (size_t)P);
                 float beta = 0.0f;
                 int n = fit_channel(W + k * d, d, M, P, c, G, tol, cal, refit,
-                                    clipG > 0 ? &cl : NULL, eta, gw, offsets != NULL, &beta,
+                                    clipG > 0 ? &cl : NULL, eta, gw, offsets != NULL, gate, &beta,
                                     codes + k * P * d, scales + k * P, e, xe, r, a, E);
                 if (offsets) offsets[k] = beta;
                 counts[k] = n;
@@ -531,23 +567,24 @@ int oracle_fit(const float *W, int64_t C, int64_t d, int bits, int P,
                const float *grid, int G, double tol, int8_t *codes,
                float *scales, int32_t *counts, double *err, int n_threads)
 {
-    return fit_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, NULL, 0, 0, 0.0, NULL, codes, scales,
-                     counts, err, NULL, n_threads);
+    return fit_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, NULL, 0, 0, 0.0, 0, NULL, codes,
+                     scales, counts, err, NULL, n_threads);
 }
 
 /* The fit with its options: calib == 0 for the stopping rule S1 with tol,
  * else S4 on X [d][N] with eps / relative; refit != 0 for reading A2;
  * clipG > 0 for reading C1 on X with clipG candidates (the paper's 20);
  * eta > 0 for the paper's grid of Eq. (11) (reading G3; the paper's 2^-10)
- * instead of the G-point grid. */
+ * instead of the G-point grid; gate != 0 for Algorithm 2's naive first
+ * point (reading F1; not with clipG). */
 int oracle_fit_ex(const float *W, int64_t C, int64_t d, int bits, int P, const float *grid, int G,
                   double tol, const float *X, int64_t N, int calib, double eps, int relative,
-                  int refit, int clipG, double eta, float *offsets, int8_t *codes, float *scales,
-                  int32_t *counts, double *err, double *xerr, int n_threads)
+                  int refit, int clipG, double eta, int gate, float *offsets, int8_t *codes,
+                  float *scales, int32_t *counts, double *err, double *xerr, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
     return fit_layer(W, C, d, bits, P, grid, G, tol, calib ? &cal : NULL, refit, X, N, clipG, eta,
-                     offsets, codes, scales, counts, err, calib ? xerr : NULL, n_threads);
+                     gate, offsets, codes, scales, counts, err, calib ? xerr : NULL, n_threads);
 }
 
 /* The fit with the stopping rule S4 on the calibration batch X [d][N]. */
@@ -557,8 +594,8 @@ int oracle_fit_calib(const float *W, int64_t C, int64_t d, int bits, int P,
                      double *err, double *xerr, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
-    return fit_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, NULL, 0, 0, 0.0, NULL, codes, scales,
-                     counts, err, xerr, n_threads);
+    return fit_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, NULL, 0, 0, 0.0, 0, NULL, codes,
+                     scales, counts, err, xerr, n_threads);
 }
 
 /* ------------------------------------------------------------------------
@@ -591,9 +628,15 @@ int oracle_fit_calib(const float *W, int64_t C, int64_t d, int bits, int P,
  * be a clipping candidate whose output error is within 1e-5 relative plus
  * the fp32 evaluation allowance (calib_slack) of the smallest one, and its
  * codes Eq. (10)'s at that scale (up to code ties).
+ * With Algorithm 2's naive first point (reading F1, gate != 0), point 1 may
+ * be the naive point (a_N, [r_1 / a_N]_Q) only if the stopping rule holds
+ * for it (or its error is within the stop-tie band of the threshold, a
+ * "stop tie"); then the channel must stop there.  If the rule holds and the
+ * other side took another first point, the status is 10.
  * status: 0 ok, 1 count, 2 scale not a candidate, 3 scale not optimal,
  *         4 code, 5 nonzero unused slot, 6 err value, 7 bad count range,
- *         8 output-error value, 9 offset (reading B2).
+ *         8 output-error value, 9 offset (reading B2), 10 the naive-point
+ *         decision of reading F1.
  * ------------------------------------------------------------------------ */
 
 /* V4 / V4x for one fp32 output: 1e-5 relative plus slack, one fp32
@@ -631,7 +674,7 @@ static int codes_agree(const double *r, int64_t d, double as, int M, const int8_
 
 static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                         const float *grid, int G, double tol, const calib_rule *cal, int refit,
-                        const float *clipX, int64_t clipN, int clipG, double eta,
+                        const float *clipX, int64_t clipN, int clipG, double eta, int gate,
                         const float *offsets,
                         const int8_t *codes, const float *scales, const int32_t *counts,
                         const float *err, const float *xerr, const int64_t *chan,
@@ -734,6 +777,40 @@ static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                         } else { st = 1; break; }
                     }
                     if (stop_other) break;
+                    if (n == 0 && gate && clipG == 0 && Ew > 0.0) {
+                        /* F1: the naive point, kept only if the rule holds for it */
+                        const float one = 1.0f;
+                        float aN;
+                        oracle_candidate_scales(r, d, M, &one, 1, &aN);
+                        if (aN != 0.0f) {
+                            double *R = gw;
+                            for (int64_t j = 0; j < d; ++j)
+                                R[j] = r[j] - (double)aN * nearest_code(r[j] / (double)aN, M);
+                            const double EN = sum_sq(R, d);
+                            const double eN = cal ? calib_error(R, d, cal->X, cal->N) : 0.0;
+                            const int pass = cal ? calib_should_stop(1, P, EN, eN, thr)
+                                                 : should_stop(1, P, EN, Ew, tol);
+                            int nearN = 0;
+                            if (cal) {
+                                nearN = fabs(eN - thr) <= 1e-5 * thr +
+                                                              calib_slack(R, d, cal->X, cal->N) +
+                                                              thr_slack;
+                            } else if (tol * Ew > 0.0) {
+                                nearN = fabs(EN / (tol * Ew) - 1.0) <= 1e-6;
+                            }
+                            int qtN = 0;
+                            const int kept = ak[0] == aN && codes_agree(r, d, (double)aN, M, qk, &qtN);
+                            if (kept && (pass || nearN)) {
+                                qt += qtN;
+                                if (!pass) stt++;
+                                for (int64_t j = 0; j < d; ++j) r[j] = r[j] - (double)aN * (double)qk[j];
+                                if (cal) e = calib_error(r, d, cal->X, cal->N);
+                                continue;
+                            }
+                            if (pass && !nearN) { st = 10; break; }
+                            if (pass) stt++;   /* discarded within the stop-tie band */
+                        }
+                    }
                     /* V1 */
                     if (gbest < 0) {           /* the other side went on past a stop */
                         if (eta > 0.0) { st = 1; break; }
@@ -836,24 +913,24 @@ int oracle_verify(const float *W, int64_t C, int64_t d, int bits, int P,
                   int32_t *cand_ties, int32_t *code_ties, int32_t *stop_ties,
                   double *err_relmax, int n_threads)
 {
-    return verify_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, NULL, 0, 0, 0.0, NULL, codes, scales,
-                        counts, err, NULL, chan, n_chan, status, cand_ties, code_ties, stop_ties,
-                        err_relmax, n_threads);
+    return verify_layer(W, C, d, bits, P, grid, G, tol, NULL, 0, NULL, 0, 0, 0.0, 0, NULL, codes,
+                        scales, counts, err, NULL, chan, n_chan, status, cand_ties, code_ties,
+                        stop_ties, err_relmax, n_threads);
 }
 
 /* The lockstep check of a fit with its options (as oracle_fit_ex). */
 int oracle_verify_ex(const float *W, int64_t C, int64_t d, int bits, int P, const float *grid,
                      int G, double tol, const float *X, int64_t N, int calib, double eps,
-                     int relative, int refit, int clipG, double eta, const float *offsets,
-                     const int8_t *codes, const float *scales,
+                     int relative, int refit, int clipG, double eta, int gate,
+                     const float *offsets, const int8_t *codes, const float *scales,
                      const int32_t *counts, const float *err, const float *xerr,
                      const int64_t *chan, int64_t n_chan, int32_t *status, int32_t *cand_ties,
                      int32_t *code_ties, int32_t *stop_ties, double *err_relmax, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
     return verify_layer(W, C, d, bits, P, grid, G, tol, calib ? &cal : NULL, refit, X, N, clipG, eta,
-                        offsets, codes, scales, counts, err, calib ? xerr : NULL, chan, n_chan, status,
-                        cand_ties, code_ties, stop_ties, err_relmax, n_threads);
+                        gate, offsets, codes, scales, counts, err, calib ? xerr : NULL, chan, n_chan,
+                        status, cand_ties, code_ties, stop_ties, err_relmax, n_threads);
 }
 
 /* The lockstep check of a fit with the calibration rule S4; xerr [C][P] is
@@ -867,9 +944,9 @@ int oracle_verify_calib(const float *W, int64_t C, int64_t d, int bits, int P,
                         double *err_relmax, int n_threads)
 {
     calib_rule cal = {X, N, eps, relative};
-    return verify_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, NULL, 0, 0, 0.0, NULL, codes, scales,
-                        counts, err, xerr, chan, n_chan, status, cand_ties, code_ties, stop_ties,
-                        err_relmax, n_threads);
+    return verify_layer(W, C, d, bits, P, grid, G, 0.0, &cal, 0, NULL, 0, 0, 0.0, 0, NULL, codes,
+                        scales, counts, err, xerr, chan, n_chan, status, cand_ties, code_ties,
+                        stop_ties, err_relmax, n_threads);
 }
 
 /* Residual D = w - sum_{i<n} a_i q_i of one channel, summed in point order

@@ -485,6 +485,145 @@ def check_calib_verifier_fp32_evaluation(orc):
             assert (v["status"] == 8).all()
 
 
+# ------------------------------------------- reading F1: Algorithm 2's naive first point
+def _naive_point(w, bits):
+    """The naive quantization [w]_Q of Algorithm 2 in numpy: code step
+    fl32(fl32(max|w|) / M), codes rounded half to even and clipped."""
+    M = 2 ** (bits - 1) - 1
+    a = np.float32(np.float64(np.float32(np.abs(w).max())) / M)
+    if a == 0:
+        return a, np.zeros(w.shape, np.int8)
+    q = np.clip(np.round(w.astype(np.float64) / np.float64(a)), -M, M)
+    return a, q.astype(np.int8)
+
+
+def check_gate_worked_example(orc):
+    """Reading F1 on the hand-derived case (tests/golden): the naive point is
+    kept when its output error passes, and discarded (Algorithm 1 from w)
+    when it does not."""
+    g = _golden("naive_first_gate")
+    W = np.array([g["w"]], np.float32)
+    for v in g["variants"]:
+        X = np.array(v["X"], np.float32)
+        for key, gate in (("gate", True), ("no_gate", False)):
+            c, s, n, _, x = orc.fit_calib(W, g["bits"], g["max_points"], g["n_grid"], X,
+                                          g["eps"], False, gate=gate)
+            e = v[key]
+            assert n[0] == e["count"], (key, v["X"], n)
+            assert s[0].tolist() == e["scales"], (key, s)
+            assert c[0].tolist() == e["codes"], (key, c)
+            assert x[0].tolist() == e["xerr"], (key, x)
+
+
+def _gate_threshold(values):
+    """A threshold halfway between two well-separated sorted values, so that
+    about half the channels pass and none sits near it."""
+    v = np.sort(np.asarray(values, np.float64))
+    gaps = np.diff(v) / np.maximum(v[1:], 1e-300)
+    lo = len(v) // 4
+    i = lo + int(np.argmax(gaps[lo:len(v) - lo]))
+    return 0.5 * (v[i] + v[i + 1])
+
+
+def check_gate_definition(orc):
+    """Reading F1 against its definition, per channel, in numpy: the naive
+    point of Algorithm 2 is kept (count 1) when its error under the rule in
+    force is at most the threshold; otherwise the fit is exactly the fit
+    without the gate (Algorithm 1 from w)."""
+    W, X = _calib_case(seed=31, C=24, d=40, N=50)
+    Xd = X.astype(np.float64)
+    for bits, P, G in ((4, 6, 64), (3, 5, 32)):
+        eN, EN = [], []
+        for k in range(W.shape[0]):
+            a, q = _naive_point(W[k], bits)
+            R = W[k].astype(np.float64) - np.float64(a) * q
+            eN.append(float(np.mean((R @ Xd) ** 2)))
+            EN.append(float(R @ R))
+        live = W.any(axis=1)
+        # S4, absolute threshold
+        eps = _gate_threshold(np.array(eN)[live])
+        c1, s1, n1, _, x1 = orc.fit_calib(W, bits, P, G, X, eps, False, gate=True)
+        c0, s0, n0, _, x0 = orc.fit_calib(W, bits, P, G, X, eps, False)
+        kept = 0
+        for k in range(W.shape[0]):
+            if not live[k]:
+                assert n1[k] == 0
+                continue
+            a, q = _naive_point(W[k], bits)
+            if eN[k] <= eps:
+                kept += 1
+                assert n1[k] == 1 and s1[k, 0] == a and np.array_equal(c1[k, 0], q), k
+                assert abs(x1[k, 0] - eN[k]) <= 1e-12 * eN[k] + 1e-300
+            else:
+                assert n1[k] == n0[k] and np.array_equal(s1[k], s0[k]) and np.array_equal(c1[k], c0[k])
+        assert 0 < kept < live.sum()
+        # S1 (isotropic), relative tolerance
+        Ew = (W.astype(np.float64) ** 2).sum(axis=1)
+        ratio = np.array(EN)[live] / Ew[live]
+        tol = _gate_threshold(ratio)
+        c1, s1, n1, _ = orc.fit(W, bits, P, G, tol, gate=True)
+        c0, s0, n0, _ = orc.fit(W, bits, P, G, tol)
+        for k in np.nonzero(live)[0]:
+            a, q = _naive_point(W[k], bits)
+            if EN[k] <= tol * Ew[k]:
+                assert n1[k] == 1 and s1[k, 0] == a and np.array_equal(c1[k, 0], q), k
+            else:
+                assert n1[k] == n0[k] and np.array_equal(s1[k], s0[k]) and np.array_equal(c1[k], c0[k])
+
+
+def check_gate_hadamard_is_isotropic(orc):
+    """Reading F1 with X X^T = N I: the output error is ||r||^2 and the
+    relative threshold eps ||w||^2, so the gated S4 fit equals the gated
+    isotropic fit with tol = eps; the gate changes the first point of some
+    channels (against the fit without it)."""
+    rng = np.random.default_rng(8)
+    d, N = 48, 64
+    X = bf.hadamard(N)[:d].astype(np.float32)
+    W = (rng.standard_normal((16, d)) * np.exp(0.3 * rng.standard_normal((16, 1)))).astype(np.float32)
+    changed = 0
+    for bits, P, G in ((4, 6, 64), (3, 8, 32)):
+        ratio = []
+        for k in range(W.shape[0]):
+            a, q = _naive_point(W[k], bits)
+            R = W[k].astype(np.float64) - np.float64(a) * q
+            ratio.append(float(R @ R) / float(W[k].astype(np.float64) @ W[k].astype(np.float64)))
+        eps = _gate_threshold(ratio)
+        c1, s1, n1, e1, x1 = orc.fit_calib(W, bits, P, G, X, eps, True, gate=True)
+        c0, s0, n0, e0 = orc.fit(W, bits, P, G, eps, gate=True)
+        assert np.array_equal(n1, n0) and np.array_equal(s1, s0) and np.array_equal(c1, c0)
+        assert np.allclose(x1, e0, rtol=1e-9, atol=0)
+        cg, sg, ng, _ = orc.fit(W, bits, P, G, eps)
+        changed += int(((sg[:, 0] != s0[:, 0]) & (n0 == 1)).sum())
+    assert changed > 0
+
+
+def check_gate_verifier(orc):
+    """The verifier with reading F1 accepts gated fits (S1 and S4) and flags,
+    with status 10, a fit that took Algorithm 1's point where the naive one
+    passes."""
+    W, X = _calib_case(seed=33, C=16, d=30, N=40)
+    bits, P, G = 4, 6, 64
+    eN = []
+    for k in range(W.shape[0] - 1):
+        a, q = _naive_point(W[k], bits)
+        R = W[k].astype(np.float64) - np.float64(a) * q
+        eN.append(float(np.mean((R @ X.astype(np.float64)) ** 2)))
+    eps = _gate_threshold(eN)
+    c1, s1, n1, e1, x1 = orc.fit_calib(W, bits, P, G, X, eps, False, gate=True)
+    v = orc.verify_calib(W, bits, P, G, X, eps, False, c1, s1, n1, e1.astype(np.float32),
+                         x1.astype(np.float32), gate=True)
+    assert (v["status"] == 0).all(), v["status"]
+    c0, s0, n0, e0, x0 = orc.fit_calib(W, bits, P, G, X, eps, False)
+    v = orc.verify_calib(W, bits, P, G, X, eps, False, c0, s0, n0, None, None, gate=True)
+    differs = (s0[:, 0] != s1[:, 0]) & (n1 == 1)
+    assert differs.any()
+    assert (v["status"][differs] == 10).all(), v["status"]
+    tol = 1e-2
+    c1, s1, n1, e1 = orc.fit(W, bits, P, G, tol, gate=True)
+    v = orc.verify(W, bits, P, G, tol, c1, s1, n1, e1.astype(np.float32), gate=True)
+    assert (v["status"] == 0).all(), v["status"]
+
+
 # ------------------------------------------- reading A2: least-squares refit
 def check_refit_one_point(orc):
     """One point: the codes are Eq. (10)'s at the searched scale (unchanged
@@ -687,6 +826,113 @@ def check_paper_search_bruteforce(orc):
             assert g == gref or (not exact and E[g - 1] == E[gref - 1]), (bits, case, g, gref)
 
 
+def _exact_search(r, M, gamma, count):
+    """Argmin of Eq. (9) over the grid a_g = fl64(g gamma), g = 1..count, with
+    every error evaluated exactly: r and a are dyadic rationals, so with a
+    common power of two 2^S, r_j 2^S and a 2^S are integers, the code
+    [r_j / a] (ties to even, clipped) comes from an integer division, and
+    E 2^(2S) is an integer.  Returns (g, exact E of every g as Fractions)."""
+    from fractions import Fraction
+    ratios = [float(v).as_integer_ratio() for v in r]
+    a_ratios = [float(g * gamma).as_integer_ratio() for g in range(1, count + 1)]
+    S = max(den.bit_length() for _, den in ratios + a_ratios)
+    R = [num * ((1 << S) // den) for num, den in ratios]
+    best, bestE = 0, None
+    Es = []
+    for g, (an, ad) in enumerate(a_ratios, start=1):
+        A = an * ((1 << S) // ad)
+        E = 0
+        for x in R:
+            q, rem = divmod(abs(x), A)
+            if 2 * rem > A or (2 * rem == A and q % 2 == 1):
+                q += 1
+            q = min(q, M)
+            e = abs(x) - A * q
+            E += e * e
+        Es.append(Fraction(E, 1 << (2 * S)))
+        if bestE is None or E < bestE:
+            best, bestE = g, E
+    return best, Es
+
+
+def check_paper_search_exact_rational(orc):
+    """Eq. (11) on inputs off any lattice: the oracle's candidate-set argmin
+    against the exact enumeration of the whole grid (rational errors), for
+    both branches of the step, gamma = Delta / M (a step set by the data) and
+    gamma = eta, with d up to 16.  The oracle evaluates in fp64, so its
+    choice may differ from the exact argmin only between errors within
+    rounding (1e-12 relative) of each other."""
+    rng = np.random.default_rng(54)
+    cases = [0, 0]   # grids with gamma = Delta / M, with gamma = eta
+    for bits in (2, 3, 4):
+        M = 2 ** (bits - 1) - 1
+        for case in range(6):
+            d = int(rng.integers(2, 17))
+            fine = case % 2 == 0
+            # random magnitudes, off any lattice: close ones give the step
+            # Delta / M (a fine grid), far apart ones leave eta the smaller
+            gaps = rng.uniform(0.04, 0.3, d) if fine else rng.uniform(0.3, 0.6, d)
+            r = np.cumsum(gaps) * np.where(rng.random(d) < 0.5, -1.0, 1.0)
+            rng.shuffle(r)
+            eta = 1.0 if fine else 2.0 ** -6
+            gamma, count = orc.paper_grid(r, bits, eta)
+            m = np.abs(r)
+            diffs = np.abs(m[:, None] - m[None, :])
+            delta = diffs[diffs > 0].min() / 2
+            assert gamma == min(delta / M, eta), (gamma, delta, M, eta)
+            assert fine == (gamma < eta)
+            if count > 40000:
+                continue
+            cases[0 if fine else 1] += 1
+            gref, Es = _exact_search(r, M, gamma, count)
+            g, Eg = orc.paper_grid_search(r, bits, gamma, count)
+            assert 1 <= g <= count
+            Eo, Er = float(Es[g - 1]), float(Es[gref - 1])
+            assert g == gref or Eo <= Er * (1 + 1e-12), (bits, case, d, g, gref, Eo, Er)
+            assert abs(Eg - Eo) <= 1e-12 * Eo + 1e-300
+    assert min(cases) >= 6, cases
+
+
+def _fl32_exact(F):
+    """The fp32 value nearest the rational F (ties to the even significand)."""
+    from fractions import Fraction
+    x = np.float32(float(F))
+    cands = {x}
+    for _ in range(2):
+        cands |= {np.nextafter(c, np.float32(np.inf)) for c in list(cands)}
+        cands |= {np.nextafter(c, np.float32(-np.inf)) for c in list(cands)}
+    best = None
+    for c in cands:
+        dist = abs(Fraction(float(c)) - F)
+        key = (dist, int(np.array(c, np.float32).view(np.uint32)) & 1)
+        if best is None or key < best[0]:
+            best = (key, c)
+    return best[1]
+
+
+def check_candidate_scales_exact(orc):
+    """Reading G2 at every candidate, not only c = 1: a_g is the fp32 value
+    nearest the exact rational fl32(max|r|) c_g / M, and the default
+    multipliers c_g are the fp32 values nearest g / G; for residuals of
+    many magnitudes, bits 2-8, the default grid and a random one."""
+    from fractions import Fraction
+    rng = np.random.default_rng(56)
+    for G in (7, 128, 512, 1000):
+        c = orc.default_grid(G)
+        for g in range(G):
+            assert c[g] == _fl32_exact(Fraction(g + 1, G)), (G, g)
+    for bits in (2, 3, 4, 5, 8):
+        M = 2 ** (bits - 1) - 1
+        for scale in (1e-30, 3e-7, 0.37, 1.0, 4099.5, 1e30):
+            r = rng.standard_normal(20) * scale
+            m = Fraction(float(np.float32(np.abs(r).max())))
+            for grid in (orc.default_grid(256),
+                         np.sort(rng.uniform(0.01, 1.0, 64)).astype(np.float32)):
+                a = orc.candidate_scales(r, bits, grid)
+                want = [_fl32_exact(m * Fraction(float(cg)) / M) for cg in grid]
+                assert np.array_equal(a, np.array(want, np.float32)), (bits, scale)
+
+
 def check_paper_fit(orc):
     """A fit on the paper's grid: the error never increases, each point's
     scale is fl32 of a grid point, and the verifier accepts it and flags a
@@ -864,10 +1110,13 @@ ALL_CHECKS = [
     check_reconstruct, check_invariances, check_output_error, check_stop_rule,
     check_exponential_decay, check_verifier, check_calib_hadamard_is_isotropic,
     check_calib_stop_definition, check_calib_runs_to_cap, check_calib_zero_batch, check_calib_scaling,
-    check_calib_verifier, check_calib_verifier_fp32_evaluation, check_refit_one_point,
+    check_calib_verifier, check_calib_verifier_fp32_evaluation, check_gate_worked_example,
+    check_gate_definition, check_gate_hadamard_is_isotropic, check_gate_verifier,
+    check_refit_one_point,
     check_refit_residual_chain, check_refit_verifier, check_clip_bruteforce, check_clip_hadamard_is_eq9,
     check_clip_then_algorithm1, check_clip_zero_batch, check_clip_verifier, check_min_gap,
-    check_paper_grid_size, check_paper_search_bruteforce, check_paper_fit, check_asym_translation,
+    check_paper_grid_size, check_paper_search_bruteforce, check_paper_search_exact_rational,
+    check_candidate_scales_exact, check_paper_fit, check_asym_translation,
     check_asym_is_the_centred_fit, check_asym_edges, check_asym_error_and_reconstruct,
     check_asym_verifier, check_integer_scales,
     check_integer_forward_exact, check_integer_forward_one_point, check_integer_forward_approximates,

@@ -95,6 +95,16 @@ MUTANTS = [
     ("asym_error_no_offset", "D[j] = (double)w[j] - (double)beta;", "D[j] = (double)w[j];"),
     ("calib_stop_ignores_cap", "if (n >= P || Er == 0.0) return 1;", "if (Er == 0.0) return 1;"),
     ("calib_no_minimum_one_point", "if (n >= 1 && e <= thr) return 1;", "if (e <= thr) return 1;"),
+    ("gate_keeps_failing_naive",
+     "if (cal ? calib_should_stop(1, P, EN, eN, thr) : should_stop(1, P, EN, Ew, tol)) {",
+     "if (1) {"),
+    ("gate_naive_wrong_step", "oracle_candidate_scales(r, d, M, &one, 1, &aN);    /* a_N = fl32(m / M) */",
+     "oracle_candidate_scales(r, d, M + 1, &one, 1, &aN);"),
+    ("gate_continues_from_naive",
+     "            memset(codes, 0, (size_t)d);                    /* discarded: Algorithm 1 from w */",
+     "            memcpy(r, R, sizeof(double) * (size_t)d);\n            scales[0] = aN;\n"
+     "            err[0] = EN;\n            n = 1;\n            e = eN;"),
+    ("gate_verifier_accepts_any", "if (pass && !nearN) { st = 10; break; }", "if (0) { st = 10; break; }"),
 ]
 
 
