@@ -296,8 +296,17 @@ int mpq_fit_layers_calib(const mpq_layer *layers, int n_layers, int bits, int ma
  *             searched exactly without enumerating it; the chosen scale is
  *             stored as fl32(g * gamma), and the point's codes and residual
  *             use that value.  grid_host and n_grid are ignored.  Only with
- *             the isotropic stopping rule (not with refit, calib or
- *             clip_grid); d <= 8192 (else MPQ_ERR_SHAPE).
+ *             the isotropic stopping rule (not with refit, calib,
+ *             clip_grid, asym or gate); d <= 8192 (else MPQ_ERR_SHAPE).
+ *   gate      nonzero: Algorithm 2's naive first point (Sec. 3.3).  Each
+ *             channel is first quantized naively, a_N = fl32(fl32(max|w|) / M)
+ *             (the candidate c = 1), q = [w / a_N]_Q; if that point already
+ *             meets the threshold of the stopping rule (isotropic:
+ *             ||w - a_N q||^2 <= tol ||w||^2; calib: its output error
+ *             e <= thr), it is the channel's only point; otherwise it is
+ *             discarded and Algorithm 1 runs from w (max_points bounds
+ *             Algorithm 1 only).  Without it point 1 is always Algorithm 1's.
+ *             Not with clip_grid or paper_eta; with calib not with asym.
  * refit, calib and clip_grid need the histogram search for every layer
  * (d <= 32768; else MPQ_ERR_SHAPE).  Errors as for mpq_fit_layers /
  * mpq_fit_layers_calib.
@@ -310,6 +319,7 @@ typedef struct mpq_fit_options {
     int clip_grid;
     float paper_eta;
     int asym;
+    int gate;
 } mpq_fit_options;
 int mpq_fit_layers_ex(const mpq_layer *layers, int n_layers, int bits, int max_points,
                       const float *grid_host, int n_grid, float tol, const mpq_fit_options *opt,

@@ -189,11 +189,11 @@ class Oracle:
 
     def fit_asym(self, W, bits: int, max_points: int, n_grid: int, tol: float = 0.0, X=None,
                  calib: bool = False, eps: float = 0.0, relative: bool = True, refit: bool = False,
-                 grid=None, n_threads: int = 0):
+                 grid=None, n_threads: int = 0, gate: bool = False):
         """Fit with the per-channel offset of reading B2 (the asymmetric set of
         Eq. (1)).  Returns (codes, scales, counts, err, xerr, offsets[C] f32)."""
         return self._fit(W, bits, max_points, n_grid, tol, X, eps, relative, refit, grid, n_threads,
-                         calib=calib, asym=True)
+                         calib=calib, asym=True, gate=gate)
 
     def _fit(self, W, bits, P, n_grid, tol, X, eps, relative, refit, grid, n_threads, calib=None,
              clip_grid=0, eta=0.0, asym=False, gate=False):
@@ -250,12 +250,12 @@ class Oracle:
     def verify_asym(self, W, bits, max_points, n_grid, codes_, scales, counts, offsets, err=None,
                     xerr=None, tol: float = 0.0, X=None, calib: bool = False, eps: float = 0.0,
                     relative: bool = True, refit: bool = False, grid=None, channels=None,
-                    n_threads: int = 0):
+                    n_threads: int = 0, gate: bool = False):
         """Lockstep check of a fit with the per-channel offset of reading B2
         (status 9: an offset that is not the fp32 midpoint)."""
         return self._verify(W, bits, max_points, n_grid, tol, X, eps, relative, refit, codes_,
                             scales, counts, err, xerr, grid, channels, n_threads, calib=calib,
-                            offsets=offsets)
+                            offsets=offsets, gate=gate)
 
     def _verify(self, W, bits, P, n_grid, tol, X, eps, relative, refit, codes_, scales, counts,
                 err, xerr, grid, channels, n_threads, calib=None, clip_grid=0, eta=0.0, offsets=None,

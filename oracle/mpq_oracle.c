@@ -46,10 +46,11 @@
  *   F1     Variant (gate != 0), Algorithm 2's first step: the channel is
  *          first quantized naively, w~ = a_N [w / a_N]_Q with the max-abs
  *          code step a_N = fl32(fl32(max|w|) / M) (fp64 quotient; the
- *          candidate c = 1 of reading G2); if the stopping rule in force
- *          (S1, or S4 on the batch) already holds for that one point, it is
- *          the channel's only point; otherwise it is discarded and
- *          Algorithm 1 runs from r_1 = w as without the gate.  Without the
+ *          candidate c = 1 of reading G2); if its error already meets the
+ *          threshold of the rule in force (S1: ||w - w~||^2 <= tol ||w||^2;
+ *          S4: e <= thr on the batch), it is the channel's only point;
+ *          otherwise it is discarded and Algorithm 1 runs from r_1 = w as
+ *          without the gate (the cap max_points bounds Algorithm 1 only).  Without the
  *          gate (the default) point 1 is Algorithm 1's grid search from the
  *          start, so a channel whose naive point would pass can get a
  *          different first point, and under S4 more points.
@@ -444,7 +445,7 @@ static int fit_channel(const float *w, int64_t d, int M, int P, const float *c,
             for (int64_t j = 0; j < d; ++j) R[j] = r[j] - (double)aN * (double)codes[j];
             const double EN = sum_sq(R, d);
             const double eN = cal ? calib_error(R, d, cal->X, cal->N) : 0.0;
-            if (cal ? calib_should_stop(1, P, EN, eN, thr) : should_stop(1, P, EN, Ew, tol)) {
+            if (cal ? eN <= thr : EN <= tol * Ew) {            /* Algorithm 2's test */
                 memcpy(r, R, sizeof(double) * (size_t)d);  /* kept: the only point */
                 scales[0] = aN;
                 err[0] = EN;
@@ -788,8 +789,7 @@ static int verify_layer(const float *W, int64_t C, int64_t d, int bits, int P,
                                 R[j] = r[j] - (double)aN * nearest_code(r[j] / (double)aN, M);
                             const double EN = sum_sq(R, d);
                             const double eN = cal ? calib_error(R, d, cal->X, cal->N) : 0.0;
-                            const int pass = cal ? calib_should_stop(1, P, EN, eN, thr)
-                                                 : should_stop(1, P, EN, Ew, tol);
+                            const int pass = cal ? eN <= thr : EN <= tol * Ew;
                             int nearN = 0;
                             if (cal) {
                                 nearN = fabs(eN - thr) <= 1e-5 * thr +
@@ -962,7 +962,10 @@ static void channel_residual(const float *w, float beta, const int8_t *q, const 
 
 /* Eq. (12): err[k] = (1/N) sum_n ((w_k - w~_k) . x_n)^2 and, if ref is not
  * NULL, ref[k] = (1/N) sum_n (w_k . x_n)^2, for the listed channels
- * (chan == NULL: all C channels, outputs indexed by channel). */
+ * (chan == NULL: all C channels, outputs indexed by channel).  Every dot
+ * product sums over j in index order and the squares over n in column
+ * order; X is first copied to column-contiguous rows, and four columns'
+ * dot products run side by side, which changes no operation of any sum. */
 int oracle_output_error_ex(const float *W, const float *offsets, const int8_t *codes,
                            const float *scales, const int32_t *counts, int64_t C, int64_t d, int P,
                            const float *X, int64_t N, const int64_t *chan,
@@ -970,6 +973,10 @@ int oracle_output_error_ex(const float *W, const float *offsets, const int8_t *c
 {
     int nt = n_threads_or_default(n_threads);
     int64_t cnt = chan ? n_chan : C;
+    float *Xt = (float *)malloc(sizeof(float) * (size_t)(N * d));   /* Xt[n][j] = X[j][n] */
+    if (!Xt) return -1;
+    for (int64_t j = 0; j < d; ++j)
+        for (int64_t n = 0; n < N; ++n) Xt[n * d + j] = X[j * N + n];
     int fail = 0;
 #pragma omp parallel num_threads(nt)
     {
@@ -985,10 +992,26 @@ int oracle_output_error_ex(const float *W, const float *offsets, const int8_t *c
                 channel_residual(w, offsets ? offsets[k] : 0.0f, codes + k * P * d, scales + k * P,
                                  counts[k], d, D);
                 double se = 0.0, sr = 0.0;
-                for (int64_t n = 0; n < N; ++n) {
+                int64_t n = 0;
+                for (; n + 4 <= N; n += 4) {
+                    double y[4] = {0.0, 0.0, 0.0, 0.0}, yr[4] = {0.0, 0.0, 0.0, 0.0};
+                    const float *x0 = Xt + n * d;
+                    for (int64_t j = 0; j < d; ++j) {
+                        for (int u = 0; u < 4; ++u) {
+                            double x = (double)x0[u * d + j];
+                            y[u] += D[j] * x;
+                            yr[u] += (double)w[j] * x;
+                        }
+                    }
+                    for (int u = 0; u < 4; ++u) {
+                        se += y[u] * y[u];
+                        sr += yr[u] * yr[u];
+                    }
+                }
+                for (; n < N; ++n) {
                     double y = 0.0, yr = 0.0;
                     for (int64_t j = 0; j < d; ++j) {
-                        double x = (double)X[j * N + n];
+                        double x = (double)Xt[n * d + j];
                         y += D[j] * x;
                         yr += (double)w[j] * x;
                     }
@@ -1001,6 +1024,7 @@ int oracle_output_error_ex(const float *W, const float *offsets, const int8_t *c
         }
         free(D);
     }
+    free(Xt);
     return fail ? -1 : 0;
 }
 

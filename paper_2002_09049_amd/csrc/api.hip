@@ -411,7 +411,7 @@ int require_hist(const mpq_layer *layers, int n_layers, bool hist_fits, const ch
 
 int fit_layers_impl(Search mode, const mpq_layer *layers, int n_layers, int bits, int max_points,
                     const float *grid_host, int n_grid, float tol, void *stream, int refit = 0,
-                    int clip_grid = 0, int asym = 0)
+                    int clip_grid = 0, int asym = 0, int gate = 0)
 {
     if (asym && n_layers > 0 && layers) {
         for (int l = 0; l < n_layers; ++l)
@@ -430,6 +430,8 @@ int fit_layers_impl(Search mode, const mpq_layer *layers, int n_layers, int bits
     if (clip_grid && (rc = require_hist(layers, n_layers, hist_fits, "the clipping")) != MPQ_OK)
         return rc;
     if (asym && (rc = require_hist(layers, n_layers, hist_fits, "asym")) != MPQ_OK) return rc;
+    if (gate && (rc = require_hist(layers, n_layers, hist_fits, "the naive first point")) != MPQ_OK)
+        return rc;
     hipStream_t s = (hipStream_t)stream;
     float *dgrid = nullptr;
     rc = upload_grid(grid_host, n_grid, s, &dgrid);
@@ -437,9 +439,11 @@ int fit_layers_impl(Search mode, const mpq_layer *layers, int n_layers, int bits
     const int M = (1 << (bits - 1)) - 1;
     std::vector<FitJob> jobs = build_fit_jobs(mode, hist_fits, layers, n_layers, M, max_points,
                                               dgrid, n_grid, tol, -1.0, refit);
-    if (asym)
-        for (FitJob &j : jobs)
+    for (FitJob &j : jobs) {
+        j.b.gate = gate;
+        if (asym)
             for (int i = 0; i < j.b.n_layers; ++i) j.b.L[i].offsets = layers[j.layers[i]].offsets;
+    }
     if (clip_grid) {   // point 1 from the clipping, then the fit resumes from it
         rc = clip_first_points(layers, n_layers, M, max_points, clip_grid, false, {}, s);
         if (rc != MPQ_OK) {
@@ -803,7 +807,7 @@ int clip_first_points(const mpq_layer *layers, int n_layers, int M, int P, int G
 // threshold's output error of W runs beside the first fit step.
 int calib_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
                const float *grid_host, int n_grid, float eps, int relative, void *stream,
-               int refit = 0, int clip_grid = 0, int asym = 0)
+               int refit = 0, int clip_grid = 0, int asym = 0, int gate = 0)
 {
     if (asym && n_layers > 0 && layers) {
         for (int l = 0; l < n_layers; ++l)
@@ -867,6 +871,7 @@ int calib_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
                                               n_grid, 0.0f, -1.0, refit);
     for (FitJob &j : jobs) {
         j.b.eps = (double)eps;
+        j.b.gate = gate;   // read at step 0 only
         for (int i = 0; i < j.b.n_layers; ++i) {
             const int l = j.layers[i];
             mpq::HistLayer &H = j.b.L[i];
@@ -908,15 +913,19 @@ int calib_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
     std::vector<double> fit_work;
     for (const FitJob &j : jobs) fit_work.push_back(j.work);
     int first = 0;
-    if (clip_grid && e == hipSuccess) {
-        // point 1 from the clipping (its output error is e_1), with the
-        // reference errors of the relative threshold in the same pass
-        rc = clip_first_points(layers, n_layers, M, P, clip_grid, true, in_ref, s);
+    // point 1 from the clipping, or (gate, reading F1) the naive point: the
+    // one clipping candidate c = 1, so fl32(max|w|) / M; its output error is
+    // e_1.  The reference errors of the relative threshold ride in the same
+    // pass.  A clipped fit continues from point 1; a gated one decides at
+    // step 0 whether the naive point stays or the fit restarts from w.
+    const bool pre = clip_grid || gate;
+    if (pre && e == hipSuccess) {
+        rc = clip_first_points(layers, n_layers, M, P, clip_grid ? clip_grid : 1, true, in_ref, s);
         if (rc != MPQ_OK) {
             release();
             return rc;
         }
-        first = 1;
+        first = clip_grid ? 1 : 0;
     }
     for (int step = first; step < P && e == hipSuccess; ++step) {
         for (FitJob &j : jobs) {
@@ -926,7 +935,7 @@ int calib_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
         // the fit step; at step 0 beside it the output error of W (ref)
         std::vector<double> w = fit_work;
         const int n_fit = (int)w.size();
-        if (step == 0 && !clip_grid) w.insert(w.end(), ej_ref.work.begin(), ej_ref.work.end());
+        if (step == 0 && !pre) w.insert(w.end(), ej_ref.work.begin(), ej_ref.work.end());
         e = run_concurrently(s, w, [&](int i, hipStream_t st) {
             return i < n_fit ? launch_fit_job(jobs[i], n_grid, st)
                              : launch_err_job(in_ref, ej_ref, i - n_fit, P, st);
@@ -1225,9 +1234,9 @@ int mpq_fit_layers_ex(const mpq_layer *layers, int n_layers, int bits, int max_p
                       void *stream)
 {
     if (opt && opt->paper_eta != 0.0f) {
-        if (opt->calib || opt->refit || opt->clip_grid || opt->asym)
+        if (opt->calib || opt->refit || opt->clip_grid || opt->asym || opt->gate)
             return fail(MPQ_ERR_INVALID_ARG,
-                        "paper_eta cannot be combined with calib, refit, clip_grid or asym");
+                        "paper_eta cannot be combined with calib, refit, clip_grid, asym or gate");
         return paper_impl(layers, n_layers, bits, max_points, tol, opt->paper_eta, stream);
     }
     if (!opt) return fit_layers_impl(Search::kAuto, layers, n_layers, bits, max_points, grid_host,
@@ -1237,11 +1246,16 @@ int mpq_fit_layers_ex(const mpq_layer *layers, int n_layers, int bits, int max_p
     if (opt->asym && opt->clip_grid)
         return fail(MPQ_ERR_INVALID_ARG, "asym and clip_grid cannot be combined");
     if (opt->clip_grid < 0) return fail(MPQ_ERR_INVALID_ARG, "clip_grid must be >= 0");
+    if (opt->gate && opt->clip_grid)
+        return fail(MPQ_ERR_INVALID_ARG, "gate and clip_grid cannot be combined");
+    if (opt->gate && opt->calib && opt->asym)
+        return fail(MPQ_ERR_INVALID_ARG, "gate and asym cannot be combined with calib");
     if (opt->calib)
         return calib_impl(layers, n_layers, bits, max_points, grid_host, n_grid, opt->eps,
-                          opt->relative, stream, opt->refit != 0, opt->clip_grid, opt->asym != 0);
+                          opt->relative, stream, opt->refit != 0, opt->clip_grid, opt->asym != 0,
+                          opt->gate != 0);
     return fit_layers_impl(Search::kAuto, layers, n_layers, bits, max_points, grid_host, n_grid, tol,
-                           stream, opt->refit != 0, opt->clip_grid, opt->asym != 0);
+                           stream, opt->refit != 0, opt->clip_grid, opt->asym != 0, opt->gate != 0);
 }
 
 int mpq_output_error(const float *W, const int8_t *codes, const float *scales,

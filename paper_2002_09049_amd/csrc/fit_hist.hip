@@ -399,7 +399,19 @@ fit_hist_kernel(const HistBatch B)
     float apend = 0.0f;
     int n = 0;
     bool more = false;   // calibration step: the channel took its point and goes on
-    for (int i = s0;; ++i) {
+    // Algorithm 2's naive point (reading F1).  Calibration fit, first step:
+    // the point is stored with its output error; the channel keeps it (and
+    // takes no other) when that error meets the threshold.  Fresh fit:
+    // gstate 1 takes the naive point at step 0, gstate 2 decides at step 1,
+    // after it is applied, whether it stays or the fit restarts from w.
+    bool kept = false;
+    if (B.gate && stepping && s0 == 0) {
+        const double thr = Ly.ref ? B.eps * (double)Ly.ref[k] : B.eps;
+        kept = Ly.counts[k] == 1 && (double)Ly.xerr[k * P] <= thr;   // uniform
+        if (kept) n = 1;
+    }
+    int gstate = (B.gate && !stepping && s0 == 0) ? 1 : 0;
+    for (int i = s0; !kept; ++i) {
         // ---- apply the pending point: codes of Eq. (10), residual of Eq. (7)
         float lmax = 0.0f;
         double lsum = 0.0;
@@ -430,7 +442,7 @@ fit_hist_kernel(const HistBatch B)
         // the scale the residual update uses: the searched one, or (refit)
         // the least-squares scale of the codes, fl32(<r, q> / <q, q>)
         double aupd = ap;
-        if (B.refit && i > s0) {
+        if (B.refit && i > s0 && gstate != 2) {   // the naive point keeps its scale
             double rq = 0.0, qq = 0.0;
 #pragma unroll kUnroll
             for (int u = 0; u < EPT; ++u) {
@@ -459,7 +471,7 @@ fit_hist_kernel(const HistBatch B)
             double ru = kGlobal ? rebuild(u, i > s0 ? i - 1 : i) : r[u];
             if (i > s0 && j < d) {
                 const double c = code_of(ru);
-                if (!B.refit) qrow[j] = (int8_t)(int)c;
+                if (!B.refit || gstate == 2) qrow[j] = (int8_t)(int)c;
                 ru = fma(-aupd, c, ru);
             }
             if constexpr (!kGlobal) {
@@ -497,9 +509,39 @@ fit_hist_kernel(const HistBatch B)
                 stop = Er <= B.tol * Ew;
             }
         }
+        if (gstate == 2) {   // step 1 of a gated fit: the naive point is applied
+            gstate = 0;
+            if (Er <= B.tol * Ew) {   // Algorithm 2's test: the only point
+                n = 1;
+                break;
+            }
+            // discarded: restart from w (its codes, scale and err are
+            // rewritten by the point that replaces it)
+            if constexpr (!kGlobal) {
+#pragma unroll
+                for (int u = 0; u < EPT; ++u) r[u] = rebuild(u, 0);
+            }
+            i = -1;
+            __syncthreads();   // the next step's reduction rewrites s_redf, s_redd
+            continue;
+        }
         if (stop) {
             n = i;
             break;
+        }
+        if (gstate == 1) {   // step 0 of a gated fit: the naive point first
+            gstate = 0;
+            const float aN = (float)((double)m / Md);   // the candidate c = 1
+            if (aN != 0.0f) {
+                gstate = 2;
+                apend = aN;
+                if (t == 0) {
+                    Ly.scales[k * P] = aN;
+                    s_scale[0] = aN;
+                }
+                __syncthreads();   // s_scale (rebuilt residual); s_redf, s_redd
+                continue;
+            }
         }
 
         // ---- candidates, cleared histograms

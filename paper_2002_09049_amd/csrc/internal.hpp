@@ -104,6 +104,13 @@ struct HistBatch {
     double eps;
     // reading A2: each point's scale refitted by least squares for its codes
     int refit;
+    // reading F1, Algorithm 2's naive point first.  A fresh fit (start 0,
+    // single 0) applies the point (fl32(max|w|) / M, [w / a]_Q), keeps it as
+    // the only point when ||r||^2 <= tol ||w||^2, and otherwise restarts from
+    // w.  A calibration fit's first step (start 0, single != 0) finds the
+    // naive point already stored (count 1, its output error in xerr) and
+    // keeps it when xerr <= thr; every other channel restarts from w.
+    int gate;
     HistLayer L[kMaxBatchLayers];
 };
 static_assert(sizeof(HistBatch) <= 4096, "kernel arguments");

@@ -51,7 +51,7 @@ class FitOptions(ctypes.Structure):
     """struct mpq_fit_options (include/mpq.h)."""
     _fields_ = [("refit", ctypes.c_int), ("calib", ctypes.c_int), ("eps", ctypes.c_float),
                 ("relative", ctypes.c_int), ("clip_grid", ctypes.c_int),
-                ("paper_eta", ctypes.c_float), ("asym", ctypes.c_int)]
+                ("paper_eta", ctypes.c_float), ("asym", ctypes.c_int), ("gate", ctypes.c_int)]
 
 
 class IntLayer(ctypes.Structure):
@@ -412,16 +412,18 @@ class LayerSet:
 
     def fit_ex(self, bits: int, n_grid: int, tol: float = 0.0, refit: bool = False,
                calib: bool = False, eps: float = 0.0, relative: bool = True, clip_grid: int = 0,
-               paper_eta: float = 0.0, asym: bool = False, grid=None, stream=None):
+               paper_eta: float = 0.0, asym: bool = False, gate: bool = False, grid=None,
+               stream=None):
         """mpq_fit_layers_ex: the fit with options (refit: reading A2; calib:
         Algorithm 2's stopping rule on the calibration batches; clip_grid:
         point 1 from the clipping of Eq. (13) with that many factors;
-        paper_eta: the paper's own grid of Eq. (11) with that maximal step)."""
+        paper_eta: the paper's own grid of Eq. (11) with that maximal step;
+        gate: Algorithm 2's naive first point, reading F1)."""
         if (calib or clip_grid) and self.X is None:
             raise ValueError("LayerSet was built without calibration batches")
         g = self._grid(grid, n_grid)
         opt = FitOptions(1 if refit else 0, 1 if calib else 0, float(eps), 1 if relative else 0,
-                         int(clip_grid), float(paper_eta), 1 if asym else 0)
+                         int(clip_grid), float(paper_eta), 1 if asym else 0, 1 if gate else 0)
         # the offsets take part in the fit and, afterwards, in the layer's
         # output error and reconstruction only when the fit is asymmetric
         for i in range(self.n):

@@ -532,7 +532,9 @@ def check_gate_definition(orc):
     without the gate (Algorithm 1 from w)."""
     W, X = _calib_case(seed=31, C=24, d=40, N=50)
     Xd = X.astype(np.float64)
-    for bits, P, G in ((4, 6, 64), (3, 5, 32)):
+    # P = 1: the cap bounds Algorithm 1 only, so a failing naive point still
+    # gives way to Algorithm 1's first point
+    for bits, P, G in ((4, 6, 64), (3, 5, 32), (4, 1, 64)):
         eN, EN = [], []
         for k in range(W.shape[0]):
             a, q = _naive_point(W[k], bits)

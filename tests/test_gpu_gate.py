@@ -1,0 +1,216 @@
+"""Parity of Algorithm 2's naive first point (Sec. 3.3, reading F1) with the
+oracle, through the C ABI (mpq_fit_layers_ex with gate).
+
+A channel is first quantized naively, (a_N, [w / a_N]_Q) with
+a_N = fl32(fl32(max|w|) / M); if that point already meets the threshold of
+the stopping rule in force it is the channel's only point, otherwise
+Algorithm 1 runs from w.  The oracle's lockstep verifier (gate mode) accepts
+the naive point only where its error meets the threshold (or ties with it)
+and flags the opposite decision with status 10.  Thresholds are placed at
+the median of the channels' naive errors (numpy fp64 of the naive points), so
+about half the channels keep their naive point."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from gpu_util import say, to_dev
+from paper_2002_09049_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "worked_examples.json")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from paper_2002_09049_amd import mpq
+    mpq.load()
+    yield
+
+
+def _fit_gate(W, bits, P, G, tol=0.0, X=None, eps=0.0, relative=True, refit=False, asym=False):
+    import torch
+    from paper_2002_09049_amd import mpq
+    ls = mpq.LayerSet([to_dev(W)], P, calib=None if X is None else [to_dev(X)])
+    ls.fit_ex(bits, G, tol, refit=refit, calib=X is not None, eps=eps, relative=relative,
+              asym=asym, gate=True)
+    torch.cuda.synchronize()
+    out = (ls.codes[0].cpu().numpy(), ls.scales[0].cpu().numpy(), ls.counts[0].cpu().numpy(),
+           ls.fit_err[0].cpu().numpy())
+    if X is not None:
+        out = out + (ls.xerr[0].cpu().numpy(),)
+    if asym:
+        out = out + (ls.offsets[0].cpu().numpy(),)
+    return out
+
+
+def _ok(v):
+    bad = np.nonzero(v["status"])[0]
+    assert bad.size == 0, (f"{bad.size} channels fail: channels {v['channels'][bad][:8]} "
+                           f"status {v['status'][bad][:8]}")
+
+
+def _naive(W, bits, beta=None):
+    """The naive points (a_N [C], codes [C, d]) and residuals, numpy."""
+    M = 2 ** (bits - 1) - 1
+    Wd = W.astype(np.float64) - (0.0 if beta is None else beta.astype(np.float64)[:, None])
+    m = np.abs(Wd).max(axis=1).astype(np.float32).astype(np.float64)
+    a = (m / M).astype(np.float32)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        q = np.where(a[:, None] > 0, np.clip(np.round(Wd / a[:, None].astype(np.float64)), -M, M), 0)
+    R = Wd - a[:, None].astype(np.float64) * q
+    return a, q.astype(np.int8), R
+
+
+def _kept(counts, scales, codes, a, q):
+    return (counts == 1) & (scales[:, 0] == a) & (codes[:, 0] == q).all(axis=1)
+
+
+def test_gate_worked_example():
+    g = next(c for c in json.load(open(GOLDEN))["cases"] if c["name"] == "naive_first_gate")
+    W = np.array([g["w"]], np.float32)
+    for v in g["variants"]:
+        say(f"case gate golden X={v['X']}")
+        X = np.array(v["X"], np.float32)
+        codes, scales, counts, err, xerr = _fit_gate(W, g["bits"], g["max_points"], g["n_grid"],
+                                                     X=X, eps=g["eps"], relative=False)
+        e = v["gate"]
+        assert counts[0] == e["count"] and scales[0].tolist() == e["scales"]
+        assert codes[0].tolist() == e["codes"] and xerr[0].tolist() == e["xerr"]
+
+
+GATE = [
+    # (C, d, bits, P, G, N): the variants of the fit kernel (64 x 1 ... the
+    # 1024 x 32 variant that rebuilds its residual)
+    (5, 1, 4, 4, 128, 7),
+    (60, 9, 4, 8, 512, 64),
+    (64, 147, 4, 4, 256, 300),
+    (64, 576, 3, 6, 128, 256),
+    (20, 2304, 4, 8, 256, 512),
+    (9, 4608, 3, 8, 512, 257),
+    (5, 9000, 4, 4, 64, 100),
+    (4, 20000, 3, 4, 256, 64),
+]
+
+
+@pytest.mark.parametrize("C,d,bits,P,G,N", GATE, ids=[f"C{c}_d{d}_b{b}_P{p}_G{g}_N{n}" for c, d, b, p, g, n in GATE])
+def test_gate_calib_parity(orc, C, d, bits, P, G, N):
+    """Algorithm 2's rule on the batch with the naive first point, absolute
+    threshold (the paper's) and relative."""
+    W = wl.random_weights(C, d, seed=5 * C + d)
+    X = wl.random_calib(d, N, seed=N + 1)
+    a, q, R = _naive(W, bits)
+    eN = np.mean((R @ X.astype(np.float64)) ** 2, axis=1)
+    ref = np.mean((W.astype(np.float64) @ X.astype(np.float64)) ** 2, axis=1)
+    for relative, eps in ((False, float(np.median(eN))), (True, float(np.median(eN / ref)))):
+        eps32 = float(np.float32(eps))
+        say(f"case gate calib C={C} d={d} bits={bits} P={P} G={G} N={N} relative={relative}")
+        codes, scales, counts, err, xerr = _fit_gate(W, bits, P, G, X=X, eps=eps32, relative=relative)
+        v = orc.verify_calib(W, bits, P, G, X, eps32, relative, codes, scales, counts, err, xerr,
+                             gate=True)
+        _ok(v)
+        kept = _kept(counts, scales, codes, a, q)
+        say(f"  kept naive: {int(kept.sum())} of {C}; stop ties {int(v['stop_ties'].sum())}")
+        if C >= 9:
+            assert 0 < kept.sum() < C
+
+
+@pytest.mark.parametrize("C,d,bits,P,G,N", GATE[1:6], ids=[f"C{c}_d{d}" for c, d, *_ in GATE[1:6]])
+def test_gate_isotropic_parity(orc, C, d, bits, P, G, N):
+    """The isotropic rule with the naive first point: kept when
+    ||w - a_N q||^2 <= tol ||w||^2; also with the refit of later points and
+    with asymmetric codes."""
+    W = wl.random_weights(C, d, seed=7 * C + d)
+    a, q, R = _naive(W, bits)
+    ratio = (R ** 2).sum(axis=1) / (W.astype(np.float64) ** 2).sum(axis=1)
+    tol = float(np.float32(np.median(ratio)))
+    say(f"case gate isotropic C={C} d={d} bits={bits} P={P} G={G} tol={tol:.3g}")
+    codes, scales, counts, err = _fit_gate(W, bits, P, G, tol=tol)
+    _ok(orc.verify(W, bits, P, G, tol, codes, scales, counts, err, gate=True))
+    kept = _kept(counts, scales, codes, a, q)
+    assert 0 < kept.sum() < C
+    codes, scales, counts, err = _fit_gate(W, bits, P, G, tol=tol, refit=True)
+    _ok(orc.verify(W, bits, P, G, tol, codes, scales, counts, err, gate=True, refit=True))
+    codes, scales, counts, err, off = _fit_gate(W, bits, P, G, tol=tol, asym=True)
+    _ok(orc.verify_asym(W, bits, P, G, codes, scales, counts, off, err, tol=tol, gate=True))
+
+
+def test_gate_edges(orc):
+    """Zero, subnormal and equal-magnitude channels; a cap of one point (a
+    failing naive point gives way to Algorithm 1's)."""
+    d, N = 40, 32
+    rng = np.random.default_rng(9)
+    W = np.zeros((6, d), np.float32)
+    W[1, :3] = [1e-45, 0.0, -1e-45]
+    W[2] = 0.3 * np.sign(rng.standard_normal(d))
+    W[3:] = rng.standard_normal((3, d))
+    X = wl.random_calib(d, N, seed=3)
+    for P in (1, 4):
+        say(f"case gate edges P={P}")
+        codes, scales, counts, err, xerr = _fit_gate(W, 4, P, 64, X=X, eps=1e-3, relative=True)
+        _ok(orc.verify_calib(W, 4, P, 64, X, float(np.float32(1e-3)), True, codes, scales, counts,
+                             err, xerr, gate=True))
+        assert counts[0] == 0 and counts[1] == 0 and counts[2] == 1
+        codes, scales, counts, err = _fit_gate(W, 4, P, 64, tol=1e-3)
+        _ok(orc.verify(W, 4, P, 64, float(np.float32(1e-3)), codes, scales, counts, err, gate=True))
+
+
+def test_gate_with_refit_calib(orc):
+    C, d, N = 50, 576, 256
+    W = wl.random_weights(C, d, seed=19)
+    X = wl.random_calib(d, N, seed=20)
+    a, q, R = _naive(W, 4)
+    eps = float(np.float32(np.median(np.mean((R @ X.astype(np.float64)) ** 2, axis=1))))
+    say("case gate + refit + Algorithm 2 rule (absolute)")
+    codes, scales, counts, err, xerr = _fit_gate(W, 4, 6, 128, X=X, eps=eps, relative=False, refit=True)
+    _ok(orc.verify_calib(W, 4, 6, 128, X, eps, False, codes, scales, counts, err, xerr, refit=True,
+                         gate=True))
+
+
+def test_gate_workload_resnet18_sampled(orc):
+    """Every ResNet-18 layer at full size, one call, absolute threshold (the
+    paper's form): a sample of channels of every layer in lockstep."""
+    import torch
+    from paper_2002_09049_amd import mpq
+    w = wl.get("resnet18")
+    idx = list(range(len(w.layers)))
+    Ws = [to_dev(wl.layer_weights(w, i)) for i in idx]
+    Xs = [to_dev(wl.layer_calib(w, i, n=256)) for i in idx]
+    # the absolute threshold: the median naive output error of layer 10
+    W10, X10 = Ws[10].cpu().numpy(), Xs[10].cpu().numpy()
+    _, _, R = _naive(W10, w.bits)
+    eps = float(np.float32(np.median(np.mean((R @ X10.astype(np.float64)) ** 2, axis=1))))
+    say(f"case gate resnet18 full size, eps={eps:.4g}")
+    ls = mpq.LayerSet(Ws, w.max_points, calib=Xs)
+    ls.fit_ex(w.bits, w.n_grid, calib=True, eps=eps, relative=False, gate=True)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(4)
+    kept_total = 0
+    for li, (C, d) in enumerate(w.layers):
+        ch = np.unique(np.concatenate([[0, C - 1], rng.choice(C, size=min(8, C), replace=False)]))
+        W = Ws[li].cpu().numpy()
+        out = (ls.codes[li].cpu().numpy(), ls.scales[li].cpu().numpy(), ls.counts[li].cpu().numpy(),
+               ls.fit_err[li].cpu().numpy(), ls.xerr[li].cpu().numpy())
+        _ok(orc.verify_calib(W, w.bits, w.max_points, w.n_grid, Xs[li].cpu().numpy(), eps, False,
+                             *out, channels=ch, gate=True))
+        a, q, _ = _naive(W, w.bits)
+        kept_total += int(_kept(out[2], out[1], out[0], a, q).sum())
+    say(f"  channels keeping their naive point: {kept_total}")
+    assert kept_total > 0
+
+
+def test_gate_rejections():
+    import torch
+    from paper_2002_09049_amd import mpq
+    W = to_dev(wl.random_weights(4, 64, seed=1))
+    X = to_dev(wl.random_calib(64, 8, seed=1))
+    ls = mpq.LayerSet([W], 4, calib=[X])
+    for kw in (dict(clip_grid=20), dict(paper_eta=2.0 ** -10), dict(calib=True, eps=1e-3, asym=True)):
+        with pytest.raises(mpq.MPQError) as e:
+            ls.fit_ex(4, 64, 1e-3, gate=True, **kw)
+        assert e.value.status == mpq.MPQ_ERR_INVALID_ARG
+    torch.cuda.synchronize()

@@ -36,7 +36,7 @@ MUTANTS = [
     ("stop_ignores_cap", "if (n >= P) return 1;", "if (n > P) return 1;"),
     ("err_before_update", "err[n - 1] = sum_sq(r, d);", "err[n - 1] = Er;"),
     ("codes_at_wrong_scale", "oracle_codes(r, d, as, M, q);", "oracle_codes(r, d, (double)a[0], M, q);"),
-    ("x_transposed", "double x = (double)X[j * N + n];", "double x = (double)X[n * d + j];"),
+    ("x_transposed", "Xt[n * d + j] = X[j * N + n];", "Xt[n * d + j] = X[n * d + j];"),
     ("output_error_not_mean", "err[s] = se / (double)N;", "err[s] = se;"),
     ("reconstruct_drops_last_point", "for (int i = 0; i < counts[k]; ++i)\n                s = s +",
      "for (int i = 0; i + 1 < counts[k]; ++i)\n                s = s +"),
@@ -95,8 +95,7 @@ MUTANTS = [
     ("asym_error_no_offset", "D[j] = (double)w[j] - (double)beta;", "D[j] = (double)w[j];"),
     ("calib_stop_ignores_cap", "if (n >= P || Er == 0.0) return 1;", "if (Er == 0.0) return 1;"),
     ("calib_no_minimum_one_point", "if (n >= 1 && e <= thr) return 1;", "if (e <= thr) return 1;"),
-    ("gate_keeps_failing_naive",
-     "if (cal ? calib_should_stop(1, P, EN, eN, thr) : should_stop(1, P, EN, Ew, tol)) {",
+    ("gate_keeps_failing_naive", "if (cal ? eN <= thr : EN <= tol * Ew) {            /* Algorithm 2's test */",
      "if (1) {"),
     ("gate_naive_wrong_step", "oracle_candidate_scales(r, d, M, &one, 1, &aN);    /* a_N = fl32(m / M) */",
      "oracle_candidate_scales(r, d, M + 1, &one, 1, &aN);"),
