@@ -150,6 +150,29 @@ int mpq_output_error(const float *W, const int8_t *codes, const float *scales,
                      const float *X, int64_t n, float *err, float *ref_opt, void *stream);
 
 /*
+ * mpq_output_error_noalloc - mpq_output_error for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, kernels and results
+ * (bitwise those of mpq_output_error on the same inputs); the call
+ * allocates nothing.  Its workspace (the residual rows in tiles, row
+ * partials and per-K-range outputs) is a fixed array of MPQ_NOALLOC_BYTES
+ * per device, held by the library from the moment its code loads on that
+ * device until the process ends.  A call whose workspace would exceed it
+ * (about 4 ceil(c_out / 128) 128 ceil(d / 32) 32 bytes for the residual,
+ * doubled with ref_opt, plus 8 c_out ceil(n / 128) and, for long d,
+ * 4 c_out n per K range) returns MPQ_ERR_SHAPE before anything is enqueued.
+ * Every call on one device shares that device's array and leaves its
+ * contents behind: calls that overlap on one device (on different streams,
+ * or from different threads before the first finishes) race and must be
+ * ordered by the caller.  Errors: MPQ_ERR_INVALID_ARG, MPQ_ERR_SHAPE,
+ * MPQ_ERR_HIP.
+ */
+#define MPQ_NOALLOC_BYTES (64 << 20)
+int mpq_output_error_noalloc(const float *W, const int8_t *codes, const float *scales,
+                             const int32_t *counts, int64_t c_out, int64_t d, int max_points,
+                             const float *X, int64_t n, float *err, float *ref_opt, void *stream);
+
+/*
  * mpq_reconstruct - the quantized weights of Eq. (4):
  *   W_hat[k][j] = fl32( sum_{i<counts[k]} scales[k][i] * codes[k][i][j] ),
  * summed in fp64 in point order.

@@ -508,9 +508,14 @@ struct ErrJobs {
     std::vector<size_t> off;
     std::vector<double> work;
     char *scratch = nullptr;
+    bool owned = true;   // allocated by err_jobs (else a caller-held block)
 };
 
-int err_jobs(const std::vector<mpq::ErrLayerIn> &in, hipStream_t s, ErrJobs *j)
+// fixed != nullptr: the groups' scratch is that caller-held block of
+// fixed_bytes (nothing is allocated); a call that needs more fails with
+// MPQ_ERR_SHAPE.
+int err_jobs(const std::vector<mpq::ErrLayerIn> &in, hipStream_t s, ErrJobs *j,
+             char *fixed = nullptr, size_t fixed_bytes = 0)
 {
     const int ng = mpq::err_group_count(in.data(), (int)in.size());
     size_t total = 0;
@@ -518,6 +523,14 @@ int err_jobs(const std::vector<mpq::ErrLayerIn> &in, hipStream_t s, ErrJobs *j)
         j->off.push_back(total);
         total += (mpq::err_group_scratch_bytes(in.data(), (int)in.size(), g) + 255) / 256 * 256;
         j->work.push_back(mpq::err_group_flop(in.data(), (int)in.size(), g));
+    }
+    if (fixed) {
+        if (total > fixed_bytes)
+            return fail(MPQ_ERR_SHAPE, "the output error needs %zu bytes of workspace; the fixed "
+                        "workspace holds %zu", total, fixed_bytes);
+        j->scratch = fixed;
+        j->owned = false;
+        return MPQ_OK;
     }
     const hipError_t e = mpq::scratch_alloc((void **)&j->scratch, total, s);
     if (e != hipSuccess) {
@@ -533,7 +546,8 @@ hipError_t launch_err_job(const std::vector<mpq::ErrLayerIn> &in, const ErrJobs 
     return mpq::launch_output_error_group(in.data(), (int)in.size(), g, P, j.scratch + j.off[g], st);
 }
 
-int output_error_impl(const mpq_layer *layers, int n_layers, int max_points, void *stream)
+int output_error_impl(const mpq_layer *layers, int n_layers, int max_points, void *stream,
+                      char *fixed = nullptr, size_t fixed_bytes = 0)
 {
     if (n_layers < 0 || (n_layers > 0 && !layers))
         return fail(MPQ_ERR_INVALID_ARG, "layers must hold n_layers >= 0 entries");
@@ -551,13 +565,42 @@ int output_error_impl(const mpq_layer *layers, int n_layers, int max_points, voi
     if (in.empty()) return MPQ_OK;
     hipStream_t s = (hipStream_t)stream;
     ErrJobs jobs;
-    int rc = err_jobs(in, s, &jobs);
+    int rc = err_jobs(in, s, &jobs, fixed, fixed_bytes);
     if (rc != MPQ_OK) return rc;
     const hipError_t e = run_concurrently(s, jobs.work, [&](int i, hipStream_t st) {
         return launch_err_job(in, jobs, i, max_points, st);
     });
-    if (jobs.scratch) (void)mpq::scratch_free(jobs.scratch, s);
+    if (jobs.scratch && jobs.owned) (void)mpq::scratch_free(jobs.scratch, s);
     if (e != hipSuccess) return hip_fail(e, "output error kernel launch");
+    return MPQ_OK;
+}
+
+// The workspace of mpq_output_error_noalloc: one array per device, part of
+// the library's code object, so it is in device memory from the moment the
+// library's kernels load until the process ends and no call allocates it.
+// Host code never passes its name to a kernel (on the host the name is a
+// stand-in, not a device address): each device's address comes from
+// hipGetSymbolAddress, once, with that device current.
+static __device__ __align__(256) char scratch[MPQ_NOALLOC_BYTES];
+
+std::mutex g_noalloc_mu;
+char *g_noalloc_ptr[kMaxDevices];
+
+int noalloc_workspace(char **ws)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(MPQ_ERR_HIP, "device index %d out of range", dev);
+    std::lock_guard<std::mutex> lk(g_noalloc_mu);
+    if (!g_noalloc_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(workspace)");
+        if (!p) return fail(MPQ_ERR_HIP, "hipGetSymbolAddress(workspace) returned NULL");
+        g_noalloc_ptr[dev] = (char *)p;
+    }
+    *ws = g_noalloc_ptr[dev];
     return MPQ_OK;
 }
 
@@ -1279,6 +1322,30 @@ int mpq_output_error(const float *W, const int8_t *codes, const float *scales,
 int mpq_output_error_layers(const mpq_layer *layers, int n_layers, int max_points, void *stream)
 {
     return output_error_impl(layers, n_layers, max_points, stream);
+}
+
+int mpq_output_error_noalloc(const float *W, const int8_t *codes, const float *scales,
+                             const int32_t *counts, int64_t c_out, int64_t d, int max_points,
+                             const float *X, int64_t n, float *err, float *ref_opt, void *stream)
+{
+    mpq_layer L = {};
+    L.W = W;
+    L.c_out = c_out;
+    L.d = d;
+    L.codes = (int8_t *)codes;
+    L.scales = (float *)scales;
+    L.counts = (int32_t *)counts;
+    L.X = X;
+    L.n = n;
+    L.out_err = err;
+    L.out_ref = ref_opt;
+    // the argument checks come first: the workspace lookup is a HIP call
+    int rc = check_error_layer(L, max_points, true);
+    if (rc != MPQ_OK || c_out == 0) return rc;
+    char *ws = nullptr;
+    rc = noalloc_workspace(&ws);
+    if (rc != MPQ_OK) return rc;
+    return output_error_impl(&L, 1, max_points, stream, ws, (size_t)MPQ_NOALLOC_BYTES);
 }
 
 int mpq_reconstruct(const int8_t *codes, const float *scales, const int32_t *counts, int64_t c_out,

@@ -33,7 +33,7 @@ EXPORTS = ("mpq_fit_layer", "mpq_fit_layer_dense", "mpq_fit_layers", "mpq_fit_ma
            "mpq_reconstruct_layers", "mpq_last_error", "mpq_timing_enable", "mpq_timing_only", "mpq_timing_read",
            "mpq_fit_kernel_of", "mpq_quantize_layers", "mpq_fit_layer_calib",
            "mpq_fit_layers_calib", "mpq_integer_scales", "mpq_integer_forward",
-           "mpq_integer_forward_layers", "mpq_fit_layers_ex")
+           "mpq_integer_forward_layers", "mpq_fit_layers_ex", "mpq_output_error_noalloc")
 
 
 class Layer(ctypes.Structure):
@@ -104,6 +104,8 @@ def load(path: str = LIB_PATH):
     lib.mpq_fit_max_dim.restype = i64
     lib.mpq_output_error.argtypes = [P, P, P, P, i64, i64, i32, P, i64, P, P, P]
     lib.mpq_output_error.restype = i32
+    lib.mpq_output_error_noalloc.argtypes = [P, P, P, P, i64, i64, i32, P, i64, P, P, P]
+    lib.mpq_output_error_noalloc.restype = i32
     lib.mpq_reconstruct.argtypes = [P, P, P, i64, i64, i32, P, P]
     lib.mpq_reconstruct.restype = i32
     lib.mpq_fit_layers.argtypes = [P, i32, i32, i32, P, i32, f32, P]
@@ -233,8 +235,12 @@ def fit_max_dim(n_grid: int) -> int:
 
 def output_error(W: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, counts: torch.Tensor,
                  X: torch.Tensor, with_ref: bool = False, stream=None,
-                 out: Optional[Tuple[torch.Tensor, Optional[torch.Tensor]]] = None):
-    """mpq_output_error.  X: [d, n] fp32.  Returns (err [C], ref [C] or None)."""
+                 out: Optional[Tuple[torch.Tensor, Optional[torch.Tensor]]] = None,
+                 noalloc: bool = False):
+    """mpq_output_error (noalloc: mpq_output_error_noalloc, whose workspace is
+    the library's fixed per-device array; pass `out` to allocate nothing on
+    the Python side either).  X: [d, n] fp32.  Returns (err [C], ref [C] or
+    None)."""
     C, d = W.shape
     P = codes.shape[1]
     if codes.shape != (C, P, d) or scales.shape != (C, P) or counts.shape != (C,):
@@ -247,12 +253,12 @@ def output_error(W: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, cou
         ref = torch.empty((C,), dtype=torch.float32, device=W.device) if with_ref else None
     else:
         err, ref = out
-    rc = load().mpq_output_error(_dev(W, torch.float32, "W"), _dev(codes, torch.int8, "codes"),
-                                 _dev(scales, torch.float32, "scales"),
-                                 _dev(counts, torch.int32, "counts"), C, d, P,
-                                 _dev(X, torch.float32, "X"), n, _dev(err, torch.float32, "err"),
-                                 None if ref is None else _dev(ref, torch.float32, "ref"),
-                                 _stream(stream))
+    lib = load()
+    fn = lib.mpq_output_error_noalloc if noalloc else lib.mpq_output_error
+    rc = fn(_dev(W, torch.float32, "W"), _dev(codes, torch.int8, "codes"),
+            _dev(scales, torch.float32, "scales"), _dev(counts, torch.int32, "counts"), C, d, P,
+            _dev(X, torch.float32, "X"), n, _dev(err, torch.float32, "err"),
+            None if ref is None else _dev(ref, torch.float32, "ref"), _stream(stream))
     _check(rc)
     return err, ref
 

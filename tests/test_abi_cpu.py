@@ -91,6 +91,23 @@ def test_output_error_and_reconstruct_reject_invalid_arguments(lib):
     assert rc(None, None, None, 0, 4, 2, None, None) == 0
 
 
+def test_output_error_noalloc_rejects_invalid_arguments(lib):
+    """The no-allocation output error checks its arguments as mpq_output_error
+    does, before its workspace lookup (a HIP call) and before any launch."""
+    from paper_2002_09049_amd import mpq
+    E = mpq.MPQ_ERR_INVALID_ARG
+    oe = lib.mpq_output_error_noalloc
+    assert oe(1, 1, 1, 1, -1, 4, 2, 1, 8, 1, None, None) == E
+    assert oe(1, 1, 1, 1, 4, 0, 2, 1, 8, 1, None, None) == E
+    assert oe(1, 1, 1, 1, 4, 4, 2, 1, 0, 1, None, None) == E
+    assert oe(1, 1, 1, 1, 4, 4, 0, 1, 8, 1, None, None) == E
+    assert oe(1, 1, 1, 1, 4, 4, 2, None, 8, 1, None, None) == E
+    assert oe(1, 1, 1, 1, 4, 4, 2, 1, 8, None, None, None) == E
+    assert oe(1, 1, 1, 1, (1 << 24) + 1, 4, 2, 1, 8, 1, None, None) == E
+    assert oe(None, None, None, None, 0, 4, 2, None, 8, None, None, None) == 0
+    assert re.search(r"#define MPQ_NOALLOC_BYTES \(64 << 20\)", open(HEADER).read())
+
+
 def test_fit_max_dim_rejects_bad_grid(lib):
     from paper_2002_09049_amd import mpq
     assert lib.mpq_fit_max_dim(0) == mpq.MPQ_ERR_INVALID_ARG
