@@ -5,9 +5,10 @@ One step = the whole path over one synthetic workload already resident in
 HBM: for every layer, the greedy fit, the output error on the layer's
 calibration batch and the reconstruction, in one mpq_quantize_layers call
 (--separate: mpq_fit_layers, mpq_output_error_layers, mpq_reconstruct_layers
-in turn, with the time of each stage).  The default workload is the
-ResNet-18-shaped stack (21 layers, 5,800 channels, 4 bits, up to 4 points,
-256 candidate scales, tol 1e-3, 1,024 calibration columns).
+in turn, with the time of each stage).  The default workload is the largest
+4-bit one, the ResNet-50-shaped stack (54 layers, 27,560 channels, 4 bits,
+up to 8 points, 256 candidate scales, tol 1e-3, 1,024 calibration columns);
+--workload names the others (conv64x576, resnet18, mobilenetv2, vgg16fc).
 
 --rule calib times the path with Algorithm 2's stopping rule on the
 calibration batch instead (mpq_fit_layers_calib, whose per-point output
@@ -24,10 +25,19 @@ multiply-add of the points actually used).
 
 Prints one JSON line.  `value` is channel-points fitted per second over the
 whole step (sum of the per-channel point counts of all layers / step time).
-Every kernel launch of the timed steps is timed by HIP events that the
-library records on the launch's own stream (mpq_timing_enable); `roofline`
-describes the kernel with the most time per step, `kernels` all of them.
-`cpu_baseline` times the fp64 CPU oracle on a sample of the same workload.
+An untimed profile step first times every kernel launch by HIP events that
+the library records on the launch's own stream (mpq_timing_enable); the
+timed steps then carry events around the error GEMM's launches only.
+`roofline` is the error GEMM (the path's one dense contraction, FP32 MFMA),
+timed in the timed steps; `kernels` lists every kernel.  The fit kernels'
+`dense_equivalent_tflops` prices their candidate search at 7 FLOP per
+(element, candidate) pair, the work a dense evaluation of Eq. (9) does; the
+histogram search does O(d M + G) per step instead, so that figure is not an
+instruction rate and is kept out of any fraction of peak.  `search` carries
+the rocprofv3 counter figures of the longest fit kernel (VALU FLOP rates,
+VALU-busy and wait shares, HBM bytes) when a stored counter summary of this
+workload matches the current kernel sources.  `cpu_baseline` times the fp64
+CPU oracle on a sample of the same workload, on all host cores and on one.
 """
 from __future__ import annotations
 
@@ -48,7 +58,8 @@ PEAK_MFMA_I8_TOPS = 5000.0              # dense int8 MFMA
 PEAK_VALU_F32_NONPACKED_TFLOPS = 78.6   # 256 CU x 64 lanes x 2 FLOP x 2.4 GHz
 FLOP_PER_EVAL = 7                       # scale-mul, round, clamp, fma (2), square-acc fma (2)
 
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "resnet18_hbm_traffic.md")
+PROFILES = os.path.join(ROOT, "profiles")
+ROOFLINE_KERNEL = "gemm_err_kernel"
 COPY_BYTES = 256 << 20
 STAGES = (("fit", ("fit_hist_kernel", "fit_dense_kernel")),
           ("output_error", ("form_d_kernel", "gemm_err_kernel", "finish_err_kernel")),
@@ -61,7 +72,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="resnet18")
+    ap.add_argument("--workload", default="resnet50")
     ap.add_argument("--cpu-stride", type=int, default=1,
                     help="cpu_baseline fits every n-th channel of every layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -90,10 +101,10 @@ def parse():
                          "2^-10 = 0.0009765625; mpq_fit_layers_ex; implies --separate)")
     ap.add_argument("--separate", action="store_true",
                     help="the three batched calls in turn instead of mpq_quantize_layers")
-    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
-                    help="print the HBM-traffic summary of two rocprofv3 --pmc runs "
-                         "(FETCH_SIZE, WRITE_SIZE) of `bench.py --steps 1 --warmup 1 "
-                         "--copy-calibration` and exit")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="PMC_DIR",
+                    help="print the per-kernel counter summary of rocprofv3 --pmc runs (one per "
+                         "counter pass) of `bench.py --workload W --steps 1 --warmup 1 "
+                         "--no-cpu-baseline --copy-calibration` and exit")
     ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
                     help="print the per-kernel summary of a rocprofv3 --kernel-trace --stats run "
                          "and exit")
@@ -102,7 +113,7 @@ def parse():
                          "same build, compared kernel by kernel")
     ap.add_argument("--traced-steps", type=int, default=None,
                     help="with --summarize-*: steps the traced process ran (warm-up, profile "
-                         "step and timed; default 3 for --summarize-pmc; for --summarize-trace "
+                         "step and timed; default 3 for --summarize-counters; for --summarize-trace "
                          "those of the --bench-json line, which has no profile step with --deploy)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before the steps, copy a 256 MiB device buffer once (a kernel of known "
@@ -150,69 +161,151 @@ def stage_of(key):
     return None
 
 
-def summarize_pmc(fetch_dir, write_dir, steps=3):
-    """HBM bytes per step and kernel from the FETCH_SIZE / WRITE_SIZE counters,
-    each scaled so that the 256 MiB calibration copy reads / writes 256 MiB."""
+COUNTER_PASSES = (
+    ("SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_WAIT_ANY", "SQ_ACTIVE_INST_VALU", "SQ_INSTS_VALU",
+     "SQ_INSTS_LDS", "SQ_WAIT_INST_LDS", "SQ_BUSY_CYCLES"),
+    ("SQ_INSTS_VALU_FLOPS_FP32", "SQ_INSTS_VALU_FLOPS_FP32_TRANS", "SQ_INSTS_VALU_FLOPS_FP64",
+     "SQ_INSTS_VALU_FLOPS_FP64_TRANS", "SQ_INSTS_VALU_IOPS", "SQ_VALU_MFMA_BUSY_CYCLES",
+     "SQ_INSTS_VALU_MFMA_MOPS_F32", "SQ_BUSY_CU_CYCLES"),
+    ("FETCH_SIZE",),
+    ("WRITE_SIZE",),
+)
+PEAK_VALU_F64_TFLOPS = 78.6
+
+
+def counters_path(workload):
+    return os.path.join(PROFILES, f"{workload}_counters.md")
+
+
+def summarize_counters(dirs, workload, steps=3):
+    """Per-kernel figures of rocprofv3 --pmc runs of `bench.py --workload W
+    --steps 1 --warmup 1 --no-cpu-baseline --copy-calibration` (one run per
+    pass of COUNTER_PASSES): counters averaged per dispatch, the dispatch's
+    own duration (counter runs serialize the dispatches), and derived rates.
+    FETCH_SIZE and WRITE_SIZE (KiB) are scaled so that the 256 MiB
+    calibration copy reads and writes 256 MiB."""
     import csv
     import glob
 
-    def per_kernel(d):
+    per = {}        # kernel -> counter -> [sum, n]
+    dur = {}        # kernel -> [sum ns, n]
+    launches = {}   # kernel -> dispatches in the run (largest over the passes)
+    scale = {}
+    for d in dirs:
         rows = []
         for f in glob.glob(os.path.join(d, "*counter_collection.csv")):
             rows += list(csv.DictReader(open(f)))
-        cal = [r for r in rows if "copyBuffer" in r["Kernel_Name"] and int(r["Grid_Size"]) == 131072]
-        if not cal:
-            raise SystemExit(f"no calibration copy in {d}")
-        factor = COPY_BYTES / 1024.0 / float(cal[0]["Counter_Value"])
-        out, launches = {}, {}
+        if not rows:
+            raise SystemExit(f"no counter_collection.csv in {d}")
+        names = {r["Counter_Name"] for r in rows}
+        for c in ("FETCH_SIZE", "WRITE_SIZE"):
+            if c in names:
+                cal = [r for r in rows if "copyBuffer" in r["Kernel_Name"] and r["Counter_Name"] == c
+                       and int(r["Grid_Size"]) == 131072]
+                if not cal:
+                    raise SystemExit(f"no calibration copy in {d}")
+                scale[c] = COPY_BYTES / 1024.0 / float(cal[0]["Counter_Value"])
+        seen = {}
         for r in rows:
             k = kernel_key(r["Kernel_Name"])
             if not stage_of(k):
                 continue
-            out[k] = out.get(k, 0.0) + float(r["Counter_Value"]) * factor * 1024.0
-            launches[k] = launches.get(k, 0) + 1
-        return factor, out, launches
+            c = r["Counter_Name"]
+            a = per.setdefault(k, {}).setdefault(c, [0.0, 0])
+            a[0] += float(r["Counter_Value"])
+            a[1] += 1
+            did = r["Dispatch_Id"]
+            if (k, did) not in seen:
+                seen[(k, did)] = 1
+                t = dur.setdefault(k, [0.0, 0])
+                t[0] += float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+                t[1] += 1
+        cnt = {}
+        for k, _ in seen:
+            cnt[k] = cnt.get(k, 0) + 1
+        for k, v in cnt.items():
+            launches[k] = max(launches.get(k, 0), v)
+    out = {}
+    for k, cs in per.items():
+        avg = {c: v[0] / v[1] for c, v in cs.items()}
+        us = dur[k][0] / dur[k][1] / 1e3
+        f = {"launches_per_step": launches[k] / steps, "avg_us_serialized": us}
+        for c in ("FETCH_SIZE", "WRITE_SIZE"):
+            if c in avg:
+                f[c.lower() + "_bytes"] = avg[c] * scale[c] * 1024.0
+        if "fetch_size_bytes" in f and "write_size_bytes" in f:
+            f["hbm_bytes"] = f["fetch_size_bytes"] + f["write_size_bytes"]
+            f["hbm_gbs"] = f["hbm_bytes"] / us / 1e3
+        if "SQ_WAVE_CYCLES" in avg and avg["SQ_WAVE_CYCLES"] > 0:
+            f["valu_active_share"] = avg.get("SQ_ACTIVE_INST_VALU", 0.0) / avg["SQ_WAVE_CYCLES"]
+            f["wait_any_share"] = avg.get("SQ_WAIT_ANY", 0.0) / avg["SQ_WAVE_CYCLES"]
+            f["lds_wait_share"] = avg.get("SQ_WAIT_INST_LDS", 0.0) / avg["SQ_WAVE_CYCLES"]
+        if "SQ_INSTS_VALU_FLOPS_FP32" in avg:
+            f32 = avg["SQ_INSTS_VALU_FLOPS_FP32"] + avg.get("SQ_INSTS_VALU_FLOPS_FP32_TRANS", 0.0)
+            f64 = avg.get("SQ_INSTS_VALU_FLOPS_FP64", 0.0) + avg.get("SQ_INSTS_VALU_FLOPS_FP64_TRANS", 0.0)
+            f["valu_fp32_tflops"] = f32 / us / 1e6
+            f["valu_fp32_frac"] = f["valu_fp32_tflops"] / PEAK_VALU_F32_TFLOPS
+            f["valu_fp64_tflops"] = f64 / us / 1e6
+            f["valu_fp64_frac"] = f["valu_fp64_tflops"] / PEAK_VALU_F64_TFLOPS
+            f["valu_iops_tops"] = avg.get("SQ_INSTS_VALU_IOPS", 0.0) / us / 1e6
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in avg and avg.get("SQ_BUSY_CU_CYCLES", 0) > 0:
+            f["mfma_busy_per_cu_busy"] = avg["SQ_VALU_MFMA_BUSY_CYCLES"] / (4 * avg["SQ_BUSY_CU_CYCLES"])
+        f["counters"] = {c: round(v, 1) for c, v in sorted(avg.items())}
+        out[k] = f
 
-    ff, fetch, launches = per_kernel(fetch_dir)
-    wf, write, _ = per_kernel(write_dir)
-    lines = ["# HBM traffic per step and kernel: ResNet-18-shaped workload", "",
-             "Two rocprofv3 counter runs (one counter each), from the repository root:", "",
-             "```",
-             "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_FETCH_SIZE -o p -- \\",
-             "    python3 bench.py --steps 1 --warmup 1 --no-cpu-baseline --copy-calibration",
-             "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_WRITE_SIZE -o p -- \\",
-             "    python3 bench.py --steps 1 --warmup 1 --no-cpu-baseline --copy-calibration",
-             "python3 bench.py --summarize-pmc gpurun_out/pmc_FETCH_SIZE gpurun_out/pmc_WRITE_SIZE",
+    def fmt(v, spec):
+        return "" if v is None else format(v, spec)
+
+    cmds = [f"rocprofv3 --pmc {' '.join(cs)} --output-format csv -d gpurun_out/pmc_{workload}_{i} -o p -- \\\n"
+            f"    python3 bench.py --workload {workload} --steps 1 --warmup 1 --no-cpu-baseline --copy-calibration"
+            for i, cs in enumerate(COUNTER_PASSES)]
+    lines = [f"# Counters per kernel: {workload} workload, bench step", "",
+             "One rocprofv3 counter run per pass (from the repository root; each run holds "
+             f"{steps} steps: warm-up, profile and timed), then the summary:", "", "```", *cmds,
+             f"python3 bench.py --workload {workload} --summarize-counters "
+             + " ".join(f"gpurun_out/pmc_{workload}_{i}" for i in range(len(COUNTER_PASSES))),
              "```", "",
-             f"Scale factors from a 256 MiB device copy: FETCH_SIZE x {ff:.4f}, WRITE_SIZE x {wf:.4f}.",
-             f"Bytes per step (the run holds {steps} steps) and per launch.", "",
-             "| kernel | launches/step | fetch bytes/step | write bytes/step | bytes/launch |",
-             "|---|---:|---:|---:|---:|"]
-    for k in sorted(fetch, key=lambda k: -(fetch[k] + write.get(k, 0.0))):
-        f_, w_ = fetch[k] / steps, write.get(k, 0.0) / steps
-        per = launches[k] / steps
-        lines.append(f"| {k} | {per:g} | {f_:.0f} | {w_:.0f} | {(f_ + w_) / per:.0f} |")
-    lines += ["", f"sources: {sources_digest()}", ""]
+             "Per dispatch.  Counter runs serialize the dispatches, so `us` is the kernel alone.",
+             "FETCH_SIZE / WRITE_SIZE are scaled by a 256 MiB device copy "
+             f"(x {scale.get('FETCH_SIZE', float('nan')):.4f}, x {scale.get('WRITE_SIZE', float('nan')):.4f}).",
+             "VALU-active and wait shares are SQ_ACTIVE_INST_VALU and SQ_WAIT_ANY over SQ_WAVE_CYCLES;",
+             "FLOP rates are SQ_INSTS_VALU_FLOPS_FP32 (+ _TRANS) and _FP64 over the dispatch's duration,",
+             f"against {PEAK_VALU_F32_TFLOPS} (FP32) and {PEAK_VALU_F64_TFLOPS} (FP64) TFLOP/s.", "",
+             "| kernel | launches/step | us | HBM MB | HBM GB/s | VALU active | wait | FP32 TFLOP/s (frac) | FP64 TFLOP/s (frac) | INT TOP/s | MFMA busy |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    for k in sorted(out, key=lambda k: -out[k]["avg_us_serialized"] * out[k]["launches_per_step"]):
+        f = out[k]
+        hb = f.get("hbm_bytes")
+        lines.append(
+            f"| `{k}` | {f['launches_per_step']:g} | {f['avg_us_serialized']:.1f} | "
+            f"{fmt(None if hb is None else hb / 1e6, '.1f')} | {fmt(f.get('hbm_gbs'), '.0f')} | "
+            f"{fmt(f.get('valu_active_share'), '.1%')} | {fmt(f.get('wait_any_share'), '.1%')} | "
+            + ("" if "valu_fp32_tflops" not in f else
+               f"{f['valu_fp32_tflops']:.2f} ({f['valu_fp32_frac']:.1%}) | "
+               f"{f['valu_fp64_tflops']:.2f} ({f['valu_fp64_frac']:.1%}) | {f['valu_iops_tops']:.2f} | ")
+            + ("| | | " if "valu_fp32_tflops" not in f else "")
+            + f"{fmt(f.get('mfma_busy_per_cu_busy'), '.1%')} |")
+    lines += ["", "counters-json: " + json.dumps(out, sort_keys=True), "",
+              f"sources: {sources_digest()}", ""]
     print("\n".join(lines))
 
 
-def measured_traffic(key):
-    """HBM bytes per launch of a kernel from the stored counter summary, or
+def stored_counters(workload):
+    """The per-kernel counter figures of profiles/<workload>_counters.md, or
     None when it is missing or was taken on other kernel sources."""
     try:
-        text = open(TRAFFIC_SUMMARY).read()
+        text = open(counters_path(workload)).read()
     except OSError:
         return None
     if f"sources: {sources_digest()}" not in text:
         return None
     for ln in text.splitlines():
-        cells = [c.strip() for c in ln.strip("|").split("|")]
-        if len(cells) == 5 and cells[0] == key:
-            return int(float(cells[4]))
+        if ln.startswith("counters-json: "):
+            return json.loads(ln[len("counters-json: "):])
     return None
 
 
-def summarize_trace(trace_dir, bench_json=None, steps=None, rule="tol"):
+def summarize_trace(trace_dir, bench_json=None, steps=None, rule="tol", workload="resnet50"):
     """Per-kernel average duration of a traced bench run (kernel_stats.csv of
     rocprofv3 --stats), beside the event-timed averages of a bench.py line
     whose --steps / --warmup the traced run used too (steps: the steps the
@@ -247,9 +340,13 @@ def summarize_trace(trace_dir, bench_json=None, steps=None, rule="tol"):
                       "p = 16) on int8 activations of 8 images of 224 x 224 (N = 8 x output positions),\n"
                       "through mpq_integer_forward_layers; the fit and the scales are untimed set-up."
             }.get(rule, "fit + output error + reconstruction of every layer through the batched C ABI calls.")
-    lines = [f"# rocprofv3 kernel summary: ResNet-18-shaped workload, bench step{r}", "",
-             "Workload: 21 layers (5,800 channels, 11,678,912 weights), 4 bits, up to 4 points,",
-             "256 candidate scales, tol 1e-3, calibration batches d x 1024.  One step =",
+    from paper_2002_09049_amd import workloads as wl
+    wk = wl.get(workload)
+    r = f" --workload {workload}" + r
+    lines = [f"# rocprofv3 kernel summary: {workload} workload, bench step{r}", "",
+             f"Workload: {len(wk.layers)} layers ({wk.channels:,} channels, {wk.weights:,} weights), "
+             f"{wk.bits} bits, up to {wk.max_points} points,",
+             f"{wk.n_grid} candidate scales, tol {wk.tol:g}, calibration batches d x {wk.n_calib}.  One step =",
              what, "",
              "Commands (one MI355X, from the repository root):", "", "```",
              "rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof -o kt -- \\",
@@ -279,12 +376,12 @@ def summarize_trace(trace_dir, bench_json=None, steps=None, rule="tol"):
 
 def main():
     args = parse()
-    if args.summarize_pmc:
-        summarize_pmc(*args.summarize_pmc, steps=args.traced_steps or 3)
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters, args.workload, steps=args.traced_steps or 3)
         return 0
     if args.summarize_trace:
         summarize_trace(args.summarize_trace, args.bench_json, steps=args.traced_steps,
-                        rule="deploy" if args.deploy else args.rule)
+                        rule="deploy" if args.deploy else args.rule, workload=args.workload)
         return 0
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -421,11 +518,15 @@ def main():
             w = work.get(name, {})
             lps = cnt / nsteps
             if "evals" in w:
+                # the histogram search does O(d M + G) per channel-step: the
+                # dense-equivalent rate is what a dense evaluation of Eq. (9)
+                # would have to sustain, not an instruction rate (no frac)
                 ev_launch = w["evals"] / lps
-                k.update({"bound": "alu", "unit": "TFLOP/s", "peak": PEAK_VALU_F32_TFLOPS,
-                          "candidate_evals_per_launch": ev_launch,
-                          "achieved": FLOP_PER_EVAL * ev_launch / avg_s / 1e12,
-                          "hbm_gbs_algorithmic": w["bytes"] / lps / avg_s / 1e9})
+                k.update({"unit": "TFLOP/s", "candidate_evals_per_launch": ev_launch,
+                          "dense_equivalent_tflops": FLOP_PER_EVAL * ev_launch / avg_s / 1e12,
+                          "bytes_per_launch": w["bytes"] / lps,
+                          "hbm_gbs_algorithmic": w["bytes"] / lps / avg_s / 1e9,
+                          "hbm_frac_algorithmic": w["bytes"] / lps / avg_s / 1e9 / PEAK_HBM_GBS})
             elif "flop" in w:
                 k.update({"bound": "mfma", "unit": "TFLOP/s", "peak": PEAK_MFMA_F32_TFLOPS,
                           "flop_per_launch": w["flop"] / lps, "achieved": w["flop"] / lps / avg_s / 1e12})
@@ -434,9 +535,16 @@ def main():
                           "bytes_per_launch": w["bytes"] / lps, "achieved": w["bytes"] / lps / avg_s / 1e9})
             if "achieved" in k:
                 k["frac"] = k["achieved"] / k["peak"]
-            k["hbm_bytes_per_launch_measured"] = measured_traffic(name)
+            c = (counters or {}).get(name)
+            if c:
+                k["counters"] = {kk: c[kk] for kk in (
+                    "hbm_bytes", "avg_us_serialized", "valu_active_share", "wait_any_share",
+                    "valu_fp32_tflops", "valu_fp32_frac", "valu_fp64_tflops", "valu_fp64_frac",
+                    "valu_iops_tops", "mfma_busy_per_cu_busy") if kk in c}
             kernels[name] = k
         return kernels
+
+    counters = stored_counters(wk.name)
 
     # profile step (untimed): every launch between HIP events, to rank the
     # kernels; then the timed steps carry events around the dominant kernel
@@ -449,7 +557,10 @@ def main():
     mpq.timing_enable(False)
     for k in kernels.values():
         k["timed_in"] = "profile step"
-    dom = max((k for k in kernels if "achieved" in kernels[k]), key=lambda k: kernels[k]["us_per_step"])
+    # the roofline kernel: the error GEMM (the path's one dense contraction);
+    # a step without it (none here) would take the longest-running kernel
+    dom = ROOFLINE_KERNEL if ROOFLINE_KERNEL in kernels else \
+        max(kernels, key=lambda k: kernels[k]["us_per_step"])
 
     nl = len(Ws)
     ev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4)) for _ in range(args.steps)]
@@ -478,13 +589,25 @@ def main():
         for i, st in enumerate(("fit", "output_error", "reconstruct")):
             stages[st] = sum(e[i].elapsed_time(e[i + 1]) for e in ev) / steps
     K = kernels[dom]
-    roofline = {"kernel": dom, "bound": K["bound"], "achieved": round(K["achieved"], 4),
-                "peak": K["peak"], "unit": K["unit"], "frac": round(K["frac"], 5),
-                "traffic": K["hbm_bytes_per_launch_measured"],
-                "avg_launch_us": round(K["avg_us"], 3)}
-    if K["bound"] == "alu":
-        roofline["achieved_is"] = ("algorithmic FLOP/s: 7 FLOP per (element, candidate) evaluation "
-                                   "of Eq. (9), G per element and point")
+    traffic = (counters or {}).get(dom, {}).get("hbm_bytes")
+    roofline = {"kernel": dom, "bound": K.get("bound"), "achieved": round(K.get("achieved", 0.0), 4),
+                "peak": K.get("peak"), "unit": K.get("unit"), "frac": round(K.get("frac", 0.0), 5),
+                "traffic": None if traffic is None else int(traffic),
+                "avg_launch_us": round(K["avg_us"], 3),
+                "achieved_is": "2 C d n FLOP per layer (Eq. (12)'s products) / event-timed launch duration"}
+    # the candidate search: the fit kernel with the most time per step, with
+    # the counter figures of the stored summary (FP32 / FP64 VALU rates
+    # against their peaks, VALU-active and wait shares, HBM bytes)
+    fits = [k for k in kernels if stage_of(k) == "fit"]
+    search = None
+    if fits:
+        fk = max(fits, key=lambda k: kernels[k]["us_per_step"])
+        F = kernels[fk]
+        search = {"kernel": fk, "avg_launch_us": round(F["avg_us"], 3),
+                  "dense_equivalent_tflops": round(F.get("dense_equivalent_tflops", 0.0), 3),
+                  "counters": F.get("counters"),
+                  "counters_from": (os.path.relpath(counters_path(wk.name), ROOT)
+                                    if F.get("counters") else None)}
 
     value = points * steps / (ms_total * 1e-3)
     res = {
@@ -513,6 +636,7 @@ def main():
                              "separate" if separate else "mpq_quantize_layers"),
                    "parallelism": "none"},
         "roofline": roofline,
+        "search": search,
         "stages_ms_per_step": {k: round(v, 5) for k, v in stages.items()} or None,
         "kernels": {k: {kk: (round(vv, 5) if isinstance(vv, float) else vv) for kk, vv in v.items()}
                     for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["us_per_step"])},
@@ -619,34 +743,60 @@ def deploy_main(args):
     return 0
 
 
-def cpu_baseline(wk, stride, calib=False):
-    """The fp64 oracle, as it stands, on every stride-th channel of every layer
-    (calib: its fit with Algorithm 2's rule on the layer's batch)."""
+def cpu_model():
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or None
+
+
+def _oracle_rate(orc, wk, stride, threads, calib=False):
+    """(channel-points, seconds) of the oracle's fit of every stride-th
+    channel of every layer of wk on `threads` threads."""
     import numpy as np
 
-    import oracle
     from paper_2002_09049_amd import workloads as wl
-    orc = oracle.load()
-    cores = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
-    pts = 0
-    secs = 0.0
+    pts, secs = 0, 0.0
     for li in range(len(wk.layers)):
         W = np.ascontiguousarray(wl.layer_weights(wk, li)[::stride])
         X = wl.layer_calib(wk, li) if calib else None
         t0 = time.perf_counter()
         if calib:
             counts = orc.fit_calib(W, wk.bits, wk.max_points, wk.n_grid, X, float(np.float32(wk.tol)),
-                                   True, n_threads=cores)[2]
+                                   True, n_threads=threads)[2]
         else:
-            _, _, counts, _ = orc.fit(W, wk.bits, wk.max_points, wk.n_grid,
-                                      float(np.float32(wk.tol)), n_threads=cores)
+            counts = orc.fit(W, wk.bits, wk.max_points, wk.n_grid, float(np.float32(wk.tol)),
+                             n_threads=threads)[2]
         secs += time.perf_counter() - t0
         pts += int(counts.sum())
+    return pts, secs
+
+
+def cpu_baseline(wk, stride, calib=False):
+    """The fp64 oracle, as it stands, on every stride-th channel of every layer
+    (calib: its fit with Algorithm 2's rule on the layer's batch), on all the
+    host's cores; and on one thread on the single-conv and ResNet-18 shaped
+    workloads (the latter every 8th channel)."""
+    import oracle
+    from paper_2002_09049_amd import workloads as wl
+    orc = oracle.load()
+    cores = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    pts, secs = _oracle_rate(orc, wk, stride, cores, calib)
+    single = {}
+    for name, st in (("conv64x576", 1), ("resnet18", 8)):
+        p1, s1 = _oracle_rate(orc, wl.get(name), st, 1, calib)
+        single[name] = {"value": round(p1 / s1, 2), "unit": "channel-points/s",
+                        "sample": f"every {st}th channel ({p1} channel-points, {s1:.1f} s)"}
     return {"value": round(pts / secs, 2), "unit": "channel-points/s", "cores": cores,
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model(),
             "sample": f"{'calibration-rule fit, ' if calib else ''}"
                       f"every {stride}th channel of each of the {len(wk.layers)} layers of {wk.name} "
-                      f"({pts} channel-points, {secs:.1f} s wall)"}
+                      f"({pts} channel-points, {secs:.1f} s wall)",
+            "single_thread": single}
 
 
 if __name__ == "__main__":

@@ -31,3 +31,60 @@ def test_more_than_one_gpu_is_refused():
     p = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, timeout=120)
     assert p.returncode == 2 and "one GPU" in p.stderr
+
+
+def _pmc_csv(path, rows):
+    import csv
+    cols = ["Correlation_Id", "Dispatch_Id", "Agent_Id", "Queue_Id", "Process_Id", "Thread_Id",
+            "Grid_Size", "Kernel_Id", "Kernel_Name", "Workgroup_Size", "LDS_Block_Size",
+            "Scratch_Size", "VGPR_Count", "Accum_VGPR_Count", "SGPR_Count", "Counter_Name",
+            "Counter_Value", "Start_Timestamp", "End_Timestamp"]
+    os.makedirs(path, exist_ok=True)
+    with open(os.path.join(path, "p_counter_collection.csv"), "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=cols)
+        w.writeheader()
+        for did, name, grid, c, v, t0, t1 in rows:
+            w.writerow({"Correlation_Id": did, "Dispatch_Id": did, "Agent_Id": "Agent 1", "Queue_Id": 1,
+                        "Process_Id": 1, "Thread_Id": 1, "Grid_Size": grid, "Kernel_Id": 1,
+                        "Kernel_Name": name, "Workgroup_Size": 256, "LDS_Block_Size": 0,
+                        "Scratch_Size": 0, "VGPR_Count": 8, "Accum_VGPR_Count": 0, "SGPR_Count": 16,
+                        "Counter_Name": c, "Counter_Value": v, "Start_Timestamp": t0,
+                        "End_Timestamp": t1})
+
+
+def test_counter_summary_arithmetic(tmp_path, capsys):
+    """The counter summary scales FETCH_SIZE / WRITE_SIZE by the calibration
+    copy, averages per dispatch, divides FLOP counts by the dispatch's own
+    duration, and takes shares of SQ_WAVE_CYCLES."""
+    gemm = "void mpq::(anonymous namespace)::gemm_err_kernel<true>(mpq::ErrGroup)"
+    fit = "void mpq::(anonymous namespace)::fit_hist_kernel<512, 9, true, true, false>(mpq::HistBatch)"
+    copy = "__amd_rocclr_copyBuffer"
+    a, b, c = (str(tmp_path / x) for x in "abc")
+    # pass a: SQ shares, two fit dispatches of 100 us and 300 us
+    _pmc_csv(a, [(1, fit, 512, "SQ_WAVE_CYCLES", 1000.0, 0, 100000),
+                 (1, fit, 512, "SQ_ACTIVE_INST_VALU", 250.0, 0, 100000),
+                 (1, fit, 512, "SQ_WAIT_ANY", 500.0, 0, 100000),
+                 (2, fit, 512, "SQ_WAVE_CYCLES", 3000.0, 0, 300000),
+                 (2, fit, 512, "SQ_ACTIVE_INST_VALU", 750.0, 0, 300000),
+                 (2, fit, 512, "SQ_WAIT_ANY", 1500.0, 0, 300000)])
+    # pass b: FLOP counts (1e9 FP32, 2e9 FP64 FLOP per dispatch)
+    _pmc_csv(b, [(1, fit, 512, "SQ_INSTS_VALU_FLOPS_FP32", 1e9, 0, 200000),
+                 (1, fit, 512, "SQ_INSTS_VALU_FLOPS_FP64", 2e9, 0, 200000)])
+    # pass c: FETCH_SIZE with a copy that reads 256 MiB but counts half of it
+    _pmc_csv(c, [(1, copy, 131072, "FETCH_SIZE", 131072.0, 0, 10),
+                 (2, gemm, 1024, "FETCH_SIZE", 1000.0, 0, 50000)])
+    d = str(tmp_path / "d")
+    _pmc_csv(d, [(1, copy, 131072, "WRITE_SIZE", 262144.0, 0, 10),
+                 (2, gemm, 1024, "WRITE_SIZE", 10.0, 0, 50000)])
+    bench.summarize_counters([a, b, c, d], "resnet50", steps=1)
+    out = capsys.readouterr().out
+    import json
+    blob = json.loads(next(l for l in out.splitlines() if l.startswith("counters-json: "))[15:])
+    f = blob["fit_hist_kernel<512,9,lattice>"]
+    assert abs(f["valu_active_share"] - 0.25) < 1e-12 and abs(f["wait_any_share"] - 0.5) < 1e-12
+    # 1e9 FLOP over the pass-b dispatch's 200 us = 5 TFLOP/s
+    assert abs(f["valu_fp32_tflops"] - 5.0) < 1e-9 and abs(f["valu_fp64_tflops"] - 10.0) < 1e-9
+    g = blob["gemm_err_kernel"]
+    assert abs(g["fetch_size_bytes"] - 2 * 1000.0 * 1024) < 1e-6     # the copy read 2x its count
+    assert abs(g["write_size_bytes"] - 10.0 * 1024) < 1e-6
+    assert "sources: " in out
