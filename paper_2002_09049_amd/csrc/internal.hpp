@@ -171,8 +171,9 @@ struct ErrLayerIn {
     int d_ready;
 };
 // The items (an err item per layer with err, a ref item per layer with ref) go
-// in launch groups of up to 22; groups are independent and may run side by
-// side, each with its own scratch.
+// in launch groups of up to 1024 (one group for any network here); groups are
+// independent and may run side by side, each with its own scratch (whose head
+// holds the group's descriptor table).
 int err_group_count(const ErrLayerIn *in, int n_in);
 size_t err_group_scratch_bytes(const ErrLayerIn *in, int n_in, int group);
 double err_group_flop(const ErrLayerIn *in, int n_in, int group);

@@ -2,9 +2,12 @@
 // Eq. (12)): err[k] = (1/n) sum_t ((w_k - w~_k) . x_t)^2 and optionally
 // ref[k] = (1/n) sum_t (w_k . x_t)^2.
 //
-// Up to kMaxErrLayers layers (items: an err item per layer, a ref item per
-// layer that asks for ref) go through three launches together, their
-// descriptors by value in the kernel arguments:
+// All layers of a call (items: an err item per layer, a ref item per layer
+// that asks for ref; up to kMaxErrItems) go through three launches together.
+// Their descriptors sit in a table at the head of the call's scratch, filled
+// by small upload kernels that carry kDescChunk descriptors each in their
+// kernel arguments (stream-ordered, so no host buffer outlives the call);
+// each workgroup finds its item by a binary search of the table:
 //
 //  1. form (HBM-bound): D[k][j] = fl32(w_kj - sum_{i<n_k} a_i q_ij), the fp64
 //     sum in point order (D = W for a ref item), one float4 of a row per
@@ -68,7 +71,8 @@ constexpr int kMinSlabs = 4;      // shortest K range (slabs) of a listed layer'
 constexpr int kThreads = 512;   // GEMM workgroup: eight wavefronts, two per SIMD
 constexpr int kPad = 4;          // LDS row padding (floats); rows stay 16-byte aligned
 constexpr int kVec = kBK * kBM / kThreads / 4;   // float4 per thread and operand per slab
-constexpr int kMaxErrLayers = 22;
+constexpr int kMaxErrItems = 1024;   // items (err and ref) per launch group
+constexpr int kDescChunk = 20;       // descriptors per upload kernel
 constexpr int kXcds = 8;         // MI355X: workgroups are dealt to 8 XCDs in turn
 constexpr int kFormThreads = 256;
 constexpr int kPadA = 2;         // A slab rows: 130 floats, so a wavefront's 4-byte stores hit 64 banks
@@ -120,9 +124,40 @@ struct ErrGroup {
     int P;
     int extra_start;     // gemm workgroups past every layer's planned tiles start here
     int vecx;            // n % 4 == 0 and every X 16-byte aligned
-    ErrLayer L[kMaxErrLayers];
 };
-static_assert(sizeof(ErrGroup) <= 4096, "kernel arguments");
+
+// kDescChunk descriptors for the table (kernel arguments of one upload)
+struct DescChunk {
+    ErrLayer *dst;
+    int count;
+    ErrLayer L[kDescChunk];
+};
+static_assert(sizeof(DescChunk) <= 4096, "kernel arguments");
+static_assert(sizeof(ErrLayer) % 4 == 0, "copied as 32-bit words");
+
+__global__ void __launch_bounds__(64) desc_upload_kernel(const DescChunk c)
+{
+    constexpr int kWords = (int)(sizeof(ErrLayer) / 4);
+    const uint32_t *src = (const uint32_t *)c.L;
+    uint32_t *dst = (uint32_t *)c.dst;
+    for (int i = threadIdx.x; i < c.count * kWords; i += 64) dst[i] = src[i];
+}
+
+// The item of workgroup b: the last one whose begin (the member `begin`
+// picks) is at most b.  Items are in launch order, their begins
+// non-decreasing from 0; an item with no workgroups shares its begin with
+// the next one and is never found.
+template <class Begin>
+__device__ __forceinline__ int find_item(const ErrLayer *__restrict__ Ls, int n, int b, Begin begin)
+{
+    int lo = 0, hi = n - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (begin(Ls[mid]) <= b) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
 
 // The K split of the live rows 0 .. nact of D.  A layer's full rows take the
 // host's plan.  When a listed layer scores fewer rows (the later steps of the
@@ -159,11 +194,12 @@ __device__ __forceinline__ int64_t d_index(int64_t m, int64_t k, int nkb)
 
 // ---- 1. form: rows of D, four consecutive k (one float4) per thread, k
 // past d written as zeros
-__global__ void __launch_bounds__(kFormThreads) form_d_kernel(const ErrGroup g)
+__global__ void __launch_bounds__(kFormThreads) form_d_kernel(const ErrGroup g,
+                                                              const ErrLayer *__restrict__ Ls)
 {
-    int li = 0;
-    while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].form_begin) ++li;
-    const ErrLayer &L = g.L[li];
+    const int li = find_item(Ls, g.n_layers, (int)blockIdx.x,
+                             [](const ErrLayer &x) { return x.form_begin; });
+    const ErrLayer &L = Ls[li];
     const int P = g.P;
     const int64_t d = L.d, C = L.C, q4 = (int64_t)L.nkb * (kBK / 4);
     const int64_t e = (int64_t)((int)blockIdx.x - L.form_begin) * kFormThreads + threadIdx.x;
@@ -227,7 +263,7 @@ __global__ void __launch_bounds__(kFormThreads) form_d_kernel(const ErrGroup g)
 // ---- 2. gemm: Y = D X, squared and summed per row
 template <bool kVecX>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4)))
-gemm_err_kernel(const ErrGroup g)
+gemm_err_kernel(const ErrGroup g, const ErrLayer *__restrict__ Ls)
 {
     __shared__ __align__(16) float sA[2][kBK][kBM + kPadA];
     __shared__ __align__(16) float sX[2][kBK][kBN + kPad];
@@ -237,12 +273,11 @@ gemm_err_kernel(const ErrGroup g)
     // more (for the short K ranges of a listed layer's few live rows) from
     // extra_begin, after every layer's planned ones
     const bool extra = (int)blockIdx.x >= g.extra_start;
-    int li = 0;
-    if (!extra)
-        while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].block_begin) ++li;
-    else
-        while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].extra_begin) ++li;
-    const ErrLayer &L = g.L[li];
+    const int li = extra ? find_item(Ls, g.n_layers, (int)blockIdx.x,
+                                     [](const ErrLayer &x) { return x.extra_begin; })
+                         : find_item(Ls, g.n_layers, (int)blockIdx.x,
+                                     [](const ErrLayer &x) { return x.block_begin; });
+    const ErrLayer &L = Ls[li];
     // the live tiles: (split, tm, tn) over the live row tiles, split-major
     const int64_t nact = L.rows ? (int64_t)*L.nrows : (int64_t)L.C;
     LiveSplit ls = live_split(L, nact);
@@ -419,11 +454,12 @@ gemm_err_kernel(const ErrGroup g)
 // (256 rows per workgroup), or for a split layer the sum over K ranges of Y,
 // squared and summed over the columns (one wavefront per row, four rows per
 // workgroup); fixed order, fp64, divided by n
-__global__ void __launch_bounds__(256) finish_err_kernel(const ErrGroup g)
+__global__ void __launch_bounds__(256) finish_err_kernel(const ErrGroup g,
+                                                         const ErrLayer *__restrict__ Ls)
 {
-    int li = 0;
-    while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].fin_begin) ++li;
-    const ErrLayer &L = g.L[li];
+    const int li = find_item(Ls, g.n_layers, (int)blockIdx.x,
+                             [](const ErrLayer &x) { return x.fin_begin; });
+    const ErrLayer &L = Ls[li];
     const int64_t C = L.C, n = L.n;
     const int b = (int)blockIdx.x - L.fin_begin;
     const int64_t nact = L.rows ? (int64_t)*L.nrows : C;
@@ -544,12 +580,14 @@ Plan plan_item(const ErrLayerIn &I, bool list)
 }
 
 // A group's items in launch order (longest K ranges first) and the byte
-// offset of each item's scratch (D, row partials, Y ranges) in the group's.
+// offset of each item's scratch (D, row partials, Y ranges) in the group's,
+// after the descriptor table at its head.
 struct GroupLayout {
     std::vector<Plan> p;
     std::vector<int> order;
     std::vector<size_t> off;   // by item
 };
+size_t table_bytes(int cnt) { return align256(sizeof(ErrLayer) * (size_t)cnt); }
 GroupLayout group_layout(const Item *grp, int cnt)
 {
     GroupLayout G;
@@ -560,7 +598,7 @@ GroupLayout group_layout(const Item *grp, int cnt)
     std::stable_sort(G.order.begin(), G.order.end(),
                      [&](int a, int b) { return G.p[a].kchunk > G.p[b].kchunk; });
     G.off.assign(cnt, 0);
-    size_t cur = 0;
+    size_t cur = table_bytes(cnt);
     for (int o = 0; o < cnt; ++o) {
         const int i = G.order[o];
         G.off[i] = cur;
@@ -571,7 +609,7 @@ GroupLayout group_layout(const Item *grp, int cnt)
 
 size_t group_bytes(const Item *it, int cnt)
 {
-    size_t b = 0;
+    size_t b = table_bytes(cnt);
     for (int i = 0; i < cnt; ++i) {
         const Plan q = plan_item(*it[i].in, listed(*it[i].in, it[i].use_points));
         b += q.d_bytes + q.rowpart_bytes + q.ypart_bytes;
@@ -584,15 +622,15 @@ size_t group_bytes(const Item *it, int cnt)
 int err_group_count(const ErrLayerIn *in, int n_in)
 {
     const size_t n = items_of(in, n_in).size();
-    return (int)((n + kMaxErrLayers - 1) / kMaxErrLayers);
+    return (int)((n + kMaxErrItems - 1) / kMaxErrItems);
 }
 
 size_t err_group_scratch_bytes(const ErrLayerIn *in, int n_in, int group)
 {
     const std::vector<Item> it = items_of(in, n_in);
-    const size_t base = (size_t)group * kMaxErrLayers;
+    const size_t base = (size_t)group * kMaxErrItems;
     if (base >= it.size()) return 0;
-    const int cnt = (int)std::min<size_t>(kMaxErrLayers, it.size() - base);
+    const int cnt = (int)std::min<size_t>(kMaxErrItems, it.size() - base);
     return group_bytes(it.data() + base, cnt);
 }
 
@@ -601,9 +639,9 @@ int64_t err_item_d_offset(const ErrLayerIn *in, int n_in, int i, int *group)
     const std::vector<Item> it = items_of(in, n_in);
     for (size_t x = 0; x < it.size(); ++x) {
         if (it[x].in != &in[i] || it[x].use_points != 1) continue;
-        const size_t base = x / kMaxErrLayers * kMaxErrLayers;
-        const int cnt = (int)std::min<size_t>(kMaxErrLayers, it.size() - base);
-        *group = (int)(x / kMaxErrLayers);
+        const size_t base = x / kMaxErrItems * kMaxErrItems;
+        const int cnt = (int)std::min<size_t>(kMaxErrItems, it.size() - base);
+        *group = (int)(x / kMaxErrItems);
         return (int64_t)group_layout(it.data() + base, cnt).off[x - base];
     }
     return -1;
@@ -613,7 +651,7 @@ double err_group_flop(const ErrLayerIn *in, int n_in, int group)
 {
     const std::vector<Item> it = items_of(in, n_in);
     double f = 0.0;
-    for (size_t i = (size_t)group * kMaxErrLayers; i < it.size() && i < (size_t)(group + 1) * kMaxErrLayers; ++i)
+    for (size_t i = (size_t)group * kMaxErrItems; i < it.size() && i < (size_t)(group + 1) * kMaxErrItems; ++i)
         f += 2.0 * (double)item_rows(*it[i].in) * (double)it[i].in->d * (double)it[i].in->n;
     return f;
 }
@@ -622,10 +660,10 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
                                      hipStream_t s)
 {
     const std::vector<Item> it = items_of(in, n_in);
-    const size_t base = (size_t)group * kMaxErrLayers;
+    const size_t base = (size_t)group * kMaxErrItems;
     if (base >= it.size()) return hipSuccess;
     {
-        const int cnt = (int)std::min<size_t>(kMaxErrLayers, it.size() - base);
+        const int cnt = (int)std::min<size_t>(kMaxErrItems, it.size() - base);
         const Item *grp = it.data() + base;
         const GroupLayout lay = group_layout(grp, cnt);   // longest K ranges first
         const std::vector<Plan> &p = lay.p;
@@ -634,13 +672,14 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
         g.n_layers = cnt;
         g.P = P;
         g.vecx = 1;
+        std::vector<ErrLayer> table(cnt);
         int64_t blocks = 0, fblocks = 0, nblocks = 0;
         int xoff = 0;
         for (int o = 0; o < cnt; ++o) {
             const int i = order[o];
             const ErrLayerIn &I = *grp[i].in;
             const Plan &q = p[i];
-            ErrLayer &L = g.L[o];
+            ErrLayer &L = table[o];
             L.W = I.W;
             L.codes = I.codes;
             L.scales = I.scales;
@@ -692,7 +731,7 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
         if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
         g.extra_start = (int)blocks;
         for (int o = 0; o < cnt; ++o) {
-            ErrLayer &L = g.L[o];
+            ErrLayer &L = table[o];
             const int64_t planned = (int64_t)L.ntm * L.ntn * L.splits;
             L.extra_begin = (int)blocks;
             blocks += ((int64_t)L.tiles + kXcds - 1) / kXcds * kXcds -
@@ -701,22 +740,37 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
         if (blocks > 0x7fffffffLL || fblocks > 0x7fffffffLL || nblocks > 0x7fffffffLL)
             return hipErrorInvalidValue;
         hipError_t e = hipSuccess;
+        // the descriptor table at the head of the group's scratch
+        ErrLayer *dtab = (ErrLayer *)scratch;
+        for (int o = 0; o < cnt && e == hipSuccess; o += kDescChunk) {
+            DescChunk c;
+            c.dst = dtab + o;
+            c.count = std::min(kDescChunk, cnt - o);
+            for (int i = 0; i < c.count; ++i) c.L[i] = table[o + i];
+            LaunchTimer timer(s, "desc_upload_kernel");
+            hipLaunchKernelGGL(desc_upload_kernel, dim3(1), dim3(64), 0, s, c);
+            e = hipGetLastError();
+        }
+        if (e != hipSuccess) return e;
         if (fblocks > 0) {
             LaunchTimer timer(s, "form_d_kernel");
-            hipLaunchKernelGGL(form_d_kernel, dim3((unsigned)fblocks), dim3(kFormThreads), 0, s, g);
+            hipLaunchKernelGGL(form_d_kernel, dim3((unsigned)fblocks), dim3(kFormThreads), 0, s, g,
+                               (const ErrLayer *)dtab);
             e = hipGetLastError();
         }
         if (e != hipSuccess) return e;
         {
             LaunchTimer timer(s, "gemm_err_kernel");
             auto kern = g.vecx ? gemm_err_kernel<true> : gemm_err_kernel<false>;
-            hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kThreads), 0, s, g);
+            hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kThreads), 0, s, g,
+                               (const ErrLayer *)dtab);
             e = hipGetLastError();
         }
         if (e != hipSuccess) return e;
         {
             LaunchTimer timer(s, "finish_err_kernel");
-            hipLaunchKernelGGL(finish_err_kernel, dim3((unsigned)nblocks), dim3(256), 0, s, g);
+            hipLaunchKernelGGL(finish_err_kernel, dim3((unsigned)nblocks), dim3(256), 0, s, g,
+                               (const ErrLayer *)dtab);
             e = hipGetLastError();
         }
         if (e != hipSuccess) return e;
