@@ -41,7 +41,10 @@ extern "C" {
 #define MPQ_ERR_INVALID_ARG (-1) /* a null pointer, a size or value out of range */
 #define MPQ_ERR_SHAPE (-2)       /* d (with n_grid) too large for one workgroup's LDS */
 #define MPQ_ERR_HIP (-3)         /* a HIP runtime call failed; see mpq_last_error() */
-#define MPQ_ERR_NOMEM (-4)       /* device scratch allocation failed */
+#define MPQ_ERR_NOMEM (-4)       /* device scratch allocation failed (or exceeded the
+                                    MPQ_WORKSPACE_LIMIT environment variable: a cap in
+                                    bytes on each scratch allocation, checked before
+                                    any HIP call; unset means no cap) */
 
 #define MPQ_MAX_BITS 8
 #define MPQ_MAX_POINTS 64

@@ -4,6 +4,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -102,8 +103,21 @@ std::mutex g_pool_mu;
 hipMemPool_t g_pool[kMaxDevices];
 }  // namespace
 
+// MPQ_WORKSPACE_LIMIT (bytes, decimal): a cap on each stream-ordered scratch
+// allocation, checked before any HIP call; a request above it fails as an
+// allocation would (the calls then return MPQ_ERR_NOMEM).  Unset: no cap.
+static bool over_workspace_limit(size_t bytes)
+{
+    const char *v = getenv("MPQ_WORKSPACE_LIMIT");
+    if (!v || !*v) return false;
+    char *end = nullptr;
+    const unsigned long long lim = strtoull(v, &end, 10);
+    return end && *end == '\0' && (unsigned long long)bytes > lim;
+}
+
 hipError_t scratch_alloc(void **p, size_t bytes, hipStream_t s)
 {
+    if (over_workspace_limit(bytes)) return hipErrorOutOfMemory;
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;

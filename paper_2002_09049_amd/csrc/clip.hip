@@ -25,9 +25,7 @@ constexpr int kClipThreads = 256;
 
 __device__ __forceinline__ int layer_of(const ClipBatch &B)
 {
-    int li = 0;
-    while (li + 1 < B.n_layers && (int)blockIdx.x >= B.L[li + 1].c_begin) ++li;
-    return li;
+    return last_at_most(B.n_layers, (int)blockIdx.x, [&](int i) { return B.L[i].c_begin; });
 }
 
 __global__ void __launch_bounds__(kClipThreads) clip_cand_kernel(const ClipBatch B)

@@ -126,8 +126,7 @@ __global__ void __launch_bounds__(kIThreads) int_forward_kernel(const IntGroup g
     __shared__ int s_offA[kIM], s_offB[kIN];
     __shared__ int32_t s_coef[kIM];
 
-    int li = 0;
-    while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].block_begin) ++li;
+    const int li = last_at_most(g.n_layers, (int)blockIdx.x, [&](int i) { return g.L[i].block_begin; });
     const IntLayer &L = g.L[li];
     int tn = (int)blockIdx.x - L.block_begin, tm = 0;
     while (tn >= L.ntn) {

@@ -303,8 +303,7 @@ fit_hist_kernel(const HistBatch B)
     __shared__ float s_scale[MPQ_MAX_POINTS];
 
     // layer of this workgroup (uniform: the descriptors are kernel arguments)
-    int li = 0;
-    while (li + 1 < B.n_layers && (int)blockIdx.x >= B.L[li + 1].c_begin) ++li;
+    const int li = last_at_most(B.n_layers, (int)blockIdx.x, [&](int i) { return B.L[i].c_begin; });
     const HistLayer &Ly = B.L[li];
 
     const int G = B.G;
@@ -393,8 +392,11 @@ fit_hist_kernel(const HistBatch B)
         for (int u = 0; u < EPT; ++u) r[u] = rebuild(u, s0);
     }
 
+    // the default multipliers fl32((g + 1) / G): the correctly rounded fp32
+    // quotient of the two integers, which equals fl32 of the fp64 one for
+    // every g < G <= 4096 (checked exhaustively on the host)
     for (int g = t; g < G; g += T)
-        S.c[g] = B.grid ? B.grid[g] : (float)((double)(g + 1) / (double)G);
+        S.c[g] = B.grid ? B.grid[g] : __fdiv_rn((float)(g + 1), (float)G);
 
     float apend = 0.0f;
     int n = 0;
@@ -774,8 +776,18 @@ fit_hist_kernel(const HistBatch B)
         if (Ly.err) Ly.err[k * P + q] = 0.0f;
         if (Ly.xerr) Ly.xerr[k * P + q] = 0.0f;
     }
-    for (int q = n; q < P; ++q)
-        for (int j = t; j < d; j += T) qk[(int64_t)q * d + j] = 0;
+    // code rows n .. P - 1: one contiguous byte range, in 16-byte stores
+    // between its unaligned head and tail
+    int8_t *z0 = qk + (int64_t)n * d, *z1 = qk + (int64_t)P * d;
+    int8_t *a0 = (int8_t *)(((uintptr_t)z0 + 15) & ~(uintptr_t)15);
+    int8_t *a1 = (int8_t *)((uintptr_t)z1 & ~(uintptr_t)15);
+    if (a0 >= a1) {
+        for (int8_t *p = z0 + t; p < z1; p += T) *p = 0;
+    } else {
+        if (z0 + t < a0) z0[t] = 0;   // head < 16 <= T bytes
+        if (a1 + t < z1) a1[t] = 0;   // tail < 16 bytes
+        for (int64_t v = t; v < (a1 - a0) / 16; v += T) ((uint4 *)a0)[v] = make_uint4(0, 0, 0, 0);
+    }
 }
 
 template <int T, int EPT, bool kGlobal = false>
@@ -821,8 +833,12 @@ constexpr Variant kVariants[] = {{64, 1, false},   {64, 2, false},   {64, 4, fal
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 static_assert(kVariants[kNumVariants - 1].threads * kVariants[kNumVariants - 1].ept == kHistMaxDim,
               "the last variant covers the longest channels");
-// variants whose capacity reaches this length use the lattice mode
-constexpr int kLatMinDim = 2048;
+// variants whose capacity reaches this length use the lattice mode (at 4
+// bits and 256 candidates on ResNet-50's layers it beat the per-level
+// histograms on lengths 576-1024, 165 against 197 us, and lost on 512 and
+// below: its O((2M - 1) G) bucket pass per step outweighs M atomics per
+// element there)
+constexpr int kLatMinDim = 1024;
 
 }  // namespace
 

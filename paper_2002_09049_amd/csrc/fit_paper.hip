@@ -105,8 +105,7 @@ __global__ void __launch_bounds__(kPT) fit_paper_kernel(const PaperBatch B)
     __shared__ double s_redd[kPT / kWave];
     __shared__ long long s_redg[kPT / kWave];
 
-    int li = 0;
-    while (li + 1 < B.n_layers && (int)blockIdx.x >= B.L[li + 1].c_begin) ++li;
+    const int li = last_at_most(B.n_layers, (int)blockIdx.x, [&](int i) { return B.L[i].c_begin; });
     const HistLayer &Ly = B.L[li];
     const int64_t k = (int64_t)blockIdx.x - Ly.c_begin;
     const int t = threadIdx.x, d = Ly.d, P = B.P, M = B.M;

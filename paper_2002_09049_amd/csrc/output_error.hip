@@ -143,22 +143,6 @@ __global__ void __launch_bounds__(64) desc_upload_kernel(const DescChunk c)
     for (int i = threadIdx.x; i < c.count * kWords; i += 64) dst[i] = src[i];
 }
 
-// The item of workgroup b: the last one whose begin (the member `begin`
-// picks) is at most b.  Items are in launch order, their begins
-// non-decreasing from 0; an item with no workgroups shares its begin with
-// the next one and is never found.
-template <class Begin>
-__device__ __forceinline__ int find_item(const ErrLayer *__restrict__ Ls, int n, int b, Begin begin)
-{
-    int lo = 0, hi = n - 1;
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (begin(Ls[mid]) <= b) lo = mid;
-        else hi = mid - 1;
-    }
-    return lo;
-}
-
 // The K split of the live rows 0 .. nact of D.  A layer's full rows take the
 // host's plan.  When a listed layer scores fewer rows (the later steps of the
 // calibration rule), its workgroups take shorter K ranges (at least
@@ -197,8 +181,7 @@ __device__ __forceinline__ int64_t d_index(int64_t m, int64_t k, int nkb)
 __global__ void __launch_bounds__(kFormThreads) form_d_kernel(const ErrGroup g,
                                                               const ErrLayer *__restrict__ Ls)
 {
-    const int li = find_item(Ls, g.n_layers, (int)blockIdx.x,
-                             [](const ErrLayer &x) { return x.form_begin; });
+    const int li = last_at_most(g.n_layers, (int)blockIdx.x, [&](int i) { return Ls[i].form_begin; });
     const ErrLayer &L = Ls[li];
     const int P = g.P;
     const int64_t d = L.d, C = L.C, q4 = (int64_t)L.nkb * (kBK / 4);
@@ -273,10 +256,10 @@ gemm_err_kernel(const ErrGroup g, const ErrLayer *__restrict__ Ls)
     // more (for the short K ranges of a listed layer's few live rows) from
     // extra_begin, after every layer's planned ones
     const bool extra = (int)blockIdx.x >= g.extra_start;
-    const int li = extra ? find_item(Ls, g.n_layers, (int)blockIdx.x,
-                                     [](const ErrLayer &x) { return x.extra_begin; })
-                         : find_item(Ls, g.n_layers, (int)blockIdx.x,
-                                     [](const ErrLayer &x) { return x.block_begin; });
+    const int li = extra ? last_at_most(g.n_layers, (int)blockIdx.x,
+                                        [&](int i) { return Ls[i].extra_begin; })
+                         : last_at_most(g.n_layers, (int)blockIdx.x,
+                                        [&](int i) { return Ls[i].block_begin; });
     const ErrLayer &L = Ls[li];
     // the live tiles: (split, tm, tn) over the live row tiles, split-major
     const int64_t nact = L.rows ? (int64_t)*L.nrows : (int64_t)L.C;
@@ -457,8 +440,7 @@ gemm_err_kernel(const ErrGroup g, const ErrLayer *__restrict__ Ls)
 __global__ void __launch_bounds__(256) finish_err_kernel(const ErrGroup g,
                                                          const ErrLayer *__restrict__ Ls)
 {
-    const int li = find_item(Ls, g.n_layers, (int)blockIdx.x,
-                             [](const ErrLayer &x) { return x.fin_begin; });
+    const int li = last_at_most(g.n_layers, (int)blockIdx.x, [&](int i) { return Ls[i].fin_begin; });
     const ErrLayer &L = Ls[li];
     const int64_t C = L.C, n = L.n;
     const int b = (int)blockIdx.x - L.fin_begin;

@@ -15,6 +15,7 @@
 #include <algorithm>
 
 #include "internal.hpp"
+#include "reduce.hpp"
 
 namespace mpq {
 
@@ -44,8 +45,7 @@ static_assert(sizeof(RecGroup) <= 4096, "kernel arguments");
 
 __global__ void __launch_bounds__(kRecThreads) reconstruct_kernel(const RecGroup g)
 {
-    int li = 0;
-    while (li + 1 < g.n_layers && (int)blockIdx.x >= g.L[li + 1].block_begin) ++li;
+    const int li = last_at_most(g.n_layers, (int)blockIdx.x, [&](int i) { return g.L[i].block_begin; });
     const RecDesc &L = g.L[li];
     const int P = g.P;
     const int d = L.d;

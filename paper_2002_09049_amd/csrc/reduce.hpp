@@ -18,6 +18,23 @@ namespace mpq {
 
 constexpr int kWave = 64;
 
+// The last index i in [0, n) with begin(i) <= b, for non-decreasing begins
+// with begin(0) <= b: which of a launch's layers a workgroup b belongs to
+// (layers with no workgroups share their begin with the next one and are
+// never returned).  Binary search: ceil(log2 n) dependent reads of the
+// descriptors instead of one per layer.
+template <class Begin>
+__device__ __forceinline__ int last_at_most(int n, int b, Begin begin)
+{
+    int lo = 0, hi = n - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (begin(mid) <= b) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
 template <int kCtrl>
 __device__ __forceinline__ uint32_t dpp(uint32_t v)
 {

@@ -350,3 +350,16 @@ def test_fit_layers_ex_checks_arguments(lib):
     assert lib.mpq_fit_layers_ex(p, 1, 4, 4, None, 8, 1e-3, ctypes.addressof(opt), None) == E
     L.c_out = 0
     assert lib.mpq_fit_layers_ex(p, 1, 4, 4, None, 8, 1e-3, ctypes.addressof(opt), None) == 0
+
+
+def test_workspace_cap_gives_nomem(lib):
+    """MPQ_WORKSPACE_LIMIT caps each scratch allocation before any HIP call:
+    the output error's request fails with MPQ_ERR_NOMEM (no device needed)."""
+    from paper_2002_09049_amd import mpq
+    os.environ["MPQ_WORKSPACE_LIMIT"] = "64"
+    try:
+        rc = lib.mpq_output_error(1, 1, 1, 1, 4, 16, 2, 1, 8, 1, None, None)
+        assert rc == mpq.MPQ_ERR_NOMEM, rc
+        assert "scratch" in mpq.last_error()
+    finally:
+        del os.environ["MPQ_WORKSPACE_LIMIT"]
