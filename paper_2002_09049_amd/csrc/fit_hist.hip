@@ -154,32 +154,44 @@ __device__ __forceinline__ void bin_levels(const double (&r)[EPT], const HistSha
 // The per-level histogram of bin_levels, element-major: for the variant that
 // rebuilds each residual element from memory, so that an element is rebuilt
 // once per step rather than once per level.
-template <int T, int EPT, bool kLinear, class Res>
-__device__ __forceinline__ void bin_levels_elementwise(Res r, const HistShared &S, int G, int M, int d,
-                                                       float m, int sh, unsigned long long &fullA,
-                                                       int &fullB)
+// One element x = |r_j| of the per-level histogram, level by level until no
+// candidate lifts it (gm = G M / m).
+template <bool kLinear>
+__device__ __forceinline__ void bin_levels_elem(double x, const HistShared &S, int G, int M, float gm,
+                                                int sh, unsigned long long &fullA, int &fullB)
+{
+    const unsigned long long X = (unsigned long long)rint(ldexp(x, sh));
+    const float base = (float)x * gm;
+    for (int kk = 0; kk < M; ++kk) {
+        const double h = (double)kk + 0.5;
+        int nb;
+        if constexpr (kLinear) nb = count_linear(S.af, G, h, x, base * __builtin_amdgcn_rcpf((float)h));
+        else nb = count_bsearch(S.ad, G, h, x);
+        if (nb == 0) break;   // higher levels have higher boundaries
+        const int inc = 2 * kk + 1;
+        if (nb == G) {
+            fullA += X;
+            fullB += inc;
+        } else {
+            atomicAdd((unsigned long long *)&S.ha[nb - 1], X);
+            atomicAdd(&S.hb[nb - 1], inc);
+        }
+    }
+}
+
+// The same histogram over this thread's slots of four consecutive elements
+// (the variant that rebuilds its residual; r4(v, o) fills slot v).
+template <int T, int kSlots, bool kLinear, class Res4>
+__device__ __forceinline__ void bin_levels_slots(Res4 r4, const HistShared &S, int G, int M, int d,
+                                                 float m, int sh, unsigned long long &fullA, int &fullB)
 {
     const float gm = (float)G * (float)M / m;
-    for (int u = 0; u < EPT; ++u) {
-        if (T * u >= d) break;
-        const double x = fabs(r(u));
-        const unsigned long long X = (unsigned long long)rint(ldexp(x, sh));
-        const float base = (float)x * gm;
-        for (int kk = 0; kk < M; ++kk) {
-            const double h = (double)kk + 0.5;
-            int nb;
-            if constexpr (kLinear) nb = count_linear(S.af, G, h, x, base * __builtin_amdgcn_rcpf((float)h));
-            else nb = count_bsearch(S.ad, G, h, x);
-            if (nb == 0) break;   // higher levels have higher boundaries
-            const int inc = 2 * kk + 1;
-            if (nb == G) {
-                fullA += X;
-                fullB += inc;
-            } else {
-                atomicAdd((unsigned long long *)&S.ha[nb - 1], X);
-                atomicAdd(&S.hb[nb - 1], inc);
-            }
-        }
+    for (int v = 0; v < kSlots; ++v) {
+        if (4 * T * v >= d) break;
+        double o[4];
+        r4(v, o);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) bin_levels_elem<kLinear>(fabs(o[c]), S, G, M, gm, sh, fullA, fullB);
     }
 }
 
@@ -198,15 +210,11 @@ __device__ __forceinline__ void bin_levels_elementwise(Res r, const HistShared &
 // bucket word is formed by one fma: x 2^sh + 2^52 + 2^kLatShift rounds
 // x 2^sh to the nearest integer (ties to even, as rint) and its low 52 bits
 // are that integer plus the count bit.
-template <int T, int EPT, int kUnroll, class Res>
-__device__ __forceinline__ void bin_lattice(Res r, const HistShared &S, int G, int M, int d, int Lmax,
-                                            double inv, double scale)
+__device__ __forceinline__ void bin_lattice_elem(double x, const HistShared &S, int G, int M, int Lmax,
+                                                 double inv, double scale)
 {
     constexpr double kBias = 0x1p52 + (double)kLatOne;
-#pragma unroll kUnroll
-    for (int u = 0; u < EPT; ++u) {
-        if (T * u >= d) continue;   // a slot past the channel end in every thread
-        const double x = fabs(r(u));
+    {
         const double z = x * inv;
         const double Nd = rint(z);
         const int Ni = (int)Nd;
@@ -232,6 +240,32 @@ __device__ __forceinline__ void bin_lattice(Res r, const HistShared &S, int G, i
                 }
             }
         }
+    }
+}
+
+template <int T, int EPT, int kUnroll, class Res>
+__device__ __forceinline__ void bin_lattice(Res r, const HistShared &S, int G, int M, int d, int Lmax,
+                                            double inv, double scale)
+{
+#pragma unroll kUnroll
+    for (int u = 0; u < EPT; ++u) {
+        if (T * u >= d) continue;   // a slot past the channel end in every thread
+        bin_lattice_elem(fabs(r(u)), S, G, M, Lmax, inv, scale);
+    }
+}
+
+// The same over this thread's slots of four consecutive elements (the
+// variant that rebuilds its residual; r4(v, o) fills slot v).
+template <int T, int kSlots, class Res4>
+__device__ __forceinline__ void bin_lattice_slots(Res4 r4, const HistShared &S, int G, int M, int d,
+                                                  int Lmax, double inv, double scale)
+{
+    for (int v = 0; v < kSlots; ++v) {
+        if (4 * T * v >= d) break;
+        double o[4];
+        r4(v, o);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) bin_lattice_elem(fabs(o[c]), S, G, M, Lmax, inv, scale);
     }
 }
 
@@ -368,6 +402,51 @@ fit_hist_kernel(const HistBatch B)
         for (int p = 0; p < np; ++p) v = fma(-(double)s_scale[p], (double)qk[(int64_t)p * d + j], v);
         return v;
     };
+    // kGlobal: thread t owns slots of four consecutive elements, slot v
+    // holding j = 4 (t + T v) + c (c < 4), so that a slot's weights load as
+    // one float4 and each stored point's codes as one 32-bit word (rows of a
+    // multiple of 4 bytes; otherwise one element at a time).  Each element is
+    // rebuilt with the fp64 operations of rebuild, in point order.
+    constexpr int kSlots = kGlobal ? (EPT + 3) / 4 : 1;
+    const bool vec4 = kGlobal && d % 4 == 0 && (uintptr_t)wk % 16 == 0 && (uintptr_t)qk % 4 == 0;
+    auto rebuild4 = [&](int v, int np, double (&o)[4]) {
+        const int j0 = 4 * (t + T * v);
+        if (vec4 && j0 + 4 <= d) {
+            const float4 w4 = *(const float4 *)(wk + j0);
+            o[0] = (double)w4.x - beta;
+            o[1] = (double)w4.y - beta;
+            o[2] = (double)w4.z - beta;
+            o[3] = (double)w4.w - beta;
+            for (int p = 0; p < np; ++p) {
+                const uint32_t q = *(const uint32_t *)(qk + (int64_t)p * d + j0);
+                const double a = -(double)s_scale[p];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) o[c] = fma(a, (double)(int)(int8_t)(uint8_t)(q >> (8 * c)), o[c]);
+            }
+        } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int j = j0 + c;
+                double v = 0.0;
+                if (j < d) {
+                    v = (double)wk[j] - beta;
+                    for (int p = 0; p < np; ++p) v = fma(-(double)s_scale[p], (double)qk[(int64_t)p * d + j], v);
+                }
+                o[c] = v;
+            }
+        }
+    };
+    // stores the four codes of slot v (bytes past d are not stored)
+    auto store4 = [&](int8_t *row, int v, uint32_t q) {
+        const int j0 = 4 * (t + T * v);
+        if (vec4 && j0 + 4 <= d) {
+            *(uint32_t *)(row + j0) = q;
+        } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                if (j0 + c < d) row[j0 + c] = (int8_t)(uint8_t)(q >> (8 * c));
+        }
+    };
     double r[kGlobal ? 1 : EPT];
     // The channel's row of the output error's D, outside calibration steps:
     // the residual after the points so far in fp32 (the same fp64 steps, in
@@ -446,16 +525,35 @@ fit_hist_kernel(const HistBatch B)
         double aupd = ap;
         if (B.refit && i > s0 && gstate != 2) {   // the naive point keeps its scale
             double rq = 0.0, qq = 0.0;
-#pragma unroll kUnroll
-            for (int u = 0; u < EPT; ++u) {
-                const int j = t + T * u;
-                if (kGlobal && T * u >= d) break;
-                if (j < d) {
-                    const double ru = kGlobal ? rebuild(u, i - 1) : r[u];
-                    const double c = code_of(ru);
-                    qrow[j] = (int8_t)(int)c;
-                    rq = fma(ru, c, rq);
-                    qq = fma(c, c, qq);
+            if constexpr (kGlobal) {
+                for (int v = 0; v < kSlots; ++v) {
+                    if (4 * T * v >= d) break;
+                    const int j0 = 4 * (t + T * v);
+                    double o[4];
+                    rebuild4(v, i - 1, o);
+                    uint32_t qw = 0;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        if (j0 + c < d) {
+                            const double cd = code_of(o[c]);
+                            qw |= (uint32_t)(uint8_t)(int8_t)(int)cd << (8 * c);
+                            rq = fma(o[c], cd, rq);
+                            qq = fma(cd, cd, qq);
+                        }
+                    }
+                    store4(qrow, v, qw);
+                }
+            } else {
+#pragma unroll
+                for (int u = 0; u < EPT; ++u) {
+                    const int j = t + T * u;
+                    if (j < d) {
+                        const double ru = r[u];
+                        const double c = code_of(ru);
+                        qrow[j] = (int8_t)(int)c;
+                        rq = fma(ru, c, rq);
+                        qq = fma(c, c, qq);
+                    }
                 }
             }
             block_sum2<T>(rq, qq, s_redd, s_redd2);
@@ -466,25 +564,45 @@ fit_hist_kernel(const HistBatch B)
             }
             aupd = (double)afit;
         }
-#pragma unroll kUnroll
-        for (int u = 0; u < EPT; ++u) {
-            const int j = t + T * u;
-            if (kGlobal && T * u >= d) break;
-            double ru = kGlobal ? rebuild(u, i > s0 ? i - 1 : i) : r[u];
-            if (i > s0 && j < d) {
-                const double c = code_of(ru);
-                if (!B.refit || gstate == 2) qrow[j] = (int8_t)(int)c;
-                ru = fma(-aupd, c, ru);
+        if constexpr (kGlobal) {
+            const bool codes_here = i > s0 && (!B.refit || gstate == 2);
+            for (int v = 0; v < kSlots; ++v) {
+                if (4 * T * v >= d) break;
+                const int j0 = 4 * (t + T * v);
+                double o[4];
+                rebuild4(v, i > s0 ? i - 1 : i, o);
+                uint32_t qw = 0;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    double ru = o[c];
+                    if (i > s0 && j0 + c < d) {
+                        const double cd = code_of(ru);
+                        qw |= (uint32_t)(uint8_t)(int8_t)(int)cd << (8 * c);
+                        ru = fma(-aupd, cd, ru);
+                    }
+                    lmax = fmaxf(lmax, fabsf((float)ru));
+                    lsum = fma(ru, ru, lsum);
+                }
+                if (codes_here) store4(qrow, v, qw);
             }
-            if constexpr (!kGlobal) {
+        } else {
+#pragma unroll
+            for (int u = 0; u < EPT; ++u) {
+                const int j = t + T * u;
+                double ru = r[u];
+                if (i > s0 && j < d) {
+                    const double c = code_of(ru);
+                    if (!B.refit || gstate == 2) qrow[j] = (int8_t)(int)c;
+                    ru = fma(-aupd, c, ru);
+                }
                 r[u] = ru;
                 // rewritten each step: the last write holds the n points
                 if (has_d && d_chunk + u * (T / 32) < nkb)
                     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint((float)ru), rs_d,
                                                           d_voff + u * (T / 32) * 4096 * 4, 0, 0);
+                lmax = fmaxf(lmax, fabsf((float)ru));
+                lsum = fma(ru, ru, lsum);
             }
-            lmax = fmaxf(lmax, fabsf((float)ru));
-            lsum = fma(ru, ru, lsum);
         }
         // also orders S.c before use; no trailing barrier: the scratch is next
         // written after the setup barrier below
@@ -581,8 +699,13 @@ fit_hist_kernel(const HistBatch B)
             // ---- lattice buckets, their suffix sums, then every candidate
             const double inv = (double)(2 * G * M) / (double)m;
             // residual after the i points so far (kGlobal: rebuilt)
-            auto res = [&](int u) { return kGlobal ? rebuild(u, i) : r[kGlobal ? 0 : u]; };
-            bin_lattice<T, EPT, kUnroll>(res, S, G, M, d, nlat - 1, inv, ldexp(1.0, sh));
+            if constexpr (kGlobal) {
+                auto res4 = [&](int v, double (&o)[4]) { rebuild4(v, i, o); };
+                bin_lattice_slots<T, kSlots>(res4, S, G, M, d, nlat - 1, inv, ldexp(1.0, sh));
+            } else {
+                auto res = [&](int u) { return r[kGlobal ? 0 : u]; };
+                bin_lattice<T, EPT, kUnroll>(res, S, G, M, d, nlat - 1, inv, ldexp(1.0, sh));
+            }
             __syncthreads();
             block_suffix_sums<T>(S.lat, nlat, s_scan);
             for (int g = t; g < G; g += T) {
@@ -637,11 +760,11 @@ fit_hist_kernel(const HistBatch B)
             // estimate (in a lattice-mode kernel this branch only runs when
             // they do not)
             if constexpr (kGlobal) {
-                auto res = [&](int u) { return rebuild(u, i); };
+                auto res4 = [&](int v, double (&o)[4]) { rebuild4(v, i, o); };
                 if (kLinear && !kLat && m >= 0x1p-100f)
-                    bin_levels_elementwise<T, EPT, true>(res, S, G, M, d, m, sh, fullA, fullB);
+                    bin_levels_slots<T, kSlots, true>(res4, S, G, M, d, m, sh, fullA, fullB);
                 else
-                    bin_levels_elementwise<T, EPT, false>(res, S, G, M, d, m, sh, fullA, fullB);
+                    bin_levels_slots<T, kSlots, false>(res4, S, G, M, d, m, sh, fullA, fullB);
             } else if (kLinear && !kLat && m >= 0x1p-100f) {
                 bin_levels<T, EPT, true>(r, S, G, M, m, sh, fullA, fullB);
             } else {
@@ -735,15 +858,24 @@ fit_hist_kernel(const HistBatch B)
                 const int g = s_fin[f];
                 const double a = S.ad[g + 1];
                 double le = 0.0;
-#pragma unroll kUnroll
-                for (int u = 0; u < EPT; ++u) {
-                    if (kGlobal && T * u >= d) break;
-                    const double ru = kGlobal ? rebuild(u, i) : r[kGlobal ? 0 : u];
-                    // signed form: (r - a q)^2 with q = clip(rne(r / a)) equals
-                    // (|r| - a |q|)^2, and keeps |r| from being hoisted per element
+                // signed form: (r - a q)^2 with q = clip(rne(r / a)) equals
+                // (|r| - a |q|)^2, and keeps |r| from being hoisted per element
+                auto err_of = [&](double ru) {
                     const double c = fmin(fmax(rint(ru / a), -Md), Md);
                     const double e = ru - a * c;
                     le = fma(e, e, le);
+                };
+                if constexpr (kGlobal) {
+                    for (int v = 0; v < kSlots; ++v) {
+                        if (4 * T * v >= d) break;
+                        double o[4];
+                        rebuild4(v, i, o);
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) err_of(o[c]);   // 0 past d adds 0
+                    }
+                } else {
+#pragma unroll
+                    for (int u = 0; u < EPT; ++u) err_of(r[kGlobal ? 0 : u]);
                 }
                 const double E = block_reduce<T>(le, SumOp(), s_redd);
                 if (E < best.e || (E == best.e && g < best.g)) best = ArgMin{E, g};
