@@ -323,7 +323,10 @@ int mpq_fit_layers_calib(const mpq_layer *layers, int n_layers, int bits, int ma
  *             stored as fl32(g * gamma), and the point's codes and residual
  *             use that value.  grid_host and n_grid are ignored.  Only with
  *             the isotropic stopping rule (not with refit, calib,
- *             clip_grid, asym or gate); d <= 8192 (else MPQ_ERR_SHAPE).
+ *             clip_grid, asym or gate); d <= 32768 (else MPQ_ERR_SHAPE;
+ *             channels past 8192 keep their sorted magnitudes in a stream-
+ *             ordered scratch of about 8 (2 d) bytes for each of up to 1024
+ *             channels in flight).
  *   gate      nonzero: Algorithm 2's naive first point (Sec. 3.3).  Each
  *             channel is first quantized naively, a_N = fl32(fl32(max|w|) / M)
  *             (the candidate c = 1), q = [w / a_N]_Q; if that point already

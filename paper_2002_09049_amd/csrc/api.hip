@@ -1109,15 +1109,23 @@ int paper_impl(const mpq_layer *layers, int n_layers, int bits, int max_points, 
         }
     }
     if (!any) return MPQ_OK;
-    if (dmax > mpq::kPaperMaxDim)
+    if (dmax > mpq::kPaperBigMaxDim)
         return fail(MPQ_ERR_SHAPE, "the paper's grid takes d <= %lld (got %lld)",
-                    (long long)mpq::kPaperMaxDim, (long long)dmax);
+                    (long long)mpq::kPaperBigMaxDim, (long long)dmax);
+    // the LDS variants take d <= kPaperMaxDim; longer channels keep their
+    // sorted magnitudes in a global scratch
+    const int64_t dmax_lds = [&]() {
+        int64_t m = 0;
+        for (int l = 0; l < n_layers; ++l)
+            if (layers[l].c_out > 0 && layers[l].d <= mpq::kPaperMaxDim) m = std::max(m, layers[l].d);
+        return m;
+    }();
     size_t lim = 0;
     rc = device_lds_limit(&lim);
     if (rc != MPQ_OK) return rc;
-    if (mpq::paper_lds(dmax) > lim)
-        return fail(MPQ_ERR_SHAPE, "d = %lld needs %zu bytes of LDS (limit %zu)", (long long)dmax,
-                    mpq::paper_lds(dmax), lim);
+    if (dmax_lds > 0 && mpq::paper_lds(dmax_lds) > lim)
+        return fail(MPQ_ERR_SHAPE, "d = %lld needs %zu bytes of LDS (limit %zu)", (long long)dmax_lds,
+                    mpq::paper_lds(dmax_lds), lim);
     struct Job {
         mpq::PaperBatch b;
         int variant;
@@ -1126,7 +1134,7 @@ int paper_impl(const mpq_layer *layers, int n_layers, int bits, int max_points, 
     };
     std::vector<Job> jobs;
     const int M = (1 << (bits - 1)) - 1;
-    for (int v = 0; v <= mpq::paper_variant(mpq::kPaperMaxDim); ++v) {
+    for (int v = 0; v <= mpq::kPaperBigVariant; ++v) {
         Job j = {};
         auto fresh = [&]() {
             j = Job{};
@@ -1160,11 +1168,32 @@ int paper_impl(const mpq_layer *layers, int n_layers, int bits, int max_points, 
             j.work += (double)L.c_out * (double)L.d * (double)L.d;
         }
     }
+    // scratch of the long-channel launches (sorted magnitudes and prefix sums
+    // of one channel per workgroup)
+    hipStream_t s = (hipStream_t)stream;
+    std::vector<size_t> big_off(jobs.size(), 0);
+    size_t big_bytes = 0;
+    for (size_t i = 0; i < jobs.size(); ++i) {
+        if (jobs[i].variant != mpq::kPaperBigVariant) continue;
+        big_off[i] = big_bytes;
+        big_bytes += (sizeof(double) * mpq::paper_big_slice(jobs[i].dmax) *
+                          (size_t)mpq::paper_big_grid(jobs[i].channels) + 255) / 256 * 256;
+    }
+    char *big = nullptr;
+    if (big_bytes > 0) {
+        const hipError_t ea = mpq::scratch_alloc((void **)&big, big_bytes, s);
+        if (ea != hipSuccess) return fail(MPQ_ERR_NOMEM, "scratch of %zu bytes: %s", big_bytes,
+                                          hipGetErrorString(ea));
+    }
     std::vector<double> work;
     for (const Job &j : jobs) work.push_back(j.work);
-    const hipError_t e = run_concurrently((hipStream_t)stream, work, [&](int i, hipStream_t st) {
+    const hipError_t e = run_concurrently(s, work, [&](int i, hipStream_t st) {
+        if (jobs[i].variant == mpq::kPaperBigVariant)
+            return mpq::launch_fit_paper_big(jobs[i].b, jobs[i].channels, jobs[i].dmax,
+                                             (double *)(big + big_off[i]), st);
         return mpq::launch_fit_paper(jobs[i].b, jobs[i].variant, jobs[i].channels, jobs[i].dmax, st);
     });
+    if (big) (void)mpq::scratch_free(big, s);
     if (e != hipSuccess) return hip_fail(e, "paper-grid fit kernel launch");
     return MPQ_OK;
 }

@@ -137,6 +137,17 @@ struct PaperBatch {
 static_assert(sizeof(PaperBatch) <= 4096, "kernel arguments");
 int paper_variant(int64_t d);        // layers with equal variants may share a launch
 size_t paper_lds(int64_t dmax);      // dynamic LDS for channels of up to dmax weights
+// Channels longer than kPaperMaxDim (up to kPaperBigMaxDim): the variant
+// kPaperBigVariant, whose sorted magnitudes and prefix sums live in a global
+// scratch of paper_big_slice(dmax) doubles per workgroup; paper_big_grid
+// workgroups take the channels in turn.
+constexpr int kPaperBigVariant = 5;
+constexpr int64_t kPaperBigMaxDim = 32768;
+constexpr int64_t kPaperBigGrid = 1024;
+int paper_big_grid(int64_t channels);
+size_t paper_big_slice(int64_t dmax);
+hipError_t launch_fit_paper_big(const PaperBatch &b, int64_t channels, int64_t dmax, double *scratch,
+                                hipStream_t s);
 hipError_t launch_fit_paper(const PaperBatch &b, int variant, int64_t channels, int64_t dmax,
                             hipStream_t s);
 

@@ -216,6 +216,9 @@ PAPER = [
     (3, 2304, 4, 3, 0.0, 2.0 ** -10),
     (2, 4608, 4, 2, 1e-3, 2.0 ** -10),
     (2, 8192, 2, 2, 0.0, 2.0 ** -10),
+    # past 8192: the variant with its sorted magnitudes in global scratch
+    # (the oracle's exact search costs O(d^2 M) per step: few channels)
+    (2, 9000, 4, 2, 0.0, 2.0 ** -10),
 ]
 
 
@@ -244,9 +247,31 @@ def test_paper_grid_exact_on_dyadic_weights(orc):
         _ok(orc.verify_paper(W, bits, 4, 0.0, *out))
 
 
+@pytest.mark.timeout(600)
+def test_paper_grid_vgg16fc_length(orc):
+    """VGG-16 fc's 25088-long channels (3 bits) on the paper's grid, with a
+    layer of short channels in the same call (both kernels side by side):
+    lockstep parity of the first point (the oracle's exact search takes about
+    a minute per such channel and step)."""
+    import torch
+    from paper_2002_09049_amd import mpq
+    w = wl.get("vgg16fc")
+    W = np.ascontiguousarray(wl.layer_weights(w, 0)[:2])
+    W2 = wl.random_weights(4, 300, seed=8)
+    say("case paper grid d=25088 (2 channels) + d=300")
+    ls = mpq.LayerSet([to_dev(W), to_dev(W2)], 1)
+    ls.fit_ex(w.bits, 1, w.tol, paper_eta=2.0 ** -10)
+    torch.cuda.synchronize()
+    for i, Wi in enumerate((W, W2)):
+        out = (ls.codes[i].cpu().numpy(), ls.scales[i].cpu().numpy(), ls.counts[i].cpu().numpy(),
+               ls.fit_err[i].cpu().numpy())
+        _ok(orc.verify_paper(Wi, w.bits, 1, float(np.float32(w.tol)), *out))
+        assert (out[2] == 1).all()
+
+
 def test_paper_grid_limits():
     from paper_2002_09049_amd import mpq
-    W = wl.random_weights(2, 9000, seed=1)
+    W = wl.random_weights(1, 32769, seed=1)
     with pytest.raises(mpq.MPQError) as e:
         _fit_paper(W, 4, 2, 0.0, 2.0 ** -10)
     assert e.value.status == mpq.MPQ_ERR_SHAPE
