@@ -171,6 +171,7 @@ COUNTER_PASSES = (
     ("WRITE_SIZE",),
 )
 PEAK_VALU_F64_TFLOPS = 78.6
+CAL_MULS = 1 << 24   # multiplies of each known-FLOP calibration kernel
 
 
 def counters_path(workload):
@@ -205,6 +206,12 @@ def summarize_counters(dirs, workload, steps=3):
                 if not cal:
                     raise SystemExit(f"no calibration copy in {d}")
                 scale[c] = COPY_BYTES / 1024.0 / float(cal[0]["Counter_Value"])
+        # the FLOP counters against the multiply kernels of known work
+        for c, ty in (("SQ_INSTS_VALU_FLOPS_FP64", "double"), ("SQ_INSTS_VALU_FLOPS_FP32", "float")):
+            if c in names:
+                cal = [r for r in rows if r["Counter_Name"] == c and f"MulFunctor<{ty}>" in r["Kernel_Name"]]
+                if cal and float(cal[0]["Counter_Value"]) > 0:
+                    scale[c] = CAL_MULS / float(cal[0]["Counter_Value"])
         seen = {}
         for r in rows:
             k = kernel_key(r["Kernel_Name"])
@@ -241,8 +248,12 @@ def summarize_counters(dirs, workload, steps=3):
             f["wait_any_share"] = avg.get("SQ_WAIT_ANY", 0.0) / avg["SQ_WAVE_CYCLES"]
             f["lds_wait_share"] = avg.get("SQ_WAIT_INST_LDS", 0.0) / avg["SQ_WAVE_CYCLES"]
         if "SQ_INSTS_VALU_FLOPS_FP32" in avg:
-            f32 = avg["SQ_INSTS_VALU_FLOPS_FP32"] + avg.get("SQ_INSTS_VALU_FLOPS_FP32_TRANS", 0.0)
-            f64 = avg.get("SQ_INSTS_VALU_FLOPS_FP64", 0.0) + avg.get("SQ_INSTS_VALU_FLOPS_FP64_TRANS", 0.0)
+            # counts scaled by what they read for the known-FLOP multiplies
+            # (the fp64 factor also for fp32 when that one is missing)
+            s64 = scale.get("SQ_INSTS_VALU_FLOPS_FP64", 1.0)
+            s32 = scale.get("SQ_INSTS_VALU_FLOPS_FP32", s64)
+            f32 = (avg["SQ_INSTS_VALU_FLOPS_FP32"] + avg.get("SQ_INSTS_VALU_FLOPS_FP32_TRANS", 0.0)) * s32
+            f64 = (avg.get("SQ_INSTS_VALU_FLOPS_FP64", 0.0) + avg.get("SQ_INSTS_VALU_FLOPS_FP64_TRANS", 0.0)) * s64
             f["valu_fp32_tflops"] = f32 / us / 1e6
             f["valu_fp32_frac"] = f["valu_fp32_tflops"] / PEAK_VALU_F32_TFLOPS
             f["valu_fp64_tflops"] = f64 / us / 1e6
@@ -267,7 +278,10 @@ def summarize_counters(dirs, workload, steps=3):
              "```", "",
              "Per dispatch.  Counter runs serialize the dispatches, so `us` is the kernel alone.",
              "FETCH_SIZE / WRITE_SIZE are scaled by a 256 MiB device copy "
-             f"(x {scale.get('FETCH_SIZE', float('nan')):.4f}, x {scale.get('WRITE_SIZE', float('nan')):.4f}).",
+             f"(x {scale.get('FETCH_SIZE', float('nan')):.4f}, x {scale.get('WRITE_SIZE', float('nan')):.4f});",
+             f"the FLOP counters by {CAL_MULS} fp64 and fp32 multiplies (torch) of the same run "
+             f"(x {scale.get('SQ_INSTS_VALU_FLOPS_FP64', float('nan')):.4f} fp64, "
+             f"x {scale.get('SQ_INSTS_VALU_FLOPS_FP32', float('nan')):.4f} fp32).",
              "VALU-active and wait shares are SQ_ACTIVE_INST_VALU and SQ_WAIT_ANY over SQ_WAVE_CYCLES;",
              "FLOP rates are SQ_INSTS_VALU_FLOPS_FP32 (+ _TRANS) and _FP64 over the dispatch's duration,",
              f"against {PEAK_VALU_F32_TFLOPS} (FP32) and {PEAK_VALU_F64_TFLOPS} (FP64) TFLOP/s.", "",
@@ -412,8 +426,14 @@ def main():
         src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
         dst.copy_(src)            # reads and writes 256 MiB
+        # kernels of known VALU work for the FLOP counters: 2^24 fp64 and
+        # 2^24 fp32 multiplies (one FLOP each)
+        x64 = torch.full((CAL_MULS,), 1.5, dtype=torch.float64, device=dev)
+        y64 = x64 * x64
+        x32 = torch.full((CAL_MULS,), 1.5, dtype=torch.float32, device=dev)
+        y32 = x32 * x32
         torch.cuda.synchronize()
-        del src, dst
+        del src, dst, x64, y64, x32, y32
 
     separate = (args.separate or args.dense or args.paper_eta > 0
                 or ((args.refit or args.clip or args.asym) and args.rule != "calib"))
