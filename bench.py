@@ -61,7 +61,7 @@ FLOP_PER_EVAL = 7                       # scale-mul, round, clamp, fma (2), squa
 PROFILES = os.path.join(ROOT, "profiles")
 ROOFLINE_KERNEL = "gemm_err_kernel"
 COPY_BYTES = 256 << 20
-STAGES = (("fit", ("fit_hist_kernel", "fit_dense_kernel")),
+STAGES = (("fit", ("fit_hist_kernel", "fit_small_kernel", "fit_dense_kernel")),
           ("output_error", ("form_d_kernel", "gemm_err_kernel", "finish_err_kernel")),
           ("reconstruct", ("reconstruct_kernel",)),
           ("deploy", ("int_forward_kernel", "integer_scales_kernel")))
@@ -140,13 +140,16 @@ def sources_digest():
 def kernel_key(profiler_name):
     """The library's timing name of a kernel from the demangled name rocprofv3
     prints (fit_hist_kernel<T, EPT, kLinear, kLat, kGlobal> ->
-    fit_hist_kernel<T,EPT,mode[,rebuilt]>)."""
+    fit_hist_kernel<T,EPT,mode[,rebuilt]>; fit_small_kernel<d>)."""
     m = re.search(r"fit_hist_kernel<(\d+), (\d+), (true|false), (true|false), (true|false)>",
                   profiler_name)
     if m:
         mode = "lattice" if m.group(4) == "true" else "linear" if m.group(3) == "true" else "grid"
         rebuilt = ",rebuilt" if m.group(5) == "true" else ""
         return f"fit_hist_kernel<{m.group(1)},{m.group(2)},{mode}{rebuilt}>"
+    m = re.search(r"fit_small_kernel<(\d+)>", profiler_name)
+    if m:
+        return f"fit_small_kernel<{m.group(1)}>"
     m = re.search(r"int_forward_kernel<(\d)>", profiler_name)
     if m:
         return f"int_forward_kernel<{(16, 4, 1)[int(m.group(1))]}>"

@@ -320,7 +320,11 @@ std::vector<FitJob> build_fit_jobs(Search mode, bool hist_fits, const mpq_layer 
         H.d = (int)L.d;
         H.c_begin = (int)j.channels;
         j.channels += L.c_out;
-        j.work += (double)L.c_out * (double)L.d;
+        // estimated time: a histogram-search channel costs ~ d + G per step
+        // (its elements' levels, then the candidates); a short channel's
+        // direct search ~ d G / 24 (both measured on MI355X)
+        j.work += (double)L.c_out *
+                  (L.d <= mpq::kSmallMaxDim ? (double)L.d * (double)n_grid / 24.0 : (double)(L.d + n_grid));
         j.layers.push_back(l);
     };
     for (int l = 0; l < n_layers; ++l) {
@@ -330,7 +334,7 @@ std::vector<FitJob> build_fit_jobs(Search mode, bool hist_fits, const mpq_layer 
         add_layer(j, l);
         jobs.push_back(j);
     }
-    for (int v = 0; v <= mpq::hist_variant(mpq::kHistMaxDim); ++v) {
+    for (int v = 0; v < mpq::hist_variant_count(); ++v) {
         FitJob j = fresh(v);
         for (int l = 0; l <= n_layers; ++l) {
             const bool flush = l == n_layers || j.b.n_layers == mpq::kMaxBatchLayers ||
@@ -345,6 +349,10 @@ std::vector<FitJob> build_fit_jobs(Search mode, bool hist_fits, const mpq_layer 
             add_layer(j, l);
         }
     }
+    // a launch takes at least the serial steps of one channel (~15 us, as
+    // long as ~4e5 units of the estimate above), however few its channels
+    for (FitJob &j : jobs)
+        if (!j.dense) j.work = std::max(j.work, 4e5);
     return jobs;
 }
 
@@ -691,51 +699,25 @@ int quantize_impl(const mpq_layer *layers, int n_layers, int bits, int max_point
     }
     // a fit that keeps its residual in registers writes its layers' rows of
     // D for the output error, which then forms none for them
+    std::vector<int64_t> d_off(err.size());
+    std::vector<int> d_grp(err.size());
+    if (!err.empty()) mpq::err_item_d_offsets(err.data(), (int)err.size(), d_off.data(), d_grp.data());
     for (FitJob &j : jobs) {
         if (j.dense || !mpq::hist_variant_writes_d(j.variant)) continue;
         for (int i = 0; i < j.b.n_layers; ++i) {
             const int l = j.layers[i];
-            if (err_of[l] < 0) continue;
-            int grp = 0;
-            const int64_t off = mpq::err_item_d_offset(err.data(), (int)err.size(), err_of[l], &grp);
-            if (off < 0) continue;
-            j.b.L[i].dres = (float *)(ej.scratch + ej.off[grp] + off);
+            if (err_of[l] < 0 || d_off[err_of[l]] < 0) continue;
+            j.b.L[i].dres = (float *)(ej.scratch + ej.off[d_grp[err_of[l]]] + d_off[err_of[l]]);
             err[err_of[l]].d_ready = 1;
         }
     }
-    // The reconstruction of a fit launch's layers follows it on its stream,
-    // in the longest fit's shadow, but for the longest fit's own layers:
-    // theirs runs beside the output error.
-    int big = 0;
-    for (int i = 1; i < (int)jobs.size(); ++i)
-        if (jobs[i].work > jobs[big].work) big = i;
-    std::vector<std::vector<mpq::RecLayer>> rec_after(jobs.size());
-    {
-        std::vector<int> rec_of(n_layers, -1);
-        for (int l = 0, r = 0; l < n_layers; ++l)
-            if (layers[l].c_out > 0 && layers[l].W_hat) rec_of[l] = r++;
-        std::vector<mpq::RecLayer> rest;
-        bytes = 0.0;
-        for (int i = 0; i < (int)jobs.size(); ++i)
-            for (int l : jobs[i].layers) {
-                if (rec_of[l] < 0) continue;
-                if (i != big) {
-                    rec_after[i].push_back(rec[rec_of[l]]);
-                } else {
-                    rest.push_back(rec[rec_of[l]]);
-                    bytes += 5.0 * (double)layers[l].c_out * (double)layers[l].d;
-                }
-            }
-        rec.swap(rest);
-    }
+    // The reconstruction of every layer: one launch beside the output error
+    // (it reads only the fit's outputs and is bound by HBM, the GEMM by MFMA).
     // 1. every fit, side by side (as mpq_fit_layers)
     std::vector<double> work;
     for (const FitJob &j : jobs) work.push_back(j.work);
     hipError_t e = run_concurrently(s, work, [&](int i, hipStream_t st) {
-        hipError_t e1 = launch_fit_job(jobs[i], n_grid, st);
-        if (e1 == hipSuccess && !rec_after[i].empty())
-            e1 = mpq::launch_reconstruct(rec_after[i].data(), (int)rec_after[i].size(), max_points, st);
-        return e1;
+        return launch_fit_job(jobs[i], n_grid, st);
     });
     if (dgrid) (void)mpq::scratch_free(dgrid, s);
     if (e != hipSuccess) {

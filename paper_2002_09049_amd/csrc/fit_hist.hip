@@ -38,6 +38,7 @@
 
 #include "internal.hpp"
 #include "mpq.h"
+#include "point_code.hpp"
 #include "reduce.hpp"
 
 namespace mpq {
@@ -497,29 +498,10 @@ fit_hist_kernel(const HistBatch B)
         float lmax = 0.0f;
         double lsum = 0.0;
         int8_t *qrow = qk + (int64_t)(i - 1) * d;
-        const double ap = (double)apend;
-        const double ia = 1.0 / ap;
-        // code of Eq. (10) at the searched scale.  First in fp32: with
-        // 2^-100 <= a <= 2^100, y32 = fl32(r) fl32(1 / a) is within |y| 3 2^-24 of
-        // r / a, under 2^-12 for |y| < 2^10 (larger quotients clip to the
-        // same M either way), so unless y32 lies within 2^-12 of a
-        // half-integer it rounds as r / a does.  Else in fp64: y is within
-        // |y| 2^-51 of the fp64 quotient fl(r / a), and only within 2^-40 of
-        // a half-integer is the quotient formed.
-        const bool fast = ap >= 0x1p-100 && ap <= 0x1p100;   // 1 / a a normal fp32
-        const float ia32 = (float)ia;
-        const float Mf = (float)M;
-        auto code_of = [&](double ru) {
-            if (fast) {
-                const float y32 = (float)ru * ia32;
-                const float c32 = rintf(y32);
-                if (fabsf(fabsf(y32 - c32) - 0.5f) > 0x1p-12f) return (double)fminf(fmaxf(c32, -Mf), Mf);
-            }
-            const double y = ru * ia;
-            double c = rint(y);
-            if (fabs(fabs(y - c) - 0.5) < 0x1p-40) c = rint(ru / ap);
-            return fmin(fmax(c, -Md), Md);
-        };
+        // code of Eq. (10) at the searched scale (fp32 first, fp64 near a
+        // half-integer)
+        const PointCode code_of(apend, M);
+        const double ap = code_of.ap;
         // the scale the residual update uses: the searched one, or (refit)
         // the least-squares scale of the codes, fl32(<r, q> / <q, q>)
         double aupd = ap;
@@ -982,10 +964,21 @@ size_t fit_hist_lds(int G)
 
 bool fit_hist_supports(int64_t d) { return d >= 1 && d <= kHistMaxDim; }
 
-bool hist_variant_writes_d(int v) { return v >= 0 && v < kNumVariants && !kVariants[v].rebuilt; }
+// the short-channel variants (fit_small.hip), one per length 1 ..
+// kSmallMaxDim, follow the histogram ones
+constexpr int kSmallVariant = kNumVariants;
+
+bool hist_variant_writes_d(int v)
+{
+    return (v >= kSmallVariant && v < kSmallVariant + kSmallMaxDim) ||
+           (v >= 0 && v < kNumVariants && !kVariants[v].rebuilt);
+}
+
+int hist_variant_count() { return kNumVariants + (int)kSmallMaxDim; }
 
 int hist_variant(int64_t d)
 {
+    if (d >= 1 && d <= kSmallMaxDim) return kSmallVariant + (int)d - 1;
     int v = 0;
     while (v + 1 < kNumVariants && d > (int64_t)kVariants[v].threads * kVariants[v].ept) ++v;
     return v;
@@ -1010,6 +1003,7 @@ int lattice_buckets(int variant, int M, int G, bool default_grid)
 std::string hist_kernel_name(int64_t d, int M, int G, bool default_grid)
 {
     const int v = hist_variant(d);
+    if (v >= kSmallVariant) return fit_small_name((int)d);
     char name[64];
     snprintf(name, sizeof name, "fit_hist_kernel<%d,%d,%s%s>", kVariants[v].threads, kVariants[v].ept,
              !default_grid ? "grid" : lattice_buckets(v, M, G, true) ? "lattice" : "linear",
@@ -1037,6 +1031,8 @@ hipError_t launch_zero_i32(int32_t *p, int64_t n, hipStream_t s)
 hipError_t launch_fit_hist(const HistBatch &batch, int variant, int64_t channels, hipStream_t s)
 {
     HistBatch b = batch;
+    if (variant >= kSmallVariant && variant < kSmallVariant + kSmallMaxDim)
+        return launch_fit_small(b, variant - kSmallVariant + 1, channels, s);
     if (variant < 0 || variant >= kNumVariants) return hipErrorInvalidValue;
     b.nlat = lattice_buckets(variant, b.M, b.G, !b.grid);
     const size_t lds = fit_hist_lds(b.G) + (size_t)b.nlat * sizeof(unsigned long long);

@@ -78,7 +78,7 @@ struct HistLayer {
     // (the midpoint of w, written by the fit; the points fit w - offset)
     float *offsets;
     // nullptr, or the output error's D for this layer (tiles of 128 rows by
-    // 32 k, row-major inside; see err_item_d_offset): the fit (not in
+    // 32 k, row-major inside; see err_item_d_offsets): the fit (not in
     // calibration steps) writes each channel's final residual there in fp32,
     // k past d zero (variants that keep the residual in registers only)
     float *dres;
@@ -118,7 +118,15 @@ static_assert(sizeof(HistBatch) <= 4096, "kernel arguments");
 size_t fit_hist_lds(int G);
 bool fit_hist_supports(int64_t d);
 int hist_variant(int64_t d);   // layers with equal variants may share a launch
+int hist_variant_count();      // variants are 0 .. hist_variant_count() - 1
 bool hist_variant_writes_d(int v);   // the variant's fit fills HistLayer::dres
+// Channels of up to kSmallMaxDim weights take the short-channel variants
+// (fit_small.hip), one per length d: one wavefront per channel, lanes over
+// the candidates, evaluated directly; the same batch descriptors and
+// results.  Every layer of a launch has channels of length d.
+constexpr int64_t kSmallMaxDim = 16;
+hipError_t launch_fit_small(const HistBatch &b, int d, int64_t channels, hipStream_t s);
+std::string fit_small_name(int d);
 // Name of the histogram kernel that fits channels of length d (default grid
 // when default_grid, else a caller's grid), as LaunchTimer records it.
 std::string hist_kernel_name(int64_t d, int M, int G, bool default_grid);
@@ -191,10 +199,11 @@ double err_group_flop(const ErrLayerIn *in, int n_in, int group);
 hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, int P, void *scratch,
                                      hipStream_t s);
 // Where the err item of in[i] keeps its rows of D (fp32 tiles [ceil(C / 128)]
-// [ceil(d / 32)][128][32], row-major inside, k past d zero):
-// the byte offset inside its group's scratch, and the group in *group; -1
-// when in[i] has no err item or its rows are clipping candidates.
-int64_t err_item_d_offset(const ErrLayerIn *in, int n_in, int i, int *group);
+// [ceil(d / 32)][128][32], row-major inside, k past d zero): for each
+// in[i], the byte offset inside its group's scratch in off[i] and the group
+// in group[i]; -1 for both when in[i] has no err item or its rows are
+// clipping candidates.  Every group's layout is formed once.
+void err_item_d_offsets(const ErrLayerIn *in, int n_in, int64_t *off, int *group);
 
 // Clipping of Eq. (13) as the first point: candidate scales, then (after the
 // output error of the candidates) the choice of point 1.  One workgroup per

@@ -616,17 +616,25 @@ size_t err_group_scratch_bytes(const ErrLayerIn *in, int n_in, int group)
     return group_bytes(it.data() + base, cnt);
 }
 
-int64_t err_item_d_offset(const ErrLayerIn *in, int n_in, int i, int *group)
+void err_item_d_offsets(const ErrLayerIn *in, int n_in, int64_t *off, int *group)
 {
-    const std::vector<Item> it = items_of(in, n_in);
-    for (size_t x = 0; x < it.size(); ++x) {
-        if (it[x].in != &in[i] || it[x].use_points != 1) continue;
-        const size_t base = x / kMaxErrItems * kMaxErrItems;
-        const int cnt = (int)std::min<size_t>(kMaxErrItems, it.size() - base);
-        *group = (int)(x / kMaxErrItems);
-        return (int64_t)group_layout(it.data() + base, cnt).off[x - base];
+    for (int i = 0; i < n_in; ++i) {
+        off[i] = -1;
+        group[i] = -1;
     }
-    return -1;
+    const std::vector<Item> it = items_of(in, n_in);
+    // each group's layout once
+    for (size_t base = 0; base < it.size(); base += kMaxErrItems) {
+        const int cnt = (int)std::min<size_t>(kMaxErrItems, it.size() - base);
+        const GroupLayout lay = group_layout(it.data() + base, cnt);
+        for (int x = 0; x < cnt; ++x) {
+            const Item &I = it[base + (size_t)x];
+            if (I.use_points != 1) continue;
+            const int i = (int)(I.in - in);
+            off[i] = (int64_t)lay.off[x];
+            group[i] = (int)(base / kMaxErrItems);
+        }
+    }
 }
 
 double err_group_flop(const ErrLayerIn *in, int n_in, int group)

@@ -21,6 +21,8 @@ def test_kernel_key_maps_profiler_names():
     assert k("void mpq::(anonymous namespace)::gemm_err_kernel<true>(mpq::ErrGroup)") == "gemm_err_kernel"
     assert bench.stage_of("form_d_kernel") == "output_error"
     assert bench.stage_of("fit_hist_kernel<64,1,linear>") == "fit"
+    assert k("void mpq::(anonymous namespace)::fit_small_kernel<9>(mpq::HistBatch, int)") == "fit_small_kernel<9>"
+    assert bench.stage_of("fit_small_kernel<16>") == "fit"
     assert bench.stage_of("zero_i32_kernel") is None
     assert k("void mpq::(anonymous namespace)::int_forward_kernel<0>(mpq::IntGroup)") == "int_forward_kernel<16>"
     assert k("int_forward_kernel<2>(mpq::IntGroup)") == "int_forward_kernel<1>"

@@ -49,6 +49,8 @@ CASES = [
     # (C, d, bits, P, G, N, eps, relative)
     (3, 1, 4, 4, 128, 1, 1e-3, True),
     (40, 9, 4, 8, 512, 64, 1e-3, True),
+    (61, 16, 3, 6, 128, 40, 1e-2, True),
+    (50, 5, 4, 8, 512, 16, 1e-3, False),
     (33, 17, 3, 8, 7, 5, 1e-2, True),
     (130, 147, 4, 4, 256, 300, 1e-3, True),
     (64, 576, 4, 4, 128, 256, 1e-3, True),

@@ -94,6 +94,7 @@ GATE = [
     (9, 4608, 3, 8, 512, 257),
     (5, 9000, 4, 4, 64, 100),
     (4, 20000, 3, 4, 256, 64),
+    (61, 16, 3, 6, 128, 40),
 ]
 
 

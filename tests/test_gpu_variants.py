@@ -43,6 +43,8 @@ REFIT = [
     (3, 1, 4, 4, 128, 1e-3),
     (40, 9, 4, 8, 512, 1e-3),
     (33, 17, 3, 8, 7, 1e-4),
+    (50, 16, 3, 6, 7, 0.0),
+    (30, 4, 8, 4, 1000, 1e-4),
     (64, 147, 4, 4, 256, 1e-3),
     (64, 576, 4, 4, 128, 1e-3),
     (20, 1000, 2, 6, 1000, 0.0),
@@ -120,6 +122,7 @@ CLIP = [
     # (C, d, bits, P, G, N, tol)
     (3, 1, 4, 4, 128, 5, 1e-3),
     (40, 9, 4, 8, 512, 64, 1e-3),
+    (41, 16, 3, 6, 64, 20, 1e-4),
     (70, 147, 4, 4, 256, 300, 1e-3),
     (64, 576, 3, 6, 128, 256, 1e-4),
     (20, 2304, 4, 4, 256, 1024, 1e-3),
@@ -301,6 +304,7 @@ ASYM = [
     # (C, d, bits, P, G, tol, shift): channels with a common offset exercise B2
     (5, 1, 4, 4, 128, 1e-3, 0.0),
     (40, 9, 4, 8, 512, 1e-3, 0.3),
+    (43, 16, 3, 6, 128, 1e-4, -0.7),
     (64, 147, 4, 4, 256, 1e-3, 1.0),
     (64, 576, 3, 6, 128, 1e-4, -0.5),
     (10, 2304, 4, 4, 256, 1e-3, 2.0),
