@@ -150,7 +150,7 @@ def kernel_key(profiler_name):
     m = re.search(r"fit_small_kernel<(\d+)>", profiler_name)
     if m:
         return f"fit_small_kernel<{m.group(1)}>"
-    m = re.search(r"int_forward_kernel<(\d)>", profiler_name)
+    m = re.search(r"int_forward_kernel<(\d)(, \d+)?>", profiler_name)
     if m:
         return f"int_forward_kernel<{(16, 4, 1)[int(m.group(1))]}>"
     m = re.search(r"(\w+_kernel)\b", profiler_name)

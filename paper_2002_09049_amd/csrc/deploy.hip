@@ -10,17 +10,22 @@
 //   Step 1  z_i = q_i . x_t            (int8 MFMA, 32-bit accumulators)
 //   Step 2  s   = sum_{i<n_k} A_i z_i   (64 bits)
 //   Step 3  y   = s >> p                (arithmetic shift: floor(s / 2^p))
-// The GEMM's rows are (channel, point) pairs: row k * Pp + i is point i of
-// channel k, with Pp = max_points rounded up to a power of two, so a tile of
-// 128 rows holds 128 / Pp whole channels.  A row past the channel's count
-// (or past max_points) loads as zeros and adds nothing.  A workgroup of four
-// wavefronts computes a 128 x 128 tile of z (v_mfma_i32_32x32x32_i8, 64-deep
-// K slabs through double-buffered LDS); the epilogue puts the int32 tile in
-// LDS and each thread forms Step 2 and 3 for (channel, column) pairs and
-// writes Y [C][N] row-contiguously.  Codes [C][P][d] and X [N][d] are both
+// A workgroup of four wavefronts owns 32 channels by 128 columns.  The GEMM's
+// rows are point-major: row block i (32 rows) holds point i of the 32
+// channels, and the points run in chunks of kPts (4, or 8 when max_points
+// > 4) only up to the largest count among the tile's channels, so points
+// that no channel of the tile has are neither loaded nor multiplied; a row
+// past its channel's count loads as zeros and adds nothing.  Wavefront w
+// multiplies every row block by its 32 columns (v_mfma_i32_32x32x32_i8,
+// 64-deep K slabs through double-buffered LDS), so a lane holds, for one
+// column, z of every point of the 16 channels it covers: Step 2 and 3 run
+// in its registers (no exchange), and each store writes a column run of
+// two channels' rows of Y [C][N].  Codes [C][P][d] and X [N][d] are both
 // k-contiguous, so both operands are staged alike, as rows of 64 bytes;
 // buffer loads return zeros past the rows and past d.
 #include <stdio.h>
+
+#include <algorithm>
 
 #include "internal.hpp"
 #include "mpq.h"
@@ -33,11 +38,13 @@ namespace {
 typedef int int32x16 __attribute__((ext_vector_type(16)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kIM = 128, kIN = 128, kIK = 64;   // tile and K slab (bytes)
+constexpr int kICh = 32, kIN = 128, kIK = 128; // channels and columns of a tile; K slab (bytes)
+constexpr int kIPieces = kIK / 16;             // 16-byte pieces of a slab row
 constexpr int kIPad = 16;                       // LDS row: 80 bytes
 constexpr int kIRow = kIK + kIPad;
 constexpr int kIThreads = 256;
 constexpr uint32_t kIOob = 0x80000000u;
+constexpr int kIXcds = 8;                       // MI355X: workgroups are dealt to 8 XCDs in turn
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes)
 {
@@ -67,27 +74,31 @@ __global__ void integer_scales_kernel(const float *scales, const int32_t *counts
 // aligned), 4-byte words (d % 4 == 0, 4-byte aligned) or bytes.
 enum { kLoad16 = 0, kLoad4 = 1, kLoad1 = 2 };
 
-// Row r of the A operand starts at byte rowoff[r] of the codes, or is
-// absent (rowoff < 0: zeros); row r of B at byte r * d of X.
-template <int kMode>
-__device__ __forceinline__ void load_rows(__amdgpu_buffer_rsrc_t rs, const int *rowoff, int64_t d, int64_t k0,
-                                          i32x4 (&v)[2])
+// kRows rows of 64 bytes from K offset k0, four 16-byte pieces a row, kRows /
+// 64 pieces per thread.  Row r starts at byte rowoff[r] of the buffer, or
+// is absent (rowoff < 0, or r >= live: zeros, nothing loaded).
+template <int kMode, int kRows>
+__device__ __forceinline__ void load_rows(__amdgpu_buffer_rsrc_t rs, const int *rowoff, int live, int64_t d,
+                                          int64_t k0, i32x4 (&v)[kRows * kIPieces / kIThreads])
 {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < kRows * kIPieces / kIThreads; ++h) {
         const int piece = (int)threadIdx.x + h * kIThreads;
-        const int ro = rowoff[piece / 4];
-        const int64_t k = k0 + 16 * (piece % 4);
+        const int row = piece / kIPieces;
+        const int ro = row < live ? rowoff[row] : -1;
+        const int64_t k = k0 + 16 * (piece % kIPieces);
         const bool ok = ro >= 0;
         const int64_t at = (int64_t)ro + k;
-        if constexpr (kMode == kLoad16) {
+        if (!ok) {
+            v[h] = i32x4{0, 0, 0, 0};
+        } else if constexpr (kMode == kLoad16) {
             v[h] = __builtin_bit_cast(i32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                 rs, (ok && k < d) ? (uint32_t)at : kIOob, 0, 0));
+                                                 rs, k < d ? (uint32_t)at : kIOob, 0, 0));
         } else if constexpr (kMode == kLoad4) {
 #pragma unroll
             for (int w = 0; w < 4; ++w)
                 v[h][w] = (int)__builtin_amdgcn_raw_buffer_load_b32(
-                    rs, (ok && k + 4 * w < d) ? (uint32_t)(at + 4 * w) : kIOob, 0, 0);
+                    rs, k + 4 * w < d ? (uint32_t)(at + 4 * w) : kIOob, 0, 0);
         } else {
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
@@ -96,7 +107,7 @@ __device__ __forceinline__ void load_rows(__amdgpu_buffer_rsrc_t rs, const int *
                 for (int b = 0; b < 4; ++b) {
                     const int64_t kk = 4 * w + b;
                     word |= (uint32_t)__builtin_amdgcn_raw_buffer_load_b8(
-                                rs, (ok && k + kk < d) ? (uint32_t)(at + kk) : kIOob, 0, 0)
+                                rs, k + kk < d ? (uint32_t)(at + kk) : kIOob, 0, 0)
                             << (8 * b);
                 }
                 v[h][w] = (int)word;
@@ -105,136 +116,156 @@ __device__ __forceinline__ void load_rows(__amdgpu_buffer_rsrc_t rs, const int *
     }
 }
 
-__device__ __forceinline__ void store_slab(int8_t *s, const i32x4 (&v)[2])
+template <int kRows>
+__device__ __forceinline__ void store_slab(int8_t *s, const i32x4 (&v)[kRows * kIPieces / kIThreads])
 {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < kRows * kIPieces / kIThreads; ++h) {
         const int piece = (int)threadIdx.x + h * kIThreads;
-        *(i32x4 *)(s + (piece / 4) * kIRow + 16 * (piece % 4)) = v[h];
+        *(i32x4 *)(s + (piece / kIPieces) * kIRow + 16 * (piece % kIPieces)) = v[h];
     }
 }
 
-constexpr int kSlabBytes = kIM * kIRow;          // one operand, one buffer
-constexpr int kZRow = 72;                        // int32 row of the z tile (bank spread)
-constexpr int kLdsBytes = 4 * kSlabBytes;        // 2 operands x 2 buffers
-static_assert(kIM * kZRow * 4 <= kLdsBytes, "the z tile reuses the staging LDS");
-
-template <int kMode>
-__global__ void __launch_bounds__(kIThreads) int_forward_kernel(const IntGroup g)
+// Step 1 for one chunk of kN live points (row blocks 0 .. kN - 1 of the A
+// slab): z of the wavefront's 32 columns, K slab by K slab, into acc, and
+// Step 2's terms added to the lane's 64-bit sums.  The point count is a
+// template argument so that the LDS reads of a K step are issued ahead of
+// its MFMAs.
+template <int kMode, int kPts, int kN>
+__device__ __forceinline__ void chunk_sums(__amdgpu_buffer_rsrc_t rsA, __amdgpu_buffer_rsrc_t rsB,
+                                           const int *s_offA, const int *s_offB, const int32_t *s_coef,
+                                           int8_t (*ldsA)[kPts * kICh * kIRow], int8_t (*ldsB)[kIN * kIRow],
+                                           int64_t d, long long (&sum)[16])
 {
-    __shared__ __align__(16) int8_t lds[kLdsBytes];
-    __shared__ int s_offA[kIM], s_offB[kIN];
-    __shared__ int32_t s_coef[kIM];
-
-    const int li = last_at_most(g.n_layers, (int)blockIdx.x, [&](int i) { return g.L[i].block_begin; });
-    const IntLayer &L = g.L[li];
-    int tn = (int)blockIdx.x - L.block_begin, tm = 0;
-    while (tn >= L.ntn) {
-        tn -= L.ntn;
-        ++tm;
-    }
-    const int P = g.P, lp = g.log2_pp, Pp = 1 << lp;
-    const int64_t C = L.C, d = L.d, N = L.N;
-    const int64_t row0 = (int64_t)tm * kIM, col0 = (int64_t)tn * kIN;
-    const int t = threadIdx.x;
-    const int lane = t % kWave, wid = t / kWave;
-    const int wm = wid / 2, wn = wid % 2;
-
-    // rows of this tile: point i of channel k (or absent) and its A_i
-    if (t < kIM) {
-        const int64_t r = row0 + t, k = r >> lp;
-        const int i = (int)(r & (Pp - 1));
-        const bool ok = k < C && i < P && i < L.counts[k];
-        s_offA[t] = ok ? (int)((k * P + i) * d) : -1;   // codes below 2^31 bytes (host check)
-        s_coef[t] = ok ? L.A[k * P + i] : 0;
-    } else {
-        const int64_t c = col0 + (t - kIM);
-        s_offB[t - kIM] = c < N ? (int)(c * d) : -1;    // X below 2^31 bytes (host check)
-    }
-    const __amdgpu_buffer_rsrc_t rsA = rsrc(L.codes, (uint32_t)(C * P * d));
-    const __amdgpu_buffer_rsrc_t rsB = rsrc(L.X, (uint32_t)(N * d));
-    __syncthreads();
-
-    int32x16 acc[2][2];
+    constexpr int kARows = kPts * kICh;
+    const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
+    int32x16 acc[kN];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int i = 0; i < kN; ++i)
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) acc[a][b][v] = 0;
-
-    // Step 1: the tile of z, K slab by K slab
-    auto sA = [&](int b) { return lds + b * kSlabBytes; };
-    auto sB = [&](int b) { return lds + (2 + b) * kSlabBytes; };
-    i32x4 ra[2], rb[2];
+        for (int v = 0; v < 16; ++v) acc[i][v] = 0;
+    i32x4 ra[kARows * kIPieces / kIThreads], rb[kIN * kIPieces / kIThreads];
     int buf = 0;
-    load_rows<kMode>(rsA, s_offA, d, 0, ra);
-    load_rows<kMode>(rsB, s_offB, d, 0, rb);
-    store_slab(sA(0), ra);
-    store_slab(sB(0), rb);
+    load_rows<kMode, kARows>(rsA, s_offA, kN * kICh, d, 0, ra);
+    load_rows<kMode, kIN>(rsB, s_offB, kIN, d, 0, rb);
+    store_slab<kARows>(ldsA[0], ra);
+    store_slab<kIN>(ldsB[0], rb);
     __syncthreads();
     for (int64_t k0 = 0; k0 < d; k0 += kIK) {
         const bool more = k0 + kIK < d;
         if (more) {   // global loads in flight during the MFMAs
-            load_rows<kMode>(rsA, s_offA, d, k0 + kIK, ra);
-            load_rows<kMode>(rsB, s_offB, d, k0 + kIK, rb);
+            load_rows<kMode, kARows>(rsA, s_offA, kN * kICh, d, k0 + kIK, ra);
+            load_rows<kMode, kIN>(rsB, s_offB, kIN, d, k0 + kIK, rb);
         }
         // v_mfma_i32_32x32x32_i8: lane l supplies row (or column) l % 32,
         // bytes 16 * (l / 32) .. +15 of the 32-deep K step
 #pragma unroll
         for (int ks = 0; ks < kIK; ks += 32) {
             const int kk = ks + 16 * (lane / 32);
-            i32x4 av[2], bv[2];
+            const i32x4 bv = *(const i32x4 *)(ldsB[buf] + (wid * 32 + lane % 32) * kIRow + kk);
+            i32x4 av[kN];
 #pragma unroll
-            for (int a = 0; a < 2; ++a)
-                av[a] = *(const i32x4 *)(sA(buf) + (wm * 64 + a * 32 + lane % 32) * kIRow + kk);
+            for (int i = 0; i < kN; ++i) av[i] = *(const i32x4 *)(ldsA[buf] + (i * kICh + lane % 32) * kIRow + kk);
 #pragma unroll
-            for (int b = 0; b < 2; ++b)
-                bv[b] = *(const i32x4 *)(sB(buf) + (wn * 64 + b * 32 + lane % 32) * kIRow + kk);
-#pragma unroll
-            for (int a = 0; a < 2; ++a)
-#pragma unroll
-                for (int b = 0; b < 2; ++b)
-                    acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(av[a], bv[b], acc[a][b], 0, 0, 0);
+            for (int i = 0; i < kN; ++i) acc[i] = __builtin_amdgcn_mfma_i32_32x32x32_i8(av[i], bv, acc[i], 0, 0, 0);
         }
         if (more) {
-            store_slab(sA(buf ^ 1), ra);
-            store_slab(sB(buf ^ 1), rb);
+            store_slab<kARows>(ldsA[buf ^ 1], ra);
+            store_slab<kIN>(ldsB[buf ^ 1], rb);
         }
         __syncthreads();
         buf ^= 1;
     }
+    // Step 2 for the chunk's points, in the lane's registers
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        const int ch = 8 * (v / 4) + 4 * (lane / 32) + v % 4;
+#pragma unroll
+        for (int i = 0; i < kN; ++i) sum[v] += (long long)s_coef[i * kICh + ch] * (long long)acc[i][v];
+        // one channel's terms at a time (hoisting every coefficient read
+        // ahead would hold them all in registers)
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
 
-    // Steps 2 and 3, one half of the columns at a time: the waves of that
-    // half put their z blocks in LDS (lane holds column lane % 32 and, in
-    // register v, row 8 * (v / 4) + 4 * (lane / 32) + (v % 4) of a 32 x 32
-    // block), then every thread sums A_i z_i over the rows of a channel
-    int32_t *Z = (int32_t *)lds;   // [kIM][kZRow], columns 0..63 of the half
-    const int cpt = kIM >> lp;     // channels per tile
-    for (int half = 0; half < 2; ++half) {
-        if (wn == half) {
+template <int kMode, int kPts>
+__global__ void __launch_bounds__(kIThreads) int_forward_kernel(const IntGroup g)
+{
+    constexpr int kARows = kPts * kICh;   // rows of a chunk's A slab
+    __shared__ __align__(16) int8_t ldsA[2][kARows * kIRow];
+    __shared__ __align__(16) int8_t ldsB[2][kIN * kIRow];
+    __shared__ int s_offA[kARows], s_offB[kIN];
+    __shared__ int32_t s_coef[kARows];
+    __shared__ int s_imax;
+
+    const int li = last_at_most(g.n_layers, (int)blockIdx.x, [&](int i) { return g.L[i].block_begin; });
+    const IntLayer &L = g.L[li];
+    // XCD-contiguous tiles: block_begin is a multiple of kIXcds, so b % kIXcds
+    // is the XCD this block runs on.  Each XCD takes a contiguous run of the
+    // layer's tiles, row tiles fastest, so the row tiles that read one
+    // column tile of X run together under one L2.
+    const int b = (int)blockIdx.x - L.block_begin;
+    const int T = L.ntm * L.ntn;
+    const int xcd = b % kIXcds, slot = b / kIXcds;
+    const int q = T / kIXcds, rem = T % kIXcds;
+    if (slot >= q + (xcd < rem ? 1 : 0)) return;   // padding block
+    const int tile = xcd * q + (xcd < rem ? xcd : rem) + slot;
+    const int tn = tile / L.ntm, tm = tile - tn * L.ntm;
+    const int P = g.P;
+    const int64_t C = L.C, d = L.d, N = L.N;
+    const int64_t ch0 = (int64_t)tm * kICh, col0 = (int64_t)tn * kIN;
+    const int t = threadIdx.x;
+    const int lane = t % kWave, wid = t / kWave;   // wavefront wid: columns 32 wid ..
+
+    // the columns of the tile, and the largest point count of its channels
+    if (t < kIN) {
+        const int64_t c = col0 + t;
+        s_offB[t] = c < N ? (int)(c * d) : -1;    // X below 2^31 bytes (host check)
+    }
+    if (t < kWave) {
+        const int64_t k = ch0 + t;
+        int n = (t < kICh && k < C) ? L.counts[k] : 0;
+        n = wave_reduce(n, MaxOp());
+        if (t == 0) s_imax = n < P ? n : P;
+    }
+    const __amdgpu_buffer_rsrc_t rsA = rsrc(L.codes, (uint32_t)(C * P * d));
+    const __amdgpu_buffer_rsrc_t rsB = rsrc(L.X, (uint32_t)(N * d));
+    __syncthreads();
+    const int imax = s_imax;
+
+    // lane: column col0 + 32 wid + lane % 32; in register v of a 32 x 32
+    // block, row (channel of the tile) 8 (v / 4) + 4 (lane / 32) + v % 4
+    long long sum[16];
 #pragma unroll
-            for (int a = 0; a < 2; ++a)
-#pragma unroll
-                for (int b = 0; b < 2; ++b)
-#pragma unroll
-                    for (int v = 0; v < 16; ++v) {
-                        const int r = wm * 64 + a * 32 + 8 * (v / 4) + 4 * (lane / 32) + (v % 4);
-                        Z[r * kZRow + b * 32 + lane % 32] = acc[a][b][v];
-                    }
+    for (int v = 0; v < 16; ++v) sum[v] = 0;
+    for (int p0 = 0; p0 < imax; p0 += kPts) {
+        // rows of the chunk: point p0 + r / 32 of channel ch0 + r % 32
+        for (int r = t; r < kARows; r += kIThreads) {
+            const int64_t k = ch0 + r % kICh;
+            const int i = p0 + r / kICh;
+            const bool ok = k < C && i < P && i < L.counts[k];
+            s_offA[r] = ok ? (int)((k * P + i) * d) : -1;   // codes below 2^31 bytes (host check)
+            s_coef[r] = ok ? L.A[k * P + i] : 0;
         }
         __syncthreads();
-        for (int e = t; e < cpt * 64; e += kIThreads) {
-            const int kk = e / 64, c = e % 64;
-            const int64_t k = (row0 >> lp) + kk, col = col0 + half * 64 + c;
-            long long sum = 0;
-            for (int i = 0; i < Pp; ++i) {
-                const int r = kk * Pp + i;
-                sum += (long long)s_coef[r] * (long long)Z[r * kZRow + c];
-            }
-            if (k < C && col < N) L.Y[k * N + col] = sum >> g.p;
+        const int npts = imax - p0 < kPts ? imax - p0 : kPts;   // uniform
+        switch (npts) {
+#define MPQ_CHUNK(n) \
+    case n: if constexpr (n <= kPts) chunk_sums<kMode, kPts, n>(rsA, rsB, s_offA, s_offB, s_coef, ldsA, ldsB, d, sum); break;
+            MPQ_CHUNK(1) MPQ_CHUNK(2) MPQ_CHUNK(3) MPQ_CHUNK(4)
+            MPQ_CHUNK(5) MPQ_CHUNK(6) MPQ_CHUNK(7) MPQ_CHUNK(8)
+#undef MPQ_CHUNK
+        default: break;
         }
-        __syncthreads();
+        __syncthreads();   // the next chunk rewrites s_offA and s_coef
+    }
+
+    // Step 3 and the stores: a store writes two 32-column runs of Y rows
+    const int64_t col = col0 + wid * 32 + lane % 32;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        const int64_t k = ch0 + 8 * (v / 4) + 4 * (lane / 32) + v % 4;
+        if (k < C && col < N) L.Y[k * N + col] = sum[v] >> g.p;
     }
 }
 
@@ -261,21 +292,27 @@ int int_forward_mode(const IntLayer &L)
 
 hipError_t launch_int_forward(IntGroup &h, int mode, hipStream_t s)
 {
-    int lp = 0;
-    while ((1 << lp) < h.P) ++lp;
-    h.log2_pp = lp;
+    // longest K first: a long layer's tiles start before the short ones that
+    // fill in beside them (the layers are independent)
+    std::stable_sort(h.L, h.L + h.n_layers, [](const IntLayer &a, const IntLayer &b) { return a.d > b.d; });
     int64_t blocks = 0;
     for (int l = 0; l < h.n_layers; ++l) {
         IntLayer &L = h.L[l];
         if (int_forward_mode(L) != mode) return hipErrorInvalidValue;
         L.ntn = (int)((L.N + kIN - 1) / kIN);
-        L.block_begin = (int)blocks;
-        blocks += ((L.C << lp) + kIM - 1) / kIM * L.ntn;
+        L.ntm = (int)((L.C + kICh - 1) / kICh);
+        L.block_begin = (int)blocks;   // a multiple of kIXcds
+        const int64_t tiles = (int64_t)L.ntm * L.ntn;
+        if (tiles > 0x7fffffffLL) return hipErrorInvalidValue;
+        blocks += (tiles + kIXcds - 1) / kIXcds * kIXcds;
     }
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    auto kern = mode == kLoad16 ? int_forward_kernel<kLoad16>
-              : mode == kLoad4 ? int_forward_kernel<kLoad4> : int_forward_kernel<kLoad1>;
+    // chunks of four points, or eight when a channel may hold more than four
+    const bool wide = h.P > 4;
+    auto kern = mode == kLoad16 ? (wide ? int_forward_kernel<kLoad16, 8> : int_forward_kernel<kLoad16, 4>)
+              : mode == kLoad4  ? (wide ? int_forward_kernel<kLoad4, 8> : int_forward_kernel<kLoad4, 4>)
+                                : (wide ? int_forward_kernel<kLoad1, 8> : int_forward_kernel<kLoad1, 4>);
     const char *name = mode == kLoad16 ? "int_forward_kernel<16>"
                      : mode == kLoad4 ? "int_forward_kernel<4>" : "int_forward_kernel<1>";
     LaunchTimer timer(s, name);

@@ -251,9 +251,9 @@ hipError_t launch_integer_scales(const float *scales, const int32_t *counts, int
                                  int32_t *A, unsigned long long *clamped, hipStream_t s);
 
 // Integer forward of up to kMaxIntLayers layers of one load mode in one
-// launch (one workgroup per 128-row x 128-column tile of the (channel,
-// point) x column product); ntn, block_begin and log2_pp are set by
-// launch_int_forward.  Each layer's codes and X are below 2^31 bytes.
+// launch (one workgroup per tile of 32 channels by 128 columns); ntm, ntn
+// and block_begin are set by launch_int_forward.  Each layer's codes and X
+// are below 2^31 bytes.
 struct IntLayer {
     const int8_t *codes;    // [C][P][d]
     const int32_t *A;       // [C][P]
@@ -261,13 +261,12 @@ struct IntLayer {
     const int8_t *X;        // [N][d]
     int64_t *Y;             // [C][N]
     int64_t C, d, N;
-    int ntn, block_begin;
+    int ntm, ntn, block_begin;
 };
 constexpr int kMaxIntLayers = 32;
 struct IntGroup {
     int n_layers;
     int P, p;
-    int log2_pp;            // rows per channel: max_points rounded up to a power of two
     IntLayer L[kMaxIntLayers];
 };
 static_assert(sizeof(IntGroup) <= 4096, "kernel arguments");

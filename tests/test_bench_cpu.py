@@ -26,6 +26,7 @@ def test_kernel_key_maps_profiler_names():
     assert bench.stage_of("zero_i32_kernel") is None
     assert k("void mpq::(anonymous namespace)::int_forward_kernel<0>(mpq::IntGroup)") == "int_forward_kernel<16>"
     assert k("int_forward_kernel<2>(mpq::IntGroup)") == "int_forward_kernel<1>"
+    assert k("void mpq::(anonymous namespace)::int_forward_kernel<1, 8>(mpq::IntGroup)") == "int_forward_kernel<4>"
     assert bench.stage_of("int_forward_kernel<16>") == "deploy"
 
 
