@@ -521,7 +521,7 @@ std::vector<Item> items_of(const ErrLayerIn *in, int n_in)
     return it;
 }
 
-// K split of a layer: K ranges of about kRangeK, or of work / 512 slabs (two
+// K split of a layer: K ranges of at most kRangeK, or of work / 512 slabs (two
 // tiles per CU) for a layer that alone fills the GPU, and K ranges whose rows
 // of X stay below 2^31 bytes (a row tile of D does: d <= MPQ_MAX_ERR_D).  The ranges of a split layer make the
 // GEMM store fp32 Y tiles that the finish kernel reads back, so a layer of
@@ -540,7 +540,9 @@ Plan plan_item(const ErrLayerIn &I, bool list)
     const int64_t slabs = (I.d + kBK - 1) / kBK;
     const double work = (double)(q.ntm * q.ntn) * (double)slabs;
     const int64_t target = std::max<int64_t>(kRangeK / kBK, (int64_t)(work / 512.0 + 0.5));
-    int64_t sp = (slabs + target / 2) / target;
+    // enough ranges that none exceeds the target (MobileNetV2's d = 960
+    // layers, 30 slabs, took ~100 us as one range; 15-slab halves, 88 us)
+    int64_t sp = (slabs + target - 1) / target;
     sp = std::max<int64_t>(1, std::min<int64_t>(sp, slabs));
     int64_t kchunk = (slabs + sp - 1) / sp * kBK;
     const int64_t max_chunk = ((1LL << 31) - 1) / (4 * I.n) / kBK * kBK;   // >= kBK (n < 2^24)
