@@ -563,9 +563,9 @@ int err_jobs(const std::vector<mpq::ErrLayerIn> &in, hipStream_t s, ErrJobs *j,
 }
 
 hipError_t launch_err_job(const std::vector<mpq::ErrLayerIn> &in, const ErrJobs &j, int g, int P,
-                          hipStream_t st)
+                          hipStream_t st, int parts = mpq::kErrUpload | mpq::kErrKernels)
 {
-    return mpq::launch_output_error_group(in.data(), (int)in.size(), g, P, j.scratch + j.off[g], st);
+    return mpq::launch_output_error_group(in.data(), (int)in.size(), g, P, j.scratch + j.off[g], st, parts);
 }
 
 int output_error_impl(const mpq_layer *layers, int n_layers, int max_points, void *stream,
@@ -713,11 +713,20 @@ int quantize_impl(const mpq_layer *layers, int n_layers, int bits, int max_point
     }
     // The reconstruction of every layer: one launch beside the output error
     // (it reads only the fit's outputs and is bound by HBM, the GEMM by MFMA).
-    // 1. every fit, side by side (as mpq_fit_layers)
+    // 1. every fit, side by side (as mpq_fit_layers), and beside them the
+    // upload of the output error's descriptor tables, which reads nothing
+    // the fits write (so the GEMM starts as soon as the last fit ends)
     std::vector<double> work;
     for (const FitJob &j : jobs) work.push_back(j.work);
+    const int n_fit_jobs = (int)work.size();
+    const int n_groups = (int)ej.work.size();
+    if (n_groups > 0) work.push_back(0.0);
     hipError_t e = run_concurrently(s, work, [&](int i, hipStream_t st) {
-        return launch_fit_job(jobs[i], n_grid, st);
+        if (i < n_fit_jobs) return launch_fit_job(jobs[i], n_grid, st);
+        hipError_t e1 = hipSuccess;
+        for (int g = 0; g < n_groups && e1 == hipSuccess; ++g)
+            e1 = launch_err_job(err, ej, g, max_points, st, mpq::kErrUpload);
+        return e1;
     });
     if (dgrid) (void)mpq::scratch_free(dgrid, s);
     if (e != hipSuccess) {
@@ -730,7 +739,7 @@ int quantize_impl(const mpq_layer *layers, int n_layers, int bits, int max_point
     const int n_err_jobs = (int)w2.size();
     if (!rec.empty()) w2.push_back(bytes * 50.0);
     e = run_concurrently(s, w2, [&](int i, hipStream_t st) {
-        return i < n_err_jobs ? launch_err_job(err, ej, i, max_points, st)
+        return i < n_err_jobs ? launch_err_job(err, ej, i, max_points, st, mpq::kErrKernels)
                               : mpq::launch_reconstruct(rec.data(), (int)rec.size(), max_points, st);
     });
     if (ej.scratch) (void)mpq::scratch_free(ej.scratch, s);

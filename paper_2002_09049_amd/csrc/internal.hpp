@@ -196,8 +196,13 @@ struct ErrLayerIn {
 int err_group_count(const ErrLayerIn *in, int n_in);
 size_t err_group_scratch_bytes(const ErrLayerIn *in, int n_in, int group);
 double err_group_flop(const ErrLayerIn *in, int n_in, int group);
+// The parts of a group's launch: the upload of its descriptor table (small
+// kernels that depend on nothing the fit writes) and the form, GEMM and
+// finish kernels; a caller may enqueue the uploads earlier, beside other work.
+constexpr int kErrUpload = 1, kErrKernels = 2;
 hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, int P, void *scratch,
-                                     hipStream_t s);
+                                     hipStream_t s,
+                                     int parts = kErrUpload | kErrKernels);
 // Where the err item of in[i] keeps its rows of D (fp32 tiles [ceil(C / 128)]
 // [ceil(d / 32)][128][32], row-major inside, k past d zero): for each
 // in[i], the byte offset inside its group's scratch in off[i] and the group

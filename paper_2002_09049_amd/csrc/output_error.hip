@@ -649,7 +649,7 @@ double err_group_flop(const ErrLayerIn *in, int n_in, int group)
 }
 
 hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, int P, void *scratch,
-                                     hipStream_t s)
+                                     hipStream_t s, int parts)
 {
     const std::vector<Item> it = items_of(in, n_in);
     const size_t base = (size_t)group * kMaxErrItems;
@@ -734,7 +734,7 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
         hipError_t e = hipSuccess;
         // the descriptor table at the head of the group's scratch
         ErrLayer *dtab = (ErrLayer *)scratch;
-        for (int o = 0; o < cnt && e == hipSuccess; o += kDescChunk) {
+        for (int o = 0; (parts & kErrUpload) && o < cnt && e == hipSuccess; o += kDescChunk) {
             DescChunk c;
             c.dst = dtab + o;
             c.count = std::min(kDescChunk, cnt - o);
@@ -743,7 +743,7 @@ hipError_t launch_output_error_group(const ErrLayerIn *in, int n_in, int group, 
             hipLaunchKernelGGL(desc_upload_kernel, dim3(1), dim3(64), 0, s, c);
             e = hipGetLastError();
         }
-        if (e != hipSuccess) return e;
+        if (e != hipSuccess || !(parts & kErrKernels)) return e;
         if (fblocks > 0) {
             LaunchTimer timer(s, "form_d_kernel");
             hipLaunchKernelGGL(form_d_kernel, dim3((unsigned)fblocks), dim3(kFormThreads), 0, s, g,
