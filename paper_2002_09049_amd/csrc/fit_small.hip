@@ -119,7 +119,6 @@ __global__ void __launch_bounds__(kSmallWaves * kWave) fit_small_kernel(const Hi
     const int P = B.P;
     const int M = B.M;
     const double Md = (double)M;
-    const float Mf = (float)M;
     int8_t *qk = Ly.codes + k * (int64_t)P * d;
     const float *wk = Ly.W + k * (int64_t)d;
 
