@@ -365,10 +365,19 @@ gemm_err_kernel(const ErrGroup g, const ErrLayer *__restrict__ Ls)
         for (int v = 0; v < 16; ++v) acc[a][v] = 0.0f;
 
     // MFMA block a of a wavefront takes its rows 2 i + a (i < 32), so one
-    // 8-byte LDS read gives a lane both blocks' A operands
-    auto compute = [&](int buf) {
+    // 8-byte LDS read gives a lane both blocks' A operands.  A wavefront whose
+    // 64 rows hold no live row of D (a layer of 64 channels or fewer, a few
+    // listed rows) multiplies nothing, and a slab stops at the K range's end
+    // (a d = 9 layer takes 5 of the 16 steps): the skipped products are of
+    // zero padding, so the sums are unchanged.
+    const bool rows_live = row0 + wm * 64 < nact;   // uniform per wavefront
+    auto compute = [&](int buf, int s) {
+        if (!rows_live) return;
+        const int64_t left = kend - (kbeg + (int64_t)s * kBK);      // live k of the slab
+        const int klim = left >= kBK ? kBK : (int)((left + 1) & ~1);
 #pragma unroll
         for (int kk = 0; kk < kBK; kk += 2) {
+            if (kk >= klim) break;
             const int kr = kk + lane / 32;
             const float2 a2 = *(const float2 *)&sA[buf][kr][wm * 64 + 2 * (lane % 32)];
             const float bx = sX[buf][kr][wn * 32 + lane % 32];
@@ -384,12 +393,12 @@ gemm_err_kernel(const ErrGroup g, const ErrLayer *__restrict__ Ls)
     if (nslab > 2) load(ra0, rx0, 2);
     for (int s = 0; s < nslab; s += 2) {
         // buffer 0 holds slab s, set 1 slab s + 1, set 0 slab s + 2 (in flight)
-        compute(0);
+        compute(0, s);
         if (s + 1 < nslab) store(ra1, rx1, 1);
         __syncthreads();
         if (s + 1 >= nslab) break;
         if (s + 3 < nslab) load(ra1, rx1, s + 3);
-        compute(1);
+        compute(1, s + 1);
         if (s + 2 < nslab) store(ra0, rx0, 0);
         __syncthreads();
         if (s + 4 < nslab) load(ra0, rx0, s + 4);
