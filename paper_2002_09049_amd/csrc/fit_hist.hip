@@ -54,24 +54,36 @@ constexpr unsigned long long kLatMask = kLatOne - 1;
 constexpr int kLatMaxBuckets = 4096;
 
 struct HistShared {
-    double *ad;      // [G + 2]: ad[0] = 0, ad[g + 1] = a_g (an fp32 value), ad[G + 1] = +inf
-    float *af;       // [G + 2]: the same values in fp32 (half the LDS bytes per read)
-    float *c;        // [G]: grid multipliers c_g
+    // ha and hb hold a candidate's histogram sums until its error is formed;
+    // the same slots then hold that error (fp64 bits) and its bound (fp32
+    // bits, rounded up, in units of 2^be with be the exponent of ||r||^2, so
+    // that the ratio lies far inside fp32's range)
     long long *ha;   // [G] fixed-point sum of x per bin (lattice mode: per-candidate corrections)
     int *hb;         // [G] sum of (2k + 1) per bin (lattice mode: corrections)
-    double *e;       // [G] approximate candidate errors
-    double *bnd;     // [G] their error bounds
+    float *af;       // [G + 2]: af[0] = 0, af[g + 1] = a_g, af[G + 1] = +inf
     unsigned long long *lat;   // [nlat] lattice buckets (lattice mode only)
+
+    // the bound in fp32 above b 2^-be: that value is at least 2^-51 (b holds
+    // 8 2^-53 ||r||^2), so fl32 is normal and within relative 2^-24, and the
+    // product by 1 + 2^-22, rounded, lies above it
+    __device__ void put_err(int g, double e, double b, int be) const
+    {
+        ha[g] = __double_as_longlong(e);
+        hb[g] = __float_as_int((float)ldexp(b, -be) * 0x1.000004p0f);
+    }
+    __device__ double err(int g) const { return __longlong_as_double(ha[g]); }
+    __device__ double bnd(int g, int be) const { return ldexp((double)__int_as_float(hb[g]), be); }
 };
 
 // n = #{ g : h * a_g < x } over the non-decreasing candidates, by binary
-// search (general grids).  ad is the sentinel table of HistShared.
-__device__ __forceinline__ int count_bsearch(const double *ad, int G, double h, double x)
+// search (general grids).  af is the sentinel table of HistShared (a_g is an
+// fp32 value, so its fp64 widening is exact).
+__device__ __forceinline__ int count_bsearch(const float *af, int G, double h, double x)
 {
     int lo = 0, hi = G;
     while (lo < hi) {
         const int mid = (lo + hi) >> 1;
-        if (fma(h, ad[mid + 1], -x) < 0.0) lo = mid + 1;
+        if (fma(h, (double)af[mid + 1], -x) < 0.0) lo = mid + 1;
         else hi = mid;
     }
     return lo;
@@ -83,7 +95,7 @@ __device__ __forceinline__ int count_bsearch(const double *ad, int G, double h, 
 // value E, so for G <= 4096 the only candidate whose side of the boundary is
 // not fixed by E lies within 0.002 of E, and the exact count n satisfies
 // n0 - 1 <= n <= n0 + 1.  Hence n = n0 - 1 + [a_{n0-1} below] + [a_{n0} below]
-// (ad[n0] and ad[n0 + 1]; the sentinels cover n0 = 0 and n0 = G).  The sign
+// (af[n0] and af[n0 + 1]; the sentinels cover n0 = 0 and n0 = G).  The sign
 // of fma(h, a, -x) is exact: h a is exact in fp64 and the fma rounds once.
 __device__ __forceinline__ int count_linear(const float *af, int G, double h, double x, float est)
 {
@@ -131,7 +143,7 @@ __device__ __forceinline__ void bin_levels(const double (&r)[EPT], const HistSha
                     const float base = kKeep ? Bk[kKeep ? u : 0] : (float)x * gm;
                     nb[v] = count_linear(S.af, G, h, x, base * rh);
                 } else {
-                    nb[v] = count_bsearch(S.ad, G, h, x);
+                    nb[v] = count_bsearch(S.af, G, h, x);
                 }
             }
 #pragma unroll
@@ -167,7 +179,7 @@ __device__ __forceinline__ void bin_levels_elem(double x, const HistShared &S, i
         const double h = (double)kk + 0.5;
         int nb;
         if constexpr (kLinear) nb = count_linear(S.af, G, h, x, base * __builtin_amdgcn_rcpf((float)h));
-        else nb = count_bsearch(S.ad, G, h, x);
+        else nb = count_bsearch(S.af, G, h, x);
         if (nb == 0) break;   // higher levels have higher boundaries
         const int inc = 2 * kk + 1;
         if (nb == G) {
@@ -235,7 +247,7 @@ __device__ __forceinline__ void bin_lattice_elem(double x, const HistShared &S, 
                 if (q < 1) break;
                 if (q * o != Ni || q > G) continue;
                 const int g = q - 1;
-                if (fma((double)kk + 0.5, S.ad[g + 1], -x) < 0.0) {
+                if (fma((double)kk + 0.5, (double)S.af[g + 1], -x) < 0.0) {
                     atomicAdd((unsigned long long *)&S.ha[g], X);
                     atomicAdd(&S.hb[g], o);
                 }
@@ -308,10 +320,19 @@ __device__ __forceinline__ void block_suffix_sums(unsigned long long *h, int n,
     __syncthreads();
 }
 
-// at most 128 VGPRs (four wavefronts per SIMD) unless the residual alone
-// needs more; a workgroup of 1024 threads needs four per SIMD
-template <int T, int EPT, bool kGlobal>
-constexpr int hist_waves_per_simd() { return (EPT >= 32 && !kGlobal && T <= 512) ? 2 : 4; }
+// Wavefronts per SIMD the register budget aims at.  The search is VALU
+// bound, so more wavefronts hide its LDS and barrier waits: seven (72 VGPRs)
+// for two elements per thread or fewer and six (80) for four, in the
+// per-level modes; four (128) for the lattice mode and longer residuals,
+// unless the residual alone needs more (EPT = 32: two); a workgroup of 1024
+// threads needs four per SIMD.
+template <int T, int EPT, bool kLat, bool kGlobal>
+constexpr int hist_waves_per_simd()
+{
+    if (EPT >= 32 && !kGlobal && T <= 512) return 2;
+    if (kLat || kGlobal || EPT > 4) return 4;
+    return EPT == 4 ? 6 : 7;
+}
 
 // kGlobal: the residual is not held in registers; each phase rebuilds
 // element j as fl64 w_j - sum_{p<i} a_p q_pj from the weights, the codes this
@@ -320,7 +341,7 @@ constexpr int hist_waves_per_simd() { return (EPT >= 32 && !kGlobal && T <= 512)
 // value), for channels longer than the registers of a workgroup hold.
 template <int T, int EPT, bool kLinear, bool kLat, bool kGlobal>
 __global__ void __launch_bounds__(T)
-__attribute__((amdgpu_waves_per_eu(hist_waves_per_simd<T, EPT, kGlobal>())))
+__attribute__((amdgpu_waves_per_eu(hist_waves_per_simd<T, EPT, kLat, kGlobal>())))
 fit_hist_kernel(const HistBatch B)
 {
     constexpr int kWaves = T / kWave;
@@ -343,15 +364,11 @@ fit_hist_kernel(const HistBatch B)
 
     const int G = B.G;
     HistShared S;
-    S.e = hsmem;
-    S.bnd = S.e + G;
-    S.ha = (long long *)(S.bnd + G);
-    S.ad = (double *)(S.ha + G);
-    S.lat = (unsigned long long *)(S.ad + G + 2);
+    S.ha = (long long *)hsmem;
+    S.lat = (unsigned long long *)(S.ha + G);
     const int nlat = kLat ? B.nlat : 0;
     S.af = (float *)(S.lat + nlat);
-    S.c = S.af + G + 2;
-    S.hb = (int *)(S.c + G);
+    S.hb = (int *)(S.af + G + 2);
 
     const int64_t k = (int64_t)blockIdx.x - Ly.c_begin;
     const int t = threadIdx.x;
@@ -472,11 +489,15 @@ fit_hist_kernel(const HistBatch B)
         for (int u = 0; u < EPT; ++u) r[u] = rebuild(u, s0);
     }
 
-    // the default multipliers fl32((g + 1) / G): the correctly rounded fp32
-    // quotient of the two integers, which equals fl32 of the fp64 one for
-    // every g < G <= 4096 (checked exhaustively on the host)
-    for (int g = t; g < G; g += T)
-        S.c[g] = B.grid ? B.grid[g] : __fdiv_rn((float)(g + 1), (float)G);
+    // the grid multiplier c_g: the caller's, or the default fl32((g + 1) / G),
+    // the correctly rounded fp32 quotient of the two integers (which equals
+    // fl32 of the fp64 one for every g < G <= 4096, checked exhaustively on
+    // the host); for G = 2^k that is (g + 1) 2^-k exactly
+    const bool pow2 = (G & (G - 1)) == 0;
+    const float invG = __fdiv_rn(1.0f, (float)G);
+    auto mult = [&](int g) {
+        return B.grid ? B.grid[g] : pow2 ? (float)(g + 1) * invG : __fdiv_rn((float)(g + 1), (float)G);
+    };
 
     float apend = 0.0f;
     int n = 0;
@@ -586,8 +607,8 @@ fit_hist_kernel(const HistBatch B)
                 lsum = fma(ru, ru, lsum);
             }
         }
-        // also orders S.c before use; no trailing barrier: the scratch is next
-        // written after the setup barrier below
+        // no trailing barrier: the scratch is next written after the setup
+        // barrier below
         block_max_sum<T, false>(lmax, lsum, s_redf, s_redd);
         const float m = lmax;
         const double Er = lsum;
@@ -648,8 +669,7 @@ fit_hist_kernel(const HistBatch B)
 
         // ---- candidates, cleared histograms
         for (int g = t; g < G; g += T) {
-            const float a = (float)((double)m * (double)S.c[g] / Md);
-            S.ad[g + 1] = (double)a;
+            const float a = (float)((double)m * (double)mult(g) / Md);
             S.af[g + 1] = a;
             S.ha[g] = 0;
             S.hb[g] = 0;
@@ -660,8 +680,6 @@ fit_hist_kernel(const HistBatch B)
             for (int b = t; b < nlat; b += T) S.lat[b] = 0;
         if (t == 0) {
             s_other = 0;
-            S.ad[0] = 0.0;
-            S.ad[G + 1] = INFINITY;
             S.af[0] = 0.0f;
             S.af[G + 1] = INFINITY;
         }
@@ -676,6 +694,8 @@ fit_hist_kernel(const HistBatch B)
 
         const double q2 = ldexp(1.0, -sh);
         const double slack = Md * (double)d * q2;   // fixed-point error of A, per unit a
+        int be = 0;                                  // ||r||^2 < 2^be: the unit of stored bounds
+        (void)frexp(Er, &be);
         ArgMin best{INFINITY, 0x7fffffff};
         if (lat) {
             // ---- lattice buckets, their suffix sums, then every candidate
@@ -711,7 +731,7 @@ fit_hist_kernel(const HistBatch B)
                         }
                     }
                 }
-                const double a = S.ad[g + 1];
+                const double a = (double)S.af[g + 1];
                 double e = INFINITY, b = 0.0;
                 if (a != 0.0) {
                     const double Ad = ldexp((double)A, -sh);
@@ -719,19 +739,18 @@ fit_hist_kernel(const HistBatch B)
                     e = (Er - t2) + t3;
                     b = a * slack + 8.0 * 0x1p-53 * (Er + t2 + t3);
                 }
-                S.e[g] = e;
-                S.bnd[g] = b;
+                S.put_err(g, e, b, be);
                 if (e < best.e || (e == best.e && g < best.g)) best = ArgMin{e, g};
             }
-            // its barrier publishes S.e, S.bnd; s_arg is next written a step later
+            // its barrier publishes the errors and bounds; s_arg is next written a step later
             best = block_argmin<T, false>(best, s_arg);
             // another candidate whose interval reaches the best one's (rare)
             // is flagged by its own thread, so that in the common case no
             // wavefront scans the candidates again
-            const double thr0 = best.e == INFINITY ? INFINITY : best.e + S.bnd[best.g];
+            const double thr0 = best.e == INFINITY ? INFINITY : best.e + S.bnd(best.g, be);
             bool other = false;
             for (int g = t; g < G; g += T)
-                other = other || (g != best.g && S.e[g] != INFINITY && S.e[g] - S.bnd[g] <= thr0);
+                other = other || (g != best.g && S.err(g) != INFINITY && S.err(g) - S.bnd(g, be) <= thr0);
             if (other) s_other = 1;
             __syncthreads();
         } else {
@@ -784,7 +803,7 @@ fit_hist_kernel(const HistBatch B)
             for (int g = g1 - 1; g >= g0; --g) {
                 A += S.ha[g];
                 B += S.hb[g];
-                const double a = S.ad[g + 1];
+                const double a = (double)S.af[g + 1];
                 double e = INFINITY, b = 0.0;
                 if (a != 0.0) {
                     const double Ad = ldexp((double)A, -sh);
@@ -792,17 +811,16 @@ fit_hist_kernel(const HistBatch B)
                     e = (Er - t2) + t3;
                     b = a * slack + 8.0 * 0x1p-53 * (Er + t2 + t3);
                 }
-                S.e[g] = e;
-                S.bnd[g] = b;
+                S.put_err(g, e, b, be);
                 if (e < best.e || (e == best.e && g < best.g)) best = ArgMin{e, g};
             }
             best = wave_argmin(best);
             }
             // finalists: candidates whose interval reaches the best one's
-            const double thr = best.e == INFINITY ? INFINITY : best.e + S.bnd[best.g];
+            const double thr = best.e == INFINITY ? INFINITY : best.e + S.bnd(best.g, be);
             int cnt = 0;
             for (int g = g0; g < g1; ++g)
-                if (S.e[g] != INFINITY && S.e[g] - S.bnd[g] <= thr) ++cnt;
+                if (S.err(g) != INFINITY && S.err(g) - S.bnd(g, be) <= thr) ++cnt;
             cnt = wave_reduce(cnt, SumOp());
             if (t == 0) {
                 s_gbest = best.e == INFINITY ? -1 : best.g;
@@ -816,8 +834,8 @@ fit_hist_kernel(const HistBatch B)
                 for (; nf < kMaxFinalists && nf < cnt; ++nf) {
                     ArgMin c{INFINITY, 0x7fffffff};
                     for (int g = g0; g < g1; ++g) {
-                        const double e = S.e[g];
-                        if (e == INFINITY || e - S.bnd[g] > thr) continue;
+                        const double e = S.err(g);
+                        if (e == INFINITY || e - S.bnd(g, be) > thr) continue;
                         const bool after = e > last_e || (e == last_e && g > last_g);
                         if (after && (e < c.e || (e == c.e && g < c.g))) c = ArgMin{e, g};
                     }
@@ -838,7 +856,7 @@ fit_hist_kernel(const HistBatch B)
             ArgMin best{INFINITY, 0x7fffffff};
             for (int f = 0; f < nfin; ++f) {
                 const int g = s_fin[f];
-                const double a = S.ad[g + 1];
+                const double a = (double)S.af[g + 1];
                 double le = 0.0;
                 // signed form: (r - a q)^2 with q = clip(rne(r / a)) equals
                 // (|r| - a |q|)^2, and keeps |r| from being hoisted per element
@@ -868,12 +886,12 @@ fit_hist_kernel(const HistBatch B)
             n = i;
             break;
         }
-        apend = (float)S.ad[gstar + 1];
+        apend = S.af[gstar + 1];
         if (t == 0) {
             Ly.scales[k * P + i] = apend;
             s_scale[i] = apend;
         }
-        // the next step rewrites S.ad only after its first barrier; this one
+        // the next step rewrites S.af only after its first barrier; this one
         // is needed when the finalists' reductions used s_redd, which the next
         // step's first reduction writes, or when the rebuilt residual reads
         // s_scale[i]
@@ -958,8 +976,7 @@ constexpr int kLatMinDim = 1024;
 
 size_t fit_hist_lds(int G)
 {
-    return (size_t)G * (3 * sizeof(double) + sizeof(long long) + 2 * sizeof(float) + sizeof(int)) +
-           2 * sizeof(double) + 2 * sizeof(float);
+    return (size_t)G * (sizeof(long long) + 2 * sizeof(float)) + 2 * sizeof(float);
 }
 
 bool fit_hist_supports(int64_t d) { return d >= 1 && d <= kHistMaxDim; }
