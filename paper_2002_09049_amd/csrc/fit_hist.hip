@@ -90,18 +90,23 @@ __device__ __forceinline__ int count_bsearch(const float *af, int G, double h, d
 }
 
 // The same count for the default grid a_g = fl32(m fl32((g+1)/G) / M), from
-// n0 = floor(min(est, G)) with est = fl32 of x G M / (h m).  a_g is within
-// relative 2^-23 of m (g+1) / (G M) and est within a few 2^-24 of its exact
-// value E, so for G <= 4096 the only candidate whose side of the boundary is
-// not fixed by E lies within 0.002 of E, and the exact count n satisfies
-// n0 - 1 <= n <= n0 + 1.  Hence n = n0 - 1 + [a_{n0-1} below] + [a_{n0} below]
-// (af[n0] and af[n0 + 1]; the sentinels cover n0 = 0 and n0 = G).  The sign
-// of fma(h, a, -x) is exact: h a is exact in fp64 and the fma rounds once.
+// est = fl32 of x G M / (h m), computed as fl32(fl32(fl32(x) fl32(G M / m))
+// rcp(h)): within relative 6 2^-24 of E = x G M / (h m) (five roundings and
+// the reciprocal's one ulp), so within 0.0015 of E while est <= G + 1.  The
+// boundary test (k + 1/2) a_g < x reads (g + 1)(1 + delta) < E with |delta|
+// <= 2^-23 (the roundings of c_g and a_g), within 0.0005 of (g + 1) < E for
+// G <= 4096.  So unless an integer N in [1, G] lies within 0.003 of est, the
+// count is min(floor(est), G) with no table read; otherwise only candidate
+// N - 1 is undecided and one exact comparison settles it (h a is exact in
+// fp64 and the fma rounds once, so its sign is exact; af[N] = a_{N-1}).
 __device__ __forceinline__ int count_linear(const float *af, int G, double h, double x, float est)
 {
-    const int n0 = (int)fminf(est, (float)G);
-    const double lo = (double)af[n0], hi = (double)af[n0 + 1];
-    return n0 - 1 + (fma(h, lo, -x) < 0.0 ? 1 : 0) + (fma(h, hi, -x) < 0.0 ? 1 : 0);
+    const float Nf = rintf(est);
+    const int N = (int)Nf;
+    int n = min((int)est, G);
+    if (fabsf(est - Nf) <= 0.003f && N >= 1 && N <= G)
+        n = N - 1 + (fma(h, (double)af[N], -x) < 0.0 ? 1 : 0);
+    return n;
 }
 
 // Histogram of the level boundaries of this thread's elements.  Level-major:
@@ -323,13 +328,15 @@ __device__ __forceinline__ void block_suffix_sums(unsigned long long *h, int n,
 // Wavefronts per SIMD the register budget aims at.  The search is VALU
 // bound, so more wavefronts hide its LDS and barrier waits: seven (72 VGPRs)
 // for two elements per thread or fewer and six (80) for four, in the
-// per-level modes; four (128) for the lattice mode and longer residuals,
-// unless the residual alone needs more (EPT = 32: two); a workgroup of 1024
-// threads needs four per SIMD.
+// per-level modes; five (96) for the 256-thread lattice variants of up to
+// eight elements; four (128) for the others, unless the residual alone
+// needs more (EPT = 32: two); a workgroup of 1024 threads needs four per
+// SIMD.
 template <int T, int EPT, bool kLat, bool kGlobal>
 constexpr int hist_waves_per_simd()
 {
     if (EPT >= 32 && !kGlobal && T <= 512) return 2;
+    if (kLat && !kGlobal && T <= 256 && EPT <= 8) return 5;
     if (kLat || kGlobal || EPT > 4) return 4;
     return EPT == 4 ? 6 : 7;
 }
