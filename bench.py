@@ -264,6 +264,11 @@ def summarize_counters(dirs, workload, steps=3):
             f["valu_iops_tops"] = avg.get("SQ_INSTS_VALU_IOPS", 0.0) / us / 1e6
         if "SQ_VALU_MFMA_BUSY_CYCLES" in avg and avg.get("SQ_BUSY_CU_CYCLES", 0) > 0:
             f["mfma_busy_per_cu_busy"] = avg["SQ_VALU_MFMA_BUSY_CYCLES"] / (4 * avg["SQ_BUSY_CU_CYCLES"])
+        if "SQ_ACTIVE_INST_VALU" in avg and avg.get("SQ_BUSY_CU_CYCLES", 0) > 0:
+            # each VALU wave-instruction holds its SIMD's VALU for 4 cycles
+            # (SQ_ACTIVE_INST_VALU counts them in those 4-cycle units) and a
+            # CU has 4 SIMDs: the SIMDs' VALU issue share of the busy cycles
+            f["valu_busy_per_cu_busy"] = avg["SQ_ACTIVE_INST_VALU"] / avg["SQ_BUSY_CU_CYCLES"]
         f["counters"] = {c: round(v, 1) for c, v in sorted(avg.items())}
         out[k] = f
 
@@ -285,17 +290,20 @@ def summarize_counters(dirs, workload, steps=3):
              f"the FLOP counters by {CAL_MULS} fp64 and fp32 multiplies (torch) of the same run "
              f"(x {scale.get('SQ_INSTS_VALU_FLOPS_FP64', float('nan')):.4f} fp64, "
              f"x {scale.get('SQ_INSTS_VALU_FLOPS_FP32', float('nan')):.4f} fp32).",
-             "VALU-active and wait shares are SQ_ACTIVE_INST_VALU and SQ_WAIT_ANY over SQ_WAVE_CYCLES;",
+             "VALU-active and wait shares are SQ_ACTIVE_INST_VALU and SQ_WAIT_ANY over SQ_WAVE_CYCLES",
+             "(per wave); SIMD VALU busy is SQ_ACTIVE_INST_VALU (in 4-cycle issue units) over",
+             "SQ_BUSY_CU_CYCLES (4 SIMDs per CU): the share of the SIMDs' VALU issue capacity used;",
              "FLOP rates are SQ_INSTS_VALU_FLOPS_FP32 (+ _TRANS) and _FP64 over the dispatch's duration,",
              f"against {PEAK_VALU_F32_TFLOPS} (FP32) and {PEAK_VALU_F64_TFLOPS} (FP64) TFLOP/s.", "",
-             "| kernel | launches/step | us | HBM MB | HBM GB/s | VALU active | wait | FP32 TFLOP/s (frac) | FP64 TFLOP/s (frac) | INT TOP/s | MFMA busy |",
-             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+             "| kernel | launches/step | us | HBM MB | HBM GB/s | SIMD VALU busy | VALU active | wait | FP32 TFLOP/s (frac) | FP64 TFLOP/s (frac) | INT TOP/s | MFMA busy |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
     for k in sorted(out, key=lambda k: -out[k]["avg_us_serialized"] * out[k]["launches_per_step"]):
         f = out[k]
         hb = f.get("hbm_bytes")
         lines.append(
             f"| `{k}` | {f['launches_per_step']:g} | {f['avg_us_serialized']:.1f} | "
             f"{fmt(None if hb is None else hb / 1e6, '.1f')} | {fmt(f.get('hbm_gbs'), '.0f')} | "
+            f"{fmt(f.get('valu_busy_per_cu_busy'), '.1%')} | "
             f"{fmt(f.get('valu_active_share'), '.1%')} | {fmt(f.get('wait_any_share'), '.1%')} | "
             + ("" if "valu_fp32_tflops" not in f else
                f"{f['valu_fp32_tflops']:.2f} ({f['valu_fp32_frac']:.1%}) | "
@@ -561,7 +569,8 @@ def main():
             c = (counters or {}).get(name)
             if c:
                 k["counters"] = {kk: c[kk] for kk in (
-                    "hbm_bytes", "avg_us_serialized", "valu_active_share", "wait_any_share",
+                    "hbm_bytes", "avg_us_serialized", "valu_busy_per_cu_busy", "valu_active_share",
+                    "wait_any_share",
                     "valu_fp32_tflops", "valu_fp32_frac", "valu_fp64_tflops", "valu_fp64_frac",
                     "valu_iops_tops", "mfma_busy_per_cu_busy") if kk in c}
             kernels[name] = k

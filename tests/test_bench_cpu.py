@@ -69,7 +69,9 @@ def test_counter_summary_arithmetic(tmp_path, capsys):
                  (1, fit, 512, "SQ_WAIT_ANY", 500.0, 0, 100000),
                  (2, fit, 512, "SQ_WAVE_CYCLES", 3000.0, 0, 300000),
                  (2, fit, 512, "SQ_ACTIVE_INST_VALU", 750.0, 0, 300000),
-                 (2, fit, 512, "SQ_WAIT_ANY", 1500.0, 0, 300000)])
+                 (2, fit, 512, "SQ_WAIT_ANY", 1500.0, 0, 300000),
+                 (1, fit, 512, "SQ_BUSY_CU_CYCLES", 400.0, 0, 100000),
+                 (2, fit, 512, "SQ_BUSY_CU_CYCLES", 1600.0, 0, 300000)])
     # pass b: FLOP counts (1e9 FP32, 2e9 FP64 FLOP per dispatch)
     _pmc_csv(b, [(1, fit, 512, "SQ_INSTS_VALU_FLOPS_FP32", 1e9, 0, 200000),
                  (1, fit, 512, "SQ_INSTS_VALU_FLOPS_FP64", 2e9, 0, 200000)])
@@ -85,6 +87,8 @@ def test_counter_summary_arithmetic(tmp_path, capsys):
     blob = json.loads(next(l for l in out.splitlines() if l.startswith("counters-json: "))[15:])
     f = blob["fit_hist_kernel<512,9,lattice>"]
     assert abs(f["valu_active_share"] - 0.25) < 1e-12 and abs(f["wait_any_share"] - 0.5) < 1e-12
+    # SIMD VALU busy: mean SQ_ACTIVE_INST_VALU (500) over mean SQ_BUSY_CU_CYCLES (1000)
+    assert abs(f["valu_busy_per_cu_busy"] - 0.5) < 1e-12
     # 1e9 FLOP over the pass-b dispatch's 200 us = 5 TFLOP/s
     assert abs(f["valu_fp32_tflops"] - 5.0) < 1e-9 and abs(f["valu_fp64_tflops"] - 10.0) < 1e-9
     g = blob["gemm_err_kernel"]
