@@ -644,8 +644,23 @@ int reconstruct_impl(const mpq_layer *layers, int n_layers, int max_points, void
     return MPQ_OK;
 }
 
-int quantize_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
-                  const float *grid_host, int n_grid, float tol, void *stream)
+// The launches of one whole-path step (mpq_quantize_layers), planned from
+// the layers: the fit jobs, the output error's items and launch groups, and
+// the reconstruction.
+struct QuantizeStep {
+    std::vector<FitJob> jobs;
+    std::vector<mpq::ErrLayerIn> err;
+    std::vector<mpq::RecLayer> rec;
+    std::vector<int> err_of;   // by layer: its err item, or -1
+    ErrJobs ej;
+    double rec_bytes = 0.0;
+    int n_grid = 0, max_points = 0;
+};
+
+// The checks of mpq_quantize_layers, before any HIP call but the device
+// queries of fit_checks.  any: a layer with channels.
+int quantize_checks(const mpq_layer *layers, int n_layers, int bits, int max_points,
+                    const float *grid_host, int n_grid, float tol, bool *any, bool *hist_fits)
 {
     if (n_layers < 0 || (n_layers > 0 && !layers))
         return fail(MPQ_ERR_INVALID_ARG, "layers must hold n_layers >= 0 entries");
@@ -658,91 +673,113 @@ int quantize_impl(const mpq_layer *layers, int n_layers, int bits, int max_point
         if (rc == MPQ_OK && L.W_hat) rc = check_error_layer(L, max_points, false);
         if (rc != MPQ_OK) return n_layers > 1 ? fail(rc, "layer %d: %s", l, g_last_error.c_str()) : rc;
     }
+    return fit_checks(Search::kAuto, layers, n_layers, bits, max_points, grid_host, n_grid, tol, any,
+                      hist_fits);
+}
+
+// The step's launches (no HIP call): the fit jobs on the device grid dgrid
+// (NULL: the default grid), the output error of every layer that asks for it
+// (a group's GEMM fills the device only with many layers' tiles) and the
+// reconstruction (both only read the fit's outputs).
+void quantize_build(const mpq_layer *layers, int n_layers, int bits, int max_points, const float *dgrid,
+                    int n_grid, float tol, bool hist_fits, QuantizeStep *q)
+{
+    const int M = (1 << (bits - 1)) - 1;
+    q->n_grid = n_grid;
+    q->max_points = max_points;
+    q->jobs = build_fit_jobs(Search::kAuto, hist_fits, layers, n_layers, M, max_points, dgrid, n_grid,
+                             tol, -1.0);
+    q->err_of.assign(n_layers, -1);
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_layer &L = layers[l];
+        if (L.c_out == 0) continue;
+        if (L.out_err) {
+            q->err_of[l] = (int)q->err.size();
+            q->err.push_back(mpq::ErrLayerIn{L.W, L.codes, L.scales, L.counts, L.X, L.out_err, L.out_ref,
+                                             L.c_out, L.d, L.n});
+        }
+        if (L.W_hat) {
+            q->rec.push_back(mpq::RecLayer{L.codes, L.scales, L.counts, L.W_hat, L.c_out, L.d, nullptr});
+            q->rec_bytes += 5.0 * (double)L.c_out * (double)L.d;
+        }
+    }
+}
+
+// Once the output error's scratch is placed (q->ej): a fit that keeps its
+// residual in registers writes its layers' rows of D for the output error,
+// which then forms none for them.
+void quantize_link_d(QuantizeStep *q)
+{
+    if (q->err.empty()) return;
+    std::vector<int64_t> d_off(q->err.size());
+    std::vector<int> d_grp(q->err.size());
+    mpq::err_item_d_offsets(q->err.data(), (int)q->err.size(), d_off.data(), d_grp.data());
+    for (FitJob &j : q->jobs) {
+        if (j.dense || !mpq::hist_variant_writes_d(j.variant)) continue;
+        for (int i = 0; i < j.b.n_layers; ++i) {
+            const int e = q->err_of[j.layers[i]];
+            if (e < 0 || d_off[e] < 0) continue;
+            j.b.L[i].dres = (float *)(q->ej.scratch + q->ej.off[d_grp[e]] + d_off[e]);
+            q->err[e].d_ready = 1;
+        }
+    }
+}
+
+// Enqueues the step on s: (1) every fit, side by side (as mpq_fit_layers),
+// and beside them the upload of the output error's descriptor tables, which
+// reads nothing the fits write (so the GEMM starts as soon as the last fit
+// ends); (2) the output error's launch groups and, beside them, one
+// reconstruction of every layer (it reads only the fit's outputs and is
+// bound by HBM, the GEMM by MFMA).
+hipError_t quantize_enqueue(QuantizeStep &q, hipStream_t s)
+{
+    std::vector<double> work;
+    for (const FitJob &j : q.jobs) work.push_back(j.work);
+    const int n_fit_jobs = (int)work.size();
+    const int n_groups = (int)q.ej.work.size();
+    if (n_groups > 0) work.push_back(0.0);
+    hipError_t e = run_concurrently(s, work, [&](int i, hipStream_t st) {
+        if (i < n_fit_jobs) return launch_fit_job(q.jobs[i], q.n_grid, st);
+        hipError_t e1 = hipSuccess;
+        for (int g = 0; g < n_groups && e1 == hipSuccess; ++g)
+            e1 = launch_err_job(q.err, q.ej, g, q.max_points, st, mpq::kErrUpload);
+        return e1;
+    });
+    if (e != hipSuccess) return e;
+    // work in GEMM FLOP and, for the reconstruction, bytes (at ~2 TB/s
+    // against ~100 TFLOP/s: x 50)
+    std::vector<double> w2 = q.ej.work;
+    const int n_err_jobs = (int)w2.size();
+    if (!q.rec.empty()) w2.push_back(q.rec_bytes * 50.0);
+    return run_concurrently(s, w2, [&](int i, hipStream_t st) {
+        return i < n_err_jobs ? launch_err_job(q.err, q.ej, i, q.max_points, st, mpq::kErrKernels)
+                              : mpq::launch_reconstruct(q.rec.data(), (int)q.rec.size(), q.max_points, st);
+    });
+}
+
+int quantize_impl(const mpq_layer *layers, int n_layers, int bits, int max_points,
+                  const float *grid_host, int n_grid, float tol, void *stream)
+{
     bool any = false, hist_fits = false;
-    rc = fit_checks(Search::kAuto, layers, n_layers, bits, max_points, grid_host, n_grid, tol, &any,
-                    &hist_fits);
+    int rc = quantize_checks(layers, n_layers, bits, max_points, grid_host, n_grid, tol, &any, &hist_fits);
     if (rc != MPQ_OK || !any) return rc;
     hipStream_t s = (hipStream_t)stream;
     float *dgrid = nullptr;
     rc = upload_grid(grid_host, n_grid, s, &dgrid);
     if (rc != MPQ_OK) return rc;
-    const int M = (1 << (bits - 1)) - 1;
-    std::vector<FitJob> jobs = build_fit_jobs(Search::kAuto, hist_fits, layers, n_layers, M,
-                                              max_points, dgrid, n_grid, tol, -1.0);
-    // the output error of every layer that asks for it, in its launch groups
-    // (a group's GEMM fills the device only with many layers' tiles), and the
-    // reconstruction: both only read the fit's outputs
-    std::vector<mpq::ErrLayerIn> err;
-    std::vector<mpq::RecLayer> rec;
-    std::vector<int> err_of(n_layers, -1);
-    double bytes = 0.0;
-    for (int l = 0; l < n_layers; ++l) {
-        const mpq_layer &L = layers[l];
-        if (L.c_out == 0) continue;
-        if (L.out_err) {
-            err_of[l] = (int)err.size();
-            err.push_back(mpq::ErrLayerIn{L.W, L.codes, L.scales, L.counts, L.X, L.out_err, L.out_ref,
-                                          L.c_out, L.d, L.n});
-        }
-        if (L.W_hat) {
-            rec.push_back(mpq::RecLayer{L.codes, L.scales, L.counts, L.W_hat, L.c_out, L.d, nullptr});
-            bytes += 5.0 * (double)L.c_out * (double)L.d;
-        }
-    }
-    ErrJobs ej;
-    if (!err.empty()) {
-        rc = err_jobs(err, s, &ej);
+    QuantizeStep q;
+    quantize_build(layers, n_layers, bits, max_points, dgrid, n_grid, tol, hist_fits, &q);
+    if (!q.err.empty()) {
+        rc = err_jobs(q.err, s, &q.ej);
         if (rc != MPQ_OK) {
             if (dgrid) (void)mpq::scratch_free(dgrid, s);
             return rc;
         }
     }
-    // a fit that keeps its residual in registers writes its layers' rows of
-    // D for the output error, which then forms none for them
-    std::vector<int64_t> d_off(err.size());
-    std::vector<int> d_grp(err.size());
-    if (!err.empty()) mpq::err_item_d_offsets(err.data(), (int)err.size(), d_off.data(), d_grp.data());
-    for (FitJob &j : jobs) {
-        if (j.dense || !mpq::hist_variant_writes_d(j.variant)) continue;
-        for (int i = 0; i < j.b.n_layers; ++i) {
-            const int l = j.layers[i];
-            if (err_of[l] < 0 || d_off[err_of[l]] < 0) continue;
-            j.b.L[i].dres = (float *)(ej.scratch + ej.off[d_grp[err_of[l]]] + d_off[err_of[l]]);
-            err[err_of[l]].d_ready = 1;
-        }
-    }
-    // The reconstruction of every layer: one launch beside the output error
-    // (it reads only the fit's outputs and is bound by HBM, the GEMM by MFMA).
-    // 1. every fit, side by side (as mpq_fit_layers), and beside them the
-    // upload of the output error's descriptor tables, which reads nothing
-    // the fits write (so the GEMM starts as soon as the last fit ends)
-    std::vector<double> work;
-    for (const FitJob &j : jobs) work.push_back(j.work);
-    const int n_fit_jobs = (int)work.size();
-    const int n_groups = (int)ej.work.size();
-    if (n_groups > 0) work.push_back(0.0);
-    hipError_t e = run_concurrently(s, work, [&](int i, hipStream_t st) {
-        if (i < n_fit_jobs) return launch_fit_job(jobs[i], n_grid, st);
-        hipError_t e1 = hipSuccess;
-        for (int g = 0; g < n_groups && e1 == hipSuccess; ++g)
-            e1 = launch_err_job(err, ej, g, max_points, st, mpq::kErrUpload);
-        return e1;
-    });
+    quantize_link_d(&q);
+    const hipError_t e = quantize_enqueue(q, s);
     if (dgrid) (void)mpq::scratch_free(dgrid, s);
-    if (e != hipSuccess) {
-        if (ej.scratch) (void)mpq::scratch_free(ej.scratch, s);
-        return hip_fail(e, "fit kernel launch");
-    }
-    // 2. the output error's launch groups (work in GEMM FLOP) and the
-    // reconstruction (bytes, at ~2 TB/s against ~100 TFLOP/s: x 50), side by side
-    std::vector<double> w2 = ej.work;
-    const int n_err_jobs = (int)w2.size();
-    if (!rec.empty()) w2.push_back(bytes * 50.0);
-    e = run_concurrently(s, w2, [&](int i, hipStream_t st) {
-        return i < n_err_jobs ? launch_err_job(err, ej, i, max_points, st, mpq::kErrKernels)
-                              : mpq::launch_reconstruct(rec.data(), (int)rec.size(), max_points, st);
-    });
-    if (ej.scratch) (void)mpq::scratch_free(ej.scratch, s);
+    if (q.ej.scratch) (void)mpq::scratch_free(q.ej.scratch, s);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     return MPQ_OK;
 }
