@@ -808,6 +808,10 @@ def _oracle_rate(orc, wk, stride, threads, calib=False):
     return pts, secs
 
 
+def _every(st):
+    return "every channel" if st == 1 else f"every {st}th channel"
+
+
 def cpu_baseline(wk, stride, calib=False):
     """The fp64 oracle, as it stands, on every stride-th channel of every layer
     (calib: its fit with Algorithm 2's rule on the layer's batch), on all the
@@ -822,11 +826,11 @@ def cpu_baseline(wk, stride, calib=False):
     for name, st in (("conv64x576", 1), ("resnet18", 8)):
         p1, s1 = _oracle_rate(orc, wl.get(name), st, 1, calib)
         single[name] = {"value": round(p1 / s1, 2), "unit": "channel-points/s",
-                        "sample": f"every {st}th channel ({p1} channel-points, {s1:.1f} s)"}
+                        "sample": f"{_every(st)} ({p1} channel-points, {s1:.1f} s)"}
     return {"value": round(pts / secs, 2), "unit": "channel-points/s", "cores": cores,
             "kind": "oracle", "cpu_model": cpu_model(),
             "sample": f"{'calibration-rule fit, ' if calib else ''}"
-                      f"every {stride}th channel of each of the {len(wk.layers)} layers of {wk.name} "
+                      f"{_every(stride)} of each of the {len(wk.layers)} layers of {wk.name} "
                       f"({pts} channel-points, {secs:.1f} s wall)",
             "single_thread": single}
 
