@@ -105,6 +105,8 @@ def parse():
                     help="print the per-kernel counter summary of rocprofv3 --pmc runs (one per "
                          "counter pass) of `bench.py --workload W --steps 1 --warmup 1 "
                          "--no-cpu-baseline --copy-calibration` and exit")
+    ap.add_argument("--summarize-benches", nargs="+", metavar="BENCH_JSON",
+                    help="print a markdown table of bench.py lines (one per workload)")
     ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
                     help="print the per-kernel summary of a rocprofv3 --kernel-trace --stats run "
                          "and exit")
@@ -330,6 +332,63 @@ def stored_counters(workload):
     return None
 
 
+def _stride_of(bench):
+    """The CPU-sample stride of a bench line's cpu_baseline (from its sample text)."""
+    sample = (bench.get("cpu_baseline") or {}).get("sample", "")
+    if "every channel" in sample:
+        return 1
+    m = re.search(r"every (\d+)th channel", sample)
+    return int(m.group(1)) if m else "-"
+
+
+def summarize_benches(paths):
+    """Markdown table of bench.py lines: rate, step time, the GEMM's roofline
+    and HBM traffic, the longest fit, the search kernel's SIMD VALU busy
+    share (from its stored counters) and the oracle's rate."""
+    rows = [json.load(open(p)) for p in paths]
+    lines = ["# Bench line per workload (one MI355X, one mpq_quantize_layers call per step)", "",
+             "Commands (from the repository root), per workload W and CPU-sample stride S, then the table:",
+             "", "```", "python3 bench.py --workload W --cpu-stride S > gpurun_out/wl/W.json",
+             "python3 bench.py --summarize-benches " + " ".join(f"gpurun_out/wl/{b['config']['workload']}.json"
+                                                                for b in rows),
+             "```", "",
+             "Strides: " + ", ".join(f"{b['config']['workload']} {_stride_of(b)}" for b in rows)
+             + f"; {rows[0]['steps'] if rows else 0} timed steps after {rows[0]['warmup'] if rows else 0} "
+               "warm-up steps.",
+             "The roofline kernel is the error GEMM (2 C d n FLOP per layer, event-timed in the timed steps);",
+             "the other kernels are timed in the untimed profile step, where the fit launches share the",
+             "device (so a fit's duration includes its neighbours).  `search` is the fit kernel with the",
+             "most time per step; its SIMD VALU busy share (the share of the SIMDs' VALU issue capacity it",
+             "used, SQ_ACTIVE_INST_VALU over SQ_BUSY_CU_CYCLES) and the GEMM's HBM traffic come from the",
+             "stored counter summary `profiles/<workload>_counters.md` of the same sources.", "",
+             "| workload | channel-points/s | ms/step | points/step | GEMM (roofline) | GEMM HBM traffic | "
+             "longest fit | search SIMD VALU busy | oracle (cores) |",
+             "|---|---:|---:|---:|---|---:|---|---:|---:|"]
+    tops = []
+    for b in rows:
+        w = b["config"]["workload"]
+        r = b["roofline"]
+        fits = {k: v for k, v in b["kernels"].items() if v.get("stage") == "fit"}
+        lf = max(fits.items(), key=lambda kv: kv[1]["us_per_step"])
+        cb = b.get("cpu_baseline") or {}
+        srch = b.get("search") or {}
+        vb = (srch.get("counters") or {}).get("valu_busy_per_cu_busy")
+        tr = r.get("traffic")
+        lines.append(
+            f"| {w} | {b['value'] / 1e6:.2f} M | {b['ms_per_step']:.3f} | {b['config']['points_per_step']} | "
+            f"{r['achieved']:.1f} TFLOP/s ({100 * r['frac']:.0f}% of {r['peak']}), {r['avg_launch_us']:.1f} us | "
+            + ("-" if tr is None else f"{tr / 1e6:.0f} MB") + " | "
+            f"`{lf[0]}` {lf[1]['avg_us']:.1f} us | "
+            + ("-" if vb is None else f"{100 * vb:.1f}%") + f" (`{srch.get('kernel')}`) | "
+            f"{cb.get('value', 0) / 1e3:.2f} k ({cb.get('cores')}) |")
+        tops.append((w, sorted(b["kernels"].items(), key=lambda kv: -kv[1]["us_per_step"])[:5]))
+    lines += ["", "Top kernels per workload (microseconds per launch, launches per step):", ""]
+    for w, ks in tops:
+        lines.append(f"- **{w}**: " + "; ".join(f"`{k}` x{v['launches_per_step']:g} {v['avg_us']:.1f}"
+                                                for k, v in ks))
+    print("\n".join(lines))
+
+
 def summarize_trace(trace_dir, bench_json=None, steps=None, rule="tol", workload="resnet50"):
     """Per-kernel average duration of a traced bench run (kernel_stats.csv of
     rocprofv3 --stats), beside the event-timed averages of a bench.py line
@@ -403,6 +462,9 @@ def main():
     args = parse()
     if args.summarize_counters:
         summarize_counters(args.summarize_counters, args.workload, steps=args.traced_steps or 3)
+        return 0
+    if args.summarize_benches:
+        summarize_benches(args.summarize_benches)
         return 0
     if args.summarize_trace:
         summarize_trace(args.summarize_trace, args.bench_json, steps=args.traced_steps,

@@ -95,3 +95,29 @@ def test_counter_summary_arithmetic(tmp_path, capsys):
     assert abs(g["fetch_size_bytes"] - 2 * 1000.0 * 1024) < 1e-6     # the copy read 2x its count
     assert abs(g["write_size_bytes"] - 10.0 * 1024) < 1e-6
     assert "sources: " in out
+
+
+def test_bench_table(tmp_path, capsys):
+    """The workload table reads each bench line's rate, roofline, traffic,
+    longest fit, search counters and CPU sample stride."""
+    import json
+    line = {"value": 2.5e6, "ms_per_step": 1.25, "steps": 20, "warmup": 3,
+            "config": {"workload": "resnet18", "points_per_step": 3125},
+            "roofline": {"achieved": 90.0, "frac": 0.5722, "peak": 157.3, "avg_launch_us": 250.0,
+                         "traffic": 4.36e8},
+            "kernels": {"fit_hist_kernel<512,9,lattice>": {"stage": "fit", "us_per_step": 240.0,
+                                                           "avg_us": 240.0, "launches_per_step": 1.0},
+                        "gemm_err_kernel": {"stage": "output_error", "us_per_step": 250.0,
+                                            "avg_us": 250.0, "launches_per_step": 1.0}},
+            "search": {"kernel": "fit_hist_kernel<512,9,lattice>",
+                       "counters": {"valu_busy_per_cu_busy": 0.503}},
+            "cpu_baseline": {"value": 12360.0, "cores": 16,
+                             "sample": "every 8th channel of each of the 21 layers of resnet18"}}
+    p = tmp_path / "resnet18.json"
+    p.write_text(json.dumps(line))
+    bench.summarize_benches([str(p)])
+    out = capsys.readouterr().out
+    row = next(l for l in out.splitlines() if l.startswith("| resnet18 |"))
+    assert "2.50 M" in row and "1.250" in row and "90.0 TFLOP/s (57% of 157.3)" in row
+    assert "436 MB" in row and "50.3%" in row and "12.36 k (16)" in row
+    assert "resnet18 8;" in out
