@@ -650,7 +650,8 @@ int reconstruct_impl(const mpq_layer *layers, int n_layers, int max_points, void
 struct QuantizeStep {
     std::vector<FitJob> jobs;
     std::vector<mpq::ErrLayerIn> err;
-    std::vector<mpq::RecLayer> rec;
+    std::vector<mpq::RecLayer> rec;                 // reconstructed beside the output error
+    std::vector<std::vector<mpq::RecLayer>> rec_after;   // by fit job: right behind it
     std::vector<int> err_of;   // by layer: its err item, or -1
     ErrJobs ej;
     double rec_bytes = 0.0;
@@ -692,14 +693,40 @@ void quantize_build(const mpq_layer *layers, int n_layers, int bits, int max_poi
     q->err_of.assign(n_layers, -1);
     for (int l = 0; l < n_layers; ++l) {
         const mpq_layer &L = layers[l];
-        if (L.c_out == 0) continue;
-        if (L.out_err) {
-            q->err_of[l] = (int)q->err.size();
-            q->err.push_back(mpq::ErrLayerIn{L.W, L.codes, L.scales, L.counts, L.X, L.out_err, L.out_ref,
-                                             L.c_out, L.d, L.n});
+        if (L.c_out == 0 || !L.out_err) continue;
+        q->err_of[l] = (int)q->err.size();
+        q->err.push_back(mpq::ErrLayerIn{L.W, L.codes, L.scales, L.counts, L.X, L.out_err, L.out_ref,
+                                         L.c_out, L.d, L.n});
+    }
+    // The reconstruction (bound by HBM) of a fit launch's layers runs right
+    // behind that launch, beside the other fits (bound by VALU), when the
+    // launch holds at least kRecBehind weights and is not the longest one;
+    // the rest runs in one launch beside the output error (bound by MFMA).
+    // Small launches stay in that one launch: a launch costs host time that
+    // the shorter steps (MobileNetV2's) cannot hide.
+    constexpr double kRecBehind = 2e6;
+    int longest = -1;
+    for (int i = 0; i < (int)q->jobs.size(); ++i)
+        if (longest < 0 || q->jobs[i].work > q->jobs[longest].work) longest = i;
+    q->rec_after.assign(q->jobs.size(), {});
+    std::vector<int> job_of(n_layers, -1);
+    for (int i = 0; i < (int)q->jobs.size(); ++i) {
+        double w = 0.0;
+        for (int l : q->jobs[i].layers) {
+            job_of[l] = i;
+            if (layers[l].W_hat) w += (double)layers[l].c_out * (double)layers[l].d;
         }
-        if (L.W_hat) {
-            q->rec.push_back(mpq::RecLayer{L.codes, L.scales, L.counts, L.W_hat, L.c_out, L.d, nullptr});
+        if (i == longest || w < kRecBehind) continue;
+        for (int l : q->jobs[i].layers) job_of[l] = -2 - i;   // behind job i
+    }
+    for (int l = 0; l < n_layers; ++l) {
+        const mpq_layer &L = layers[l];
+        if (L.c_out == 0 || !L.W_hat) continue;
+        const mpq::RecLayer R{L.codes, L.scales, L.counts, L.W_hat, L.c_out, L.d, nullptr};
+        if (job_of[l] <= -2) {
+            q->rec_after[-2 - job_of[l]].push_back(R);
+        } else {
+            q->rec.push_back(R);
             q->rec_bytes += 5.0 * (double)L.c_out * (double)L.d;
         }
     }
@@ -726,11 +753,12 @@ void quantize_link_d(QuantizeStep *q)
 }
 
 // Enqueues the step on s: (1) every fit, side by side (as mpq_fit_layers),
-// and beside them the upload of the output error's descriptor tables, which
-// reads nothing the fits write (so the GEMM starts as soon as the last fit
-// ends); (2) the output error's launch groups and, beside them, one
-// reconstruction of every layer (it reads only the fit's outputs and is
-// bound by HBM, the GEMM by MFMA).
+// each followed on its stream by the reconstruction of its layers when it
+// has one (rec_after), and beside them the upload of the output error's
+// descriptor tables, which reads nothing the fits write (so the GEMM starts
+// as soon as the last fit ends); (2) the output error's launch groups and,
+// beside them, one reconstruction of the remaining layers (it reads only
+// the fit's outputs and is bound by HBM, the GEMM by MFMA).
 hipError_t quantize_enqueue(QuantizeStep &q, hipStream_t s)
 {
     std::vector<double> work;
@@ -739,7 +767,13 @@ hipError_t quantize_enqueue(QuantizeStep &q, hipStream_t s)
     const int n_groups = (int)q.ej.work.size();
     if (n_groups > 0) work.push_back(0.0);
     hipError_t e = run_concurrently(s, work, [&](int i, hipStream_t st) {
-        if (i < n_fit_jobs) return launch_fit_job(q.jobs[i], q.n_grid, st);
+        if (i < n_fit_jobs) {
+            hipError_t e0 = launch_fit_job(q.jobs[i], q.n_grid, st);
+            const std::vector<mpq::RecLayer> &r = q.rec_after[i];
+            if (e0 == hipSuccess && !r.empty())
+                e0 = mpq::launch_reconstruct(r.data(), (int)r.size(), q.max_points, st);
+            return e0;
+        }
         hipError_t e1 = hipSuccess;
         for (int g = 0; g < n_groups && e1 == hipSuccess; ++g)
             e1 = launch_err_job(q.err, q.ej, g, q.max_points, st, mpq::kErrUpload);
