@@ -71,15 +71,19 @@ __global__ void integer_scales_kernel(const float *scales, const int32_t *counts
 }
 
 // Load mode of the operands: 16-byte chunks (d % 16 == 0, rows 16-byte
-// aligned), 4-byte words (d % 4 == 0, 4-byte aligned) or bytes.
+// aligned), 4-byte words (d % 4 == 0, 4-byte aligned) or bytes (aligned
+// dwords shifted into place when the buffer's base is 4-byte aligned).
 enum { kLoad16 = 0, kLoad4 = 1, kLoad1 = 2 };
 
 // kRows rows of kIK bytes from K offset k0, kIPieces 16-byte pieces a row,
 // kRows kIPieces / kIThreads pieces per thread.  Row r starts at byte rowoff[r] of the buffer, or
-// is absent (rowoff < 0, or r >= live: zeros, nothing loaded).
+// is absent (rowoff < 0, or r >= live: zeros, nothing loaded).  words: in
+// bytes mode, the bytes of the buffer that aligned dwords may serve (0 when
+// its base is not 4-byte aligned; a dword that reaches past the buffer's
+// end loads as zero, so the last bytes go one by one).
 template <int kMode, int kRows>
 __device__ __forceinline__ void load_rows(__amdgpu_buffer_rsrc_t rs, const int *rowoff, int live, int64_t d,
-                                          int64_t k0, i32x4 (&v)[kRows * kIPieces / kIThreads])
+                                          int64_t k0, int64_t words, i32x4 (&v)[kRows * kIPieces / kIThreads])
 {
 #pragma unroll
     for (int h = 0; h < kRows * kIPieces / kIThreads; ++h) {
@@ -99,6 +103,24 @@ __device__ __forceinline__ void load_rows(__amdgpu_buffer_rsrc_t rs, const int *
             for (int w = 0; w < 4; ++w)
                 v[h][w] = (int)__builtin_amdgcn_raw_buffer_load_b32(
                     rs, k + 4 * w < d ? (uint32_t)(at + 4 * w) : kIOob, 0, 0);
+        } else if ((at & ~(int64_t)3) + 20 <= words) {
+            // the five aligned dwords around the 16 bytes (those wholly at
+            // or past d not loaded), funnel-shifted into place; the bytes at
+            // or past d zeroed
+            const int sh = (int)(at & 3);
+            const int64_t a0 = at - sh;
+            uint32_t wd[5];
+#pragma unroll
+            for (int q = 0; q < 5; ++q)
+                wd[q] = __builtin_amdgcn_raw_buffer_load_b32(
+                    rs, k - sh + 4 * q < d ? (uint32_t)(a0 + 4 * q) : kIOob, 0, 0);
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                uint32_t word = __builtin_amdgcn_alignbyte(wd[w + 1], wd[w], (uint32_t)sh);
+                const int64_t left = d - (k + 4 * w);   // bytes of the word before d
+                if (left < 4) word = left <= 0 ? 0u : word & ((1u << (8 * (int)left)) - 1u);
+                v[h][w] = (int)word;
+            }
         } else {
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
@@ -133,6 +155,7 @@ __device__ __forceinline__ void store_slab(int8_t *s, const i32x4 (&v)[kRows * k
 // its MFMAs.
 template <int kMode, int kPts, int kN>
 __device__ __forceinline__ void chunk_sums(__amdgpu_buffer_rsrc_t rsA, __amdgpu_buffer_rsrc_t rsB,
+                                           int64_t wordsA, int64_t wordsB,
                                            const int *s_offA, const int *s_offB, const int32_t *s_coef,
                                            int8_t (*ldsA)[kPts * kICh * kIRow], int8_t (*ldsB)[kIN * kIRow],
                                            int64_t d, long long (&sum)[16])
@@ -146,16 +169,16 @@ __device__ __forceinline__ void chunk_sums(__amdgpu_buffer_rsrc_t rsA, __amdgpu_
         for (int v = 0; v < 16; ++v) acc[i][v] = 0;
     i32x4 ra[kARows * kIPieces / kIThreads], rb[kIN * kIPieces / kIThreads];
     int buf = 0;
-    load_rows<kMode, kARows>(rsA, s_offA, kN * kICh, d, 0, ra);
-    load_rows<kMode, kIN>(rsB, s_offB, kIN, d, 0, rb);
+    load_rows<kMode, kARows>(rsA, s_offA, kN * kICh, d, 0, wordsA, ra);
+    load_rows<kMode, kIN>(rsB, s_offB, kIN, d, 0, wordsB, rb);
     store_slab<kARows>(ldsA[0], ra);
     store_slab<kIN>(ldsB[0], rb);
     __syncthreads();
     for (int64_t k0 = 0; k0 < d; k0 += kIK) {
         const bool more = k0 + kIK < d;
         if (more) {   // global loads in flight during the MFMAs
-            load_rows<kMode, kARows>(rsA, s_offA, kN * kICh, d, k0 + kIK, ra);
-            load_rows<kMode, kIN>(rsB, s_offB, kIN, d, k0 + kIK, rb);
+            load_rows<kMode, kARows>(rsA, s_offA, kN * kICh, d, k0 + kIK, wordsA, ra);
+            load_rows<kMode, kIN>(rsB, s_offB, kIN, d, k0 + kIK, wordsB, rb);
         }
         // v_mfma_i32_32x32x32_i8: lane l supplies row (or column) l % 32,
         // bytes 16 * (l / 32) .. +15 of the 32-deep K step
@@ -230,6 +253,8 @@ __global__ void __launch_bounds__(kIThreads) int_forward_kernel(const IntGroup g
     }
     const __amdgpu_buffer_rsrc_t rsA = rsrc(L.codes, (uint32_t)(C * P * d));
     const __amdgpu_buffer_rsrc_t rsB = rsrc(L.X, (uint32_t)(N * d));
+    const int64_t wordsA = ((uintptr_t)L.codes & 3) == 0 ? C * P * d : 0;
+    const int64_t wordsB = ((uintptr_t)L.X & 3) == 0 ? N * d : 0;
     __syncthreads();
     const int imax = s_imax;
 
@@ -251,7 +276,7 @@ __global__ void __launch_bounds__(kIThreads) int_forward_kernel(const IntGroup g
         const int npts = imax - p0 < kPts ? imax - p0 : kPts;   // uniform
         switch (npts) {
 #define MPQ_CHUNK(n) \
-    case n: if constexpr (n <= kPts) chunk_sums<kMode, kPts, n>(rsA, rsB, s_offA, s_offB, s_coef, ldsA, ldsB, d, sum); break;
+    case n: if constexpr (n <= kPts) chunk_sums<kMode, kPts, n>(rsA, rsB, wordsA, wordsB, s_offA, s_offB, s_coef, ldsA, ldsB, d, sum); break;
             MPQ_CHUNK(1) MPQ_CHUNK(2) MPQ_CHUNK(3) MPQ_CHUNK(4)
             MPQ_CHUNK(5) MPQ_CHUNK(6) MPQ_CHUNK(7) MPQ_CHUNK(8)
 #undef MPQ_CHUNK
