@@ -182,6 +182,29 @@ def test_lattice_mode_channels(orc, d):
         assert not (diff & ~tie).any(), f"channels {np.nonzero(diff & ~tie)[0]} differ without a tie"
 
 
+@pytest.mark.parametrize("d", [40, 64, 130, 256, 400, 512])
+def test_per_level_mode_boundaries(orc, d):
+    """The per-level histogram of the default grid (channels of up to 512,
+    below the lattice mode), whose level counts come from an fp32 estimate
+    and take one exact comparison only when the estimate lies near an
+    integer: the rows of the lattice test put many elements exactly on a
+    boundary (estimate an integer), plus random, tiny-scale, outlier and
+    equal-magnitude rows; lockstep parity, and agreement with the binary
+    search of the explicit grid."""
+    rng = np.random.default_rng(1000 + d)
+    W = _lattice_rows(d, rng)
+    for bits, G, P, tol in ((4, 256, 4, 1e-3), (4, 256, 8, 0.0), (3, 512, 5, 1e-4), (5, 128, 3, 1e-3)):
+        say(f"case per-level boundaries d={d} bits={bits} G={G} P={P} tol={tol}")
+        out = gpu_fit(W, bits, P, G, tol)
+        v = assert_parity(orc, W, bits, P, G, tol, out)
+        grid = (np.arange(1, G + 1, dtype=np.float64) / G).astype(np.float32)
+        ref = gpu_fit(W, bits, P, G, tol, grid=grid)
+        diff = ((out[2] != ref[2]) | (out[1] != ref[1]).any(axis=1)
+                | (out[0] != ref[0]).any(axis=(1, 2)))
+        tie = (v["cand_ties"] + v["code_ties"] + v["stop_ties"]) > 0
+        assert not (diff & ~tie).any(), f"channels {np.nonzero(diff & ~tie)[0]} differ without a tie"
+
+
 def test_exact_ties_between_candidates(orc):
     """Channels built so that several candidate scales give exactly the same
     error (dyadic values): the smallest scale must win, in both searches."""
