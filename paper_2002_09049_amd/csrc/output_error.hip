@@ -16,20 +16,22 @@
 //     slab of a row tile is one contiguous block.  Items whose rows the fit
 //     already wrote (d_ready) are not formed.
 //
-//  2. gemm: Y = D X on MFMA (v_mfma_f32_32x32x2f32, fp32 in and accumulate),
-//     the path's one dense contraction.  A slab of D (one block) is staged
-//     transposed into K-major LDS rows; X is K-major, its slab kBK rows of
-//     128 consecutive floats.  A workgroup of eight wavefronts owns a 128 x 128 tile of Y and
-//     one K range; each wavefront owns 64 x 32 as 2 MFMA blocks.  The K
-//     loop stages slabs through double-buffered LDS from two register sets:
-//     while the MFMAs consume one slab, the next waits in registers for its
-//     LDS buffer and the one after is in flight (buffer loads: offsets past a
-//     range read as zeros), so a load has two slabs of MFMA time to arrive.
-//     Two workgroups per CU (four wavefronts per SIMD) cover each other's
-//     LDS and barrier waits.  The epilogue squares Y (fp64) and sums each row
-//     over the tile's columns into a partial per (column tile, row); a layer
-//     whose K is split (to balance a grid of long and short K ranges) stores
-//     its fp32 Y tiles per K range instead.
+//  2. gemm: Y = D X, the path's one dense contraction, in fp32 from bf16
+//     matrix products: each fp32 operand is split into three bf16 pieces
+//     (hi + mid + lo, exact) and six of the nine piece products are summed
+//     by v_mfma_f32_32x32x16_bf16 with fp32 accumulation (the three left
+//     out lie below one rounding of the fp32 product).  A workgroup of four
+//     wavefronts owns a 128 x 128 tile of Y and one K range; each wavefront
+//     owns 64 x 64 as 2 x 2 MFMA blocks.  A slab of D (one block, rows of
+//     kBK k) and of X (kBK rows of 128 samples) is split once per workgroup
+//     into piece tiles in LDS, both with k contiguous per row and column;
+//     two register sets keep the slab after next in flight while one is
+//     multiplied and the next is split and stored (buffer loads: offsets
+//     past a range read as zeros).  Two workgroups per CU cover each
+//     other's split, store and barrier phases.  The epilogue squares Y
+//     (fp64) and sums each row over the tile's columns into a partial per
+//     (column tile, row); a layer whose K is split (to balance a grid of
+//     long and short K ranges) stores its fp32 Y tiles per K range instead.
 //
 // An err item may be restricted to a device list of channels (rows of D =
 // the listed channels, in list order; the list length is read by each
@@ -64,18 +66,20 @@ namespace {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kBM = 128, kBN = 128, kBK = 32;
 constexpr int kRangeK = 768;      // K of a split layer's K range, about
 constexpr int kMinSlabs = 4;      // shortest K range (slabs) of a listed layer's live rows
-constexpr int kThreads = 512;   // GEMM workgroup: eight wavefronts, two per SIMD
-constexpr int kPad = 4;          // LDS row padding (floats); rows stay 16-byte aligned
-constexpr int kVec = kBK * kBM / kThreads / 4;   // float4 per thread and operand per slab
+constexpr int kThreads = 256;   // GEMM workgroup: four wavefronts (one per SIMD), 64 x 64 of the tile each
+constexpr int kPieces = 3;      // bf16 pieces of an fp32 operand
+constexpr int kRowK = kBK + 8;  // LDS row of a piece: kBK bf16 and 16 bytes of padding (80 bytes)
 constexpr int kMaxErrItems = 1024;   // items (err and ref) per launch group
 constexpr int kDescChunk = 20;       // descriptors per upload kernel
 constexpr int kXcds = 8;         // MI355X: workgroups are dealt to 8 XCDs in turn
 constexpr int kFormThreads = 256;
-constexpr int kPadA = 2;         // A slab rows: 130 floats, so a wavefront's 4-byte stores hit 64 banks
 constexpr int kFinRows = 256 / kWave;   // finish: rows of a split layer per workgroup
 
 // Raw buffer resource (gfx9 descriptor word 3: 32-bit dwords, no swizzle).
@@ -244,13 +248,61 @@ __global__ void __launch_bounds__(kFormThreads) form_d_kernel(const ErrGroup g,
 }
 
 // ---- 2. gemm: Y = D X, squared and summed per row
+
+// The three bf16 pieces of fp32 values, in pairs: x = hi + mid + lo exactly
+// for finite x below bf16's largest value.  Each piece is the remainder so
+// far rounded to nearest (8 significant bits): x - hi is exact in fp32
+// (at most 16 bits), and so is its remainder after mid, which has at most 8
+// bits and is lo.
+__device__ __forceinline__ void split_pair(float x0, float x1, bf16x2 &h, bf16x2 &m, bf16x2 &l)
+{
+    const f32x2 x = {x0, x1};
+    h = __builtin_convertvector(x, bf16x2);
+    const f32x2 r1 = x - __builtin_convertvector(h, f32x2);
+    m = __builtin_convertvector(r1, bf16x2);
+    const f32x2 r2 = r1 - __builtin_convertvector(m, f32x2);
+    l = __builtin_convertvector(r2, bf16x2);
+}
+
+// Sixteen consecutive k of one row (D) or one column (X): the pieces as two
+// 16-byte vectors each, stored to rows of the piece tiles.
+__device__ __forceinline__ void split_store16(const float (&v)[16], __bf16 *h, __bf16 *m, __bf16 *l)
+{
+    bf16x2 ph[8], pm[8], pl[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) split_pair(v[2 * i], v[2 * i + 1], ph[i], pm[i], pl[i]);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        bf16x8 vh, vm, vl;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            vh[2 * i] = ph[4 * q + i][0]; vh[2 * i + 1] = ph[4 * q + i][1];
+            vm[2 * i] = pm[4 * q + i][0]; vm[2 * i + 1] = pm[4 * q + i][1];
+            vl[2 * i] = pl[4 * q + i][0]; vl[2 * i + 1] = pl[4 * q + i][1];
+        }
+        *(bf16x8 *)(h + 8 * q) = vh;
+        *(bf16x8 *)(m + 8 * q) = vm;
+        *(bf16x8 *)(l + 8 * q) = vl;
+    }
+}
+
+// Y = D X in fp32 from bf16 matrix products (v_mfma_f32_32x32x16_bf16):
+// with D = Dh + Dm + Dl and X = Xh + Xm + Xl (split_pair), each product
+// D X is summed from the six piece products Dh Xh, Dh Xm, Dm Xh, Dh Xl,
+// Dl Xh and Dm Xm (bf16 products are exact in fp32, accumulated in fp32).
+// The three left out (Dm Xl, Dl Xm, Dl Xl) are below 2^-23 |D X| together,
+// under one rounding of the fp32 product, so the sums carry the error of an
+// fp32 accumulation.  Six bf16 products cost 6/16 of one fp32 product's
+// matrix-core time.
 template <bool kVecX>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4)))
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
 gemm_err_kernel(const ErrGroup g, const ErrLayer *__restrict__ Ls)
 {
-    __shared__ __align__(16) float sA[2][kBK][kBM + kPadA];
-    __shared__ __align__(16) float sX[2][kBK][kBN + kPad];
-    __shared__ double sPart[kBN / 32][kBM];
+    // piece tiles of the slab: rows of D (channels) and columns of X
+    // (samples), kBK k each; a 16-byte read of 16 rows covers the 64 banks once
+    __shared__ __align__(16) __bf16 sD[kPieces][kBM][kRowK];
+    __shared__ __align__(16) __bf16 sX[kPieces][kBN][kRowK];
+    __shared__ double sPart[2][kBM];
 
     // a layer's workgroups: the planned tiles' from block_begin, and any
     // more (for the short K ranges of a listed layer's few live rows) from
@@ -294,7 +346,7 @@ gemm_err_kernel(const ErrGroup g, const ErrLayer *__restrict__ Ls)
 
     const int t = threadIdx.x;
     const int lane = t % kWave, wid = t / kWave;
-    const int wm = wid / 4, wn = wid % 4;   // rows wm * 64 + [0, 64), columns wn * 32 + [0, 32)
+    const int wm = wid / 2, wn = wid % 2;   // rows wm * 64 + [0, 64), columns wn * 64 + [0, 64)
     const int64_t C = L.C, n = L.n;
     const int64_t col0 = (int64_t)tn * kBN;
     const int64_t kbeg = (int64_t)split * ls.kchunk;
@@ -305,140 +357,159 @@ gemm_err_kernel(const ErrGroup g, const ErrLayer *__restrict__ Ls)
     // each; rows past C feed only output rows nobody reads) and this K
     // range's rows of X (below 2^31 bytes, see plan_item; rows past kend read
     // as zeros)
-    const __amdgpu_buffer_rsrc_t rsA =
+    const __amdgpu_buffer_rsrc_t rsD =
         make_rsrc(L.D + (int64_t)tm * L.nkb * (kBM * kBK), (uint32_t)L.nkb * (kBM * kBK * 4));
     const __amdgpu_buffer_rsrc_t rsX = make_rsrc(L.X + kbeg * n, (uint32_t)((kend - kbeg) * n * 4));
-    // staging roles.  A: float4 number t + kThreads v of the slab block, rows
-    // of kBK / 4 float4: row ar + kARowStep v, k ak .. ak + 3 (D's k past d
-    // are zeros).
-    // X: float4 number t + kThreads v, rows of kBN / 4 float4: row sk +
-    // kRowStep v, columns sm .. sm + 3, so each load instruction of a
-    // wavefront covers whole rows
-    constexpr int kF4RowA = kBK / 4;
-    constexpr int kARowStep = kThreads / kF4RowA;
-    const int ar = t / kF4RowA, ak = (t % kF4RowA) * 4;
-    constexpr int kF4Row = kBN / 4;
-    constexpr int kRowStep = kThreads / kF4Row;
-    const int sk = t / kF4Row, sm = (t % kF4Row) * 4;
-    uint32_t offA[kVec], offX[kVec];
-#pragma unroll
-    for (int v = 0; v < kVec; ++v) {
-        const int64_t c = col0 + sm;
-        offA[v] = (uint32_t)((kbeg / kBK * (kBM * kBK) + (ar + kARowStep * v) * kBK + ak) * 4);
-        offX[v] = (kVecX && c < n) ? (uint32_t)(((int64_t)(sk + kRowStep * v) * n + c) * 4) : kOob;   // n % 4 == 0
-    }
-    const uint32_t stepA = (uint32_t)(kBM * kBK * 4), stepX = (uint32_t)(kBK * n * 4);
+    // staging roles: D row dr, k dh * 16 .. + 15 (four float4 of the slab
+    // block); X column xc, k xh * 16 .. + 15 (sixteen floats, one per row
+    // of X: a wavefront's load covers 64 consecutive columns)
+    const int dr = t / 2, dh = t % 2;
+    const int xc = t % kBN, xh = t / kBN;
+    const uint32_t offD = (uint32_t)((kbeg / kBK * (kBM * kBK) + dr * kBK + dh * 16) * 4);
+    const uint32_t offX = col0 + xc < n ? (uint32_t)(((int64_t)xh * 16 * n + col0 + xc) * 4) : kOob;
+    const uint32_t stepD = (uint32_t)(kBM * kBK * 4), stepX = (uint32_t)(kBK * n * 4), rowX = (uint32_t)(n * 4);
 
     // two register sets: the slab after next is in flight while a slab is
-    // multiplied and the next one is stored
-    f32x4 ra0[kVec], rx0[kVec], ra1[kVec], rx1[kVec];
-    auto load = [&](f32x4 (&ra)[kVec], f32x4 (&rx)[kVec], int s) {
+    // multiplied and the next one is split and stored
+    float rd0[16], rx0[16], rd1[16], rx1[16];
+    auto load = [&](float (&rd)[16], float (&rx)[16], int s) {
 #pragma unroll
-        for (int v = 0; v < kVec; ++v) {
-            ra[v] = load4(rsA, offA[v] + (uint32_t)s * stepA);
-            if constexpr (kVecX) {
-                rx[v] = load4(rsX, offX[v] == kOob ? kOob : offX[v] + (uint32_t)s * stepX);
-            } else {
-                const int64_t c = col0 + sm, kr = (int64_t)s * kBK + sk + kRowStep * v;
+        for (int v = 0; v < 4; ++v) {
+            const f32x4 a = load4(rsD, offD + (uint32_t)s * stepD + 16 * v);
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const uint32_t o = c + u < n ? (uint32_t)((kr * n + c + u) * 4) : kOob;
-                    rx[v][u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsX, o, 0, 0));
+            for (int u = 0; u < 4; ++u) rd[4 * v + u] = a[u];
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+            const uint32_t o = offX == kOob ? kOob : offX + (uint32_t)s * stepX + (uint32_t)u * rowX;
+            rx[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsX, o, 0, 0));
+        }
+    };
+    auto store = [&](const float (&rd)[16], const float (&rx)[16]) {
+        split_store16(rd, &sD[0][dr][dh * 16], &sD[1][dr][dh * 16], &sD[2][dr][dh * 16]);
+        split_store16(rx, &sX[0][xc][xh * 16], &sX[1][xc][xh * 16], &sX[2][xc][xh * 16]);
+    };
+
+    // acc[cb][rb]: samples wn * 64 + cb * 32 + [0, 32) by rows wm * 64 + rb
+    // * 32 + [0, 32).  The blocks hold Y transposed (X's pieces as the MFMA's
+    // A operand, D's as its B), so a lane's registers run over samples of
+    // one row.
+    floatx16 acc[2][2];
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[cb][rb][v] = 0.0f;
+
+    // A row block with no live row of D (a layer of few channels, a few
+    // listed rows) multiplies nothing, and a slab stops at the K range's
+    // end (a d = 9 layer takes one of the two 16-k steps): the skipped
+    // products are of zero padding, so the sums are unchanged.
+    const bool live0 = row0 + wm * 64 < nact, live1 = row0 + wm * 64 + 32 < nact;   // uniform per wavefront
+    auto compute = [&](int s) {
+        if (!live0) return;
+        const int64_t left = kend - (kbeg + (int64_t)s * kBK);      // live k of the slab
+#pragma unroll
+        for (int ks = 0; ks < kBK / 16; ++ks) {
+            if (ks * 16 >= left) break;
+            const int ko = ks * 16 + 8 * (lane / 32);
+            bf16x8 xp[2][kPieces], dp[2][kPieces];
+#pragma unroll
+            for (int p = 0; p < kPieces; ++p) {
+#pragma unroll
+                for (int c = 0; c < 2; ++c) {
+                    xp[c][p] = *(const bf16x8 *)&sX[p][wn * 64 + c * 32 + lane % 32][ko];
+                    dp[c][p] = *(const bf16x8 *)&sD[p][wm * 64 + c * 32 + lane % 32][ko];
+                }
+            }
+            // the small products first
+            constexpr int kPx[6] = {1, 2, 0, 1, 0, 0}, kPd[6] = {1, 0, 2, 0, 1, 0};
+#pragma unroll
+            for (int z = 0; z < 6; ++z) {
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) {
+                    acc[cb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xp[cb][kPx[z]], dp[0][kPd[z]], acc[cb][0], 0, 0, 0);
+                    if (live1)
+                        acc[cb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xp[cb][kPx[z]], dp[1][kPd[z]], acc[cb][1], 0, 0, 0);
                 }
             }
         }
     };
-    auto store = [&](const f32x4 (&ra)[kVec], const f32x4 (&rx)[kVec], int buf) {
-#pragma unroll
-        for (int v = 0; v < kVec; ++v) {
-            // A transposed into K-major rows: four 4-byte stores
-#pragma unroll
-            for (int u = 0; u < 4; ++u) sA[buf][ak + u][ar + kARowStep * v] = ra[v][u];
-            *(f32x4 *)&sX[buf][sk + kRowStep * v][sm] = rx[v];
-        }
-    };
 
-    floatx16 acc[2];
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[a][v] = 0.0f;
-
-    // MFMA block a of a wavefront takes its rows 2 i + a (i < 32), so one
-    // 8-byte LDS read gives a lane both blocks' A operands.  A wavefront whose
-    // 64 rows hold no live row of D (a layer of 64 channels or fewer, a few
-    // listed rows) multiplies nothing, and a slab stops at the K range's end
-    // (a d = 9 layer takes 5 of the 16 steps): the skipped products are of
-    // zero padding, so the sums are unchanged.
-    const bool rows_live = row0 + wm * 64 < nact;   // uniform per wavefront
-    auto compute = [&](int buf, int s) {
-        if (!rows_live) return;
-        const int64_t left = kend - (kbeg + (int64_t)s * kBK);      // live k of the slab
-        const int klim = left >= kBK ? kBK : (int)((left + 1) & ~1);
-#pragma unroll
-        for (int kk = 0; kk < kBK; kk += 2) {
-            if (kk >= klim) break;
-            const int kr = kk + lane / 32;
-            const float2 a2 = *(const float2 *)&sA[buf][kr][wm * 64 + 2 * (lane % 32)];
-            const float bx = sX[buf][kr][wn * 32 + lane % 32];
-            acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a2.x, bx, acc[0], 0, 0, 0);
-            acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a2.y, bx, acc[1], 0, 0, 0);
-        }
-    };
-
-    load(ra0, rx0, 0);
-    if (nslab > 1) load(ra1, rx1, 1);
-    store(ra0, rx0, 0);
+    load(rd0, rx0, 0);
+    if (nslab > 1) load(rd1, rx1, 1);
+    store(rd0, rx0);
     __syncthreads();
-    if (nslab > 2) load(ra0, rx0, 2);
+    if (nslab > 2) load(rd0, rx0, 2);
     for (int s = 0; s < nslab; s += 2) {
-        // buffer 0 holds slab s, set 1 slab s + 1, set 0 slab s + 2 (in flight)
-        compute(0, s);
-        if (s + 1 < nslab) store(ra1, rx1, 1);
-        __syncthreads();
+        // the tiles hold slab s, set 1 slab s + 1, set 0 slab s + 2 (in flight)
+        compute(s);
         if (s + 1 >= nslab) break;
-        if (s + 3 < nslab) load(ra1, rx1, s + 3);
-        compute(1, s + 1);
-        if (s + 2 < nslab) store(ra0, rx0, 0);
         __syncthreads();
-        if (s + 4 < nslab) load(ra0, rx0, s + 4);
+        store(rd1, rx1);
+        __syncthreads();
+        if (s + 3 < nslab) load(rd1, rx1, s + 3);
+        compute(s + 1);
+        if (s + 2 >= nslab) break;
+        __syncthreads();
+        store(rd0, rx0);
+        __syncthreads();
+        if (s + 4 < nslab) load(rd0, rx0, s + 4);
     }
 
     // Output layout of a 32 x 32 MFMA block: lane holds block column
-    // lane % 32 and, in register v, block row 8 (v / 4) + 4 (lane / 32) + v % 4
-    auto row_of = [&](int a, int v) {
-        return row0 + wm * 64 + 2 * (8 * (v / 4) + 4 * (lane / 32) + (v % 4)) + a;
-    };
-    const int64_t col = col0 + wn * 32 + lane % 32;
+    // lane % 32 (here row rb * 32 + lane % 32 of the wavefront's 64) and, in
+    // register v, block row 8 (v / 4) + 4 (lane / 32) + v % 4 (here a
+    // sample: four consecutive ones per group v / 4)
+    const int64_t row_w = row0 + wm * 64 + lane % 32;   // + rb * 32
+    auto col_of = [&](int cb, int grp) { return col0 + wn * 64 + cb * 32 + 8 * grp + 4 * (lane / 32); };
 
     if (ls.splits > 1) {
         // this K range's Y tile (rows of stride nact); the finish kernel sums
         // the ranges
         float *yp = L.ypart;
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+        for (int rb = 0; rb < 2; ++rb) {
+            const int64_t r = row_w + rb * 32;
+            if (r >= nact) continue;
+            float *yr = yp + ((int64_t)split * nact + r) * n;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int64_t r = row_of(a, v);
-                if (r < nact && col < n) yp[((int64_t)split * nact + r) * n + col] = acc[a][v];
-            }
+            for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+                for (int grp = 0; grp < 4; ++grp) {
+                    const int64_t c = col_of(cb, grp);
+                    const floatx16 &y = acc[cb][rb];
+                    if (kVecX) {   // n % 4 == 0: the four samples lie inside the row or past it
+                        if (c < n)
+                            *(f32x4 *)(yr + c) = f32x4{y[4 * grp], y[4 * grp + 1], y[4 * grp + 2], y[4 * grp + 3]};
+                    } else {
+#pragma unroll
+                        for (int u = 0; u < 4; ++u)
+                            if (c + u < n) yr[c + u] = y[4 * grp + u];
+                    }
+                }
+        }
         return;
     }
 
     // squares summed over the tile's columns, per row (fp64, fixed order):
-    // each wavefront's 32 columns, then the four column quarters in order
+    // a lane's 32 samples (block cb, then register order), then the other
+    // half-wave's 32 (samples past n are zeros), then the two column halves
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int rb = 0; rb < 2; ++rb) {
+        double sq = 0.0;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const double y = (double)acc[a][v];
-            const double s = half_wave_reduce(y * y, SumOp());
-            if (lane % 32 == 0) sPart[wn][(int)(row_of(a, v) - row0)] = s;
-        }
+        for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) sq = fma((double)acc[cb][rb][v], (double)acc[cb][rb][v], sq);
+        const double o = __shfl_xor(sq, 32);
+        if (lane < 32) sPart[wn][wm * 64 + rb * 32 + lane] = sq + o;
+    }
     __syncthreads();
-    for (int r = t; r < kBM; r += kThreads) {
-        const int64_t gr = row0 + r;
-        if (gr < C) L.rowpart[(int64_t)tn * C + gr] = ((sPart[0][r] + sPart[1][r]) + sPart[2][r]) + sPart[3][r];
+    if (t < kBM) {
+        const int64_t gr = row0 + t;
+        if (gr < C) L.rowpart[(int64_t)tn * C + gr] = sPart[0][t] + sPart[1][t];
     }
 }
 
