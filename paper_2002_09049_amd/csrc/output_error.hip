@@ -73,9 +73,12 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 constexpr int kBM = 128, kBN = 128, kBK = 32;
 constexpr int kRangeK = 768;      // K of a split layer's K range, about
 constexpr int kMinSlabs = 4;      // shortest K range (slabs) of a listed layer's live rows
-constexpr int kThreads = 256;   // GEMM workgroup: four wavefronts (one per SIMD), 64 x 64 of the tile each
+constexpr int kThreads = 512;   // GEMM workgroup: four wavefronts multiply (64 x 64 of the tile each), four stage
+constexpr int kStageT = 256;    // threads of the staging wavefronts
 constexpr int kPieces = 3;      // bf16 pieces of an fp32 operand
-constexpr int kRowK = kBK + 8;  // LDS row of a piece: kBK bf16 and 16 bytes of padding (80 bytes)
+constexpr int kSlabK = 16;      // k per staged slab (one 16-k MFMA step)
+constexpr int kRowK = kSlabK + 8;   // LDS row of a piece: 16 bf16 and 16 bytes of padding (48 bytes)
+constexpr int kRing = 4;        // staging register sets: loads run four slabs ahead
 constexpr int kMaxErrItems = 1024;   // items (err and ref) per launch group
 constexpr int kDescChunk = 20;       // descriptors per upload kernel
 constexpr int kXcds = 8;         // MI355X: workgroups are dealt to 8 XCDs in turn
@@ -264,26 +267,22 @@ __device__ __forceinline__ void split_pair(float x0, float x1, bf16x2 &h, bf16x2
     l = __builtin_convertvector(r2, bf16x2);
 }
 
-// Sixteen consecutive k of one row (D) or one column (X): the pieces as two
-// 16-byte vectors each, stored to rows of the piece tiles.
-__device__ __forceinline__ void split_store16(const float (&v)[16], __bf16 *h, __bf16 *m, __bf16 *l)
+// Eight consecutive k of one row (D) or one column (X): the pieces, one
+// 16-byte vector each, stored to a row of each piece tile.
+__device__ __forceinline__ void split_store8(const float (&v)[8], __bf16 *h, __bf16 *m, __bf16 *l)
 {
-    bf16x2 ph[8], pm[8], pl[8];
+    bf16x8 vh, vm, vl;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) split_pair(v[2 * i], v[2 * i + 1], ph[i], pm[i], pl[i]);
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-        bf16x8 vh, vm, vl;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            vh[2 * i] = ph[4 * q + i][0]; vh[2 * i + 1] = ph[4 * q + i][1];
-            vm[2 * i] = pm[4 * q + i][0]; vm[2 * i + 1] = pm[4 * q + i][1];
-            vl[2 * i] = pl[4 * q + i][0]; vl[2 * i + 1] = pl[4 * q + i][1];
-        }
-        *(bf16x8 *)(h + 8 * q) = vh;
-        *(bf16x8 *)(m + 8 * q) = vm;
-        *(bf16x8 *)(l + 8 * q) = vl;
+    for (int i = 0; i < 4; ++i) {
+        bf16x2 ph, pm, pl;
+        split_pair(v[2 * i], v[2 * i + 1], ph, pm, pl);
+        vh[2 * i] = ph[0]; vh[2 * i + 1] = ph[1];
+        vm[2 * i] = pm[0]; vm[2 * i + 1] = pm[1];
+        vl[2 * i] = pl[0]; vl[2 * i + 1] = pl[1];
     }
+    *(bf16x8 *)h = vh;
+    *(bf16x8 *)m = vm;
+    *(bf16x8 *)l = vl;
 }
 
 // Y = D X in fp32 from bf16 matrix products (v_mfma_f32_32x32x16_bf16):
@@ -295,13 +294,13 @@ __device__ __forceinline__ void split_store16(const float (&v)[16], __bf16 *h, _
 // fp32 accumulation.  Six bf16 products cost 6/16 of one fp32 product's
 // matrix-core time.
 template <bool kVecX>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4)))
 gemm_err_kernel(const ErrGroup g, const ErrLayer *__restrict__ Ls)
 {
-    // piece tiles of the slab: rows of D (channels) and columns of X
-    // (samples), kBK k each; a 16-byte read of 16 rows covers the 64 banks once
-    __shared__ __align__(16) __bf16 sD[kPieces][kBM][kRowK];
-    __shared__ __align__(16) __bf16 sX[kPieces][kBN][kRowK];
+    // double-buffered piece tiles of a 16-k slab: rows of D (channels) and
+    // columns of X (samples); a 16-byte read of 16 rows covers the 64 banks once
+    __shared__ __align__(16) __bf16 sD[2][kPieces][kBM][kRowK];
+    __shared__ __align__(16) __bf16 sX[2][kPieces][kBN][kRowK];
     __shared__ double sPart[2][kBM];
 
     // a layer's workgroups: the planned tiles' from block_begin, and any
@@ -345,50 +344,14 @@ gemm_err_kernel(const ErrGroup g, const ErrLayer *__restrict__ Ls)
     const int64_t row0 = (int64_t)tm * kBM;
 
     const int t = threadIdx.x;
-    const int lane = t % kWave, wid = t / kWave;
-    const int wm = wid / 2, wn = wid % 2;   // rows wm * 64 + [0, 64), columns wn * 64 + [0, 64)
+    const int lane = t % kWave, wid = __builtin_amdgcn_readfirstlane(t / kWave);   // uniform per wavefront
+    const bool stager = wid >= 4;           // wavefronts 4 .. 7 stage, 0 .. 3 multiply
+    const int wm = (wid % 4) / 2, wn = wid % 2;   // rows wm * 64 + [0, 64), columns wn * 64 + [0, 64)
     const int64_t C = L.C, n = L.n;
     const int64_t col0 = (int64_t)tn * kBN;
-    const int64_t kbeg = (int64_t)split * ls.kchunk;
+    const int64_t kbeg = (int64_t)split * ls.kchunk;   // a multiple of kBK
     const int64_t kend = min(kbeg + (int64_t)ls.kchunk, (int64_t)L.d);
-    const int nslab = (int)((kend - kbeg + kBK - 1) / kBK);
-
-    // buffer resources: this row tile's slabs of D (one contiguous block
-    // each; rows past C feed only output rows nobody reads) and this K
-    // range's rows of X (below 2^31 bytes, see plan_item; rows past kend read
-    // as zeros)
-    const __amdgpu_buffer_rsrc_t rsD =
-        make_rsrc(L.D + (int64_t)tm * L.nkb * (kBM * kBK), (uint32_t)L.nkb * (kBM * kBK * 4));
-    const __amdgpu_buffer_rsrc_t rsX = make_rsrc(L.X + kbeg * n, (uint32_t)((kend - kbeg) * n * 4));
-    // staging roles: D row dr, k dh * 16 .. + 15 (four float4 of the slab
-    // block); X column xc, k xh * 16 .. + 15 (sixteen floats, one per row
-    // of X: a wavefront's load covers 64 consecutive columns)
-    const int dr = t / 2, dh = t % 2;
-    const int xc = t % kBN, xh = t / kBN;
-    const uint32_t offD = (uint32_t)((kbeg / kBK * (kBM * kBK) + dr * kBK + dh * 16) * 4);
-    const uint32_t offX = col0 + xc < n ? (uint32_t)(((int64_t)xh * 16 * n + col0 + xc) * 4) : kOob;
-    const uint32_t stepD = (uint32_t)(kBM * kBK * 4), stepX = (uint32_t)(kBK * n * 4), rowX = (uint32_t)(n * 4);
-
-    // two register sets: the slab after next is in flight while a slab is
-    // multiplied and the next one is split and stored
-    float rd0[16], rx0[16], rd1[16], rx1[16];
-    auto load = [&](float (&rd)[16], float (&rx)[16], int s) {
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const f32x4 a = load4(rsD, offD + (uint32_t)s * stepD + 16 * v);
-#pragma unroll
-            for (int u = 0; u < 4; ++u) rd[4 * v + u] = a[u];
-        }
-#pragma unroll
-        for (int u = 0; u < 16; ++u) {
-            const uint32_t o = offX == kOob ? kOob : offX + (uint32_t)s * stepX + (uint32_t)u * rowX;
-            rx[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rsX, o, 0, 0));
-        }
-    };
-    auto store = [&](const float (&rd)[16], const float (&rx)[16]) {
-        split_store16(rd, &sD[0][dr][dh * 16], &sD[1][dr][dh * 16], &sD[2][dr][dh * 16]);
-        split_store16(rx, &sX[0][xc][xh * 16], &sX[1][xc][xh * 16], &sX[2][xc][xh * 16]);
-    };
+    const int nslab = (int)((kend - kbeg + kSlabK - 1) / kSlabK);
 
     // acc[cb][rb]: samples wn * 64 + cb * 32 + [0, 32) by rows wm * 64 + rb
     // * 32 + [0, 32).  The blocks hold Y transposed (X's pieces as the MFMA's
@@ -402,60 +365,97 @@ gemm_err_kernel(const ErrGroup g, const ErrLayer *__restrict__ Ls)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[cb][rb][v] = 0.0f;
 
-    // A row block with no live row of D (a layer of few channels, a few
-    // listed rows) multiplies nothing, and a slab stops at the K range's
-    // end (a d = 9 layer takes one of the two 16-k steps): the skipped
-    // products are of zero padding, so the sums are unchanged.
-    const bool live0 = row0 + wm * 64 < nact, live1 = row0 + wm * 64 + 32 < nact;   // uniform per wavefront
-    auto compute = [&](int s) {
-        if (!live0) return;
-        const int64_t left = kend - (kbeg + (int64_t)s * kBK);      // live k of the slab
+    // One barrier per slab for all eight wavefronts: the multiplying ones
+    // read slab s from buffer s % 2 while the staging ones split slab s + 1
+    // into the other buffer.
+    if (stager) {
+        // buffer resources: this row tile's 32-k chunks of D (one
+        // contiguous block each; rows past C feed only output rows nobody
+        // reads) and this K range's rows of X (below 2^31 bytes, see
+        // plan_item; rows past kend read as zeros)
+        const __amdgpu_buffer_rsrc_t rsD =
+            make_rsrc(L.D + (int64_t)tm * L.nkb * (kBM * kBK), (uint32_t)L.nkb * (kBM * kBK * 4));
+        const __amdgpu_buffer_rsrc_t rsX = make_rsrc(L.X + kbeg * n, (uint32_t)((kend - kbeg) * n * 4));
+        // staging roles: D row dr, k dh * 8 .. + 7 of the slab (two float4
+        // of the chunk's row); X column xc, k xh * 8 .. + 7 (eight floats,
+        // one per row of X: a wavefront's load covers 64 consecutive columns)
+        const int st = t - kStageT;
+        const int dr = st / 2, dh = st % 2;
+        const int xc = st % kBN, xh = st / kBN;
+        const uint32_t offD = (uint32_t)((kbeg / kBK * (kBM * kBK) + dr * kBK + dh * 8) * 4);
+        // a column past n reads at offset 2^32 - 1 (past every range, as a
+        // bit mask: no carry); the others stay below 2^32, as kchunk n 4 < 2^31
+        const uint32_t offX = (uint32_t)(((int64_t)xh * 8 * n + col0 + xc) * 4);
+        const uint32_t oobX = col0 + xc < n ? 0u : 0xffffffffu;
+        const uint32_t rowX = (uint32_t)(n * 4);
+        // slab s: chunk s / 2 of the range, k (s % 2) 16 within it
+        auto load = [&](float (&r)[16], int s) {
+            const uint32_t o = offD + (uint32_t)(s / 2) * (kBM * kBK * 4) + (uint32_t)(s % 2) * (kSlabK * 4);
+            const f32x4 a = load4(rsD, o), b = load4(rsD, o + 16);
 #pragma unroll
-        for (int ks = 0; ks < kBK / 16; ++ks) {
-            if (ks * 16 >= left) break;
-            const int ko = ks * 16 + 8 * (lane / 32);
-            bf16x8 xp[2][kPieces], dp[2][kPieces];
-#pragma unroll
-            for (int p = 0; p < kPieces; ++p) {
-#pragma unroll
-                for (int c = 0; c < 2; ++c) {
-                    xp[c][p] = *(const bf16x8 *)&sX[p][wn * 64 + c * 32 + lane % 32][ko];
-                    dp[c][p] = *(const bf16x8 *)&sD[p][wm * 64 + c * 32 + lane % 32][ko];
-                }
+            for (int u = 0; u < 4; ++u) {
+                r[u] = a[u];
+                r[4 + u] = b[u];
             }
-            // the small products first
-            constexpr int kPx[6] = {1, 2, 0, 1, 0, 0}, kPd[6] = {1, 0, 2, 0, 1, 0};
 #pragma unroll
-            for (int z = 0; z < 6; ++z) {
+            for (int u = 0; u < 8; ++u)
+                r[8 + u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                    rsX, (offX + (uint32_t)(s * kSlabK + u) * rowX) | oobX, 0, 0));
+        };
+        auto store = [&](const float (&r)[16], int buf) {
+            const float(&rd)[8] = *(const float(*)[8])&r[0];
+            const float(&rx)[8] = *(const float(*)[8])&r[8];
+            split_store8(rd, &sD[buf][0][dr][dh * 8], &sD[buf][1][dr][dh * 8], &sD[buf][2][dr][dh * 8]);
+            split_store8(rx, &sX[buf][0][xc][xh * 8], &sX[buf][1][xc][xh * 8], &sX[buf][2][xc][xh * 8]);
+        };
+        float ring[kRing][16];
 #pragma unroll
-                for (int cb = 0; cb < 2; ++cb) {
-                    acc[cb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xp[cb][kPx[z]], dp[0][kPd[z]], acc[cb][0], 0, 0, 0);
-                    if (live1)
-                        acc[cb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xp[cb][kPx[z]], dp[1][kPd[z]], acc[cb][1], 0, 0, 0);
-                }
+        for (int j = 0; j < kRing; ++j)
+            if (j < nslab) load(ring[j], j);
+        store(ring[0], 0);
+        if (kRing < nslab) load(ring[0], kRing);
+        __syncthreads();
+        for (int s0 = 0; s0 < nslab; s0 += kRing) {
+#pragma unroll
+            for (int j = 0; j < kRing; ++j) {
+                const int s = s0 + j;   // the multiplying wavefronts read slab s
+                if (s >= nslab) break;
+                if (s + 1 < nslab) store(ring[(j + 1) % kRing], (s + 1) % 2);
+                if (s + 1 + kRing < nslab) load(ring[(j + 1) % kRing], s + 1 + kRing);
+                __syncthreads();
             }
         }
-    };
-
-    load(rd0, rx0, 0);
-    if (nslab > 1) load(rd1, rx1, 1);
-    store(rd0, rx0);
-    __syncthreads();
-    if (nslab > 2) load(rd0, rx0, 2);
-    for (int s = 0; s < nslab; s += 2) {
-        // the tiles hold slab s, set 1 slab s + 1, set 0 slab s + 2 (in flight)
-        compute(s);
-        if (s + 1 >= nslab) break;
+    } else {
+        // A wavefront with no live row of D (a layer of few channels, a few
+        // listed rows) multiplies nothing: its products are of rows nobody
+        // reads.  Slabs past d hold zeros.
+        const bool rows_live = row0 + wm * 64 < nact;   // uniform per wavefront
+        constexpr int kPx[6] = {1, 2, 0, 1, 0, 0}, kPd[6] = {1, 0, 2, 0, 1, 0};   // the small products first
+        const int ko = 8 * (lane / 32);
         __syncthreads();
-        store(rd1, rx1);
-        __syncthreads();
-        if (s + 3 < nslab) load(rd1, rx1, s + 3);
-        compute(s + 1);
-        if (s + 2 >= nslab) break;
-        __syncthreads();
-        store(rd0, rx0);
-        __syncthreads();
-        if (s + 4 < nslab) load(rd0, rx0, s + 4);
+        for (int s = 0; s < nslab; ++s) {
+            if (rows_live) {
+                const int buf = s % 2;
+                bf16x8 xp[2][kPieces], dp[2][kPieces];
+#pragma unroll
+                for (int p = 0; p < kPieces; ++p) {
+#pragma unroll
+                    for (int c = 0; c < 2; ++c) {
+                        xp[c][p] = *(const bf16x8 *)&sX[buf][p][wn * 64 + c * 32 + lane % 32][ko];
+                        dp[c][p] = *(const bf16x8 *)&sD[buf][p][wm * 64 + c * 32 + lane % 32][ko];
+                    }
+                }
+#pragma unroll
+                for (int z = 0; z < 6; ++z)
+#pragma unroll
+                    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+                        for (int rb = 0; rb < 2; ++rb)
+                            acc[cb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xp[cb][kPx[z]], dp[rb][kPd[z]],
+                                                                                  acc[cb][rb], 0, 0, 0);
+            }
+            __syncthreads();
+        }
     }
 
     // Output layout of a 32 x 32 MFMA block: lane holds block column
@@ -468,6 +468,7 @@ gemm_err_kernel(const ErrGroup g, const ErrLayer *__restrict__ Ls)
     if (ls.splits > 1) {
         // this K range's Y tile (rows of stride nact); the finish kernel sums
         // the ranges
+        if (stager) return;
         float *yp = L.ypart;
 #pragma unroll
         for (int rb = 0; rb < 2; ++rb) {
@@ -504,7 +505,7 @@ gemm_err_kernel(const ErrGroup g, const ErrLayer *__restrict__ Ls)
 #pragma unroll
             for (int v = 0; v < 16; ++v) sq = fma((double)acc[cb][rb][v], (double)acc[cb][rb][v], sq);
         const double o = __shfl_xor(sq, 32);
-        if (lane < 32) sPart[wn][wm * 64 + rb * 32 + lane] = sq + o;
+        if (!stager && lane < 32) sPart[wn][wm * 64 + rb * 32 + lane] = sq + o;
     }
     __syncthreads();
     if (t < kBM) {
