@@ -28,8 +28,9 @@ whole step (sum of the per-channel point counts of all layers / step time).
 An untimed profile step first times every kernel launch by HIP events that
 the library records on the launch's own stream (mpq_timing_enable); the
 timed steps then carry events around the error GEMM's launches only.
-`roofline` is the error GEMM (the path's one dense contraction, FP32 MFMA),
-timed in the timed steps; `kernels` lists every kernel.  The fit kernels'
+`roofline` is the error GEMM (the path's one dense contraction: fp32 products
+of Eq. (12) from six bf16 piece products each, on bf16 MFMA), timed in the
+timed steps, against the dense bf16 MFMA peak; `kernels` lists every kernel.  The fit kernels'
 `dense_equivalent_tflops` prices their candidate search at 7 FLOP per
 (element, candidate) pair, the work a dense evaluation of Eq. (9) does; the
 histogram search does O(d M + G) per step instead, so that figure is not an
@@ -52,7 +53,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
-PEAK_MFMA_F32_TFLOPS = 157.3
+PEAK_MFMA_BF16_TFLOPS = 2500.0          # dense bf16 MFMA
+GEMM_PIECE_PRODUCTS = 6                 # bf16 products per fp32 product of the error GEMM
 PEAK_VALU_F32_TFLOPS = 157.3            # published (packed) FP32 vector peak
 PEAK_MFMA_I8_TOPS = 5000.0              # dense int8 MFMA
 PEAK_VALU_F32_NONPACKED_TFLOPS = 78.6   # 256 CU x 64 lanes x 2 FLOP x 2.4 GHz
@@ -171,7 +173,7 @@ COUNTER_PASSES = (
      "SQ_INSTS_LDS", "SQ_WAIT_INST_LDS", "SQ_BUSY_CYCLES"),
     ("SQ_INSTS_VALU_FLOPS_FP32", "SQ_INSTS_VALU_FLOPS_FP32_TRANS", "SQ_INSTS_VALU_FLOPS_FP64",
      "SQ_INSTS_VALU_FLOPS_FP64_TRANS", "SQ_INSTS_VALU_IOPS", "SQ_VALU_MFMA_BUSY_CYCLES",
-     "SQ_INSTS_VALU_MFMA_MOPS_F32", "SQ_BUSY_CU_CYCLES"),
+     "SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_BUSY_CU_CYCLES"),
     ("FETCH_SIZE",),
     ("WRITE_SIZE",),
 )
@@ -355,7 +357,8 @@ def summarize_benches(paths):
              "Strides: " + ", ".join(f"{b['config']['workload']} {_stride_of(b)}" for b in rows)
              + f"; {rows[0]['steps'] if rows else 0} timed steps after {rows[0]['warmup'] if rows else 0} "
                "warm-up steps.",
-             "The roofline kernel is the error GEMM (2 C d n FLOP per layer, event-timed in the timed steps);",
+             "The roofline kernel is the error GEMM (6 x 2 C d n bf16 FLOP per layer against the dense bf16",
+             "MFMA peak; fp32 equivalent: 2 C d n; event-timed in the timed steps);",
              "the other kernels are timed in the untimed profile step, where the fit launches share the",
              "device (so a fit's duration includes its neighbours).  `search` is the fit kernel with the",
              "most time per step; its SIMD VALU busy share (the share of the SIMDs' VALU issue capacity it",
@@ -376,7 +379,7 @@ def summarize_benches(paths):
         tr = r.get("traffic")
         lines.append(
             f"| {w} | {b['value'] / 1e6:.2f} M | {b['ms_per_step']:.3f} | {b['config']['points_per_step']} | "
-            f"{r['achieved']:.1f} TFLOP/s ({100 * r['frac']:.0f}% of {r['peak']}), {r['avg_launch_us']:.1f} us | "
+            f"{r['achieved']:.1f} TFLOP/s ({100 * r['frac']:.0f}% of {r['peak']:g}), {r['avg_launch_us']:.1f} us | "
             + ("-" if tr is None else f"{tr / 1e6:.0f} MB") + " | "
             f"`{lf[0]}` {lf[1]['avg_us']:.1f} us | "
             + ("-" if vb is None else f"{100 * vb:.1f}%") + f" (`{srch.get('kernel')}`) | "
@@ -621,8 +624,12 @@ def main():
                           "hbm_gbs_algorithmic": w["bytes"] / lps / avg_s / 1e9,
                           "hbm_frac_algorithmic": w["bytes"] / lps / avg_s / 1e9 / PEAK_HBM_GBS})
             elif "flop" in w:
-                k.update({"bound": "mfma", "unit": "TFLOP/s", "peak": PEAK_MFMA_F32_TFLOPS,
-                          "flop_per_launch": w["flop"] / lps, "achieved": w["flop"] / lps / avg_s / 1e12})
+                # w["flop"]: 2 C d n, the fp32 products of Eq. (12); the GEMM
+                # runs each as GEMM_PIECE_PRODUCTS bf16 products on the matrix cores
+                bf = GEMM_PIECE_PRODUCTS * w["flop"] / lps
+                k.update({"bound": "mfma", "unit": "TFLOP/s", "peak": PEAK_MFMA_BF16_TFLOPS,
+                          "flop_per_launch": bf, "achieved": bf / avg_s / 1e12,
+                          "fp32_equivalent_tflops": w["flop"] / lps / avg_s / 1e12})
             elif "bytes" in w:
                 k.update({"bound": "hbm", "unit": "GB/s", "peak": PEAK_HBM_GBS,
                           "bytes_per_launch": w["bytes"] / lps, "achieved": w["bytes"] / lps / avg_s / 1e9})
@@ -688,7 +695,10 @@ def main():
                 "peak": K.get("peak"), "unit": K.get("unit"), "frac": round(K.get("frac", 0.0), 5),
                 "traffic": None if traffic is None else int(traffic),
                 "avg_launch_us": round(K["avg_us"], 3),
-                "achieved_is": "2 C d n FLOP per layer (Eq. (12)'s products) / event-timed launch duration"}
+                "fp32_equivalent_tflops": round(K.get("fp32_equivalent_tflops", 0.0), 4),
+                "achieved_is": "6 x 2 C d n bf16 FLOP per layer (six bf16 piece products for each of "
+                               "Eq. (12)'s fp32 products) / event-timed launch duration, against the "
+                               "dense bf16 MFMA peak"}
     # the candidate search: the fit kernel with the most time per step, with
     # the counter figures of the stored summary (FP32 / FP64 VALU rates
     # against their peaks, VALU-active and wait shares, HBM bytes)
@@ -715,7 +725,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f64+f32+bf16",
         "data": "synthetic",
         "config": {"workload": wk.name, "layers": nl, "channels": wk.channels,
                    "weights": wk.weights, "bits": wk.bits, "max_points": wk.max_points,

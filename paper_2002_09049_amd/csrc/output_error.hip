@@ -20,15 +20,16 @@
 //     matrix products: each fp32 operand is split into three bf16 pieces
 //     (hi + mid + lo, exact) and six of the nine piece products are summed
 //     by v_mfma_f32_32x32x16_bf16 with fp32 accumulation (the three left
-//     out lie below one rounding of the fp32 product).  A workgroup of four
-//     wavefronts owns a 128 x 128 tile of Y and one K range; each wavefront
-//     owns 64 x 64 as 2 x 2 MFMA blocks.  A slab of D (one block, rows of
-//     kBK k) and of X (kBK rows of 128 samples) is split once per workgroup
-//     into piece tiles in LDS, both with k contiguous per row and column;
-//     two register sets keep the slab after next in flight while one is
-//     multiplied and the next is split and stored (buffer loads: offsets
-//     past a range read as zeros).  Two workgroups per CU cover each
-//     other's split, store and barrier phases.  The epilogue squares Y
+//     out lie below one rounding of the fp32 product).  A workgroup owns a
+//     128 x 128 tile of Y and one K range, with eight wavefronts: four
+//     multiply (64 x 64 each, as 2 x 2 MFMA blocks) and four stage.  The
+//     staging ones load a 16-k slab of D (a half of a tile block's rows) and
+//     of X (16 rows of 128 samples) four slabs ahead into a ring of
+//     registers, split it once into bf16 piece tiles (k contiguous per row
+//     of D and per column of X) and store it to one of two LDS buffers
+//     while the multiplying ones read the other: one barrier per slab
+//     (buffer loads: offsets past a range read as zeros).  Two workgroups
+//     per CU cover each other's start and end.  The epilogue squares Y
 //     (fp64) and sums each row over the tile's columns into a partial per
 //     (column tile, row); a layer whose K is split (to balance a grid of
 //     long and short K ranges) stores its fp32 Y tiles per K range instead.

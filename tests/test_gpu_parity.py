@@ -281,6 +281,24 @@ def test_output_error_and_reconstruct(orc, C, d, n):
     assert np.array_equal(Wh.cpu().numpy(), orc.reconstruct(codes, scales, counts))
 
 
+def test_output_error_wide_range(orc):
+    """The GEMM's bf16 pieces keep fp32's exponent range: rows of W scaled by
+    2^-30 .. 2^30 and columns of X by 2^-20 .. 2^20 (exact scalings) keep the
+    1e-5 relative agreement with the fp64 output error on every row."""
+    C, d, n = 96, 300, 200
+    say(f"case output error, wide range C={C} d={d} n={n}")
+    rs = np.ldexp(1.0, np.round(np.linspace(-30, 30, C)).astype(int)).astype(np.float32)
+    cs = np.ldexp(1.0, np.round(np.linspace(-20, 20, n)).astype(int)).astype(np.float32)
+    W = (wl.random_weights(C, d, seed=31) * rs[:, None]).astype(np.float32)
+    X = (wl.random_calib(d, n, seed=32) * cs[None, :]).astype(np.float32)
+    out = gpu_fit(W, 4, 4, 128, 1e-3)
+    eo, ro = _oracle_err(orc, W, out, X)
+    eg, rg = _gpu_err(W, out, X)
+    assert np.all(np.isfinite(eg)) and np.all(eo > 0)
+    assert np.all(np.abs(eg - eo) <= 1e-5 * eo), np.max(np.abs(eg - eo) / eo)
+    assert np.all(np.abs(rg - ro) <= 1e-5 * ro)
+
+
 def test_output_error_hadamard(orc):
     say("case output error, X X^T = N I")
     d, N = 100, 128
