@@ -238,9 +238,9 @@ int mpq_reconstruct_layers(const mpq_layer *layers, int n_layers, int max_points
  * The fit launches run side by side (as in mpq_fit_layers), with the upload
  * of the output error's descriptor tables beside them; a fit launch of at
  * least 2e6 weights other than the longest one is followed on its stream by
- * its layers' reconstruction; a fit that keeps its residual in registers
- * also writes its layers' rows of the output error's residual D (bitwise
- * what the output error would form from the stored points).  Then the
+ * its layers' reconstruction; every fit also writes its layers' rows of the
+ * output error's residual D (bitwise what the output error would form from
+ * the stored points).  Then the
  * output errors of all layers run as one batch while the remaining layers
  * are reconstructed beside them.  The streams are the caller's and
  * library-owned ones joined back to it.

@@ -905,6 +905,26 @@ fit_hist_kernel(const HistBatch B)
         if (kGlobal || nfin > 1) __syncthreads();
     }
 
+    if constexpr (kGlobal) {
+        // the channel's row of the output error's D, outside calibration
+        // steps: the residual after its n points in fp32 (rebuild4's fp64
+        // steps in point order, as forming it from the stored points does),
+        // zero past d; the slots cover the row's nkb 32-k chunks, four
+        // consecutive k each (one float4 of a chunk; each thread reads back
+        // only the codes it wrote)
+        if (Ly.dres && !stepping) {
+            float *drow = Ly.dres + (k / 128) * nkb * 4096 + (k % 128) * 32;
+            for (int v = 0; v < kSlots; ++v) {
+                if (4 * T * v >= d) break;
+                const int j0 = 4 * (t + T * v);
+                if (j0 >= nkb * 32) continue;
+                double o[4];
+                rebuild4(v, n, o);
+                *(float4 *)(drow + (j0 / 32) * 4096 + j0 % 32) =
+                    make_float4((float)o[0], (float)o[1], (float)o[2], (float)o[3]);
+            }
+        }
+    }
     if (t == 0) Ly.counts[k] = n;
     if (more) {
         if (t == 0) Ly.list[atomicAdd(Ly.nlist + s0, 1)] = (int32_t)k;
@@ -994,8 +1014,7 @@ constexpr int kSmallVariant = kNumVariants;
 
 bool hist_variant_writes_d(int v)
 {
-    return (v >= kSmallVariant && v < kSmallVariant + kSmallMaxDim) ||
-           (v >= 0 && v < kNumVariants && !kVariants[v].rebuilt);
+    return (v >= kSmallVariant && v < kSmallVariant + kSmallMaxDim) || (v >= 0 && v < kNumVariants);
 }
 
 int hist_variant_count() { return kNumVariants + (int)kSmallMaxDim; }

@@ -80,7 +80,7 @@ struct HistLayer {
     // nullptr, or the output error's D for this layer (tiles of 128 rows by
     // 32 k, row-major inside; see err_item_d_offsets): the fit (not in
     // calibration steps) writes each channel's final residual there in fp32,
-    // k past d zero (variants that keep the residual in registers only)
+    // k past d zero
     float *dres;
     int d;
     int c_begin;        // first workgroup of this layer in the launch
