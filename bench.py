@@ -584,10 +584,10 @@ def main():
         else:
             # fit: G candidate errors per (element, point); reads W once, writes the codes
             # (with --clip, point 1 comes from the clipping pass, not the search);
-            # in the whole-path call a fit that holds its residual in registers
-            # also writes the rows of D (fp32), and no forming runs for them
+            # in the whole-path call the fit also writes the rows of D (fp32),
+            # and no forming runs for them
             searched = n - int((cnt > 0).sum()) if args.clip else n
-            fit_writes_d = not separate and not args.dense and "rebuilt" not in fk
+            fit_writes_d = not separate and not args.dense
             add(fk, evals=searched * wk.n_grid * d, bytes=4 * C * d + n * d + (4 * C * d if fit_writes_d else 0))
             add("gemm_err_kernel", flop=2 * C * d * N)
             # form: reads W and the codes of the used points, writes D
