@@ -135,8 +135,10 @@ int64_t mpq_fit_max_dim(int n_grid);
  *   ref[k] = (1/n) sum_t ( w_k . x_t )^2          (if ref_opt != NULL)
  * where w~_k = sum_{i<counts[k]} scales[k][i] * codes[k][i] and x_t is
  * column t of X.  The difference w_k - w~_k is formed in fp64 and rounded
- * to fp32; the products run on fp32 MFMA with fp32 accumulation; the sum
- * over the batch is fp64.
+ * to fp32; each fp32 product is summed from six products of the operands'
+ * exact three-piece bf16 splits on the bf16 matrix cores, with fp32
+ * accumulation (within one rounding of the fp32 product of an fp32 MFMA);
+ * the sum over the batch is fp64.
  *
  * Arguments
  *   W, codes, scales, counts   as produced for mpq_fit_layer (inputs);
@@ -257,7 +259,7 @@ int mpq_quantize_layers(const mpq_layer *layers, int n_layers, int bits, int max
  * isotropic one.  For each channel k, after each point n >= 1:
  *   e_n = (1/n_cols) sum_t ( (w_k - w~_k,n) . x_t )^2     (x_t: column t of X)
  * is computed as mpq_output_error does (fp64 difference rounded to fp32,
- * fp32 MFMA products, fp64 sum over the batch), and the channel stops once
+ * fp32 products from bf16 pieces, fp64 sum over the batch), and the channel stops once
  *   e_n <= thr,  thr = eps * (1/n_cols) sum_t (w_k . x_t)^2   (relative != 0)
  *                thr = eps                                  (relative == 0),
  * or at max_points, or when its residual is zero.  The points themselves
